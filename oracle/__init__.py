@@ -1,0 +1,181 @@
+"""CPU oracle for TSS evaluation and receiver/donor rebalancing.
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and
+the CPU-baseline leg of ``bench.py`` may import this package.  The GPU
+library never calls it and shares no code with it.
+
+The arithmetic lives in ``tre_oracle.c`` (plain C, fp64, single thread,
+compiled with ``-ffp-contract=off``); this module only builds it and
+marshals numpy arrays.  Function-level citations of the paper are in the C
+source.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Dict, Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "tre_oracle.c")
+_LIB = os.path.join(_HERE, "libtre_oracle.so")
+
+CFLAGS = ["-O2", "-fPIC", "-shared", "-ffp-contract=off", "-fno-fast-math", "-std=c11"]
+
+RESCUE, REBALANCE, POOL = 1, 2, 0xFF
+IDLE, INIT = 1, 2
+
+PROFILE_DTYPE = np.dtype([("w_p", "<f8"), ("w_q", "<f8"), ("alpha", "<f8"), ("theta", "<f8"),
+                          ("tau_crit", "<f8"), ("tau_surplus", "<f8"), ("r_min", "<i4"),
+                          ("r_init", "<i4")])
+SCENARIO_DTYPE = np.dtype([("trace", "<u4"), ("max_moves", "<u4"), ("theta_scale", "<f8"),
+                           ("tau_crit_override", "<f8")])
+MOVE_DTYPE = np.dtype([("window", "<u4"), ("path", "u1"), ("receiver", "u1"), ("donor", "u1"),
+                       ("pad", "u1")])
+assert PROFILE_DTYPE.itemsize == 56 and SCENARIO_DTYPE.itemsize == 24 and MOVE_DTYPE.itemsize == 8
+
+
+def build(force: bool = True, src: str = _SRC, out: str = _LIB) -> str:
+    """Compile the oracle with gcc (building the checker is not using it)."""
+    if force or not os.path.exists(out) or os.path.getmtime(out) < os.path.getmtime(src):
+        tmp = out + ".tmp"
+        subprocess.check_call(["gcc", *CFLAGS, "-o", tmp, src, "-lm"])
+        os.replace(tmp, out)
+    return out
+
+
+class Oracle:
+    """ctypes view of one compiled oracle library (the default, or a variant
+    compiled from edited source by the pin-strength tests)."""
+
+    def __init__(self, path: str):
+        L = ctypes.CDLL(path)
+        vp, i64, i32, u32, f64 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint32, ctypes.c_double
+        L.oracle_raw_tss.restype = f64
+        L.oracle_raw_tss.argtypes = [f64, f64, i64, i64, i64, i64, i64]
+        L.oracle_smooth.restype = f64
+        L.oracle_smooth.argtypes = [f64, f64, f64]
+        L.oracle_tss_trace.restype = ctypes.c_int
+        L.oracle_tss_trace.argtypes = [vp, vp, vp, vp, i64, i64, i64, i32, vp, vp, vp, vp, vp, vp, vp]
+        L.oracle_control.restype = ctypes.c_int
+        L.oracle_control.argtypes = [i64, i64, i64, i64, i32, i32, vp, vp, vp, vp, vp, u32, vp, vp, vp]
+        self.L = L
+        self.path = path
+
+    # ---------------------------------------------------------------- scalar
+    def raw_tss(self, w_p, w_q, P, D, A_int, W_int, window_ms) -> float:
+        return self.L.oracle_raw_tss(w_p, w_q, int(P), int(D), int(A_int), int(W_int), int(window_ms))
+
+    def smooth(self, alpha, raw, s_prev) -> float:
+        return self.L.oracle_smooth(alpha, raw, s_prev)
+
+    # ----------------------------------------------------------------- trace
+    def tss_trace(self, ev: Dict[str, np.ndarray], window_ms: int, duration_ms: int,
+                  prof: np.ndarray) -> Dict[str, np.ndarray]:
+        """Window tallies and smoothed TSS of one trace; arrays [n_windows][M]."""
+        prof = np.ascontiguousarray(prof, dtype=PROFILE_DTYPE)
+        M = prof.shape[0]
+        nW = duration_ms // window_ms
+        ts = np.ascontiguousarray(ev["ts"], np.int64)
+        model = np.ascontiguousarray(ev["model"], np.uint8)
+        typ = np.ascontiguousarray(ev["type"], np.uint8)
+        tok = np.ascontiguousarray(ev["tokens"], np.uint16)
+        out = {k: np.zeros((nW, M), np.int64) for k in ("P", "D", "A_int", "W_int")}
+        out["S"] = np.zeros((nW, M), np.float64)
+        out["flags"] = np.zeros((nW, M), np.uint8)
+        rc = self.L.oracle_tss_trace(ts.ctypes.data, model.ctypes.data, typ.ctypes.data, tok.ctypes.data,
+                                     ts.shape[0], window_ms, duration_ms, M, prof.ctypes.data,
+                                     out["P"].ctypes.data, out["D"].ctypes.data, out["A_int"].ctypes.data,
+                                     out["W_int"].ctypes.data, out["S"].ctypes.data, out["flags"].ctypes.data)
+        if rc:
+            raise ValueError(f"oracle_tss_trace rejected the trace ({rc})")
+        return out
+
+    def control(self, cfg: Dict[str, int], prof: np.ndarray, S: np.ndarray, flags: np.ndarray,
+                sc: np.ndarray, move_cap: Optional[int] = None) -> Dict[str, np.ndarray]:
+        """Control replay of one scenario (a 1-element SCENARIO_DTYPE array)."""
+        prof = np.ascontiguousarray(prof, dtype=PROFILE_DTYPE)
+        sc = np.ascontiguousarray(np.atleast_1d(sc), dtype=SCENARIO_DTYPE)
+        M = prof.shape[0]
+        nW = cfg["duration_ms"] // cfg["window_ms"]
+        if move_cap is None:
+            move_cap = max(1, nW * int(sc[0]["max_moves"]))
+        S = np.ascontiguousarray(S, np.float64)
+        flags = np.ascontiguousarray(flags, np.uint8)
+        moves = np.zeros(move_cap, MOVE_DTYPE)
+        n_moves = np.zeros(1, np.uint32)
+        r_final = np.zeros(M, np.int32)
+        r_windows = np.zeros(M, np.int64)
+        rc = self.L.oracle_control(cfg["window_ms"], cfg["duration_ms"], cfg["fast_period_ms"],
+                                   cfg["slow_period_ms"], M, cfg["budget"], prof.ctypes.data,
+                                   S.ctypes.data, flags.ctypes.data, sc.ctypes.data, moves.ctypes.data,
+                                   move_cap, n_moves.ctypes.data, r_final.ctypes.data,
+                                   r_windows.ctypes.data)
+        if rc:
+            raise ValueError(f"oracle_control rejected the scenario ({rc})")
+        n = int(n_moves[0])
+        return {"moves": moves[:min(n, move_cap)].copy(), "n_moves": n, "r_final": r_final,
+                "r_windows": r_windows}
+
+
+_default: Optional[Oracle] = None
+
+
+def get() -> Oracle:
+    global _default
+    if _default is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build(force=True)
+        _default = Oracle(_LIB)
+    return _default
+
+
+def pack_profiles(cols: Dict[str, np.ndarray]) -> np.ndarray:
+    n = cols["w_p"].shape[0]
+    a = np.zeros(n, PROFILE_DTYPE)
+    for k in PROFILE_DTYPE.names:
+        a[k] = cols[k]
+    return a
+
+
+def pack_scenarios(cols: Dict[str, np.ndarray]) -> np.ndarray:
+    n = cols["trace"].shape[0]
+    a = np.zeros(n, SCENARIO_DTYPE)
+    for k in SCENARIO_DTYPE.names:
+        a[k] = cols[k]
+    return a
+
+
+def run(events, trace_off: np.ndarray, cfg: Dict[str, int], prof_cols: Dict[str, np.ndarray],
+        sc_cols: Dict[str, np.ndarray], traces=None, scenarios=None, keep_tss: bool = True):
+    """Oracle over a set of traces and scenarios.
+
+    events: dict of host columns; trace_off: CSR offsets (trace i is
+    events[off[i]:off[i+1]]); prof_cols: profile columns [n_traces*M];
+    sc_cols: scenario columns.  ``traces`` / ``scenarios`` restrict the work
+    to subsets (scenarios whose trace is not computed are skipped).
+    Returns {"tss": {trace: dict}, "ctl": {scenario: dict}}.
+    """
+    o = get()
+    M = cfg["n_models"]
+    prof = pack_profiles(prof_cols)
+    sc = pack_scenarios(sc_cols)
+    n_traces = len(trace_off) - 1
+    traces = range(n_traces) if traces is None else traces
+    tss = {}
+    for t in traces:
+        a, b = int(trace_off[t]), int(trace_off[t + 1])
+        ev = {k: events[k][a:b] for k in ("ts", "model", "type", "tokens")}
+        tss[t] = o.tss_trace(ev, cfg["window_ms"], cfg["duration_ms"], prof[t * M:(t + 1) * M])
+    scenarios = range(sc.shape[0]) if scenarios is None else scenarios
+    ctl = {}
+    for s in scenarios:
+        t = int(sc[s]["trace"])
+        if t not in tss:
+            continue
+        ctl[s] = o.control(cfg, prof[t * M:(t + 1) * M], tss[t]["S"], tss[t]["flags"], sc[s:s + 1])
+    if not keep_tss:
+        tss = {}
+    return {"tss": tss, "ctl": ctl}
