@@ -1,0 +1,248 @@
+#!/usr/bin/env python3
+"""Throughput of the TSS + rebalancing replay on one MI355X.
+
+One step = one ``tre_sweep`` call over the whole resident workload: stream
+every event column from HBM, per-(trace, model, window) tallies, carry scan,
+Eq. (1) TSS + smoothing, then per scenario Eq. (2), regions, cadence and the
+bounded receiver/donor moves.  Events are generated on the host (seeded),
+copied to HBM and validated before the timed region; the timed region only
+contains the sweeps.
+
+Prints ONE JSON line (rank 0).  ``value`` is request-events per second
+(sum over scenarios of the events of that scenario's trace, per second of
+sweep time).  ``roofline`` describes the dominant kernel (``tss_stream``):
+algorithmic bytes per launch = 12 bytes per physical event (ts 8 + model 1 +
+type 1 + tokens 2; the request-id column is never read) divided by the
+kernel's mean launch time measured with HIP events on its stream.
+``cpu_baseline`` times the CPU oracle (single thread) on a bounded sample
+of the same traces and checks the GPU's decisions on that sample.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+WORKLOADS = {"tiny": 0, "bursty": 1, "sweep": 2, "diverse": 3, "stress": 4}
+HBM_PEAK_GBS = 8000.0
+ALG_BYTES_PER_EVENT = 12
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "tss_stream_traffic.json")
+KERNEL_SRC = os.path.join(ROOT, "paper_2609_29160_amd", "csrc", "tre.hip")
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def kernel_sha() -> str:
+    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+
+
+def traffic_for(workload_name: str, events: int):
+    """HBM bytes per tss_stream launch from committed rocprofv3 counters, if
+    they were taken on this kernel source and workload; else None."""
+    try:
+        t = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_sha") != kernel_sha() or t.get("workload") != workload_name or t.get("events") != events:
+        return None
+    return t.get("bytes_per_launch")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="stress", choices=sorted(WORKLOADS))
+    ap.add_argument("--traces", type=int, default=None, help="use only the first N traces")
+    ap.add_argument("--cpu-sample", type=int, default=None, help="traces timed on the CPU oracle")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle leg")
+    ap.add_argument("--emit-tss", action="store_true", help="also write per-window fp32 TSS")
+    ap.add_argument("--threads", type=int, default=None)
+    ap.add_argument("--copy-calib-gb", type=float, default=0.0,
+                    help="after the run, copy this many GB device-to-device (counter calibration)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(traces and scenarios would shard across GPUs with no exchange)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import tracegen as tg
+    from paper_2609_29160_amd import device, tre
+
+    torch.cuda.set_device(0)
+    w = tg.standard(WORKLOADS[args.workload])
+    if args.traces:
+        n = min(args.traces, w.n_traces)
+        w = w.scaled(n_traces=n, n_scenarios=n if (w.n_scenarios and w.scenario_trace == "identity") else w.n_scenarios)
+    sc_cols = w.scenario_columns()
+    n_sc = len(sc_cols["trace"])
+
+    # CPU sample: traces whose scenarios the oracle replays
+    if args.no_cpu:
+        sample = []
+    else:
+        n_s = args.cpu_sample
+        if n_s is None:
+            n_s = {"stress": 96, "diverse": 16}.get(args.workload, w.n_traces)
+        n_s = max(1, min(n_s, w.n_traces))
+        sample = list(range(n_s))
+
+    t0 = time.time()
+    dt = device.upload(w, threads=args.threads, log=log, keep_host=sample)
+    log(f"resident: {dt.n_events} events, {dt.stored_bytes / 1e9:.1f} GB stored ({time.time() - t0:.1f} s)")
+    ev = device.load(dt, validate=True)
+    prof = device.profiles(w)
+    sc = device.scenarios(sc_cols)
+    tre.tre_check_params(ev, prof, sc)
+    max_k = int(np.max(sc_cols["max_moves"]))
+    move_cap = max(1, ev.n_ticks * max_k)
+    out = tre.ctl_outputs(ev, n_sc, move_cap)
+    ws = torch.empty(tre.tre_workspace_size(ev, n_sc), dtype=torch.uint8, device="cuda")
+    tss32 = None
+    if args.emit_tss:
+        tss32 = torch.empty((ev.n_traces, ev.n_windows, ev.n_models), dtype=torch.float32, device="cuda")
+    counts = dt.counts
+    logical = int(sum(int(counts[int(t)]) for t in sc_cols["trace"]))
+    log(f"{ev.n_traces} traces, {n_sc} scenarios, {ev.n_windows} windows, {ev.n_ticks} ticks, "
+        f"{logical} logical events")
+
+    for _ in range(args.warmup):
+        tre.tre_sweep(ev, prof, sc, out, ws, tss32=tss32)
+    torch.cuda.synchronize()
+    log("warmup done")
+
+    stream = torch.cuda.current_stream()
+    tre.tre_set_timing(True)
+    tre.tre_kernel_time("tss_stream")
+    tre.tre_kernel_time("rebalance")
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        tre.tre_sweep(ev, prof, sc, out, ws, tss32=tss32)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    tre.tre_set_timing(False)
+    step_ms = e0.elapsed_time(e1) / args.steps
+    k_ms, k_n = tre.tre_kernel_time("tss_stream")
+    r_ms, r_n = tre.tre_kernel_time("rebalance")
+    stream_ms = k_ms / max(k_n, 1)
+    reb_ms = r_ms / max(r_n, 1)
+    log(f"step {step_ms:.3f} ms (wall {1e3 * wall / args.steps:.3f} ms); tss_stream {stream_ms:.3f} ms, "
+        f"rebalance {reb_ms:.3f} ms")
+
+    value = logical / (step_ms / 1e3)
+    alg_bytes = ALG_BYTES_PER_EVENT * dt.n_events
+    achieved = alg_bytes / (stream_ms / 1e3) / 1e9
+    traffic = traffic_for(w.name, dt.n_events)
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                "kernel": "tss_stream", "kernel_ms": round(stream_ms, 4),
+                "alg_bytes_per_launch": alg_bytes}
+
+    cpu = None
+    parity = None
+    if sample:
+        cpu, parity = cpu_leg(w, dt, sample, sc_cols, out, move_cap, tre)
+
+    result = {
+        "metric": "request-events/sec through TSS+rebalance (1 GPU); achieved HBM GB/s vs peak",
+        "value": round(value, 1),
+        "unit": "request-events/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(step_ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic (seeded generator; the paper's traces are not available)",
+        "config": {"workload": w.name, "traces": ev.n_traces, "scenarios": n_sc, "models": ev.n_models,
+                   "window_ms": w.window_ms, "duration_s": w.duration_ms // 1000,
+                   "events": dt.n_events, "logical_events": logical,
+                   "stored_gb": round(dt.stored_bytes / 1e9, 2), "emit_tss": bool(args.emit_tss)},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "parity": parity,
+        "rebalance_ms": round(reb_ms, 4),
+    }
+    print(json.dumps(result), flush=True)
+
+    if args.copy_calib_gb > 0:
+        n = int(args.copy_calib_gb * 1e9) // 4
+        src = torch.ones(n, dtype=torch.int32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"copy calibration: 3 x {4 * n} bytes read + written")
+    ev.close()
+
+
+def cpu_leg(w, dt, sample, sc_cols, out, move_cap, tre):
+    """Time the oracle (one thread) on the sample traces and compare the GPU's
+    decisions for the scenarios on those traces."""
+    import numpy as np
+
+    import oracle as O
+
+    o = O.get()
+    M = w.n_models
+    prof_all = O.pack_profiles(w.profile_columns(max(sample) + 1))
+    sc_all = O.pack_scenarios(sc_cols)
+    cfg = w.trace_cfg()
+    by_trace = {}
+    for s, t in enumerate(sc_cols["trace"]):
+        by_trace.setdefault(int(t), []).append(s)
+    t0 = time.perf_counter()
+    logical = 0
+    refs = {}
+    for t in sample:
+        host = dt.host[t]
+        prof = prof_all[t * M:(t + 1) * M]
+        r = o.tss_trace(host, w.window_ms, w.duration_ms, prof)
+        for s in by_trace.get(t, []):
+            refs[s] = o.control(cfg, prof, r["S"], r["flags"], sc_all[s:s + 1], move_cap)
+            logical += len(host["ts"])
+    cpu_s = time.perf_counter() - t0
+    # parity of the last timed sweep on the sampled scenarios
+    n_moves = out["n_moves"].cpu().numpy()
+    r_final = out["r_final"].cpu().numpy()
+    r_windows = out["r_windows"].cpu().numpy()
+    moves = tre.unpack_moves(out["moves"]).reshape(-1)
+    bad = 0
+    for s, ref in refs.items():
+        k = int(n_moves[s])
+        ok = k == ref["n_moves"] and np.array_equal(r_final[s], ref["r_final"]) and \
+            np.array_equal(r_windows[s], ref["r_windows"])
+        if ok:
+            got = moves[s * move_cap:s * move_cap + min(k, move_cap)]
+            exp = ref["moves"][:min(k, move_cap)]
+            ok = all(np.array_equal(got[f], exp[f]) for f in ("window", "path", "receiver", "donor"))
+        bad += 0 if ok else 1
+    cpu = {"value": round(logical / cpu_s, 1), "unit": "request-events/s", "cores": 1, "kind": "oracle",
+           "sample": f"{len(sample)} of {w.n_traces} traces ({sum(len(dt.host[t]['ts']) for t in sample)} events), "
+                     f"{len(refs)} scenarios, {cpu_s:.1f} s on one host thread"}
+    parity = {"scenarios_checked": len(refs), "mismatches": bad, "bit_exact": bad == 0}
+    log(f"cpu oracle: {cpu['value']:.3g} events/s; parity {parity}")
+    return cpu, parity
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,249 @@
+/*
+ * tre.h - C ABI of the MI355X (gfx950) replay library for Token Service
+ * Share (TSS) evaluation and TSS-guided receiver/donor rebalancing.
+ *
+ * Paper: "Cross-Model Autoscaling for Shared LLM Serving" (TRE).
+ *   - TSS, Eq. (1): effective token service per active-or-waiting request,
+ *     Section "Design Rationale and Definition";
+ *   - smoothing, Eq. (2) normalisation Z = TSS/theta and the three regions
+ *     tau_crit < 1 < tau_surplus, Section "Smoothing, Normalization, and
+ *     Calibration";
+ *   - rescue / rebalancing cadences and Eq. (3) receiver = argmin Z, donor
+ *     preference, Section "Dual-Speed Control";
+ *   - one bounded transition per pair and tick, receiver below its boundary,
+ *     donor above its floor, fixed budget, Section "Bounded Pairwise Transfer".
+ *
+ * Conventions
+ *   - Every call returns a status (TRE_OK = 0); nothing throws or exits.
+ *     tre_last_error() gives a message for the calling thread's last error.
+ *   - "device" pointers are HIP device memory owned by the caller; "host"
+ *     pointers are ordinary host memory, read during the call only.
+ *   - Hot calls (tre_eval_tss, tre_rebalance, tre_sweep) only check their
+ *     arguments on the host and enqueue work on `stream` (a hipStream_t, or
+ *     NULL for the default stream); they return before the work completes.
+ *     Parameter tables are checked by tre_check_params (synchronous); the
+ *     hot calls trust them. Invalid tables cannot make a kernel read or write
+ *     out of bounds, but their results are unspecified.
+ *   - Per-cell arrays are laid out [trace][window][model], row-major.
+ *   - Handles are immutable after tre_load_events; concurrent calls on one
+ *     handle with distinct outputs and workspaces are safe.
+ *   - Floating point: IEEE binary64, round to nearest even, no contraction,
+ *     in the operation order documented at tre_eval_tss; results are
+ *     bit-identical across launches and grid shapes.
+ */
+#ifndef TRE_H
+#define TRE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ------------------------------------------------------------- status */
+#define TRE_OK 0
+#define TRE_EINVAL 1  /* bad argument, configuration or parameter table       */
+#define TRE_EORDER 2  /* timestamps unsorted within a trace or out of range    */
+#define TRE_ESCHEMA 3 /* model index >= n_models or undefined type bits        */
+#define TRE_ERANGE 4  /* a trace exceeds the library's counting limits         */
+#define TRE_ENOMEM 5  /* workspace too small                                   */
+#define TRE_EHIP 6    /* HIP runtime error                                     */
+
+/* Maximum models per trace (one wavefront lane per model). */
+#define TRE_MAX_MODELS 64
+/* Maximum events that may fall in one window of one trace (keeps every
+   per-window tally inside its packed 32/40-bit field). */
+#define TRE_MAX_EVENTS_PER_WINDOW 65535
+
+/* ------------------------------------------------------------- events
+ * One event per row, structure of arrays, sorted by ts within each trace:
+ *   ts      int64   ms from trace start, 0 <= ts < duration_ms
+ *   model   uint8   model index < n_models
+ *   req     uint32  request id (stored, never read by the replay)
+ *   type    uint8   bits 0-1 kind: 0 ARRIVE (joins the model's waiting
+ *                   queue), 1 PREFILL (prompt tokens served), 2 DECODE
+ *                   (output tokens served), 3 FINISH (leaves the active set);
+ *                   bit 7 ADMIT, only on a PREFILL (waiting -> active);
+ *                   other bits 0
+ *   tokens  uint16  tokens served by a PREFILL / DECODE; ignored otherwise
+ * The active count A_m(t) and waiting count W_m(t) of Eq. (1) are the
+ * running sums of these transitions, starting at 0. */
+#define TRE_ARRIVE 0
+#define TRE_PREFILL 1
+#define TRE_DECODE 2
+#define TRE_FINISH 3
+#define TRE_ADMIT 0x80
+
+/* Shared shape of every trace in a handle. window_ms must divide
+   duration_ms and both periods. The fast period is the rescue cadence, the
+   slow period the rebalancing cadence (Section "Dual-Speed Control"). */
+typedef struct {
+  int64_t window_ms;
+  int64_t duration_ms;
+  int64_t fast_period_ms;
+  int64_t slow_period_ms;
+  int32_t n_models;  /* 1 .. TRE_MAX_MODELS */
+  int32_t budget;    /* fixed replica budget (unit footprint) */
+} tre_trace_cfg;
+
+/* Per-(trace, model) control profile: the paper's six scalars per
+   model-SLO pair (Section "Smoothing, Normalization, and Calibration") plus
+   the minimum routable-replica floor and the initial routable replicas.
+   Requirements (tre_check_params): w_p >= 0, w_q >= 0, 0 < alpha <= 1,
+   theta > 0, 0 <= tau_crit < tau_surplus, r_min >= 0, r_init >= 0. */
+typedef struct {
+  double w_p, w_q, alpha, theta, tau_crit, tau_surplus;
+  int32_t r_min, r_init;
+} tre_profile; /* 56 bytes */
+
+/* One what-if scenario: a trace, the moves allowed per tick (K), a scale
+   applied to every healthy boundary theta, and a rescue threshold that
+   replaces every profile's tau_crit when >= 0. */
+typedef struct {
+  uint32_t trace;
+  uint32_t max_moves;
+  double theta_scale;
+  double tau_crit_override;
+} tre_scenario; /* 24 bytes */
+
+#define TRE_PATH_RESCUE 1
+#define TRE_PATH_REBALANCE 2
+#define TRE_DONOR_POOL 0xFF
+
+/* One capacity transition decided at the end of window `window`; donor
+   TRE_DONOR_POOL means idle budget. */
+typedef struct {
+  uint32_t window;
+  uint8_t path, receiver, donor, pad;
+} tre_move; /* 8 bytes */
+
+typedef struct tre_events tre_events; /* opaque */
+
+typedef struct {
+  uint32_t n_traces;
+  uint32_t n_models;
+  int64_t n_events;   /* trace_off[n_traces] - trace_off[0] */
+  int64_t n_windows;  /* duration_ms / window_ms */
+  int64_t n_ticks;    /* windows that end on a fast or slow period */
+} tre_info;
+
+/* Optional per-cell outputs of tre_eval_tss, each [n_traces][n_windows]
+   [n_models] in device memory, any may be NULL:
+     prefill, decode  tokens served in the window;
+     a_int, w_int     integral of A_m(t), W_m(t) over the window (request*ms);
+     tss64            smoothed TSS (fp64);
+     tss32            smoothed TSS rounded to fp32;
+     flags            bit 0: idle window (no tokens, nothing active or
+                      waiting), bit 1: smoothed value initialised. */
+typedef struct {
+  uint32_t* prefill;
+  uint32_t* decode;
+  int64_t* a_int;
+  int64_t* w_int;
+  double* tss64;
+  float* tss32;
+  uint8_t* flags;
+} tre_tss_out;
+
+#define TRE_FLAG_IDLE 1
+#define TRE_FLAG_INIT 2
+
+/* Outputs of the control replay, device memory:
+     moves      [n_scenarios][move_cap]: moves in selection order; only the
+                first min(n_moves[s], move_cap) entries of a scenario are
+                written;
+     n_moves    [n_scenarios]: moves decided (may exceed move_cap);
+     r_final    [n_scenarios][n_models]: routable replicas after the last
+                window;
+     r_windows  [n_scenarios][n_models]: sum over windows of the replicas in
+                force during the window. */
+typedef struct {
+  tre_move* moves;
+  uint32_t move_cap;
+  uint32_t* n_moves;
+  int32_t* r_final;
+  int64_t* r_windows;
+} tre_ctl_out;
+
+/* Message for the calling thread's last non-OK status ("" if none). */
+const char* tre_last_error(void);
+
+/* Register event columns (device, borrowed: the caller keeps them alive
+   and unchanged while the handle is used) and CSR trace offsets (host,
+   copied: trace i is rows [trace_off[i], trace_off[i+1]) of every column,
+   non-decreasing, trace_off[0] >= 0). `cfg` (host) is copied. Column
+   pointers need 16-byte alignment (ts, tokens) or 8-byte (model, type).
+   With flags & TRE_VALIDATE the events are checked on the device and the
+   call waits for the result (TRE_EORDER, TRE_ESCHEMA, TRE_ERANGE). The
+   handle owns small device tables (offsets, tick list); free it with
+   tre_free_events. */
+#define TRE_VALIDATE 1u
+int tre_load_events(const int64_t* ts, const uint8_t* model, const uint32_t* req,
+                    const uint8_t* type, const uint16_t* tokens, const int64_t* trace_off,
+                    uint32_t n_traces, const tre_trace_cfg* cfg, uint32_t flags, void* stream,
+                    tre_events** out);
+
+/* Release a handle (NULL is a no-op). Does not touch the event columns. */
+void tre_free_events(tre_events* ev);
+
+int tre_events_info(const tre_events* ev, tre_info* info);
+
+/* Check a profile table ([n_traces][n_models], device) and a scenario table
+   ([n_scenarios], device, may be NULL when n_scenarios is 0) against the
+   requirements above and the budget (sum of r_init <= budget per trace).
+   Synchronous. */
+int tre_check_params(const tre_events* ev, const tre_profile* prof, const tre_scenario* sc,
+                     uint32_t n_scenarios);
+
+/* Workspace bytes for tre_sweep with n_scenarios scenarios (0 for the other
+   calls). */
+int tre_workspace_size(const tre_events* ev, uint32_t n_scenarios, size_t* bytes);
+
+/* Steps a1-a4: per (trace, model, window) tallies, active / waiting
+   integrals and smoothed TSS. For each model the raw ratio of Eq. (1) with
+   rates in tokens/s, A and W the window time averages and a floor of one
+   request is evaluated as
+     num = w_p*P; num = num + D; num = num*1000;
+     q = w_q*W_int; den = A_int + q; if (den < window_ms) den = window_ms;
+     raw = num/den
+   (all fp64), then S = alpha*raw + (1-alpha)*S_prev as t1 = alpha*raw,
+   t2 = (1-alpha)*S_prev, S = t1 + t2; an idle window holds S; the first
+   non-idle window sets S = raw. prof: device [n_traces][n_models]. */
+int tre_eval_tss(const tre_events* ev, const tre_profile* prof, const tre_tss_out* out,
+                 void* stream);
+
+/* Steps a5-a8 for n_scenarios scenarios over per-cell smoothed TSS and
+   flags produced by tre_eval_tss (device, [n_traces][n_windows][n_models]).
+   At each tick window: Z = S/(theta*theta_scale) (+inf when idle or not
+   initialised); critical Z < tau_crit, surplus Z > tau_surplus. If a model
+   is critical: at a fast tick rescue (receivers = critical models),
+   otherwise no action. Else at a slow tick rebalance (receivers = Z < 1).
+   Up to max_moves greedy moves: receiver = argmin Z over unused eligible
+   models; source = idle budget if any, else argmax Z over unused surplus
+   models, else over unused nominal models, with R > r_min and Z above the
+   receiver's; no source ends the tick; ties go to the lowest model index.
+   sc: device [n_scenarios]. */
+int tre_rebalance(const tre_events* ev, const tre_profile* prof, const double* tss64,
+                  const uint8_t* flags, const tre_scenario* sc, uint32_t n_scenarios,
+                  const tre_ctl_out* out, void* stream);
+
+/* Steps a1-a8 in one call: the smoothed TSS is kept only at tick windows
+   (in the workspace) and fed to the control replay. Outputs as
+   tre_rebalance; tss32 (device [n_traces][n_windows][n_models]) may be
+   NULL. ws: device workspace of at least tre_workspace_size bytes. */
+int tre_sweep(const tre_events* ev, const tre_profile* prof, const tre_scenario* sc,
+              uint32_t n_scenarios, const tre_ctl_out* out, float* tss32, void* ws,
+              size_t ws_bytes, void* stream);
+
+/* Kernel timing (HIP events recorded around each launch on its stream).
+   tre_set_timing(1) starts recording; tre_kernel_time waits for the
+   recorded launches of `kernel` ("tss_stream", "rebalance", "validate")
+   and returns their total milliseconds and count, then forgets them. */
+int tre_set_timing(int enable);
+int tre_kernel_time(const char* kernel, double* total_ms, uint64_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TRE_H */

@@ -1,0 +1,247 @@
+"""Python binding of the C ABI in ``include/tre.h`` (argument marshalling only).
+
+Every step of the replay runs in the HIP kernels of ``libtre.so``; this
+module only converts torch tensors (device memory) and the current torch
+stream into plain pointers, and raises on a non-OK status.  There is no CPU
+fallback: if the library is missing, importing the binding fails loudly.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, Optional
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtre.so")
+
+TRE_OK, TRE_EINVAL, TRE_EORDER, TRE_ESCHEMA, TRE_ERANGE, TRE_ENOMEM, TRE_EHIP = range(7)
+TRE_VALIDATE = 1
+TRE_FLAG_IDLE, TRE_FLAG_INIT = 1, 2
+TRE_PATH_RESCUE, TRE_PATH_REBALANCE, TRE_DONOR_POOL = 1, 2, 0xFF
+TRE_MAX_MODELS = 64
+
+# struct layouts of tre.h
+PROFILE_DTYPE = np.dtype([("w_p", "<f8"), ("w_q", "<f8"), ("alpha", "<f8"), ("theta", "<f8"),
+                          ("tau_crit", "<f8"), ("tau_surplus", "<f8"), ("r_min", "<i4"),
+                          ("r_init", "<i4")])
+SCENARIO_DTYPE = np.dtype([("trace", "<u4"), ("max_moves", "<u4"), ("theta_scale", "<f8"),
+                           ("tau_crit_override", "<f8")])
+MOVE_DTYPE = np.dtype([("window", "<u4"), ("path", "u1"), ("receiver", "u1"), ("donor", "u1"),
+                       ("pad", "u1")])
+
+
+class TreError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"TRE status {code}: {msg}")
+        self.code = code
+
+
+class _TraceCfg(ctypes.Structure):
+    _fields_ = [("window_ms", ctypes.c_int64), ("duration_ms", ctypes.c_int64),
+                ("fast_period_ms", ctypes.c_int64), ("slow_period_ms", ctypes.c_int64),
+                ("n_models", ctypes.c_int32), ("budget", ctypes.c_int32)]
+
+
+class _Info(ctypes.Structure):
+    _fields_ = [("n_traces", ctypes.c_uint32), ("n_models", ctypes.c_uint32),
+                ("n_events", ctypes.c_int64), ("n_windows", ctypes.c_int64),
+                ("n_ticks", ctypes.c_int64)]
+
+
+class _TssOut(ctypes.Structure):
+    _fields_ = [(k, ctypes.c_void_p) for k in
+                ("prefill", "decode", "a_int", "w_int", "tss64", "tss32", "flags")]
+
+
+class _CtlOut(ctypes.Structure):
+    _fields_ = [("moves", ctypes.c_void_p), ("move_cap", ctypes.c_uint32),
+                ("n_moves", ctypes.c_void_p), ("r_final", ctypes.c_void_p),
+                ("r_windows", ctypes.c_void_p)]
+
+
+EXPORTS = ["tre_last_error", "tre_load_events", "tre_free_events", "tre_events_info",
+           "tre_check_params", "tre_workspace_size", "tre_eval_tss", "tre_rebalance", "tre_sweep",
+           "tre_set_timing", "tre_kernel_time"]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, u32, i32, sz = ctypes.c_void_p, ctypes.c_uint32, ctypes.c_int, ctypes.c_size_t
+    L.tre_last_error.restype = ctypes.c_char_p
+    L.tre_last_error.argtypes = []
+    L.tre_load_events.restype = i32
+    L.tre_load_events.argtypes = [vp, vp, vp, vp, vp, vp, u32, ctypes.POINTER(_TraceCfg), u32, vp,
+                                  ctypes.POINTER(ctypes.c_void_p)]
+    L.tre_free_events.restype = None
+    L.tre_free_events.argtypes = [vp]
+    L.tre_events_info.restype = i32
+    L.tre_events_info.argtypes = [vp, ctypes.POINTER(_Info)]
+    L.tre_check_params.restype = i32
+    L.tre_check_params.argtypes = [vp, vp, vp, u32]
+    L.tre_workspace_size.restype = i32
+    L.tre_workspace_size.argtypes = [vp, u32, ctypes.POINTER(sz)]
+    L.tre_eval_tss.restype = i32
+    L.tre_eval_tss.argtypes = [vp, vp, ctypes.POINTER(_TssOut), vp]
+    L.tre_rebalance.restype = i32
+    L.tre_rebalance.argtypes = [vp, vp, vp, vp, vp, u32, ctypes.POINTER(_CtlOut), vp]
+    L.tre_sweep.restype = i32
+    L.tre_sweep.argtypes = [vp, vp, vp, u32, ctypes.POINTER(_CtlOut), vp, vp, sz, vp]
+    L.tre_set_timing.restype = i32
+    L.tre_set_timing.argtypes = [i32]
+    L.tre_kernel_time.restype = i32
+    L.tre_kernel_time.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
+                                  ctypes.POINTER(ctypes.c_uint64)]
+    return L
+
+
+_L = _load()
+
+
+def _check(rc: int):
+    if rc != TRE_OK:
+        raise TreError(rc, _L.tre_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("device tensor expected")
+    if not t.is_contiguous():
+        raise ValueError("contiguous tensor expected")
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream or None
+
+
+class Events:
+    """A loaded trace set (wraps ``tre_events*``); keeps its columns alive."""
+
+    def __init__(self, handle: int, cols: Dict[str, torch.Tensor], cfg: Dict[str, int]):
+        self.handle = handle
+        self.cols = cols
+        self.cfg = dict(cfg)
+        info = _Info()
+        _check(_L.tre_events_info(handle, ctypes.byref(info)))
+        self.n_traces = info.n_traces
+        self.n_models = info.n_models
+        self.n_events = info.n_events
+        self.n_windows = info.n_windows
+        self.n_ticks = info.n_ticks
+
+    def close(self):
+        if self.handle:
+            _L.tre_free_events(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def tre_load_events(ts: torch.Tensor, model: torch.Tensor, req: Optional[torch.Tensor],
+                    type: torch.Tensor, tokens: torch.Tensor, trace_off, cfg: Dict[str, int],
+                    validate: bool = True, stream=None) -> Events:
+    off = np.ascontiguousarray(np.asarray(trace_off, dtype=np.int64))
+    c = _TraceCfg(cfg["window_ms"], cfg["duration_ms"], cfg["fast_period_ms"], cfg["slow_period_ms"],
+                  cfg["n_models"], cfg["budget"])
+    for name, t, dt in (("ts", ts, torch.int64), ("model", model, torch.uint8),
+                        ("type", type, torch.uint8), ("tokens", tokens, torch.uint16)):
+        if t.dtype != dt:
+            raise ValueError(f"{name} must be {dt}")
+    h = ctypes.c_void_p()
+    _check(_L.tre_load_events(_ptr(ts), _ptr(model), _ptr(req), _ptr(type), _ptr(tokens),
+                              off.ctypes.data, len(off) - 1, ctypes.byref(c),
+                              TRE_VALIDATE if validate else 0, _stream(stream), ctypes.byref(h)))
+    return Events(h.value, {"ts": ts, "model": model, "req": req, "type": type, "tokens": tokens}, cfg)
+
+
+def pack(cols: Dict[str, np.ndarray], dtype: np.dtype, device="cuda") -> torch.Tensor:
+    """Columns -> array of tre.h structs, as a byte tensor on `device`."""
+    n = len(next(iter(cols.values())))
+    a = np.zeros(n, dtype)
+    for k in dtype.names:
+        if k in cols:
+            a[k] = cols[k]
+    return torch.from_numpy(a.view(np.uint8).copy()).to(device)
+
+
+def unpack_moves(moves: torch.Tensor) -> np.ndarray:
+    return moves.cpu().numpy().view(MOVE_DTYPE)
+
+
+def tre_check_params(ev: Events, prof: torch.Tensor, sc: Optional[torch.Tensor] = None):
+    n_sc = 0 if sc is None else sc.numel() // SCENARIO_DTYPE.itemsize
+    _check(_L.tre_check_params(ev.handle, _ptr(prof), _ptr(sc), n_sc))
+
+
+def tre_workspace_size(ev: Events, n_scenarios: int) -> int:
+    n = ctypes.c_size_t()
+    _check(_L.tre_workspace_size(ev.handle, n_scenarios, ctypes.byref(n)))
+    return n.value
+
+
+def tss_outputs(ev: Events, which=("prefill", "decode", "a_int", "w_int", "tss64", "tss32", "flags"),
+                device="cuda") -> Dict[str, torch.Tensor]:
+    shape = (ev.n_traces, ev.n_windows, ev.n_models)
+    dt = {"prefill": torch.int32, "decode": torch.int32, "a_int": torch.int64, "w_int": torch.int64,
+          "tss64": torch.float64, "tss32": torch.float32, "flags": torch.uint8}
+    return {k: torch.empty(shape, dtype=dt[k], device=device) for k in which}
+
+
+def tre_eval_tss(ev: Events, prof: torch.Tensor, out: Dict[str, torch.Tensor], stream=None):
+    """Fill the given per-cell outputs (prefill/decode are uint32 data in
+    int32 tensors)."""
+    o = _TssOut(*[_ptr(out.get(k)) for k in ("prefill", "decode", "a_int", "w_int", "tss64", "tss32", "flags")])
+    _check(_L.tre_eval_tss(ev.handle, _ptr(prof), ctypes.byref(o), _stream(stream)))
+
+
+def ctl_outputs(ev: Events, n_scenarios: int, move_cap: int, device="cuda") -> Dict[str, torch.Tensor]:
+    M = ev.n_models
+    return {"moves": torch.zeros(max(1, n_scenarios * move_cap) * MOVE_DTYPE.itemsize, dtype=torch.uint8, device=device),
+            "move_cap": move_cap,
+            "n_moves": torch.zeros(max(1, n_scenarios), dtype=torch.int32, device=device),
+            "r_final": torch.zeros((max(1, n_scenarios), M), dtype=torch.int32, device=device),
+            "r_windows": torch.zeros((max(1, n_scenarios), M), dtype=torch.int64, device=device)}
+
+
+def _ctl(out) -> _CtlOut:
+    return _CtlOut(_ptr(out["moves"]), int(out["move_cap"]), _ptr(out["n_moves"]), _ptr(out["r_final"]),
+                   _ptr(out["r_windows"]))
+
+
+def tre_rebalance(ev: Events, prof: torch.Tensor, tss64: torch.Tensor, flags: torch.Tensor,
+                  sc: torch.Tensor, out: Dict[str, torch.Tensor], stream=None):
+    n_sc = sc.numel() // SCENARIO_DTYPE.itemsize
+    o = _ctl(out)
+    _check(_L.tre_rebalance(ev.handle, _ptr(prof), _ptr(tss64), _ptr(flags), _ptr(sc), n_sc,
+                            ctypes.byref(o), _stream(stream)))
+
+
+def tre_sweep(ev: Events, prof: torch.Tensor, sc: torch.Tensor, out: Dict[str, torch.Tensor],
+              ws: torch.Tensor, tss32: Optional[torch.Tensor] = None, stream=None):
+    n_sc = sc.numel() // SCENARIO_DTYPE.itemsize
+    o = _ctl(out)
+    _check(_L.tre_sweep(ev.handle, _ptr(prof), _ptr(sc), n_sc, ctypes.byref(o), _ptr(tss32), _ptr(ws),
+                        ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def tre_set_timing(enable: bool):
+    _check(_L.tre_set_timing(1 if enable else 0))
+
+
+def tre_kernel_time(kernel: str):
+    ms, n = ctypes.c_double(), ctypes.c_uint64()
+    _check(_L.tre_kernel_time(kernel.encode(), ctypes.byref(ms), ctypes.byref(n)))
+    return ms.value, n.value
