@@ -52,8 +52,9 @@ extern "C" {
 
 /* Maximum models per trace (one wavefront lane per model). */
 #define TRE_MAX_MODELS 64
-/* Maximum events that may fall in one window of one trace (keeps every
-   per-window tally inside its packed 32/40-bit field). */
+/* Maximum events that may fall in one window of one trace; the limit is
+   also at most (2^31 - 1) / window_ms, which keeps every per-window sum
+   inside its packed 32-bit field. */
 #define TRE_MAX_EVENTS_PER_WINDOW 65535
 
 /* ------------------------------------------------------------- events
@@ -173,7 +174,10 @@ const char* tre_last_error(void);
    and unchanged while the handle is used) and CSR trace offsets (host,
    copied: trace i is rows [trace_off[i], trace_off[i+1]) of every column,
    non-decreasing, trace_off[0] >= 0). `cfg` (host) is copied. Column
-   pointers need 16-byte alignment (ts, tokens) or 8-byte (model, type).
+   pointers need 16-byte alignment (ts, tokens) or 8-byte (model, type),
+   and every column must stay readable for 16 bytes past its last row
+   (row trace_off[n_traces] - 1): tile loads are rounded up to 16 bytes.
+   duration_ms must be below 2^32 and a trace below 2^27 events.
    With flags & TRE_VALIDATE the events are checked on the device and the
    call waits for the result (TRE_EORDER, TRE_ESCHEMA, TRE_ERANGE). The
    handle owns small device tables (offsets, tick list); free it with

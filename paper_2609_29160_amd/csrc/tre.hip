@@ -22,6 +22,7 @@
 //   validate    checks the event columns once, at load time.
 #include <hip/hip_runtime.h>
 
+#include <limits.h>
 #include <math.h>
 #include <stdarg.h>
 #include <stdint.h>
@@ -80,12 +81,9 @@ struct tre_events {
 };
 
 // ------------------------------------------------------------ constants
-constexpr int kBlock = 512;                // tss_stream workgroup
-constexpr int kEPT = 8;                    // events per producer lane per tile
-constexpr int kProducers = kBlock - 64;    // wave 0 is the consumer
-constexpr int kTile = kProducers * kEPT;   // events per tile
-constexpr int kRingBytes = 48 * 1024;      // LDS budget of the tally ring
-constexpr uint64_t kOne40 = 1ull << 40;    // packed (count << 40) + integral
+constexpr int kStreamWaves = 4;            // tss_stream workgroup (waves)
+constexpr int kStreamEPT = 4;              // rows per lane per tile
+constexpr int kRingBytes = 24 * 1024;      // LDS budget of the tally ring
 constexpr uint32_t kNoDefer = 0xFFFFFFFFu;
 
 typedef long long v2i64 __attribute__((ext_vector_type(2)));
@@ -106,6 +104,7 @@ struct StreamParams {
   int32_t n_windows;
   int32_t M;
   uint32_t wcap;    // ring windows, power of two
+  int32_t chunk;    // windows evaluated per step (cells <= threads)
   int32_t fast_w;   // fast period in windows
   int32_t slow_w;   // slow period in windows
   int32_t n_ticks;
@@ -131,93 +130,304 @@ __device__ __forceinline__ void div_window(uint32_t rel, uint32_t magic, uint32_
   }
 }
 
-// sign-extended low 40 bits and the count above them
-__device__ __forceinline__ void unpack40(unsigned long long v, long long& count, long long& integ) {
-  long long s = (long long)v;
-  integ = (long long)(v << 24) >> 24;
-  count = (s - integ) >> 40;
+// One producer lane's share of a tile: kEPT consecutive rows.
+template <int kEPT>
+struct Slice {
+  long long ts[kEPT];
+  uint32_t mw[kEPT / 4];  // model bytes, 4 per word
+  uint32_t tw[kEPT / 4];  // type bytes
+  uint32_t kw[kEPT / 2];  // tokens, 2 per word
+};
+
+// Buffer resources over one trace's rows of each column, from its first
+// kEPT-aligned row; a load past the range reads zeros (no fault), so tile
+// loads need no bounds branches and never touch another trace's rows
+// beyond the 16-byte rounding of the range.
+struct TraceRsrc {
+  __amdgpu_buffer_rsrc_t ts, model, type, tokens;
+};
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base, long long bytes) {
+  const long long n = (bytes + 15) & ~15ll;  // columns are readable 16 bytes past the last row
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n, 0x00020000);
 }
 
-__global__ __launch_bounds__(kBlock) void tss_stream(StreamParams p) {
+template <int kEPT>
+__device__ __forceinline__ void load_slice(Slice<kEPT>& s, const TraceRsrc& rs, int r0) {
+  // r0: first row of the lane's slice, relative to the resources' base row
+#pragma unroll
+  for (int j = 0; j < kEPT / 2; ++j) {
+    const v4u32 v = __builtin_bit_cast(
+        v4u32, __builtin_amdgcn_raw_buffer_load_b128(rs.ts, r0 * 8 + 16 * j, 0, 0));
+    s.ts[2 * j] = (long long)(((unsigned long long)v.y << 32) | v.x);
+    s.ts[2 * j + 1] = (long long)(((unsigned long long)v.w << 32) | v.z);
+  }
+  if constexpr (kEPT == 4) {
+    s.mw[0] = __builtin_amdgcn_raw_buffer_load_b32(rs.model, r0, 0, 0);
+    s.tw[0] = __builtin_amdgcn_raw_buffer_load_b32(rs.type, r0, 0, 0);
+    const v2u32 k = __builtin_bit_cast(v2u32, __builtin_amdgcn_raw_buffer_load_b64(rs.tokens, r0 * 2, 0, 0));
+    s.kw[0] = k.x; s.kw[1] = k.y;
+  } else if constexpr (kEPT == 8) {
+    const v2u32 m = __builtin_bit_cast(v2u32, __builtin_amdgcn_raw_buffer_load_b64(rs.model, r0, 0, 0));
+    const v2u32 t = __builtin_bit_cast(v2u32, __builtin_amdgcn_raw_buffer_load_b64(rs.type, r0, 0, 0));
+    const v4u32 k = __builtin_bit_cast(v4u32, __builtin_amdgcn_raw_buffer_load_b128(rs.tokens, r0 * 2, 0, 0));
+    s.mw[0] = m.x; s.mw[1] = m.y;
+    s.tw[0] = t.x; s.tw[1] = t.y;
+    s.kw[0] = k.x; s.kw[1] = k.y; s.kw[2] = k.z; s.kw[3] = k.w;
+  } else {
+    static_assert(kEPT % 16 == 0, "kEPT is 4, 8 or a multiple of 16");
+#pragma unroll
+    for (int j = 0; j < kEPT / 16; ++j) {
+      const v4u32 m = __builtin_bit_cast(v4u32, __builtin_amdgcn_raw_buffer_load_b128(rs.model, r0 + 16 * j, 0, 0));
+      const v4u32 t = __builtin_bit_cast(v4u32, __builtin_amdgcn_raw_buffer_load_b128(rs.type, r0 + 16 * j, 0, 0));
+      s.mw[4 * j] = m.x; s.mw[4 * j + 1] = m.y; s.mw[4 * j + 2] = m.z; s.mw[4 * j + 3] = m.w;
+      s.tw[4 * j] = t.x; s.tw[4 * j + 1] = t.y; s.tw[4 * j + 2] = t.z; s.tw[4 * j + 3] = t.w;
+    }
+#pragma unroll
+    for (int j = 0; j < kEPT / 8; ++j) {
+      const v4u32 k = __builtin_bit_cast(v4u32, __builtin_amdgcn_raw_buffer_load_b128(rs.tokens, r0 * 2 + 16 * j, 0, 0));
+      s.kw[4 * j] = k.x; s.kw[4 * j + 1] = k.y; s.kw[4 * j + 2] = k.z; s.kw[4 * j + 3] = k.w;
+    }
+  }
+}
+
+// Tally the lane's rows in [e0, e_end) whose window fits the ring
+// [cbase, cbase + wcap). Each (window, model) cell holds three 64-bit words:
+//   tokens     P (low 32 bits) | D (high 32 bits)
+//   counts     (dA << 32) + dW          summed over the window's rows
+//   integrals  (dA*te << 32) + dW*te    te = t_end - ts, 1..window_ms
+// with dA = [ADMIT] - [FINISH], dW = [ARRIVE] - [ADMIT]; sums of the signed
+// low halves stay inside 32 bits (events per window * window_ms < 2^31).
+// Every row issues the same three LDS atomics (adding zero when it has
+// nothing to add), so rows need no branches. The first row that does not
+// fit is published in *defer (relative to a0) with its window in *wdef; the
+// lane holding row t_last (the tile's last) stores that row's window in
+// *wlast. Offsets are 32-bit: timestamps are below 2^32 ms.
+template <int kEPT>
+__device__ __forceinline__ void tally_slice(const Slice<kEPT>& s, int c0, int a0, int e0, int e_end,
+                                            int t_last, int cbase, uint32_t base_lo, uint32_t cap,
+                                            uint32_t magic, uint32_t win32, uint32_t wmask, int M,
+                                            int ncell, unsigned long long* ring, unsigned* defer,
+                                            int* wdef, int* wlast) {
+  // row indices are relative to the trace's aligned first row
+  const int lo0 = e0 - c0, hi0 = e_end - c0, l0 = t_last - c0;
+  const int lo = lo0 < 0 ? 0 : (lo0 > kEPT ? kEPT : lo0);
+  const int hi = hi0 < 0 ? 0 : (hi0 > kEPT ? kEPT : hi0);
+  const int jl = (l0 >= 0 && l0 < kEPT) ? l0 : -1;
+  const uint32_t vmask = ((1u << hi) - 1u) & ~((1u << lo) - 1u);  // rows in [e0, e_end)
+  int jdef = kEPT;  // first row that does not fit the ring
+  int wdf = INT_MAX, wlt = -1;
+  uint32_t* pd32 = (uint32_t*)ring;  // token words
+#pragma unroll
+  for (int j = 0; j < kEPT; ++j) {
+    const uint32_t d = (uint32_t)s.ts[j] - base_lo;
+    uint32_t q, r;
+    div_window(d, magic, win32, q, r);
+    const uint32_t mdl = (s.mw[j >> 2] >> (8 * (j & 3))) & 0xFFu;
+    const uint32_t ty = (s.tw[j >> 2] >> (8 * (j & 3))) & 0xFFu;
+    const uint32_t tok = (s.kw[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
+    // the high dword and model checks only fail on unvalidated input
+    const bool row = ((vmask >> j) & 1u) && ((unsigned long long)s.ts[j] >> 32) == 0 && jdef == kEPT;
+    const bool over = row && d >= cap;
+    if (over) {
+      jdef = j;
+      wdf = cbase + (int)q;
+    }
+    const bool ok = row && !over && mdl < (uint32_t)M;
+    const int w = cbase + (int)q;
+    if (ok && j == jl) wlt = w;
+    const int c = (int)((uint32_t)w & wmask) * M + (int)(mdl < (uint32_t)M ? mdl : 0u);
+    const uint32_t kind = ty & 3u;
+    const bool admit = (ty & TRE_ADMIT) != 0;
+    const bool tk = ok && (kind == TRE_PREFILL || kind == TRE_DECODE);
+    const int dA = !ok ? 0 : (admit ? 1 : (kind == TRE_FINISH ? -1 : 0));
+    const int dW = !ok ? 0 : (kind == TRE_ARRIVE ? 1 : (admit ? -1 : 0));
+    const int te = (int)(win32 - r);
+    const int iA = dA > 0 ? te : (dA < 0 ? -te : 0);  // dA * te without a multiply
+    const int iW = dW > 0 ? te : (dW < 0 ? -te : 0);
+    const unsigned long long cnt = ((unsigned long long)(long long)dA << 32) + (unsigned long long)(long long)dW;
+    const unsigned long long itg = ((unsigned long long)(long long)iA << 32) + (unsigned long long)(long long)iW;
+    atomicAdd(&pd32[2 * c + (kind == TRE_DECODE ? 1 : 0)], tk ? tok : 0u);
+    atomicAdd(&ring[ncell + c], cnt);
+    atomicAdd(&ring[2 * ncell + c], itg);
+  }
+  if (wlt >= 0) *wlast = wlt;
+  if (__ballot(jdef < kEPT)) {  // rare: some row of this wave waits for a later tile
+    if (jdef < kEPT) {
+      atomicMin(defer, (unsigned)(c0 + jdef - a0));
+      atomicMin(wdef, wdf);
+    }
+  }
+}
+
+// a packed (high << 32) + signed low word: the signed low half and the high
+// half it leaves after removing the low half's sign extension
+__device__ __forceinline__ void unpack32(unsigned long long v, int& hi, int& lo) {
+  lo = (int)(uint32_t)v;
+  hi = (int)(uint32_t)(v >> 32) + (int)((uint32_t)v >> 31);
+}
+
+// tick bookkeeping for one window: returns the tick ordinal or -1
+__device__ __forceinline__ int next_tick(int& fctr, int& sctr, int& tick, int fast_w, int slow_w) {
+  ++fctr;
+  ++sctr;
+  const bool fast = fctr == fast_w;
+  const bool slow = sctr == slow_w;
+  if (fast) fctr = 0;
+  if (slow) sctr = 0;
+  if (fast || slow) return tick++;
+  return -1;
+}
+
+// One workgroup per trace; every thread tallies and evaluates, one barrier
+// per step. Step k, with [cA, cB) the chunk evaluated in step k-1 and
+// [cB, cC), cC = min(wl, cB + C), the windows completed by earlier tiles:
+//   - issue the loads of tile k+1, tally tile k into the LDS ring;
+//   - evaluate [cB, cC), one (window, model) cell per thread: carry prefix
+//     over the chunk, window integrals, Eq. (1) -> raw ratio and idle flag
+//     staged in LDS (two staging buffers, by step parity);
+//   - wave 0 runs the smoothing chain over [cA, cB) from the other buffer;
+//   - clear the ring cells of [cA, cB);
+//   -- barrier -- the tile's rows are in; windows < wl are complete.
+// Ring slots in use are windows [cA, cA + wcap): rows whose window reaches
+// cA + wcap wait for a later tile, so a slot is never tallied while its
+// window is being evaluated, smoothed or cleared. Tile rows come after
+// every row of a complete window, so they never land in [cA, cC).
+template <int kWaves, int kEPT, bool kCells>
+__global__ __launch_bounds__(kWaves * 64) void tss_stream(StreamParams p) {
+  constexpr int kThreads = kWaves * 64;
+  constexpr long long kTile = (long long)kThreads * kEPT;
   extern __shared__ unsigned long long ring[];
-  __shared__ long long s_e;
-  __shared__ int s_wdone;
-  __shared__ int s_wnext;
-  __shared__ unsigned s_defer;
+  __shared__ long long s_carry[2][2][TRE_MAX_MODELS];  // [parity][active, waiting][model]
+  __shared__ double s_S[TRE_MAX_MODELS];               // smoothed TSS per model
+  __shared__ double s_alpha[TRE_MAX_MODELS];
+  __shared__ uint8_t s_init[TRE_MAX_MODELS];
+  __shared__ int s_tick[3];                            // fast / slow counters, tick ordinal
+  __shared__ unsigned s_defer[3];
+  __shared__ int s_wdef[3];
+  __shared__ int s_wlast[3];  // window of the tile's last row
 
   const int trace = blockIdx.x;
   const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const bool consumer = tid < 64;
   const int M = p.M;
   const uint32_t wcap = p.wcap;
+  const int C = p.chunk;
   const int ncell = (int)wcap * M;
-  unsigned long long* r_pd = ring;              // P (low 32) | D (high 32)
-  unsigned long long* r_a = ring + ncell;       // (dA << 40) + dA*(t_end - ts)
-  unsigned long long* r_w = ring + 2 * ncell;   // (dW << 40) + dW*(t_end - ts)
-  const int64_t e_begin = p.off[trace];
-  const int64_t e_end = p.off[trace + 1];
-  const int64_t win = p.window_ms;
+  unsigned long long* r_pd = ring;              // tokens: P (low 32) | D (high 32)
+  unsigned long long* r_a = ring + ncell;       // counts: (dA << 32) + dW
+  unsigned long long* r_w = ring + 2 * ncell;   // integrals: (dA*te << 32) + dW*te
+  // [2][C][M] staged raw ratios (>= 0), -1 marks an idle window
+  double* st_raw = (double*)(ring + 3 * ncell);
+  const long long e_begin = p.off[trace];
+  const long long e_end = p.off[trace + 1];
+  const long long win = p.window_ms;
   const uint32_t win32 = (uint32_t)win;
+  const double dwin = (double)win;
   const int nW = p.n_windows;
+  constexpr bool cells = kCells;
 
-  for (int i = tid; i < 3 * ncell; i += kBlock) ring[i] = 0ull;
-  if (tid == 0) {
-    s_e = e_begin;
-    s_wdone = 0;
-    s_defer = kNoDefer;
+  for (int i = tid; i < 3 * ncell; i += kThreads) ring[i] = 0ull;
+  for (int i = tid; i < 2 * 2 * TRE_MAX_MODELS; i += kThreads) (&s_carry[0][0][0])[i] = 0;
+  if (tid < 3) {
+    s_defer[tid] = kNoDefer;
+    s_wdef[tid] = INT_MAX;
+    s_wlast[tid] = -1;
   }
 
-  // consumer state: lane m owns model m
-  const bool own = consumer && lane < M;
-  long long a_start = 0, w_start = 0;
-  double S = 0.0;
-  bool init = false;
-  double w_p = 0.0, w_q = 0.0, alpha = 0.0, oma = 0.0;
-  if (own) {
-    const tre_profile pr = p.prof[(int64_t)trace * M + lane];
+  // the cell this thread evaluates: model rm, window offset rj in the chunk
+  // (C is a power of two and C * M <= threads)
+  const int rm = tid / C, rj = tid & (C - 1);
+  const bool r_thread = rm < M;
+  double w_p = 0.0, w_q = 0.0;
+  if (r_thread) {
+    const tre_profile pr = p.prof[(int64_t)trace * M + rm];
     w_p = pr.w_p;
     w_q = pr.w_q;
-    alpha = pr.alpha;
-    oma = 1.0 - alpha;
   }
-  int fctr = 0, sctr = 0, tick = 0;
-  const double dwin = (double)win;
-  const bool cells = p.prefill || p.decode || p.a_int || p.w_int || p.tss64 || p.tss32 || p.flags;
+  // smoothing chain: one wave per step (rotating), lane m owns model m; its
+  // state lives in LDS between steps
+  if (tid < M) {
+    s_alpha[tid] = p.prof[(int64_t)trace * M + tid].alpha;
+    s_S[tid] = 0.0;
+    s_init[tid] = 0;
+  }
+  if (tid < 3) s_tick[tid] = 0;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63;
 
+  // rows are counted from the trace's first kEPT-aligned row (below 2^27)
+  const long long brow = e_begin & ~(long long)(kEPT - 1);
+  const int rend = (int)(e_end - brow);  // one past the trace's last row
+  int e0 = (int)(e_begin - brow);        // first row not yet tallied
+  int cA = 0, cB = 0, wl = 0;
+  TraceRsrc rs;
+  rs.ts = rsrc(p.ts + brow, (long long)rend * 8);
+  rs.model = rsrc(p.model + brow, rend);
+  rs.type = rsrc(p.type + brow, rend);
+  rs.tokens = rsrc(p.tokens + brow, (long long)rend * 2);
+  Slice<kEPT> buf0, buf1;
+  int held = 0;  // tile base held by the current buffer
+  load_slice<kEPT>(buf0, rs, tid * kEPT);
   __syncthreads();
-  for (;;) {
-    const long long e0 = s_e;
-    const int wd = s_wdone;
-    if (wd >= nW) break;
-    if (consumer) {
-      // windows before the first unprocessed event are complete
-      long long wl64 = nW;
-      if (e0 < e_end) wl64 = p.ts[e0] / win;
-      // never backwards, never past the last window (only matters for
-      // unvalidated, unsorted input)
-      const int wl = (int)(wl64 < wd ? wd : (wl64 > nW ? nW : wl64));
-      for (int w = wd; w < wl; ++w) {
-        unsigned long long pd = 0, ap = 0, wp = 0;
-        if (own && w < wd + (int)wcap) {
-          const int c = (int)((uint32_t)w & (wcap - 1)) * M + lane;
-          pd = r_pd[c];
-          ap = r_a[c];
-          wp = r_w[c];
-          r_pd[c] = 0ull;
-          r_a[c] = 0ull;
-          r_w[c] = 0ull;
+
+  // one step; returns true when every window has been smoothed
+  auto step = [&](Slice<kEPT>& cur, Slice<kEPT>& nxt, int k) -> bool {
+    if (cA >= nW) return true;
+    const int b3 = k % 3;
+    // ---- tally tile k (tile k+1 loading meanwhile), capacity [cA, cA + wcap)
+    const int a0 = e0 & ~(kEPT - 1);
+    if (held != a0) load_slice<kEPT>(cur, rs, a0 + tid * kEPT);  // prefetch missed
+    const int pref = a0 + (int)kTile;
+    load_slice<kEPT>(nxt, rs, pref + tid * kEPT);  // zeros past the trace
+    const int t_last = (pref < rend ? pref : rend) - 1;
+    tally_slice<kEPT>(cur, a0 + tid * kEPT, a0, e0, rend, t_last, cA,
+                      (uint32_t)((long long)cA * win), wcap * win32, p.magic, win32, wcap - 1, M,
+                      ncell, ring, &s_defer[b3], &s_wdef[b3], &s_wlast[b3]);
+    // ---- evaluate [cB, cC), one cell per thread (groups of C lanes per model)
+    const int cC = wl < cB + C ? wl : cB + C;
+    const int n = cC - cB;
+    const long long* cin = s_carry[k & 1][0];
+    long long* cout = s_carry[(k + 1) & 1][0];
+    double* sr = st_raw + (k & 1) * C * M;
+    if (r_thread) {  // uniform over each group of C lanes
+      const bool valid = rj < n;
+      unsigned long long pd = 0, ap = 0, wp = 0;
+      if (valid) {
+        const int c = (int)((uint32_t)(cB + rj) & (wcap - 1)) * M + rm;
+        pd = r_pd[c];
+        ap = r_a[c];
+        wp = r_w[c];
+      }
+      int ca, cw, la32, lw32;
+      unpack32(ap, ca, cw);      // counts word
+      unpack32(wp, la32, lw32);  // integrals word
+      int ia = ca, iw = cw;  // inclusive prefix over the chunk's windows
+      if (C <= 16) {
+        // row shifts by 1, 2, 4, 8 lanes; groups are aligned inside a row
+        if (C > 1) { const int ya = __builtin_amdgcn_update_dpp(0, ia, 0x111, 0xF, 0xF, false), yw = __builtin_amdgcn_update_dpp(0, iw, 0x111, 0xF, 0xF, false); if (rj >= 1) { ia += ya; iw += yw; } }
+        if (C > 2) { const int ya = __builtin_amdgcn_update_dpp(0, ia, 0x112, 0xF, 0xF, false), yw = __builtin_amdgcn_update_dpp(0, iw, 0x112, 0xF, 0xF, false); if (rj >= 2) { ia += ya; iw += yw; } }
+        if (C > 4) { const int ya = __builtin_amdgcn_update_dpp(0, ia, 0x114, 0xF, 0xF, false), yw = __builtin_amdgcn_update_dpp(0, iw, 0x114, 0xF, 0xF, false); if (rj >= 4) { ia += ya; iw += yw; } }
+        if (C > 8) { const int ya = __builtin_amdgcn_update_dpp(0, ia, 0x118, 0xF, 0xF, false), yw = __builtin_amdgcn_update_dpp(0, iw, 0x118, 0xF, 0xF, false); if (rj >= 8) { ia += ya; iw += yw; } }
+      } else {
+        for (int dd = 1; dd < C; dd <<= 1) {
+          const int ya = __shfl_up(ia, dd, C);
+          const int yw = __shfl_up(iw, dd, C);
+          if (rj >= dd) {
+            ia += ya;
+            iw += yw;
+          }
         }
-        long long na, la, nw, lw;
-        unpack40(ap, na, la);
-        unpack40(wp, nw, lw);
-        const long long A_int = a_start * win + la;
-        const long long W_int = w_start * win + lw;
-        a_start += na;
-        w_start += nw;
-        const uint32_t P = (uint32_t)pd;
-        const uint32_t Dt = (uint32_t)(pd >> 32);
+      }
+      if (valid) {
+        const int w = cB + rj;
+        const long long la = la32, lw = lw32;
+        const long long A0 = cin[rm] + (ia - ca), W0 = cin[TRE_MAX_MODELS + rm] + (iw - cw);
+        // counts are below 2^31 and windows below 2^23 ms: 32x32->64 products
+        const long long A_int = (long long)(int)A0 * (long long)(int)win + la;
+        const long long W_int = (long long)(int)W0 * (long long)(int)win + lw;
+        const uint32_t P = (uint32_t)pd, Dt = (uint32_t)(pd >> 32);
         const bool idle = pd == 0ull && A_int == 0 && W_int == 0;
+        double raw = 0.0;
         if (!idle) {
           // Eq. (1), evaluated in the documented order
           double num = w_p * (double)P;
@@ -226,131 +436,115 @@ __global__ __launch_bounds__(kBlock) void tss_stream(StreamParams p) {
           const double q = w_q * (double)W_int;
           double den = (double)A_int + q;
           if (den < dwin) den = dwin;
-          const double raw = num / den;
-          if (init) {
+          raw = num / den;
+        }
+        sr[rj * M + rm] = idle ? -1.0 : raw;
+        if (cells) {
+          const int64_t o = ((int64_t)trace * nW + w) * M + rm;
+          if (p.prefill) p.prefill[o] = P;
+          if (p.decode) p.decode[o] = Dt;
+          if (p.a_int) p.a_int[o] = A_int;
+          if (p.w_int) p.w_int[o] = W_int;
+        }
+        if (rj == n - 1) {
+          cout[rm] = cin[rm] + ia;
+          cout[TRE_MAX_MODELS + rm] = cin[TRE_MAX_MODELS + rm] + iw;
+        }
+      }
+    }
+    if (n == 0 && tid < M) {
+      cout[tid] = cin[tid];
+      cout[TRE_MAX_MODELS + tid] = cin[TRE_MAX_MODELS + tid];
+    }
+    // ---- smooth [cA, cB) (staged last step); wave k mod kWaves, lanes < M
+    if (wave == k % kWaves && cB > cA) {
+      const bool own = lane < M;
+      const int m = own ? lane : 0;
+      const double* pr = st_raw + ((k + 1) & 1) * C * M + m;
+      const double alpha = s_alpha[m];
+      const double oma = 1.0 - alpha;
+      double S = s_S[m];
+      bool init = s_init[m] != 0;
+      int fctr = s_tick[0], sctr = s_tick[1], tick = s_tick[2];
+      const int nw = cB - cA;
+      for (int u0 = 0; u0 < nw; u0 += 4) {
+        double rv[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) rv[u] = pr[((u0 + u) & (C - 1)) * M];  // past nw: unused
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          if (u0 + u < nw) {
+            const int w = cA + u0 + u;
+            const double raw = rv[u];
+            const bool idle = raw < 0.0;
             const double t1 = alpha * raw;
             const double t2 = oma * S;
-            S = t1 + t2;
-          } else {
-            S = raw;
-            init = true;
-          }
-        }
-        if (own && cells) {
-          const int64_t c = ((int64_t)trace * nW + w) * M + lane;
-          if (p.prefill) p.prefill[c] = P;
-          if (p.decode) p.decode[c] = Dt;
-          if (p.a_int) p.a_int[c] = A_int;
-          if (p.w_int) p.w_int[c] = W_int;
-          if (p.tss64) p.tss64[c] = S;
-          if (p.tss32) p.tss32[c] = (float)S;
-          if (p.flags) p.flags[c] = (uint8_t)((idle ? TRE_FLAG_IDLE : 0) | (init ? TRE_FLAG_INIT : 0));
-        }
-        ++fctr;
-        ++sctr;
-        const bool fast = fctr == p.fast_w;
-        const bool slow = sctr == p.slow_w;
-        if (fast) fctr = 0;
-        if (slow) sctr = 0;
-        if (fast || slow) {
-          if (own && p.snap && tick < p.n_ticks)
-            p.snap[((int64_t)trace * p.n_ticks + tick) * M + lane] = (idle || !init) ? INFINITY : S;
-          ++tick;
-        }
-      }
-      if (lane == 0) s_wnext = wl;
-    } else {
-      // producers: events [max(e0, a0), min(a0 + tile, e_end)) whose window
-      // fits the ring; the first that does not is where the next tile starts
-      const int pt = tid - 64;
-      const long long a0 = e0 & ~(long long)(kEPT - 1);
-      const long long c0 = a0 + (long long)pt * kEPT;
-      if (c0 + kEPT > e0 && c0 < e_end) {
-        long long tsv[kEPT];
-        uint32_t mw[2], tw[2], kw[4];
-        if (c0 + kEPT <= p.n_rows) {
-          const v2i64* tp = (const v2i64*)(p.ts + c0);
-#pragma unroll
-          for (int j = 0; j < kEPT / 2; ++j) {
-            v2i64 v = __builtin_nontemporal_load(tp + j);
-            tsv[2 * j] = v.x;
-            tsv[2 * j + 1] = v.y;
-          }
-          v2u32 mv = __builtin_nontemporal_load((const v2u32*)(p.model + c0));
-          v2u32 tv = __builtin_nontemporal_load((const v2u32*)(p.type + c0));
-          v4u32 kv = __builtin_nontemporal_load((const v4u32*)(p.tokens + c0));
-          mw[0] = mv.x; mw[1] = mv.y;
-          tw[0] = tv.x; tw[1] = tv.y;
-          kw[0] = kv.x; kw[1] = kv.y; kw[2] = kv.z; kw[3] = kv.w;
-        } else {
-          // ragged end of the columns: element loads inside [0, n_rows)
-          mw[0] = mw[1] = tw[0] = tw[1] = 0;
-          kw[0] = kw[1] = kw[2] = kw[3] = 0;
-#pragma unroll
-          for (int j = 0; j < kEPT; ++j) {
-            const long long i = c0 + j;
-            tsv[j] = 0;
-            if (i < p.n_rows) {
-              tsv[j] = p.ts[i];
-              mw[j >> 2] |= (uint32_t)p.model[i] << (8 * (j & 3));
-              tw[j >> 2] |= (uint32_t)p.type[i] << (8 * (j & 3));
-              kw[j >> 1] |= (uint32_t)p.tokens[i] << (16 * (j & 1));
+            const double Sn = t1 + t2;
+            S = idle ? S : (init ? Sn : raw);
+            init = init || !idle;
+            if (cells && own) {
+              const int64_t c = ((int64_t)trace * nW + w) * M + m;
+              if (p.tss64) p.tss64[c] = S;
+              if (p.tss32) p.tss32[c] = (float)S;
+              if (p.flags) p.flags[c] = (uint8_t)((idle ? TRE_FLAG_IDLE : 0) | (init ? TRE_FLAG_INIT : 0));
             }
-          }
-        }
-        const long long base_ms = (long long)wd * win;
-        const long long cap_ms = (long long)wcap * win;
-#pragma unroll
-        for (int j = 0; j < kEPT; ++j) {
-          const long long i = c0 + j;
-          if (i < e0 || i >= e_end) continue;
-          const int mdl = (mw[j >> 2] >> (8 * (j & 3))) & 0xFF;
-          const uint32_t ty = (tw[j >> 2] >> (8 * (j & 3))) & 0xFF;
-          const uint32_t tok = (kw[j >> 1] >> (16 * (j & 1))) & 0xFFFF;
-          const long long d = tsv[j] - base_ms;
-          if (d >= cap_ms) {
-            atomicMin(&s_defer, (unsigned)(i - a0));
-            break;  // later events of this lane are not earlier
-          }
-          if (d < 0 || mdl >= M) continue;  // only reachable with unvalidated input
-          uint32_t q, r;
-          div_window((uint32_t)d, p.magic, win32, q, r);
-          const int c = (int)(((uint32_t)wd + q) & (wcap - 1)) * M + mdl;
-          const unsigned long long one = kOne40 + (unsigned long long)(win32 - r);
-          switch (ty & 3u) {
-            case TRE_ARRIVE:
-              atomicAdd(&r_w[c], one);
-              break;
-            case TRE_PREFILL:
-              atomicAdd(&r_pd[c], (unsigned long long)tok);
-              if (ty & TRE_ADMIT) {
-                atomicAdd(&r_w[c], 0ull - one);
-                atomicAdd(&r_a[c], one);
-              }
-              break;
-            case TRE_DECODE:
-              atomicAdd(&r_pd[c], (unsigned long long)tok << 32);
-              break;
-            default:
-              atomicAdd(&r_a[c], 0ull - one);
-              break;
+            const int tk = next_tick(fctr, sctr, tick, p.fast_w, p.slow_w);
+            if (own && tk >= 0 && p.snap && tk < p.n_ticks)
+              p.snap[((int64_t)trace * p.n_ticks + tk) * M + m] = (idle || !init) ? INFINITY : S;
           }
         }
       }
+      if (own) {
+        s_S[m] = S;
+        s_init[m] = init ? 1 : 0;
+      }
+      if (lane == 0) {
+        s_tick[0] = fctr;
+        s_tick[1] = sctr;
+        s_tick[2] = tick;
+      }
     }
-    __syncthreads();
+    // ---- clear [cA, cB)
+    const int nclr = (cB - cA) * M;
+    for (int i = tid; i < nclr; i += kThreads) {
+      const int c = (int)((uint32_t)(cA + i / M) & (wcap - 1)) * M + (i % M);
+      r_pd[c] = 0ull;
+      r_a[c] = 0ull;
+      r_w[c] = 0ull;
+    }
     if (tid == 0) {
-      const long long a0 = e0 & ~(long long)(kEPT - 1);
-      long long en = a0 + kTile;
-      if (en > e_end) en = e_end;
-      if (en < e0) en = e0;
-      const unsigned dfr = s_defer;
-      if (dfr != kNoDefer) en = a0 + dfr;
-      s_e = en;
-      s_wdone = s_wnext;
-      s_defer = kNoDefer;
+      const int r = (k + 2) % 3;
+      s_defer[r] = kNoDefer;
+      s_wdef[r] = INT_MAX;
+      s_wlast[r] = -1;
     }
     __syncthreads();
+    // ---- the next tile and the completeness bound (same on every thread;
+    // shared scalars are read into scalar registers)
+    const unsigned dfr = (unsigned)__builtin_amdgcn_readfirstlane((int)s_defer[b3]);
+    int en = a0 + (int)kTile;
+    if (en > rend) en = rend;
+    if (en < e0) en = e0;
+    int wn;
+    if (dfr != kNoDefer) {
+      en = a0 + dfr;
+      wn = __builtin_amdgcn_readfirstlane(s_wdef[b3]);
+    } else if (en >= rend) {
+      wn = nW;
+    } else {
+      wn = __builtin_amdgcn_readfirstlane(s_wlast[b3]);
+    }
+    wn = wn > nW ? nW : wn;
+    e0 = en;
+    wl = wn < wl ? wl : wn;
+    held = pref;
+    cA = cB;
+    cB = cC;
+    return false;
+  };
+  for (int k = 0;; k += 2) {
+    if (step(buf0, buf1, k)) break;
+    if (step(buf1, buf0, k + 1)) break;
   }
 }
 
@@ -366,7 +560,6 @@ struct CtlParams {
   int32_t n_ticks;
   int32_t n_windows;
   int32_t M;
-  int32_t g_log2;
   int32_t budget;
   uint32_t n_traces;
   tre_move* moves;
@@ -380,27 +573,61 @@ __device__ __forceinline__ unsigned long long dbits(double x) {
   return (unsigned long long)__double_as_longlong(x);
 }
 
+// lane permutations pairing lanes across groups of 2, 4, 8, 16 and 32 (DPP
+// quad_perm / half-row mirror / row mirror, then an LDS swizzle)
+template <int kStep>
+__device__ __forceinline__ uint32_t lane_pair(uint32_t x) {
+  if constexpr (kStep == 1) return (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, 0xB1, 0xF, 0xF, false);
+  else if constexpr (kStep == 2) return (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x4E, 0xF, 0xF, false);
+  else if constexpr (kStep == 4) return (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x141, 0xF, 0xF, false);
+  else if constexpr (kStep == 8) return (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x140, 0xF, 0xF, false);
+  else return (uint32_t)__builtin_amdgcn_ds_swizzle((int)x, 0x401F);  // lane ^ 16 within 32
+}
+
+template <bool kMax, int kStep>
+__device__ __forceinline__ unsigned long long key_step(unsigned long long key) {
+  const uint32_t lo = lane_pair<kStep>((uint32_t)key);
+  const uint32_t hi = lane_pair<kStep>((uint32_t)(key >> 32));
+  const unsigned long long o = ((unsigned long long)hi << 32) | lo;
+  return kMax ? (o > key ? o : key) : (o < key ? o : key);
+}
+
+// min / max of a 64-bit key over each aligned group of G lanes
+template <bool kMax, int G>
+__device__ __forceinline__ unsigned long long group_reduce(unsigned long long key) {
+  if constexpr (G >= 2) key = key_step<kMax, 1>(key);
+  if constexpr (G >= 4) key = key_step<kMax, 2>(key);
+  if constexpr (G >= 8) key = key_step<kMax, 4>(key);
+  if constexpr (G >= 16) key = key_step<kMax, 8>(key);
+  if constexpr (G >= 32) key = key_step<kMax, 16>(key);
+  if constexpr (G == 64) {
+    const unsigned long long a =
+        ((unsigned long long)(uint32_t)__builtin_amdgcn_readlane((int)(key >> 32), 0) << 32) |
+        (uint32_t)__builtin_amdgcn_readlane((int)key, 0);
+    const unsigned long long b =
+        ((unsigned long long)(uint32_t)__builtin_amdgcn_readlane((int)(key >> 32), 32) << 32) |
+        (uint32_t)__builtin_amdgcn_readlane((int)key, 32);
+    key = kMax ? (a > b ? a : b) : (a < b ? a : b);
+  }
+  return key;
+}
+
 // lowest lane of the group holding the minimum (or maximum) Z among
 // candidates; Z >= 0 so its bit pattern orders like its value; -1 if none
-template <bool kMax>
-__device__ __forceinline__ int group_arg(bool cand, double Z, int G, int gbase,
-                                         unsigned long long gmask) {
+template <bool kMax, int G>
+__device__ __forceinline__ int group_arg(bool cand, double Z, int gbase, unsigned long long gmask) {
   const unsigned long long any = __ballot(cand) & gmask;
   if (any == 0ull) return -1;
-  unsigned long long key = cand ? dbits(Z) : (kMax ? 0ull : ~0ull);
-  for (int off = G >> 1; off > 0; off >>= 1) {
-    const unsigned long long o = __shfl_xor(key, off, G);
-    key = kMax ? (o > key ? o : key) : (o < key ? o : key);
-  }
+  const unsigned long long key = group_reduce<kMax, G>(cand ? dbits(Z) : (kMax ? 0ull : ~0ull));
   const unsigned long long win = __ballot(cand && dbits(Z) == key) & gmask;
   return __ffsll((long long)win) - 1 - gbase;
 }
 
+template <int G>
 __global__ __launch_bounds__(256) void rebalance(CtlParams p) {
   const int lane = threadIdx.x & 63;
-  const int G = 1 << p.g_log2;
   const uint32_t wave = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;
-  const uint32_t s = wave * (uint32_t)(64 >> p.g_log2) + (uint32_t)(lane >> p.g_log2);
+  const uint32_t s = wave * (uint32_t)(64 / G) + (uint32_t)(lane / G);
   const int m = lane & (G - 1);
   const int gbase = lane & ~(G - 1);
   const unsigned long long gmask = G == 64 ? ~0ull : (((1ull << G) - 1ull) << gbase);
@@ -428,27 +655,31 @@ __global__ __launch_bounds__(256) void rebalance(CtlParams p) {
     r_min = pr.r_min;
   }
   int rsum = R;
+#pragma unroll
   for (int off = G >> 1; off > 0; off >>= 1) rsum += __shfl_xor(rsum, off, G);
   int pool = p.budget - rsum;
   long long rw = 0;
   int wprev = -1;
   uint32_t nm = 0;
 
+  // value of tick t for this lane: S, or +inf when idle / not initialised
+  auto tick_value = [&](int t) -> double {
+    if (!act || t >= p.n_ticks) return INFINITY;
+    if (p.flags) {
+      const int64_t c = ((int64_t)trace * p.n_windows + p.tick_window[t]) * M + m;
+      const uint8_t f = p.flags[c];
+      return ((f & TRE_FLAG_IDLE) || !(f & TRE_FLAG_INIT)) ? INFINITY : p.vals[c];
+    }
+    return p.vals[((int64_t)trace * p.n_ticks + t) * M + m];
+  };
+  double v_next = tick_value(0);
+
   for (int t = 0; t < p.n_ticks; ++t) {
     const int w = (int)p.tick_window[t];
     const uint32_t kind = p.tick_kind[t];
-    double Z = INFINITY;
-    if (act) {
-      double v;
-      if (p.flags) {
-        const int64_t c = ((int64_t)trace * p.n_windows + w) * M + m;
-        const uint8_t f = p.flags[c];
-        v = ((f & TRE_FLAG_IDLE) || !(f & TRE_FLAG_INIT)) ? INFINITY : p.vals[c];
-      } else {
-        v = p.vals[((int64_t)trace * p.n_ticks + t) * M + m];
-      }
-      Z = v / theta_eff;  // Eq. (2)
-    }
+    const double v = v_next;
+    v_next = tick_value(t + 1);  // in flight during this tick's decisions
+    const double Z = act ? v / theta_eff : INFINITY;  // Eq. (2)
     rw += (long long)R * (w - wprev);
     wprev = w;
     const bool crit = act && Z < tau_c;
@@ -468,7 +699,7 @@ __global__ __launch_bounds__(256) void rebalance(CtlParams p) {
     }
     bool used = false;
     for (uint32_t k = 0; k < K; ++k) {
-      const int r = group_arg<false>(ok && !used, Z, G, gbase, gmask);  // Eq. (3)
+      const int r = group_arg<false, G>(ok && !used, Z, gbase, gmask);  // Eq. (3)
       if (r < 0) break;
       const double Zr = __shfl(Z, r, G);
       int d;
@@ -477,8 +708,8 @@ __global__ __launch_bounds__(256) void rebalance(CtlParams p) {
         d = TRE_DONOR_POOL;
       } else {
         const bool cd = act && !used && m != r && R > r_min && Z > Zr && !crit;
-        d = group_arg<true>(cd && sur, Z, G, gbase, gmask);
-        if (d < 0) d = group_arg<true>(cd && !sur, Z, G, gbase, gmask);
+        d = group_arg<true, G>(cd && sur, Z, gbase, gmask);
+        if (d < 0) d = group_arg<true, G>(cd && !sur, Z, gbase, gmask);
         if (d < 0) break;
         if (m == d) {
           R -= 1;
@@ -519,6 +750,7 @@ struct ValParams {
   int64_t duration_ms;
   int64_t window_ms;
   int32_t M;
+  int64_t max_per_window;
   unsigned* err;             // bit 0 order, bit 1 schema, bit 2 range
   unsigned long long* first; // lowest failing row
 };
@@ -537,7 +769,7 @@ __global__ __launch_bounds__(256) void validate(ValParams p) {
       unsigned bad = 0;
       if (t_i < 0 || t_i >= p.duration_ms || (i > b && t_i < p.ts[i - 1])) bad |= 1u;
       if (p.model[i] >= p.M || (ty & 0x7Cu) || ((ty & TRE_ADMIT) && (ty & 3u) != TRE_PREFILL)) bad |= 2u;
-      const int64_t j = i + TRE_MAX_EVENTS_PER_WINDOW;
+      const int64_t j = i + p.max_per_window;
       if (!(bad & 1u) && j < e && p.ts[j] / p.window_ms == t_i / p.window_ms) bad |= 4u;
       if (bad) {
         atomicOr(p.err, bad);
@@ -622,10 +854,30 @@ static int check_device(const tre_events* ev) {
   return TRE_OK;
 }
 
+// events one window of one trace may hold: the packed per-window sums stay
+// inside their 32-bit halves
+static int64_t max_events_per_window(int64_t window_ms) {
+  const int64_t by_integral = 2147483647ll / window_ms;
+  return by_integral < TRE_MAX_EVENTS_PER_WINDOW ? by_integral : TRE_MAX_EVENTS_PER_WINDOW;
+}
+
 static uint32_t ring_windows(int M) {
   uint32_t w = 256;
   while (w > 2 && (size_t)3 * w * (size_t)M * 8 > (size_t)kRingBytes) w >>= 1;
   return w;
+}
+
+// windows evaluated per step: a power of two, one cell per thread, at most
+// half the ring
+static int chunk_windows(int M, uint32_t wcap) {
+  int c = 32;
+  while (c > 1 && (c * M > kStreamWaves * 64 || c > (int)wcap / 2)) c >>= 1;
+  return c;
+}
+
+static size_t stream_lds(const tre_events* ev) {
+  const size_t M = (size_t)ev->cfg.n_models, C = (size_t)chunk_windows(ev->cfg.n_models, ev->wcap);
+  return 3 * ev->wcap * M * 8 + 2 * C * M * 8;
 }
 
 extern "C" int tre_load_events(const int64_t* ts, const uint8_t* model, const uint32_t* req,
@@ -646,6 +898,7 @@ extern "C" int tre_load_events(const int64_t* ts, const uint8_t* model, const ui
     return fail(TRE_EINVAL, "window_ms %lld outside [1, 2^23]", (long long)c.window_ms);
   if (c.duration_ms <= 0 || c.duration_ms % c.window_ms)
     return fail(TRE_EINVAL, "duration_ms must be a positive multiple of window_ms");
+  if (c.duration_ms >= (1ll << 32)) return fail(TRE_EINVAL, "duration_ms must be below 2^32");
   if (c.duration_ms / c.window_ms > (1ll << 30)) return fail(TRE_EINVAL, "too many windows");
   if (c.fast_period_ms <= 0 || c.slow_period_ms <= 0 || c.fast_period_ms % c.window_ms ||
       c.slow_period_ms % c.window_ms)
@@ -656,8 +909,8 @@ extern "C" int tre_load_events(const int64_t* ts, const uint8_t* model, const ui
   if (trace_off[0] < 0) return fail(TRE_EINVAL, "trace_off[0] < 0");
   for (uint32_t i = 0; i < n_traces; ++i) {
     if (trace_off[i + 1] < trace_off[i]) return fail(TRE_EINVAL, "trace_off decreases at %u", i);
-    if (trace_off[i + 1] - trace_off[i] >= (1ll << 31))
-      return fail(TRE_ERANGE, "trace %u has 2^31 or more events", i);
+    if (trace_off[i + 1] - trace_off[i] >= (1ll << 27))
+      return fail(TRE_ERANGE, "trace %u has 2^27 or more events", i);
   }
   tre_events* ev = new (std::nothrow) tre_events();
   if (!ev) return fail(TRE_EINVAL, "out of host memory");
@@ -717,7 +970,8 @@ extern "C" int tre_load_events(const int64_t* ts, const uint8_t* model, const ui
     unsigned h_err = 0;
     bool ok = hipMemcpyAsync(scratch, h_init, 16, hipMemcpyHostToDevice, st) == hipSuccess;
     if (ok && maxlen > 0) {
-      ValParams vp{ts, model, type, ev->d_off, n_traces, c.duration_ms, c.window_ms, c.n_models, d_err, d_first};
+      ValParams vp{ts, model, type, ev->d_off, n_traces, c.duration_ms, c.window_ms, c.n_models,
+                   max_events_per_window(c.window_ms), d_err, d_first};
       dim3 grid((unsigned)((maxlen + kValChunk - 1) / kValChunk), std::min<uint32_t>(n_traces, 65535u));
       LaunchTimer lt("validate", st);
       hipLaunchKernelGGL(validate, grid, dim3(256), 0, st, vp);
@@ -732,8 +986,8 @@ extern "C" int tre_load_events(const int64_t* ts, const uint8_t* model, const ui
     if (h_err & 1u) rc = fail(TRE_EORDER, "row %llu: timestamp unsorted or outside [0, duration)", h_first);
     else if (h_err & 2u) rc = fail(TRE_ESCHEMA, "row %llu: model index or type byte invalid", h_first);
     else if (h_err & 4u)
-      rc = fail(TRE_ERANGE, "row %llu: more than %d events in one window", h_first,
-                TRE_MAX_EVENTS_PER_WINDOW);
+      rc = fail(TRE_ERANGE, "row %llu: more than %lld events in one window", h_first,
+                (long long)max_events_per_window(c.window_ms));
     if (rc != TRE_OK) return cleanup(rc);
   }
   *out = ev;
@@ -821,6 +1075,7 @@ static StreamParams stream_params(const tre_events* ev, const tre_profile* prof)
   p.n_windows = (int32_t)ev->n_windows;
   p.M = ev->cfg.n_models;
   p.wcap = ev->wcap;
+  p.chunk = chunk_windows(ev->cfg.n_models, ev->wcap);
   p.fast_w = (int32_t)(ev->cfg.fast_period_ms / ev->cfg.window_ms);
   p.slow_w = (int32_t)(ev->cfg.slow_period_ms / ev->cfg.window_ms);
   p.n_ticks = (int32_t)ev->n_ticks;
@@ -828,18 +1083,24 @@ static StreamParams stream_params(const tre_events* ev, const tre_profile* prof)
 }
 
 static int launch_stream(const tre_events* ev, const StreamParams& p, hipStream_t st) {
-  const size_t lds = (size_t)3 * ev->wcap * (size_t)ev->cfg.n_models * sizeof(unsigned long long);
+  const size_t lds = stream_lds(ev);
   LaunchTimer lt("tss_stream", st);
-  hipLaunchKernelGGL(tss_stream, dim3(ev->n_traces), dim3(kBlock), lds, st, p);
+  const bool cells = p.prefill || p.decode || p.a_int || p.w_int || p.tss64 || p.tss32 || p.flags;
+  if (cells)
+    hipLaunchKernelGGL((tss_stream<kStreamWaves, kStreamEPT, true>), dim3(ev->n_traces),
+                       dim3(kStreamWaves * 64), lds, st, p);
+  else
+    hipLaunchKernelGGL((tss_stream<kStreamWaves, kStreamEPT, false>), dim3(ev->n_traces),
+                       dim3(kStreamWaves * 64), lds, st, p);
   const hipError_t e = hipGetLastError();
   lt.done();
   if (e != hipSuccess) return fail(TRE_EHIP, "tss_stream launch: %s", hipGetErrorString(e));
   return TRE_OK;
 }
 
-static int g_log2_for(int M) {
-  int g = 0;
-  while ((1 << g) < M) ++g;
+static int group_size(int M) {
+  int g = 1;
+  while (g < M) g <<= 1;
   return g;
 }
 
@@ -857,7 +1118,6 @@ static int launch_rebalance(const tre_events* ev, const tre_profile* prof, const
   c.n_ticks = (int32_t)ev->n_ticks;
   c.n_windows = (int32_t)ev->n_windows;
   c.M = ev->cfg.n_models;
-  c.g_log2 = g_log2_for(ev->cfg.n_models);
   c.budget = ev->cfg.budget;
   c.n_traces = ev->n_traces;
   c.moves = out->moves;
@@ -865,11 +1125,20 @@ static int launch_rebalance(const tre_events* ev, const tre_profile* prof, const
   c.n_moves = out->n_moves;
   c.r_final = out->r_final;
   c.r_windows = out->r_windows;
-  const uint32_t spw = 64u >> c.g_log2;
+  const int G = group_size(c.M);
+  const uint32_t spw = 64u / (uint32_t)G;
   const uint64_t waves = ((uint64_t)n_sc + spw - 1) / spw;
-  const uint64_t blocks = (waves + 3) / 4;
+  const dim3 grid((unsigned)((waves + 3) / 4)), block(256);
   LaunchTimer lt("rebalance", st);
-  hipLaunchKernelGGL(rebalance, dim3((unsigned)blocks), dim3(256), 0, st, c);
+  switch (G) {
+    case 1: hipLaunchKernelGGL(rebalance<1>, grid, block, 0, st, c); break;
+    case 2: hipLaunchKernelGGL(rebalance<2>, grid, block, 0, st, c); break;
+    case 4: hipLaunchKernelGGL(rebalance<4>, grid, block, 0, st, c); break;
+    case 8: hipLaunchKernelGGL(rebalance<8>, grid, block, 0, st, c); break;
+    case 16: hipLaunchKernelGGL(rebalance<16>, grid, block, 0, st, c); break;
+    case 32: hipLaunchKernelGGL(rebalance<32>, grid, block, 0, st, c); break;
+    default: hipLaunchKernelGGL(rebalance<64>, grid, block, 0, st, c); break;
+  }
   const hipError_t e = hipGetLastError();
   lt.done();
   if (e != hipSuccess) return fail(TRE_EHIP, "rebalance launch: %s", hipGetErrorString(e));

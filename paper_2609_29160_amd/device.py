@@ -15,6 +15,8 @@ import torch
 
 from . import tre
 
+PAD_ROWS = 16  # rows past the end that stay readable (tile loads round up to 16 bytes)
+
 COLUMNS = (("ts", np.int64, torch.int64), ("model", np.uint8, torch.uint8),
            ("req", np.uint32, torch.uint32), ("type", np.uint8, torch.uint8),
            ("tokens", np.uint16, torch.uint16))
@@ -62,7 +64,8 @@ def upload(workload, t0: int = 0, t1: Optional[int] = None, threads: Optional[in
     total = int(off[-1])
     if log:
         log(f"counted {total} events in {t1 - t0} traces ({time.time() - t_start:.1f} s)")
-    cols = {k: torch.empty(max(total, 8), dtype=tdt, device="cuda") for k, _, tdt in COLUMNS}
+    # the library reads each column up to 16 bytes past its last row
+    cols = {k: torch.zeros(total + PAD_ROWS, dtype=tdt, device="cuda") for k, _, tdt in COLUMNS}
     # pinned staging, reused across batches
     max_batch = max(int(counts.max(initial=0)), min(batch_events, total))
     stage = {k: torch.empty(max(max_batch, 1), dtype=tdt, pin_memory=True) for k, _, tdt in COLUMNS}

@@ -31,12 +31,14 @@ def lib():
 
 
 def _columns_from_host(torch, traces, pad_front=0, pad_back=0):
-    """Concatenate host traces into device columns; returns cols, offsets."""
+    """Concatenate host traces into device columns; returns cols, offsets.
+    Columns keep 16 readable rows past the last one (the ABI's requirement)
+    plus `pad_back` more."""
     counts = [len(t["ts"]) for t in traces]
     off = np.zeros(len(traces) + 1, np.int64)
     off[0] = pad_front
     off[1:] = pad_front + np.cumsum(counts)
-    n = int(off[-1]) + pad_back
+    n = int(off[-1]) + 16 + pad_back
     cols = {}
     for k, dt in (("ts", np.int64), ("model", np.uint8), ("req", np.uint32), ("type", np.uint8),
                   ("tokens", np.uint16)):
