@@ -30,6 +30,7 @@ sys.path.insert(0, ROOT)
 WORKLOADS = {"tiny": 0, "bursty": 1, "sweep": 2, "diverse": 3, "stress": 4}
 HBM_PEAK_GBS = 8000.0
 ALG_BYTES_PER_EVENT = 12
+CPU_EVENT_BUDGET = 1_500_000_000
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "tss_stream_traffic.json")
 KERNEL_SRC = os.path.join(ROOT, "paper_2609_29160_amd", "csrc", "tre.hip")
 
@@ -61,7 +62,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="stress", choices=sorted(WORKLOADS))
     ap.add_argument("--traces", type=int, default=None, help="use only the first N traces")
-    ap.add_argument("--cpu-sample", type=int, default=None, help="traces timed on the CPU oracle")
+    ap.add_argument("--cpu-sample", type=int, default=None,
+                    help="traces timed on the CPU oracle (default: the leading traces "
+                         "within 1.5e9 events)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle leg")
     ap.add_argument("--emit-tss", action="store_true", help="also write per-window fp32 TSS")
     ap.add_argument("--threads", type=int, default=None)
@@ -89,18 +92,8 @@ def main():
     sc_cols = w.scenario_columns()
     n_sc = len(sc_cols["trace"])
 
-    # CPU sample: traces whose scenarios the oracle replays
-    if args.no_cpu:
-        sample = []
-    else:
-        n_s = args.cpu_sample
-        if n_s is None:
-            n_s = {"stress": 96, "diverse": 16}.get(args.workload, w.n_traces)
-        n_s = max(1, min(n_s, w.n_traces))
-        sample = list(range(n_s))
-
     t0 = time.time()
-    dt = device.upload(w, threads=args.threads, log=log, keep_host=sample)
+    dt = device.upload(w, threads=args.threads, log=log)
     log(f"resident: {dt.n_events} events, {dt.stored_bytes / 1e9:.1f} GB stored ({time.time() - t0:.1f} s)")
     ev = device.load(dt, validate=True)
     prof = device.profiles(w)
@@ -157,8 +150,14 @@ def main():
 
     cpu = None
     parity = None
-    if sample:
-        cpu, parity = cpu_leg(w, dt, sample, sc_cols, out, move_cap, tre)
+    if not args.no_cpu:
+        # the leading traces whose events fit the oracle's budget (about 15 s
+        # of one host thread at ~1e8 events/s), or --cpu-sample traces
+        if args.cpu_sample:
+            n_s = min(args.cpu_sample, w.n_traces)
+        else:
+            n_s = max(1, int(np.searchsorted(np.cumsum(dt.counts), CPU_EVENT_BUDGET, side="right")))
+        cpu, parity = cpu_leg(w, list(range(n_s)), sc_cols, out, move_cap, tre, args.threads)
 
     result = {
         "metric": "request-events/sec through TSS+rebalance (1 GPU); achieved HBM GB/s vs peak",
@@ -195,9 +194,11 @@ def main():
     ev.close()
 
 
-def cpu_leg(w, dt, sample, sc_cols, out, move_cap, tre):
+def cpu_leg(w, sample, sc_cols, out, move_cap, tre, threads):
     """Time the oracle (one thread) on the sample traces and compare the GPU's
-    decisions for the scenarios on those traces."""
+    decisions for the scenarios on those traces.  The sample's host columns
+    are generated again in batches (same seeds as the device copy); only the
+    oracle calls are timed."""
     import numpy as np
 
     import oracle as O
@@ -210,17 +211,25 @@ def cpu_leg(w, dt, sample, sc_cols, out, move_cap, tre):
     by_trace = {}
     for s, t in enumerate(sc_cols["trace"]):
         by_trace.setdefault(int(t), []).append(s)
-    t0 = time.perf_counter()
+    cpu_s = 0.0
     logical = 0
+    events = 0
     refs = {}
-    for t in sample:
-        host = dt.host[t]
-        prof = prof_all[t * M:(t + 1) * M]
-        r = o.tss_trace(host, w.window_ms, w.duration_ms, prof)
-        for s in by_trace.get(t, []):
-            refs[s] = o.control(cfg, prof, r["S"], r["flags"], sc_all[s:s + 1], move_cap)
-            logical += len(host["ts"])
-    cpu_s = time.perf_counter() - t0
+    batch = 32
+    for b0 in range(0, len(sample), batch):
+        tr = sample[b0:b0 + batch]
+        host = w.generate(tr[0], tr[-1] + 1, threads=threads)
+        t0 = time.perf_counter()
+        for i, t in enumerate(tr):
+            ev = host.trace(i)
+            prof = prof_all[t * M:(t + 1) * M]
+            r = o.tss_trace(ev, w.window_ms, w.duration_ms, prof)
+            for s in by_trace.get(t, []):
+                refs[s] = o.control(cfg, prof, r["S"], r["flags"], sc_all[s:s + 1], move_cap)
+                logical += len(ev["ts"])
+            events += len(ev["ts"])
+        cpu_s += time.perf_counter() - t0
+        del host
     # parity of the last timed sweep on the sampled scenarios
     n_moves = out["n_moves"].cpu().numpy()
     r_final = out["r_final"].cpu().numpy()
@@ -237,7 +246,7 @@ def cpu_leg(w, dt, sample, sc_cols, out, move_cap, tre):
             ok = all(np.array_equal(got[f], exp[f]) for f in ("window", "path", "receiver", "donor"))
         bad += 0 if ok else 1
     cpu = {"value": round(logical / cpu_s, 1), "unit": "request-events/s", "cores": 1, "kind": "oracle",
-           "sample": f"{len(sample)} of {w.n_traces} traces ({sum(len(dt.host[t]['ts']) for t in sample)} events), "
+           "sample": f"{len(sample)} of {w.n_traces} traces ({events} events), "
                      f"{len(refs)} scenarios, {cpu_s:.1f} s on one host thread"}
     parity = {"scenarios_checked": len(refs), "mismatches": bad, "bit_exact": bad == 0}
     log(f"cpu oracle: {cpu['value']:.3g} events/s; parity {parity}")

@@ -40,7 +40,7 @@ assert PROFILE_DTYPE.itemsize == 56 and SCENARIO_DTYPE.itemsize == 24 and MOVE_D
 def build(force: bool = True, src: str = _SRC, out: str = _LIB) -> str:
     """Compile the oracle with gcc (building the checker is not using it)."""
     if force or not os.path.exists(out) or os.path.getmtime(out) < os.path.getmtime(src):
-        tmp = out + ".tmp"
+        tmp = f"{out}.{os.getpid()}.tmp"
         subprocess.check_call(["gcc", *CFLAGS, "-o", tmp, src, "-lm"])
         os.replace(tmp, out)
     return out

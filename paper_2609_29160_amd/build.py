@@ -18,7 +18,7 @@ FLAGS = [
 
 
 def build_library(out: str = LIB, extra=()) -> str:
-    tmp = out + ".tmp"
+    tmp = f"{out}.{os.getpid()}.tmp"
     cmd = [HIPCC, *FLAGS, *extra, "-I", os.path.join(ROOT, "include"), "-o", tmp, SRC]
     subprocess.run(cmd, check=True, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)
     os.replace(tmp, out)
