@@ -8,13 +8,14 @@
 // Transfer").
 //
 // Kernels
-//   tss_stream  one workgroup per trace. Producer waves stream the SoA event
-//               columns (nontemporal 16/8-byte vector loads, 8 events per
-//               lane) and tally each event into an LDS ring of per-(window,
-//               model) cells with 64-bit LDS atomics (three packed words per
-//               cell). One consumer wave, lanes = models, walks the completed
-//               windows in order: carry scan of the active / waiting counts,
-//               in-window integrals, Eq. (1) in fp64, smoothing, outputs.
+//   tss_stream  one workgroup (4 waves) per trace, one barrier per tile of
+//               rows. Every thread loads (per-trace buffer resources, the
+//               next tile in flight while the current one is tallied) and
+//               tallies its rows into an LDS ring of (window, model) cells
+//               with three packed 64-bit LDS atomics per row; completed
+//               windows are then evaluated one cell per thread (carry scan,
+//               in-window integrals, Eq. (1) in fp64) and one wave per step
+//               runs the smoothing chain over the previous chunk.
 //   rebalance   one lane group of G = next_pow2(n_models) lanes per scenario
 //               (64/G scenarios per wave64): Eq. (2), regions, cadence, and
 //               the greedy receiver/donor moves with wave ballots and
@@ -83,7 +84,7 @@ struct tre_events {
 // ------------------------------------------------------------ constants
 constexpr int kStreamWaves = 4;            // tss_stream workgroup (waves)
 constexpr int kStreamEPT = 4;              // rows per lane per tile
-constexpr int kRingBytes = 24 * 1024;      // LDS budget of the tally ring
+constexpr int kRingBytes = 13 * 1024;      // LDS budget of the tally ring
 constexpr uint32_t kNoDefer = 0xFFFFFFFFu;
 
 typedef long long v2i64 __attribute__((ext_vector_type(2)));
@@ -104,6 +105,7 @@ struct StreamParams {
   int32_t n_windows;
   int32_t M;
   uint32_t wcap;    // ring windows, power of two
+  double inv2_window;  // 1 / (2 window_ms), rounded to nearest
   int32_t chunk;    // windows evaluated per step (cells <= threads)
   int32_t fast_w;   // fast period in windows
   int32_t slow_w;   // slow period in windows
@@ -191,73 +193,111 @@ __device__ __forceinline__ void load_slice(Slice<kEPT>& s, const TraceRsrc& rs, 
   }
 }
 
-// Tally the lane's rows in [e0, e_end) whose window fits the ring
-// [cbase, cbase + wcap). Each (window, model) cell holds three 64-bit words:
-//   tokens     P (low 32 bits) | D (high 32 bits)
-//   counts     (dA << 32) + dW          summed over the window's rows
-//   integrals  (dA*te << 32) + dW*te    te = t_end - ts, 1..window_ms
+// Ring layout: window slot s, model m owns the three 64-bit words at
+// s * (3M + 1) + 3m (the odd slot stride puts one model's cells of
+// neighbouring windows on different LDS banks):
+//   +0 tokens     P (low 32 bits) | D (high 32 bits)
+//   +1 counts     (dA << 32) + dW          summed over the window's rows
+//   +2 integrals  (dA*te << 32) + dW*te    te = t_end - ts, 1..window_ms
 // with dA = [ADMIT] - [FINISH], dW = [ARRIVE] - [ADMIT]; sums of the signed
 // low halves stay inside 32 bits (events per window * window_ms < 2^31).
-// Every row issues the same three LDS atomics (adding zero when it has
-// nothing to add), so rows need no branches. The first row that does not
-// fit is published in *defer (relative to a0) with its window in *wdef; the
-// lane holding row t_last (the tile's last) stores that row's window in
-// *wlast. Offsets are 32-bit: timestamps are below 2^32 ms.
+//
+// One row into its cell c (word index): tokens by kind, the packed count
+// and integral words (see the ring layout) from the kind and te.
+__device__ __forceinline__ void tally_row(unsigned long long* ring, uint32_t c, uint32_t ty,
+                                          uint32_t tok, uint32_t te) {
+  uint32_t* pd32 = (uint32_t*)ring;
+  const bool arr = ty == TRE_ARRIVE, adm = ty == (TRE_PREFILL | TRE_ADMIT);
+  const bool fin = ty == TRE_FINISH, dec = ty == TRE_DECODE;
+  // ARRIVE: dW = 1; PREFILL|ADMIT: dA = 1, dW = -1; FINISH: dA = -1
+  const uint32_t cnt_lo = arr ? 1u : (adm ? 0xFFFFFFFFu : 0u);
+  const uint32_t cnt_hi = fin ? 0xFFFFFFFFu : 0u;
+  const uint32_t itg_lo = arr ? te : (adm ? 0u - te : 0u);
+  const uint32_t itg_hi = adm ? te - 1u : (fin ? 0u - te : 0u);
+  atomicAdd(&pd32[2 * c + (dec ? 1 : 0)], (arr || fin) ? 0u : tok);
+  atomicAdd(&ring[c + 1], ((unsigned long long)cnt_hi << 32) | cnt_lo);
+  atomicAdd(&ring[c + 2], ((unsigned long long)itg_hi << 32) | itg_lo);
+}
+
+// General tally of the lane's rows in [e0, e_end) whose window fits the
+// ring [cbase, cbase + wcap), with per-row checks (first and last tiles of a
+// trace, and tiles that reach past the ring). The first row that does not
+// fit stops the lane and is published in *defer (relative to a0) with its
+// window in *wdef; the lane holding row t_last (the tile's last) stores
+// that row's window in *wlast. Offsets are 32-bit: timestamps are below
+// 2^32 ms; a row whose high timestamp word is set (unvalidated input only)
+// is skipped.
 template <int kEPT>
 __device__ __forceinline__ void tally_slice(const Slice<kEPT>& s, int c0, int a0, int e0, int e_end,
                                             int t_last, int cbase, uint32_t base_lo, uint32_t cap,
-                                            uint32_t magic, uint32_t win32, uint32_t wmask, int M,
-                                            int ncell, unsigned long long* ring, unsigned* defer,
-                                            int* wdef, int* wlast) {
-  // row indices are relative to the trace's aligned first row
-  const int lo0 = e0 - c0, hi0 = e_end - c0, l0 = t_last - c0;
+                                            uint32_t magic, uint32_t win32, uint32_t wmask,
+                                            uint32_t sstride, uint32_t mlast,
+                                            unsigned long long* ring, unsigned* defer, int* wdef,
+                                            int* wlast) {
+  const int lo0 = e0 - c0, hi0 = e_end - c0;
   const int lo = lo0 < 0 ? 0 : (lo0 > kEPT ? kEPT : lo0);
   const int hi = hi0 < 0 ? 0 : (hi0 > kEPT ? kEPT : hi0);
-  const int jl = (l0 >= 0 && l0 < kEPT) ? l0 : -1;
-  const uint32_t vmask = ((1u << hi) - 1u) & ~((1u << lo) - 1u);  // rows in [e0, e_end)
-  int jdef = kEPT;  // first row that does not fit the ring
-  int wdf = INT_MAX, wlt = -1;
-  uint32_t* pd32 = (uint32_t*)ring;  // token words
+  int jdef = kEPT, wdf = INT_MAX;
+  bool go = true;  // rows are sorted: the lane stops at its first row past the ring
 #pragma unroll
   for (int j = 0; j < kEPT; ++j) {
-    const uint32_t d = (uint32_t)s.ts[j] - base_lo;
-    uint32_t q, r;
-    div_window(d, magic, win32, q, r);
-    const uint32_t mdl = (s.mw[j >> 2] >> (8 * (j & 3))) & 0xFFu;
-    const uint32_t ty = (s.tw[j >> 2] >> (8 * (j & 3))) & 0xFFu;
-    const uint32_t tok = (s.kw[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
-    // the high dword and model checks only fail on unvalidated input
-    const bool row = ((vmask >> j) & 1u) && ((unsigned long long)s.ts[j] >> 32) == 0 && jdef == kEPT;
-    const bool over = row && d >= cap;
-    if (over) {
-      jdef = j;
-      wdf = cbase + (int)q;
+    const long long ts = s.ts[j];
+    if (go && j >= lo && j < hi && ((unsigned long long)ts >> 32) == 0) {
+      const uint32_t d = (uint32_t)ts - base_lo;
+      uint32_t q, r;
+      div_window(d, magic, win32, q, r);
+      const int w = cbase + (int)q;
+      if (d >= cap) {
+        jdef = j;
+        wdf = w;
+        go = false;
+      } else {
+        if (c0 + j == t_last) *wlast = w;
+        uint32_t mdl = (s.mw[j >> 2] >> (8 * (j & 3))) & 0xFFu;
+        mdl = mdl < mlast ? mdl : mlast;
+        const uint32_t ty = (s.tw[j >> 2] >> (8 * (j & 3))) & 0xFFu;
+        const uint32_t tok = (s.kw[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
+        tally_row(ring, ((uint32_t)w & wmask) * sstride + 3u * mdl, ty, tok, win32 - r);
+      }
     }
-    const bool ok = row && !over && mdl < (uint32_t)M;
-    const int w = cbase + (int)q;
-    if (ok && j == jl) wlt = w;
-    const int c = (int)((uint32_t)w & wmask) * M + (int)(mdl < (uint32_t)M ? mdl : 0u);
-    const uint32_t kind = ty & 3u;
-    const bool admit = (ty & TRE_ADMIT) != 0;
-    const bool tk = ok && (kind == TRE_PREFILL || kind == TRE_DECODE);
-    const int dA = !ok ? 0 : (admit ? 1 : (kind == TRE_FINISH ? -1 : 0));
-    const int dW = !ok ? 0 : (kind == TRE_ARRIVE ? 1 : (admit ? -1 : 0));
-    const int te = (int)(win32 - r);
-    const int iA = dA > 0 ? te : (dA < 0 ? -te : 0);  // dA * te without a multiply
-    const int iW = dW > 0 ? te : (dW < 0 ? -te : 0);
-    const unsigned long long cnt = ((unsigned long long)(long long)dA << 32) + (unsigned long long)(long long)dW;
-    const unsigned long long itg = ((unsigned long long)(long long)iA << 32) + (unsigned long long)(long long)iW;
-    atomicAdd(&pd32[2 * c + (kind == TRE_DECODE ? 1 : 0)], tk ? tok : 0u);
-    atomicAdd(&ring[ncell + c], cnt);
-    atomicAdd(&ring[2 * ncell + c], itg);
   }
-  if (wlt >= 0) *wlast = wlt;
-  if (__ballot(jdef < kEPT)) {  // rare: some row of this wave waits for a later tile
+  if (__ballot(jdef < kEPT)) {  // some row of this wave waits for a later tile
     if (jdef < kEPT) {
       atomicMin(defer, (unsigned)(c0 + jdef - a0));
       atomicMin(wdef, wdf);
     }
   }
+}
+
+// Tally of a lane whose rows all lie in the trace with the last one inside
+// the ring (rows are sorted, so every row fits): no per-row checks. Here
+// d = ts - base < 2^31 and the quotient q = floor(d / window) < 2^8 is
+// trunc((2d + 1) * fl(1 / (2 window))) in fp64: (2d + 1) / (2 window) lies
+// at least 1/(2 window) >= 2^-24 away from every integer, far above the
+// product's rounding error (below 2^-43). te = (q + 1) * window - d.
+// Model bytes are clamped to M - 1, so unvalidated input cannot leave the
+// ring.
+template <int kEPT>
+__device__ __forceinline__ void tally_fast(const Slice<kEPT>& s, uint32_t base_lo, double inv2_win,
+                                           uint32_t win32, uint32_t cbm, uint32_t wmask,
+                                           uint32_t sstride, uint32_t mlast, bool last, int cbase,
+                                           unsigned long long* ring, int* wlast) {
+  const uint32_t odd = 1u - 2u * base_lo;  // (ts << 1) + odd = 2d + 1
+  const uint32_t wb = win32 + base_lo;     // q * window + wb - ts = te
+  uint32_t ql = 0;
+#pragma unroll
+  for (int j = 0; j < kEPT; ++j) {
+    const uint32_t t = (uint32_t)s.ts[j];
+    const uint32_t q = (uint32_t)((double)((t << 1) + odd) * inv2_win);
+    const uint32_t te = __umul24(q, win32) + wb - t;
+    ql = q;
+    uint32_t mdl = (s.mw[j >> 2] >> (8 * (j & 3))) & 0xFFu;
+    mdl = mdl < mlast ? mdl : mlast;
+    const uint32_t ty = (s.tw[j >> 2] >> (8 * (j & 3))) & 0xFFu;
+    const uint32_t tok = (s.kw[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
+    tally_row(ring, __umul24((q + cbm) & wmask, sstride) + 3u * mdl, ty, tok, te);
+  }
+  if (last) *wlast = cbase + (int)ql;
 }
 
 // a packed (high << 32) + signed low word: the signed low half and the high
@@ -286,7 +326,8 @@ __device__ __forceinline__ int next_tick(int& fctr, int& sctr, int& tick, int fa
 //   - evaluate [cB, cC), one (window, model) cell per thread: carry prefix
 //     over the chunk, window integrals, Eq. (1) -> raw ratio and idle flag
 //     staged in LDS (two staging buffers, by step parity);
-//   - wave 0 runs the smoothing chain over [cA, cB) from the other buffer;
+//   - wave k % kWaves runs the smoothing chain over [cA, cB) from the
+//     other buffer (state in LDS, so the chain can move between waves);
 //   - clear the ring cells of [cA, cB);
 //   -- barrier -- the tile's rows are in; windows < wl are complete.
 // Ring slots in use are windows [cA, cA + wcap): rows whose window reaches
@@ -298,7 +339,7 @@ __global__ __launch_bounds__(kWaves * 64) void tss_stream(StreamParams p) {
   constexpr int kThreads = kWaves * 64;
   constexpr long long kTile = (long long)kThreads * kEPT;
   extern __shared__ unsigned long long ring[];
-  __shared__ long long s_carry[2][2][TRE_MAX_MODELS];  // [parity][active, waiting][model]
+  __shared__ int s_carry[2][2][TRE_MAX_MODELS];  // [parity][active, waiting][model], |count| < 2^27
   __shared__ double s_S[TRE_MAX_MODELS];               // smoothed TSS per model
   __shared__ double s_alpha[TRE_MAX_MODELS];
   __shared__ uint8_t s_init[TRE_MAX_MODELS];
@@ -312,12 +353,10 @@ __global__ __launch_bounds__(kWaves * 64) void tss_stream(StreamParams p) {
   const int M = p.M;
   const uint32_t wcap = p.wcap;
   const int C = p.chunk;
-  const int ncell = (int)wcap * M;
-  unsigned long long* r_pd = ring;              // tokens: P (low 32) | D (high 32)
-  unsigned long long* r_a = ring + ncell;       // counts: (dA << 32) + dW
-  unsigned long long* r_w = ring + 2 * ncell;   // integrals: (dA*te << 32) + dW*te
+  const uint32_t sstride = 3u * (uint32_t)M + 1u;  // ring words per window slot
+  const int nring = (int)(wcap * sstride);
   // [2][C][M] staged raw ratios (>= 0), -1 marks an idle window
-  double* st_raw = (double*)(ring + 3 * ncell);
+  double* st_raw = (double*)(ring + nring);
   const long long e_begin = p.off[trace];
   const long long e_end = p.off[trace + 1];
   const long long win = p.window_ms;
@@ -326,7 +365,7 @@ __global__ __launch_bounds__(kWaves * 64) void tss_stream(StreamParams p) {
   const int nW = p.n_windows;
   constexpr bool cells = kCells;
 
-  for (int i = tid; i < 3 * ncell; i += kThreads) ring[i] = 0ull;
+  for (int i = tid; i < nring; i += kThreads) ring[i] = 0ull;
   for (int i = tid; i < 2 * 2 * TRE_MAX_MODELS; i += kThreads) (&s_carry[0][0][0])[i] = 0;
   if (tid < 3) {
     s_defer[tid] = kNoDefer;
@@ -374,29 +413,43 @@ __global__ __launch_bounds__(kWaves * 64) void tss_stream(StreamParams p) {
   auto step = [&](Slice<kEPT>& cur, Slice<kEPT>& nxt, int k) -> bool {
     if (cA >= nW) return true;
     const int b3 = k % 3;
-    // ---- tally tile k (tile k+1 loading meanwhile), capacity [cA, cA + wcap)
+    // ---- tally tile k (tile k+1 loading meanwhile), capacity [cB, cB + wcap)
     const int a0 = e0 & ~(kEPT - 1);
     if (held != a0) load_slice<kEPT>(cur, rs, a0 + tid * kEPT);  // prefetch missed
     const int pref = a0 + (int)kTile;
     load_slice<kEPT>(nxt, rs, pref + tid * kEPT);  // zeros past the trace
     const int t_last = (pref < rend ? pref : rend) - 1;
-    tally_slice<kEPT>(cur, a0 + tid * kEPT, a0, e0, rend, t_last, cA,
-                      (uint32_t)((long long)cA * win), wcap * win32, p.magic, win32, wcap - 1, M,
-                      ncell, ring, &s_defer[b3], &s_wdef[b3], &s_wlast[b3]);
-    // ---- evaluate [cB, cC), one cell per thread (groups of C lanes per model)
+    {
+      const int c0 = a0 + tid * kEPT;
+      const uint32_t base_lo = (uint32_t)((long long)cB * win);
+      const uint32_t cap = wcap * win32;
+      const bool lane_fast = c0 >= e0 && c0 + kEPT <= rend && (uint32_t)cur.ts[kEPT - 1] - base_lo < cap;
+      if (__ballot(!lane_fast) == 0ull)  // wave-uniform
+        tally_fast<kEPT>(cur, base_lo, p.inv2_window, win32, (uint32_t)cB & (wcap - 1), wcap - 1, sstride,
+                         (uint32_t)M - 1u, c0 + kEPT - 1 == t_last, cB, ring, &s_wlast[b3]);
+      else
+        tally_slice<kEPT>(cur, c0, a0, e0, rend, t_last, cB, base_lo, cap, p.magic, win32, wcap - 1,
+                          sstride, (uint32_t)M - 1u, ring, &s_defer[b3], &s_wdef[b3], &s_wlast[b3]);
+    }
+    // ---- evaluate [cB, cC), one cell per thread (groups of C lanes per
+    // model), clearing each cell once read: no row of this tile falls below
+    // the completeness bound
     const int cC = wl < cB + C ? wl : cB + C;
     const int n = cC - cB;
-    const long long* cin = s_carry[k & 1][0];
-    long long* cout = s_carry[(k + 1) & 1][0];
+    const int* cin = s_carry[k & 1][0];
+    int* cout = s_carry[(k + 1) & 1][0];
     double* sr = st_raw + (k & 1) * C * M;
     if (r_thread) {  // uniform over each group of C lanes
       const bool valid = rj < n;
       unsigned long long pd = 0, ap = 0, wp = 0;
       if (valid) {
-        const int c = (int)((uint32_t)(cB + rj) & (wcap - 1)) * M + rm;
-        pd = r_pd[c];
-        ap = r_a[c];
-        wp = r_w[c];
+        const uint32_t c = ((uint32_t)(cB + rj) & (wcap - 1)) * sstride + 3u * (uint32_t)rm;
+        pd = ring[c];
+        ap = ring[c + 1];
+        wp = ring[c + 2];
+        ring[c] = 0ull;
+        ring[c + 1] = 0ull;
+        ring[c + 2] = 0ull;
       }
       int ca, cw, la32, lw32;
       unpack32(ap, ca, cw);      // counts word
@@ -420,21 +473,22 @@ __global__ __launch_bounds__(kWaves * 64) void tss_stream(StreamParams p) {
       }
       if (valid) {
         const int w = cB + rj;
-        const long long la = la32, lw = lw32;
-        const long long A0 = cin[rm] + (ia - ca), W0 = cin[TRE_MAX_MODELS + rm] + (iw - cw);
-        // counts are below 2^31 and windows below 2^23 ms: 32x32->64 products
-        const long long A_int = (long long)(int)A0 * (long long)(int)win + la;
-        const long long W_int = (long long)(int)W0 * (long long)(int)win + lw;
+        const int A0 = cin[rm] + (ia - ca), W0 = cin[TRE_MAX_MODELS + rm] + (iw - cw);
+        // the window integrals in fp64, exactly: a trace has fewer than 2^27
+        // rows, so |A0|, |W0| < 2^27, A0 * window < 2^50 and the sum with the
+        // in-window term (below 2^31) stays below 2^53
+        const double A_f = __builtin_fma((double)A0, dwin, (double)la32);
+        const double W_f = __builtin_fma((double)W0, dwin, (double)lw32);
         const uint32_t P = (uint32_t)pd, Dt = (uint32_t)(pd >> 32);
-        const bool idle = pd == 0ull && A_int == 0 && W_int == 0;
+        const bool idle = pd == 0ull && A_f == 0.0 && W_f == 0.0;
         double raw = 0.0;
         if (!idle) {
           // Eq. (1), evaluated in the documented order
           double num = w_p * (double)P;
           num = num + (double)Dt;
           num = num * 1000.0;
-          const double q = w_q * (double)W_int;
-          double den = (double)A_int + q;
+          const double q = w_q * W_f;
+          double den = A_f + q;
           if (den < dwin) den = dwin;
           raw = num / den;
         }
@@ -443,8 +497,8 @@ __global__ __launch_bounds__(kWaves * 64) void tss_stream(StreamParams p) {
           const int64_t o = ((int64_t)trace * nW + w) * M + rm;
           if (p.prefill) p.prefill[o] = P;
           if (p.decode) p.decode[o] = Dt;
-          if (p.a_int) p.a_int[o] = A_int;
-          if (p.w_int) p.w_int[o] = W_int;
+          if (p.a_int) p.a_int[o] = (long long)A0 * win + la32;
+          if (p.w_int) p.w_int[o] = (long long)W0 * win + lw32;
         }
         if (rj == n - 1) {
           cout[rm] = cin[rm] + ia;
@@ -503,14 +557,6 @@ __global__ __launch_bounds__(kWaves * 64) void tss_stream(StreamParams p) {
         s_tick[1] = sctr;
         s_tick[2] = tick;
       }
-    }
-    // ---- clear [cA, cB)
-    const int nclr = (cB - cA) * M;
-    for (int i = tid; i < nclr; i += kThreads) {
-      const int c = (int)((uint32_t)(cA + i / M) & (wcap - 1)) * M + (i % M);
-      r_pd[c] = 0ull;
-      r_a[c] = 0ull;
-      r_w[c] = 0ull;
     }
     if (tid == 0) {
       const int r = (k + 2) % 3;
@@ -863,7 +909,7 @@ static int64_t max_events_per_window(int64_t window_ms) {
 
 static uint32_t ring_windows(int M) {
   uint32_t w = 256;
-  while (w > 2 && (size_t)3 * w * (size_t)M * 8 > (size_t)kRingBytes) w >>= 1;
+  while (w > 2 && (size_t)w * (3 * (size_t)M + 1) * 8 > (size_t)kRingBytes) w >>= 1;
   return w;
 }
 
@@ -877,7 +923,7 @@ static int chunk_windows(int M, uint32_t wcap) {
 
 static size_t stream_lds(const tre_events* ev) {
   const size_t M = (size_t)ev->cfg.n_models, C = (size_t)chunk_windows(ev->cfg.n_models, ev->wcap);
-  return 3 * ev->wcap * M * 8 + 2 * C * M * 8;
+  return ev->wcap * (3 * M + 1) * 8 + 2 * C * M * 8;
 }
 
 extern "C" int tre_load_events(const int64_t* ts, const uint8_t* model, const uint32_t* req,
@@ -1072,6 +1118,7 @@ static StreamParams stream_params(const tre_events* ev, const tre_profile* prof)
   p.window_ms = ev->cfg.window_ms;
   p.magic = ev->cfg.window_ms == 1 ? 0xFFFFFFFFu
                                    : (uint32_t)((1ull << 32) / (uint64_t)ev->cfg.window_ms);
+  p.inv2_window = 0.5 / (double)ev->cfg.window_ms;
   p.n_windows = (int32_t)ev->n_windows;
   p.M = ev->cfg.n_models;
   p.wcap = ev->wcap;
