@@ -413,6 +413,23 @@ __global__ __launch_bounds__(kWaves * 64) void tss_stream(StreamParams p) {
   auto step = [&](Slice<kEPT>& cur, Slice<kEPT>& nxt, int k) -> bool {
     if (cA >= nW) return true;
     const int b3 = k % 3;
+    // ---- read and clear the cells of [cB, cC), one cell per thread (groups
+    // of C lanes per model): complete windows that no row of this tile
+    // reaches. LDS operations of a wave retire in order, so these reads go
+    // ahead of the tally's atomics.
+    const int cC = wl < cB + C ? wl : cB + C;
+    const int n = cC - cB;
+    const bool valid = r_thread && rj < n;
+    unsigned long long pd = 0, ap = 0, wp = 0;
+    if (valid) {
+      const uint32_t c = ((uint32_t)(cB + rj) & (wcap - 1)) * sstride + 3u * (uint32_t)rm;
+      pd = ring[c];
+      ap = ring[c + 1];
+      wp = ring[c + 2];
+      ring[c] = 0ull;
+      ring[c + 1] = 0ull;
+      ring[c + 2] = 0ull;
+    }
     // ---- tally tile k (tile k+1 loading meanwhile), capacity [cB, cB + wcap)
     const int a0 = e0 & ~(kEPT - 1);
     if (held != a0) load_slice<kEPT>(cur, rs, a0 + tid * kEPT);  // prefetch missed
@@ -431,26 +448,11 @@ __global__ __launch_bounds__(kWaves * 64) void tss_stream(StreamParams p) {
         tally_slice<kEPT>(cur, c0, a0, e0, rend, t_last, cB, base_lo, cap, p.magic, win32, wcap - 1,
                           sstride, (uint32_t)M - 1u, ring, &s_defer[b3], &s_wdef[b3], &s_wlast[b3]);
     }
-    // ---- evaluate [cB, cC), one cell per thread (groups of C lanes per
-    // model), clearing each cell once read: no row of this tile falls below
-    // the completeness bound
-    const int cC = wl < cB + C ? wl : cB + C;
-    const int n = cC - cB;
+    // ---- evaluate [cB, cC): carry prefix, window integrals, Eq. (1)
     const int* cin = s_carry[k & 1][0];
     int* cout = s_carry[(k + 1) & 1][0];
     double* sr = st_raw + (k & 1) * C * M;
     if (r_thread) {  // uniform over each group of C lanes
-      const bool valid = rj < n;
-      unsigned long long pd = 0, ap = 0, wp = 0;
-      if (valid) {
-        const uint32_t c = ((uint32_t)(cB + rj) & (wcap - 1)) * sstride + 3u * (uint32_t)rm;
-        pd = ring[c];
-        ap = ring[c + 1];
-        wp = ring[c + 2];
-        ring[c] = 0ull;
-        ring[c + 1] = 0ull;
-        ring[c + 2] = 0ull;
-      }
       int ca, cw, la32, lw32;
       unpack32(ap, ca, cw);      // counts word
       unpack32(wp, la32, lw32);  // integrals word
@@ -558,8 +560,12 @@ __global__ __launch_bounds__(kWaves * 64) void tss_stream(StreamParams p) {
         s_tick[2] = tick;
       }
     }
+    // entries rotate over three steps: step k writes entry k % 3, every wave
+    // reads it right after the barrier that ends step k, and it is reset
+    // here in step k + 2 (a barrier after those reads, a barrier before its
+    // next use in step k + 3)
     if (tid == 0) {
-      const int r = (k + 2) % 3;
+      const int r = (k + 1) % 3;
       s_defer[r] = kNoDefer;
       s_wdef[r] = INT_MAX;
       s_wlast[r] = -1;

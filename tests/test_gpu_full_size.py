@@ -1,0 +1,100 @@
+"""GPU parity at full size, in the launch configuration the benchmark times.
+
+The stress workload (4096 traces x 32 models, 3600 s in 250 ms windows,
+9.36e9 events, 150 GB of columns) and the diverse workload (256 traces x 16
+models, 7200 s in 1 s windows, 1.57e9 events) are uploaded whole and swept
+three times: the three results must be identical (the kernels share LDS
+between waves; a missing barrier shows up as launch-to-launch differences
+only at this scale), and sampled scenarios and per-cell fp32 TSS of sampled
+traces must match the CPU oracle exactly. The oracle regenerates each
+sampled trace on the host from the same seeds.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import tracegen as tg
+import parity as PT
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _outputs(out):
+    return {k: out[k].cpu().numpy().copy() for k in ("moves", "n_moves", "r_final", "r_windows")}
+
+
+def _run_full(workload_index, sample_traces, tss_traces):
+    import torch
+
+    from paper_2609_29160_amd import device, tre
+
+    w = tg.standard(workload_index)
+    say(f"{w.name}: uploading")
+    dt = device.upload(w)
+    ev = device.load(dt, validate=True)
+    prof = device.profiles(w)
+    sc_cols = w.scenario_columns()
+    n_sc = len(sc_cols["trace"])
+    sc = device.scenarios(sc_cols)
+    tre.tre_check_params(ev, prof, sc)
+    move_cap = max(1, ev.n_ticks * int(np.max(sc_cols["max_moves"])))
+    out = tre.ctl_outputs(ev, n_sc, move_cap)
+    ws = torch.empty(tre.tre_workspace_size(ev, n_sc), dtype=torch.uint8, device="cuda")
+    say(f"{w.name}: {dt.n_events} events, {n_sc} scenarios; three sweeps")
+    runs = []
+    for _ in range(3):
+        tre.tre_sweep(ev, prof, sc, out, ws)
+        torch.cuda.synchronize()
+        runs.append(_outputs(out))
+    for r in runs[1:]:
+        for k in runs[0]:
+            assert np.array_equal(runs[0][k], r[k]), f"{w.name}: sweep output {k} differs between launches"
+    # the same launch with the per-cell fp32 TSS written
+    t32 = torch.empty((ev.n_traces, ev.n_windows, ev.n_models), dtype=torch.float32, device="cuda")
+    tre.tre_sweep(ev, prof, sc, out, ws, tss32=t32)
+    torch.cuda.synchronize()
+    with_tss = _outputs(out)
+    for k in runs[0]:
+        assert np.array_equal(runs[0][k], with_tss[k]), f"{w.name}: emitting TSS changed {k}"
+
+    M = w.n_models
+    prof_all = PT.O.pack_profiles(w.profile_columns())
+    by_trace = {}
+    for s, t in enumerate(sc_cols["trace"]):
+        by_trace.setdefault(int(t), []).append(s)
+    moves = tre.unpack_moves(out["moves"]).reshape(n_sc, move_cap)
+    checked = 0
+    for t in sorted(set(sample_traces) | set(tss_traces)):
+        host = w.generate(t, t + 1).trace(0)
+        ref = PT.O.get().tss_trace(host, w.window_ms, w.duration_ms, prof_all[t * M:(t + 1) * M])
+        if t in tss_traces:
+            PT.compare_tss32(t32[t].cpu().numpy(), ref["S"], f"{w.name} trace {t} tss32")
+        if t in sample_traces:
+            for s in by_trace.get(t, []):
+                row = {k: v[s] for k, v in sc_cols.items()}
+                exp = PT.oracle_control(w, PT.trace_profile(w.profile_columns(t + 1), t, M), ref["S"],
+                                        ref["flags"], row, move_cap)
+                PT.compare_ctl(moves[s], int(runs[0]["n_moves"][s]), runs[0]["r_final"][s],
+                               runs[0]["r_windows"][s], exp, f"{w.name} scenario {s}")
+                checked += 1
+    say(f"{w.name}: {checked} scenarios and {len(tss_traces)} traces of TSS match the oracle")
+    assert checked > 0
+    ev.close()
+
+
+def test_stress_full_size():
+    rng = np.random.default_rng(11)
+    sample = sorted({0, 1, 2047, 4095, *rng.integers(0, 4096, 4).tolist()})
+    _run_full(4, sample, [0, 4095])
+
+
+def test_diverse_full_size():
+    rng = np.random.default_rng(12)
+    sample = sorted({0, 255, *rng.integers(0, 256, 3).tolist()})
+    _run_full(3, sample, [0, 255])
