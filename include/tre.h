@@ -179,7 +179,9 @@ const char* tre_last_error(void);
    (row trace_off[n_traces] - 1): tile loads are rounded up to 16 bytes.
    duration_ms must be below 2^32 and a trace below 2^27 events.
    With flags & TRE_VALIDATE the events are checked on the device and the
-   call waits for the result (TRE_EORDER, TRE_ESCHEMA, TRE_ERANGE). The
+   call waits for the result (TRE_EORDER, TRE_ESCHEMA, TRE_ERANGE); without
+   it, events that break these rules give unspecified results, never an
+   access outside the columns, outputs or workspace. The
    handle owns small device tables (offsets, tick list); free it with
    tre_free_events. */
 #define TRE_VALIDATE 1u
