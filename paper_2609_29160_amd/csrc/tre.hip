@@ -16,10 +16,10 @@
 //               windows are then evaluated one cell per thread (carry scan,
 //               in-window integrals, Eq. (1) in fp64) and one wave per step
 //               runs the smoothing chain over the previous chunk.
-//   rebalance   one lane group of G = next_pow2(n_models) lanes per scenario
-//               (64/G scenarios per wave64): Eq. (2), regions, cadence, and
-//               the greedy receiver/donor moves with wave ballots and
-//               shuffles for argmin / argmax (lowest index on ties).
+//   rebalance   one wave per scenario, lane = model: Eq. (2), regions,
+//               cadence and the greedy receiver/donor moves, with ballots
+//               as candidate sets and DPP wave folds for argmin / argmax
+//               (lowest index on ties), so every decision is a scalar.
 //   validate    checks the event columns once, at load time.
 #include <hip/hip_runtime.h>
 
@@ -625,154 +625,160 @@ __device__ __forceinline__ unsigned long long dbits(double x) {
   return (unsigned long long)__double_as_longlong(x);
 }
 
-// lane permutations pairing lanes across groups of 2, 4, 8, 16 and 32 (DPP
-// quad_perm / half-row mirror / row mirror, then an LDS swizzle)
-template <int kStep>
-__device__ __forceinline__ uint32_t lane_pair(uint32_t x) {
-  if constexpr (kStep == 1) return (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, 0xB1, 0xF, 0xF, false);
-  else if constexpr (kStep == 2) return (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x4E, 0xF, 0xF, false);
-  else if constexpr (kStep == 4) return (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x141, 0xF, 0xF, false);
-  else if constexpr (kStep == 8) return (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x140, 0xF, 0xF, false);
-  else return (uint32_t)__builtin_amdgcn_ds_swizzle((int)x, 0x401F);  // lane ^ 16 within 32
+// Wave-wide min / max of a 32-bit value, broadcast as a scalar: butterfly
+// within quads and rows (DPP quad_perm, half-row and row mirrors), then
+// rows folded through row broadcasts; lane 63 ends with the result.
+template <bool kMax>
+__device__ __forceinline__ uint32_t wave_fold(uint32_t x) {
+  // lanes a step does not reach read the identity, so each step is one
+  // DPP-sourced min / max
+  constexpr int id = kMax ? 0 : -1;
+  auto op = [](uint32_t a, uint32_t b) { return kMax ? (a > b ? a : b) : (a < b ? a : b); };
+  x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, (int)x, 0xB1, 0xF, 0xF, false));   // quad_perm 1,0,3,2
+  x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, (int)x, 0x4E, 0xF, 0xF, false));   // quad_perm 2,3,0,1
+  x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, (int)x, 0x141, 0xF, 0xF, false));  // row_half_mirror
+  x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, (int)x, 0x140, 0xF, 0xF, false));  // row_mirror
+  x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, (int)x, 0x142, 0xA, 0xF, false));  // row_bcast:15
+  x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, (int)x, 0x143, 0xC, 0xF, false));  // row_bcast:31
+  return (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
 }
 
-template <bool kMax, int kStep>
-__device__ __forceinline__ unsigned long long key_step(unsigned long long key) {
-  const uint32_t lo = lane_pair<kStep>((uint32_t)key);
-  const uint32_t hi = lane_pair<kStep>((uint32_t)(key >> 32));
-  const unsigned long long o = ((unsigned long long)hi << 32) | lo;
-  return kMax ? (o > key ? o : key) : (o < key ? o : key);
-}
-
-// min / max of a 64-bit key over each aligned group of G lanes
-template <bool kMax, int G>
-__device__ __forceinline__ unsigned long long group_reduce(unsigned long long key) {
-  if constexpr (G >= 2) key = key_step<kMax, 1>(key);
-  if constexpr (G >= 4) key = key_step<kMax, 2>(key);
-  if constexpr (G >= 8) key = key_step<kMax, 4>(key);
-  if constexpr (G >= 16) key = key_step<kMax, 8>(key);
-  if constexpr (G >= 32) key = key_step<kMax, 16>(key);
-  if constexpr (G == 64) {
-    const unsigned long long a =
-        ((unsigned long long)(uint32_t)__builtin_amdgcn_readlane((int)(key >> 32), 0) << 32) |
-        (uint32_t)__builtin_amdgcn_readlane((int)key, 0);
-    const unsigned long long b =
-        ((unsigned long long)(uint32_t)__builtin_amdgcn_readlane((int)(key >> 32), 32) << 32) |
-        (uint32_t)__builtin_amdgcn_readlane((int)key, 32);
-    key = kMax ? (a > b ? a : b) : (a < b ? a : b);
+// Lowest lane among the candidates (bit per lane in cand) holding the
+// minimum (kMax: maximum) of Z, or -1. Z >= 0 and never NaN, so its bit
+// pattern orders like its value: the high words decide, and the low words
+// only where several candidates share the highest / lowest high word
+// (for +inf the low word is zero).
+template <bool kMax>
+__device__ __forceinline__ int wave_arg(unsigned long long cand, double Z, int lane) {
+  if (cand == 0ull) return -1;
+  const bool c = (cand >> lane) & 1ull;
+  const unsigned long long key = dbits(Z);
+  const uint32_t hi = (uint32_t)(key >> 32), lo = (uint32_t)key;
+  const uint32_t h = wave_fold<kMax>(c ? hi : (kMax ? 0u : 0xFFFFFFFFu));
+  unsigned long long tie = __ballot(c && hi == h);
+  if (__popcll(tie) > 1 && h != 0x7FF00000u) {
+    const bool c2 = (tie >> lane) & 1ull;
+    const uint32_t l = wave_fold<kMax>(c2 ? lo : (kMax ? 0u : 0xFFFFFFFFu));
+    tie = __ballot(c2 && lo == l);
   }
-  return key;
+  return __ffsll((long long)tie) - 1;
 }
 
-// lowest lane of the group holding the minimum (or maximum) Z among
-// candidates; Z >= 0 so its bit pattern orders like its value; -1 if none
-template <bool kMax, int G>
-__device__ __forceinline__ int group_arg(bool cand, double Z, int gbase, unsigned long long gmask) {
-  const unsigned long long any = __ballot(cand) & gmask;
-  if (any == 0ull) return -1;
-  const unsigned long long key = group_reduce<kMax, G>(cand ? dbits(Z) : (kMax ? 0ull : ~0ull));
-  const unsigned long long win = __ballot(cand && dbits(Z) == key) & gmask;
-  return __ffsll((long long)win) - 1 - gbase;
+__device__ __forceinline__ double read_lane_f64(double x, int l) {
+  const unsigned long long b = dbits(x);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)b, l);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(b >> 32), l);
+  return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
 }
 
-template <int G>
+constexpr int kTickBlock = 8;  // ticks loaded and normalised per block
+
+// One wave per scenario, lane m = model m: every decision is wave-uniform
+// (ballots are the candidate sets, receiver and donor are scalars). Per
+// tick: Eq. (2), regions, the cadence rule, then up to K greedy moves with
+// Eq. (3) for the receiver and the donor order of the bounded transfer.
 __global__ __launch_bounds__(256) void rebalance(CtlParams p) {
   const int lane = threadIdx.x & 63;
-  const uint32_t wave = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;
-  const uint32_t s = wave * (uint32_t)(64 / G) + (uint32_t)(lane / G);
-  const int m = lane & (G - 1);
-  const int gbase = lane & ~(G - 1);
-  const unsigned long long gmask = G == 64 ? ~0ull : (((1ull << G) - 1ull) << gbase);
-  const bool sc_ok = s < p.n_sc;
+  const uint32_t s = (uint32_t)((blockIdx.x * blockDim.x + threadIdx.x) >> 6);
+  if (s >= p.n_sc) return;  // whole wave
   const int M = p.M;
-
-  uint32_t trace = 0, K = 0;
-  double theta_scale = 1.0, ovr = -1.0;
-  if (sc_ok) {
-    const tre_scenario sc = p.sc[s];
-    trace = sc.trace < p.n_traces ? sc.trace : 0;
-    K = sc.max_moves;
-    theta_scale = sc.theta_scale;
-    ovr = sc.tau_crit_override;
-  }
-  const bool act = sc_ok && m < M;
-  double theta_eff = 1.0, tau_c = 0.0, tau_s = INFINITY;
-  int R = 0, r_min = 0;
-  if (act) {
-    const tre_profile pr = p.prof[(int64_t)trace * M + m];
-    theta_eff = pr.theta * theta_scale;
-    tau_c = ovr >= 0.0 ? ovr : pr.tau_crit;
-    tau_s = pr.tau_surplus;
-    R = pr.r_init;
-    r_min = pr.r_min;
-  }
+  const bool act = lane < M;
+  const int mc = act ? lane : 0;
+  const tre_scenario sc = p.sc[s];
+  const uint32_t trace = sc.trace < p.n_traces ? sc.trace : 0;
+  const uint32_t K = sc.max_moves;
+  const tre_profile pr = p.prof[(int64_t)trace * M + mc];
+  const double theta_eff = pr.theta * sc.theta_scale;
+  const double tau_c = sc.tau_crit_override >= 0.0 ? sc.tau_crit_override : pr.tau_crit;
+  const double tau_s = pr.tau_surplus;
+  const int r_min = pr.r_min;
+  int R = act ? pr.r_init : 0;
   int rsum = R;
-#pragma unroll
-  for (int off = G >> 1; off > 0; off >>= 1) rsum += __shfl_xor(rsum, off, G);
-  int pool = p.budget - rsum;
+  rsum += __shfl_xor(rsum, 1);
+  rsum += __shfl_xor(rsum, 2);
+  rsum += __shfl_xor(rsum, 4);
+  rsum += __shfl_xor(rsum, 8);
+  rsum += __shfl_xor(rsum, 16);
+  rsum += __shfl_xor(rsum, 32);
+  int pool = p.budget - __builtin_amdgcn_readfirstlane(rsum);
+  const unsigned long long live_lanes = __ballot(act);
+  // replica-window sums accumulate when a lane's R changes: windows
+  // [since, w] ran with the old R, a move at tick window w applies from w+1
   long long rw = 0;
-  int wprev = -1;
+  int since = 0;
   uint32_t nm = 0;
 
-  // value of tick t for this lane: S, or +inf when idle / not initialised
-  auto tick_value = [&](int t) -> double {
-    if (!act || t >= p.n_ticks) return INFINITY;
-    if (p.flags) {
-      const int64_t c = ((int64_t)trace * p.n_windows + p.tick_window[t]) * M + m;
-      const uint8_t f = p.flags[c];
-      return ((f & TRE_FLAG_IDLE) || !(f & TRE_FLAG_INIT)) ? INFINITY : p.vals[c];
+  const int nt = p.n_ticks;
+  const int64_t tbase = (int64_t)trace * (p.flags ? p.n_windows : nt);
+  // normalised values of ticks [t0, t0 + kTickBlock): unconditional loads
+  // from clamped indices, then the divisions, independent of each other
+  // (the tick's window and kind ride along: loads that other threads'
+  // stores might alias stay vector loads, so they are issued a block ahead)
+  auto load_block = [&](int t0, double (&v)[kTickBlock], uint32_t (&f)[kTickBlock],
+                        uint32_t (&tw)[kTickBlock]) {
+#pragma unroll
+    for (int u = 0; u < kTickBlock; ++u) {
+      const int t = t0 + u < nt ? t0 + u : nt - 1;
+      tw[u] = p.tick_window[t] | ((uint32_t)p.tick_kind[t] << 30);
+      if (p.flags) {
+        const int64_t c = (tbase + p.tick_window[t]) * M + mc;
+        v[u] = p.vals[c];
+        f[u] = p.flags[c];
+      } else {
+        v[u] = p.vals[(tbase + t) * M + mc];
+        f[u] = TRE_FLAG_INIT;
+      }
     }
-    return p.vals[((int64_t)trace * p.n_ticks + t) * M + m];
   };
-  double v_next = tick_value(0);
-
-  for (int t = 0; t < p.n_ticks; ++t) {
-    const int w = (int)p.tick_window[t];
-    const uint32_t kind = p.tick_kind[t];
-    const double v = v_next;
-    v_next = tick_value(t + 1);  // in flight during this tick's decisions
-    const double Z = act ? v / theta_eff : INFINITY;  // Eq. (2)
-    rw += (long long)R * (w - wprev);
-    wprev = w;
-    const bool crit = act && Z < tau_c;
-    const bool sur = act && Z > tau_s;
-    const bool any_crit = (__ballot(crit) & gmask) != 0ull;
+  auto normalise = [&](double (&v)[kTickBlock], const uint32_t (&f)[kTickBlock]) {
+#pragma unroll
+    for (int u = 0; u < kTickBlock; ++u) {
+      const bool live = act && !(f[u] & TRE_FLAG_IDLE) && (f[u] & TRE_FLAG_INIT);
+      v[u] = live ? v[u] / theta_eff : INFINITY;  // Eq. (2); +inf when idle or not initialised
+    }
+  };
+  auto decide = [&](uint32_t twk, double Z) {
+    const uint32_t tws = (uint32_t)__builtin_amdgcn_readfirstlane((int)twk);
+    const int w = (int)(tws & 0x3FFFFFFFu);
+    const uint32_t kind = tws >> 30;
+    const unsigned long long crit = __ballot(act && Z < tau_c);
+    unsigned long long ok;
     int path;
-    bool ok;
-    if (any_crit) {
-      if (!(kind & 1u)) continue;  // rescue pending: rebalancing defers
+    if (crit) {
+      if (!(kind & 1u)) return;  // rescue pending: rebalancing defers
       path = TRE_PATH_RESCUE;
       ok = crit;
     } else if (kind & 2u) {
       path = TRE_PATH_REBALANCE;
-      ok = act && Z < 1.0;
+      ok = __ballot(act && Z < 1.0);
     } else {
-      continue;
+      return;
     }
-    bool used = false;
+    const unsigned long long sur = __ballot(act && Z > tau_s);
+    unsigned long long used = 0ull;
     for (uint32_t k = 0; k < K; ++k) {
-      const int r = group_arg<false, G>(ok && !used, Z, gbase, gmask);  // Eq. (3)
+      const int r = wave_arg<false>(ok & ~used, Z, lane);  // Eq. (3)
       if (r < 0) break;
-      const double Zr = __shfl(Z, r, G);
       int d;
       if (pool > 0) {
         pool -= 1;
         d = TRE_DONOR_POOL;
       } else {
-        const bool cd = act && !used && m != r && R > r_min && Z > Zr && !crit;
-        d = group_arg<true, G>(cd && sur, Z, gbase, gmask);
-        if (d < 0) d = group_arg<true, G>(cd && !sur, Z, gbase, gmask);
+        const double Zr = read_lane_f64(Z, r);
+        const unsigned long long cd =
+            __ballot(act && R > r_min && Z > Zr) & ~crit & ~used & ~(1ull << r) & live_lanes;
+        d = wave_arg<true>(cd & sur, Z, lane);
+        if (d < 0) d = wave_arg<true>(cd & ~sur, Z, lane);
         if (d < 0) break;
-        if (m == d) {
-          R -= 1;
-          used = true;
-        }
+        used |= 1ull << d;
       }
-      if (m == r) {
-        R += 1;
-        used = true;
+      used |= 1ull << r;
+      if (lane == r || lane == d) {
+        rw += (long long)R * (w + 1 - since);
+        since = w + 1;
+        R += lane == r ? 1 : -1;
       }
-      if (m == 0 && nm < p.move_cap) {
+      if (lane == 0 && nm < p.move_cap) {
         tre_move mv;
         mv.window = (uint32_t)w;
         mv.path = (uint8_t)path;
@@ -783,13 +789,30 @@ __global__ __launch_bounds__(256) void rebalance(CtlParams p) {
       }
       ++nm;
     }
+  };
+  if (nt > 0) {
+    double va[kTickBlock], vb[kTickBlock];
+    uint32_t fa[kTickBlock], fb[kTickBlock], wa[kTickBlock], wb[kTickBlock];
+    load_block(0, va, fa, wa);
+    for (int t0 = 0; t0 < nt; t0 += 2 * kTickBlock) {
+      load_block(t0 + kTickBlock, vb, fb, wb);
+      normalise(va, fa);
+#pragma unroll
+      for (int u = 0; u < kTickBlock; ++u)
+        if (t0 + u < nt) decide(wa[u], va[u]);
+      load_block(t0 + 2 * kTickBlock, va, fa, wa);
+      normalise(vb, fb);
+#pragma unroll
+      for (int u = 0; u < kTickBlock; ++u)
+        if (t0 + kTickBlock + u < nt) decide(wb[u], vb[u]);
+    }
   }
-  rw += (long long)R * (p.n_windows - 1 - wprev);
+  rw += (long long)R * (p.n_windows - since);
   if (act) {
-    p.r_final[(int64_t)s * M + m] = R;
-    p.r_windows[(int64_t)s * M + m] = rw;
+    p.r_final[(int64_t)s * M + lane] = R;
+    p.r_windows[(int64_t)s * M + lane] = rw;
   }
-  if (sc_ok && m == 0) p.n_moves[s] = nm;
+  if (lane == 0) p.n_moves[s] = nm;
 }
 
 // ---------------------------------------------------------------- validate
@@ -1151,12 +1174,6 @@ static int launch_stream(const tre_events* ev, const StreamParams& p, hipStream_
   return TRE_OK;
 }
 
-static int group_size(int M) {
-  int g = 1;
-  while (g < M) g <<= 1;
-  return g;
-}
-
 static int launch_rebalance(const tre_events* ev, const tre_profile* prof, const double* vals,
                             const uint8_t* flags, const tre_scenario* sc, uint32_t n_sc,
                             const tre_ctl_out* out, hipStream_t st) {
@@ -1178,20 +1195,10 @@ static int launch_rebalance(const tre_events* ev, const tre_profile* prof, const
   c.n_moves = out->n_moves;
   c.r_final = out->r_final;
   c.r_windows = out->r_windows;
-  const int G = group_size(c.M);
-  const uint32_t spw = 64u / (uint32_t)G;
-  const uint64_t waves = ((uint64_t)n_sc + spw - 1) / spw;
-  const dim3 grid((unsigned)((waves + 3) / 4)), block(256);
+  // one wave per scenario, four per workgroup
+  const dim3 grid((unsigned)(((uint64_t)n_sc + 3) / 4)), block(256);
   LaunchTimer lt("rebalance", st);
-  switch (G) {
-    case 1: hipLaunchKernelGGL(rebalance<1>, grid, block, 0, st, c); break;
-    case 2: hipLaunchKernelGGL(rebalance<2>, grid, block, 0, st, c); break;
-    case 4: hipLaunchKernelGGL(rebalance<4>, grid, block, 0, st, c); break;
-    case 8: hipLaunchKernelGGL(rebalance<8>, grid, block, 0, st, c); break;
-    case 16: hipLaunchKernelGGL(rebalance<16>, grid, block, 0, st, c); break;
-    case 32: hipLaunchKernelGGL(rebalance<32>, grid, block, 0, st, c); break;
-    default: hipLaunchKernelGGL(rebalance<64>, grid, block, 0, st, c); break;
-  }
+  hipLaunchKernelGGL(rebalance, grid, block, 0, st, c);
   const hipError_t e = hipGetLastError();
   lt.done();
   if (e != hipSuccess) return fail(TRE_EHIP, "rebalance launch: %s", hipGetErrorString(e));
