@@ -109,6 +109,8 @@ struct StreamParams {
   int32_t chunk;    // windows evaluated per step (cells <= threads)
   int32_t fast_w;   // fast period in windows
   int32_t slow_w;   // slow period in windows
+  uint32_t magic_fast;  // floor(2^32 / fast_w), 2^32 - 1 for 1
+  uint32_t magic_slow;
   int32_t n_ticks;
   uint32_t* prefill;
   uint32_t* decode;
@@ -307,33 +309,31 @@ __device__ __forceinline__ void unpack32(unsigned long long v, int& hi, int& lo)
   hi = (int)(uint32_t)(v >> 32) + (int)((uint32_t)v >> 31);
 }
 
-// tick bookkeeping for one window: returns the tick ordinal or -1
-__device__ __forceinline__ int next_tick(int& fctr, int& sctr, int& tick, int fast_w, int slow_w) {
-  ++fctr;
-  ++sctr;
-  const bool fast = fctr == fast_w;
-  const bool slow = sctr == slow_w;
-  if (fast) fctr = 0;
-  if (slow) sctr = 0;
-  if (fast || slow) return tick++;
-  return -1;
+// x mod d for x < 2^32, with magic = floor(2^32 / d) (2^32 - 1 for d = 1):
+// the multiply-high undershoots the quotient by at most one
+__device__ __forceinline__ uint32_t mod_magic(uint32_t x, uint32_t d, uint32_t magic) {
+  const uint32_t r = x - __umulhi(x, magic) * d;
+  return r >= d ? r - d : r;
 }
 
 // One workgroup per trace; every thread tallies and evaluates, one barrier
 // per step. Step k, with [cA, cB) the chunk evaluated in step k-1 and
-// [cB, cC), cC = min(wl, cB + C), the windows completed by earlier tiles:
-//   - issue the loads of tile k+1, tally tile k into the LDS ring;
-//   - evaluate [cB, cC), one (window, model) cell per thread: carry prefix
-//     over the chunk, window integrals, Eq. (1) -> raw ratio and idle flag
-//     staged in LDS (two staging buffers, by step parity);
+// [cB, cC), cC = min(wl, cB + C), the windows completed by earlier tiles
+// (wl: the window of the last row tallied so far, or of the first row
+// deferred):
 //   - wave k % kWaves runs the smoothing chain over [cA, cB) from the
-//     other buffer (state in LDS, so the chain can move between waves);
-//   - clear the ring cells of [cA, cB);
+//     staging buffer of step k-1 (state in LDS, so the chain can move
+//     between waves), its tick windows from one ballot; first, so that its
+//     LDS reads find the queue the barrier just drained;
+//   - read and clear the ring cells of [cB, cC): complete windows;
+//   - issue the loads of tile k+1 and tally tile k into the ring: rows
+//     whose window reaches cB + wcap wait for a later tile. Rows of tile k
+//     come after every row of a complete window, so they land in windows
+//     >= cC, on slots disjoint from the chunk's;
+//   - evaluate [cB, cC), one (window, model) cell per thread: carry prefix
+//     over the chunk, window integrals, Eq. (1) -> raw ratio, staged in LDS
+//     (two staging buffers, by step parity);
 //   -- barrier -- the tile's rows are in; windows < wl are complete.
-// Ring slots in use are windows [cA, cA + wcap): rows whose window reaches
-// cA + wcap wait for a later tile, so a slot is never tallied while its
-// window is being evaluated, smoothed or cleared. Tile rows come after
-// every row of a complete window, so they never land in [cA, cC).
 template <int kWaves, int kEPT, bool kCells>
 __global__ __launch_bounds__(kWaves * 64) void tss_stream(StreamParams p) {
   constexpr int kThreads = kWaves * 64;
@@ -413,6 +413,63 @@ __global__ __launch_bounds__(kWaves * 64) void tss_stream(StreamParams p) {
   auto step = [&](Slice<kEPT>& cur, Slice<kEPT>& nxt, int k) -> bool {
     if (cA >= nW) return true;
     const int b3 = k % 3;
+    // ---- smooth [cA, cB) (staged last step); wave k mod kWaves, lanes < M
+    if (wave == k % kWaves && cB > cA) {
+      const bool own = lane < M;
+      const int m = own ? lane : 0;
+      const double* pr = st_raw + ((k + 1) & 1) * C * M + m;
+      const double alpha = s_alpha[m];
+      const double oma = 1.0 - alpha;
+      double S = s_S[m];
+      bool init = s_init[m] != 0;
+      // windows since the last fast / slow tick before cA, ticks so far
+      const uint32_t fctr = (uint32_t)s_tick[0], sctr = (uint32_t)s_tick[1];
+      int tick = s_tick[2];
+      const int nw = cB - cA;
+      // tick windows of the chunk: bit u for window cA + u (lanes u < nw)
+      const uint32_t u1 = (uint32_t)lane + 1u;
+      const uint32_t tm = (uint32_t)__ballot(lane < nw &&
+          (mod_magic(fctr + u1, (uint32_t)p.fast_w, p.magic_fast) == 0u ||
+           mod_magic(sctr + u1, (uint32_t)p.slow_w, p.magic_slow) == 0u));
+      for (int u0 = 0; u0 < nw; u0 += 4) {
+        double rv[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) rv[u] = pr[((u0 + u) & (C - 1)) * M];  // past nw: unused
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          if (u0 + u < nw) {
+            const int w = cA + u0 + u;
+            const double raw = rv[u];
+            const bool idle = raw < 0.0;
+            const double t1 = alpha * raw;
+            const double t2 = oma * S;
+            const double Sn = t1 + t2;
+            S = idle ? S : (init ? Sn : raw);
+            init = init || !idle;
+            if (cells && own) {
+              const int64_t c = ((int64_t)trace * nW + w) * M + m;
+              if (p.tss64) p.tss64[c] = S;
+              if (p.tss32) p.tss32[c] = (float)S;
+              if (p.flags) p.flags[c] = (uint8_t)((idle ? TRE_FLAG_IDLE : 0) | (init ? TRE_FLAG_INIT : 0));
+            }
+            if ((tm >> (u0 + u)) & 1u) {
+              if (own && p.snap && tick < p.n_ticks)
+                p.snap[((int64_t)trace * p.n_ticks + tick) * M + m] = (idle || !init) ? INFINITY : S;
+              ++tick;
+            }
+          }
+        }
+      }
+      if (own) {
+        s_S[m] = S;
+        s_init[m] = init ? 1 : 0;
+      }
+      if (lane == 0) {
+        s_tick[0] = (int)mod_magic(fctr + (uint32_t)nw, (uint32_t)p.fast_w, p.magic_fast);
+        s_tick[1] = (int)mod_magic(sctr + (uint32_t)nw, (uint32_t)p.slow_w, p.magic_slow);
+        s_tick[2] = tick;
+      }
+    }
     // ---- read and clear the cells of [cB, cC), one cell per thread (groups
     // of C lanes per model): complete windows that no row of this tile
     // reaches. LDS operations of a wave retire in order, so these reads go
@@ -511,54 +568,6 @@ __global__ __launch_bounds__(kWaves * 64) void tss_stream(StreamParams p) {
     if (n == 0 && tid < M) {
       cout[tid] = cin[tid];
       cout[TRE_MAX_MODELS + tid] = cin[TRE_MAX_MODELS + tid];
-    }
-    // ---- smooth [cA, cB) (staged last step); wave k mod kWaves, lanes < M
-    if (wave == k % kWaves && cB > cA) {
-      const bool own = lane < M;
-      const int m = own ? lane : 0;
-      const double* pr = st_raw + ((k + 1) & 1) * C * M + m;
-      const double alpha = s_alpha[m];
-      const double oma = 1.0 - alpha;
-      double S = s_S[m];
-      bool init = s_init[m] != 0;
-      int fctr = s_tick[0], sctr = s_tick[1], tick = s_tick[2];
-      const int nw = cB - cA;
-      for (int u0 = 0; u0 < nw; u0 += 4) {
-        double rv[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) rv[u] = pr[((u0 + u) & (C - 1)) * M];  // past nw: unused
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          if (u0 + u < nw) {
-            const int w = cA + u0 + u;
-            const double raw = rv[u];
-            const bool idle = raw < 0.0;
-            const double t1 = alpha * raw;
-            const double t2 = oma * S;
-            const double Sn = t1 + t2;
-            S = idle ? S : (init ? Sn : raw);
-            init = init || !idle;
-            if (cells && own) {
-              const int64_t c = ((int64_t)trace * nW + w) * M + m;
-              if (p.tss64) p.tss64[c] = S;
-              if (p.tss32) p.tss32[c] = (float)S;
-              if (p.flags) p.flags[c] = (uint8_t)((idle ? TRE_FLAG_IDLE : 0) | (init ? TRE_FLAG_INIT : 0));
-            }
-            const int tk = next_tick(fctr, sctr, tick, p.fast_w, p.slow_w);
-            if (own && tk >= 0 && p.snap && tk < p.n_ticks)
-              p.snap[((int64_t)trace * p.n_ticks + tk) * M + m] = (idle || !init) ? INFINITY : S;
-          }
-        }
-      }
-      if (own) {
-        s_S[m] = S;
-        s_init[m] = init ? 1 : 0;
-      }
-      if (lane == 0) {
-        s_tick[0] = fctr;
-        s_tick[1] = sctr;
-        s_tick[2] = tick;
-      }
     }
     // entries rotate over three steps: step k writes entry k % 3, every wave
     // reads it right after the barrier that ends step k, and it is reset
@@ -1154,6 +1163,8 @@ static StreamParams stream_params(const tre_events* ev, const tre_profile* prof)
   p.chunk = chunk_windows(ev->cfg.n_models, ev->wcap);
   p.fast_w = (int32_t)(ev->cfg.fast_period_ms / ev->cfg.window_ms);
   p.slow_w = (int32_t)(ev->cfg.slow_period_ms / ev->cfg.window_ms);
+  p.magic_fast = p.fast_w == 1 ? 0xFFFFFFFFu : (uint32_t)((1ull << 32) / (uint64_t)p.fast_w);
+  p.magic_slow = p.slow_w == 1 ? 0xFFFFFFFFu : (uint32_t)((1ull << 32) / (uint64_t)p.slow_w);
   p.n_ticks = (int32_t)ev->n_ticks;
   return p;
 }
