@@ -20,6 +20,7 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "tre_oracle.c")
+_SRC_ACT = os.path.join(_HERE, "tre_oracle_act.c")  # control replay with the actuation model
 _LIB = os.path.join(_HERE, "libtre_oracle.so")
 
 CFLAGS = ["-O2", "-fPIC", "-shared", "-ffp-contract=off", "-fno-fast-math", "-std=c11"]
@@ -38,10 +39,14 @@ assert PROFILE_DTYPE.itemsize == 56 and SCENARIO_DTYPE.itemsize == 24 and MOVE_D
 
 
 def build(force: bool = True, src: str = _SRC, out: str = _LIB) -> str:
-    """Compile the oracle with gcc (building the checker is not using it)."""
-    if force or not os.path.exists(out) or os.path.getmtime(out) < os.path.getmtime(src):
+    """Compile the oracle with gcc (building the checker is not using it).
+    The default library also holds the actuation-model replay; a library
+    built from another base source (the pin-strength tests) does not."""
+    srcs = [src] + ([_SRC_ACT] if src == _SRC else [])
+    stale = not os.path.exists(out) or any(os.path.getmtime(out) < os.path.getmtime(x) for x in srcs)
+    if force or stale:
         tmp = f"{out}.{os.getpid()}.tmp"
-        subprocess.check_call(["gcc", *CFLAGS, "-o", tmp, src, "-lm"])
+        subprocess.check_call(["gcc", *CFLAGS, "-o", tmp, *srcs, "-lm"])
         os.replace(tmp, out)
     return out
 
@@ -61,6 +66,11 @@ class Oracle:
         L.oracle_tss_trace.argtypes = [vp, vp, vp, vp, i64, i64, i64, i32, vp, vp, vp, vp, vp, vp, vp]
         L.oracle_control.restype = ctypes.c_int
         L.oracle_control.argtypes = [i64, i64, i64, i64, i32, i32, vp, vp, vp, vp, vp, u32, vp, vp, vp]
+        self.has_act = hasattr(L, "oracle_control_act")
+        if self.has_act:
+            L.oracle_control_act.restype = ctypes.c_int
+            L.oracle_control_act.argtypes = [i64, i64, i64, i64, i32, i32, vp, vp, vp, vp, i64, i64, vp, vp,
+                                             vp, u32, vp, vp, vp, vp, vp]
         self.L = L
         self.path = path
 
@@ -120,14 +130,48 @@ class Oracle:
                 "r_windows": r_windows}
 
 
+    def control_act(self, cfg: Dict[str, int], prof: np.ndarray, S: np.ndarray, flags: np.ndarray,
+                    sc: np.ndarray, wake_w: int, sleep_w: int, footprint: Optional[np.ndarray] = None,
+                    veto: Optional[np.ndarray] = None, move_cap: Optional[int] = None) -> Dict[str, np.ndarray]:
+        """Control replay of one scenario with the actuation model: delays in
+        whole windows, footprint [M] GPUs per replica (None: 1), veto
+        [n_ticks] uint64 donor-release masks (None: none)."""
+        prof = np.ascontiguousarray(prof, dtype=PROFILE_DTYPE)
+        sc = np.ascontiguousarray(np.atleast_1d(sc), dtype=SCENARIO_DTYPE)
+        M = prof.shape[0]
+        nW = cfg["duration_ms"] // cfg["window_ms"]
+        if move_cap is None:
+            move_cap = max(1, nW * int(sc[0]["max_moves"]))
+        S = np.ascontiguousarray(S, np.float64)
+        flags = np.ascontiguousarray(flags, np.uint8)
+        fp = None if footprint is None else np.ascontiguousarray(footprint, np.int32)
+        vt = None if veto is None else np.ascontiguousarray(veto, np.uint64)
+        moves = np.zeros(move_cap, MOVE_DTYPE)
+        n_moves = np.zeros(1, np.uint32)
+        r_final = np.zeros(M, np.int32)
+        r_windows = np.zeros(M, np.int64)
+        idle = np.zeros(1, np.int64)
+        held = np.zeros(M, np.int32)
+        rc = self.L.oracle_control_act(
+            cfg["window_ms"], cfg["duration_ms"], cfg["fast_period_ms"], cfg["slow_period_ms"], M, cfg["budget"],
+            prof.ctypes.data, S.ctypes.data, flags.ctypes.data, sc.ctypes.data, int(wake_w), int(sleep_w),
+            None if fp is None else fp.ctypes.data, None if vt is None else vt.ctypes.data, moves.ctypes.data,
+            move_cap, n_moves.ctypes.data, r_final.ctypes.data, r_windows.ctypes.data, idle.ctypes.data,
+            held.ctypes.data)
+        if rc:
+            raise ValueError(f"oracle_control_act rejected the scenario ({rc})")
+        n = int(n_moves[0])
+        return {"moves": moves[:min(n, move_cap)].copy(), "n_moves": n, "r_final": r_final,
+                "r_windows": r_windows, "idle_final": int(idle[0]), "held_final": held}
+
+
 _default: Optional[Oracle] = None
 
 
 def get() -> Oracle:
     global _default
     if _default is None:
-        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
-            build(force=True)
+        build(force=False)  # rebuilds when a source is newer
         _default = Oracle(_LIB)
     return _default
 
