@@ -242,6 +242,52 @@ int tre_sweep(const tre_events* ev, const tre_profile* prof, const tre_scenario*
               uint32_t n_scenarios, const tre_ctl_out* out, float* tss32, void* ws,
               size_t ws_bytes, void* stream);
 
+/* ------------------------------------------------------- actuation model
+ * Optional model of how a decided transition is carried out (Sections
+ * "Dual-Speed Control", "Bounded Pairwise Transfer", "System Boundary and
+ * Replica State"; the paper measures seconds for sleep and wake):
+ *   - cfg.budget counts GPUs and a replica of model m holds footprint[m]
+ *     GPUs (NULL: 1 each); idle GPUs = budget - GPUs of routable, waking and
+ *     draining replicas;
+ *   - idle capacity: if at least g_r GPUs are idle the receiver wakes a
+ *     replica on them; it is routable wake_ms later;
+ *   - donor release: the donor's replica stops being routable at once
+ *     (hidden while it drains and sleeps, sleep_ms); its GPUs reach the
+ *     receiver when the sleep completes and the receiver's wake starts then;
+ *     a shortfall g_r - g_d is taken from the idle GPUs at the move (a donor
+ *     qualifies only if enough are idle), an excess returns to them after the
+ *     sleep;
+ *   - a model with a transition in flight is neither receiver nor donor (a
+ *     transfer in progress is not pre-empted);
+ *   - veto (NULL: none): [n_traces][n_ticks] masks, bit m set when the
+ *     donor-side release guard refuses model m at that tick;
+ *   - delays are rounded up to whole windows; a transition completing at the
+ *     end of window u counts from window u + 1 (routable replicas, idle GPUs
+ *     for the next tick); r_final counts transitions completing by the end of
+ *     the last window.
+ * With zero delays, unit footprints and no vetoes the results equal those of
+ * the calls without the model. footprint and veto are device memory. */
+typedef struct {
+  int64_t wake_ms;
+  int64_t sleep_ms;
+  const int32_t* footprint;  /* device [n_traces][n_models], >= 1, or NULL */
+  const uint64_t* veto;      /* device [n_traces][n_ticks], or NULL        */
+} tre_actuation;
+
+/* Check an actuation model against a profile table (device): footprints in
+   1 .. budget and the initial replicas' GPUs within the budget per trace.
+   Synchronous. */
+int tre_check_actuation(const tre_events* ev, const tre_profile* prof, const tre_actuation* act);
+
+/* tre_rebalance and tre_sweep with the actuation model (act: host, read
+   during the call). */
+int tre_rebalance_act(const tre_events* ev, const tre_profile* prof, const double* tss64,
+                      const uint8_t* flags, const tre_scenario* sc, uint32_t n_scenarios,
+                      const tre_actuation* act, const tre_ctl_out* out, void* stream);
+int tre_sweep_act(const tre_events* ev, const tre_profile* prof, const tre_scenario* sc,
+                  uint32_t n_scenarios, const tre_actuation* act, const tre_ctl_out* out,
+                  float* tss32, void* ws, size_t ws_bytes, void* stream);
+
 /* Kernel timing (HIP events recorded around each launch on its stream).
    tre_set_timing(1) starts recording; tre_kernel_time waits for the
    recorded launches of `kernel` ("tss_stream", "rebalance", "validate")

@@ -628,6 +628,11 @@ struct CtlParams {
   uint32_t* n_moves;
   int32_t* r_final;
   int64_t* r_windows;
+  // actuation model (the kAct instantiation)
+  int32_t wake_w;            // windows from a wake's start until routable
+  int32_t sleep_w;           // windows a released replica hides, drains and sleeps
+  const int32_t* footprint;  // [trace][M] GPUs per replica, or NULL (1)
+  const uint64_t* veto;      // [trace][tick] donor releases refused, or NULL
 };
 
 __device__ __forceinline__ unsigned long long dbits(double x) {
@@ -686,6 +691,15 @@ constexpr int kTickBlock = 8;  // ticks loaded and normalised per block
 // (ballots are the candidate sets, receiver and donor are scalars). Per
 // tick: Eq. (2), regions, the cadence rule, then up to K greedy moves with
 // Eq. (3) for the receiver and the donor order of the bounded transfer.
+// kAct adds the actuation model: the budget counts GPUs (footprint g per
+// replica); a woken replica becomes routable wake_w windows after its wake
+// starts; a donor's replica stops being routable at once and its GPUs reach
+// the receiver after sleep_w windows, when the receiver's wake starts (any
+// shortfall g_r - g_d comes from the idle GPUs at the move, any excess
+// returns to them after the sleep); a model with a transition in flight is
+// neither receiver nor donor; vetoed models do not release. A transition
+// completing at the end of window u counts from window u + 1.
+template <bool kAct>
 __global__ __launch_bounds__(256) void rebalance(CtlParams p) {
   const int lane = threadIdx.x & 63;
   const uint32_t s = (uint32_t)((blockIdx.x * blockDim.x + threadIdx.x) >> 6);
@@ -702,33 +716,60 @@ __global__ __launch_bounds__(256) void rebalance(CtlParams p) {
   const double tau_s = pr.tau_surplus;
   const int r_min = pr.r_min;
   int R = act ? pr.r_init : 0;
-  int rsum = R;
+  // GPUs per replica (1 without the actuation model)
+  int g = 1;
+  if (kAct && p.footprint && act) g = p.footprint[(int64_t)trace * M + lane];
+  int rsum = R * g;
   rsum += __shfl_xor(rsum, 1);
   rsum += __shfl_xor(rsum, 2);
   rsum += __shfl_xor(rsum, 4);
   rsum += __shfl_xor(rsum, 8);
   rsum += __shfl_xor(rsum, 16);
   rsum += __shfl_xor(rsum, 32);
-  int pool = p.budget - __builtin_amdgcn_readfirstlane(rsum);
+  int pool = p.budget - __builtin_amdgcn_readfirstlane(rsum);  // idle replicas / GPUs
   const unsigned long long live_lanes = __ballot(act);
   // replica-window sums accumulate when a lane's R changes: windows
-  // [since, w] ran with the old R, a move at tick window w applies from w+1
+  // [since, w] ran with the old R, a change at the end of window w applies
+  // from w+1
   long long rw = 0;
   int since = 0;
   uint32_t nm = 0;
+  // actuation state of the lane's model: transition in flight (0 none,
+  // 1 wake, 2 sleep), the window at whose end it completes, GPUs a sleep
+  // returns to the idle pool
+  int tkind = 0, tuntil = 0, tret = 0;
+  auto complete = [&](int w) {  // transitions that completed before window w
+    if constexpr (kAct) {
+      const bool done = tkind != 0 && tuntil < w;
+      if (done && tkind == 1) {
+        rw += (long long)R * (tuntil + 1 - since);
+        since = tuntil + 1;
+        R += 1;
+      }
+      unsigned long long back = __ballot(done && tkind == 2 && tret > 0);
+      while (back) {
+        const int l = __ffsll((long long)back) - 1;
+        pool += __builtin_amdgcn_readlane(tret, l);
+        back &= back - 1ull;
+      }
+      if (done) tkind = 0;
+    }
+  };
 
   const int nt = p.n_ticks;
   const int64_t tbase = (int64_t)trace * (p.flags ? p.n_windows : nt);
   // normalised values of ticks [t0, t0 + kTickBlock): unconditional loads
   // from clamped indices, then the divisions, independent of each other
-  // (the tick's window and kind ride along: loads that other threads'
-  // stores might alias stay vector loads, so they are issued a block ahead)
+  // (the tick's window, kind and vetoes ride along: loads that other
+  // threads' stores might alias stay vector loads, so they are issued a
+  // block ahead)
   auto load_block = [&](int t0, double (&v)[kTickBlock], uint32_t (&f)[kTickBlock],
-                        uint32_t (&tw)[kTickBlock]) {
+                        uint32_t (&tw)[kTickBlock], unsigned long long (&vt)[kTickBlock]) {
 #pragma unroll
     for (int u = 0; u < kTickBlock; ++u) {
       const int t = t0 + u < nt ? t0 + u : nt - 1;
       tw[u] = p.tick_window[t] | ((uint32_t)p.tick_kind[t] << 30);
+      vt[u] = (kAct && p.veto) ? p.veto[(int64_t)trace * nt + t] : 0ull;
       if (p.flags) {
         const int64_t c = (tbase + p.tick_window[t]) * M + mc;
         v[u] = p.vals[c];
@@ -746,10 +787,11 @@ __global__ __launch_bounds__(256) void rebalance(CtlParams p) {
       v[u] = live ? v[u] / theta_eff : INFINITY;  // Eq. (2); +inf when idle or not initialised
     }
   };
-  auto decide = [&](uint32_t twk, double Z) {
+  auto decide = [&](uint32_t twk, double Z, unsigned long long vetoed) {
     const uint32_t tws = (uint32_t)__builtin_amdgcn_readfirstlane((int)twk);
     const int w = (int)(tws & 0x3FFFFFFFu);
     const uint32_t kind = tws >> 30;
+    complete(w);
     const unsigned long long crit = __ballot(act && Z < tau_c);
     unsigned long long ok;
     int path;
@@ -764,28 +806,55 @@ __global__ __launch_bounds__(256) void rebalance(CtlParams p) {
       return;
     }
     const unsigned long long sur = __ballot(act && Z > tau_s);
-    unsigned long long used = 0ull;
+    // models already in a transition: earlier in this tick, or in flight
+    unsigned long long used = kAct ? __ballot(tkind != 0) : 0ull;
+    // both halves widened as unsigned (a set bit 31 must not sign-extend)
+    const unsigned long long veto_mask =
+        kAct ? ((unsigned long long)(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)vetoed) |
+                ((unsigned long long)(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(vetoed >> 32)) << 32))
+             : 0ull;
     for (uint32_t k = 0; k < K; ++k) {
       const int r = wave_arg<false>(ok & ~used, Z, lane);  // Eq. (3)
       if (r < 0) break;
+      const int g_r = kAct ? __builtin_amdgcn_readlane(g, r) : 1;
       int d;
-      if (pool > 0) {
-        pool -= 1;
+      if (pool >= g_r) {
+        pool -= g_r;
         d = TRE_DONOR_POOL;
+        if (kAct && lane == r) {
+          tkind = 1;
+          tuntil = w + p.wake_w;
+        }
       } else {
         const double Zr = read_lane_f64(Z, r);
         const unsigned long long cd =
-            __ballot(act && R > r_min && Z > Zr) & ~crit & ~used & ~(1ull << r) & live_lanes;
+            __ballot(act && R > r_min && Z > Zr && (!kAct || pool >= g_r - g)) & ~crit & ~used &
+            ~(1ull << r) & live_lanes & ~veto_mask;
         d = wave_arg<true>(cd & sur, Z, lane);
         if (d < 0) d = wave_arg<true>(cd & ~sur, Z, lane);
         if (d < 0) break;
         used |= 1ull << d;
+        if constexpr (kAct) {
+          const int short_by = g_r - __builtin_amdgcn_readlane(g, d);
+          if (short_by > 0) pool -= short_by;
+          if (lane == d) {
+            tkind = 2;
+            tuntil = w + p.sleep_w;
+            tret = short_by < 0 ? -short_by : 0;
+          }
+          if (lane == r) {
+            tkind = 1;
+            tuntil = w + p.sleep_w + p.wake_w;
+          }
+        }
       }
       used |= 1ull << r;
-      if (lane == r || lane == d) {
+      // routable changes: the donor's at once (from w+1), the receiver's
+      // here only without the actuation model (else when its wake completes)
+      if (lane == d || (!kAct && lane == r)) {
         rw += (long long)R * (w + 1 - since);
         since = w + 1;
-        R += lane == r ? 1 : -1;
+        R += lane == d ? -1 : 1;
       }
       if (lane == 0 && nm < p.move_cap) {
         tre_move mv;
@@ -802,20 +871,22 @@ __global__ __launch_bounds__(256) void rebalance(CtlParams p) {
   if (nt > 0) {
     double va[kTickBlock], vb[kTickBlock];
     uint32_t fa[kTickBlock], fb[kTickBlock], wa[kTickBlock], wb[kTickBlock];
-    load_block(0, va, fa, wa);
+    unsigned long long xa[kTickBlock], xb[kTickBlock];
+    load_block(0, va, fa, wa, xa);
     for (int t0 = 0; t0 < nt; t0 += 2 * kTickBlock) {
-      load_block(t0 + kTickBlock, vb, fb, wb);
+      load_block(t0 + kTickBlock, vb, fb, wb, xb);
       normalise(va, fa);
 #pragma unroll
       for (int u = 0; u < kTickBlock; ++u)
-        if (t0 + u < nt) decide(wa[u], va[u]);
-      load_block(t0 + 2 * kTickBlock, va, fa, wa);
+        if (t0 + u < nt) decide(wa[u], va[u], xa[u]);
+      load_block(t0 + 2 * kTickBlock, va, fa, wa, xa);
       normalise(vb, fb);
 #pragma unroll
       for (int u = 0; u < kTickBlock; ++u)
-        if (t0 + kTickBlock + u < nt) decide(wb[u], vb[u]);
+        if (t0 + kTickBlock + u < nt) decide(wb[u], vb[u], xb[u]);
     }
   }
+  complete(p.n_windows);  // transitions completing at the end of the last window count as done
   rw += (long long)R * (p.n_windows - since);
   if (act) {
     p.r_final[(int64_t)s * M + lane] = R;
@@ -1185,9 +1256,32 @@ static int launch_stream(const tre_events* ev, const StreamParams& p, hipStream_
   return TRE_OK;
 }
 
+// the actuation model in whole windows (delays rounded up)
+struct ActWindows {
+  int32_t wake_w, sleep_w;
+  const int32_t* footprint;
+  const uint64_t* veto;
+};
+
+static int act_windows(const tre_events* ev, const tre_actuation* act, ActWindows* aw) {
+  if (!act) return fail(TRE_EINVAL, "NULL actuation model");
+  if (act->wake_ms < 0 || act->sleep_ms < 0)
+    return fail(TRE_EINVAL, "actuation delays must be >= 0");
+  const int64_t win = ev->cfg.window_ms;
+  // whole windows, rounded up; a transition completing after the last window
+  // never counts, so the delays are capped just past the trace
+  const int64_t cap = ev->n_windows + 1;
+  auto to_windows = [&](int64_t ms) { return ms > cap * win ? cap : (ms + win - 1) / win; };
+  aw->wake_w = (int32_t)to_windows(act->wake_ms);
+  aw->sleep_w = (int32_t)to_windows(act->sleep_ms);
+  aw->footprint = act->footprint;
+  aw->veto = act->veto;
+  return TRE_OK;
+}
+
 static int launch_rebalance(const tre_events* ev, const tre_profile* prof, const double* vals,
                             const uint8_t* flags, const tre_scenario* sc, uint32_t n_sc,
-                            const tre_ctl_out* out, hipStream_t st) {
+                            const tre_ctl_out* out, const ActWindows* aw, hipStream_t st) {
   CtlParams c{};
   c.prof = prof;
   c.sc = sc;
@@ -1206,10 +1300,19 @@ static int launch_rebalance(const tre_events* ev, const tre_profile* prof, const
   c.n_moves = out->n_moves;
   c.r_final = out->r_final;
   c.r_windows = out->r_windows;
+  if (aw) {
+    c.wake_w = aw->wake_w;
+    c.sleep_w = aw->sleep_w;
+    c.footprint = aw->footprint;
+    c.veto = aw->veto;
+  }
   // one wave per scenario, four per workgroup
   const dim3 grid((unsigned)(((uint64_t)n_sc + 3) / 4)), block(256);
   LaunchTimer lt("rebalance", st);
-  hipLaunchKernelGGL(rebalance, grid, block, 0, st, c);
+  if (aw)
+    hipLaunchKernelGGL(rebalance<true>, grid, block, 0, st, c);
+  else
+    hipLaunchKernelGGL(rebalance<false>, grid, block, 0, st, c);
   const hipError_t e = hipGetLastError();
   lt.done();
   if (e != hipSuccess) return fail(TRE_EHIP, "rebalance launch: %s", hipGetErrorString(e));
@@ -1239,28 +1342,34 @@ extern "C" int tre_eval_tss(const tre_events* ev, const tre_profile* prof, const
   return launch_stream(ev, p, (hipStream_t)stream);
 }
 
-extern "C" int tre_rebalance(const tre_events* ev, const tre_profile* prof, const double* tss64,
-                             const uint8_t* flags, const tre_scenario* sc, uint32_t n_scenarios,
-                             const tre_ctl_out* out, void* stream) {
-  if (!ev || !prof || !tss64 || !flags) return fail(TRE_EINVAL, "tre_rebalance: NULL argument");
-  if (n_scenarios && !sc) return fail(TRE_EINVAL, "tre_rebalance: NULL scenarios");
+static int rebalance_impl(const tre_events* ev, const tre_profile* prof, const double* tss64,
+                          const uint8_t* flags, const tre_scenario* sc, uint32_t n_scenarios,
+                          const tre_actuation* act, const tre_ctl_out* out, void* stream,
+                          const char* who) {
+  if (!ev || !prof || !tss64 || !flags) return fail(TRE_EINVAL, "%s: NULL argument", who);
+  if (n_scenarios && !sc) return fail(TRE_EINVAL, "%s: NULL scenarios", who);
   int rc = check_ctl_out(out, n_scenarios);
   if (rc) return rc;
   rc = check_device(ev);
   if (rc) return rc;
+  ActWindows aw;
+  if (act && (rc = act_windows(ev, act, &aw))) return rc;
   if (n_scenarios == 0) return TRE_OK;
-  return launch_rebalance(ev, prof, tss64, flags, sc, n_scenarios, out, (hipStream_t)stream);
+  return launch_rebalance(ev, prof, tss64, flags, sc, n_scenarios, out, act ? &aw : nullptr,
+                          (hipStream_t)stream);
 }
 
-extern "C" int tre_sweep(const tre_events* ev, const tre_profile* prof, const tre_scenario* sc,
-                         uint32_t n_scenarios, const tre_ctl_out* out, float* tss32, void* ws,
-                         size_t ws_bytes, void* stream) {
-  if (!ev || !prof) return fail(TRE_EINVAL, "tre_sweep: NULL argument");
-  if (n_scenarios && !sc) return fail(TRE_EINVAL, "tre_sweep: NULL scenarios");
+static int sweep_impl(const tre_events* ev, const tre_profile* prof, const tre_scenario* sc,
+                      uint32_t n_scenarios, const tre_actuation* act, const tre_ctl_out* out,
+                      float* tss32, void* ws, size_t ws_bytes, void* stream, const char* who) {
+  if (!ev || !prof) return fail(TRE_EINVAL, "%s: NULL argument", who);
+  if (n_scenarios && !sc) return fail(TRE_EINVAL, "%s: NULL scenarios", who);
   int rc = check_ctl_out(out, n_scenarios);
   if (rc) return rc;
   rc = check_device(ev);
   if (rc) return rc;
+  ActWindows aw;
+  if (act && (rc = act_windows(ev, act, &aw))) return rc;
   size_t need = 0;
   tre_workspace_size(ev, n_scenarios, &need);
   if (!ws || ws_bytes < need)
@@ -1272,5 +1381,60 @@ extern "C" int tre_sweep(const tre_events* ev, const tre_profile* prof, const tr
   p.snap = (double*)ws;
   rc = launch_stream(ev, p, st);
   if (rc || n_scenarios == 0) return rc;
-  return launch_rebalance(ev, prof, (const double*)ws, nullptr, sc, n_scenarios, out, st);
+  return launch_rebalance(ev, prof, (const double*)ws, nullptr, sc, n_scenarios, out,
+                          act ? &aw : nullptr, st);
+}
+
+extern "C" int tre_rebalance(const tre_events* ev, const tre_profile* prof, const double* tss64,
+                             const uint8_t* flags, const tre_scenario* sc, uint32_t n_scenarios,
+                             const tre_ctl_out* out, void* stream) {
+  return rebalance_impl(ev, prof, tss64, flags, sc, n_scenarios, nullptr, out, stream, "tre_rebalance");
+}
+
+extern "C" int tre_sweep(const tre_events* ev, const tre_profile* prof, const tre_scenario* sc,
+                         uint32_t n_scenarios, const tre_ctl_out* out, float* tss32, void* ws,
+                         size_t ws_bytes, void* stream) {
+  return sweep_impl(ev, prof, sc, n_scenarios, nullptr, out, tss32, ws, ws_bytes, stream, "tre_sweep");
+}
+
+extern "C" int tre_rebalance_act(const tre_events* ev, const tre_profile* prof, const double* tss64,
+                                 const uint8_t* flags, const tre_scenario* sc, uint32_t n_scenarios,
+                                 const tre_actuation* act, const tre_ctl_out* out, void* stream) {
+  if (!act) return fail(TRE_EINVAL, "tre_rebalance_act: NULL actuation model");
+  return rebalance_impl(ev, prof, tss64, flags, sc, n_scenarios, act, out, stream, "tre_rebalance_act");
+}
+
+extern "C" int tre_sweep_act(const tre_events* ev, const tre_profile* prof, const tre_scenario* sc,
+                             uint32_t n_scenarios, const tre_actuation* act, const tre_ctl_out* out,
+                             float* tss32, void* ws, size_t ws_bytes, void* stream) {
+  if (!act) return fail(TRE_EINVAL, "tre_sweep_act: NULL actuation model");
+  return sweep_impl(ev, prof, sc, n_scenarios, act, out, tss32, ws, ws_bytes, stream, "tre_sweep_act");
+}
+
+extern "C" int tre_check_actuation(const tre_events* ev, const tre_profile* prof,
+                                   const tre_actuation* act) {
+  if (!ev || !prof || !act) return fail(TRE_EINVAL, "tre_check_actuation: NULL argument");
+  int rc = check_device(ev);
+  if (rc) return rc;
+  ActWindows aw;
+  if ((rc = act_windows(ev, act, &aw))) return rc;
+  const size_t M = (size_t)ev->cfg.n_models;
+  std::vector<tre_profile> hp((size_t)ev->n_traces * M);
+  HIP_TRY(hipMemcpy(hp.data(), prof, hp.size() * sizeof(tre_profile), hipMemcpyDeviceToHost));
+  std::vector<int32_t> g(hp.size(), 1);
+  if (act->footprint)
+    HIP_TRY(hipMemcpy(g.data(), act->footprint, g.size() * sizeof(int32_t), hipMemcpyDeviceToHost));
+  for (uint32_t t = 0; t < ev->n_traces; ++t) {
+    long long gsum = 0;
+    for (size_t m = 0; m < M; ++m) {
+      const int32_t gm = g[t * M + m];
+      if (gm < 1 || gm > ev->cfg.budget)
+        return fail(TRE_EINVAL, "trace %u model %zu: footprint %d outside 1 .. budget", t, m, gm);
+      gsum += (long long)gm * hp[t * M + m].r_init;
+    }
+    if (gsum > ev->cfg.budget)
+      return fail(TRE_EINVAL, "trace %u: initial replicas hold %lld GPUs, above the budget %d", t,
+                  gsum, ev->cfg.budget);
+  }
+  return TRE_OK;
 }

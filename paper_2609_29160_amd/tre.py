@@ -62,9 +62,14 @@ class _CtlOut(ctypes.Structure):
                 ("r_windows", ctypes.c_void_p)]
 
 
+class _Actuation(ctypes.Structure):
+    _fields_ = [("wake_ms", ctypes.c_int64), ("sleep_ms", ctypes.c_int64), ("footprint", ctypes.c_void_p),
+                ("veto", ctypes.c_void_p)]
+
+
 EXPORTS = ["tre_last_error", "tre_load_events", "tre_free_events", "tre_events_info",
            "tre_check_params", "tre_workspace_size", "tre_eval_tss", "tre_rebalance", "tre_sweep",
-           "tre_set_timing", "tre_kernel_time"]
+           "tre_set_timing", "tre_kernel_time", "tre_check_actuation", "tre_rebalance_act", "tre_sweep_act"]
 
 
 def _load():
@@ -91,6 +96,12 @@ def _load():
     L.tre_rebalance.argtypes = [vp, vp, vp, vp, vp, u32, ctypes.POINTER(_CtlOut), vp]
     L.tre_sweep.restype = i32
     L.tre_sweep.argtypes = [vp, vp, vp, u32, ctypes.POINTER(_CtlOut), vp, vp, sz, vp]
+    L.tre_check_actuation.restype = i32
+    L.tre_check_actuation.argtypes = [vp, vp, ctypes.POINTER(_Actuation)]
+    L.tre_rebalance_act.restype = i32
+    L.tre_rebalance_act.argtypes = [vp, vp, vp, vp, vp, u32, ctypes.POINTER(_Actuation), ctypes.POINTER(_CtlOut), vp]
+    L.tre_sweep_act.restype = i32
+    L.tre_sweep_act.argtypes = [vp, vp, vp, u32, ctypes.POINTER(_Actuation), ctypes.POINTER(_CtlOut), vp, vp, sz, vp]
     L.tre_set_timing.restype = i32
     L.tre_set_timing.argtypes = [i32]
     L.tre_kernel_time.restype = i32
@@ -235,6 +246,37 @@ def tre_sweep(ev: Events, prof: torch.Tensor, sc: torch.Tensor, out: Dict[str, t
     o = _ctl(out)
     _check(_L.tre_sweep(ev.handle, _ptr(prof), _ptr(sc), n_sc, ctypes.byref(o), _ptr(tss32), _ptr(ws),
                         ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def actuation(wake_ms: int, sleep_ms: int, footprint: Optional[torch.Tensor] = None,
+              veto: Optional[torch.Tensor] = None) -> _Actuation:
+    """The actuation model of include/tre.h: delays in ms; footprint (int32
+    [n_traces][n_models]) and veto (uint64 / int64 [n_traces][n_ticks]) are
+    device tensors or None. Keep the tensors alive while the model is used."""
+    for t, name in ((footprint, "footprint"), (veto, "veto")):
+        if t is not None and not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+    return _Actuation(int(wake_ms), int(sleep_ms), _ptr(footprint), _ptr(veto))
+
+
+def tre_check_actuation(ev: Events, prof: torch.Tensor, act: _Actuation):
+    _check(_L.tre_check_actuation(ev.handle, _ptr(prof), ctypes.byref(act)))
+
+
+def tre_rebalance_act(ev: Events, prof: torch.Tensor, tss64: torch.Tensor, flags: torch.Tensor,
+                      sc: torch.Tensor, act: _Actuation, out: Dict[str, torch.Tensor], stream=None):
+    n_sc = sc.numel() // SCENARIO_DTYPE.itemsize
+    o = _ctl(out)
+    _check(_L.tre_rebalance_act(ev.handle, _ptr(prof), _ptr(tss64), _ptr(flags), _ptr(sc), n_sc,
+                                ctypes.byref(act), ctypes.byref(o), _stream(stream)))
+
+
+def tre_sweep_act(ev: Events, prof: torch.Tensor, sc: torch.Tensor, act: _Actuation, out: Dict[str, torch.Tensor],
+                  ws: torch.Tensor, tss32: Optional[torch.Tensor] = None, stream=None):
+    n_sc = sc.numel() // SCENARIO_DTYPE.itemsize
+    o = _ctl(out)
+    _check(_L.tre_sweep_act(ev.handle, _ptr(prof), _ptr(sc), n_sc, ctypes.byref(act), ctypes.byref(o), _ptr(tss32),
+                            _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 
 def tre_set_timing(enable: bool):

@@ -45,6 +45,7 @@ def test_struct_layouts():
     assert ctypes.sizeof(tre._TraceCfg) == 40
     assert ctypes.sizeof(tre._CtlOut) == 40
     assert ctypes.sizeof(tre._TssOut) == 56
+    assert ctypes.sizeof(tre._Actuation) == 32
 
 
 def test_error_message_without_gpu_call():

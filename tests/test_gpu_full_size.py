@@ -29,7 +29,10 @@ def _outputs(out):
     return {k: out[k].cpu().numpy().copy() for k in ("moves", "n_moves", "r_final", "r_windows")}
 
 
-def _run_full(workload_index, sample_traces, tss_traces):
+def _run_full(workload_index, sample_traces, tss_traces, act_seed=None):
+    """act_seed: run with the actuation model (the paper's 1.31 s wake and
+    1.87 s sleep, footprints of 1 or 2 GPUs drawn from the seed, the budget
+    raised to fit with 8 GPUs to spare, vetoes on 10% of the ticks)."""
     import torch
 
     from paper_2609_29160_amd import device, tre
@@ -37,8 +40,27 @@ def _run_full(workload_index, sample_traces, tss_traces):
     w = tg.standard(workload_index)
     say(f"{w.name}: uploading")
     dt = device.upload(w)
-    ev = device.load(dt, validate=True)
+    cfg = dict(w.trace_cfg())
+    M = w.n_models
+    act = g = veto = None
+    if act_seed is not None:
+        rng = np.random.default_rng(act_seed)
+        g = rng.integers(1, 3, (w.n_traces, M)).astype(np.int32)
+        r_init = np.asarray(w.profile_columns()["r_init"]).reshape(w.n_traces, M)
+        cfg["budget"] = int((g * r_init).sum(axis=1).max()) + 8
+    c = dt.cols
+    ev = tre.tre_load_events(c["ts"], c["model"], c["req"], c["type"], c["tokens"], dt.off, cfg, validate=True)
     prof = device.profiles(w)
+    if act_seed is not None:
+        veto = rng.integers(0, 1 << 62, (w.n_traces, ev.n_ticks), dtype=np.int64).astype(np.uint64)
+        veto &= np.uint64((1 << M) - 1)
+        veto[rng.random(veto.shape) > 0.1] = 0
+        g_t = torch.from_numpy(g).cuda()
+        v_t = torch.from_numpy(veto.view(np.int64)).cuda()
+        act = tre.actuation(1310, 1870, g_t, v_t)
+        tre.tre_check_actuation(ev, prof, act)
+    sweep = (lambda **kw: tre.tre_sweep(ev, prof, sc, out, ws, **kw)) if act is None else \
+        (lambda **kw: tre.tre_sweep_act(ev, prof, sc, act, out, ws, **kw))
     sc_cols = w.scenario_columns()
     n_sc = len(sc_cols["trace"])
     sc = device.scenarios(sc_cols)
@@ -49,7 +71,7 @@ def _run_full(workload_index, sample_traces, tss_traces):
     say(f"{w.name}: {dt.n_events} events, {n_sc} scenarios; three sweeps")
     runs = []
     for _ in range(3):
-        tre.tre_sweep(ev, prof, sc, out, ws)
+        sweep()
         torch.cuda.synchronize()
         runs.append(_outputs(out))
     for r in runs[1:]:
@@ -57,13 +79,12 @@ def _run_full(workload_index, sample_traces, tss_traces):
             assert np.array_equal(runs[0][k], r[k]), f"{w.name}: sweep output {k} differs between launches"
     # the same launch with the per-cell fp32 TSS written
     t32 = torch.empty((ev.n_traces, ev.n_windows, ev.n_models), dtype=torch.float32, device="cuda")
-    tre.tre_sweep(ev, prof, sc, out, ws, tss32=t32)
+    sweep(tss32=t32)
     torch.cuda.synchronize()
     with_tss = _outputs(out)
     for k in runs[0]:
         assert np.array_equal(runs[0][k], with_tss[k]), f"{w.name}: emitting TSS changed {k}"
 
-    M = w.n_models
     prof_all = PT.O.pack_profiles(w.profile_columns())
     by_trace = {}
     for s, t in enumerate(sc_cols["trace"]):
@@ -78,8 +99,17 @@ def _run_full(workload_index, sample_traces, tss_traces):
         if t in sample_traces:
             for s in by_trace.get(t, []):
                 row = {k: v[s] for k, v in sc_cols.items()}
-                exp = PT.oracle_control(w, PT.trace_profile(w.profile_columns(t + 1), t, M), ref["S"],
-                                        ref["flags"], row, move_cap)
+                if act is None:
+                    exp = PT.oracle_control(w, PT.trace_profile(w.profile_columns(t + 1), t, M), ref["S"],
+                                            ref["flags"], row, move_cap)
+                else:
+                    r1 = np.zeros(1, PT.O.SCENARIO_DTYPE)
+                    for k in PT.O.SCENARIO_DTYPE.names:
+                        r1[k] = row[k]
+                    win = cfg["window_ms"]
+                    exp = PT.O.get().control_act(cfg, prof_all[t * M:(t + 1) * M], ref["S"], ref["flags"], r1,
+                                                 -(-1310 // win), -(-1870 // win), footprint=g[t], veto=veto[t],
+                                                 move_cap=move_cap)
                 PT.compare_ctl(moves[s], int(runs[0]["n_moves"][s]), runs[0]["r_final"][s],
                                runs[0]["r_windows"][s], exp, f"{w.name} scenario {s}")
                 checked += 1
@@ -92,6 +122,12 @@ def test_stress_full_size():
     rng = np.random.default_rng(11)
     sample = sorted({0, 1, 2047, 4095, *rng.integers(0, 4096, 4).tolist()})
     _run_full(4, sample, [0, 4095])
+
+
+def test_stress_full_size_with_actuation():
+    rng = np.random.default_rng(13)
+    sample = sorted({0, 4095, *rng.integers(0, 4096, 3).tolist()})
+    _run_full(4, sample, [], act_seed=14)
 
 
 def test_diverse_full_size():
