@@ -17,6 +17,13 @@ kernel's mean launch time measured with HIP events on its stream.
 ``cpu_baseline`` times the CPU oracle (one trace per call, on a pool of
 host threads) on a bounded sample of the same traces and checks the GPU's
 decisions on that sample.
+
+``--actuation`` replays the same workload under the actuation model
+(``tre_sweep_act``): the paper's measured wake and sleep times (1.31 s and
+1.87 s, rounded up to whole windows), footprints of 1 or 2 GPUs per replica
+drawn from a fixed seed with the GPU budget set to the largest initial
+footprint sum plus 8, and donor-release vetoes on 10% of the ticks; the CPU
+leg then runs the oracle's actuation replay.
 """
 import argparse
 import hashlib
@@ -33,6 +40,8 @@ HBM_PEAK_GBS = 8000.0
 ALG_BYTES_PER_EVENT = 12
 CPU_EVENT_BUDGET = 3_000_000_000
 CPU_WORKERS = 16  # the host CPU share of one GPU
+ACT_WAKE_MS, ACT_SLEEP_MS = 1310, 1870  # measured reactivation and sleep times
+ACT_SEED = 2609
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "tss_stream_traffic.json")
 KERNEL_SRC = os.path.join(ROOT, "paper_2609_29160_amd", "csrc", "tre.hip")
 
@@ -70,6 +79,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle leg")
     ap.add_argument("--emit-tss", action="store_true", help="also write per-window fp32 TSS")
     ap.add_argument("--threads", type=int, default=None)
+    ap.add_argument("--actuation", action="store_true",
+                    help="wake/sleep delays, 1-2 GPU footprints and vetoes (tre_sweep_act)")
     ap.add_argument("--copy-calib-gb", type=float, default=0.0,
                     help="after the run, copy this many GB device-to-device (counter calibration)")
     args = ap.parse_args()
@@ -97,8 +108,16 @@ def main():
     t0 = time.time()
     dt = device.upload(w, threads=args.threads, log=log)
     log(f"resident: {dt.n_events} events, {dt.stored_bytes / 1e9:.1f} GB stored ({time.time() - t0:.1f} s)")
-    ev = device.load(dt, validate=True)
+    act_in = actuation_inputs(w) if args.actuation else None
+    ev = device.load(dt, validate=True, budget=None if act_in is None else act_in["budget"])
     prof = device.profiles(w)
+    act = None
+    if act_in is not None:
+        act_in["veto"] = actuation_vetoes(w, ev.n_ticks)
+        act_in["g_dev"] = torch.from_numpy(act_in["g"]).cuda()
+        act_in["veto_dev"] = torch.from_numpy(act_in["veto"].view(np.int64)).cuda()
+        act = tre.actuation(ACT_WAKE_MS, ACT_SLEEP_MS, act_in["g_dev"], act_in["veto_dev"])
+        tre.tre_check_actuation(ev, prof, act)
     sc = device.scenarios(sc_cols)
     tre.tre_check_params(ev, prof, sc)
     max_k = int(np.max(sc_cols["max_moves"]))
@@ -113,8 +132,14 @@ def main():
     log(f"{ev.n_traces} traces, {n_sc} scenarios, {ev.n_windows} windows, {ev.n_ticks} ticks, "
         f"{logical} logical events")
 
+    def sweep():
+        if act is None:
+            tre.tre_sweep(ev, prof, sc, out, ws, tss32=tss32)
+        else:
+            tre.tre_sweep_act(ev, prof, sc, act, out, ws, tss32=tss32)
+
     for _ in range(args.warmup):
-        tre.tre_sweep(ev, prof, sc, out, ws, tss32=tss32)
+        sweep()
     torch.cuda.synchronize()
     log("warmup done")
 
@@ -128,7 +153,7 @@ def main():
     wall0 = time.perf_counter()
     e0.record(stream)
     for _ in range(args.steps):
-        tre.tre_sweep(ev, prof, sc, out, ws, tss32=tss32)
+        sweep()
     e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
@@ -159,7 +184,7 @@ def main():
             n_s = min(args.cpu_sample, w.n_traces)
         else:
             n_s = max(1, int(np.searchsorted(np.cumsum(dt.counts), CPU_EVENT_BUDGET, side="right")))
-        cpu, parity = cpu_leg(w, list(range(n_s)), sc_cols, out, move_cap, tre, args.threads)
+        cpu, parity = cpu_leg(w, list(range(n_s)), sc_cols, out, move_cap, tre, args.threads, act_in)
 
     result = {
         "metric": "request-events/sec through TSS+rebalance (1 GPU); achieved HBM GB/s vs peak",
@@ -177,7 +202,10 @@ def main():
         "config": {"workload": w.name, "traces": ev.n_traces, "scenarios": n_sc, "models": ev.n_models,
                    "window_ms": w.window_ms, "duration_s": w.duration_ms // 1000,
                    "events": dt.n_events, "logical_events": logical,
-                   "stored_gb": round(dt.stored_bytes / 1e9, 2), "emit_tss": bool(args.emit_tss)},
+                   "stored_gb": round(dt.stored_bytes / 1e9, 2), "emit_tss": bool(args.emit_tss),
+                   "actuation": None if act_in is None else
+                   {"wake_ms": ACT_WAKE_MS, "sleep_ms": ACT_SLEEP_MS, "footprint_gpus": "1-2, seeded",
+                    "budget_gpus": act_in["budget"], "veto_tick_fraction": 0.1}},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "parity": parity,
@@ -196,7 +224,30 @@ def main():
     ev.close()
 
 
-def cpu_leg(w, sample, sc_cols, out, move_cap, tre, threads):
+def actuation_inputs(w):
+    """Footprints (1 or 2 GPUs per replica, [trace][model]) and the GPU
+    budget that holds every trace's initial replicas with 8 GPUs to spare."""
+    import numpy as np
+
+    rng = np.random.default_rng(ACT_SEED)
+    g = rng.integers(1, 3, (w.n_traces, w.n_models)).astype(np.int32)
+    r_init = np.asarray(w.profile_columns()["r_init"]).reshape(w.n_traces, w.n_models)
+    return {"g": g, "budget": int((g * r_init).sum(axis=1).max()) + 8}
+
+
+def actuation_vetoes(w, n_ticks):
+    """Donor-release veto masks [trace][tick]: on 10% of the ticks, a random
+    subset of the models."""
+    import numpy as np
+
+    rng = np.random.default_rng(ACT_SEED + 1)
+    full = np.uint64((1 << w.n_models) - 1) if w.n_models < 64 else np.uint64(0xFFFFFFFFFFFFFFFF)
+    veto = rng.integers(0, 1 << 63, (w.n_traces, n_ticks), dtype=np.int64).astype(np.uint64) & full
+    veto[rng.random(veto.shape) >= 0.1] = 0
+    return veto
+
+
+def cpu_leg(w, sample, sc_cols, out, move_cap, tre, threads, act_in=None):
     """Time the oracle on the sample traces and compare the GPU's decisions
     for the scenarios on those traces.  The sample's host columns are
     generated again in batches (same seeds as the device copy); the oracle
@@ -220,12 +271,23 @@ def cpu_leg(w, sample, sc_cols, out, move_cap, tre, threads):
         by_trace.setdefault(int(t), []).append(s)
     n_workers = max(1, min(CPU_WORKERS, os.cpu_count() or 1))
 
+    if act_in is not None:
+        cfg = dict(cfg, budget=act_in["budget"])
+        # delays in whole windows: rounded up, at most one past the end
+        n_w = w.duration_ms // w.window_ms
+        wake_w, sleep_w = (min(-(-ms // w.window_ms), n_w + 1) for ms in (ACT_WAKE_MS, ACT_SLEEP_MS))
+
     def one(ev, t):
         c0 = time.thread_time()
         prof = prof_all[t * M:(t + 1) * M]
         r = o.tss_trace(ev, w.window_ms, w.duration_ms, prof)
-        refs = {s: o.control(cfg, prof, r["S"], r["flags"], sc_all[s:s + 1], move_cap)
-                for s in by_trace.get(t, [])}
+        if act_in is None:
+            refs = {s: o.control(cfg, prof, r["S"], r["flags"], sc_all[s:s + 1], move_cap)
+                    for s in by_trace.get(t, [])}
+        else:
+            refs = {s: o.control_act(cfg, prof, r["S"], r["flags"], sc_all[s:s + 1], wake_w, sleep_w,
+                                     footprint=act_in["g"][t], veto=act_in["veto"][t], move_cap=move_cap)
+                    for s in by_trace.get(t, [])}
         return refs, time.thread_time() - c0
 
     wall = 0.0

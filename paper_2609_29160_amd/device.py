@@ -97,10 +97,14 @@ def upload(workload, t0: int = 0, t1: Optional[int] = None, threads: Optional[in
     return dt
 
 
-def load(dt: DeviceTraces, validate: bool = True) -> tre.Events:
+def load(dt: DeviceTraces, validate: bool = True, budget: Optional[int] = None) -> tre.Events:
+    """budget: replaces the workload's budget (GPUs under the actuation model)."""
     c = dt.cols
-    return tre.tre_load_events(c["ts"], c["model"], c["req"], c["type"], c["tokens"], dt.off,
-                               dt.workload.trace_cfg(), validate=validate)
+    cfg = dict(dt.workload.trace_cfg())
+    if budget is not None:
+        cfg["budget"] = int(budget)
+    return tre.tre_load_events(c["ts"], c["model"], c["req"], c["type"], c["tokens"], dt.off, cfg,
+                               validate=validate)
 
 
 def profiles(workload, n_traces: Optional[int] = None) -> torch.Tensor:
