@@ -21,6 +21,7 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "tre_oracle.c")
 _SRC_ACT = os.path.join(_HERE, "tre_oracle_act.c")  # control replay with the actuation model
+_SRC_CALIB = os.path.join(_HERE, "tre_oracle_calib.c")  # calibration sweep
 _LIB = os.path.join(_HERE, "libtre_oracle.so")
 
 CFLAGS = ["-O2", "-fPIC", "-shared", "-ffp-contract=off", "-fno-fast-math", "-std=c11"]
@@ -35,14 +36,22 @@ SCENARIO_DTYPE = np.dtype([("trace", "<u4"), ("max_moves", "<u4"), ("theta_scale
                            ("tau_crit_override", "<f8")])
 MOVE_DTYPE = np.dtype([("window", "<u4"), ("path", "u1"), ("receiver", "u1"), ("donor", "u1"),
                        ("pad", "u1")])
+SLO_DTYPE = np.dtype([("ttft_ms", "<f8"), ("tpot_ms", "<f8"), ("e2e_ms", "<f8"), ("attain_q", "<f8"),
+                      ("reliability", "<f8")])
+FIT_DTYPE = np.dtype([("theta", "<f8"), ("n_cand", "<u4"), ("n_healthy", "<u4"), ("n_above", "<u4"),
+                      ("healthy_above", "<u4")])
+REQ_DTYPE = np.dtype([("ttft_ms", "<i8"), ("e2e_ms", "<i8"), ("tpot_ms", "<f8"), ("model", "<i4"),
+                      ("complete", "u1"), ("has_tpot", "u1"), ("ok", "u1"), ("pad", "u1")])
 assert PROFILE_DTYPE.itemsize == 56 and SCENARIO_DTYPE.itemsize == 24 and MOVE_DTYPE.itemsize == 8
+assert SLO_DTYPE.itemsize == 40 and FIT_DTYPE.itemsize == 24 and REQ_DTYPE.itemsize == 32
 
 
 def build(force: bool = True, src: str = _SRC, out: str = _LIB) -> str:
     """Compile the oracle with gcc (building the checker is not using it).
-    The default library also holds the actuation-model replay; a library
-    built from another base source (the pin-strength tests) does not."""
-    srcs = [src] + ([_SRC_ACT] if src == _SRC else [])
+    The default library also holds the actuation-model replay and the
+    calibration sweep; a library built from another base source (the
+    pin-strength tests) does not."""
+    srcs = [src] + ([_SRC_ACT, _SRC_CALIB] if src == _SRC else [])
     stale = not os.path.exists(out) or any(os.path.getmtime(out) < os.path.getmtime(x) for x in srcs)
     if force or stale:
         tmp = f"{out}.{os.getpid()}.tmp"
@@ -71,6 +80,12 @@ class Oracle:
             L.oracle_control_act.restype = ctypes.c_int
             L.oracle_control_act.argtypes = [i64, i64, i64, i64, i32, i32, vp, vp, vp, vp, i64, i64, vp, vp,
                                              vp, u32, vp, vp, vp, vp, vp]
+        self.has_calib = hasattr(L, "oracle_calib_requests")
+        if self.has_calib:
+            L.oracle_calib_requests.restype = i64
+            L.oracle_calib_requests.argtypes = [i64, i64, i32, i64, vp, vp, vp, vp, vp, vp, u32, vp, vp, vp]
+            L.oracle_calib_fit.restype = ctypes.c_int
+            L.oracle_calib_fit.argtypes = [i64, i32, vp, vp, vp, vp, vp, vp]
         self.L = L
         self.path = path
 
@@ -163,6 +178,65 @@ class Oracle:
         n = int(n_moves[0])
         return {"moves": moves[:min(n, move_cap)].copy(), "n_moves": n, "r_final": r_final,
                 "r_windows": r_windows, "idle_final": int(idle[0]), "held_final": held}
+
+
+    # ----------------------------------------------------------- calibration
+    def calib_requests(self, ev: Dict[str, np.ndarray], window_ms: int, duration_ms: int, slo: np.ndarray,
+                       req_cap: int) -> Dict[str, np.ndarray]:
+        """Per-request latencies and per-window SLO attainment of one trace:
+        judged / ok [M][n_windows] uint32, reqs [req_cap] REQ_DTYPE, and the
+        count of events whose request id is >= req_cap."""
+        slo = np.ascontiguousarray(slo, dtype=SLO_DTYPE)
+        M = slo.shape[0]
+        nW = duration_ms // window_ms if window_ms > 0 else 0  # the C side rejects bad shapes
+        cols = [np.ascontiguousarray(ev[k], dt) for k, dt in
+                (("ts", np.int64), ("model", np.uint8), ("req", np.uint32), ("type", np.uint8),
+                 ("tokens", np.uint16))]
+        judged = np.zeros((M, nW), np.uint32)
+        ok = np.zeros((M, nW), np.uint32)
+        reqs = np.zeros(max(int(req_cap), 1), REQ_DTYPE)
+        bad = self.L.oracle_calib_requests(window_ms, duration_ms, M, cols[0].shape[0], *[c.ctypes.data for c in cols],
+                                           slo.ctypes.data, int(req_cap), judged.ctypes.data, ok.ctypes.data,
+                                           reqs.ctypes.data)
+        if bad < 0:
+            raise ValueError("oracle_calib_requests rejected the trace")
+        return {"judged": judged, "ok": ok, "reqs": reqs[:int(req_cap)], "bad_ids": int(bad)}
+
+    def calib_fit(self, S: np.ndarray, flags: np.ndarray, judged: np.ndarray, ok: np.ndarray,
+                  slo: np.ndarray) -> np.ndarray:
+        """theta fit per model of one trace: S, flags [n_windows][M]; judged,
+        ok [M][n_windows]. Returns FIT_DTYPE [M]."""
+        slo = np.ascontiguousarray(slo, dtype=SLO_DTYPE)
+        S = np.ascontiguousarray(S, np.float64)
+        flags = np.ascontiguousarray(flags, np.uint8)
+        judged = np.ascontiguousarray(judged, np.uint32)
+        ok = np.ascontiguousarray(ok, np.uint32)
+        nW, M = S.shape
+        assert flags.shape == (nW, M) and judged.shape == (M, nW) and ok.shape == (M, nW) and slo.shape == (M,)
+        fit = np.zeros(M, FIT_DTYPE)
+        rc = self.L.oracle_calib_fit(nW, M, S.ctypes.data, flags.ctypes.data, judged.ctypes.data, ok.ctypes.data,
+                                     slo.ctypes.data, fit.ctypes.data)
+        if rc:
+            raise ValueError("oracle_calib_fit rejected its arguments")
+        return fit
+
+    def calibrate(self, ev: Dict[str, np.ndarray], window_ms: int, duration_ms: int, prof: np.ndarray,
+                  slo: np.ndarray, req_cap: int) -> Dict[str, np.ndarray]:
+        """The whole calibration sweep of one trace: TSS, per-request join and
+        attainment, then the fit."""
+        r = self.tss_trace(ev, window_ms, duration_ms, prof)
+        q = self.calib_requests(ev, window_ms, duration_ms, slo, req_cap)
+        q["fit"] = self.calib_fit(r["S"], r["flags"], q["judged"], q["ok"], slo)
+        q["S"], q["flags"] = r["S"], r["flags"]
+        return q
+
+
+def pack_slo(cols: Dict[str, np.ndarray]) -> np.ndarray:
+    n = cols["ttft_ms"].shape[0]
+    a = np.zeros(n, SLO_DTYPE)
+    for k in SLO_DTYPE.names:
+        a[k] = cols[k]
+    return a
 
 
 _default: Optional[Oracle] = None
