@@ -288,9 +288,75 @@ int tre_sweep_act(const tre_events* ev, const tre_profile* prof, const tre_scena
                   uint32_t n_scenarios, const tre_actuation* act, const tre_ctl_out* out,
                   float* tss32, void* ws, size_t ws_bytes, void* stream);
 
+/* ------------------------------------------------------ calibration sweep
+ * Per-request latencies, per-window SLO attainment and the fit of each
+ * model's healthy boundary theta (Section "Smoothing, Normalization, and
+ * Calibration": theta_m is the smallest smoothed TSS that still achieves the
+ * target SLO reliability; SLOs are stated on TTFT, TPOT and E2E latency as
+ * tail percentiles):
+ *   - a request's record is joined from the events with its id (the
+ *     handle's req column, ids below req_cap): its first ARRIVE (time,
+ *     model), first DECODE and first FINISH events and the sum of its
+ *     DECODE tokens (below 2^32); ids >= req_cap are ignored and counted;
+ *   - a request is judged when all three events are in its trace (requests
+ *     cut off by the end are censored): TTFT = t(first DECODE) - t(ARRIVE),
+ *     E2E = t(FINISH) - t(ARRIVE), TPOT = (t(FINISH) - t(first DECODE)) /
+ *     (DECODE tokens after the first DECODE event) when that count is
+ *     positive; it meets the SLO when TTFT <= ttft_ms, E2E <= e2e_ms and
+ *     (no TPOT or TPOT <= tpot_ms), compared in fp64;
+ *   - it counts in the window of its arrival; a window with judged >= 1 is
+ *     healthy when ok >= attain_q * judged (fp64);
+ *   - candidates of (trace, model): windows with judged >= 1 whose TSS is
+ *     initialised and not idle. theta = the smallest candidate S such that,
+ *     over the candidates with S >= theta, healthy >= reliability * count
+ *     (fp64); +inf when none qualifies. */
+typedef struct {
+  double ttft_ms, tpot_ms, e2e_ms;  /* bounds; +inf disables one            */
+  double attain_q;                  /* window healthy when ok >= q * judged */
+  double reliability;               /* target healthy fraction above theta  */
+} tre_slo;                          /* 40 bytes */
+
+typedef struct {
+  double theta;                     /* +inf when no candidate qualifies     */
+  uint32_t n_cand, n_healthy;       /* candidate windows, healthy ones      */
+  uint32_t n_above, healthy_above;  /* candidates with S >= theta, healthy  */
+} tre_fit;                          /* 24 bytes */
+
+#define TRE_REQ_ARRIVED 1   /* an ARRIVE event was seen                  */
+#define TRE_REQ_COMPLETE 2  /* judged: ARRIVE, DECODE and FINISH present */
+#define TRE_REQ_TPOT 4      /* tpot_ms defined                           */
+#define TRE_REQ_OK 8        /* met its model's SLO                       */
+typedef struct {
+  uint32_t ttft_ms, e2e_ms;         /* valid with TRE_REQ_COMPLETE          */
+  double tpot_ms;                   /* valid with TRE_REQ_TPOT              */
+  uint8_t model;                    /* 0xFF without an ARRIVE               */
+  uint8_t flags;
+  uint8_t pad[6];
+} tre_req_latency;                  /* 24 bytes */
+
+/* Workspace bytes of tre_calibrate: 16 per request slot and trace, plus 256. */
+int tre_calib_workspace_size(const tre_events* ev, uint32_t req_cap, size_t* bytes);
+
+/* The calibration sweep over the handle's traces (device pointers):
+     slo     [n_traces][n_models] (any values; comparisons follow IEEE);
+     tss64, flags  [n_traces][n_windows][n_models] from tre_eval_tss;
+     counts  [n_traces][n_models][n_windows] (16-byte aligned) receives
+             judged << 16 | ok per window of arrival;
+     fit     [n_traces][n_models];
+     reqs    [n_traces][req_cap] per-request latencies, or NULL;
+     n_bad_ids  one uint64: events whose id is >= req_cap, or NULL.
+   The handle needs its req column; at most 16384 windows (TRE_ERANGE).
+   ws: 16-byte aligned device workspace of tre_calib_workspace_size bytes.
+   Enqueued on `stream`. */
+int tre_calibrate(const tre_events* ev, const tre_slo* slo, const double* tss64,
+                  const uint8_t* flags, uint32_t req_cap, uint32_t* counts, tre_fit* fit,
+                  tre_req_latency* reqs, uint64_t* n_bad_ids, void* ws, size_t ws_bytes,
+                  void* stream);
+
 /* Kernel timing (HIP events recorded around each launch on its stream).
    tre_set_timing(1) starts recording; tre_kernel_time waits for the
-   recorded launches of `kernel` ("tss_stream", "rebalance", "validate")
+   recorded launches of `kernel` ("tss_stream", "rebalance", "validate",
+   "calib_fill", "calib_join", "calib_judge", "calib_fit")
    and returns their total milliseconds and count, then forgets them. */
 int tre_set_timing(int enable);
 int tre_kernel_time(const char* kernel, double* total_ms, uint64_t* launches);

@@ -4,7 +4,7 @@ import subprocess
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SRC = os.path.join(HERE, "csrc", "tre.hip")
+SRCS = [os.path.join(HERE, "csrc", "tre.hip"), os.path.join(HERE, "csrc", "calib.hip")]
 LIB = os.path.join(HERE, "libtre.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
@@ -19,7 +19,8 @@ FLAGS = [
 
 def build_library(out: str = LIB, extra=()) -> str:
     tmp = f"{out}.{os.getpid()}.tmp"
-    cmd = [HIPCC, *FLAGS, *extra, "-I", os.path.join(ROOT, "include"), "-o", tmp, SRC]
+    cmd = [HIPCC, *FLAGS, *extra, "-I", os.path.join(ROOT, "include"), "-I", os.path.join(HERE, "csrc"), "-o", tmp,
+           *SRCS]
     subprocess.run(cmd, check=True, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)
     os.replace(tmp, out)
     return out

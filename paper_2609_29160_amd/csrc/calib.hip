@@ -1,0 +1,501 @@
+// calib.hip - the calibration sweep on MI355X (gfx950): per-request latencies
+// joined from the event stream by request id, per-window SLO attainment, and
+// the fit of each model's healthy boundary theta from the smoothed TSS.
+//
+// Paper: "Cross-Model Autoscaling for Shared LLM Serving" (TRE). SLOs are
+// stated on TTFT, TPOT and E2E latency as tail percentiles (background
+// section on SLOs); theta_m is the smallest smoothed TSS that still achieves
+// the target SLO reliability, derived offline across the healthy-to-degraded
+// transition (Section "Smoothing, Normalization, and Calibration"); RQ1 asks
+// that TSS follow the SLO-health ordering, reported here as the healthy
+// counts above the fitted boundary.
+//
+// Kernels (all on the caller's stream)
+//   fill_u32     sets the request table to all ones and the counts to zero.
+//   calib_join   streams (req, type, tokens); per event one or two global
+//                atomics on the request's 16-byte record: the minimum row of
+//                its ARRIVE, DECODE and FINISH events and the complemented
+//                DECODE token sum.
+//   calib_judge  one thread per request slot: latencies from the rows (ts,
+//                model and tokens gathered), the SLO test, one atomic add
+//                into the arrival window's packed (judged, ok) counter.
+//   calib_fit    one 1024-thread workgroup per (trace, model): candidate keys
+//                (S bit pattern, health bit) in registers, an LSD radix sort
+//                in LDS (8-bit digits, constant digits skipped, stable ranks
+//                from wave ballots), then one scan for the smallest
+//                qualifying threshold.
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <algorithm>
+
+#include "tre.h"
+#include "tre_internal.h"
+
+#pragma clang fp contract(off)
+
+using tre_internal::check_device;
+using tre_internal::fail;
+using tre_internal::LaunchTimer;
+
+namespace {
+
+constexpr uint32_t kNone = 0xFFFFFFFFu;
+constexpr int kJoinChunk = 8192;    // events per calib_join workgroup
+constexpr int kFitThreads = 1024;   // calib_fit workgroup
+constexpr int kFitWaves = kFitThreads / 64;
+constexpr int kFitMaxKPT = 16;      // keys per thread: windows up to 16384
+
+__device__ __forceinline__ uint64_t dbits(double x) { return (uint64_t)__double_as_longlong(x); }
+
+// ------------------------------------------------------------------- fill
+__global__ __launch_bounds__(256) void fill_u32(uint32_t* p, uint64_t n, uint32_t v) {
+  const uint64_t n4 = n / 4;
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  uint4* q = (uint4*)p;
+  const uint4 vv = make_uint4(v, v, v, v);
+  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) q[i] = vv;
+  for (uint64_t i = 4 * n4 + (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = v;
+}
+
+// ------------------------------------------------------------------- join
+struct JoinParams {
+  const uint32_t* req;
+  const uint8_t* type;
+  const uint16_t* tokens;
+  const int64_t* off;
+  uint32_t n_traces;
+  uint32_t req_cap;
+  uint32_t* tab;                // [n_traces][req_cap][4]: a, f, e, ~dsum
+  unsigned long long* n_bad;    // events whose id is >= req_cap
+};
+
+__global__ __launch_bounds__(256) void calib_join(JoinParams p) {
+  unsigned bad = 0;
+  for (uint32_t t = blockIdx.y; t < p.n_traces; t += gridDim.y) {
+    const int64_t b = p.off[t], e = p.off[t + 1];
+    const int64_t c0 = b + (int64_t)blockIdx.x * kJoinChunk;
+    if (c0 >= e) continue;
+    const int64_t c1 = c0 + kJoinChunk < e ? c0 + kJoinChunk : e;
+    uint32_t* tt = p.tab + (uint64_t)t * p.req_cap * 4;
+    for (int64_t i = c0 + threadIdx.x; i < c1; i += 256) {
+      const uint32_t r = p.req[i];
+      if (r >= p.req_cap) {
+        ++bad;
+        continue;
+      }
+      const uint32_t k = p.type[i] & 3u;
+      const uint32_t row = (uint32_t)(i - b);
+      uint32_t* rec = tt + (uint64_t)r * 4;
+      if (k == TRE_ARRIVE) {
+        atomicMin(rec, row);
+      } else if (k == TRE_DECODE) {
+        atomicMin(rec + 1, row);
+        atomicSub(rec + 3, (uint32_t)p.tokens[i]);
+      } else if (k == TRE_FINISH) {
+        atomicMin(rec + 2, row);
+      }
+    }
+  }
+  // one atomic per wave for the ids out of range
+  unsigned s = bad;
+  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+  if ((threadIdx.x & 63) == 0 && s) atomicAdd(p.n_bad, (unsigned long long)s);
+}
+
+// ------------------------------------------------------------------ judge
+struct JudgeParams {
+  const int64_t* ts;
+  const uint8_t* model;
+  const uint16_t* tokens;
+  const int64_t* off;
+  const uint32_t* tab;
+  const tre_slo* slo;           // [n_traces][M]
+  uint32_t* counts;             // [n_traces][M][n_windows]: judged << 16 | ok
+  tre_req_latency* reqs;        // [n_traces][req_cap] or NULL
+  uint32_t n_traces;
+  uint32_t req_cap;
+  int32_t M;
+  int64_t window_ms;
+  int64_t n_windows;
+};
+
+__global__ __launch_bounds__(256) void calib_judge(JudgeParams p) {
+  const uint32_t r = blockIdx.x * 256 + threadIdx.x;
+  if (r >= p.req_cap) return;
+  for (uint32_t t = blockIdx.y; t < p.n_traces; t += gridDim.y) {
+    const uint64_t slot = (uint64_t)t * p.req_cap + r;
+    const uint4 rec = ((const uint4*)p.tab)[slot];
+    const int64_t b = p.off[t];
+    tre_req_latency out;
+    out.ttft_ms = 0;
+    out.e2e_ms = 0;
+    out.tpot_ms = 0.0;
+    out.model = 0xFF;
+    out.flags = 0;
+    for (int i = 0; i < 6; ++i) out.pad[i] = 0;
+    if (rec.x != kNone) {
+      const uint32_t m = p.model[b + rec.x];
+      out.model = (uint8_t)m;
+      out.flags = TRE_REQ_ARRIVED;
+      if (rec.y != kNone && rec.z != kNone && m < (uint32_t)p.M) {
+        const int64_t ta = p.ts[b + rec.x], tf = p.ts[b + rec.y], te = p.ts[b + rec.z];
+        const uint32_t after_first = ~rec.w - (uint32_t)p.tokens[b + rec.y];
+        const tre_slo s = p.slo[(uint64_t)t * p.M + m];
+        const int64_t ttft = tf - ta, e2e = te - ta;
+        bool good = (double)ttft <= s.ttft_ms && (double)e2e <= s.e2e_ms;
+        out.flags |= TRE_REQ_COMPLETE;
+        if (after_first > 0) {
+          const double tpot = (double)(te - tf) / (double)after_first;
+          good = good && tpot <= s.tpot_ms;
+          out.tpot_ms = tpot;
+          out.flags |= TRE_REQ_TPOT;
+        }
+        if (good) out.flags |= TRE_REQ_OK;
+        out.ttft_ms = (uint32_t)ttft;
+        out.e2e_ms = (uint32_t)e2e;
+        const int64_t w = ta / p.window_ms;  // window of arrival
+        if (w >= 0 && w < p.n_windows)
+          atomicAdd(p.counts + ((uint64_t)t * p.M + m) * p.n_windows + w, (1u << 16) | (good ? 1u : 0u));
+      }
+    }
+    if (p.reqs) p.reqs[slot] = out;
+  }
+}
+
+// -------------------------------------------------------------------- fit
+struct FitParams {
+  const double* tss64;          // [n_traces][n_windows][M]
+  const uint8_t* flags;         // [n_traces][n_windows][M]
+  const uint32_t* counts;       // [n_traces][M][n_windows]
+  const tre_slo* slo;           // [n_traces][M]
+  tre_fit* fit;                 // [n_traces][M]
+  uint32_t n_traces;
+  int32_t M;
+  int64_t n_windows;
+};
+
+// exclusive prefix sum over the workgroup of one value per thread; `tot`
+// receives the total. Uses sc[kFitWaves + 1].
+__device__ __forceinline__ uint32_t block_exclusive_sum(uint32_t v, uint32_t* sc, uint32_t& tot) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  uint32_t x = v;
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) sc[wave] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t run = 0;
+    for (int w = 0; w < kFitWaves; ++w) {
+      const uint32_t c = sc[w];
+      sc[w] = run;
+      run += c;
+    }
+    sc[kFitWaves] = run;
+  }
+  __syncthreads();
+  const uint32_t r = sc[wave] + x - v;
+  tot = sc[kFitWaves];
+  __syncthreads();
+  return r;
+}
+
+__device__ __forceinline__ uint64_t block_or_and(uint64_t v, bool want_or, uint64_t* sc) {
+  uint64_t x = v;
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint64_t y = ((uint64_t)(uint32_t)__shfl_xor((int)(x >> 32), o) << 32) | (uint32_t)__shfl_xor((int)(uint32_t)x, o);
+    x = want_or ? (x | y) : (x & y);
+  }
+  if ((threadIdx.x & 63) == 0) sc[threadIdx.x >> 6] = x;
+  __syncthreads();
+  uint64_t r = sc[0];
+  for (int w = 1; w < kFitWaves; ++w) r = want_or ? (r | sc[w]) : (r & sc[w]);
+  __syncthreads();
+  return r;
+}
+
+// Element e of the sorted sequence lives in wave e / (KPT*64), slot
+// (e / 64) % KPT, lane e % 64: a wave's keys are a contiguous block and
+// within a wave slots come before lanes, so ranks that follow (wave, slot,
+// lane) order keep every pass stable.
+template <int KPT>
+__global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
+  __shared__ uint64_t keys_lds[kFitThreads * KPT];
+  __shared__ uint32_t hist[256 * kFitWaves];  // [digit][wave]
+  __shared__ uint64_t sc64[kFitWaves];
+  __shared__ uint32_t sc32[kFitWaves + 1];
+
+  // XCD-aware block order: consecutive blocks go to different XCDs, so the
+  // models of one trace are numbered to land on one XCD and share its L2
+  // for the strided per-cell reads
+  const uint32_t b = blockIdx.x;
+  const uint32_t xcd = b & 7u, k = b >> 3;
+  const uint32_t t = (k / (uint32_t)p.M) * 8u + xcd;
+  const uint32_t m = k % (uint32_t)p.M;
+  if (t >= p.n_traces) return;  // whole block
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t nW = p.n_windows;
+  const tre_slo s = p.slo[(uint64_t)t * p.M + m];
+  const uint32_t* cnt = p.counts + ((uint64_t)t * p.M + m) * nW;
+
+  // candidate keys go to LDS in element order; non-candidates are marked ~0
+  // (no key of a finite S reaches it) until the largest key is known
+  uint64_t kmax = 0, kor = 0, kand = ~0ull;
+  uint32_t n_real = 0;
+#pragma unroll 2
+  for (int j = 0; j < KPT; ++j) {
+    const int64_t w = (int64_t)wave * KPT * 64 + j * 64 + lane;
+    uint64_t kk = ~0ull;
+    if (w < nW) {
+      const uint32_t c = cnt[w];
+      const uint32_t judged = c >> 16, ok = c & 0xFFFFu;
+      const uint64_t cell = ((uint64_t)t * nW + w) * p.M + m;
+      const uint8_t fl = p.flags[cell];
+      if (judged > 0 && (fl & TRE_FLAG_INIT) && !(fl & TRE_FLAG_IDLE)) {
+        const bool healthy = (double)ok >= s.attain_q * (double)judged;
+        kk = (dbits(p.tss64[cell]) << 1) | (healthy ? 1ull : 0ull);
+        kmax = kk > kmax ? kk : kmax;
+        kor |= kk;
+        kand &= kk;
+        ++n_real;
+      }
+    }
+    keys_lds[wave * KPT * 64 + j * 64 + lane] = kk;
+  }
+  uint32_t n_cand;
+  (void)block_exclusive_sum(n_real, sc32, n_cand);
+  tre_fit out;
+  out.theta = INFINITY;
+  out.n_cand = n_cand;
+  out.n_healthy = 0;
+  out.n_above = 0;
+  out.healthy_above = 0;
+  if (n_cand == 0) {
+    if (threadIdx.x == 0) p.fit[(uint64_t)t * p.M + m] = out;
+    return;
+  }
+  // non-candidates become copies of the largest key: they sort after every
+  // candidate, and only positions below n_cand are counted
+  {
+    uint64_t x = kmax;
+    for (int o = 32; o > 0; o >>= 1) {
+      const uint64_t y = ((uint64_t)(uint32_t)__shfl_xor((int)(x >> 32), o) << 32) | (uint32_t)__shfl_xor((int)(uint32_t)x, o);
+      x = y > x ? y : x;
+    }
+    if (lane == 0) sc64[wave] = x;
+    __syncthreads();
+    kmax = sc64[0];
+    for (int w = 1; w < kFitWaves; ++w) kmax = sc64[w] > kmax ? sc64[w] : kmax;
+    __syncthreads();
+  }
+  const uint64_t vary = block_or_and(kor, true, sc64) ^ block_or_and(kand, false, sc64);
+  // each thread rewrites only its own elements
+#pragma unroll
+  for (int j = 0; j < KPT; ++j) {
+    uint64_t* q = keys_lds + wave * KPT * 64 + j * 64 + lane;
+    if (*q == ~0ull) *q = kmax;
+  }
+  __syncthreads();
+
+  const uint64_t lt_mask = (1ull << lane) - 1ull;
+  for (int pass = 0; pass < 8; ++pass) {
+    const int shift = pass * 8;
+    if (((vary >> shift) & 0xFFull) == 0) continue;  // digit equal in every key
+    for (int i = threadIdx.x; i < 256 * kFitWaves; i += kFitThreads) hist[i] = 0;
+    __syncthreads();
+    uint32_t pos[(KPT + 1) / 2];  // ranks within the wave's digit bucket, two 16-bit halves each
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) {
+      const uint32_t d = (uint32_t)(keys_lds[wave * KPT * 64 + j * 64 + lane] >> shift) & 0xFFu;
+      uint64_t peers = ~0ull;
+#pragma unroll
+      for (int bit = 0; bit < 8; ++bit) {
+        const uint64_t bl = __ballot((d >> bit) & 1u);
+        peers &= ((d >> bit) & 1u) ? bl : ~bl;
+      }
+      const uint32_t below = (uint32_t)__popcll(peers & lt_mask);
+      uint32_t* h = hist + d * kFitWaves + wave;
+      const uint32_t base = *h;
+      if (j & 1) pos[j >> 1] |= (base + below) << 16;
+      else pos[j >> 1] = base + below;
+      // the lowest lane of each digit group advances the wave's count; the
+      // loads above complete first (a wave's LDS operations stay in order)
+      __builtin_amdgcn_wave_barrier();
+      if (below == 0) *h = base + (uint32_t)__popcll(peers);
+      __builtin_amdgcn_wave_barrier();
+    }
+    __syncthreads();
+    // exclusive offsets in (digit, wave) order: 4 entries per thread
+    {
+      uint32_t* h4 = hist + threadIdx.x * 4;
+      const uint32_t a0 = h4[0], a1 = h4[1], a2 = h4[2], a3 = h4[3];
+      uint32_t tot;
+      const uint32_t base = block_exclusive_sum(a0 + a1 + a2 + a3, sc32, tot);
+      h4[0] = base;
+      h4[1] = base + a0;
+      h4[2] = base + a0 + a1;
+      h4[3] = base + a0 + a1 + a2;
+    }
+    // every key is read before any is written back
+    uint64_t key[KPT];
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) key[j] = keys_lds[wave * KPT * 64 + j * 64 + lane];
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) {
+      const uint32_t d = (uint32_t)(key[j] >> shift) & 0xFFu;
+      keys_lds[hist[d * kFitWaves + wave] + ((pos[j >> 1] >> ((j & 1) * 16)) & 0xFFFFu)] = key[j];
+    }
+    __syncthreads();
+  }
+  // keys_lds holds the keys in ascending order (also when no digit varied)
+  // healthy candidates per wave; a wave's elements are one contiguous block
+  uint32_t hsum = 0, hbits = 0;
+#pragma unroll
+  for (int j = 0; j < KPT; ++j) {
+    const uint32_t e = (uint32_t)(wave * KPT * 64 + j * 64 + lane);
+    const uint32_t hb = (e < n_cand) ? (uint32_t)(keys_lds[e] & 1ull) : 0u;
+    hbits |= hb << j;
+    hsum += hb;
+  }
+  __syncthreads();
+  for (int o = 32; o > 0; o >>= 1) hsum += __shfl_xor(hsum, o);
+  if (lane == 0) sc32[wave] = hsum;
+  __syncthreads();
+  uint32_t wbase = 0, Ht = 0;
+  for (int w = 0; w < kFitWaves; ++w) {
+    const uint32_t c = sc32[w];
+    wbase += w < wave ? c : 0u;
+    Ht += c;
+  }
+  __syncthreads();
+  // a threshold at a group of equal S covers the whole group and everything
+  // above it: evaluate at each group's first (lowest) position
+  uint32_t best = kNone, best_h = 0;
+  uint32_t run = wbase;  // healthy candidates before the current slot
+#pragma unroll
+  for (int j = 0; j < KPT; ++j) {
+    const uint32_t e = (uint32_t)(wave * KPT * 64 + j * 64 + lane);
+    const uint64_t hbal = __ballot((hbits >> j) & 1u);
+    const uint32_t before = run + (uint32_t)__popcll(hbal & lt_mask);
+    run += (uint32_t)__popcll(hbal);
+    if (e < n_cand) {
+      const bool start = e == 0 || (keys_lds[e - 1] >> 1) != (keys_lds[e] >> 1);
+      if (start) {
+        const uint32_t N = n_cand - e, H = Ht - before;
+        if ((double)H >= s.reliability * (double)N && e < best) {
+          best = e;
+          best_h = H;
+        }
+      }
+    }
+  }
+  // smallest qualifying group start (the lowest position is the smallest S)
+  uint32_t bmin = best;
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint32_t y = (uint32_t)__shfl_xor((int)bmin, o);
+    bmin = y < bmin ? y : bmin;
+  }
+  if (lane == 0) sc32[wave] = bmin;
+  __syncthreads();
+  uint32_t g = kNone;
+  for (int w = 0; w < kFitWaves; ++w) g = sc32[w] < g ? sc32[w] : g;
+  out.n_healthy = Ht;
+  if (g != kNone && best == g) {
+    // the thread that holds position g writes the result
+    out.theta = __longlong_as_double((long long)(keys_lds[g] >> 1));
+    out.n_above = n_cand - g;
+    out.healthy_above = best_h;
+    p.fit[(uint64_t)t * p.M + m] = out;
+  } else if (g == kNone && threadIdx.x == 0) {
+    p.fit[(uint64_t)t * p.M + m] = out;
+  }
+}
+
+}  // namespace
+
+// --------------------------------------------------------------- host ABI
+static uint64_t calib_table_bytes(const tre_events* ev, uint32_t req_cap) {
+  return (uint64_t)ev->n_traces * req_cap * 16ull;
+}
+
+extern "C" int tre_calib_workspace_size(const tre_events* ev, uint32_t req_cap, size_t* bytes) {
+  if (!ev || !bytes) return fail(TRE_EINVAL, "tre_calib_workspace_size: NULL argument");
+  *bytes = (size_t)(256 + calib_table_bytes(ev, req_cap));
+  return TRE_OK;
+}
+
+extern "C" int tre_calibrate(const tre_events* ev, const tre_slo* slo, const double* tss64,
+                             const uint8_t* flags, uint32_t req_cap, uint32_t* counts, tre_fit* fit,
+                             tre_req_latency* reqs, uint64_t* n_bad_ids, void* ws, size_t ws_bytes,
+                             void* stream) {
+  if (!ev || !slo || !tss64 || !flags || !counts || !fit || !ws)
+    return fail(TRE_EINVAL, "tre_calibrate: NULL argument");
+  if (!ev->req) return fail(TRE_EINVAL, "tre_calibrate: the handle has no request-id column");
+  if (req_cap == 0) return fail(TRE_EINVAL, "tre_calibrate: req_cap is 0");
+  if (ev->n_windows > (int64_t)kFitThreads * kFitMaxKPT)
+    return fail(TRE_ERANGE, "tre_calibrate: %lld windows, at most %d", (long long)ev->n_windows,
+                kFitThreads * kFitMaxKPT);
+  if (((uintptr_t)counts & 15) || ((uintptr_t)ws & 15))
+    return fail(TRE_EINVAL, "tre_calibrate: counts and workspace need 16-byte alignment");
+  size_t need = 0;
+  tre_calib_workspace_size(ev, req_cap, &need);
+  if (ws_bytes < need) return fail(TRE_ENOMEM, "tre_calibrate: workspace %zu < %zu bytes", ws_bytes, need);
+  int rc = check_device(ev);
+  if (rc) return rc;
+  hipStream_t st = (hipStream_t)stream;
+  const int M = ev->cfg.n_models;
+  const int64_t nW = ev->n_windows;
+  unsigned long long* bad = n_bad_ids ? (unsigned long long*)n_bad_ids : (unsigned long long*)ws;
+  uint32_t* tab = (uint32_t*)((char*)ws + 256);
+  const uint64_t tab_words = calib_table_bytes(ev, req_cap) / 4;
+  const uint64_t cnt_words = (uint64_t)ev->n_traces * M * nW;
+  int64_t maxlen = 0;
+  for (uint32_t i = 0; i < ev->n_traces; ++i) maxlen = std::max<int64_t>(maxlen, ev->h_off[i + 1] - ev->h_off[i]);
+  {
+    LaunchTimer lt("calib_fill", st);
+    hipLaunchKernelGGL(fill_u32, dim3(4096), dim3(256), 0, st, tab, tab_words, kNone);
+    hipLaunchKernelGGL(fill_u32, dim3(4096), dim3(256), 0, st, counts, cnt_words, 0u);
+    hipLaunchKernelGGL(fill_u32, dim3(1), dim3(256), 0, st, (uint32_t*)bad, (uint64_t)2, 0u);
+    lt.done();
+  }
+  HIP_TRY(hipGetLastError());
+  if (maxlen > 0) {
+    JoinParams jp{ev->req, ev->type, ev->tokens, ev->d_off, ev->n_traces, req_cap, tab, bad};
+    dim3 grid((unsigned)((maxlen + kJoinChunk - 1) / kJoinChunk), std::min<uint32_t>(ev->n_traces, 65535u));
+    LaunchTimer lt("calib_join", st);
+    hipLaunchKernelGGL(calib_join, grid, dim3(256), 0, st, jp);
+    lt.done();
+    HIP_TRY(hipGetLastError());
+  }
+  {
+    JudgeParams pp{ev->ts, ev->model, ev->tokens, ev->d_off, tab, slo, counts, reqs,
+                   ev->n_traces, req_cap, M, ev->cfg.window_ms, nW};
+    dim3 grid((req_cap + 255) / 256, std::min<uint32_t>(ev->n_traces, 65535u));
+    LaunchTimer lt("calib_judge", st);
+    hipLaunchKernelGGL(calib_judge, grid, dim3(256), 0, st, pp);
+    lt.done();
+    HIP_TRY(hipGetLastError());
+  }
+  {
+    FitParams fp{tss64, flags, counts, slo, fit, ev->n_traces, M, nW};
+    const uint32_t blocks = ((ev->n_traces + 7) / 8) * 8 * (uint32_t)M;
+    const int kpt = nW <= 1024 ? 1 : nW <= 2048 ? 2 : nW <= 4096 ? 4 : nW <= 8192 ? 8 : 16;
+    LaunchTimer lt("calib_fit", st);
+    switch (kpt) {
+      case 1: hipLaunchKernelGGL(calib_fit<1>, dim3(blocks), dim3(kFitThreads), 0, st, fp); break;
+      case 2: hipLaunchKernelGGL(calib_fit<2>, dim3(blocks), dim3(kFitThreads), 0, st, fp); break;
+      case 4: hipLaunchKernelGGL(calib_fit<4>, dim3(blocks), dim3(kFitThreads), 0, st, fp); break;
+      case 8: hipLaunchKernelGGL(calib_fit<8>, dim3(blocks), dim3(kFitThreads), 0, st, fp); break;
+      default: hipLaunchKernelGGL(calib_fit<16>, dim3(blocks), dim3(kFitThreads), 0, st, fp); break;
+    }
+    lt.done();
+    HIP_TRY(hipGetLastError());
+  }
+  return TRE_OK;
+}

@@ -36,13 +36,18 @@
 #include <vector>
 
 #include "tre.h"
+#include "tre_internal.h"
 
 #pragma clang fp contract(off)
+
+using tre_internal::check_device;
+using tre_internal::fail;
+using tre_internal::LaunchTimer;
 
 // ------------------------------------------------------------------ errors
 static thread_local std::string g_err;
 
-static int fail(int code, const char* fmt, ...) {
+int tre_internal::fail(int code, const char* fmt, ...) {
   char buf[512];
   va_list ap;
   va_start(ap, fmt);
@@ -52,34 +57,9 @@ static int fail(int code, const char* fmt, ...) {
   return code;
 }
 
-#define HIP_TRY(expr)                                                              \
-  do {                                                                             \
-    hipError_t e_ = (expr);                                                        \
-    if (e_ != hipSuccess) return fail(TRE_EHIP, "%s: %s", #expr, hipGetErrorString(e_)); \
-  } while (0)
-
 extern "C" const char* tre_last_error(void) { return g_err.c_str(); }
 
 // ------------------------------------------------------------------ handle
-struct tre_events {
-  const int64_t* ts;
-  const uint8_t* model;
-  const uint32_t* req;
-  const uint8_t* type;
-  const uint16_t* tokens;
-  uint32_t n_traces;
-  tre_trace_cfg cfg;
-  int64_t n_windows;
-  int64_t n_ticks;
-  int64_t n_events;
-  int64_t n_rows;  // rows [0, n_rows) of every column are readable
-  int64_t* d_off;
-  uint32_t* d_tick_window;
-  uint8_t* d_tick_kind;
-  std::vector<int64_t> h_off;
-  uint32_t wcap;
-  int device;
-};
 
 // ------------------------------------------------------------ constants
 constexpr int kStreamWaves = 4;            // tss_stream workgroup (waves)
@@ -944,30 +924,28 @@ std::mutex g_tmu;
 bool g_timing = false;
 std::vector<Pending> g_pending;
 
-struct LaunchTimer {
-  Pending pe{};
-  bool on = false;
-  hipStream_t st;
-  LaunchTimer(const char* name, hipStream_t s) : st(s) {
-    std::lock_guard<std::mutex> lk(g_tmu);
-    if (!g_timing) return;
-    pe.name = name;
-    if (hipEventCreate(&pe.start) != hipSuccess) return;
-    if (hipEventCreate(&pe.stop) != hipSuccess) {
-      (void)hipEventDestroy(pe.start);
-      return;
-    }
-    on = hipEventRecord(pe.start, st) == hipSuccess;
-  }
-  void done() {
-    if (!on) return;
-    (void)hipEventRecord(pe.stop, st);
-    std::lock_guard<std::mutex> lk(g_tmu);
-    g_pending.push_back(pe);
-    on = false;
-  }
-};
 }  // namespace
+
+tre_internal::LaunchTimer::LaunchTimer(const char* name, hipStream_t s) : st_(s) {
+  std::lock_guard<std::mutex> lk(g_tmu);
+  if (!g_timing) return;
+  name_ = name;
+  if (hipEventCreate(&start_) != hipSuccess) return;
+  if (hipEventCreate(&stop_) != hipSuccess) {
+    (void)hipEventDestroy(start_);
+    return;
+  }
+  on_ = hipEventRecord(start_, st_) == hipSuccess;
+}
+
+void tre_internal::LaunchTimer::done() {
+  if (!on_) return;
+  (void)hipEventRecord(stop_, st_);
+  std::lock_guard<std::mutex> lk(g_tmu);
+  g_pending.push_back(Pending{name_, start_, stop_});
+  on_ = false;
+}
+
 
 extern "C" int tre_set_timing(int enable) {
   std::lock_guard<std::mutex> lk(g_tmu);
@@ -1001,7 +979,7 @@ extern "C" int tre_kernel_time(const char* kernel, double* total_ms, uint64_t* l
 }
 
 // --------------------------------------------------------------- host ABI
-static int check_device(const tre_events* ev) {
+int tre_internal::check_device(const tre_events* ev) {
   int dev = -1;
   HIP_TRY(hipGetDevice(&dev));
   if (dev != ev->device)

@@ -31,6 +31,13 @@ SCENARIO_DTYPE = np.dtype([("trace", "<u4"), ("max_moves", "<u4"), ("theta_scale
                            ("tau_crit_override", "<f8")])
 MOVE_DTYPE = np.dtype([("window", "<u4"), ("path", "u1"), ("receiver", "u1"), ("donor", "u1"),
                        ("pad", "u1")])
+SLO_DTYPE = np.dtype([("ttft_ms", "<f8"), ("tpot_ms", "<f8"), ("e2e_ms", "<f8"), ("attain_q", "<f8"),
+                      ("reliability", "<f8")])
+FIT_DTYPE = np.dtype([("theta", "<f8"), ("n_cand", "<u4"), ("n_healthy", "<u4"), ("n_above", "<u4"),
+                      ("healthy_above", "<u4")])
+REQ_LATENCY_DTYPE = np.dtype([("ttft_ms", "<u4"), ("e2e_ms", "<u4"), ("tpot_ms", "<f8"), ("model", "u1"),
+                              ("flags", "u1"), ("pad", "u1", (6,))])
+TRE_REQ_ARRIVED, TRE_REQ_COMPLETE, TRE_REQ_TPOT, TRE_REQ_OK = 1, 2, 4, 8
 
 
 class TreError(RuntimeError):
@@ -69,7 +76,8 @@ class _Actuation(ctypes.Structure):
 
 EXPORTS = ["tre_last_error", "tre_load_events", "tre_free_events", "tre_events_info",
            "tre_check_params", "tre_workspace_size", "tre_eval_tss", "tre_rebalance", "tre_sweep",
-           "tre_set_timing", "tre_kernel_time", "tre_check_actuation", "tre_rebalance_act", "tre_sweep_act"]
+           "tre_set_timing", "tre_kernel_time", "tre_check_actuation", "tre_rebalance_act", "tre_sweep_act",
+           "tre_calib_workspace_size", "tre_calibrate"]
 
 
 def _load():
@@ -102,6 +110,10 @@ def _load():
     L.tre_rebalance_act.argtypes = [vp, vp, vp, vp, vp, u32, ctypes.POINTER(_Actuation), ctypes.POINTER(_CtlOut), vp]
     L.tre_sweep_act.restype = i32
     L.tre_sweep_act.argtypes = [vp, vp, vp, u32, ctypes.POINTER(_Actuation), ctypes.POINTER(_CtlOut), vp, vp, sz, vp]
+    L.tre_calib_workspace_size.restype = i32
+    L.tre_calib_workspace_size.argtypes = [vp, u32, ctypes.POINTER(sz)]
+    L.tre_calibrate.restype = i32
+    L.tre_calibrate.argtypes = [vp, vp, vp, vp, u32, vp, vp, vp, vp, vp, sz, vp]
     L.tre_set_timing.restype = i32
     L.tre_set_timing.argtypes = [i32]
     L.tre_kernel_time.restype = i32
@@ -277,6 +289,43 @@ def tre_sweep_act(ev: Events, prof: torch.Tensor, sc: torch.Tensor, act: _Actuat
     o = _ctl(out)
     _check(_L.tre_sweep_act(ev.handle, _ptr(prof), _ptr(sc), n_sc, ctypes.byref(act), ctypes.byref(o), _ptr(tss32),
                             _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def tre_calib_workspace_size(ev: Events, req_cap: int) -> int:
+    n = ctypes.c_size_t()
+    _check(_L.tre_calib_workspace_size(ev.handle, int(req_cap), ctypes.byref(n)))
+    return n.value
+
+
+def calib_outputs(ev: Events, req_cap: int, with_reqs: bool = False, device="cuda") -> Dict[str, torch.Tensor]:
+    """Output tensors of tre_calibrate: counts [n_traces][n_models][n_windows]
+    (int32 holding judged << 16 | ok), fit and optional per-request records
+    as byte tensors (unpack with unpack_fit / unpack_reqs), the id counter and
+    the workspace."""
+    out = {"counts": torch.empty((ev.n_traces, ev.n_models, ev.n_windows), dtype=torch.int32, device=device),
+           "fit": torch.empty(ev.n_traces * ev.n_models * FIT_DTYPE.itemsize, dtype=torch.uint8, device=device),
+           "n_bad": torch.empty(1, dtype=torch.int64, device=device),
+           "ws": torch.empty(tre_calib_workspace_size(ev, req_cap), dtype=torch.uint8, device=device),
+           "req_cap": int(req_cap)}
+    out["reqs"] = (torch.empty(ev.n_traces * int(req_cap) * REQ_LATENCY_DTYPE.itemsize, dtype=torch.uint8,
+                               device=device) if with_reqs else None)
+    return out
+
+
+def tre_calibrate(ev: Events, slo: torch.Tensor, tss64: torch.Tensor, flags: torch.Tensor,
+                  out: Dict[str, torch.Tensor], stream=None):
+    ws = out["ws"]
+    _check(_L.tre_calibrate(ev.handle, _ptr(slo), _ptr(tss64), _ptr(flags), int(out["req_cap"]), _ptr(out["counts"]),
+                            _ptr(out["fit"]), _ptr(out.get("reqs")), _ptr(out.get("n_bad")), _ptr(ws),
+                            ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def unpack_fit(fit: torch.Tensor) -> np.ndarray:
+    return fit.cpu().numpy().view(FIT_DTYPE)
+
+
+def unpack_reqs(reqs: torch.Tensor) -> np.ndarray:
+    return reqs.cpu().numpy().view(REQ_LATENCY_DTYPE)
 
 
 def tre_set_timing(enable: bool):

@@ -46,6 +46,8 @@ def test_struct_layouts():
     assert ctypes.sizeof(tre._CtlOut) == 40
     assert ctypes.sizeof(tre._TssOut) == 56
     assert ctypes.sizeof(tre._Actuation) == 32
+    assert tre.SLO_DTYPE.itemsize == 40 and tre.FIT_DTYPE.itemsize == 24
+    assert tre.REQ_LATENCY_DTYPE.itemsize == 24
 
 
 def test_error_message_without_gpu_call():

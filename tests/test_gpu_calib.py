@@ -1,0 +1,246 @@
+"""GPU parity of the calibration sweep (tre_calibrate) against the oracle.
+
+For each trace the per-request records (judged or not, model, TTFT, E2E,
+TPOT bit for bit, SLO met), the per-window (judged, ok) counts, the count of
+out-of-range request ids and the per-model fit (theta bit for bit and the
+four counts) must equal the oracle's. The oracle's fit runs on the GPU's
+smoothed TSS and flags (those are compared with the oracle's own TSS by the
+TSS parity tests), with its own per-window counts.
+
+Inputs: the tiny, bursty, diverse and stress workloads (short and whole
+traces, so every key-per-thread variant of the fit runs), hand-built traces
+with censored requests, id gaps and ids past req_cap, constant-load traces
+whose TSS repeats (long runs of equal keys), and argument errors.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle as O
+import tracegen as tg
+import calib_pins as CP
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2609_29160_amd import device, tre
+    return tre, device, torch
+
+
+def _columns(torch, traces):
+    counts = [len(t["ts"]) for t in traces]
+    off = np.zeros(len(traces) + 1, np.int64)
+    off[1:] = np.cumsum(counts)
+    n = int(off[-1]) + 16
+    cols = {}
+    for k, dt in (("ts", np.int64), ("model", np.uint8), ("req", np.uint32), ("type", np.uint8),
+                  ("tokens", np.uint16)):
+        a = np.zeros(n, dt)
+        for i, t in enumerate(traces):
+            a[off[i]:off[i + 1]] = t[k]
+        cols[k] = torch.from_numpy(a).cuda()
+    return cols, off
+
+
+def _slo_rows(slo_cols, t, M):
+    a = np.zeros(M, O.SLO_DTYPE)
+    for k in O.SLO_DTYPE.names:
+        a[k] = slo_cols[k][t * M:(t + 1) * M]
+    return a
+
+
+def _check(lib, name, cfg, traces, prof_cols, slo_cols, req_cap, check_traces=None):
+    tre, device, torch = lib
+    M = cfg["n_models"]
+    cols, off = _columns(torch, traces)
+    ev = tre.tre_load_events(cols["ts"], cols["model"], cols["req"], cols["type"], cols["tokens"], off, cfg)
+    prof = tre.pack(prof_cols, tre.PROFILE_DTYPE)
+    slo = tre.pack(slo_cols, tre.SLO_DTYPE)
+    tss = tre.tss_outputs(ev, which=("tss64", "flags"))
+    tre.tre_eval_tss(ev, prof, tss)
+    out = tre.calib_outputs(ev, req_cap, with_reqs=True)
+    tre.tre_calibrate(ev, slo, tss["tss64"], tss["flags"], out)
+    torch.cuda.synchronize()
+    S = tss["tss64"].cpu().numpy()
+    fl = tss["flags"].cpu().numpy()
+    counts = out["counts"].cpu().numpy().view(np.uint32)
+    fit = tre.unpack_fit(out["fit"]).reshape(len(traces), M)
+    reqs = tre.unpack_reqs(out["reqs"]).reshape(len(traces), req_cap)
+    o = O.get()
+    bad_total = 0
+    for t in (range(len(traces)) if check_traces is None else check_traces):
+        slo_t = _slo_rows(slo_cols, t, M)
+        r = o.calib_requests(traces[t], cfg["window_ms"], cfg["duration_ms"], slo_t, req_cap)
+        bad_total += r["bad_ids"]
+        what = f"{name} trace {t}"
+        g, q = reqs[t], r["reqs"]
+        arrived = q["model"] >= 0
+        assert np.array_equal((g["flags"] & tre.TRE_REQ_ARRIVED) != 0, arrived), what
+        assert np.array_equal(g["model"][arrived], q["model"][arrived].astype(np.uint8)), what
+        done = q["complete"] == 1
+        assert np.array_equal((g["flags"] & tre.TRE_REQ_COMPLETE) != 0, done), f"{what}: judged requests"
+        assert np.array_equal(g["ttft_ms"][done].astype(np.int64), q["ttft_ms"][done]), f"{what}: TTFT"
+        assert np.array_equal(g["e2e_ms"][done].astype(np.int64), q["e2e_ms"][done]), f"{what}: E2E"
+        has = q["has_tpot"] == 1
+        assert np.array_equal((g["flags"] & tre.TRE_REQ_TPOT) != 0, has), f"{what}: TPOT defined"
+        assert np.array_equal(g["tpot_ms"][has].view(np.uint64), q["tpot_ms"][has].view(np.uint64)), f"{what}: TPOT"
+        assert np.array_equal((g["flags"] & tre.TRE_REQ_OK) != 0, q["ok"] == 1), f"{what}: SLO met"
+        assert np.array_equal(counts[t] >> 16, r["judged"]), f"{what}: judged per window"
+        assert np.array_equal(counts[t] & 0xFFFF, r["ok"]), f"{what}: ok per window"
+        ref = o.calib_fit(S[t], fl[t], r["judged"], r["ok"], slo_t)
+        for k in ("n_cand", "n_healthy", "n_above", "healthy_above"):
+            assert np.array_equal(fit[t][k], ref[k]), f"{what}: fit {k} {fit[t][k]} vs {ref[k]}"
+        assert np.array_equal(fit[t]["theta"].view(np.uint64), ref["theta"].view(np.uint64)), \
+            f"{what}: theta {fit[t]['theta']} vs {ref['theta']}"
+    if check_traces is None:
+        assert int(out["n_bad"].cpu().numpy()[0]) == bad_total, f"{name}: ids past req_cap"
+    ev.close()
+    return fit
+
+
+def _req_cap(traces):
+    return max(int(t["req"].max()) + 1 if len(t["req"]) else 1 for t in traces)
+
+
+def test_tiny(lib):
+    w = tg.standard(0)
+    traces = [w.generate(0, 1).trace(0)]
+    _check(lib, "tiny", w.trace_cfg(), traces, w.profile_columns(1), w.slo_columns(1), _req_cap(traces))
+
+
+def test_bursty_with_several_reliability_targets(lib):
+    w = tg.standard(1)
+    traces = [w.generate(0, 1).trace(0)]
+    slo = w.slo_columns(1)
+    for rho, q in ((0.98, 0.95), (0.5, 0.9), (0.0, 1.0), (1.0, 0.0)):
+        s = dict(slo)
+        s["reliability"] = np.full_like(slo["reliability"], rho)
+        s["attain_q"] = np.full_like(slo["attain_q"], q)
+        say(f"bursty rho {rho} q {q}")
+        _check(lib, f"bursty-{rho}-{q}", w.trace_cfg(), traces, w.profile_columns(1), s, _req_cap(traces))
+
+
+def test_diverse_short(lib):
+    w = tg.standard(3).scaled(n_traces=6, duration_ms=3_600_000)
+    h = w.generate(0, 6)
+    traces = [h.trace(i) for i in range(6)]
+    _check(lib, "diverse-short", w.trace_cfg(), traces, w.profile_columns(6), w.slo_columns(6), _req_cap(traces))
+
+
+def test_stress_whole_traces(lib):
+    """14400 windows: the widest fit variant (16 keys per thread)."""
+    w = tg.standard(4).scaled(n_traces=5, n_scenarios=5)
+    h = w.generate(0, 5)
+    traces = [h.trace(i) for i in range(5)]
+    _check(lib, "stress-5tr", w.trace_cfg(), traces, w.profile_columns(5), w.slo_columns(5), _req_cap(traces))
+
+
+def test_req_cap_below_and_above_the_ids(lib):
+    w = tg.standard(1).scaled(duration_ms=600_000)
+    traces = [w.generate(0, 1).trace(0)]
+    cap = _req_cap(traces)
+    for rc in (cap // 3, cap, 2 * cap + 5):
+        say(f"req_cap {rc} (ids up to {cap - 1})")
+        _check(lib, f"cap-{rc}", w.trace_cfg(), traces, w.profile_columns(1), w.slo_columns(1), rc)
+
+
+def test_hand_trace_and_empty_traces(lib):
+    cfg = {"window_ms": 100, "duration_ms": 1000, "fast_period_ms": 100, "slow_period_ms": 200,
+           "n_models": 2, "budget": 4}
+    hand = CP._trace(CP.HAND)
+    empty = {k: v[:0] for k, v in hand.items()}
+    traces = [empty, hand, empty, hand]
+    prof = {"w_p": np.full(8, 0.2), "w_q": np.full(8, 2.0), "alpha": np.full(8, 0.5), "theta": np.full(8, 10.0),
+            "tau_crit": np.full(8, 0.5), "tau_surplus": np.full(8, 1.5), "r_min": np.ones(8, np.int32),
+            "r_init": np.full(8, 2, np.int32)}
+    slo_rows = np.array(CP.HAND_SLO * 4, dtype=object)
+    slo = {k: np.array([r[i] for r in slo_rows], np.float64)
+           for i, k in enumerate(("ttft_ms", "tpot_ms", "e2e_ms", "attain_q", "reliability"))}
+    _check(lib, "hand", cfg, traces, prof, slo, 8)
+
+
+def test_constant_load_runs_of_equal_keys(lib):
+    """Steady traces give long runs of equal smoothed TSS (ties across many
+    windows) and windows where every digit of the keys agrees."""
+    M = 3
+    cfg = {"window_ms": 1000, "duration_ms": 1000 * 5000, "fast_period_ms": 5000, "slow_period_ms": 10000,
+           "n_models": M, "budget": 9}
+    rows = []
+    rid = 0
+    for m in range(M):
+        for i in range(4999):
+            t0 = i * 1000 + 100 * m
+            rows += [(t0, m, rid, CP.A, 10), (t0, m, rid, CP.P | CP.ADMIT, 10), (t0 + 50 + 10 * m, m, rid, CP.D, 5),
+                     (t0 + 900, m, rid, CP.D, 5), (t0 + 900, m, rid, CP.F, 0)]
+            rid += 1
+    steady = CP._trace(rows)
+    prof = {"w_p": np.full(M, 0.2), "w_q": np.full(M, 2.0), "alpha": np.full(M, 1.0), "theta": np.full(M, 10.0),
+            "tau_crit": np.full(M, 0.5), "tau_surplus": np.full(M, 1.5), "r_min": np.ones(M, np.int32),
+            "r_init": np.full(M, 3, np.int32)}
+    slo = {"ttft_ms": np.array([60.0, 60.0, 60.0]), "tpot_ms": np.array([200.0, 100.0, 1000.0]),
+           "e2e_ms": np.full(M, 1000.0), "attain_q": np.full(M, 0.95), "reliability": np.array([0.9, 0.0, 1.0])}
+    fit = _check(lib, "steady", cfg, [steady], prof, slo, rid)
+    say("steady fit", fit)
+
+
+def test_model_counts(lib):
+    for M in (1, 17, 64):
+        w = tg.Workload(name=f"m{M}", n_traces=2, model_classes=[["7B", "13B", "34B", "70B"][m % 4] for m in range(M)],
+                        interactive=[m % 2 == 0 for m in range(M)], r_init=[2] * M, budget=2 * M,
+                        window_ms=500, duration_ms=900_000, process="mmpp2", rate=[0.5] * M,
+                        proc_params={"mmpp_mult": 6.0, "mmpp_dwell_s": 60.0}, seed=40 + M)
+        h = w.generate(0, 2)
+        traces = [h.trace(i) for i in range(2)]
+        say(f"M {M}: {sum(len(t['ts']) for t in traces)} events")
+        _check(lib, f"M{M}", w.trace_cfg(), traces, w.profile_columns(2), w.slo_columns(2), _req_cap(traces))
+
+
+def test_argument_errors(lib):
+    tre, device, torch = lib
+    w = tg.standard(0)
+    traces = [w.generate(0, 1).trace(0)]
+    cols, off = _columns(torch, traces)
+    cfg = w.trace_cfg()
+    prof = tre.pack(w.profile_columns(1), tre.PROFILE_DTYPE)
+    slo = tre.pack(w.slo_columns(1), tre.SLO_DTYPE)
+    ev = tre.tre_load_events(cols["ts"], cols["model"], cols["req"], cols["type"], cols["tokens"], off, cfg)
+    tss = tre.tss_outputs(ev, which=("tss64", "flags"))
+    tre.tre_eval_tss(ev, prof, tss)
+    out = tre.calib_outputs(ev, 100)
+    bad = dict(out)
+    bad["req_cap"] = 0
+    with pytest.raises(tre.TreError) as e:
+        tre.tre_calibrate(ev, slo, tss["tss64"], tss["flags"], bad)
+    assert e.value.code == tre.TRE_EINVAL
+    small = dict(out)
+    small["ws"] = out["ws"][:64]
+    with pytest.raises(tre.TreError) as e:
+        tre.tre_calibrate(ev, slo, tss["tss64"], tss["flags"], small)
+    assert e.value.code == tre.TRE_ENOMEM
+    ev_noreq = tre.tre_load_events(cols["ts"], cols["model"], None, cols["type"], cols["tokens"], off, cfg)
+    with pytest.raises(tre.TreError) as e:
+        tre.tre_calibrate(ev_noreq, slo, tss["tss64"], tss["flags"], out)
+    assert e.value.code == tre.TRE_EINVAL
+    ev_noreq.close()
+    # more windows than the fit holds
+    long_cfg = dict(cfg, window_ms=10, duration_ms=10 * 20000, fast_period_ms=10, slow_period_ms=20)
+    t2 = {k: v[:0] for k, v in traces[0].items()}
+    cols2, off2 = _columns(torch, [t2])
+    ev2 = tre.tre_load_events(cols2["ts"], cols2["model"], cols2["req"], cols2["type"], cols2["tokens"], off2, long_cfg)
+    tss2 = tre.tss_outputs(ev2, which=("tss64", "flags"))
+    out2 = tre.calib_outputs(ev2, 4)
+    with pytest.raises(tre.TreError) as e:
+        tre.tre_calibrate(ev2, slo, tss2["tss64"], tss2["flags"], out2)
+    assert e.value.code == tre.TRE_ERANGE
+    ev2.close()
+    ev.close()
