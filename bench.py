@@ -81,6 +81,8 @@ def main():
     ap.add_argument("--threads", type=int, default=None)
     ap.add_argument("--actuation", action="store_true",
                     help="wake/sleep delays, 1-2 GPU footprints and vetoes (tre_sweep_act)")
+    ap.add_argument("--calibrate", action="store_true",
+                    help="time the calibration sweep (tre_eval_tss + tre_calibrate) instead")
     ap.add_argument("--copy-calib-gb", type=float, default=0.0,
                     help="after the run, copy this many GB device-to-device (counter calibration)")
     args = ap.parse_args()
@@ -108,6 +110,8 @@ def main():
     t0 = time.time()
     dt = device.upload(w, threads=args.threads, log=log)
     log(f"resident: {dt.n_events} events, {dt.stored_bytes / 1e9:.1f} GB stored ({time.time() - t0:.1f} s)")
+    if args.calibrate:
+        return calibrate_main(args, w, dt, device, tre, torch, np)
     act_in = actuation_inputs(w) if args.actuation else None
     ev = device.load(dt, validate=True, budget=None if act_in is None else act_in["budget"])
     prof = device.profiles(w)
@@ -222,6 +226,146 @@ def main():
         torch.cuda.synchronize()
         log(f"copy calibration: 3 x {4 * n} bytes read + written")
     ev.close()
+
+
+CALIB_KERNELS = ("tss_stream", "calib_fill", "calib_join", "calib_judge", "calib_fit")
+
+
+def calibrate_main(args, w, dt, device, tre, torch, np):
+    """One step = tre_eval_tss writing the per-cell smoothed TSS and flags,
+    then tre_calibrate (request join, SLO attainment, theta fit) over the
+    whole resident workload. Algorithmic bytes per launch: tss_stream 12 per
+    event + 9 per cell written; calib_fill 16 per request slot + 4 per cell;
+    calib_join 7 per event (id 4, type 1, tokens 2); calib_judge 16 per
+    request slot + 35 per finished request (three timestamps, model, tokens
+    and its counter read and written: the join does this part for requests
+    whose events lie in one chunk, so the join's own figure is a lower
+    bound); calib_fit 13 per cell (counter, TSS, flags)."""
+    ev = device.load(dt, validate=True)
+    prof = device.profiles(w)
+    slo = device.slos(w)
+    T, M, nW = ev.n_traces, ev.n_models, ev.n_windows
+    cells = T * M * nW
+    tss = {"tss64": torch.empty((T, nW, M), dtype=torch.float64, device="cuda"),
+           "flags": torch.empty((T, nW, M), dtype=torch.uint8, device="cuda")}
+    out = tre.calib_outputs(ev, dt.req_cap)
+    log(f"calibration: {T} traces, {dt.n_events} events, {dt.n_arrive} requests ({dt.n_finish} finished), "
+        f"req_cap {dt.req_cap}, workspace {out['ws'].numel() / 1e9:.1f} GB")
+
+    def step():
+        tre.tre_eval_tss(ev, prof, tss)
+        tre.tre_calibrate(ev, slo, tss["tss64"], tss["flags"], out)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    tre.tre_set_timing(True)
+    for k in CALIB_KERNELS:
+        tre.tre_kernel_time(k)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    tre.tre_set_timing(False)
+    step_ms = e0.elapsed_time(e1) / args.steps
+    kms = {}
+    for k in CALIB_KERNELS:
+        tot, n = tre.tre_kernel_time(k)
+        kms[k] = tot / max(n, 1)
+    slots = T * dt.req_cap
+    alg = {"tss_stream": ALG_BYTES_PER_EVENT * dt.n_events + 9 * cells,
+           "calib_fill": 16 * slots + 4 * cells,
+           "calib_join": 7 * dt.n_events,
+           "calib_judge": 16 * slots + 35 * dt.n_finish,
+           "calib_fit": 13 * cells}
+    kernels = {k: {"ms": round(kms[k], 4), "alg_bytes": alg[k],
+                   "gbs": round(alg[k] / (kms[k] / 1e3) / 1e9, 1) if kms[k] > 0 else None} for k in CALIB_KERNELS}
+    calib_only = [k for k in CALIB_KERNELS if k != "tss_stream"]
+    dom = max(calib_only, key=lambda k: kms[k])
+    roofline = {"bound": "hbm", "achieved": kernels[dom]["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(kernels[dom]["gbs"] / HBM_PEAK_GBS, 4), "traffic": None, "kernel": dom,
+                "kernel_ms": kernels[dom]["ms"], "alg_bytes_per_launch": alg[dom]}
+    log("kernels " + ", ".join(f"{k} {kms[k]:.3f} ms" for k in CALIB_KERNELS) + f"; step {step_ms:.3f} ms")
+    cpu = parity = None
+    if not args.no_cpu:
+        n_s = max(1, int(np.searchsorted(np.cumsum(dt.counts), CPU_EVENT_BUDGET // 3, side="right")))
+        cpu, parity = calib_cpu_leg(w, list(range(n_s)), out, tss, dt.req_cap, tre, args.threads)
+    result = {
+        "metric": "request-events/sec through TSS + calibration sweep (1 GPU)",
+        "value": round(dt.n_events / (step_ms / 1e3), 1),
+        "unit": "request-events/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(step_ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f64",
+        "data": "synthetic (seeded generator; the paper's traces are not available)",
+        "config": {"workload": w.name, "traces": T, "models": M, "window_ms": w.window_ms,
+                   "duration_s": w.duration_ms // 1000, "events": dt.n_events, "requests": dt.n_arrive,
+                   "req_cap": dt.req_cap, "mode": "calibration"},
+        "roofline": roofline, "kernels": kernels, "cpu_baseline": cpu, "parity": parity,
+    }
+    print(json.dumps(result), flush=True)
+    ev.close()
+
+
+def calib_cpu_leg(w, sample, out, tss, req_cap, tre, threads):
+    """The oracle's calibration (TSS, join, attainment, fit) of the sample
+    traces on a pool of host threads, timed like the replay's CPU leg; the
+    GPU's counts and fits of those traces must equal the oracle's."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    import numpy as np
+
+    import oracle as O
+
+    o = O.get()
+    M = w.n_models
+    prof_all = O.pack_profiles(w.profile_columns(max(sample) + 1))
+    slo_all = O.pack_slo(w.slo_columns(max(sample) + 1))
+    n_workers = max(1, min(CPU_WORKERS, os.cpu_count() or 1))
+
+    def one(ev, t):
+        c0 = time.thread_time()
+        r = o.calibrate(ev, w.window_ms, w.duration_ms, prof_all[t * M:(t + 1) * M], slo_all[t * M:(t + 1) * M],
+                        req_cap)
+        return {"judged": r["judged"], "ok": r["ok"], "fit": r["fit"]}, time.thread_time() - c0
+
+    wall = cpu_s = 0.0
+    events = 0
+    refs = {}
+    batch = 4 * n_workers
+    with ThreadPoolExecutor(max_workers=n_workers) as pool:
+        for b0 in range(0, len(sample), batch):
+            tr = sample[b0:b0 + batch]
+            host = w.generate(tr[0], tr[-1] + 1, threads=threads)
+            evs = [host.trace(i) for i in range(len(tr))]
+            t0 = time.perf_counter()
+            results = list(pool.map(one, evs, tr))
+            wall += time.perf_counter() - t0
+            for ev, t, (rf, c) in zip(evs, tr, results):
+                refs[t] = rf
+                cpu_s += c
+                events += len(ev["ts"])
+            del host, evs
+    fit = tre.unpack_fit(out["fit"]).reshape(-1, M)
+    bad = 0
+    for t, rf in refs.items():
+        cnt = out["counts"][t].cpu().numpy().view(np.uint32)
+        ok = np.array_equal(cnt >> 16, rf["judged"]) and np.array_equal(cnt & 0xFFFF, rf["ok"])
+        ok = ok and np.array_equal(fit[t]["theta"].view(np.uint64), rf["fit"]["theta"].view(np.uint64))
+        for k in ("n_cand", "n_healthy", "n_above", "healthy_above"):
+            ok = ok and np.array_equal(fit[t][k], rf["fit"][k])
+        bad += 0 if ok else 1
+    cpu = {"value": round(events / wall, 1), "unit": "request-events/s", "cores": n_workers, "kind": "oracle",
+           "sample": f"{len(sample)} of {w.n_traces} traces ({events} events): {wall:.1f} s wall on {n_workers} "
+                     f"host threads (one trace per oracle call), {cpu_s:.1f} s of their CPU time",
+           "one_core_value": round(events / cpu_s, 1)}
+    parity = {"traces_checked": len(refs), "mismatches": bad, "bit_exact": bad == 0}
+    log(f"cpu oracle (calibration): {cpu['value']:.3g} events/s on {n_workers} threads; parity {parity}")
+    return cpu, parity
 
 
 def actuation_inputs(w):

@@ -12,13 +12,16 @@
 //
 // Kernels (all on the caller's stream)
 //   fill_u32     sets the request table to all ones and the counts to zero.
-//   calib_join   streams (req, type, tokens); per event one or two global
-//                atomics on the request's 16-byte record: the minimum row of
-//                its ARRIVE, DECODE and FINISH events and the complemented
-//                DECODE token sum.
-//   calib_judge  one thread per request slot: latencies from the rows (ts,
-//                model and tokens gathered), the SLO test, one atomic add
-//                into the arrival window's packed (judged, ok) counter.
+//   calib_join   one workgroup per chunk of a trace: streams (req, type,
+//                tokens), combines each request's events in an LDS hash table
+//                (minimum ARRIVE / DECODE / FINISH rows, DECODE token sum),
+//                judges the requests whose events all lie in the chunk
+//                (latencies, SLO test, one atomic add into the arrival
+//                window's packed (judged, ok) counter) and merges the others
+//                into their 16-byte global records with atomics.
+//   calib_judge  one thread per request slot: the requests that spanned
+//                chunks or never finished, judged the same way from their
+//                records (ts, model and tokens gathered at the rows).
 //   calib_fit    one 1024-thread workgroup per (trace, model): candidate keys
 //                (S bit pattern, health bit) in registers, an LSD radix sort
 //                in LDS (8-bit digits, constant digits skipped, stable ranks
@@ -63,47 +66,179 @@ __global__ __launch_bounds__(256) void fill_u32(uint32_t* p, uint64_t n, uint32_
 
 // ------------------------------------------------------------------- join
 struct JoinParams {
+  const int64_t* ts;
+  const uint8_t* model;
   const uint32_t* req;
   const uint8_t* type;
   const uint16_t* tokens;
   const int64_t* off;
-  uint32_t n_traces;
-  uint32_t req_cap;
+  const tre_slo* slo;           // [n_traces][M]
+  uint32_t* counts;             // [n_traces][M][n_windows]: judged << 16 | ok
+  tre_req_latency* reqs;        // [n_traces][req_cap] or NULL
   uint32_t* tab;                // [n_traces][req_cap][4]: a, f, e, ~dsum
   unsigned long long* n_bad;    // events whose id is >= req_cap
+  uint32_t n_traces;
+  uint32_t req_cap;
+  uint32_t n_chunks;            // chunks of the longest trace
+  int32_t M;
+  int64_t window_ms;
+  int64_t n_windows;
 };
 
+constexpr int kHashSlots = 2048;           // LDS records per chunk (load factor about 0.4)
+constexpr int kProbes = 16;                // linear probes before the global fallback
+constexpr int kJoinBatch = 8;              // events per thread loaded together
+constexpr uint32_t kDone = 0xFFFFFFFEu;    // record judged inside the join
+
+// latencies and the SLO test of one judged request from its event times
+__device__ __forceinline__ tre_req_latency judge_one(int64_t ta, int64_t tf, int64_t te, uint32_t after_first,
+                                                     uint32_t m, const tre_slo& s) {
+  tre_req_latency out;
+  out.model = (uint8_t)m;
+  out.flags = TRE_REQ_ARRIVED | TRE_REQ_COMPLETE;
+  for (int i = 0; i < 6; ++i) out.pad[i] = 0;
+  const int64_t ttft = tf - ta, e2e = te - ta;
+  bool good = (double)ttft <= s.ttft_ms && (double)e2e <= s.e2e_ms;
+  out.tpot_ms = 0.0;
+  if (after_first > 0) {
+    const double tpot = (double)(te - tf) / (double)after_first;
+    good = good && tpot <= s.tpot_ms;
+    out.tpot_ms = tpot;
+    out.flags |= TRE_REQ_TPOT;
+  }
+  if (good) out.flags |= TRE_REQ_OK;
+  out.ttft_ms = (uint32_t)ttft;
+  out.e2e_ms = (uint32_t)e2e;
+  return out;
+}
+
+__device__ __forceinline__ tre_req_latency not_judged(uint32_t m) {
+  tre_req_latency out;
+  out.ttft_ms = out.e2e_ms = 0;
+  out.tpot_ms = 0.0;
+  out.model = (uint8_t)m;
+  out.flags = TRE_REQ_ARRIVED;
+  for (int i = 0; i < 6; ++i) out.pad[i] = 0;
+  return out;
+}
+
+// One workgroup per chunk of kJoinChunk rows of one trace. The chunk's
+// events are first combined per request in an LDS hash table (minimum rows
+// of ARRIVE / DECODE / FINISH, DECODE token sum). A request whose ARRIVE,
+// DECODE and FINISH all fall in the chunk has every event in it (a
+// request's events lie between its ARRIVE and FINISH), so it is judged
+// right here and never touches the global table; the others merge into
+// their global records with atomics, for calib_judge. Chunks of one trace
+// are numbered onto one XCD.
 __global__ __launch_bounds__(256) void calib_join(JoinParams p) {
+  __shared__ uint32_t h_id[kHashSlots], h_a[kHashSlots], h_f[kHashSlots], h_e[kHashSlots], h_d[kHashSlots];
+  const uint32_t xcd = blockIdx.x & 7u, kk = blockIdx.x >> 3;
+  const uint32_t t = (kk / p.n_chunks) * 8u + xcd, chunk = kk % p.n_chunks;
+  if (t >= p.n_traces) return;  // whole block
+  const int64_t b = p.off[t], e = p.off[t + 1];
+  const int64_t c0 = b + (int64_t)chunk * kJoinChunk;
+  if (c0 >= e) return;  // whole block
+  const int64_t c1 = c0 + kJoinChunk < e ? c0 + kJoinChunk : e;
+  uint32_t* tt = p.tab + (uint64_t)t * p.req_cap * 4;
+  for (int i = threadIdx.x; i < kHashSlots; i += 256) {
+    h_id[i] = kNone;
+    h_a[i] = kNone;
+    h_f[i] = kNone;
+    h_e[i] = kNone;
+    h_d[i] = 0;
+  }
+  __syncthreads();
   unsigned bad = 0;
-  for (uint32_t t = blockIdx.y; t < p.n_traces; t += gridDim.y) {
-    const int64_t b = p.off[t], e = p.off[t + 1];
-    const int64_t c0 = b + (int64_t)blockIdx.x * kJoinChunk;
-    if (c0 >= e) continue;
-    const int64_t c1 = c0 + kJoinChunk < e ? c0 + kJoinChunk : e;
-    uint32_t* tt = p.tab + (uint64_t)t * p.req_cap * 4;
-    for (int64_t i = c0 + threadIdx.x; i < c1; i += 256) {
-      const uint32_t r = p.req[i];
+  for (int64_t i0 = c0 + threadIdx.x; i0 < c1; i0 += 256 * kJoinBatch) {
+    uint32_t rr[kJoinBatch], kt[kJoinBatch], tk[kJoinBatch];
+#pragma unroll
+    for (int u = 0; u < kJoinBatch; ++u) {
+      const int64_t i = i0 + 256 * u;
+      const bool in = i < c1;
+      rr[u] = in ? p.req[i] : kNone;
+      kt[u] = in ? p.type[i] : TRE_PREFILL;
+      tk[u] = in ? p.tokens[i] : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < kJoinBatch; ++u) {
+      const int64_t i = i0 + 256 * u;
+      if (i >= c1) continue;
+      const uint32_t r = rr[u];
       if (r >= p.req_cap) {
         ++bad;
         continue;
       }
-      const uint32_t k = p.type[i] & 3u;
+      const uint32_t k = kt[u] & 3u;
+      if (k == TRE_PREFILL) continue;
       const uint32_t row = (uint32_t)(i - b);
-      uint32_t* rec = tt + (uint64_t)r * 4;
-      if (k == TRE_ARRIVE) {
-        atomicMin(rec, row);
-      } else if (k == TRE_DECODE) {
-        atomicMin(rec + 1, row);
-        atomicSub(rec + 3, (uint32_t)p.tokens[i]);
-      } else if (k == TRE_FINISH) {
-        atomicMin(rec + 2, row);
+      uint32_t h = (r * 0x9E3779B1u) >> (32 - 11);
+      int slot = -1;
+      for (int q = 0; q < kProbes; ++q) {
+        const uint32_t old = atomicCAS(&h_id[h], kNone, r);
+        if (old == kNone || old == r) {
+          slot = (int)h;
+          break;
+        }
+        h = (h + 1) & (kHashSlots - 1);
+      }
+      if (slot >= 0) {
+        if (k == TRE_ARRIVE) {
+          atomicMin(&h_a[slot], row);
+        } else if (k == TRE_DECODE) {
+          atomicMin(&h_f[slot], row);
+          atomicAdd(&h_d[slot], tk[u]);
+        } else {
+          atomicMin(&h_e[slot], row);
+        }
+      } else {  // table crowded: straight to the global record
+        uint32_t* rec = tt + (uint64_t)r * 4;
+        if (k == TRE_ARRIVE) {
+          atomicMin(rec, row);
+        } else if (k == TRE_DECODE) {
+          atomicMin(rec + 1, row);
+          atomicSub(rec + 3, tk[u]);
+        } else {
+          atomicMin(rec + 2, row);
+        }
       }
     }
   }
+  __syncthreads();
+  for (int s = threadIdx.x; s < kHashSlots; s += 256) {
+    const uint32_t r = h_id[s];
+    if (r == kNone) continue;
+    uint32_t* rec = tt + (uint64_t)r * 4;
+    const uint32_t a = h_a[s], f = h_f[s], fin = h_e[s], d = h_d[s];
+    if (a != kNone && f != kNone && fin != kNone) {
+      const uint32_t m = p.model[b + a];
+      tre_req_latency out;
+      if (m < (uint32_t)p.M) {
+        const int64_t ta = p.ts[b + a];
+        out = judge_one(ta, p.ts[b + f], p.ts[b + fin], d - (uint32_t)p.tokens[b + f], m,
+                        p.slo[(uint64_t)t * p.M + m]);
+        const int64_t w = ta / p.window_ms;  // window of arrival
+        if (w >= 0 && w < p.n_windows)
+          atomicAdd(p.counts + ((uint64_t)t * p.M + m) * p.n_windows + w,
+                    (1u << 16) | ((out.flags & TRE_REQ_OK) ? 1u : 0u));
+      } else {
+        out = not_judged(m);
+      }
+      if (p.reqs) {
+        p.reqs[(uint64_t)t * p.req_cap + r] = out;
+        rec[0] = kDone;  // calib_judge leaves this slot alone
+      }
+      continue;
+    }
+    if (a != kNone) atomicMin(rec, a);
+    if (f != kNone) {
+      atomicMin(rec + 1, f);
+      atomicSub(rec + 3, d);
+    }
+    if (fin != kNone) atomicMin(rec + 2, fin);
+  }
   // one atomic per wave for the ids out of range
-  unsigned s = bad;
-  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
-  if ((threadIdx.x & 63) == 0 && s) atomicAdd(p.n_bad, (unsigned long long)s);
+  for (int o = 32; o > 0; o >>= 1) bad += __shfl_xor(bad, o);
+  if ((threadIdx.x & 63) == 0 && bad) atomicAdd(p.n_bad, (unsigned long long)bad);
 }
 
 // ------------------------------------------------------------------ judge
@@ -123,43 +258,28 @@ struct JudgeParams {
   int64_t n_windows;
 };
 
+// The requests the join could not finish: one thread per request slot.
 __global__ __launch_bounds__(256) void calib_judge(JudgeParams p) {
   const uint32_t r = blockIdx.x * 256 + threadIdx.x;
   if (r >= p.req_cap) return;
   for (uint32_t t = blockIdx.y; t < p.n_traces; t += gridDim.y) {
     const uint64_t slot = (uint64_t)t * p.req_cap + r;
     const uint4 rec = ((const uint4*)p.tab)[slot];
+    if (rec.x == kDone) continue;  // judged inside the join
     const int64_t b = p.off[t];
-    tre_req_latency out;
-    out.ttft_ms = 0;
-    out.e2e_ms = 0;
-    out.tpot_ms = 0.0;
-    out.model = 0xFF;
+    tre_req_latency out = not_judged(0xFF);
     out.flags = 0;
-    for (int i = 0; i < 6; ++i) out.pad[i] = 0;
     if (rec.x != kNone) {
       const uint32_t m = p.model[b + rec.x];
-      out.model = (uint8_t)m;
-      out.flags = TRE_REQ_ARRIVED;
+      out = not_judged(m);
       if (rec.y != kNone && rec.z != kNone && m < (uint32_t)p.M) {
-        const int64_t ta = p.ts[b + rec.x], tf = p.ts[b + rec.y], te = p.ts[b + rec.z];
-        const uint32_t after_first = ~rec.w - (uint32_t)p.tokens[b + rec.y];
-        const tre_slo s = p.slo[(uint64_t)t * p.M + m];
-        const int64_t ttft = tf - ta, e2e = te - ta;
-        bool good = (double)ttft <= s.ttft_ms && (double)e2e <= s.e2e_ms;
-        out.flags |= TRE_REQ_COMPLETE;
-        if (after_first > 0) {
-          const double tpot = (double)(te - tf) / (double)after_first;
-          good = good && tpot <= s.tpot_ms;
-          out.tpot_ms = tpot;
-          out.flags |= TRE_REQ_TPOT;
-        }
-        if (good) out.flags |= TRE_REQ_OK;
-        out.ttft_ms = (uint32_t)ttft;
-        out.e2e_ms = (uint32_t)e2e;
+        const int64_t ta = p.ts[b + rec.x];
+        out = judge_one(ta, p.ts[b + rec.y], p.ts[b + rec.z], ~rec.w - (uint32_t)p.tokens[b + rec.y], m,
+                        p.slo[(uint64_t)t * p.M + m]);
         const int64_t w = ta / p.window_ms;  // window of arrival
         if (w >= 0 && w < p.n_windows)
-          atomicAdd(p.counts + ((uint64_t)t * p.M + m) * p.n_windows + w, (1u << 16) | (good ? 1u : 0u));
+          atomicAdd(p.counts + ((uint64_t)t * p.M + m) * p.n_windows + w,
+                    (1u << 16) | ((out.flags & TRE_REQ_OK) ? 1u : 0u));
       }
     }
     if (p.reqs) p.reqs[slot] = out;
@@ -466,8 +586,10 @@ extern "C" int tre_calibrate(const tre_events* ev, const tre_slo* slo, const dou
   }
   HIP_TRY(hipGetLastError());
   if (maxlen > 0) {
-    JoinParams jp{ev->req, ev->type, ev->tokens, ev->d_off, ev->n_traces, req_cap, tab, bad};
-    dim3 grid((unsigned)((maxlen + kJoinChunk - 1) / kJoinChunk), std::min<uint32_t>(ev->n_traces, 65535u));
+    const uint32_t C = (uint32_t)((maxlen + kJoinChunk - 1) / kJoinChunk);
+    JoinParams jp{ev->ts, ev->model, ev->req, ev->type, ev->tokens, ev->d_off, slo, counts, reqs, tab, bad,
+                  ev->n_traces, req_cap, C, M, ev->cfg.window_ms, nW};
+    dim3 grid(8u * C * ((ev->n_traces + 7) / 8));
     LaunchTimer lt("calib_join", st);
     hipLaunchKernelGGL(calib_join, grid, dim3(256), 0, st, jp);
     lt.done();

@@ -71,6 +71,8 @@ def upload(workload, t0: int = 0, t1: Optional[int] = None, threads: Optional[in
     stage = {k: torch.empty(max(max_batch, 1), dtype=tdt, pin_memory=True) for k, _, tdt in COLUMNS}
     stage_np = {k: stage[k].numpy() for k in stage}
     host = {}
+    max_req = -1
+    n_arrive = n_finish = 0
     keep = set(int(i) for i in keep_host)
     i = 0
     n = t1 - t0
@@ -81,6 +83,11 @@ def upload(workload, t0: int = 0, t1: Optional[int] = None, threads: Optional[in
         nb = int(off[j] - off[i])
         ev = workload.generate(t0 + i, t0 + j, threads=threads, out=stage_np, out_offset=0,
                                counts=counts[i:j])
+        if nb:
+            max_req = max(max_req, int(stage_np["req"][:nb].max()))
+            kinds = np.bincount(stage_np["type"][:nb] & 3, minlength=4)
+            n_arrive += int(kinds[0])
+            n_finish += int(kinds[3])
         for k in cols:
             cols[k][int(off[i]):int(off[j])].copy_(stage[k][:nb], non_blocking=True)
         for r in range(i, j):
@@ -94,6 +101,8 @@ def upload(workload, t0: int = 0, t1: Optional[int] = None, threads: Optional[in
         i = j
     dt = DeviceTraces(workload, t0, t1, cols, off, counts)
     dt.host = host
+    dt.req_cap = max_req + 1  # request ids of every trace are below this
+    dt.n_arrive, dt.n_finish = n_arrive, n_finish
     return dt
 
 
@@ -109,6 +118,10 @@ def load(dt: DeviceTraces, validate: bool = True, budget: Optional[int] = None) 
 
 def profiles(workload, n_traces: Optional[int] = None) -> torch.Tensor:
     return tre.pack(workload.profile_columns(n_traces), tre.PROFILE_DTYPE)
+
+
+def slos(workload, n_traces: Optional[int] = None) -> torch.Tensor:
+    return tre.pack(workload.slo_columns(n_traces), tre.SLO_DTYPE)
 
 
 def scenarios(cols: Dict[str, np.ndarray]) -> torch.Tensor:

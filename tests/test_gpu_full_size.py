@@ -134,3 +134,53 @@ def test_diverse_full_size():
     rng = np.random.default_rng(12)
     sample = sorted({0, 255, *rng.integers(0, 256, 3).tolist()})
     _run_full(3, sample, [0, 255])
+
+
+def test_stress_full_size_calibration():
+    """The calibration sweep over the whole stress workload (every trace's
+    request table and fit in one launch each), twice: identical results, and
+    the counts and fits of sampled traces equal to the oracle's."""
+    import torch
+
+    from paper_2609_29160_amd import device, tre
+
+    w = tg.standard(4)
+    say(f"{w.name}: uploading")
+    dt = device.upload(w)
+    ev = device.load(dt, validate=True)
+    prof = device.profiles(w)
+    slo = device.slos(w)
+    T, M, nW = ev.n_traces, ev.n_models, ev.n_windows
+    tss = {"tss64": torch.empty((T, nW, M), dtype=torch.float64, device="cuda"),
+           "flags": torch.empty((T, nW, M), dtype=torch.uint8, device="cuda")}
+    out = tre.calib_outputs(ev, dt.req_cap)
+    say(f"{w.name}: {dt.n_events} events, req_cap {dt.req_cap}; two calibration sweeps")
+    runs = []
+    for _ in range(2):
+        tre.tre_eval_tss(ev, prof, tss)
+        tre.tre_calibrate(ev, slo, tss["tss64"], tss["flags"], out)
+        torch.cuda.synchronize()
+        runs.append((out["counts"].cpu().numpy().copy(), out["fit"].cpu().numpy().copy(),
+                     int(out["n_bad"].cpu().numpy()[0])))
+    assert np.array_equal(runs[0][0], runs[1][0]), "counts differ between launches"
+    assert np.array_equal(runs[0][1], runs[1][1]), "fits differ between launches"
+    assert runs[0][2] == 0
+    counts = runs[0][0].view(np.uint32)
+    fit = runs[0][1].view(tre.FIT_DTYPE).reshape(T, M)
+    rng = np.random.default_rng(17)
+    sample = sorted({0, T - 1, *rng.integers(0, T, 4).tolist()})
+    o = PT.O.get()
+    prof_all = PT.O.pack_profiles(w.profile_columns())
+    slo_all = PT.O.pack_slo(w.slo_columns())
+    for t in sample:
+        host = w.generate(t, t + 1).trace(0)
+        r = o.calibrate(host, w.window_ms, w.duration_ms, prof_all[t * M:(t + 1) * M], slo_all[t * M:(t + 1) * M],
+                        dt.req_cap)
+        assert np.array_equal(counts[t] >> 16, r["judged"]) and np.array_equal(counts[t] & 0xFFFF, r["ok"]), t
+        assert np.array_equal(fit[t]["theta"].view(np.uint64), r["fit"]["theta"].view(np.uint64)), t
+        for k in ("n_cand", "n_healthy", "n_above", "healthy_above"):
+            assert np.array_equal(fit[t][k], r["fit"][k]), (t, k)
+    say(f"{w.name}: calibration of {len(sample)} sampled traces matches the oracle")
+    ev.close()
+    del tss, out, dt
+    torch.cuda.empty_cache()
