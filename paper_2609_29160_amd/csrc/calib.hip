@@ -325,30 +325,73 @@ __device__ __forceinline__ uint32_t block_exclusive_sum(uint32_t v, uint32_t* sc
   return r;
 }
 
-__device__ __forceinline__ uint64_t block_or_and(uint64_t v, bool want_or, uint64_t* sc) {
-  uint64_t x = v;
-  for (int o = 32; o > 0; o >>= 1) {
-    const uint64_t y = ((uint64_t)(uint32_t)__shfl_xor((int)(x >> 32), o) << 32) | (uint32_t)__shfl_xor((int)(uint32_t)x, o);
-    x = want_or ? (x | y) : (x & y);
-  }
-  if ((threadIdx.x & 63) == 0) sc[threadIdx.x >> 6] = x;
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t x, int o) {
+  return ((uint64_t)(uint32_t)__shfl_xor((int)(x >> 32), o) << 32) | (uint32_t)__shfl_xor((int)(uint32_t)x, o);
+}
+
+// workgroup reductions of 64-bit values: 0 OR, 1 AND, 2 MIN, 3 MAX
+template <int kOp>
+__device__ __forceinline__ uint64_t block_reduce_u64(uint64_t v, uint64_t* sc) {
+  auto op = [](uint64_t a, uint64_t b) {
+    return kOp == 0 ? (a | b) : kOp == 1 ? (a & b) : kOp == 2 ? (a < b ? a : b) : (a > b ? a : b);
+  };
+  for (int o = 32; o > 0; o >>= 1) v = op(v, shfl_xor_u64(v, o));
+  if ((threadIdx.x & 63) == 0) sc[threadIdx.x >> 6] = v;
   __syncthreads();
   uint64_t r = sc[0];
-  for (int w = 1; w < kFitWaves; ++w) r = want_or ? (r | sc[w]) : (r & sc[w]);
+  for (int w = 1; w < kFitWaves; ++w) r = op(r, sc[w]);
   __syncthreads();
   return r;
 }
 
-// Element e of the sorted sequence lives in wave e / (KPT*64), slot
-// (e / 64) % KPT, lane e % 64: a wave's keys are a contiguous block and
-// within a wave slots come before lanes, so ranks that follow (wave, slot,
-// lane) order keep every pass stable.
+__device__ __forceinline__ uint32_t block_min_u32(uint32_t v, uint32_t* sc) {
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint32_t y = (uint32_t)__shfl_xor((int)v, o);
+    v = y < v ? y : v;
+  }
+  if ((threadIdx.x & 63) == 0) sc[threadIdx.x >> 6] = v;
+  __syncthreads();
+  uint32_t r = sc[0];
+  for (int w = 1; w < kFitWaves; ++w) r = sc[w] < r ? sc[w] : r;
+  __syncthreads();
+  return r;
+}
+
+constexpr int kBuckets = 2048;      // histogram of the fit (2^11)
+constexpr int kResolveCap = 1024;   // keys sorted exactly before the radix fallback
+
+// One 1024-thread workgroup per (trace, model). Candidate keys
+// (S bit pattern << 1 | healthy) go to LDS; they order like S, and equal S
+// differ only in bit 0. A threshold at a run of equal S covers the run and
+// every larger S; in ascending order the run starts at position g, with
+// N = n - g candidates and H = Ht - (healthy below g) healthy ones at or
+// above it, and qualifies when H >= rho * N (fp64). theta is the smallest
+// qualifying S, i.e. the lowest qualifying g.
+//   1. Histogram of the keys into 2048 buckets on the 11 highest bits above
+//      bit 0 where keys differ (equal S share a bucket); an exclusive scan
+//      gives each bucket's first position G_b and healthy count below P_b,
+//      so each bucket's first position is tested exactly.
+//   2. A position inside bucket b (c keys, u of them unhealthy) can only
+//      qualify if the test can move from failing to passing within the
+//      bucket: at most rho * u is gained, so for 0 <= rho <= 1 the bucket is
+//      skipped when rho * (N - u) >= H + 1 (the margin of one absorbs the
+//      rounding of the products); otherwise H < rho * (N - c + 1) is used.
+//   3. Let b* be the lowest bucket whose first position qualifies. The keys
+//      of the remaining buckets below b* are gathered, sorted (bitonic in
+//      LDS) and tested at each run start; the lowest qualifying one, else
+//      b*'s first position, is the answer.
+//   4. If those keys exceed kResolveCap, every key is sorted instead (LSD
+//      radix, 8-bit digits, constant digits skipped, stable ranks from wave
+//      ballots) and every run start tested.
 template <int KPT>
 __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
   __shared__ uint64_t keys_lds[kFitThreads * KPT];
-  __shared__ uint32_t hist[256 * kFitWaves];  // [digit][wave]
+  __shared__ uint32_t hist[2 * kBuckets];  // buckets: counts then (G, P), compact offsets; radix: [digit][wave]
+  __shared__ uint64_t cmp[kResolveCap];
   __shared__ uint64_t sc64[kFitWaves];
   __shared__ uint32_t sc32[kFitWaves + 1];
+  __shared__ uint32_t n_gathered;
+  static_assert(256 * kFitWaves == 2 * kBuckets, "radix histogram and bucket tables share LDS");
 
   // XCD-aware block order: consecutive blocks go to different XCDs, so the
   // models of one trace are numbered to land on one XCD and share its L2
@@ -359,14 +402,17 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
   const uint32_t m = k % (uint32_t)p.M;
   if (t >= p.n_traces) return;  // whole block
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int tid = threadIdx.x;
   const int64_t nW = p.n_windows;
   const tre_slo s = p.slo[(uint64_t)t * p.M + m];
+  const double rho = s.reliability;
   const uint32_t* cnt = p.counts + ((uint64_t)t * p.M + m) * nW;
+  tre_fit* dst = p.fit + (uint64_t)t * p.M + m;
 
-  // candidate keys go to LDS in element order; non-candidates are marked ~0
-  // (no key of a finite S reaches it) until the largest key is known
+  // candidate keys to LDS in element order; non-candidates marked ~0 (no key
+  // of a finite S reaches it)
   uint64_t kmax = 0, kor = 0, kand = ~0ull;
-  uint32_t n_real = 0;
+  uint32_t n_real = 0, h_real = 0;
 #pragma unroll 2
   for (int j = 0; j < KPT; ++j) {
     const int64_t w = (int64_t)wave * KPT * 64 + j * 64 + lane;
@@ -383,50 +429,174 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
         kor |= kk;
         kand &= kk;
         ++n_real;
+        h_real += healthy ? 1u : 0u;
       }
     }
     keys_lds[wave * KPT * 64 + j * 64 + lane] = kk;
   }
-  uint32_t n_cand;
+  uint32_t n_cand, Ht;
   (void)block_exclusive_sum(n_real, sc32, n_cand);
+  (void)block_exclusive_sum(h_real, sc32, Ht);
   tre_fit out;
   out.theta = INFINITY;
   out.n_cand = n_cand;
-  out.n_healthy = 0;
+  out.n_healthy = Ht;
   out.n_above = 0;
   out.healthy_above = 0;
   if (n_cand == 0) {
-    if (threadIdx.x == 0) p.fit[(uint64_t)t * p.M + m] = out;
+    if (tid == 0) *dst = out;
     return;
   }
-  // non-candidates become copies of the largest key: they sort after every
-  // candidate, and only positions below n_cand are counted
-  {
-    uint64_t x = kmax;
-    for (int o = 32; o > 0; o >>= 1) {
-      const uint64_t y = ((uint64_t)(uint32_t)__shfl_xor((int)(x >> 32), o) << 32) | (uint32_t)__shfl_xor((int)(uint32_t)x, o);
-      x = y > x ? y : x;
+  kmax = block_reduce_u64<3>(kmax, sc64);
+  const uint64_t vary = block_reduce_u64<0>(kor, sc64) ^ block_reduce_u64<1>(kand, sc64);
+  const uint64_t vary_s = vary & ~1ull;
+  if (vary_s == 0) {  // one value of S: a single run covering every candidate
+    if (tid == 0) {
+      if ((double)Ht >= rho * (double)n_cand) {
+        out.theta = __longlong_as_double((long long)(kmax >> 1));
+        out.n_above = n_cand;
+        out.healthy_above = Ht;
+      }
+      *dst = out;
     }
-    if (lane == 0) sc64[wave] = x;
-    __syncthreads();
-    kmax = sc64[0];
-    for (int w = 1; w < kFitWaves; ++w) kmax = sc64[w] > kmax ? sc64[w] : kmax;
-    __syncthreads();
+    return;
   }
-  const uint64_t vary = block_or_and(kor, true, sc64) ^ block_or_and(kand, false, sc64);
-  // each thread rewrites only its own elements
+
+  // ---- 1. histogram over buckets, packed (healthy << 16) | count
+  const int hb = 63 - __clzll((long long)vary_s);
+  const int lo = hb >= 11 ? hb - 10 : 1;
+  auto bucket = [&](uint64_t key) { return (uint32_t)(key >> lo) & (uint32_t)(kBuckets - 1); };
+  for (int i = tid; i < kBuckets; i += kFitThreads) hist[i] = 0;
+  __syncthreads();
+#pragma unroll 4
+  for (int j = 0; j < KPT; ++j) {
+    const uint64_t kk = keys_lds[wave * KPT * 64 + j * 64 + lane];
+    if (kk != ~0ull) atomicAdd(&hist[bucket(kk)], ((uint32_t)(kk & 1ull) << 16) | 1u);
+  }
+  __syncthreads();
+  // two buckets per thread; counts and healthy counts stay below 2^16
+  const uint32_t v0 = hist[2 * tid], v1 = hist[2 * tid + 1];
+  uint32_t tot;
+  const uint32_t ex = block_exclusive_sum(v0 + v1, sc32, tot);
+  const uint32_t offs[2] = {ex, ex + v0}, cnts[2] = {v0, v1};
+  // ---- 2. bucket status
+  uint32_t qual_b = kNone;
+  bool maybe[2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const uint32_t c = cnts[q] & 0xFFFFu, u = c - (cnts[q] >> 16);
+    const uint32_t G = offs[q] & 0xFFFFu, P = offs[q] >> 16;
+    const uint32_t N = n_cand - G, H = Ht - P;
+    maybe[q] = false;
+    if (c == 0) continue;
+    if ((double)H >= rho * (double)N) {
+      if (qual_b == kNone) qual_b = 2u * tid + q;
+    } else if (c >= 2) {
+      const bool skip = (rho >= 0.0 && rho <= 1.0) ? rho * (double)(N - u) >= (double)H + 1.0
+                                                   : (double)H < rho * (double)(N - c + 1);
+      maybe[q] = !skip;
+    }
+  }
+  const uint32_t bstar = block_min_u32(qual_b, sc32);
+  // ---- 3. keys of the undecided buckets below b*
+  uint32_t mc[2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q) mc[q] = (maybe[q] && 2u * tid + q < bstar) ? (cnts[q] & 0xFFFFu) : 0u;
+  uint32_t mtot;
+  const uint32_t mex = block_exclusive_sum(mc[0] + mc[1], sc32, mtot);
+  if (mtot <= (uint32_t)kResolveCap) {
+    // per bucket: (G, P) and the compact offset with bit 31 marking a gathered bucket
+    hist[2 * tid] = offs[0];
+    hist[2 * tid + 1] = offs[1];
+    hist[kBuckets + 2 * tid] = mex | (mc[0] ? 0x80000000u : 0u);
+    hist[kBuckets + 2 * tid + 1] = (mex + mc[0]) | (mc[1] ? 0x80000000u : 0u);
+    if (tid == 0) n_gathered = 0;
+    __syncthreads();
+    uint64_t kstar = ~0ull;  // smallest key of bucket b*
+#pragma unroll 4
+    for (int j = 0; j < KPT; ++j) {
+      const uint64_t kk = keys_lds[wave * KPT * 64 + j * 64 + lane];
+      if (kk == ~0ull) continue;
+      const uint32_t bk = bucket(kk);
+      if (bk == bstar) kstar = kk < kstar ? kk : kstar;
+      else if (hist[kBuckets + bk] & 0x80000000u) cmp[atomicAdd(&n_gathered, 1u)] = kk;
+    }
+    kstar = block_reduce_u64<2>(kstar, sc64);
+    // bitonic sort of the gathered keys, padded to a power of two
+    uint32_t p2 = 2;
+    while (p2 < mtot) p2 <<= 1;
+    for (uint32_t i = mtot + tid; i < p2; i += kFitThreads) cmp[i] = ~0ull;
+    __syncthreads();
+    for (uint32_t kk2 = 2; kk2 <= p2; kk2 <<= 1) {
+      for (uint32_t jj = kk2 >> 1; jj > 0; jj >>= 1) {
+        const uint32_t i = tid, ixj = tid ^ jj;
+        if (i < p2 && ixj > i) {
+          const uint64_t x = cmp[i], y = cmp[ixj];
+          if ((x > y) == ((i & kk2) == 0)) {
+            cmp[i] = y;
+            cmp[ixj] = x;
+          }
+        }
+        __syncthreads();
+      }
+    }
+    // healthy keys before each gathered position; the gathered keys of one
+    // bucket are contiguous, from its compact offset
+    const uint64_t ck = tid < (int)mtot ? cmp[tid] : ~0ull;
+    uint32_t unused;
+    const uint32_t hpre = block_exclusive_sum(tid < (int)mtot ? (uint32_t)(ck & 1ull) : 0u, sc32, unused);
+    uint32_t* hpre_l = (uint32_t*)keys_lds;  // the keys are no longer needed
+    hpre_l[tid] = hpre;
+    __syncthreads();
+    uint32_t cand_g = kNone, cand_h = 0;
+    if (tid < (int)mtot) {
+      const uint32_t bk = bucket(ck);
+      const uint32_t cf = hist[kBuckets + bk] & 0x7FFFFFFFu, GP = hist[bk];
+      const uint32_t i = (uint32_t)tid - cf, g = (GP & 0xFFFFu) + i;
+      if (i == 0 || (cmp[tid - 1] >> 1) != (ck >> 1)) {
+        const uint32_t H = Ht - ((GP >> 16) + hpre - hpre_l[cf]), N = n_cand - g;
+        if ((double)H >= rho * (double)N) {
+          cand_g = g;
+          cand_h = H;
+        }
+      }
+    }
+    const uint32_t gmin = block_min_u32(cand_g, sc32);
+    if (gmin != kNone) {
+      if (cand_g == gmin) {
+        out.theta = __longlong_as_double((long long)(ck >> 1));
+        out.n_above = n_cand - gmin;
+        out.healthy_above = cand_h;
+        *dst = out;
+      }
+    } else if (tid == 0) {
+      if (bstar != kNone) {
+        const uint32_t GP = hist[bstar];
+        out.theta = __longlong_as_double((long long)(kstar >> 1));
+        out.n_above = n_cand - (GP & 0xFFFFu);
+        out.healthy_above = Ht - (GP >> 16);
+      }
+      *dst = out;
+    }
+    return;
+  }
+
+  // ---- 4. fallback: sort every key. Non-candidates become copies of the
+  // largest key, so they sort after every candidate; only positions below
+  // n_cand are counted. Element e lives in wave e / (KPT*64), slot
+  // (e / 64) % KPT, lane e % 64: ranks that follow (wave, slot, lane) order
+  // keep every pass stable.
 #pragma unroll
   for (int j = 0; j < KPT; ++j) {
     uint64_t* q = keys_lds + wave * KPT * 64 + j * 64 + lane;
     if (*q == ~0ull) *q = kmax;
   }
   __syncthreads();
-
   const uint64_t lt_mask = (1ull << lane) - 1ull;
   for (int pass = 0; pass < 8; ++pass) {
     const int shift = pass * 8;
     if (((vary >> shift) & 0xFFull) == 0) continue;  // digit equal in every key
-    for (int i = threadIdx.x; i < 256 * kFitWaves; i += kFitThreads) hist[i] = 0;
+    for (int i = tid; i < 256 * kFitWaves; i += kFitThreads) hist[i] = 0;
     __syncthreads();
     uint32_t pos[(KPT + 1) / 2];  // ranks within the wave's digit bucket, two 16-bit halves each
 #pragma unroll
@@ -452,10 +622,10 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
     __syncthreads();
     // exclusive offsets in (digit, wave) order: 4 entries per thread
     {
-      uint32_t* h4 = hist + threadIdx.x * 4;
+      uint32_t* h4 = hist + tid * 4;
       const uint32_t a0 = h4[0], a1 = h4[1], a2 = h4[2], a3 = h4[3];
-      uint32_t tot;
-      const uint32_t base = block_exclusive_sum(a0 + a1 + a2 + a3, sc32, tot);
+      uint32_t tot4;
+      const uint32_t base = block_exclusive_sum(a0 + a1 + a2 + a3, sc32, tot4);
       h4[0] = base;
       h4[1] = base + a0;
       h4[2] = base + a0 + a1;
@@ -473,29 +643,23 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
     }
     __syncthreads();
   }
-  // keys_lds holds the keys in ascending order (also when no digit varied)
-  // healthy candidates per wave; a wave's elements are one contiguous block
+  // keys_lds holds the keys in ascending order; healthy count per wave (a
+  // wave's elements are one contiguous block)
   uint32_t hsum = 0, hbits = 0;
 #pragma unroll
   for (int j = 0; j < KPT; ++j) {
     const uint32_t e = (uint32_t)(wave * KPT * 64 + j * 64 + lane);
-    const uint32_t hb = (e < n_cand) ? (uint32_t)(keys_lds[e] & 1ull) : 0u;
-    hbits |= hb << j;
-    hsum += hb;
+    const uint32_t hbit = (e < n_cand) ? (uint32_t)(keys_lds[e] & 1ull) : 0u;
+    hbits |= hbit << j;
+    hsum += hbit;
   }
   __syncthreads();
   for (int o = 32; o > 0; o >>= 1) hsum += __shfl_xor(hsum, o);
   if (lane == 0) sc32[wave] = hsum;
   __syncthreads();
-  uint32_t wbase = 0, Ht = 0;
-  for (int w = 0; w < kFitWaves; ++w) {
-    const uint32_t c = sc32[w];
-    wbase += w < wave ? c : 0u;
-    Ht += c;
-  }
+  uint32_t wbase = 0;
+  for (int w = 0; w < kFitWaves; ++w) wbase += w < wave ? sc32[w] : 0u;
   __syncthreads();
-  // a threshold at a group of equal S covers the whole group and everything
-  // above it: evaluate at each group's first (lowest) position
   uint32_t best = kNone, best_h = 0;
   uint32_t run = wbase;  // healthy candidates before the current slot
 #pragma unroll
@@ -504,36 +668,22 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
     const uint64_t hbal = __ballot((hbits >> j) & 1u);
     const uint32_t before = run + (uint32_t)__popcll(hbal & lt_mask);
     run += (uint32_t)__popcll(hbal);
-    if (e < n_cand) {
-      const bool start = e == 0 || (keys_lds[e - 1] >> 1) != (keys_lds[e] >> 1);
-      if (start) {
-        const uint32_t N = n_cand - e, H = Ht - before;
-        if ((double)H >= s.reliability * (double)N && e < best) {
-          best = e;
-          best_h = H;
-        }
+    if (e < n_cand && (e == 0 || (keys_lds[e - 1] >> 1) != (keys_lds[e] >> 1))) {
+      const uint32_t N = n_cand - e, H = Ht - before;
+      if ((double)H >= rho * (double)N && e < best) {
+        best = e;
+        best_h = H;
       }
     }
   }
-  // smallest qualifying group start (the lowest position is the smallest S)
-  uint32_t bmin = best;
-  for (int o = 32; o > 0; o >>= 1) {
-    const uint32_t y = (uint32_t)__shfl_xor((int)bmin, o);
-    bmin = y < bmin ? y : bmin;
-  }
-  if (lane == 0) sc32[wave] = bmin;
-  __syncthreads();
-  uint32_t g = kNone;
-  for (int w = 0; w < kFitWaves; ++w) g = sc32[w] < g ? sc32[w] : g;
-  out.n_healthy = Ht;
+  const uint32_t g = block_min_u32(best, sc32);
   if (g != kNone && best == g) {
-    // the thread that holds position g writes the result
     out.theta = __longlong_as_double((long long)(keys_lds[g] >> 1));
     out.n_above = n_cand - g;
     out.healthy_above = best_h;
-    p.fit[(uint64_t)t * p.M + m] = out;
-  } else if (g == kNone && threadIdx.x == 0) {
-    p.fit[(uint64_t)t * p.M + m] = out;
+    *dst = out;
+  } else if (g == kNone && tid == 0) {
+    *dst = out;
   }
 }
 

@@ -244,3 +244,67 @@ def test_argument_errors(lib):
     assert e.value.code == tre.TRE_ERANGE
     ev2.close()
     ev.close()
+
+
+def _fit_cases(nW, seed):
+    """Per-model synthetic smoothed TSS and window health, chosen to take
+    every path of the fit: a clean threshold, health hovering at the target
+    rate, long runs of equal values, a dense cluster with outliers (whole
+    buckets to resolve, or the full sort), and one constant value."""
+    rng = np.random.default_rng(seed)
+    base = rng.uniform(1.0, 100.0, nW)
+    return [(base, base > 40, 0.98),
+            (base, rng.random(nW) < 0.9, 0.9),
+            (rng.choice([1.0, 2.0, 3.5, 8.0], nW), rng.random(nW) < 0.7, 0.75),
+            (np.where(rng.random(nW) < 0.02, 1e6, 5.0 + rng.random(nW) * 1e-9), rng.random(nW) < 0.9, 0.9),
+            (np.full(nW, 7.0), rng.random(nW) < 0.95, 0.9)]
+
+
+@pytest.mark.parametrize("nW,seed", [(1000, 1), (1000, 2), (14400, 1), (14400, 2)])
+def test_fit_paths_with_given_tss(lib, nW, seed):
+    """tre_calibrate takes the smoothed TSS as an input: feed chosen values,
+    with one request per (window, model) whose TTFT meets or misses the
+    bound, so every window's health is set by hand."""
+    tre, device, torch = lib
+    cases = _fit_cases(nW, seed)
+    M = len(cases)
+    win = 100
+    rows = []
+    rid = 0
+    for w in range(nW):
+        for m, (_, healthy, _) in enumerate(cases):
+            t0 = w * win + 5 * m
+            first = 10 if healthy[w] else 60  # TTFT bound 30 ms
+            rows += [(t0, m, rid, CP.A, 8), (t0, m, rid, CP.P | CP.ADMIT, 8), (t0 + first, m, rid, CP.D, 8),
+                     (t0 + 70, m, rid, CP.D, 8), (t0 + 70, m, rid, CP.F, 0)]
+            rid += 1
+    ev_h = CP._trace(rows)
+    cfg = {"window_ms": win, "duration_ms": win * (nW + 1), "fast_period_ms": win, "slow_period_ms": win,
+           "n_models": M, "budget": M}
+    cols, off = _columns(torch, [ev_h])
+    ev = tre.tre_load_events(cols["ts"], cols["model"], cols["req"], cols["type"], cols["tokens"], off, cfg)
+    nWe = ev.n_windows
+    S = np.ones((nWe, M))
+    for m, (sv, _, _) in enumerate(cases):
+        S[:nW, m] = sv
+    fl = np.full((nWe, M), tre.TRE_FLAG_INIT, np.uint8)
+    slo_cols = {"ttft_ms": np.full(M, 30.0), "tpot_ms": np.full(M, 1e9), "e2e_ms": np.full(M, 1e9),
+                "attain_q": np.full(M, 0.95), "reliability": np.array([c[2] for c in cases])}
+    slo = tre.pack(slo_cols, tre.SLO_DTYPE)
+    tss64 = torch.from_numpy(S.reshape(1, nWe, M).copy()).cuda()
+    flags = torch.from_numpy(fl.reshape(1, nWe, M).copy()).cuda()
+    out = tre.calib_outputs(ev, rid)
+    tre.tre_calibrate(ev, slo, tss64, flags, out)
+    torch.cuda.synchronize()
+    fit = tre.unpack_fit(out["fit"])
+    o = O.get()
+    slo_h = _slo_rows(slo_cols, 0, M)
+    r = o.calib_requests(ev_h, win, cfg["duration_ms"], slo_h, rid)
+    assert (r["judged"][:, :nW] == 1).all()
+    ref = o.calib_fit(S, fl, r["judged"], r["ok"], slo_h)
+    for m in range(M):
+        for k in ("n_cand", "n_healthy", "n_above", "healthy_above"):
+            assert fit[m][k] == ref[m][k], (m, k, fit[m], ref[m])
+        assert fit[m]["theta"].view(np.uint64) == ref[m]["theta"].view(np.uint64), (m, fit[m], ref[m])
+    say(f"nW {nW} seed {seed}: theta {fit['theta']}")
+    ev.close()
