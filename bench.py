@@ -218,13 +218,7 @@ def main():
     print(json.dumps(result), flush=True)
 
     if args.copy_calib_gb > 0:
-        n = int(args.copy_calib_gb * 1e9) // 4
-        src = torch.ones(n, dtype=torch.int32, device="cuda")
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        log(f"copy calibration: 3 x {4 * n} bytes read + written")
+        copy_calibration(args.copy_calib_gb, torch)
     ev.close()
 
 
@@ -308,7 +302,21 @@ def calibrate_main(args, w, dt, device, tre, torch, np):
         "roofline": roofline, "kernels": kernels, "cpu_baseline": cpu, "parity": parity,
     }
     print(json.dumps(result), flush=True)
+    if args.copy_calib_gb > 0:
+        del tss, out
+        copy_calibration(args.copy_calib_gb, torch)
     ev.close()
+
+
+def copy_calibration(gb, torch):
+    """A plain device copy of known size, for scaling the traffic counters."""
+    n = int(gb * 1e9) // 4
+    src = torch.ones(n, dtype=torch.int32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    log(f"copy calibration: 3 x {4 * n} bytes read + written")
 
 
 def calib_cpu_leg(w, sample, out, tss, req_cap, tre, threads):
