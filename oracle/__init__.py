@@ -22,6 +22,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "tre_oracle.c")
 _SRC_ACT = os.path.join(_HERE, "tre_oracle_act.c")  # control replay with the actuation model
 _SRC_CALIB = os.path.join(_HERE, "tre_oracle_calib.c")  # calibration sweep
+_SRC_LOOP = os.path.join(_HERE, "tre_oracle_loop.c")  # closed-loop replay
 _LIB = os.path.join(_HERE, "libtre_oracle.so")
 
 CFLAGS = ["-O2", "-fPIC", "-shared", "-ffp-contract=off", "-fno-fast-math", "-std=c11"]
@@ -44,6 +45,10 @@ REQ_DTYPE = np.dtype([("ttft_ms", "<i8"), ("e2e_ms", "<i8"), ("tpot_ms", "<f8"),
                       ("complete", "u1"), ("has_tpot", "u1"), ("ok", "u1"), ("pad", "u1")])
 assert PROFILE_DTYPE.itemsize == 56 and SCENARIO_DTYPE.itemsize == 24 and MOVE_DTYPE.itemsize == 8
 assert SLO_DTYPE.itemsize == 40 and FIT_DTYPE.itemsize == 24 and REQ_DTYPE.itemsize == 32
+SVC_DTYPE = np.dtype([("prefill_us", "<u4"), ("decode_us", "<u4")])
+LOOP_STATS_DTYPE = np.dtype([("n_arrived", "<u4"), ("n_started", "<u4"), ("n_done", "<u4"), ("n_ok", "<u4"),
+                             ("e2e_sum", "<i8"), ("e2e_max", "<i8")])
+assert SVC_DTYPE.itemsize == 8 and LOOP_STATS_DTYPE.itemsize == 32
 
 
 def build(force: bool = True, src: str = _SRC, out: str = _LIB) -> str:
@@ -51,7 +56,7 @@ def build(force: bool = True, src: str = _SRC, out: str = _LIB) -> str:
     The default library also holds the actuation-model replay and the
     calibration sweep; a library built from another base source (the
     pin-strength tests) does not."""
-    srcs = [src] + ([_SRC_ACT, _SRC_CALIB] if src == _SRC else [])
+    srcs = [src] + ([_SRC_ACT, _SRC_CALIB, _SRC_LOOP] if src == _SRC else [])
     stale = not os.path.exists(out) or any(os.path.getmtime(out) < os.path.getmtime(x) for x in srcs)
     if force or stale:
         tmp = f"{out}.{os.getpid()}.tmp"
@@ -86,6 +91,11 @@ class Oracle:
             L.oracle_calib_requests.argtypes = [i64, i64, i32, i64, vp, vp, vp, vp, vp, vp, u32, vp, vp, vp]
             L.oracle_calib_fit.restype = ctypes.c_int
             L.oracle_calib_fit.argtypes = [i64, i32, vp, vp, vp, vp, vp, vp]
+        self.has_loop = hasattr(L, "oracle_loop")
+        if self.has_loop:
+            L.oracle_loop.restype = ctypes.c_int
+            L.oracle_loop.argtypes = ([i64, i64, i64, i64, i32, i32, vp, vp, vp, vp, i32, i32, i32, i32, vp, vp, vp, vp,
+                                       vp, u32, vp, vp, vp, vp, vp, vp, vp, i64, vp, vp, vp, vp])
         self.L = L
         self.path = path
 
@@ -180,6 +190,63 @@ class Oracle:
                 "r_windows": r_windows, "idle_final": int(idle[0]), "held_final": held}
 
 
+    # ----------------------------------------------------------- closed loop
+    def loop(self, cfg: Dict[str, int], prof: np.ndarray, sc: np.ndarray, slo: np.ndarray, svc: np.ndarray,
+             reqs: Dict[str, np.ndarray], spr: int = 8, r_cap: int = 16, prefill_chunk: int = 2048,
+             decode_chunk: int = 24, move_cap: Optional[int] = None, want_events: bool = False,
+             want_tss: bool = False) -> Dict[str, np.ndarray]:
+        """Closed-loop replay of one scenario over one trace's request table
+        (arrival_ms, model, prompt, output; model by model, arrivals in
+        order within a model)."""
+        prof = np.ascontiguousarray(prof, dtype=PROFILE_DTYPE)
+        sc = np.ascontiguousarray(np.atleast_1d(sc), dtype=SCENARIO_DTYPE)
+        slo = np.ascontiguousarray(slo, dtype=SLO_DTYPE)
+        svc = np.ascontiguousarray(svc, dtype=SVC_DTYPE)
+        M = prof.shape[0]
+        nW = cfg["duration_ms"] // cfg["window_ms"]
+        model = np.asarray(reqs["model"], np.int64)
+        assert (np.diff(model) >= 0).all(), "requests must be grouped by model"
+        req_off = np.zeros(M + 1, np.int64)
+        req_off[1:] = np.cumsum(np.bincount(model, minlength=M)[:M])
+        arr = np.ascontiguousarray(reqs["arrival_ms"], np.int64)
+        pr = np.ascontiguousarray(reqs["prompt"], np.uint16)
+        ou = np.ascontiguousarray(reqs["output"], np.uint16)
+        if move_cap is None:
+            move_cap = max(1, nW * int(sc[0]["max_moves"]))
+        moves = np.zeros(move_cap, MOVE_DTYPE)
+        n_moves = np.zeros(1, np.uint32)
+        r_final = np.zeros(M, np.int32)
+        r_windows = np.zeros(M, np.int64)
+        stats = np.zeros(M, LOOP_STATS_DTYPE)
+        S = np.zeros((nW, M), np.float64) if want_tss else None
+        fl = np.zeros((nW, M), np.uint8) if want_tss else None
+        n_ev = np.zeros(1, np.int64)
+        cap = 0
+        ev = None
+        if want_events:
+            cap = int(len(arr) * (3 + int(pr.max(initial=0)) // prefill_chunk + int(ou.max(initial=0)) // decode_chunk + 2))
+            ev = {"ts": np.zeros(cap, np.int64), "model": np.zeros(cap, np.uint8), "type": np.zeros(cap, np.uint8),
+                  "tokens": np.zeros(cap, np.uint16)}
+        ptr = lambda a: None if a is None else a.ctypes.data
+        rc = self.L.oracle_loop(
+            cfg["window_ms"], cfg["duration_ms"], cfg["fast_period_ms"], cfg["slow_period_ms"], M, cfg["budget"],
+            prof.ctypes.data, sc.ctypes.data, slo.ctypes.data, svc.ctypes.data, spr, r_cap, prefill_chunk,
+            decode_chunk, req_off.ctypes.data, arr.ctypes.data, pr.ctypes.data, ou.ctypes.data, moves.ctypes.data,
+            move_cap, n_moves.ctypes.data, r_final.ctypes.data, r_windows.ctypes.data, stats.ctypes.data, ptr(S),
+            ptr(fl), n_ev.ctypes.data, cap, ptr(None if ev is None else ev["ts"]),
+            ptr(None if ev is None else ev["model"]), ptr(None if ev is None else ev["type"]),
+            ptr(None if ev is None else ev["tokens"]))
+        if rc:
+            raise ValueError(f"oracle_loop rejected the scenario ({rc})")
+        n = int(n_moves[0])
+        out = {"moves": moves[:min(n, move_cap)].copy(), "n_moves": n, "r_final": r_final, "r_windows": r_windows,
+               "stats": stats, "n_events": int(n_ev[0])}
+        if want_tss:
+            out["S"], out["flags"] = S, fl
+        if want_events:
+            out["events"] = {k: v[:out["n_events"]] for k, v in ev.items()}
+        return out
+
     # ----------------------------------------------------------- calibration
     def calib_requests(self, ev: Dict[str, np.ndarray], window_ms: int, duration_ms: int, slo: np.ndarray,
                        req_cap: int) -> Dict[str, np.ndarray]:
@@ -229,6 +296,14 @@ class Oracle:
         q["fit"] = self.calib_fit(r["S"], r["flags"], q["judged"], q["ok"], slo)
         q["S"], q["flags"] = r["S"], r["flags"]
         return q
+
+
+def pack_svc(cols: Dict[str, np.ndarray]) -> np.ndarray:
+    n = cols["decode_us"].shape[0]
+    a = np.zeros(n, SVC_DTYPE)
+    for k in SVC_DTYPE.names:
+        a[k] = cols[k]
+    return a
 
 
 def pack_slo(cols: Dict[str, np.ndarray]) -> np.ndarray:

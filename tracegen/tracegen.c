@@ -317,7 +317,46 @@ static void sort_by_ts(rvec* v, rec_t* tmp) {
   if (src != v->v) memcpy(v->v, src, n * sizeof(rec_t));
 }
 
-static int gen_trace(const tg_config* c, uint64_t trace, rvec* out) {
+/* request table of one model instead of its served events: the same length
+   draws as serve_model, in the same order, without the FCFS service */
+typedef struct {
+  uint32_t ts, req;
+  uint16_t prompt, output;
+  uint8_t model;
+} qrec_t;
+typedef struct { qrec_t* v; size_t n, cap; } qvec;
+
+static int list_requests(const tg_config* c, int m, uint64_t trace, const dvec* arr, qvec* out) {
+  const int64_t dur = c->duration_ms;
+  rng_t lr;
+  rng_seed(&lr, c->seed, trace + 1, (uint64_t)m + 1, 2);
+  const uint32_t M = (uint32_t)c->n_models;
+  for (size_t i = 0; i < arr->n; ++i) {
+    int prompt = clip_len(exp(c->prompt_mu[m] + c->prompt_sigma[m] * rng_normal(&lr)),
+                          c->prompt_min, c->prompt_max);
+    int output = clip_len(exp(c->out_mu[m] + c->out_sigma[m] * rng_normal(&lr)),
+                          c->out_min, c->out_max);
+    int64_t ta = to_ms(arr->v[i]);
+    if (ta >= dur) continue;
+    if (out->n == out->cap) {
+      size_t nc = out->cap ? out->cap * 2 : 4096;
+      qrec_t* p = (qrec_t*)realloc(out->v, nc * sizeof(qrec_t));
+      if (!p) return -1;
+      out->v = p; out->cap = nc;
+    }
+    qrec_t* q = &out->v[out->n++];
+    q->ts = (uint32_t)ta; q->req = (uint32_t)(i * M + (uint32_t)m);
+    q->prompt = (uint16_t)prompt; q->output = (uint16_t)output; q->model = (uint8_t)m;
+  }
+  return 0;
+}
+
+static int gen_trace_into(const tg_config* c, uint64_t trace, rvec* out, qvec* reqs);
+
+static int gen_trace(const tg_config* c, uint64_t trace, rvec* out) { return gen_trace_into(c, trace, out, 0); }
+
+/* events of one trace (reqs == NULL), or its request table (out unused) */
+static int gen_trace_into(const tg_config* c, uint64_t trace, rvec* out, qvec* reqs) {
   const double T = (double)c->duration_ms / 1000.0;
   const int M = c->n_models;
   dvec arr = {0, 0, 0};
@@ -381,7 +420,7 @@ static int gen_trace(const tg_config* c, uint64_t trace, rvec* out) {
       }
       default: rc = -2;
     }
-    if (rc == 0) rc = serve_model(c, m, trace, &arr, out);
+    if (rc == 0) rc = reqs ? list_requests(c, m, trace, &arr, reqs) : serve_model(c, m, trace, &arr, out);
   }
   free(arr.v);
   return rc;
@@ -476,4 +515,28 @@ int tg_fill(const tg_config* cfg, uint64_t t0, uint64_t t1, int n_threads, const
   j.cfg = cfg; j.t0 = t0; j.t1 = t1; j.off = off;
   j.ts = ts; j.model = model; j.req = req; j.type = type; j.tokens = tokens;
   return run_job(&j, n_threads);
+}
+
+/* Request table of one trace: per request its arrival (ms), model, id,
+   prompt and output lengths, model by model, arrivals in order within a
+   model (the draws of tg_fill, without the fixed-capacity service). With
+   cap too small, returns -5 and sets *n to the count needed. */
+int tg_requests(const tg_config* cfg, uint64_t trace, int64_t cap, int64_t* n, int64_t* arrival_ms,
+                uint8_t* model, uint32_t* req, uint16_t* prompt, uint16_t* output) {
+  if (!cfg || !n || cfg->n_models < 1 || cfg->n_models > 256) return -1;
+  qvec q = {0, 0, 0};
+  int rc = gen_trace_into(cfg, trace, 0, &q);
+  if (rc == 0) {
+    *n = (int64_t)q.n;
+    if ((int64_t)q.n > cap) {
+      rc = -5;
+    } else {
+      for (size_t i = 0; i < q.n; ++i) {
+        arrival_ms[i] = q.v[i].ts; model[i] = q.v[i].model; req[i] = q.v[i].req;
+        prompt[i] = q.v[i].prompt; output[i] = q.v[i].output;
+      }
+    }
+  }
+  free(q.v);
+  return rc;
 }
