@@ -353,10 +353,81 @@ int tre_calibrate(const tre_events* ev, const tre_slo* slo, const double* tss64,
                   tre_req_latency* reqs, uint64_t* n_bad_ids, void* ws, size_t ws_bytes,
                   void* stream);
 
+/* ---------------------------------------------------- closed-loop replay
+ * The requests of each trace are served by each model's routable replicas,
+ * the rules above move replicas at tick windows, and the TSS the controller
+ * reads comes from the events this service produces (Sections "Dual-Speed
+ * Control", "Bounded Pairwise Transfer": after each transition the
+ * controller observes the result at the next tick; Section "System
+ * Boundary and Replica State": only routable replicas take new requests, a
+ * hidden replica drains):
+ *   - a routable replica of model m has slots_per_replica slots; requests of
+ *     a model start in arrival order on the slot that frees first (lowest
+ *     index on ties) at max(arrival, its free time);
+ *   - a prompt chunk of c tokens takes ceil(c * prefill_us / 1000) ms on its
+ *     slot, an output chunk ceil(c * decode_us / 1000) ms; the events are
+ *     those of the traces (ARRIVE, one PREFILL per prompt chunk at its start
+ *     with ADMIT on the first, one DECODE per output chunk at its end, FINISH
+ *     at the last), dropped at or after the end of the trace;
+ *   - TSS per window, Eq. (1) and the smoothing as in tre_eval_tss;
+ *   - at each tick the rules of tre_rebalance, with receivers below r_cap
+ *     replicas; a move acts from the end of its window: the receiver gains
+ *     slots free from then, the donor's replica stops taking requests and its
+ *     slots that free first are removed (requests on them finish);
+ *   - a request whose FINISH lies in the trace is judged against its
+ *     model's SLO as in tre_calibrate. */
+typedef struct {
+  uint32_t prefill_us;  /* per prompt token on one slot */
+  uint32_t decode_us;   /* per output token on one slot */
+} tre_service;
+
+typedef struct {
+  const int64_t* arrival_ms;   /* device [n_requests], ms from trace start      */
+  const uint16_t* prompt;      /* device [n_requests], prompt tokens            */
+  const uint16_t* output;      /* device [n_requests], output tokens (>= 1)      */
+  const int64_t* req_off;      /* device [n_traces * n_models + 1]: requests of
+                                  (trace t, model m) are [req_off[t*M+m],
+                                  req_off[t*M+m+1]), arrivals non-decreasing    */
+  const tre_service* service;  /* device [n_traces][n_models]                   */
+  const tre_slo* slo;          /* device [n_traces][n_models]                   */
+  int32_t slots_per_replica;
+  int32_t r_cap;               /* receivers must hold fewer replicas            */
+  int32_t prefill_chunk;       /* prompt tokens per PREFILL event               */
+  int32_t decode_chunk;        /* output tokens per DECODE event                */
+  uint32_t max_prompt, max_output;         /* bounds over the table (host)      */
+  uint32_t max_prefill_us, max_decode_us;  /* bounds over service (host)        */
+} tre_loop_requests;
+
+typedef struct {
+  uint32_t n_arrived, n_started, n_done, n_ok;  /* n_done: judged requests */
+  int64_t e2e_sum, e2e_max;                     /* over judged requests, ms */
+} tre_loop_stats;                               /* 32 bytes */
+
+/* Workspace bytes of tre_loop: per scenario and model the slots
+   (min(r_cap, budget) * slots_per_replica * 8 B) and a ring of future
+   windows sized from the declared bounds, plus 256. */
+int tre_loop_workspace_size(const tre_trace_cfg* cfg, const tre_loop_requests* rq, uint32_t n_scenarios,
+                            size_t* bytes);
+
+/* Closed-loop replay of n_scenarios scenarios (device sc, as tre_rebalance)
+   over the request tables (rq: host struct of device pointers) with the
+   profiles prof (device [n_traces][n_models]) and cfg (host; budget in
+   replicas). Outputs as tre_rebalance, plus stats (device
+   [n_scenarios][n_models]) and optionally the per-window smoothed TSS
+   (device [n_scenarios][n_windows][n_models], or NULL). r_init must lie in
+   [0, min(r_cap, budget)] with the sum within the budget, and req_off must
+   index the request arrays; other inputs give unspecified results (never an
+   access outside them). Requests beyond the declared bounds give
+   unspecified results too; the workspace's first 8 bytes then count the
+   events dropped (0 otherwise). Enqueued on `stream`. */
+int tre_loop(const tre_trace_cfg* cfg, uint32_t n_traces, const tre_loop_requests* rq, const tre_profile* prof,
+             const tre_scenario* sc, uint32_t n_scenarios, const tre_ctl_out* out, tre_loop_stats* stats,
+             double* tss64, void* ws, size_t ws_bytes, void* stream);
+
 /* Kernel timing (HIP events recorded around each launch on its stream).
    tre_set_timing(1) starts recording; tre_kernel_time waits for the
    recorded launches of `kernel` ("tss_stream", "rebalance", "validate",
-   "calib_fill", "calib_join", "calib_judge", "calib_fit")
+   "calib_fill", "calib_join", "calib_judge", "calib_fit", "loop_replay")
    and returns their total milliseconds and count, then forgets them. */
 int tre_set_timing(int enable);
 int tre_kernel_time(const char* kernel, double* total_ms, uint64_t* launches);

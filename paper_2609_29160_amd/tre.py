@@ -38,6 +38,9 @@ FIT_DTYPE = np.dtype([("theta", "<f8"), ("n_cand", "<u4"), ("n_healthy", "<u4"),
 REQ_LATENCY_DTYPE = np.dtype([("ttft_ms", "<u4"), ("e2e_ms", "<u4"), ("tpot_ms", "<f8"), ("model", "u1"),
                               ("flags", "u1"), ("pad", "u1", (6,))])
 TRE_REQ_ARRIVED, TRE_REQ_COMPLETE, TRE_REQ_TPOT, TRE_REQ_OK = 1, 2, 4, 8
+SERVICE_DTYPE = np.dtype([("prefill_us", "<u4"), ("decode_us", "<u4")])
+LOOP_STATS_DTYPE = np.dtype([("n_arrived", "<u4"), ("n_started", "<u4"), ("n_done", "<u4"), ("n_ok", "<u4"),
+                             ("e2e_sum", "<i8"), ("e2e_max", "<i8")])
 
 
 class TreError(RuntimeError):
@@ -69,6 +72,12 @@ class _CtlOut(ctypes.Structure):
                 ("r_windows", ctypes.c_void_p)]
 
 
+class _LoopRequests(ctypes.Structure):
+    _fields_ = [(k, ctypes.c_void_p) for k in ("arrival_ms", "prompt", "output", "req_off", "service", "slo")] + \
+               [(k, ctypes.c_int32) for k in ("slots_per_replica", "r_cap", "prefill_chunk", "decode_chunk")] + \
+               [(k, ctypes.c_uint32) for k in ("max_prompt", "max_output", "max_prefill_us", "max_decode_us")]
+
+
 class _Actuation(ctypes.Structure):
     _fields_ = [("wake_ms", ctypes.c_int64), ("sleep_ms", ctypes.c_int64), ("footprint", ctypes.c_void_p),
                 ("veto", ctypes.c_void_p)]
@@ -77,7 +86,7 @@ class _Actuation(ctypes.Structure):
 EXPORTS = ["tre_last_error", "tre_load_events", "tre_free_events", "tre_events_info",
            "tre_check_params", "tre_workspace_size", "tre_eval_tss", "tre_rebalance", "tre_sweep",
            "tre_set_timing", "tre_kernel_time", "tre_check_actuation", "tre_rebalance_act", "tre_sweep_act",
-           "tre_calib_workspace_size", "tre_calibrate"]
+           "tre_calib_workspace_size", "tre_calibrate", "tre_loop_workspace_size", "tre_loop"]
 
 
 def _load():
@@ -114,6 +123,12 @@ def _load():
     L.tre_calib_workspace_size.argtypes = [vp, u32, ctypes.POINTER(sz)]
     L.tre_calibrate.restype = i32
     L.tre_calibrate.argtypes = [vp, vp, vp, vp, u32, vp, vp, vp, vp, vp, sz, vp]
+    L.tre_loop_workspace_size.restype = i32
+    L.tre_loop_workspace_size.argtypes = [ctypes.POINTER(_TraceCfg), ctypes.POINTER(_LoopRequests), u32,
+                                          ctypes.POINTER(sz)]
+    L.tre_loop.restype = i32
+    L.tre_loop.argtypes = [ctypes.POINTER(_TraceCfg), u32, ctypes.POINTER(_LoopRequests), vp, vp, u32,
+                           ctypes.POINTER(_CtlOut), vp, vp, vp, sz, vp]
     L.tre_set_timing.restype = i32
     L.tre_set_timing.argtypes = [i32]
     L.tre_kernel_time.restype = i32
@@ -326,6 +341,55 @@ def unpack_fit(fit: torch.Tensor) -> np.ndarray:
 
 def unpack_reqs(reqs: torch.Tensor) -> np.ndarray:
     return reqs.cpu().numpy().view(REQ_LATENCY_DTYPE)
+
+
+def _cfg(cfg: Dict[str, int]) -> _TraceCfg:
+    return _TraceCfg(cfg["window_ms"], cfg["duration_ms"], cfg["fast_period_ms"], cfg["slow_period_ms"],
+                     cfg["n_models"], cfg["budget"])
+
+
+def loop_requests(tables, n_models: int, service: np.ndarray, slo: np.ndarray, slots_per_replica: int = 8,
+                  r_cap: int = 16, prefill_chunk: int = 2048, decode_chunk: int = 24, device="cuda"):
+    """Device request tables of tre_loop from per-trace host tables
+    (arrival_ms, model, prompt, output; grouped by model, arrivals in order
+    within a model). Returns (struct, tensors); keep the tensors alive."""
+    counts = []
+    for tb in tables:
+        m = np.asarray(tb["model"], np.int64)
+        assert (np.diff(m) >= 0).all(), "requests must be grouped by model"
+        counts.append(np.bincount(m, minlength=n_models)[:n_models])
+    off = np.zeros(len(tables) * n_models + 1, np.int64)
+    off[1:] = np.cumsum(np.concatenate(counts) if counts else np.zeros(0, np.int64))
+    cat = lambda k, dt: np.concatenate([np.asarray(tb[k], dt) for tb in tables]) if tables else np.zeros(0, dt)
+    host = {"arrival_ms": cat("arrival_ms", np.int64), "prompt": cat("prompt", np.uint16),
+            "output": cat("output", np.uint16)}
+    tens = {k: torch.from_numpy(np.concatenate([v, np.zeros(1, v.dtype)])).to(device) for k, v in host.items()}
+    tens["req_off"] = torch.from_numpy(off).to(device)
+    svc = np.ascontiguousarray(service, SERVICE_DTYPE)
+    tens["service"] = torch.from_numpy(svc.view(np.uint8).copy()).to(device)
+    tens["slo"] = torch.from_numpy(np.ascontiguousarray(slo, SLO_DTYPE).view(np.uint8).copy()).to(device)
+    rq = _LoopRequests(_ptr(tens["arrival_ms"]), _ptr(tens["prompt"]), _ptr(tens["output"]), _ptr(tens["req_off"]),
+                       _ptr(tens["service"]), _ptr(tens["slo"]), slots_per_replica, r_cap, prefill_chunk,
+                       decode_chunk, int(host["prompt"].max(initial=1)), int(host["output"].max(initial=1)),
+                       int(svc["prefill_us"].max(initial=0)), int(svc["decode_us"].max(initial=0)))
+    return rq, tens
+
+
+def tre_loop_workspace_size(cfg: Dict[str, int], rq: _LoopRequests, n_scenarios: int) -> int:
+    n = ctypes.c_size_t()
+    c = _cfg(cfg)
+    _check(_L.tre_loop_workspace_size(ctypes.byref(c), ctypes.byref(rq), n_scenarios, ctypes.byref(n)))
+    return n.value
+
+
+def tre_loop(cfg: Dict[str, int], n_traces: int, rq: _LoopRequests, prof: torch.Tensor, sc: torch.Tensor,
+             out: Dict[str, torch.Tensor], stats: torch.Tensor, ws: torch.Tensor,
+             tss64: Optional[torch.Tensor] = None, stream=None):
+    n_sc = sc.numel() // SCENARIO_DTYPE.itemsize
+    c = _cfg(cfg)
+    o = _ctl(out)
+    _check(_L.tre_loop(ctypes.byref(c), n_traces, ctypes.byref(rq), _ptr(prof), _ptr(sc), n_sc, ctypes.byref(o),
+                       _ptr(stats), _ptr(tss64), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 
 def tre_set_timing(enable: bool):

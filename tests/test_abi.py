@@ -48,6 +48,8 @@ def test_struct_layouts():
     assert ctypes.sizeof(tre._Actuation) == 32
     assert tre.SLO_DTYPE.itemsize == 40 and tre.FIT_DTYPE.itemsize == 24
     assert tre.REQ_LATENCY_DTYPE.itemsize == 24
+    assert tre.SERVICE_DTYPE.itemsize == 8 and tre.LOOP_STATS_DTYPE.itemsize == 32
+    assert ctypes.sizeof(tre._LoopRequests) == 6 * 8 + 8 * 4
 
 
 def test_error_message_without_gpu_call():

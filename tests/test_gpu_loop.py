@@ -1,0 +1,211 @@
+"""GPU parity of the closed-loop replay (tre_loop) against the oracle's.
+
+For every scenario: the move log, final replicas, replica-window sums, the
+per-model latency outcomes (arrived, started, judged, SLO met, E2E sum and
+maximum) and the per-window smoothed TSS (bit for bit) must equal the
+oracle's, and no event may fall outside the ring of future windows.
+
+Inputs: the tiny and bursty workloads' request tables (the same arrivals and
+lengths as their traces) under scenario tables with 0 to 4 moves per tick,
+spare budget and replica caps that bind; the oracle's hand cases; 1, 17 and
+64 models; one and three slots per replica; argument errors.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle as O
+import tracegen as tg
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2609_29160_amd import device, tre
+    return tre, device, torch
+
+
+def _rows(cols, t, M, dtype):
+    a = np.zeros(M, dtype)
+    for k in dtype.names:
+        a[k] = cols[k][t * M:(t + 1) * M]
+    return a
+
+
+def _n_ticks(cfg):
+    nW = cfg["duration_ms"] // cfg["window_ms"]
+    return sum(1 for w in range(nW) if ((w + 1) * cfg["window_ms"]) % cfg["fast_period_ms"] == 0
+               or ((w + 1) * cfg["window_ms"]) % cfg["slow_period_ms"] == 0)
+
+
+def _check(lib, name, cfg, tables, prof_cols, slo_cols, svc_cols, sc_cols, spr=8, r_cap=16):
+    tre, device, torch = lib
+    M = cfg["n_models"]
+    T = len(tables)
+    nW = cfg["duration_ms"] // cfg["window_ms"]
+    svc = np.zeros(T * M, tre.SERVICE_DTYPE)
+    for k in tre.SERVICE_DTYPE.names:
+        svc[k] = svc_cols[k]
+    slo = np.zeros(T * M, tre.SLO_DTYPE)
+    for k in tre.SLO_DTYPE.names:
+        slo[k] = slo_cols[k]
+    rq, keep = tre.loop_requests(tables, M, svc, slo, slots_per_replica=spr, r_cap=r_cap)
+    prof = tre.pack(prof_cols, tre.PROFILE_DTYPE)
+    sc = tre.pack(sc_cols, tre.SCENARIO_DTYPE)
+    n_sc = len(sc_cols["trace"])
+    move_cap = max(1, _n_ticks(cfg) * int(np.max(sc_cols["max_moves"])))
+    out = tre.ctl_outputs(_Ev(T, M, nW), n_sc, move_cap)
+    stats = torch.zeros(n_sc * M * tre.LOOP_STATS_DTYPE.itemsize, dtype=torch.uint8, device="cuda")
+    tss = torch.zeros((n_sc, nW, M), dtype=torch.float64, device="cuda")
+    ws = torch.empty(tre.tre_loop_workspace_size(cfg, rq, n_sc), dtype=torch.uint8, device="cuda")
+    tre.tre_loop(cfg, T, rq, prof, sc, out, stats, ws, tss64=tss)
+    torch.cuda.synchronize()
+    assert int(ws[:8].cpu().numpy().view(np.uint64)[0]) == 0, f"{name}: events beyond the ring"
+    moves = tre.unpack_moves(out["moves"]).reshape(n_sc, move_cap)
+    st = stats.cpu().numpy().view(tre.LOOP_STATS_DTYPE).reshape(n_sc, M)
+    S = tss.cpu().numpy()
+    o = O.get()
+    total_moves = 0
+    for s in range(n_sc):
+        t = int(sc_cols["trace"][s])
+        row = np.zeros(1, O.SCENARIO_DTYPE)
+        for k in O.SCENARIO_DTYPE.names:
+            row[k] = sc_cols[k][s]
+        ref = o.loop(cfg, _rows(prof_cols, t, M, O.PROFILE_DTYPE), row, _rows(slo_cols, t, M, O.SLO_DTYPE),
+                     _rows(svc_cols, t, M, O.SVC_DTYPE), tables[t], spr=spr, r_cap=r_cap, move_cap=move_cap,
+                     want_tss=True)
+        what = f"{name} scenario {s}"
+        n = int(out["n_moves"][s])
+        assert n == ref["n_moves"], f"{what}: {n} moves vs {ref['n_moves']}"
+        k = min(n, move_cap)
+        for f in ("window", "path", "receiver", "donor"):
+            assert np.array_equal(moves[s][:k][f], ref["moves"][:k][f]), f"{what}: moves ({f})"
+        assert np.array_equal(out["r_final"][s].cpu().numpy(), ref["r_final"]), f"{what}: r_final"
+        assert np.array_equal(out["r_windows"][s].cpu().numpy(), ref["r_windows"]), f"{what}: r_windows"
+        for f in tre.LOOP_STATS_DTYPE.names:
+            assert np.array_equal(st[s][f], ref["stats"][f]), f"{what}: stats {f} {st[s][f]} vs {ref['stats'][f]}"
+        assert np.array_equal(S[s].view(np.uint64), ref["S"].view(np.uint64)), f"{what}: TSS"
+        total_moves += n
+    return total_moves
+
+
+class _Ev:
+    """The shape ctl_outputs needs (models), without an events handle."""
+
+    def __init__(self, T, M, nW):
+        self.n_traces, self.n_models, self.n_windows = T, M, nW
+
+
+def _scenarios(rng, n, n_traces, ks=(0, 1, 2, 4)):
+    return {"trace": (np.arange(n) % n_traces).astype(np.uint32),
+            "max_moves": np.array([ks[i % len(ks)] for i in range(n)], np.uint32),
+            "theta_scale": rng.uniform(0.5, 2.0, n),
+            "tau_crit_override": np.where(rng.random(n) < 0.5, -1.0, rng.uniform(0.2, 0.8, n))}
+
+
+def test_tiny(lib):
+    w = tg.standard(0)
+    tables = [w.requests(0)]
+    rng = np.random.default_rng(1)
+    cfg = dict(w.trace_cfg(), budget=w.budget + 2)
+    n = _check(lib, "tiny", cfg, tables, w.profile_columns(1), w.slo_columns(1), w.service_columns(1),
+               _scenarios(rng, 8, 1))
+    assert n > 0
+
+
+def test_bursty_spare_budget_and_binding_cap(lib):
+    w = tg.standard(1).scaled(duration_ms=900_000)
+    tables = [w.requests(0)]
+    rng = np.random.default_rng(2)
+    for extra, r_cap in ((0, 16), (3, 16), (3, 5)):
+        cfg = dict(w.trace_cfg(), budget=w.budget + extra)
+        say(f"bursty budget +{extra}, r_cap {r_cap}")
+        n = _check(lib, f"bursty-{extra}-{r_cap}", cfg, tables, w.profile_columns(1), w.slo_columns(1),
+                   w.service_columns(1), _scenarios(rng, 12, 1), r_cap=r_cap)
+        assert n > 0
+
+
+def test_several_traces(lib):
+    w = tg.standard(3).scaled(n_traces=3, duration_ms=600_000)
+    tables = [w.requests(t) for t in range(3)]
+    rng = np.random.default_rng(3)
+    cfg = dict(w.trace_cfg(), budget=w.budget + 4)
+    _check(lib, "diverse-3tr", cfg, tables, w.profile_columns(3), w.slo_columns(3), w.service_columns(3),
+           _scenarios(rng, 9, 3))
+
+
+def test_slots_per_replica(lib):
+    w = tg.standard(0)
+    tables = [w.requests(0)]
+    rng = np.random.default_rng(4)
+    for spr in (1, 3):
+        cfg = dict(w.trace_cfg(), budget=w.budget + 1)
+        _check(lib, f"spr{spr}", cfg, tables, w.profile_columns(1), w.slo_columns(1), w.service_columns(1),
+               _scenarios(rng, 4, 1), spr=spr)
+
+
+def test_hand_cases(lib):
+    """The oracle's hand-derived cases, through the GPU."""
+    for r_cap in (3, 2):
+        cfg = {"window_ms": 100, "duration_ms": 1000, "fast_period_ms": 100, "slow_period_ms": 100,
+               "n_models": 2, "budget": 3}
+        prof = {"w_p": np.full(2, 0.5), "w_q": np.full(2, 2.0), "alpha": np.ones(2), "theta": np.full(2, 1e12),
+                "tau_crit": np.full(2, 0.5), "tau_surplus": np.full(2, 1.5), "r_min": np.zeros(2, np.int32),
+                "r_init": np.ones(2, np.int32)}
+        slo = {"ttft_ms": np.full(2, 1e9), "tpot_ms": np.full(2, 1e9), "e2e_ms": np.full(2, 1e9),
+               "attain_q": np.full(2, 0.95), "reliability": np.full(2, 0.9)}
+        svc = {"prefill_us": np.full(2, 1000, np.uint32), "decode_us": np.full(2, 10000, np.uint32)}
+        table = {"arrival_ms": np.zeros(3, np.int64), "model": np.zeros(3, np.uint8), "prompt": np.ones(3, np.uint16),
+                 "output": np.full(3, 24, np.uint16)}
+        sc = {"trace": np.zeros(1, np.uint32), "max_moves": np.ones(1, np.uint32), "theta_scale": np.ones(1),
+              "tau_crit_override": -np.ones(1)}
+        n = _check(lib, f"hand-cap{r_cap}", cfg, [table], prof, slo, svc, sc, spr=1, r_cap=r_cap)
+        assert n == (2 if r_cap == 3 else 1)
+
+
+def test_model_counts(lib):
+    for M in (1, 17, 64):
+        w = tg.Workload(name=f"m{M}", n_traces=1, model_classes=[["7B", "13B", "34B", "70B"][m % 4] for m in range(M)],
+                        interactive=[m % 2 == 0 for m in range(M)], r_init=[2] * M, budget=2 * M + 3,
+                        window_ms=500, duration_ms=600_000, process="mmpp2", rate=[0.8] * M,
+                        proc_params={"mmpp_mult": 6.0, "mmpp_dwell_s": 60.0}, seed=60 + M)
+        tables = [w.requests(0)]
+        rng = np.random.default_rng(M)
+        say(f"M {M}: {len(tables[0]['arrival_ms'])} requests")
+        _check(lib, f"M{M}", w.trace_cfg(), tables, w.profile_columns(1), w.slo_columns(1), w.service_columns(1),
+               _scenarios(rng, 4, 1))
+
+
+def test_argument_errors(lib):
+    tre, device, torch = lib
+    w = tg.standard(0)
+    tables = [w.requests(0)]
+    svc = np.zeros(3, tre.SERVICE_DTYPE)
+    for k in tre.SERVICE_DTYPE.names:
+        svc[k] = w.service_columns(1)[k]
+    slo = np.zeros(3, tre.SLO_DTYPE)
+    for k in tre.SLO_DTYPE.names:
+        slo[k] = w.slo_columns(1)[k]
+    cfg = w.trace_cfg()
+    rq, keep = tre.loop_requests(tables, 3, svc, slo)
+    prof = tre.pack(w.profile_columns(1), tre.PROFILE_DTYPE)
+    sc = tre.pack(_scenarios(np.random.default_rng(0), 2, 1), tre.SCENARIO_DTYPE)
+    out = tre.ctl_outputs(_Ev(1, 3, 600), 2, 4)
+    stats = torch.zeros(2 * 3 * 32, dtype=torch.uint8, device="cuda")
+    ws = torch.empty(64, dtype=torch.uint8, device="cuda")
+    with pytest.raises(tre.TreError) as e:
+        tre.tre_loop(cfg, 1, rq, prof, sc, out, stats, ws)
+    assert e.value.code == tre.TRE_ENOMEM
+    bad, keep2 = tre.loop_requests(tables, 3, svc, slo, slots_per_replica=0)
+    with pytest.raises(tre.TreError) as e:
+        tre.tre_loop_workspace_size(cfg, bad, 2)
+    assert e.value.code == tre.TRE_EINVAL
