@@ -81,6 +81,10 @@ def main():
     ap.add_argument("--threads", type=int, default=None)
     ap.add_argument("--actuation", action="store_true",
                     help="wake/sleep delays, 1-2 GPU footprints and vetoes (tre_sweep_act)")
+    ap.add_argument("--loop", action="store_true",
+                    help="time the closed-loop replay (tre_loop) over the workload's request tables instead")
+    ap.add_argument("--loop-cpu-scenarios", type=int, default=16,
+                    help="scenarios replayed by the oracle in the --loop CPU leg")
     ap.add_argument("--calibrate", action="store_true",
                     help="time the calibration sweep (tre_eval_tss + tre_calibrate) instead")
     ap.add_argument("--copy-calib-gb", type=float, default=0.0,
@@ -107,6 +111,8 @@ def main():
     sc_cols = w.scenario_columns()
     n_sc = len(sc_cols["trace"])
 
+    if args.loop:
+        return loop_main(args, w, tre, torch, np)
     t0 = time.time()
     dt = device.upload(w, threads=args.threads, log=log)
     log(f"resident: {dt.n_events} events, {dt.stored_bytes / 1e9:.1f} GB stored ({time.time() - t0:.1f} s)")
@@ -223,6 +229,149 @@ def main():
 
 
 CALIB_KERNELS = ("tss_stream", "calib_fill", "calib_join", "calib_judge", "calib_fit")
+
+
+def loop_main(args, w, tre, torch, np):
+    """One step = tre_loop over every scenario of the workload: each model's
+    requests served on its replicas' slots, the controller's moves changing
+    them, the TSS from the events this service produces. The request tables
+    (the same arrivals and lengths as the workload's traces) are generated
+    on host threads and copied to HBM before the timed region. Algorithmic
+    bytes per launch: 12 per request of each scenario's trace (arrival,
+    prompt and output lengths read once); the kernel is bound by each
+    scenario's sequential chain of windows, not by bytes."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    T, M = w.n_traces, w.n_models
+    n_workers = max(1, min(CPU_WORKERS, os.cpu_count() or 1))
+    t0 = time.time()
+    with ThreadPoolExecutor(max_workers=n_workers) as pool:
+        tables = list(pool.map(w.requests, range(T)))
+    svc = np.zeros(T * M, tre.SERVICE_DTYPE)
+    for k, v in w.service_columns().items():
+        svc[k] = v
+    slo = np.zeros(T * M, tre.SLO_DTYPE)
+    for k, v in w.slo_columns().items():
+        slo[k] = v
+    rq, keep = tre.loop_requests(tables, M, svc, slo)
+    n_req_trace = np.array([len(tb["arrival_ms"]) for tb in tables], np.int64)
+    log(f"request tables: {int(n_req_trace.sum())} requests in {T} traces ({time.time() - t0:.1f} s)")
+    cfg = w.trace_cfg()
+    from paper_2609_29160_amd import device
+    prof = device.profiles(w)
+    sc_cols = w.scenario_columns()
+    n_sc = len(sc_cols["trace"])
+    sc = tre.pack(sc_cols, tre.SCENARIO_DTYPE)
+    nW = w.n_windows
+    n_ticks = sum(1 for x in range(nW) if ((x + 1) * w.window_ms) % cfg["fast_period_ms"] == 0
+                  or ((x + 1) * w.window_ms) % cfg["slow_period_ms"] == 0)
+    move_cap = max(1, n_ticks * int(np.max(sc_cols["max_moves"])))
+
+    class _Shape:
+        n_models = M
+
+    out = tre.ctl_outputs(_Shape(), n_sc, move_cap)
+    stats = torch.zeros(n_sc * M * tre.LOOP_STATS_DTYPE.itemsize, dtype=torch.uint8, device="cuda")
+    ws = torch.empty(tre.tre_loop_workspace_size(cfg, rq, n_sc), dtype=torch.uint8, device="cuda")
+    log(f"closed loop: {n_sc} scenarios, workspace {ws.numel() / 1e9:.2f} GB")
+    for _ in range(args.warmup):
+        tre.tre_loop(cfg, T, rq, prof, sc, out, stats, ws)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    tre.tre_set_timing(True)
+    tre.tre_kernel_time("loop_replay")
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(args.steps):
+        tre.tre_loop(cfg, T, rq, prof, sc, out, stats, ws)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    tre.tre_set_timing(False)
+    step_ms = e0.elapsed_time(e1) / args.steps
+    k_ms, k_n = tre.tre_kernel_time("loop_replay")
+    kern_ms = k_ms / max(k_n, 1)
+    overflow = int(ws[:8].cpu().numpy().view(np.uint64)[0])
+    logical = int(sum(int(n_req_trace[int(t)]) for t in sc_cols["trace"]))
+    alg = 12 * logical
+    log(f"step {step_ms:.3f} ms; loop_replay {kern_ms:.3f} ms; events beyond the ring {overflow}")
+    cpu = parity = None
+    if not args.no_cpu:
+        cpu, parity = loop_cpu_leg(w, tables, sc_cols, out, stats, move_cap, args.loop_cpu_scenarios, n_workers, tre)
+    result = {
+        "metric": "requests/sec through the closed-loop replay (1 GPU)",
+        "value": round(logical / (step_ms / 1e3), 1),
+        "unit": "requests/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(step_ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f64",
+        "data": "synthetic (seeded generator; the paper's traces are not available)",
+        "config": {"workload": w.name, "traces": T, "scenarios": n_sc, "models": M, "window_ms": w.window_ms,
+                   "duration_s": w.duration_ms // 1000, "requests": int(n_req_trace.sum()), "logical_requests": logical,
+                   "slots_per_replica": 8, "r_cap": 16, "mode": "closed loop"},
+        "roofline": {"bound": "hbm", "achieved": round(alg / (kern_ms / 1e3) / 1e9, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(alg / (kern_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": "loop_replay", "kernel_ms": round(kern_ms, 4), "alg_bytes_per_launch": alg},
+        "events_beyond_ring": overflow,
+        "cpu_baseline": cpu, "parity": parity,
+    }
+    print(json.dumps(result), flush=True)
+
+
+def loop_cpu_leg(w, tables, sc_cols, out, stats, move_cap, n_sample, n_workers, tre):
+    """The oracle's closed-loop replay of the first n_sample scenarios on a
+    pool of host threads (one scenario per call), timed like the other CPU
+    legs; the GPU's moves, replicas and latency outcomes of those scenarios
+    must equal the oracle's."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    import numpy as np
+
+    import oracle as O
+
+    o = O.get()
+    M = w.n_models
+    cfg = w.trace_cfg()
+    prof_all = O.pack_profiles(w.profile_columns())
+    slo_all = O.pack_slo(w.slo_columns())
+    svc_all = O.pack_svc(w.service_columns())
+    sc_all = O.pack_scenarios(sc_cols)
+    sample = list(range(min(n_sample, len(sc_all))))
+
+    def one(s):
+        c0 = time.thread_time()
+        t = int(sc_all[s]["trace"])
+        r = o.loop(cfg, prof_all[t * M:(t + 1) * M], sc_all[s:s + 1], slo_all[t * M:(t + 1) * M],
+                   svc_all[t * M:(t + 1) * M], tables[t], move_cap=move_cap)
+        return r, time.thread_time() - c0
+
+    t0 = time.perf_counter()
+    with ThreadPoolExecutor(max_workers=n_workers) as pool:
+        results = list(pool.map(one, sample))
+    wall = time.perf_counter() - t0
+    cpu_s = sum(c for _, c in results)
+    n_moves = out["n_moves"].cpu().numpy()
+    r_final = out["r_final"].cpu().numpy()
+    r_windows = out["r_windows"].cpu().numpy()
+    moves = tre.unpack_moves(out["moves"]).reshape(-1, move_cap)
+    st = stats.cpu().numpy().view(tre.LOOP_STATS_DTYPE).reshape(-1, M)
+    bad = 0
+    reqs = 0
+    for s, (r, _) in zip(sample, results):
+        reqs += len(tables[int(sc_all[s]["trace"])]["arrival_ms"])
+        k = min(int(n_moves[s]), move_cap)
+        ok = int(n_moves[s]) == r["n_moves"] and np.array_equal(r_final[s], r["r_final"]) and \
+            np.array_equal(r_windows[s], r["r_windows"]) and \
+            all(np.array_equal(moves[s][:k][f], r["moves"][:k][f]) for f in ("window", "path", "receiver", "donor")) and \
+            all(np.array_equal(st[s][f], r["stats"][f]) for f in tre.LOOP_STATS_DTYPE.names)
+        bad += 0 if ok else 1
+    cpu = {"value": round(reqs / wall, 1), "unit": "requests/s", "cores": n_workers, "kind": "oracle",
+           "sample": f"{len(sample)} of {len(sc_all)} scenarios ({reqs} requests): {wall:.1f} s wall on {n_workers} "
+                     f"host threads (one scenario per oracle call), {cpu_s:.1f} s of their CPU time",
+           "one_core_value": round(reqs / cpu_s, 1)}
+    parity = {"scenarios_checked": len(sample), "mismatches": bad, "bit_exact": bad == 0}
+    log(f"cpu oracle (closed loop): {cpu['value']:.3g} requests/s on {n_workers} threads; parity {parity}")
+    return cpu, parity
 
 
 def calibrate_main(args, w, dt, device, tre, torch, np):
