@@ -403,9 +403,13 @@ typedef struct {
   int64_t e2e_sum, e2e_max;                     /* over judged requests, ms */
 } tre_loop_stats;                               /* 32 bytes */
 
-/* Workspace bytes of tre_loop: per scenario and model the slots
-   (min(r_cap, budget) * slots_per_replica * 8 B) and a ring of future
-   windows sized from the declared bounds, plus 256. */
+/* Workspace bytes of tre_loop: 256, plus per scenario and model a ring of
+   16-byte tallies of future windows, its length the power of two that
+   covers the longest service the declared bounds allow (in windows, + 2).
+   TRE_EINVAL when n_models * (min(r_cap, budget) * slots_per_replica,
+   rounded up to 4, + 64) * 4 bytes exceed the 160 KiB of LDS one
+   scenario's workgroup may use; TRE_ERANGE when duration_ms plus that
+   longest service reaches 2^31 ms. */
 int tre_loop_workspace_size(const tre_trace_cfg* cfg, const tre_loop_requests* rq, uint32_t n_scenarios,
                             size_t* bytes);
 

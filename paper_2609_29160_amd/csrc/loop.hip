@@ -13,16 +13,22 @@
 // smoothing of Section "Smoothing, Normalization, and Calibration".
 //
 // Kernel
-//   loop_replay  one wave per scenario, lane = model, windows in order. A
-//                lane keeps its model's slot free times and a ring of the
-//                future windows' tallies (prompt and output tokens, finishes
-//                of requests already started) in the workspace; per window
-//                it takes its arrivals, starts requests FCFS on the slot that
-//                frees first while the start falls in the window, writes each
-//                started request's events into the ring, reads the window's
-//                tallies and evaluates Eq. (1) and the smoothing in fp64; at
-//                a tick the wave decides the moves (ballots over lanes) and
-//                the receiver and donor lanes change their slots.
+//   loop_replay  one wave per scenario (one workgroup), lane = model,
+//                windows in order. Its LDS holds each lane's slot free
+//                times and a ring of the next kNear windows' tallies
+//                (prompt and output tokens, finishes of requests already
+//                started); tallies further ahead go to a ring in HBM with
+//                fire-and-forget atomics and are moved into LDS one window
+//                before they can be needed. Per window a lane takes its
+//                arrivals, starts requests FCFS on the slot that frees first
+//                while the start falls in the window, adds each started
+//                request's events to the rings, reads the window's tallies
+//                and evaluates Eq. (1) and the smoothing in fp64; at a tick
+//                the wave decides the moves (ballots over lanes) and the
+//                receiver and donor lanes change their slots. Which of
+//                several equally early slots a request takes, and where a
+//                removed slot's place goes, changes no output: only the
+//                multiset of free times matters.
 #include <hip/hip_runtime.h>
 
 #include <math.h>
@@ -40,12 +46,16 @@ using tre_internal::LaunchTimer;
 
 namespace {
 
-constexpr int kLoopWaves = 4;  // scenarios per workgroup
+constexpr int kNear = 16;  // windows ahead whose tallies sit in LDS (power of two)
+constexpr int kStage = 8;  // requests per lane staged in LDS for the starts
+constexpr uint32_t kNone = 0xffffffffu;
+constexpr int64_t kNever = INT64_MAX;
+constexpr int kLdsMax = 160 * 1024;
 
-struct RingCell {         // tallies of one future window of one model
-  uint32_t p, d;          // prompt / output tokens of its PREFILL / DECODE events
-  uint32_t n_fin, pad;    // FINISH events in it
-  uint64_t e_fin;         // sum over them of (window end - finish time)
+struct FarCell {    // tallies of one window of one model, beyond the LDS ring
+  uint32_t p, d;    // prompt / output tokens of its PREFILL / DECODE events
+  uint32_t n_fin;   // FINISH events in it
+  uint32_t e_fin;   // sum over them of (window end - finish time)
 };
 
 struct LoopParams {
@@ -63,8 +73,7 @@ struct LoopParams {
   int64_t* r_windows;
   tre_loop_stats* stats;
   double* tss64;                // [scenario][window][model] or NULL
-  int64_t* slots;               // [scenario][model][slot_cap]
-  RingCell* ring;               // [scenario][model][ring_len]
+  FarCell* far;                 // [scenario][ring_len][model]
   unsigned long long* overflow; // events beyond the ring (declared bounds exceeded)
   uint32_t move_cap;
   uint32_t n_sc;
@@ -75,12 +84,15 @@ struct LoopParams {
   int32_t r_cap;
   int32_t pchunk;
   int32_t dchunk;
-  int32_t slot_cap;
-  uint32_t ring_len;            // power of two
-  int64_t window_ms;
-  int64_t duration_ms;
-  int64_t n_windows;
-  int64_t fast_w, slow_w;       // periods in windows
+  int32_t slot_cap;             // multiple of 4
+  uint64_t wmagic;              // x / window_ms == (x * wmagic) >> wshift for x < 2^31
+  int32_t wshift;
+  int32_t r_hi;                 // min(r_cap, budget): replicas the slot array holds
+  uint32_t ring_len;            // power of two, >= 2 * kNear
+  int32_t window_ms;
+  int32_t duration_ms;          // duration + longest service < 2^31
+  int32_t n_windows;
+  int32_t fast_w, slow_w;       // periods in windows
 };
 
 __device__ __forceinline__ int64_t ceil_ms(int64_t tokens, uint32_t us) {
@@ -116,12 +128,68 @@ __device__ __forceinline__ double lane_f64(double x, int l) {
   return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
 }
 
+// A lane's slot free times in LDS as a binary min-heap (node i at h[i * M]);
+// only the multiset of free times matters, so the heap order is free.
+struct Heap {
+  uint32_t* h;
+  int M;
+
+  __device__ uint32_t& at(int i) const { return h[i * M]; }
+
+  // the root (the smallest) replaced by v, n nodes
+  __device__ void replace_top(int n, uint32_t v) const {
+    int i = 0;
+    for (;;) {
+      int c = 2 * i + 1;
+      if (c >= n) break;
+      uint32_t cv = at(c);
+      if (c + 1 < n) {
+        const uint32_t c2 = at(c + 1);
+        if (c2 < cv) {
+          cv = c2;
+          ++c;
+        }
+      }
+      if (cv >= v) break;
+      at(i) = cv;
+      i = c;
+    }
+    at(i) = v;
+  }
+
+  // v added to n nodes
+  __device__ void push(int n, uint32_t v) const {
+    int i = n;
+    while (i > 0) {
+      const int par = (i - 1) >> 1;
+      const uint32_t pv = at(par);
+      if (pv <= v) break;
+      at(i) = pv;
+      i = par;
+    }
+    at(i) = v;
+  }
+};
+
+__device__ __forceinline__ void lds_add(uint32_t* a, uint32_t v) {
+  __hip_atomic_fetch_add(a, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+__device__ __forceinline__ void far_add(uint32_t* a, uint32_t v) {
+  __hip_atomic_fetch_add(a, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t far_load(uint32_t* a) {
+  return __hip_atomic_load(a, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void far_store(uint32_t* a, uint32_t v) {
+  __hip_atomic_store(a, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 __global__ void zero_u64(unsigned long long* x) { *x = 0ull; }
 
-__global__ __launch_bounds__(64 * kLoopWaves) void loop_replay(LoopParams p) {
-  const int lane = threadIdx.x & 63;
-  const uint32_t s = blockIdx.x * kLoopWaves + (threadIdx.x >> 6);
-  if (s >= p.n_sc) return;  // whole wave
+__global__ __launch_bounds__(64) void loop_replay(LoopParams p) {
+  extern __shared__ __align__(16) uint32_t lds[];
+  const int lane = threadIdx.x;
+  const uint32_t s = blockIdx.x;
   const int M = p.M;
   const bool act = lane < M;
   const int mc = act ? lane : 0;
@@ -133,22 +201,67 @@ __global__ __launch_bounds__(64 * kLoopWaves) void loop_replay(LoopParams p) {
   const tre_service sv = p.svc[tm];
   const double theta_eff = pr.theta * sc.theta_scale;
   const double tau_c = sc.tau_crit_override >= 0.0 ? sc.tau_crit_override : pr.tau_crit;
-  const int64_t W = p.window_ms, dur = p.duration_ms;
+  const int32_t W = p.window_ms, dur = p.duration_ms;
   const uint32_t L = p.ring_len;
+  const int spr = p.spr;
+  const int64_t p_full = ceil_ms(p.pchunk, sv.prefill_us), d_full = ceil_ms(p.dchunk, sv.decode_us);
+  const Heap slot{lds + mc, M};
+  uint32_t* near = lds + p.slot_cap * M + mc;  // field f of ring cell c at near[(f * kNear + c) * M]
+  // requests sbase .. sbase + kStage - 1: arrival (ms, at most the duration)
+  // at stg[2 * e * M], prompt | output << 16 at stg[(2 * e + 1) * M]
+  int32_t* stg = (int32_t*)(lds + (p.slot_cap + 4 * kNear) * M + mc);
+  FarCell* far = p.far + (uint64_t)s * L * M + mc;  // cell c at far[c * M]
   // initial replicas within the slot array (min(r_cap, budget) replicas)
-  const int r_hi = p.slot_cap / p.spr;
+  const int r_hi = p.r_hi;
   int R = act ? (pr.r_init < 0 ? 0 : (pr.r_init > r_hi ? r_hi : pr.r_init)) : 0;
   int rsum = R;
   for (int o = 32; o > 0; o >>= 1) rsum += __shfl_xor(rsum, o);
   int pool = p.budget - rsum;
-  int64_t* slot = p.slots + ((uint64_t)s * M + mc) * p.slot_cap;
-  RingCell* ring = p.ring + ((uint64_t)s * M + mc) * L;
   if (act) {
-    for (uint32_t i = 0; i < L; ++i) ring[i] = RingCell{0u, 0u, 0u, 0u, 0ull};
-    for (int i = 0; i < R * p.spr; ++i) slot[i] = 0;
+    for (int i = 0; i < 4 * kNear; ++i) near[i * M] = 0u;
+    for (int i = 0; i < R * spr; ++i) slot.at(i) = 0u;  // R <= r_hi here; equal keys form a heap
+    for (uint32_t c = 0; c < L; ++c) {
+      FarCell* fc = far + (uint64_t)c * M;
+      far_store(&fc->p, 0u);
+      far_store(&fc->d, 0u);
+      far_store(&fc->n_fin, 0u);
+      far_store(&fc->e_fin, 0u);
+    }
   }
+  // slots of R replicas: R stays within r_hi when the initial replicas fit
+  // the budget; the bound keeps other inputs inside the slot array
+  auto nslots = [&](int r) { return (r < r_hi ? r : r_hi) * spr; };
+  uint32_t bf = act && nslots(R) > 0 ? 0u : kNone;  // earliest slot free time (the heap's root)
+  const uint64_t wmagic = p.wmagic;
+  const int wshift = p.wshift;
+  auto win = [&](uint32_t x) { return (int32_t)((x * wmagic) >> wshift); };  // x / W for x < 2^31
   const int64_t q1 = act ? p.req_off[tm + 1] : 0;
   int64_t next_arr = act ? p.req_off[tm] : 0, next_start = next_arr;
+  // arrival times of requests next_arr .. next_arr + 3 (kNever past the table)
+  int64_t a0 = next_arr < q1 ? p.arrival[next_arr] : kNever;
+  int64_t a1 = next_arr + 1 < q1 ? p.arrival[next_arr + 1] : kNever;
+  int64_t a2 = next_arr + 2 < q1 ? p.arrival[next_arr + 2] : kNever;
+  int64_t a3 = next_arr + 3 < q1 ? p.arrival[next_arr + 3] : kNever;
+  // the next kStage requests to start, fetched together (one wait per kStage starts)
+  int64_t sbase = next_start;
+  auto stage = [&](int64_t from) {
+    int64_t av[kStage];
+    uint32_t pv[kStage];
+#pragma unroll
+    for (int e = 0; e < kStage; ++e) {
+      const bool in = from + e < q1;
+      av[e] = in ? p.arrival[from + e] : kNever;
+      pv[e] = in ? (uint32_t)p.prompt[from + e] | (uint32_t)p.output[from + e] << 16 : 0u;
+    }
+#pragma unroll
+    for (int e = 0; e < kStage; ++e) {
+      stg[2 * e * M] = (int32_t)(av[e] < (int64_t)dur ? (av[e] > INT32_MIN ? av[e] : INT32_MIN) : dur);
+      stg[(2 * e + 1) * M] = (int32_t)pv[e];
+    }
+    sbase = from;
+  };
+  if (act) stage(next_start);
+  uint32_t fp = 0, fd = 0, fn = 0, fe = 0;  // far cell of window w - 1 + kNear, loaded at window w - 1
   int64_t cA = 0, cW = 0;  // active / waiting requests at the current window's start
   double S = 0.0;
   bool init = false;
@@ -158,104 +271,170 @@ __global__ __launch_bounds__(64 * kLoopWaves) void loop_replay(LoopParams p) {
   uint32_t nm = 0;
   const unsigned long long live = __ballot(act);
 
-  for (int64_t w = 0; w < p.n_windows; ++w) {
-    const int64_t w_end = (w + 1) * W;
+  for (int32_t w = 0; w < p.n_windows; ++w) {
+    const int32_t w_end = (w + 1) * W;
     uint32_t P = 0, D = 0;
     int64_t eA = 0, eW = 0, dA = 0, dW = 0;
     bool idle = true;
     if (act) {
-      RingCell* rc = ring + (w & (L - 1));
-      P = rc->p;
-      D = rc->d;
-      dA -= rc->n_fin;
-      eA -= (int64_t)rc->e_fin;
-      *rc = RingCell{0u, 0u, 0u, 0u, 0ull};
+      {  // the window's tallies from requests started before it
+        uint32_t* nc = near + (w & (kNear - 1)) * M;
+        P = nc[0];
+        D = nc[kNear * M];
+        const uint32_t nf = nc[2 * kNear * M], ef = nc[3 * kNear * M];
+        nc[0] = 0u;
+        nc[kNear * M] = 0u;
+        nc[2 * kNear * M] = 0u;
+        nc[3 * kNear * M] = 0u;
+        dA -= nf;
+        eA -= ef;
+      }
       // arrivals: a request waits from its arrival
-      while (next_arr < q1 && p.arrival[next_arr] < w_end) {
-        eW += w_end - p.arrival[next_arr];
+      while (a0 < w_end) {
+        eW += w_end - a0;
         dW += 1;
         ++n_arr;
         ++next_arr;
+        a0 = a1;
+        a1 = a2;
+        a2 = a3;
+        a3 = next_arr + 3 < q1 ? p.arrival[next_arr + 3] : kNever;
       }
       // starts, in arrival order, on the slot that frees first
-      const int ns = R * p.spr;
+      const int ns = nslots(R);
       while (next_start < next_arr && ns > 0) {
-        int best = 0;
-        int64_t bf = slot[0];
-        for (int k = 1; k < ns; ++k) {
-          const int64_t f = slot[k];
-          if (f < bf) {
-            bf = f;
-            best = k;
-          }
-        }
-        const int64_t a = p.arrival[next_start];
-        const int64_t st = a > bf ? a : bf;
+        if (next_start - sbase >= kStage) stage(next_start);
+        const int e = (int)(next_start - sbase);
+        const int64_t a = stg[2 * e * M];
+        const uint32_t po = (uint32_t)stg[(2 * e + 1) * M];
+        const int64_t st = a > (int64_t)bf ? a : (int64_t)bf;
         if (st >= w_end) break;  // capacity may change at the window's end
         // admission: waiting -> active
         eW -= w_end - st;
         dW -= 1;
         eA += w_end - st;
         dA += 1;
-        int64_t tt = st;
-        int64_t left = p.prompt[next_start];
-        while (left > 0) {
-          const int64_t ch = left < p.pchunk ? left : p.pchunk;
-          if (tt < dur) {
-            const int64_t wf = tt / W;
-            if (wf == w) P += (uint32_t)ch;
-            else if (wf - w < (int64_t)L) ring[wf & (L - 1)].p += (uint32_t)ch;
-            else ++overflow;
+        // tokens of field f (0 prompt, 1 output) counted in window x: this
+        // window's (registers), the next kNear - 1 (LDS) or further (HBM)
+        auto deliver = [&](int f, int32_t x, uint32_t v) {
+          const uint32_t ahead = (uint32_t)(x - w);
+          if (ahead == 0u) {
+            if (f == 0) P += v;
+            else D += v;
+          } else if (ahead < (uint32_t)kNear) {
+            lds_add(near + (f * kNear + (x & (kNear - 1))) * M, v);
+          } else if (ahead < L) {
+            far_add(&far[(uint64_t)(x & (L - 1)) * M].p + f, v);
+          } else {
+            ++overflow;
           }
-          tt += ceil_ms(ch, sv.prefill_us);
-          left -= ch;
+        };
+        // events come in time order (times below 2^31 within the declared
+        // bounds): xw is the window of the latest, acc the tokens gathered
+        // for it, delivered when a later event falls in another window
+        int32_t xw = w;
+        uint32_t xend = (uint32_t)w_end, acc = 0;
+        auto at_time = [&](int f, uint32_t x, uint32_t v) {  // x < duration
+          if (x >= xend) {
+            if (acc) deliver(f, xw, acc);
+            acc = 0;
+            xw = win(x);
+            xend = (uint32_t)(xw + 1) * (uint32_t)W;
+          }
+          acc += v;
+        };
+        const uint32_t udur = (uint32_t)dur;
+        uint32_t tt = (uint32_t)st;
+        {  // PREFILL events at the start of each chunk
+          const uint32_t n = po & 0xffffu, nf = n / (uint32_t)p.pchunk, rem = n - nf * (uint32_t)p.pchunk;
+          for (uint32_t j = 0; j < nf; ++j) {
+            if (tt < udur) at_time(0, tt, (uint32_t)p.pchunk);
+            tt += (uint32_t)p_full;
+          }
+          if (rem) {
+            if (tt < udur) at_time(0, tt, rem);
+            tt += (uint32_t)ceil_ms(rem, sv.prefill_us);
+          }
+          if (acc) deliver(0, xw, acc);
+          acc = 0;
         }
-        const int64_t out_tok = p.output[next_start];
-        left = out_tok;
-        int64_t t_first = -1, first_ch = 0;
-        while (left > 0) {
-          const int64_t ch = left < p.dchunk ? left : p.dchunk;
-          tt += ceil_ms(ch, sv.decode_us);
-          if (t_first < 0) {
-            t_first = tt;
-            first_ch = ch;
+        const uint32_t out_tok = po >> 16;
+        int64_t t_first = -1;
+        uint32_t first_ch = 0;
+        {  // DECODE events at the end of each chunk
+          const uint32_t nf = out_tok / (uint32_t)p.dchunk, rem = out_tok - nf * (uint32_t)p.dchunk;
+          const uint32_t t_rem = rem ? (uint32_t)ceil_ms(rem, sv.decode_us) : 0u;
+          if (out_tok) {
+            first_ch = nf ? (uint32_t)p.dchunk : rem;
+            t_first = (int64_t)tt + (nf ? d_full : (int64_t)t_rem);
           }
-          if (tt < dur) {
-            const int64_t wf = tt / W;
-            if (wf == w) D += (uint32_t)ch;
-            else if (wf - w < (int64_t)L) ring[wf & (L - 1)].d += (uint32_t)ch;
-            else ++overflow;
+          for (uint32_t j = 0; j < nf; ++j) {
+            tt += (uint32_t)d_full;
+            if (tt < udur) at_time(1, tt, (uint32_t)p.dchunk);
           }
-          left -= ch;
+          if (rem) {
+            tt += t_rem;
+            if (tt < udur) at_time(1, tt, rem);
+          }
+          if (acc) deliver(1, xw, acc);
+          acc = 0;
         }
-        if (tt < dur) {  // FINISH: active -> gone
-          const int64_t wf = tt / W;
-          if (wf == w) {
-            eA -= w_end - tt;
+        if (tt < udur) {  // FINISH: active -> gone
+          if (tt >= xend) {
+            xw = win(tt);
+            xend = (uint32_t)(xw + 1) * (uint32_t)W;
+          }
+          const uint32_t ahead = (uint32_t)(xw - w), e = xend - tt;
+          if (ahead == 0u) {
+            eA -= w_end - (int64_t)tt;
             dA -= 1;
-          } else if (wf - w < (int64_t)L) {
-            RingCell& c = ring[wf & (L - 1)];
-            c.n_fin += 1;
-            c.e_fin += (uint64_t)((wf + 1) * W - tt);
+          } else if (ahead < (uint32_t)kNear) {
+            uint32_t* nc = near + (xw & (kNear - 1)) * M;
+            lds_add(nc + 2 * kNear * M, 1u);
+            lds_add(nc + 3 * kNear * M, e);
+          } else if (ahead < L) {
+            FarCell* fc = far + (uint64_t)(xw & (L - 1)) * M;
+            far_add(&fc->n_fin, 1u);
+            far_add(&fc->e_fin, e);
           } else {
             ++overflow;
           }
           if (t_first >= 0) {  // judged as in the calibration sweep
-            const int64_t ttft = t_first - a, e2e = tt - a, after = out_tok - first_ch;
+            const int64_t ttft = t_first - a, e2e = (int64_t)tt - a, after = (int64_t)out_tok - first_ch;
             bool good = (double)ttft <= sl.ttft_ms && (double)e2e <= sl.e2e_ms;
-            if (after > 0) good = good && (double)(tt - t_first) / (double)after <= sl.tpot_ms;
+            if (after > 0) good = good && (double)((int64_t)tt - t_first) / (double)after <= sl.tpot_ms;
             ++n_done;
             n_ok += good ? 1u : 0u;
             e2e_sum += e2e;
             e2e_max = e2e > e2e_max ? e2e : e2e_max;
           }
         }
-        slot[best] = tt;
+        slot.replace_top(ns, tt);  // tt >= st >= the root
+        bf = slot.at(0);
         ++n_start;
         ++next_start;
       }
+      {  // far tallies: those of window w - 1 + kNear into LDS, then fetch those of w + kNear
+        if (fp | fd | fn | fe) {
+          uint32_t* nc = near + ((w - 1) & (kNear - 1)) * M;
+          if (fp) lds_add(nc, fp);
+          if (fd) lds_add(nc + kNear * M, fd);
+          if (fn) lds_add(nc + 2 * kNear * M, fn);
+          if (fe) lds_add(nc + 3 * kNear * M, fe);
+          FarCell* fc = far + (uint64_t)((uint32_t)(w - 1 + kNear) & (L - 1)) * M;
+          far_store(&fc->p, 0u);
+          far_store(&fc->d, 0u);
+          far_store(&fc->n_fin, 0u);
+          far_store(&fc->e_fin, 0u);
+        }
+        FarCell* fc = far + (uint64_t)((uint32_t)(w + kNear) & (L - 1)) * M;
+        fp = far_load(&fc->p);
+        fd = far_load(&fc->d);
+        fn = far_load(&fc->n_fin);
+        fe = far_load(&fc->e_fin);
+      }
       // the window's tallies, Eq. (1) and the smoothing
-      const int64_t A_int = W * cA + eA, W_int = W * cW + eW;
+      const int64_t A_int = (int64_t)W * cA + eA, W_int = (int64_t)W * cW + eW;
       cA += dA;
       cW += dW;
       idle = P == 0 && D == 0 && A_int == 0 && W_int == 0;
@@ -313,20 +492,23 @@ __global__ __launch_bounds__(64 * kLoopWaves) void loop_replay(LoopParams p) {
         if (d < 0) break;
         used |= 1ull << d;
         if (lane == d) {  // the replica's slots that free first leave
-          for (int q = 0; q < p.spr; ++q) {
-            const int ns = R * p.spr - q;
-            if (ns <= 0) break;
-            int lo = 0;
-            for (int x = 1; x < ns; ++x)
-              if (slot[x] < slot[lo]) lo = x;
-            for (int x = lo; x + 1 < ns; ++x) slot[x] = slot[x + 1];
+          int ns = nslots(R);
+          const int keep = R > 0 ? nslots(R - 1) : 0;
+          while (ns > keep) {
+            --ns;
+            if (ns > 0) slot.replace_top(ns, slot.at(ns));
           }
           if (R > 0) R -= 1;
+          bf = ns > 0 ? slot.at(0) : kNone;
         }
       }
       used |= 1ull << r;
       if (lane == r) {  // the new replica's slots are free from the window's end
-        for (int q = 0; q < p.spr; ++q) slot[R * p.spr + q] = w_end;
+        if (R < r_hi) {
+          const int ns = nslots(R);
+          for (int q = 0; q < spr; ++q) slot.push(ns + q, (uint32_t)w_end);
+          bf = slot.at(0);
+        }
         R += 1;
       }
       if (lane == 0 && nm < p.move_cap) {
@@ -373,8 +555,19 @@ uint32_t ring_len(const tre_trace_cfg* cfg, const tre_loop_requests* rq) {
   return L;
 }
 
+int r_hi(const tre_trace_cfg* cfg, const tre_loop_requests* rq) {
+  return rq->r_cap < cfg->budget ? rq->r_cap : cfg->budget;
+}
+
+// slots per lane, rounded up to whole 16-byte groups
 int slot_cap(const tre_trace_cfg* cfg, const tre_loop_requests* rq) {
-  return (rq->r_cap < cfg->budget ? rq->r_cap : cfg->budget) * rq->slots_per_replica;
+  return (r_hi(cfg, rq) * rq->slots_per_replica + 3) & ~3;
+}
+
+// LDS bytes of one scenario: slots, the four planes of the near ring, the
+// staged requests (arrival, prompt and output)
+size_t lds_bytes(const tre_trace_cfg* cfg, const tre_loop_requests* rq) {
+  return ((size_t)slot_cap(cfg, rq) + 4 * kNear + 2 * kStage) * cfg->n_models * 4;
 }
 
 int check_loop_args(const tre_trace_cfg* cfg, const tre_loop_requests* rq) {
@@ -385,10 +578,16 @@ int check_loop_args(const tre_trace_cfg* cfg, const tre_loop_requests* rq) {
     return fail(TRE_EINVAL, "tre_loop: bad window, duration or periods");
   if (cfg->n_models < 1 || cfg->n_models > TRE_MAX_MODELS || cfg->budget < 0)
     return fail(TRE_EINVAL, "tre_loop: n_models outside [1, %d] or negative budget", TRE_MAX_MODELS);
-  if (rq->slots_per_replica < 1 || rq->r_cap < 1 || rq->prefill_chunk < 1 || rq->decode_chunk < 1)
-    return fail(TRE_EINVAL, "tre_loop: slots_per_replica, r_cap and chunks must be positive");
+  if (rq->slots_per_replica < 1 || rq->r_cap < 1 || rq->prefill_chunk < 1 || rq->decode_chunk < 1 ||
+      rq->slots_per_replica > 4096 || rq->r_cap > 4096)
+    return fail(TRE_EINVAL, "tre_loop: slots_per_replica, r_cap and chunks must be positive (and at most 4096)");
   if (max_service_ms(rq) / cfg->window_ms > (1 << 24))
     return fail(TRE_ERANGE, "tre_loop: a request may span more than 2^24 windows");
+  if (cfg->duration_ms + max_service_ms(rq) + 2 * cfg->window_ms >= (1ll << 31))
+    return fail(TRE_ERANGE, "tre_loop: duration plus the longest service must stay below 2^31 ms");
+  if (lds_bytes(cfg, rq) > (size_t)kLdsMax)
+    return fail(TRE_EINVAL, "tre_loop: %d models x %d slots need %zu bytes of LDS (at most %d)", cfg->n_models,
+                r_hi(cfg, rq) * rq->slots_per_replica, lds_bytes(cfg, rq), kLdsMax);
   return TRE_OK;
 }
 
@@ -400,8 +599,7 @@ extern "C" int tre_loop_workspace_size(const tre_trace_cfg* cfg, const tre_loop_
   if (!bytes) return fail(TRE_EINVAL, "tre_loop_workspace_size: NULL bytes");
   const int rc = check_loop_args(cfg, rq);
   if (rc) return rc;
-  const uint64_t per = (uint64_t)slot_cap(cfg, rq) * 8 + (uint64_t)ring_len(cfg, rq) * sizeof(RingCell);
-  *bytes = (size_t)(256 + (uint64_t)n_scenarios * cfg->n_models * per);
+  *bytes = (size_t)(256 + (uint64_t)n_scenarios * cfg->n_models * ring_len(cfg, rq) * sizeof(FarCell));
   return TRE_OK;
 }
 
@@ -427,8 +625,9 @@ extern "C" int tre_loop(const tre_trace_cfg* cfg, uint32_t n_traces, const tre_l
   const int scap = slot_cap(cfg, rq);
   char* base = (char*)ws;
   unsigned long long* overflow = (unsigned long long*)base;
-  int64_t* slots = (int64_t*)(base + 256);
-  RingCell* ring = (RingCell*)(base + 256 + (uint64_t)n_scenarios * M * scap * 8);
+  FarCell* far = (FarCell*)(base + 256);
+  const size_t lds = lds_bytes(cfg, rq);
+  HIP_TRY(hipFuncSetAttribute((const void*)loop_replay, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
   hipLaunchKernelGGL(zero_u64, dim3(1), dim3(1), 0, st, overflow);
   LoopParams lp{};
   lp.arrival = rq->arrival_ms;
@@ -445,8 +644,7 @@ extern "C" int tre_loop(const tre_trace_cfg* cfg, uint32_t n_traces, const tre_l
   lp.r_windows = out->r_windows;
   lp.stats = stats;
   lp.tss64 = tss64;
-  lp.slots = slots;
-  lp.ring = ring;
+  lp.far = far;
   lp.overflow = overflow;
   lp.move_cap = out->move_cap;
   lp.n_sc = n_scenarios;
@@ -458,15 +656,22 @@ extern "C" int tre_loop(const tre_trace_cfg* cfg, uint32_t n_traces, const tre_l
   lp.pchunk = rq->prefill_chunk;
   lp.dchunk = rq->decode_chunk;
   lp.slot_cap = scap;
+  lp.r_hi = r_hi(cfg, rq);
+  {  // x / W == (x * m) >> (32 + l) for x < 2^32, m = ceil(2^(32 + l) / W), 2^l >= W
+    int l = 0;
+    while ((1ll << l) < cfg->window_ms) ++l;
+    lp.wshift = 32 + l;
+    lp.wmagic = (uint64_t)(((1ull << (32 + l)) + (uint64_t)cfg->window_ms - 1) / (uint64_t)cfg->window_ms);
+  }
   lp.ring_len = L;
-  lp.window_ms = cfg->window_ms;
-  lp.duration_ms = cfg->duration_ms;
-  lp.n_windows = cfg->duration_ms / cfg->window_ms;
-  lp.fast_w = cfg->fast_period_ms / cfg->window_ms;
-  lp.slow_w = cfg->slow_period_ms / cfg->window_ms;
+  lp.window_ms = (int32_t)cfg->window_ms;
+  lp.duration_ms = (int32_t)cfg->duration_ms;
+  lp.n_windows = (int32_t)(cfg->duration_ms / cfg->window_ms);
+  // a period longer than the replay never ticks
+  lp.fast_w = (int32_t)std::min<int64_t>(cfg->fast_period_ms / cfg->window_ms, lp.n_windows + 1);
+  lp.slow_w = (int32_t)std::min<int64_t>(cfg->slow_period_ms / cfg->window_ms, lp.n_windows + 1);
   LaunchTimer lt("loop_replay", st);
-  hipLaunchKernelGGL(loop_replay, dim3((n_scenarios + kLoopWaves - 1) / kLoopWaves), dim3(64 * kLoopWaves), 0, st,
-                     lp);
+  hipLaunchKernelGGL(loop_replay, dim3(n_scenarios), dim3(64), lds, st, lp);
   lt.done();
   HIP_TRY(hipGetLastError());
   return TRE_OK;
