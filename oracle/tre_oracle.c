@@ -114,10 +114,12 @@ double oracle_smooth(double alpha, double raw, double s_prev) {
    splitting at window boundaries */
 static void integrate(int64_t* integ, int32_t M, int32_t m, int64_t window_ms, int64_t count,
                       int64_t from, int64_t to) {
+  const int64_t n_w = (to + window_ms - 1) / window_ms;  /* to <= duration: rows [0, n_w) exist */
   while (from < to) {
     int64_t w = from / window_ms;
     int64_t seg_end = (w + 1) * window_ms;
     if (seg_end > to) seg_end = to;
+    if (w < 0 || w >= n_w || seg_end <= from) break; /* never for valid input; keeps writes inside the rows */
     integ[w * M + m] += count * (seg_end - from);
     from = seg_end;
   }
