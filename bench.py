@@ -299,6 +299,10 @@ def loop_main(args, w, tre, torch, np):
     cpu = parity = None
     if not args.no_cpu:
         cpu, parity = loop_cpu_leg(w, tables, sc_cols, out, stats, move_cap, args.loop_cpu_scenarios, n_workers, tre)
+    if args.copy_calib_gb > 0:
+        del ws, out, stats, rq, keep
+        torch.cuda.empty_cache()
+        copy_calibration(args.copy_calib_gb, torch)
     result = {
         "metric": "requests/sec through the closed-loop replay (1 GPU)",
         "value": round(logical / (step_ms / 1e3), 1),
