@@ -50,8 +50,21 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-def kernel_sha() -> str:
-    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+def kernel_sha(src: str = None) -> str:
+    return hashlib.sha256(open(src or KERNEL_SRC, "rb").read()).hexdigest()[:16]
+
+
+def loop_traffic_for(workload_name: str):
+    """HBM bytes per loop_replay launch from committed counters taken on
+    this kernel source and workload; else None."""
+    try:
+        t = json.load(open(os.path.join(ROOT, "profiles", "loop_traffic.json")))
+    except (OSError, ValueError):
+        return None
+    src = os.path.join(ROOT, "paper_2609_29160_amd", "csrc", "loop.hip")
+    if t.get("kernel_sha") != kernel_sha(src) or t.get("workload") != workload_name:
+        return None
+    return t.get("traffic_bytes_per_launch", {}).get("loop_replay")
 
 
 def traffic_for(workload_name: str, events: int):
@@ -314,8 +327,8 @@ def loop_main(args, w, tre, torch, np):
                    "duration_s": w.duration_ms // 1000, "requests": int(n_req_trace.sum()), "logical_requests": logical,
                    "slots_per_replica": 8, "r_cap": 16, "mode": "closed loop"},
         "roofline": {"bound": "hbm", "achieved": round(alg / (kern_ms / 1e3) / 1e9, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(alg / (kern_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4), "traffic": None,
-                     "kernel": "loop_replay", "kernel_ms": round(kern_ms, 4), "alg_bytes_per_launch": alg},
+                     "unit": "GB/s", "frac": round(alg / (kern_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
+                     "traffic": loop_traffic_for(w.name) if T == 4096 else None, "kernel": "loop_replay", "kernel_ms": round(kern_ms, 4), "alg_bytes_per_launch": alg},
         "events_beyond_ring": overflow,
         "cpu_baseline": cpu, "parity": parity,
     }
