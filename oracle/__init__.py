@@ -23,12 +23,14 @@ _SRC = os.path.join(_HERE, "tre_oracle.c")
 _SRC_ACT = os.path.join(_HERE, "tre_oracle_act.c")  # control replay with the actuation model
 _SRC_CALIB = os.path.join(_HERE, "tre_oracle_calib.c")  # calibration sweep
 _SRC_LOOP = os.path.join(_HERE, "tre_oracle_loop.c")  # closed-loop replay
+_SRC_STAGE = os.path.join(_HERE, "tre_oracle_stage.c")  # stage-aware service shares
 _LIB = os.path.join(_HERE, "libtre_oracle.so")
 
 CFLAGS = ["-O2", "-fPIC", "-shared", "-ffp-contract=off", "-fno-fast-math", "-std=c11"]
 
 RESCUE, REBALANCE, POOL = 1, 2, 0xFF
 IDLE, INIT = 1, 2
+P_IDLE, P_INIT, D_IDLE, D_INIT = 1, 2, 4, 8  # stage-aware flags
 
 PROFILE_DTYPE = np.dtype([("w_p", "<f8"), ("w_q", "<f8"), ("alpha", "<f8"), ("theta", "<f8"),
                           ("tau_crit", "<f8"), ("tau_surplus", "<f8"), ("r_min", "<i4"),
@@ -56,7 +58,7 @@ def build(force: bool = True, src: str = _SRC, out: str = _LIB) -> str:
     The default library also holds the actuation-model replay and the
     calibration sweep; a library built from another base source (the
     pin-strength tests) does not."""
-    srcs = [src] + ([_SRC_ACT, _SRC_CALIB, _SRC_LOOP] if src == _SRC else [])
+    srcs = [src] + ([_SRC_ACT, _SRC_CALIB, _SRC_LOOP, _SRC_STAGE] if src == _SRC else [])
     stale = not os.path.exists(out) or any(os.path.getmtime(out) < os.path.getmtime(x) for x in srcs)
     if force or stale:
         tmp = f"{out}.{os.getpid()}.tmp"
@@ -96,6 +98,14 @@ class Oracle:
             L.oracle_loop.restype = ctypes.c_int
             L.oracle_loop.argtypes = ([i64, i64, i64, i64, i32, i32, vp, vp, vp, vp, i32, i32, i32, i32, vp, vp, vp, vp,
                                        vp, u32, vp, vp, vp, vp, vp, vp, vp, i64, vp, vp, vp, vp])
+        self.has_stage = hasattr(L, "oracle_stage_tss")
+        if self.has_stage:
+            L.oracle_stage_raw_prefill.restype = f64
+            L.oracle_stage_raw_prefill.argtypes = [f64, f64, i64, i64, i64]
+            L.oracle_stage_raw_decode.restype = f64
+            L.oracle_stage_raw_decode.argtypes = [i64, i64, i64]
+            L.oracle_stage_tss.restype = ctypes.c_int
+            L.oracle_stage_tss.argtypes = [i64, i32, i64, vp, vp, vp, vp, vp, vp, vp]
         self.L = L
         self.path = path
 
@@ -246,6 +256,28 @@ class Oracle:
         if want_events:
             out["events"] = {k: v[:out["n_events"]] for k, v in ev.items()}
         return out
+
+    # ------------------------------------------------------------ stage-aware
+    def stage_tss(self, tallies: Dict[str, np.ndarray], window_ms: int, prof: np.ndarray) -> Dict[str, np.ndarray]:
+        """Prefill- and decode-stage smoothed shares of one trace from its
+        window tallies (P, D, A_int, W_int, each [n_windows][M]): S
+        [n_windows][M][2] (prefill, decode), flags [n_windows][M]."""
+        prof = np.ascontiguousarray(prof, dtype=PROFILE_DTYPE)
+        cols = [np.ascontiguousarray(tallies[k], np.int64) for k in ("P", "D", "A_int", "W_int")]
+        nW, M = cols[0].shape
+        S = np.zeros((nW, M, 2), np.float64)
+        fl = np.zeros((nW, M), np.uint8)
+        rc = self.L.oracle_stage_tss(nW, M, window_ms, prof.ctypes.data, *[c.ctypes.data for c in cols],
+                                     S.ctypes.data, fl.ctypes.data)
+        if rc:
+            raise ValueError("oracle_stage_tss rejected its arguments")
+        return {"S": S, "flags": fl}
+
+    def stage_raw_prefill(self, w_p, w_q, P, W_int, window_ms) -> float:
+        return self.L.oracle_stage_raw_prefill(w_p, w_q, int(P), int(W_int), int(window_ms))
+
+    def stage_raw_decode(self, D, A_int, window_ms) -> float:
+        return self.L.oracle_stage_raw_decode(int(D), int(A_int), int(window_ms))
 
     # ----------------------------------------------------------- calibration
     def calib_requests(self, ev: Dict[str, np.ndarray], window_ms: int, duration_ms: int, slo: np.ndarray,
