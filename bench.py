@@ -98,6 +98,8 @@ def main():
                     help="time the closed-loop replay (tre_loop) over the workload's request tables instead")
     ap.add_argument("--loop-cpu-scenarios", type=int, default=16,
                     help="scenarios replayed by the oracle in the --loop CPU leg")
+    ap.add_argument("--stage", action="store_true",
+                    help="time the stage-aware shares (tre_eval_tss tallies + tre_stage_tss) instead")
     ap.add_argument("--calibrate", action="store_true",
                     help="time the calibration sweep (tre_eval_tss + tre_calibrate) instead")
     ap.add_argument("--copy-calib-gb", type=float, default=0.0,
@@ -131,6 +133,8 @@ def main():
     log(f"resident: {dt.n_events} events, {dt.stored_bytes / 1e9:.1f} GB stored ({time.time() - t0:.1f} s)")
     if args.calibrate:
         return calibrate_main(args, w, dt, device, tre, torch, np)
+    if args.stage:
+        return stage_main(args, w, dt, device, tre, torch, np)
     act_in = actuation_inputs(w) if args.actuation else None
     ev = device.load(dt, validate=True, budget=None if act_in is None else act_in["budget"])
     prof = device.profiles(w)
@@ -472,6 +476,144 @@ def calibrate_main(args, w, dt, device, tre, torch, np):
         del tss, out
         copy_calibration(args.copy_calib_gb, torch)
     ev.close()
+
+
+STAGE_KERNELS = ("tss_stream", "stage_tss")
+
+
+def stage_main(args, w, dt, device, tre, torch, np):
+    """One step = tre_eval_tss writing the per-cell tallies (prefill and
+    decode tokens, the active and waiting integrals), then tre_stage_tss
+    writing the prefill and decode shares (binary64) and their flags over
+    the whole resident workload. Algorithmic bytes per launch: tss_stream 12
+    per event + 24 per cell written; stage_tss 24 per cell read + 17 per
+    cell written."""
+    ev = device.load(dt, validate=True)
+    prof = device.profiles(w)
+    T, M, nW = ev.n_traces, ev.n_models, ev.n_windows
+    cells = T * M * nW
+    tal = tre.tss_outputs(ev, which=("prefill", "decode", "a_int", "w_int"))
+    out = tre.stage_outputs(ev, which=("stage64", "flags"))
+    log(f"stage shares: {T} traces, {dt.n_events} events, {cells} cells")
+
+    def step():
+        tre.tre_eval_tss(ev, prof, tal)
+        tre.tre_stage_tss(ev, prof, tal, out)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    tre.tre_set_timing(True)
+    for k in STAGE_KERNELS:
+        tre.tre_kernel_time(k)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    tre.tre_set_timing(False)
+    step_ms = e0.elapsed_time(e1) / args.steps
+    kms = {}
+    for k in STAGE_KERNELS:
+        tot, n = tre.tre_kernel_time(k)
+        kms[k] = tot / max(n, 1)
+    alg = {"tss_stream": ALG_BYTES_PER_EVENT * dt.n_events + 24 * cells, "stage_tss": 41 * cells}
+    kernels = {k: {"ms": round(kms[k], 4), "alg_bytes": alg[k],
+                   "gbs": round(alg[k] / (kms[k] / 1e3) / 1e9, 1) if kms[k] > 0 else None} for k in STAGE_KERNELS}
+    roofline = {"bound": "hbm", "achieved": kernels["stage_tss"]["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(kernels["stage_tss"]["gbs"] / HBM_PEAK_GBS, 4),
+                "traffic": stage_traffic_for(w.name, cells), "kernel": "stage_tss",
+                "kernel_ms": kernels["stage_tss"]["ms"], "alg_bytes_per_launch": alg["stage_tss"]}
+    log("kernels " + ", ".join(f"{k} {kms[k]:.3f} ms" for k in STAGE_KERNELS) + f"; step {step_ms:.3f} ms")
+    cpu = parity = None
+    if not args.no_cpu:
+        n_s = max(1, int(np.searchsorted(np.cumsum(dt.counts), CPU_EVENT_BUDGET // 3, side="right")))
+        cpu, parity = stage_cpu_leg(w, list(range(n_s)), out, args.threads)
+    result = {
+        "metric": "request-events/sec through TSS tallies + stage-aware shares (1 GPU)",
+        "value": round(dt.n_events / (step_ms / 1e3), 1),
+        "unit": "request-events/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(step_ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f64",
+        "data": "synthetic (seeded generator; the paper's traces are not available)",
+        "config": {"workload": w.name, "traces": T, "models": M, "window_ms": w.window_ms,
+                   "duration_s": w.duration_ms // 1000, "events": dt.n_events, "cells": cells, "mode": "stage"},
+        "roofline": roofline, "kernels": kernels, "cpu_baseline": cpu, "parity": parity,
+    }
+    print(json.dumps(result), flush=True)
+    if args.copy_calib_gb > 0:
+        del tal, out
+        torch.cuda.empty_cache()
+        copy_calibration(args.copy_calib_gb, torch)
+    ev.close()
+
+
+def stage_traffic_for(workload_name: str, cells: int):
+    """HBM bytes per stage_tss launch from committed counters taken on this
+    kernel source and workload; else None."""
+    try:
+        t = json.load(open(os.path.join(ROOT, "profiles", "stage_traffic.json")))
+    except (OSError, ValueError):
+        return None
+    src = os.path.join(ROOT, "paper_2609_29160_amd", "csrc", "stage.hip")
+    if t.get("kernel_sha") != kernel_sha(src) or t.get("workload") != workload_name or t.get("cells") != cells:
+        return None
+    return t.get("traffic_bytes_per_launch", {}).get("stage_tss")
+
+
+def stage_cpu_leg(w, sample, out, threads):
+    """The oracle's tallies and stage shares of the sample traces on a pool
+    of host threads; the GPU's shares (bit for bit) and flags of those
+    traces must equal the oracle's."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    import numpy as np
+
+    import oracle as O
+
+    o = O.get()
+    M = w.n_models
+    prof_all = O.pack_profiles(w.profile_columns(max(sample) + 1))
+    n_workers = max(1, min(CPU_WORKERS, os.cpu_count() or 1))
+
+    def one(ev, t):
+        c0 = time.thread_time()
+        p = prof_all[t * M:(t + 1) * M]
+        r = o.stage_tss(o.tss_trace(ev, w.window_ms, w.duration_ms, p), w.window_ms, p)
+        return r, time.thread_time() - c0
+
+    wall = cpu_s = 0.0
+    events = 0
+    bad = 0
+    batch = 4 * n_workers
+    with ThreadPoolExecutor(max_workers=n_workers) as pool:
+        for b0 in range(0, len(sample), batch):
+            tr = sample[b0:b0 + batch]
+            host = w.generate(tr[0], tr[-1] + 1, threads=threads)
+            evs = [host.trace(i) for i in range(len(tr))]
+            t0 = time.perf_counter()
+            results = list(pool.map(one, evs, tr))
+            wall += time.perf_counter() - t0
+            for ev, t, (rf, c) in zip(evs, tr, results):
+                cpu_s += c
+                events += len(ev["ts"])
+                g64 = out["stage64"][t].cpu().numpy()
+                gfl = out["flags"][t].cpu().numpy()
+                ok = np.array_equal(g64.view(np.uint64), rf["S"].view(np.uint64)) and np.array_equal(gfl, rf["flags"])
+                bad += 0 if ok else 1
+            del host, evs
+    cpu = {"value": round(events / wall, 1), "unit": "request-events/s", "cores": n_workers, "kind": "oracle",
+           "sample": f"{len(sample)} of {w.n_traces} traces ({events} events): {wall:.1f} s wall on {n_workers} "
+                     f"host threads (one trace per oracle call: tallies, TSS and stage shares), {cpu_s:.1f} s of "
+                     f"their CPU time",
+           "one_core_value": round(events / cpu_s, 1)}
+    parity = {"traces_checked": len(sample), "mismatches": bad, "bit_exact": bad == 0}
+    log(f"cpu oracle (stage shares): {cpu['value']:.3g} events/s on {n_workers} threads; parity {parity}")
+    return cpu, parity
 
 
 def copy_calibration(gb, torch):

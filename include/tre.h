@@ -428,10 +428,40 @@ int tre_loop(const tre_trace_cfg* cfg, uint32_t n_traces, const tre_loop_request
              const tre_scenario* sc, uint32_t n_scenarios, const tre_ctl_out* out, tre_loop_stats* stats,
              double* tss64, void* ws, size_t ws_bytes, void* stream);
 
+/* ------------------------------------------------- stage-aware shares */
+/* Flags of tre_stage_tss, one byte per cell. */
+#define TRE_STAGE_P_IDLE 1 /* no prompt tokens and nothing waiting in the window */
+#define TRE_STAGE_P_INIT 2 /* prefill share initialised                        */
+#define TRE_STAGE_D_IDLE 4 /* no output tokens and nothing active in the window */
+#define TRE_STAGE_D_INIT 8 /* decode share initialised                          */
+
+/* Stage-aware service shares (paper, Sections "Discussion" and "Future
+   Work": for disaggregated prefill / decode serving the scalar score becomes
+   a per-stage vector; the paper gives no formula, and these are the two
+   parts of Eq. (1), each with its one-request floor):
+     prefill  raw_p = 1000 * w_p * P / max(w_q * W_int, window_ms)
+     decode   raw_d = 1000 * D / max(A_int, window_ms)
+   evaluated in that operation order in binary64, then smoothed per stage as
+   the scalar share (Section "Smoothing, Normalization, and Calibration"): a
+   stage idle in a window (its tokens and its demand integral both zero)
+   holds its value, its first busy window sets it to the raw ratio, later
+   ones give alpha * raw + (1 - alpha) * S_prev. Where neither floor binds,
+   Eq. (1)'s raw ratio is the mediant of raw_p and raw_d.
+   tallies: the prefill, decode, a_int and w_int outputs of tre_eval_tss for
+   the same handle and profiles (device, [n_traces][n_windows][n_models]; the
+   other fields are ignored). Outputs, each optional but not all NULL:
+   stage64 (device [n_traces][n_windows][n_models][2] binary64, prefill then
+   decode; 16-byte aligned), stage32 (the same rounded to binary32; 8-byte
+   aligned), flags (device [n_traces][n_windows][n_models], TRE_STAGE_*).
+   Enqueued on `stream`. */
+int tre_stage_tss(const tre_events* ev, const tre_profile* prof, const tre_tss_out* tallies, double* stage64,
+                  float* stage32, uint8_t* flags, void* stream);
+
 /* Kernel timing (HIP events recorded around each launch on its stream).
    tre_set_timing(1) starts recording; tre_kernel_time waits for the
    recorded launches of `kernel` ("tss_stream", "rebalance", "validate",
-   "calib_fill", "calib_join", "calib_judge", "calib_fit", "loop_replay")
+   "calib_fill", "calib_join", "calib_judge", "calib_fit", "loop_replay",
+   "stage_tss")
    and returns their total milliseconds and count, then forgets them. */
 int tre_set_timing(int enable);
 int tre_kernel_time(const char* kernel, double* total_ms, uint64_t* launches);

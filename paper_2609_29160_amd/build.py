@@ -4,7 +4,7 @@ import subprocess
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SRCS = [os.path.join(HERE, "csrc", n) for n in ("tre.hip", "calib.hip", "loop.hip")]
+SRCS = [os.path.join(HERE, "csrc", n) for n in ("tre.hip", "calib.hip", "loop.hip", "stage.hip")]
 LIB = os.path.join(HERE, "libtre.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

@@ -86,7 +86,7 @@ class _Actuation(ctypes.Structure):
 EXPORTS = ["tre_last_error", "tre_load_events", "tre_free_events", "tre_events_info",
            "tre_check_params", "tre_workspace_size", "tre_eval_tss", "tre_rebalance", "tre_sweep",
            "tre_set_timing", "tre_kernel_time", "tre_check_actuation", "tre_rebalance_act", "tre_sweep_act",
-           "tre_calib_workspace_size", "tre_calibrate", "tre_loop_workspace_size", "tre_loop"]
+           "tre_calib_workspace_size", "tre_calibrate", "tre_loop_workspace_size", "tre_loop", "tre_stage_tss"]
 
 
 def _load():
@@ -129,6 +129,8 @@ def _load():
     L.tre_loop.restype = i32
     L.tre_loop.argtypes = [ctypes.POINTER(_TraceCfg), u32, ctypes.POINTER(_LoopRequests), vp, vp, u32,
                            ctypes.POINTER(_CtlOut), vp, vp, vp, sz, vp]
+    L.tre_stage_tss.restype = i32
+    L.tre_stage_tss.argtypes = [vp, vp, ctypes.POINTER(_TssOut), vp, vp, vp, vp]
     L.tre_set_timing.restype = i32
     L.tre_set_timing.argtypes = [i32]
     L.tre_kernel_time.restype = i32
@@ -243,6 +245,29 @@ def tre_eval_tss(ev: Events, prof: torch.Tensor, out: Dict[str, torch.Tensor], s
     int32 tensors)."""
     o = _TssOut(*[_ptr(out.get(k)) for k in ("prefill", "decode", "a_int", "w_int", "tss64", "tss32", "flags")])
     _check(_L.tre_eval_tss(ev.handle, _ptr(prof), ctypes.byref(o), _stream(stream)))
+
+
+STAGE_P_IDLE, STAGE_P_INIT, STAGE_D_IDLE, STAGE_D_INIT = 1, 2, 4, 8
+
+
+def stage_outputs(ev: Events, which=("stage64", "stage32", "flags"), device="cuda") -> Dict[str, torch.Tensor]:
+    """Output tensors of tre_stage_tss: stage64 / stage32 [n_traces][n_windows]
+    [n_models][2] (prefill, decode), flags [n_traces][n_windows][n_models]."""
+    shape = (ev.n_traces, ev.n_windows, ev.n_models)
+    dt = {"stage64": torch.float64, "stage32": torch.float32}
+    out = {k: torch.empty(shape + (2,), dtype=dt[k], device=device) for k in which if k in dt}
+    if "flags" in which:
+        out["flags"] = torch.empty(shape, dtype=torch.uint8, device=device)
+    return out
+
+
+def tre_stage_tss(ev: Events, prof: torch.Tensor, tallies: Dict[str, torch.Tensor], out: Dict[str, torch.Tensor],
+                  stream=None):
+    """Stage-aware shares from the prefill / decode / a_int / w_int outputs of
+    tre_eval_tss; fills the given outputs."""
+    t = _TssOut(*[_ptr(tallies.get(k)) for k in ("prefill", "decode", "a_int", "w_int")], None, None, None)
+    _check(_L.tre_stage_tss(ev.handle, _ptr(prof), ctypes.byref(t), _ptr(out.get("stage64")),
+                            _ptr(out.get("stage32")), _ptr(out.get("flags")), _stream(stream)))
 
 
 def ctl_outputs(ev: Events, n_scenarios: int, move_cap: int, device="cuda") -> Dict[str, torch.Tensor]:
