@@ -46,8 +46,9 @@ using tre_internal::LaunchTimer;
 
 namespace {
 
-constexpr int kNear = 16;  // windows ahead whose tallies sit in LDS (power of two)
-constexpr int kStage = 8;  // requests per lane staged in LDS for the starts
+constexpr int kNear = 4;  // windows ahead whose tallies sit in LDS (power of two)
+constexpr int kStage = 4;  // requests per lane staged in LDS for the starts
+constexpr int kEnt = 2;    // starts a lane records per pass of the wave's event generation
 constexpr uint32_t kNone = 0xffffffffu;
 constexpr int64_t kNever = INT64_MAX;
 constexpr int kLdsMax = 160 * 1024;
@@ -84,10 +85,13 @@ struct LoopParams {
   int32_t r_cap;
   int32_t pchunk;
   int32_t dchunk;
-  int32_t slot_cap;             // multiple of 4
+  int32_t pool_words;           // one heap pool: pool_reps * spr + M (a skew word per lane), multiple of 4
+  int32_t pool_reps;            // replicas the pool holds: min(budget, M * r_hi)
   uint64_t wmagic;              // x / window_ms == (x * wmagic) >> wshift for x < 2^31
   int32_t wshift;
-  int32_t r_hi;                 // min(r_cap, budget): replicas the slot array holds
+  uint64_t pmagic, dmagic;      // the same for the prompt and output chunk sizes
+  int32_t pshift, dshift;
+  int32_t r_hi;                 // min(r_cap, budget): replicas one model may hold
   uint32_t ring_len;            // power of two, >= 2 * kNear
   int32_t window_ms;
   int32_t duration_ms;          // duration + longest service < 2^31
@@ -128,13 +132,12 @@ __device__ __forceinline__ double lane_f64(double x, int l) {
   return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
 }
 
-// A lane's slot free times in LDS as a binary min-heap (node i at h[i * M]);
+// A lane's slot free times in LDS as a binary min-heap (node i at h[i]);
 // only the multiset of free times matters, so the heap order is free.
 struct Heap {
   uint32_t* h;
-  int M;
 
-  __device__ uint32_t& at(int i) const { return h[i * M]; }
+  __device__ uint32_t& at(int i) const { return h[i]; }
 
   // the root (the smallest) replaced by v, n nodes
   __device__ void replace_top(int n, uint32_t v) const {
@@ -205,21 +208,61 @@ __global__ __launch_bounds__(64) void loop_replay(LoopParams p) {
   const uint32_t L = p.ring_len;
   const int spr = p.spr;
   const int64_t p_full = ceil_ms(p.pchunk, sv.prefill_us), d_full = ceil_ms(p.dchunk, sv.decode_us);
-  const Heap slot{lds + mc, M};
-  uint32_t* near = lds + p.slot_cap * M + mc;  // field f of ring cell c at near[(f * kNear + c) * M]
+  // two pools of slot heaps: the models' heaps packed one after another (a
+  // skew word per model keeps their roots in different banks); a tick that
+  // moves replicas repacks them into the other pool
+  uint32_t* const pool0 = lds;
+  uint32_t* const pool1 = lds + p.pool_words;
+  uint32_t* const rest = lds + 2 * p.pool_words;
+  uint32_t* near = rest + mc;  // field f of ring cell c at near[(f * kNear + c) * M]
   // requests sbase .. sbase + kStage - 1: arrival (ms, at most the duration)
   // at stg[2 * e * M], prompt | output << 16 at stg[(2 * e + 1) * M]
-  int32_t* stg = (int32_t*)(lds + (p.slot_cap + 4 * kNear) * M + mc);
+  int32_t* stg = (int32_t*)(rest + 4 * kNear * M + mc);
+  // starts recorded for the wave's event pass: field f (start, prompt | output
+  // << 16, end of the prompt, first chunk's number) of entry k at
+  // ent[(f * kEnt + k) * M]; each lane's first chunk number and entry count;
+  // each lane's chunk times and rates (prompt chunk, output chunk, prefill_us,
+  // decode_us) at cst[i * M]
+  uint32_t* ent = rest + (4 * kNear + 2 * kStage) * M + mc;
+  uint32_t* lane_off = rest + (4 * kNear + 2 * kStage + 4 * kEnt) * M;
+  uint32_t* lane_cnt = lane_off + M;
+  uint32_t* cst = lane_cnt + M + mc;
   FarCell* far = p.far + (uint64_t)s * L * M + mc;  // cell c at far[c * M]
-  // initial replicas within the slot array (min(r_cap, budget) replicas)
+  // initial replicas: at most r_hi per model and pool_reps in all (initial
+  // replicas within the budget are never cut)
   const int r_hi = p.r_hi;
   int R = act ? (pr.r_init < 0 ? 0 : (pr.r_init > r_hi ? r_hi : pr.r_init)) : 0;
+  {
+    int incl = R;
+    for (int o = 1; o < 64; o <<= 1) {
+      const int v = __shfl_up(incl, o);
+      if (lane >= o) incl += v;
+    }
+    const int room = p.pool_reps - (incl - R);
+    R = R < room ? R : (room > 0 ? room : 0);
+  }
   int rsum = R;
   for (int o = 32; o > 0; o >>= 1) rsum += __shfl_xor(rsum, o);
   int pool = p.budget - rsum;
+  int hs = R * spr;  // heap size (R <= r_hi)
+  int base;          // first node in the current pool
+  {
+    int incl = hs;
+    for (int o = 1; o < 64; o <<= 1) {
+      const int v = __shfl_up(incl, o);
+      if (lane >= o) incl += v;
+    }
+    base = incl - hs + mc;
+  }
+  int pb = 0;  // current pool (wave-uniform)
+  auto heap = [&]() { return Heap{(pb ? pool1 : pool0) + base}; };
   if (act) {
+    cst[0] = (uint32_t)p_full;
+    cst[M] = (uint32_t)d_full;
+    cst[2 * M] = sv.prefill_us;
+    cst[3 * M] = sv.decode_us;
     for (int i = 0; i < 4 * kNear; ++i) near[i * M] = 0u;
-    for (int i = 0; i < R * spr; ++i) slot.at(i) = 0u;  // R <= r_hi here; equal keys form a heap
+    for (int i = 0; i < hs; ++i) pool0[base + i] = 0u;  // equal keys form a heap
     for (uint32_t c = 0; c < L; ++c) {
       FarCell* fc = far + (uint64_t)c * M;
       far_store(&fc->p, 0u);
@@ -228,13 +271,15 @@ __global__ __launch_bounds__(64) void loop_replay(LoopParams p) {
       far_store(&fc->e_fin, 0u);
     }
   }
-  // slots of R replicas: R stays within r_hi when the initial replicas fit
-  // the budget; the bound keeps other inputs inside the slot array
-  auto nslots = [&](int r) { return (r < r_hi ? r : r_hi) * spr; };
-  uint32_t bf = act && nslots(R) > 0 ? 0u : kNone;  // earliest slot free time (the heap's root)
+  uint32_t bf = act && hs > 0 ? 0u : kNone;  // earliest slot free time (the heap's root)
   const uint64_t wmagic = p.wmagic;
   const int wshift = p.wshift;
   auto win = [&](uint32_t x) { return (int32_t)((x * wmagic) >> wshift); };  // x / W for x < 2^31
+  const uint64_t pmagic = p.pmagic, dmagic = p.dmagic;
+  const int pshift = p.pshift, dshift = p.dshift;
+  auto div_p = [&](uint32_t x) { return (uint32_t)((x * pmagic) >> pshift); };  // x / prefill_chunk
+  auto div_d = [&](uint32_t x) { return (uint32_t)((x * dmagic) >> dshift); };  // x / decode_chunk
+  const uint32_t udur = (uint32_t)dur;
   const int64_t q1 = act ? p.req_off[tm + 1] : 0;
   int64_t next_arr = act ? p.req_off[tm] : 0, next_start = next_arr;
   // arrival times of requests next_arr .. next_arr + 3 (kNever past the table)
@@ -277,18 +322,6 @@ __global__ __launch_bounds__(64) void loop_replay(LoopParams p) {
     int64_t eA = 0, eW = 0, dA = 0, dW = 0;
     bool idle = true;
     if (act) {
-      {  // the window's tallies from requests started before it
-        uint32_t* nc = near + (w & (kNear - 1)) * M;
-        P = nc[0];
-        D = nc[kNear * M];
-        const uint32_t nf = nc[2 * kNear * M], ef = nc[3 * kNear * M];
-        nc[0] = 0u;
-        nc[kNear * M] = 0u;
-        nc[2 * kNear * M] = 0u;
-        nc[3 * kNear * M] = 0u;
-        dA -= nf;
-        eA -= ef;
-      }
       // arrivals: a request waits from its arrival
       while (a0 < w_end) {
         eW += w_end - a0;
@@ -300,119 +333,158 @@ __global__ __launch_bounds__(64) void loop_replay(LoopParams p) {
         a2 = a3;
         a3 = next_arr + 3 < q1 ? p.arrival[next_arr + 3] : kNever;
       }
-      // starts, in arrival order, on the slot that frees first
-      const int ns = nslots(R);
-      while (next_start < next_arr && ns > 0) {
-        if (next_start - sbase >= kStage) stage(next_start);
-        const int e = (int)(next_start - sbase);
-        const int64_t a = stg[2 * e * M];
-        const uint32_t po = (uint32_t)stg[(2 * e + 1) * M];
-        const int64_t st = a > (int64_t)bf ? a : (int64_t)bf;
-        if (st >= w_end) break;  // capacity may change at the window's end
-        // admission: waiting -> active
-        eW -= w_end - st;
-        dW -= 1;
-        eA += w_end - st;
-        dA += 1;
-        // tokens of field f (0 prompt, 1 output) counted in window x: this
-        // window's (registers), the next kNear - 1 (LDS) or further (HBM)
-        auto deliver = [&](int f, int32_t x, uint32_t v) {
+    }
+    // ---- starts, in arrival order, on the slot that frees first. A lane
+    // starts up to kEnt requests per pass (their finish, judging and slot
+    // in closed form) and records them; the whole wave then adds their
+    // PREFILL / DECODE events to the rings, chunks spread over the lanes.
+    bool more = act;
+    for (;;) {
+      int cnt = 0;
+      uint32_t ntot = 0;
+      if (more) {
+        const int ns = hs;
+        const Heap slot = heap();
+        more = false;
+        while (next_start < next_arr && ns > 0) {
+          if (next_start - sbase >= kStage) stage(next_start);
+          const int e = (int)(next_start - sbase);
+          const int64_t a = stg[2 * e * M];
+          const uint32_t po = (uint32_t)stg[(2 * e + 1) * M];
+          const int64_t st = a > (int64_t)bf ? a : (int64_t)bf;
+          if (st >= w_end) break;  // capacity may change at the window's end
+          // admission: waiting -> active
+          eW -= w_end - st;
+          dW -= 1;
+          eA += w_end - st;
+          dA += 1;
+          // chunks: PREFILL events at the start of each prompt chunk, DECODE
+          // events at the end of each output chunk, FINISH at the last
+          const uint32_t pt = po & 0xffffu, out_tok = po >> 16;
+          const uint32_t npf = div_p(pt), prem = pt - npf * (uint32_t)p.pchunk;
+          const uint32_t ndf = div_d(out_tok), drem = out_tok - ndf * (uint32_t)p.dchunk;
+          const uint32_t t_prem = prem ? (uint32_t)ceil_ms(prem, sv.prefill_us) : 0u;
+          const uint32_t t_drem = drem ? (uint32_t)ceil_ms(drem, sv.decode_us) : 0u;
+          const uint32_t td = (uint32_t)st + npf * (uint32_t)p_full + t_prem;  // end of the prompt
+          const uint32_t tt = td + ndf * (uint32_t)d_full + t_drem;            // the last output chunk
+          if (tt < udur) {  // FINISH: active -> gone
+            const int32_t xw = win(tt);
+            const uint32_t ahead = (uint32_t)(xw - w), ef = (uint32_t)(xw + 1) * (uint32_t)W - tt;
+            if (ahead == 0u) {
+              eA -= w_end - (int64_t)tt;
+              dA -= 1;
+            } else if (ahead < (uint32_t)kNear) {
+              uint32_t* nc = near + (xw & (kNear - 1)) * M;
+              lds_add(nc + 2 * kNear * M, 1u);
+              lds_add(nc + 3 * kNear * M, ef);
+            } else if (ahead < L) {
+              FarCell* fc = far + (uint64_t)(xw & (L - 1)) * M;
+              far_add(&fc->n_fin, 1u);
+              far_add(&fc->e_fin, ef);
+            } else {
+              ++overflow;
+            }
+            if (out_tok) {  // judged as in the calibration sweep
+              const int64_t t_first = (int64_t)td + (ndf ? d_full : (int64_t)t_drem);
+              const uint32_t first_ch = ndf ? (uint32_t)p.dchunk : drem;
+              const int64_t ttft = t_first - a, e2e = (int64_t)tt - a, after = (int64_t)out_tok - first_ch;
+              bool good = (double)ttft <= sl.ttft_ms && (double)e2e <= sl.e2e_ms;
+              if (after > 0) good = good && (double)((int64_t)tt - t_first) / (double)after <= sl.tpot_ms;
+              ++n_done;
+              n_ok += good ? 1u : 0u;
+              e2e_sum += e2e;
+              e2e_max = e2e > e2e_max ? e2e : e2e_max;
+            }
+          }
+          slot.replace_top(ns, tt);  // tt >= st >= the root
+          bf = slot.at(0);
+          ent[(0 * kEnt + cnt) * M] = (uint32_t)st;
+          ent[(1 * kEnt + cnt) * M] = po;
+          ent[(2 * kEnt + cnt) * M] = td;
+          ent[(3 * kEnt + cnt) * M] = ntot;
+          ntot += npf + (prem ? 1u : 0u) + ndf + (drem ? 1u : 0u);
+          ++cnt;
+          ++n_start;
+          ++next_start;
+          if (cnt == kEnt) {
+            more = true;
+            break;
+          }
+        }
+      }
+      if (!__ballot(cnt > 0)) break;
+      // the recorded chunks of every lane, numbered by an exclusive scan
+      uint32_t incl = ntot;
+      for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t v = (uint32_t)__shfl_up((int)incl, o);
+        if (lane >= o) incl += v;
+      }
+      const uint32_t C = (uint32_t)__shfl((int)incl, 63);
+      if (lane < M) {
+        lane_off[lane] = incl - ntot;
+        lane_cnt[lane] = (uint32_t)cnt;
+      }
+      __syncthreads();
+      for (uint32_t c = (uint32_t)lane; c < C; c += 64) {
+        int l = 0;  // the owner: the last lane whose first chunk is at or before c
+        for (int step = 32; step > 0; step >>= 1)
+          if (l + step < M && lane_off[l + step] <= c) l += step;
+        const uint32_t r = c - lane_off[l];
+        int k = 0;
+        const int cn = (int)lane_cnt[l];
+        while (k + 1 < cn && ent[(3 * kEnt + k + 1) * M + (l - mc)] <= r) ++k;
+        const uint32_t* en = ent + k * M + (l - mc);
+        const uint32_t j = r - en[3 * kEnt * M];
+        const uint32_t st = en[0], po = en[kEnt * M], td = en[2 * kEnt * M];
+        const uint32_t* cl = cst + (l - mc);  // owner's chunk times and rates
+        const uint32_t pt = po & 0xffffu, out_tok = po >> 16;
+        const uint32_t npf = div_p(pt), prem = pt - npf * (uint32_t)p.pchunk;
+        const uint32_t np = npf + (prem ? 1u : 0u);
+        uint32_t t, tok;
+        int f;
+        if (j < np) {
+          t = st + j * cl[0];
+          tok = j < npf ? (uint32_t)p.pchunk : prem;
+          f = 0;
+        } else {
+          const uint32_t q = j - np, ndf = div_d(out_tok);
+          if (q < ndf) {
+            t = td + (q + 1u) * cl[M];
+            tok = (uint32_t)p.dchunk;
+          } else {
+            const uint32_t drem = out_tok - ndf * (uint32_t)p.dchunk;
+            t = td + ndf * cl[M] + (uint32_t)ceil_ms(drem, cl[3 * M]);
+            tok = drem;
+          }
+          f = 1;
+        }
+        if (t < udur) {
+          const int32_t x = win(t);
           const uint32_t ahead = (uint32_t)(x - w);
-          if (ahead == 0u) {
-            if (f == 0) P += v;
-            else D += v;
-          } else if (ahead < (uint32_t)kNear) {
-            lds_add(near + (f * kNear + (x & (kNear - 1))) * M, v);
+          if (ahead < (uint32_t)kNear) {
+            lds_add(near + (l - mc) + (f * kNear + (x & (kNear - 1))) * M, tok);
           } else if (ahead < L) {
-            far_add(&far[(uint64_t)(x & (L - 1)) * M].p + f, v);
+            far_add(&far[(uint64_t)(x & (L - 1)) * M + (l - mc)].p + f, tok);
           } else {
             ++overflow;
           }
-        };
-        // events come in time order (times below 2^31 within the declared
-        // bounds): xw is the window of the latest, acc the tokens gathered
-        // for it, delivered when a later event falls in another window
-        int32_t xw = w;
-        uint32_t xend = (uint32_t)w_end, acc = 0;
-        auto at_time = [&](int f, uint32_t x, uint32_t v) {  // x < duration
-          if (x >= xend) {
-            if (acc) deliver(f, xw, acc);
-            acc = 0;
-            xw = win(x);
-            xend = (uint32_t)(xw + 1) * (uint32_t)W;
-          }
-          acc += v;
-        };
-        const uint32_t udur = (uint32_t)dur;
-        uint32_t tt = (uint32_t)st;
-        {  // PREFILL events at the start of each chunk
-          const uint32_t n = po & 0xffffu, nf = n / (uint32_t)p.pchunk, rem = n - nf * (uint32_t)p.pchunk;
-          for (uint32_t j = 0; j < nf; ++j) {
-            if (tt < udur) at_time(0, tt, (uint32_t)p.pchunk);
-            tt += (uint32_t)p_full;
-          }
-          if (rem) {
-            if (tt < udur) at_time(0, tt, rem);
-            tt += (uint32_t)ceil_ms(rem, sv.prefill_us);
-          }
-          if (acc) deliver(0, xw, acc);
-          acc = 0;
         }
-        const uint32_t out_tok = po >> 16;
-        int64_t t_first = -1;
-        uint32_t first_ch = 0;
-        {  // DECODE events at the end of each chunk
-          const uint32_t nf = out_tok / (uint32_t)p.dchunk, rem = out_tok - nf * (uint32_t)p.dchunk;
-          const uint32_t t_rem = rem ? (uint32_t)ceil_ms(rem, sv.decode_us) : 0u;
-          if (out_tok) {
-            first_ch = nf ? (uint32_t)p.dchunk : rem;
-            t_first = (int64_t)tt + (nf ? d_full : (int64_t)t_rem);
-          }
-          for (uint32_t j = 0; j < nf; ++j) {
-            tt += (uint32_t)d_full;
-            if (tt < udur) at_time(1, tt, (uint32_t)p.dchunk);
-          }
-          if (rem) {
-            tt += t_rem;
-            if (tt < udur) at_time(1, tt, rem);
-          }
-          if (acc) deliver(1, xw, acc);
-          acc = 0;
-        }
-        if (tt < udur) {  // FINISH: active -> gone
-          if (tt >= xend) {
-            xw = win(tt);
-            xend = (uint32_t)(xw + 1) * (uint32_t)W;
-          }
-          const uint32_t ahead = (uint32_t)(xw - w), e = xend - tt;
-          if (ahead == 0u) {
-            eA -= w_end - (int64_t)tt;
-            dA -= 1;
-          } else if (ahead < (uint32_t)kNear) {
-            uint32_t* nc = near + (xw & (kNear - 1)) * M;
-            lds_add(nc + 2 * kNear * M, 1u);
-            lds_add(nc + 3 * kNear * M, e);
-          } else if (ahead < L) {
-            FarCell* fc = far + (uint64_t)(xw & (L - 1)) * M;
-            far_add(&fc->n_fin, 1u);
-            far_add(&fc->e_fin, e);
-          } else {
-            ++overflow;
-          }
-          if (t_first >= 0) {  // judged as in the calibration sweep
-            const int64_t ttft = t_first - a, e2e = (int64_t)tt - a, after = (int64_t)out_tok - first_ch;
-            bool good = (double)ttft <= sl.ttft_ms && (double)e2e <= sl.e2e_ms;
-            if (after > 0) good = good && (double)((int64_t)tt - t_first) / (double)after <= sl.tpot_ms;
-            ++n_done;
-            n_ok += good ? 1u : 0u;
-            e2e_sum += e2e;
-            e2e_max = e2e > e2e_max ? e2e : e2e_max;
-          }
-        }
-        slot.replace_top(ns, tt);  // tt >= st >= the root
-        bf = slot.at(0);
-        ++n_start;
-        ++next_start;
+      }
+      __syncthreads();
+      if (!__ballot(more)) break;
+    }
+    if (act) {
+      {  // the window's tallies, now complete: requests started before it and in it
+        uint32_t* nc = near + (w & (kNear - 1)) * M;
+        P = nc[0];
+        D = nc[kNear * M];
+        const uint32_t nf = nc[2 * kNear * M], ef = nc[3 * kNear * M];
+        nc[0] = 0u;
+        nc[kNear * M] = 0u;
+        nc[2 * kNear * M] = 0u;
+        nc[3 * kNear * M] = 0u;
+        dA -= nf;
+        eA -= ef;
       }
       {  // far tallies: those of window w - 1 + kNear into LDS, then fetch those of w + kNear
         if (fp | fd | fn | fe) {
@@ -477,6 +549,7 @@ __global__ __launch_bounds__(64) void loop_replay(LoopParams p) {
     }
     const unsigned long long sur = __ballot(act && Z > pr.tau_surplus);
     unsigned long long used = 0ull;
+    int pops = 0, pushes = 0;  // this tick's slot changes of this lane (a model moves at most once per tick)
     for (uint32_t k = 0; k < sc.max_moves; ++k) {
       const int r = pick_lane<false>(ok & ~used & __ballot(act && R < p.r_cap), Z, lane);  // Eq. (3)
       if (r < 0) break;
@@ -491,24 +564,14 @@ __global__ __launch_bounds__(64) void loop_replay(LoopParams p) {
         if (d < 0) d = pick_lane<true>(cd & ~sur, Z, lane);
         if (d < 0) break;
         used |= 1ull << d;
-        if (lane == d) {  // the replica's slots that free first leave
-          int ns = nslots(R);
-          const int keep = R > 0 ? nslots(R - 1) : 0;
-          while (ns > keep) {
-            --ns;
-            if (ns > 0) slot.replace_top(ns, slot.at(ns));
-          }
-          if (R > 0) R -= 1;
-          bf = ns > 0 ? slot.at(0) : kNone;
+        if (lane == d && R > 0) {  // the replica's slots that free first leave
+          pops = spr;
+          R -= 1;
         }
       }
       used |= 1ull << r;
-      if (lane == r) {  // the new replica's slots are free from the window's end
-        if (R < r_hi) {
-          const int ns = nslots(R);
-          for (int q = 0; q < spr; ++q) slot.push(ns + q, (uint32_t)w_end);
-          bf = slot.at(0);
-        }
+      if (lane == r) {  // the new replica's slots, free from the window's end
+        pushes = R < r_hi ? spr : 0;
         R += 1;
       }
       if (lane == 0 && nm < p.move_cap) {
@@ -521,6 +584,31 @@ __global__ __launch_bounds__(64) void loop_replay(LoopParams p) {
         p.moves[(uint64_t)s * p.move_cap + nm] = mv;
       }
       ++nm;
+    }
+    if (__ballot(pops > 0 || pushes > 0)) {
+      // the donors' earliest-free slots leave their heaps; every heap moves
+      // to the other pool, packed again; the receivers' slots join there
+      const Heap old = heap();
+      for (int q = 0; q < pops && hs > 0; ++q) {
+        --hs;
+        if (hs > 0) old.replace_top(hs, old.at(hs));
+      }
+      const int want = act ? hs + pushes : 0;
+      int incl = want;
+      for (int o = 1; o < 64; o <<= 1) {
+        const int v = __shfl_up(incl, o);
+        if (lane >= o) incl += v;
+      }
+      const int nbase = incl - want + mc;
+      uint32_t* nxt = (pb ? pool0 : pool1) + nbase;
+      if (act)
+        for (int i = 0; i < hs; ++i) nxt[i] = old.at(i);
+      const Heap fresh{nxt};
+      for (int q = 0; q < pushes; ++q) fresh.push(hs + q, (uint32_t)w_end);
+      hs += pushes;
+      base = nbase;
+      pb ^= 1;
+      bf = act && hs > 0 ? fresh.at(0) : kNone;
     }
   }
   if (act) {
@@ -559,15 +647,29 @@ int r_hi(const tre_trace_cfg* cfg, const tre_loop_requests* rq) {
   return rq->r_cap < cfg->budget ? rq->r_cap : cfg->budget;
 }
 
-// slots per lane, rounded up to whole 16-byte groups
-int slot_cap(const tre_trace_cfg* cfg, const tre_loop_requests* rq) {
-  return (r_hi(cfg, rq) * rq->slots_per_replica + 3) & ~3;
+// replicas the heap pool holds, and its words (a skew word per model), a
+// multiple of 4
+int pool_reps(const tre_trace_cfg* cfg, const tre_loop_requests* rq) {
+  const int64_t all = (int64_t)cfg->n_models * r_hi(cfg, rq);
+  return (int)(cfg->budget < all ? cfg->budget : all);
+}
+int pool_words(const tre_trace_cfg* cfg, const tre_loop_requests* rq) {
+  return (int)(((int64_t)pool_reps(cfg, rq) * rq->slots_per_replica + cfg->n_models + 3) & ~3ll);
 }
 
-// LDS bytes of one scenario: slots, the four planes of the near ring, the
-// staged requests (arrival, prompt and output)
+// LDS bytes of one scenario: per model the slots, the four planes of the
+// near ring, the staged requests (arrival, prompt and output), the recorded
+// starts, the model's chunk offset and count, its chunk times and rates
 size_t lds_bytes(const tre_trace_cfg* cfg, const tre_loop_requests* rq) {
-  return ((size_t)slot_cap(cfg, rq) + 4 * kNear + 2 * kStage) * cfg->n_models * 4;
+  return (2 * (size_t)pool_words(cfg, rq) + (size_t)(4 * kNear + 2 * kStage + 4 * kEnt + 2 + 4) * cfg->n_models) * 4;
+}
+
+// x / d == (x * m) >> sh for x < 2^32: m = ceil(2^(32 + l) / d), 2^l >= d
+void magic_div(int64_t d, uint64_t* m, int32_t* sh) {
+  int l = 0;
+  while ((1ll << l) < d) ++l;
+  *sh = 32 + l;
+  *m = (uint64_t)(((1ull << (32 + l)) + (uint64_t)d - 1) / (uint64_t)d);
 }
 
 int check_loop_args(const tre_trace_cfg* cfg, const tre_loop_requests* rq) {
@@ -622,7 +724,6 @@ extern "C" int tre_loop(const tre_trace_cfg* cfg, uint32_t n_traces, const tre_l
   hipStream_t st = (hipStream_t)stream;
   const int M = cfg->n_models;
   const uint32_t L = ring_len(cfg, rq);
-  const int scap = slot_cap(cfg, rq);
   char* base = (char*)ws;
   unsigned long long* overflow = (unsigned long long*)base;
   FarCell* far = (FarCell*)(base + 256);
@@ -655,14 +756,12 @@ extern "C" int tre_loop(const tre_trace_cfg* cfg, uint32_t n_traces, const tre_l
   lp.r_cap = rq->r_cap;
   lp.pchunk = rq->prefill_chunk;
   lp.dchunk = rq->decode_chunk;
-  lp.slot_cap = scap;
+  lp.pool_words = pool_words(cfg, rq);
+  lp.pool_reps = pool_reps(cfg, rq);
   lp.r_hi = r_hi(cfg, rq);
-  {  // x / W == (x * m) >> (32 + l) for x < 2^32, m = ceil(2^(32 + l) / W), 2^l >= W
-    int l = 0;
-    while ((1ll << l) < cfg->window_ms) ++l;
-    lp.wshift = 32 + l;
-    lp.wmagic = (uint64_t)(((1ull << (32 + l)) + (uint64_t)cfg->window_ms - 1) / (uint64_t)cfg->window_ms);
-  }
+  magic_div(cfg->window_ms, &lp.wmagic, &lp.wshift);
+  magic_div(rq->prefill_chunk, &lp.pmagic, &lp.pshift);
+  magic_div(rq->decode_chunk, &lp.dmagic, &lp.dshift);
   lp.ring_len = L;
   lp.window_ms = (int32_t)cfg->window_ms;
   lp.duration_ms = (int32_t)cfg->duration_ms;
