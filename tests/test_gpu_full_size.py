@@ -184,3 +184,123 @@ def test_stress_full_size_calibration():
     ev.close()
     del tss, out, dt
     torch.cuda.empty_cache()
+
+
+def test_stress_full_size_stage_shares():
+    """Tallies and stage-aware shares over the whole stress workload, twice:
+    identical results, and the shares and flags of sampled traces equal to
+    the oracle's bit for bit."""
+    import torch
+
+    from paper_2609_29160_amd import device, tre
+
+    w = tg.standard(4)
+    say(f"{w.name}: uploading")
+    dt = device.upload(w)
+    ev = device.load(dt, validate=True)
+    prof = device.profiles(w)
+    T, M = ev.n_traces, ev.n_models
+    tal = tre.tss_outputs(ev, which=("prefill", "decode", "a_int", "w_int"))
+    out = tre.stage_outputs(ev, which=("stage64", "flags"))
+    runs = []
+    for _ in range(2):
+        tre.tre_eval_tss(ev, prof, tal)
+        tre.tre_stage_tss(ev, prof, tal, out)
+        torch.cuda.synchronize()
+        runs.append({k: v.cpu().numpy().copy() for k, v in out.items()})
+    for k in runs[0]:
+        assert np.array_equal(runs[0][k].view(np.uint8), runs[1][k].view(np.uint8)), f"{k} differs between launches"
+    rng = np.random.default_rng(19)
+    sample = sorted({0, T - 1, *rng.integers(0, T, 4).tolist()})
+    o = PT.O.get()
+    prof_all = PT.O.pack_profiles(w.profile_columns())
+    for t in sample:
+        host = w.generate(t, t + 1).trace(0)
+        p = prof_all[t * M:(t + 1) * M]
+        r = o.stage_tss(o.tss_trace(host, w.window_ms, w.duration_ms, p), w.window_ms, p)
+        assert np.array_equal(runs[0]["stage64"][t].view(np.uint64), r["S"].view(np.uint64)), t
+        assert np.array_equal(runs[0]["flags"][t], r["flags"]), t
+    say(f"{w.name}: stage shares of {len(sample)} sampled traces match the oracle")
+    ev.close()
+    del tal, out, dt
+    torch.cuda.empty_cache()
+
+
+def test_stress_full_size_closed_loop():
+    """The closed loop over every scenario of the stress workload (777 M
+    requests), twice: identical results; sampled scenarios equal to the
+    oracle's closed-loop replay (moves, replicas, replica-window sums,
+    latency statistics) with no event beyond the ring."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    import torch
+
+    from paper_2609_29160_amd import tre
+
+    w = tg.standard(4)
+    T, M = w.n_traces, w.n_models
+    with ThreadPoolExecutor(max_workers=16) as pool:
+        tables = list(pool.map(w.requests, range(T)))
+    say(f"{w.name}: {sum(len(t['arrival_ms']) for t in tables)} requests")
+    svc = np.zeros(T * M, tre.SERVICE_DTYPE)
+    for k, v in w.service_columns().items():
+        svc[k] = v
+    slo = np.zeros(T * M, tre.SLO_DTYPE)
+    for k, v in w.slo_columns().items():
+        slo[k] = v
+    rq, keep = tre.loop_requests(tables, M, svc, slo)
+    cfg = w.trace_cfg()
+    prof = tre.pack(w.profile_columns(), tre.PROFILE_DTYPE)
+    sc_cols = w.scenario_columns()
+    n_sc = len(sc_cols["trace"])
+    sc = tre.pack(sc_cols, tre.SCENARIO_DTYPE)
+    nW = w.n_windows
+    n_ticks = sum(1 for x in range(nW) if ((x + 1) * w.window_ms) % cfg["fast_period_ms"] == 0
+                  or ((x + 1) * w.window_ms) % cfg["slow_period_ms"] == 0)
+    move_cap = max(1, n_ticks * int(np.max(sc_cols["max_moves"])))
+
+    class _Shape:
+        n_models = M
+
+    ws = torch.empty(tre.tre_loop_workspace_size(cfg, rq, n_sc), dtype=torch.uint8, device="cuda")
+    runs = []
+    for _ in range(2):
+        out = tre.ctl_outputs(_Shape(), n_sc, move_cap)
+        stats = torch.zeros(n_sc * M * tre.LOOP_STATS_DTYPE.itemsize, dtype=torch.uint8, device="cuda")
+        tre.tre_loop(cfg, T, rq, prof, sc, out, stats, ws)
+        torch.cuda.synchronize()
+        assert int(ws[:8].cpu().numpy().view(np.uint64)[0]) == 0, "events beyond the ring"
+        runs.append((_outputs(out), stats.cpu().numpy().copy()))
+    for k in runs[0][0]:
+        assert np.array_equal(runs[0][0][k], runs[1][0][k]), f"{k} differs between launches"
+    assert np.array_equal(runs[0][1], runs[1][1]), "statistics differ between launches"
+    o = PT.O.get()
+    prof_all = PT.O.pack_profiles(w.profile_columns())
+    slo_all = PT.O.pack_slo(w.slo_columns())
+    svc_all = PT.O.pack_svc(w.service_columns())
+    sc_all = PT.O.pack_scenarios(sc_cols)
+    rng = np.random.default_rng(23)
+    sample = sorted({0, n_sc - 1, *rng.integers(0, n_sc, 2).tolist()})
+
+    def one(s):
+        t = int(sc_all[s]["trace"])
+        return o.loop(cfg, prof_all[t * M:(t + 1) * M], sc_all[s:s + 1], slo_all[t * M:(t + 1) * M],
+                      svc_all[t * M:(t + 1) * M], tables[t], move_cap=move_cap)
+
+    say(f"{w.name}: oracle closed loop of scenarios {sample}")
+    with ThreadPoolExecutor(max_workers=len(sample)) as pool:
+        refs = list(pool.map(one, sample))
+    g, st = runs[0]
+    moves = tre.unpack_moves(torch.from_numpy(g["moves"])).reshape(n_sc, move_cap)
+    st = st.view(tre.LOOP_STATS_DTYPE).reshape(n_sc, M)
+    for s, ref in zip(sample, refs):
+        n = int(g["n_moves"][s])
+        assert n == ref["n_moves"], (s, n, ref["n_moves"])
+        k = min(n, move_cap)
+        for f in ("window", "path", "receiver", "donor"):
+            assert np.array_equal(moves[s][:k][f], ref["moves"][:k][f]), (s, f)
+        assert np.array_equal(g["r_final"][s], ref["r_final"]), s
+        assert np.array_equal(g["r_windows"][s], ref["r_windows"]), s
+        for f in tre.LOOP_STATS_DTYPE.names:
+            assert np.array_equal(st[s][f], ref["stats"][f]), (s, f)
+    say(f"{w.name}: closed loop of {len(sample)} sampled scenarios matches the oracle")
