@@ -7,7 +7,10 @@ three times: the three results must be identical (the kernels share LDS
 between waves; a missing barrier shows up as launch-to-launch differences
 only at this scale), and sampled scenarios and per-cell fp32 TSS of sampled
 traces must match the CPU oracle exactly. The oracle regenerates each
-sampled trace on the host from the same seeds.
+sampled trace on the host from the same seeds. The calibration sweep, the
+stage-aware shares and the closed-loop replay of the whole stress workload
+are run twice each and checked the same way (sampled traces or scenarios
+against the oracle).
 """
 import sys
 
