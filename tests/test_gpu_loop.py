@@ -7,8 +7,9 @@ oracle's, and no event may fall outside the ring of future windows.
 
 Inputs: the tiny and bursty workloads' request tables (the same arrivals and
 lengths as their traces) under scenario tables with 0 to 4 moves per tick,
-spare budget and replica caps that bind; the oracle's hand cases; 1, 17 and
-64 models; one and three slots per replica; argument errors.
+spare budget and replica caps that bind; budgets above n_models * r_cap; the
+oracle's hand cases; 1, 17 and 64 models; one and three slots per replica;
+argument errors (including slot heaps beyond the LDS).
 """
 import sys
 
@@ -185,6 +186,21 @@ def test_model_counts(lib):
                _scenarios(rng, 4, 1))
 
 
+def test_budget_above_the_replica_caps(lib):
+    """A budget larger than n_models * r_cap: the heaps' pool holds
+    n_models * r_cap replicas and the idle budget never runs out."""
+    w = tg.standard(0)
+    tables = [w.requests(0)]
+    rng = np.random.default_rng(7)
+    for r_cap, spr in ((2, 8), (4, 1), (3, 3)):
+        cfg = dict(w.trace_cfg(), budget=3 * r_cap + 5)
+        prof = dict(w.profile_columns(1))
+        prof["r_init"] = np.minimum(np.asarray(prof["r_init"]), r_cap).astype(np.int32)
+        say(f"r_cap {r_cap}, slots per replica {spr}, budget {cfg['budget']}")
+        _check(lib, f"cap{r_cap}-spr{spr}", cfg, tables, prof, w.slo_columns(1), w.service_columns(1),
+               _scenarios(rng, 6, 1, ks=(1, 2, 4)), spr=spr, r_cap=r_cap)
+
+
 def test_argument_errors(lib):
     tre, device, torch = lib
     w = tg.standard(0)
@@ -208,4 +224,9 @@ def test_argument_errors(lib):
     bad, keep2 = tre.loop_requests(tables, 3, svc, slo, slots_per_replica=0)
     with pytest.raises(tre.TreError) as e:
         tre.tre_loop_workspace_size(cfg, bad, 2)
+    assert e.value.code == tre.TRE_EINVAL
+    # slot heaps beyond the LDS of one workgroup
+    big, keep3 = tre.loop_requests(tables, 3, svc, slo, slots_per_replica=4096, r_cap=4096)
+    with pytest.raises(tre.TreError) as e:
+        tre.tre_loop_workspace_size(dict(cfg, budget=4096), big, 2)
     assert e.value.code == tre.TRE_EINVAL
