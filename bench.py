@@ -332,7 +332,10 @@ def loop_main(args, w, tre, torch, np):
                    "slots_per_replica": 8, "r_cap": 16, "mode": "closed loop"},
         "roofline": {"bound": "hbm", "achieved": round(alg / (kern_ms / 1e3) / 1e9, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(alg / (kern_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
-                     "traffic": loop_traffic_for(w.name) if T == 4096 else None, "kernel": "loop_replay", "kernel_ms": round(kern_ms, 4), "alg_bytes_per_launch": alg},
+                     "traffic": loop_traffic_for(w.name) if T == 4096 else None, "kernel": "loop_replay",
+                     "kernel_ms": round(kern_ms, 4), "alg_bytes_per_launch": alg,
+                     "note": "latency-bound: each scenario is a sequential chain of windows; HBM is not "
+                             "the limit (profiles/loop_replay_sq_counters_stress.md)"},
         "events_beyond_ring": overflow,
         "cpu_baseline": cpu, "parity": parity,
     }
