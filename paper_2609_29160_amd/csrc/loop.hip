@@ -14,21 +14,24 @@
 //
 // Kernel
 //   loop_replay  one wave per scenario (one workgroup), lane = model,
-//                windows in order. Its LDS holds each lane's slot free
-//                times and a ring of the next kNear windows' tallies
-//                (prompt and output tokens, finishes of requests already
-//                started); tallies further ahead go to a ring in HBM with
-//                fire-and-forget atomics and are moved into LDS one window
-//                before they can be needed. Per window a lane takes its
-//                arrivals, starts requests FCFS on the slot that frees first
-//                while the start falls in the window, adds each started
-//                request's events to the rings, reads the window's tallies
-//                and evaluates Eq. (1) and the smoothing in fp64; at a tick
-//                the wave decides the moves (ballots over lanes) and the
-//                receiver and donor lanes change their slots. Which of
-//                several equally early slots a request takes, and where a
-//                removed slot's place goes, changes no output: only the
-//                multiset of free times matters.
+//                windows in order. Its LDS holds the models' slot heaps
+//                (packed in a pool; a tick that moves replicas repacks them
+//                into a second pool), a ring of the next kNear windows'
+//                tallies (prompt and output tokens, finishes of requests
+//                already started), staged requests and the starts recorded
+//                for the event pass; tallies further ahead go to a ring in
+//                HBM with fire-and-forget atomics and are moved into LDS one
+//                window before they can be needed. Per window a lane takes
+//                its arrivals and starts requests FCFS on the slot that
+//                frees first while the start falls in the window (finish,
+//                judging and slot in closed form); the whole wave then adds
+//                the recorded starts' PREFILL / DECODE events to the rings,
+//                their chunks spread over the lanes; each lane reads its
+//                window's tallies and evaluates Eq. (1) and the smoothing in
+//                fp64; at a tick the wave decides the moves (ballots over
+//                lanes). Which of several equally early slots a request
+//                takes, and where a removed slot's place goes, changes no
+//                output: only the multiset of free times matters.
 #include <hip/hip_runtime.h>
 
 #include <math.h>
@@ -92,7 +95,7 @@ struct LoopParams {
   uint64_t pmagic, dmagic;      // the same for the prompt and output chunk sizes
   int32_t pshift, dshift;
   int32_t r_hi;                 // min(r_cap, budget): replicas one model may hold
-  uint32_t ring_len;            // power of two, >= 2 * kNear
+  uint32_t ring_len;            // power of two above the longest span of a request in windows
   int32_t window_ms;
   int32_t duration_ms;          // duration + longest service < 2^31
   int32_t n_windows;
