@@ -405,11 +405,13 @@ typedef struct {
 
 /* Workspace bytes of tre_loop: 256, plus per scenario and model a ring of
    16-byte tallies of future windows, its length the power of two that
-   covers the longest service the declared bounds allow (in windows, + 2).
-   TRE_EINVAL when 4 bytes x (2 x (min(budget, n_models * min(r_cap,
-   budget)) * slots_per_replica + n_models, rounded up to 4) + 38 x
-   n_models) exceed the 160 KiB of LDS one scenario's workgroup may use;
-   TRE_ERANGE when duration_ms plus that longest service reaches 2^31 ms. */
+   covers the longest service the declared bounds allow (in windows, + 2),
+   plus per scenario the words of its slot-heap pool (below) as scratch.
+   The pool holds min(budget, n_models * min(r_cap, budget)) *
+   slots_per_replica + n_models words, rounded up to 4; TRE_EINVAL when 4
+   bytes x (that pool + 44 x n_models) exceed the 160 KiB of LDS one
+   scenario's workgroup may use; TRE_ERANGE when duration_ms plus that
+   longest service reaches 2^31 ms. */
 int tre_loop_workspace_size(const tre_trace_cfg* cfg, const tre_loop_requests* rq, uint32_t n_scenarios,
                             size_t* bytes);
 

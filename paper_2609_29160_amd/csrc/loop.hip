@@ -54,6 +54,7 @@ constexpr int kStage = 4;  // requests per lane staged in LDS for the starts
 constexpr int kEnt = 2;    // starts a lane records per pass of the wave's event generation
 constexpr uint32_t kNone = 0xffffffffu;
 constexpr int64_t kNever = INT64_MAX;
+constexpr int32_t kArrNever = INT32_MAX;
 constexpr int kLdsMax = 160 * 1024;
 
 struct FarCell {    // tallies of one window of one model, beyond the LDS ring
@@ -78,6 +79,7 @@ struct LoopParams {
   tre_loop_stats* stats;
   double* tss64;                // [scenario][window][model] or NULL
   FarCell* far;                 // [scenario][ring_len][model]
+  uint32_t* scratch;            // [scenario][pool_words]: heaps in transit at a repack
   unsigned long long* overflow; // events beyond the ring (declared bounds exceeded)
   uint32_t move_cap;
   uint32_t n_sc;
@@ -88,7 +90,7 @@ struct LoopParams {
   int32_t r_cap;
   int32_t pchunk;
   int32_t dchunk;
-  int32_t pool_words;           // one heap pool: pool_reps * spr + M (a skew word per lane), multiple of 4
+  int32_t pool_words;           // the heap pool: pool_reps * spr + M (a skew word per lane), multiple of 4
   int32_t pool_reps;            // replicas the pool holds: min(budget, M * r_hi)
   uint64_t wmagic;              // x / window_ms == (x * wmagic) >> wshift for x < 2^31
   int32_t wshift;
@@ -192,7 +194,7 @@ __device__ __forceinline__ void far_store(uint32_t* a, uint32_t v) {
 
 __global__ void zero_u64(unsigned long long* x) { *x = 0ull; }
 
-__global__ __launch_bounds__(64) void loop_replay(LoopParams p) {
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void loop_replay(LoopParams p) {
   extern __shared__ __align__(16) uint32_t lds[];
   const int lane = threadIdx.x;
   const uint32_t s = blockIdx.x;
@@ -202,39 +204,39 @@ __global__ __launch_bounds__(64) void loop_replay(LoopParams p) {
   const tre_scenario sc = p.sc[s];
   const uint32_t t = sc.trace < p.n_traces ? sc.trace : 0;
   const uint64_t tm = (uint64_t)t * M + mc;
-  const tre_profile pr = p.prof[tm];
-  const tre_slo sl = p.slo[tm];
+  // the profile's smoothing terms stay in registers; the thresholds are
+  // read again at ticks, the SLO bounds sit in LDS
+  const double w_p = p.prof[tm].w_p, w_q = p.prof[tm].w_q, alpha = p.prof[tm].alpha;
+  const int r_init = p.prof[tm].r_init;
   const tre_service sv = p.svc[tm];
-  const double theta_eff = pr.theta * sc.theta_scale;
-  const double tau_c = sc.tau_crit_override >= 0.0 ? sc.tau_crit_override : pr.tau_crit;
   const int32_t W = p.window_ms, dur = p.duration_ms;
   const uint32_t L = p.ring_len;
   const int spr = p.spr;
   const int64_t p_full = ceil_ms(p.pchunk, sv.prefill_us), d_full = ceil_ms(p.dchunk, sv.decode_us);
-  // two pools of slot heaps: the models' heaps packed one after another (a
-  // skew word per model keeps their roots in different banks); a tick that
-  // moves replicas repacks them into the other pool
-  uint32_t* const pool0 = lds;
-  uint32_t* const pool1 = lds + p.pool_words;
-  uint32_t* const rest = lds + 2 * p.pool_words;
-  uint32_t* near = rest + mc;  // field f of ring cell c at near[(f * kNear + c) * M]
+  // the slot heaps: the models' heaps packed one after another (a skew word
+  // per model keeps their roots in different banks); a tick that moves
+  // replicas repacks them through the scenario's scratch in HBM
+  uint32_t* const hpool = lds;
+  uint32_t* const rest = lds + p.pool_words;
+  double* const slo_t = (double*)rest + mc;  // ttft, tpot, e2e bounds at slo_t[i * M]
+  uint32_t* near = rest + 6 * M + mc;  // field f of ring cell c at near[(f * kNear + c) * M]
   // requests sbase .. sbase + kStage - 1: arrival (ms, at most the duration)
   // at stg[2 * e * M], prompt | output << 16 at stg[(2 * e + 1) * M]
-  int32_t* stg = (int32_t*)(rest + 4 * kNear * M + mc);
+  int32_t* stg = (int32_t*)(rest + (6 + 4 * kNear) * M + mc);
   // starts recorded for the wave's event pass: field f (start, prompt | output
   // << 16, end of the prompt, first chunk's number) of entry k at
   // ent[(f * kEnt + k) * M]; each lane's first chunk number and entry count;
   // each lane's chunk times and rates (prompt chunk, output chunk, prefill_us,
   // decode_us) at cst[i * M]
-  uint32_t* ent = rest + (4 * kNear + 2 * kStage) * M + mc;
-  uint32_t* lane_off = rest + (4 * kNear + 2 * kStage + 4 * kEnt) * M;
+  uint32_t* ent = rest + (6 + 4 * kNear + 2 * kStage) * M + mc;
+  uint32_t* lane_off = rest + (6 + 4 * kNear + 2 * kStage + 4 * kEnt) * M;
   uint32_t* lane_cnt = lane_off + M;
   uint32_t* cst = lane_cnt + M + mc;
   FarCell* far = p.far + (uint64_t)s * L * M + mc;  // cell c at far[c * M]
   // initial replicas: at most r_hi per model and pool_reps in all (initial
   // replicas within the budget are never cut)
   const int r_hi = p.r_hi;
-  int R = act ? (pr.r_init < 0 ? 0 : (pr.r_init > r_hi ? r_hi : pr.r_init)) : 0;
+  int R = act ? (r_init < 0 ? 0 : (r_init > r_hi ? r_hi : r_init)) : 0;
   {
     int incl = R;
     for (int o = 1; o < 64; o <<= 1) {
@@ -257,15 +259,18 @@ __global__ __launch_bounds__(64) void loop_replay(LoopParams p) {
     }
     base = incl - hs + mc;
   }
-  int pb = 0;  // current pool (wave-uniform)
-  auto heap = [&]() { return Heap{(pb ? pool1 : pool0) + base}; };
+  auto heap = [&]() { return Heap{hpool + base}; };
   if (act) {
+    const tre_slo sl = p.slo[tm];
+    slo_t[0] = sl.ttft_ms;
+    slo_t[M] = sl.tpot_ms;
+    slo_t[2 * M] = sl.e2e_ms;
     cst[0] = (uint32_t)p_full;
     cst[M] = (uint32_t)d_full;
     cst[2 * M] = sv.prefill_us;
     cst[3 * M] = sv.decode_us;
     for (int i = 0; i < 4 * kNear; ++i) near[i * M] = 0u;
-    for (int i = 0; i < hs; ++i) pool0[base + i] = 0u;  // equal keys form a heap
+    for (int i = 0; i < hs; ++i) hpool[base + i] = 0u;  // equal keys form a heap
     for (uint32_t c = 0; c < L; ++c) {
       FarCell* fc = far + (uint64_t)c * M;
       far_store(&fc->p, 0u);
@@ -283,23 +288,31 @@ __global__ __launch_bounds__(64) void loop_replay(LoopParams p) {
   auto div_p = [&](uint32_t x) { return (uint32_t)((x * pmagic) >> pshift); };  // x / prefill_chunk
   auto div_d = [&](uint32_t x) { return (uint32_t)((x * dmagic) >> dshift); };  // x / decode_chunk
   const uint32_t udur = (uint32_t)dur;
-  const int64_t q1 = act ? p.req_off[tm + 1] : 0;
-  int64_t next_arr = act ? p.req_off[tm] : 0, next_start = next_arr;
-  // arrival times of requests next_arr .. next_arr + 3 (kNever past the table)
-  int64_t a0 = next_arr < q1 ? p.arrival[next_arr] : kNever;
-  int64_t a1 = next_arr + 1 < q1 ? p.arrival[next_arr + 1] : kNever;
-  int64_t a2 = next_arr + 2 < q1 ? p.arrival[next_arr + 2] : kNever;
-  int64_t a3 = next_arr + 3 < q1 ? p.arrival[next_arr + 3] : kNever;
+  // the model's requests: rq0 + [0, nq); indices below relative to rq0
+  const int64_t rq0 = act ? p.req_off[tm] : 0;
+  const int64_t rq1 = act ? p.req_off[tm + 1] : 0;
+  const uint32_t nq = rq1 > rq0 ? (uint32_t)(rq1 - rq0) : 0u;
+  const int64_t* const arrival = p.arrival + rq0;
+  uint32_t next_arr = 0, next_start = 0;
+  // arrival of request i, kArrNever when past the table or at or after the
+  // end of the replay (such a request never arrives)
+  auto arr = [&](uint32_t i) -> int32_t {
+    if (i >= nq) return kArrNever;
+    const int64_t v = arrival[i];
+    return v >= (int64_t)dur ? kArrNever : (v > (int64_t)INT32_MIN ? (int32_t)v : INT32_MIN);
+  };
+  // arrival times of requests next_arr .. next_arr + 3
+  int32_t a0 = arr(0), a1 = arr(1), a2 = arr(2), a3 = arr(3);
   // the next kStage requests to start, fetched together (one wait per kStage starts)
-  int64_t sbase = next_start;
-  auto stage = [&](int64_t from) {
+  uint32_t sbase = next_start;
+  auto stage = [&](uint32_t from) {
     int64_t av[kStage];
     uint32_t pv[kStage];
 #pragma unroll
     for (int e = 0; e < kStage; ++e) {
-      const bool in = from + e < q1;
-      av[e] = in ? p.arrival[from + e] : kNever;
-      pv[e] = in ? (uint32_t)p.prompt[from + e] | (uint32_t)p.output[from + e] << 16 : 0u;
+      const bool in = from + e < nq;
+      av[e] = in ? arrival[from + e] : kNever;
+      pv[e] = in ? (uint32_t)p.prompt[rq0 + from + e] | (uint32_t)p.output[rq0 + from + e] << 16 : 0u;
     }
 #pragma unroll
     for (int e = 0; e < kStage; ++e) {
@@ -310,11 +323,12 @@ __global__ __launch_bounds__(64) void loop_replay(LoopParams p) {
   };
   if (act) stage(next_start);
   uint32_t fp = 0, fd = 0, fn = 0, fe = 0;  // far cell of window w - 1 + kNear, loaded at window w - 1
-  int64_t cA = 0, cW = 0;  // active / waiting requests at the current window's start
+  int32_t cA = 0, cW = 0;  // active / waiting requests at the current window's start
   double S = 0.0;
   bool init = false;
   uint32_t n_arr = 0, n_start = 0, n_done = 0, n_ok = 0;
-  int64_t e2e_sum = 0, e2e_max = 0, rw = 0;
+  int64_t e2e_sum = 0, rw = 0;
+  int32_t e2e_max = 0;
   unsigned overflow = 0;
   uint32_t nm = 0;
   const unsigned long long live = __ballot(act);
@@ -322,7 +336,8 @@ __global__ __launch_bounds__(64) void loop_replay(LoopParams p) {
   for (int32_t w = 0; w < p.n_windows; ++w) {
     const int32_t w_end = (w + 1) * W;
     uint32_t P = 0, D = 0;
-    int64_t eA = 0, eW = 0, dA = 0, dW = 0;
+    int64_t eA = 0, eW = 0;
+    int32_t dA = 0, dW = 0;
     bool idle = true;
     if (act) {
       // arrivals: a request waits from its arrival
@@ -334,7 +349,7 @@ __global__ __launch_bounds__(64) void loop_replay(LoopParams p) {
         a0 = a1;
         a1 = a2;
         a2 = a3;
-        a3 = next_arr + 3 < q1 ? p.arrival[next_arr + 3] : kNever;
+        a3 = arr(next_arr + 3);
       }
     }
     // ---- starts, in arrival order, on the slot that frees first. A lane
@@ -366,8 +381,8 @@ __global__ __launch_bounds__(64) void loop_replay(LoopParams p) {
           const uint32_t pt = po & 0xffffu, out_tok = po >> 16;
           const uint32_t npf = div_p(pt), prem = pt - npf * (uint32_t)p.pchunk;
           const uint32_t ndf = div_d(out_tok), drem = out_tok - ndf * (uint32_t)p.dchunk;
-          const uint32_t t_prem = prem ? (uint32_t)ceil_ms(prem, sv.prefill_us) : 0u;
-          const uint32_t t_drem = drem ? (uint32_t)ceil_ms(drem, sv.decode_us) : 0u;
+          const uint32_t t_prem = prem ? (uint32_t)ceil_ms(prem, cst[2 * M]) : 0u;
+          const uint32_t t_drem = drem ? (uint32_t)ceil_ms(drem, cst[3 * M]) : 0u;
           const uint32_t td = (uint32_t)st + npf * (uint32_t)p_full + t_prem;  // end of the prompt
           const uint32_t tt = td + ndf * (uint32_t)d_full + t_drem;            // the last output chunk
           if (tt < udur) {  // FINISH: active -> gone
@@ -391,12 +406,12 @@ __global__ __launch_bounds__(64) void loop_replay(LoopParams p) {
               const int64_t t_first = (int64_t)td + (ndf ? d_full : (int64_t)t_drem);
               const uint32_t first_ch = ndf ? (uint32_t)p.dchunk : drem;
               const int64_t ttft = t_first - a, e2e = (int64_t)tt - a, after = (int64_t)out_tok - first_ch;
-              bool good = (double)ttft <= sl.ttft_ms && (double)e2e <= sl.e2e_ms;
-              if (after > 0) good = good && (double)((int64_t)tt - t_first) / (double)after <= sl.tpot_ms;
+              bool good = (double)ttft <= slo_t[0] && (double)e2e <= slo_t[2 * M];
+              if (after > 0) good = good && (double)((int64_t)tt - t_first) / (double)after <= slo_t[M];
               ++n_done;
               n_ok += good ? 1u : 0u;
               e2e_sum += e2e;
-              e2e_max = e2e > e2e_max ? e2e : e2e_max;
+              e2e_max = e2e > (int64_t)e2e_max ? (int32_t)e2e : e2e_max;
             }
           }
           slot.replace_top(ns, tt);  // tt >= st >= the root
@@ -509,21 +524,21 @@ __global__ __launch_bounds__(64) void loop_replay(LoopParams p) {
         fe = far_load(&fc->e_fin);
       }
       // the window's tallies, Eq. (1) and the smoothing
-      const int64_t A_int = (int64_t)W * cA + eA, W_int = (int64_t)W * cW + eW;
+      const int64_t A_int = (int64_t)W * cA + eA, W_int = (int64_t)W * cW + eW;  // counts below 2^31
       cA += dA;
       cW += dW;
       idle = P == 0 && D == 0 && A_int == 0 && W_int == 0;
       if (!idle) {
-        double num = pr.w_p * (double)P;
+        double num = w_p * (double)P;
         num = num + (double)D;
         num = num * 1000.0;
-        const double q = pr.w_q * (double)W_int;
+        const double q = w_q * (double)W_int;
         double den = (double)A_int + q;
         if (den < (double)W) den = (double)W;
         const double raw = num / den;
         if (init) {
-          const double t1 = pr.alpha * raw;
-          const double t2 = (1.0 - pr.alpha) * S;
+          const double t1 = alpha * raw;
+          const double t2 = (1.0 - alpha) * S;
           S = t1 + t2;
         } else {
           S = raw;
@@ -536,6 +551,9 @@ __global__ __launch_bounds__(64) void loop_replay(LoopParams p) {
     // ---- tick: the controller's rules on this window's TSS
     const bool fast = (w + 1) % p.fast_w == 0, slow = (w + 1) % p.slow_w == 0;
     if (!fast && !slow) continue;
+    const tre_profile prt = p.prof[tm];  // the thresholds, read at ticks only
+    const double theta_eff = prt.theta * sc.theta_scale;
+    const double tau_c = sc.tau_crit_override >= 0.0 ? sc.tau_crit_override : prt.tau_crit;
     const double Z = (act && !idle && init) ? S / theta_eff : INFINITY;  // Eq. (2)
     const unsigned long long crit = __ballot(act && Z < tau_c);
     unsigned long long ok;
@@ -550,7 +568,7 @@ __global__ __launch_bounds__(64) void loop_replay(LoopParams p) {
     } else {
       continue;
     }
-    const unsigned long long sur = __ballot(act && Z > pr.tau_surplus);
+    const unsigned long long sur = __ballot(act && Z > prt.tau_surplus);
     unsigned long long used = 0ull;
     int pops = 0, pushes = 0;  // this tick's slot changes of this lane (a model moves at most once per tick)
     for (uint32_t k = 0; k < sc.max_moves; ++k) {
@@ -562,7 +580,7 @@ __global__ __launch_bounds__(64) void loop_replay(LoopParams p) {
         d = TRE_DONOR_POOL;
       } else {
         const double Zr = lane_f64(Z, r);
-        const unsigned long long cd = __ballot(act && R > pr.r_min && Z > Zr) & ~crit & ~used & ~(1ull << r) & live;
+        const unsigned long long cd = __ballot(act && R > prt.r_min && Z > Zr) & ~crit & ~used & ~(1ull << r) & live;
         d = pick_lane<true>(cd & sur, Z, lane);
         if (d < 0) d = pick_lane<true>(cd & ~sur, Z, lane);
         if (d < 0) break;
@@ -589,8 +607,10 @@ __global__ __launch_bounds__(64) void loop_replay(LoopParams p) {
       ++nm;
     }
     if (__ballot(pops > 0 || pushes > 0)) {
-      // the donors' earliest-free slots leave their heaps; every heap moves
-      // to the other pool, packed again; the receivers' slots join there
+      // the donors' earliest-free slots leave their heaps; every heap is
+      // packed again (through the scratch: each lane copies its own heap out,
+      // then, after every lane's reads, back in at its new place); the
+      // receivers' slots join there
       const Heap old = heap();
       for (int q = 0; q < pops && hs > 0; ++q) {
         --hs;
@@ -603,14 +623,15 @@ __global__ __launch_bounds__(64) void loop_replay(LoopParams p) {
         if (lane >= o) incl += v;
       }
       const int nbase = incl - want + mc;
-      uint32_t* nxt = (pb ? pool0 : pool1) + nbase;
+      uint32_t* tmp = p.scratch + (uint64_t)s * p.pool_words + nbase;
       if (act)
-        for (int i = 0; i < hs; ++i) nxt[i] = old.at(i);
-      const Heap fresh{nxt};
+        for (int i = 0; i < hs; ++i) tmp[i] = old.at(i);
+      const Heap fresh{hpool + nbase};
+      if (act)
+        for (int i = 0; i < hs; ++i) fresh.at(i) = tmp[i];
       for (int q = 0; q < pushes; ++q) fresh.push(hs + q, (uint32_t)w_end);
       hs += pushes;
       base = nbase;
-      pb ^= 1;
       bf = act && hs > 0 ? fresh.at(0) : kNone;
     }
   }
@@ -623,7 +644,7 @@ __global__ __launch_bounds__(64) void loop_replay(LoopParams p) {
     st.n_done = n_done;
     st.n_ok = n_ok;
     st.e2e_sum = e2e_sum;
-    st.e2e_max = e2e_max;
+    st.e2e_max = (int64_t)e2e_max;
     p.stats[(uint64_t)s * M + lane] = st;
   }
   if (lane == 0) p.n_moves[s] = nm;
@@ -660,11 +681,12 @@ int pool_words(const tre_trace_cfg* cfg, const tre_loop_requests* rq) {
   return (int)(((int64_t)pool_reps(cfg, rq) * rq->slots_per_replica + cfg->n_models + 3) & ~3ll);
 }
 
-// LDS bytes of one scenario: per model the slots, the four planes of the
-// near ring, the staged requests (arrival, prompt and output), the recorded
-// starts, the model's chunk offset and count, its chunk times and rates
+// LDS bytes of one scenario: the slot heaps' pool, then per model its SLO
+// bounds, the four planes of the near ring, the staged requests (arrival,
+// prompt and output), the recorded starts, the model's chunk offset and
+// count, its chunk times and rates
 size_t lds_bytes(const tre_trace_cfg* cfg, const tre_loop_requests* rq) {
-  return (2 * (size_t)pool_words(cfg, rq) + (size_t)(4 * kNear + 2 * kStage + 4 * kEnt + 2 + 4) * cfg->n_models) * 4;
+  return ((size_t)pool_words(cfg, rq) + (size_t)(6 + 4 * kNear + 2 * kStage + 4 * kEnt + 2 + 4) * cfg->n_models) * 4;
 }
 
 // x / d == (x * m) >> sh for x < 2^32: m = ceil(2^(32 + l) / d), 2^l >= d
@@ -704,7 +726,8 @@ extern "C" int tre_loop_workspace_size(const tre_trace_cfg* cfg, const tre_loop_
   if (!bytes) return fail(TRE_EINVAL, "tre_loop_workspace_size: NULL bytes");
   const int rc = check_loop_args(cfg, rq);
   if (rc) return rc;
-  *bytes = (size_t)(256 + (uint64_t)n_scenarios * cfg->n_models * ring_len(cfg, rq) * sizeof(FarCell));
+  *bytes = (size_t)(256 + (uint64_t)n_scenarios * cfg->n_models * ring_len(cfg, rq) * sizeof(FarCell) +
+                    (uint64_t)n_scenarios * pool_words(cfg, rq) * 4);
   return TRE_OK;
 }
 
@@ -730,6 +753,7 @@ extern "C" int tre_loop(const tre_trace_cfg* cfg, uint32_t n_traces, const tre_l
   char* base = (char*)ws;
   unsigned long long* overflow = (unsigned long long*)base;
   FarCell* far = (FarCell*)(base + 256);
+  uint32_t* scratch = (uint32_t*)(base + 256 + (uint64_t)n_scenarios * M * L * sizeof(FarCell));
   const size_t lds = lds_bytes(cfg, rq);
   HIP_TRY(hipFuncSetAttribute((const void*)loop_replay, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
   hipLaunchKernelGGL(zero_u64, dim3(1), dim3(1), 0, st, overflow);
@@ -749,6 +773,7 @@ extern "C" int tre_loop(const tre_trace_cfg* cfg, uint32_t n_traces, const tre_l
   lp.stats = stats;
   lp.tss64 = tss64;
   lp.far = far;
+  lp.scratch = scratch;
   lp.overflow = overflow;
   lp.move_cap = out->move_cap;
   lp.n_sc = n_scenarios;
