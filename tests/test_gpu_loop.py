@@ -7,8 +7,8 @@ oracle's, and no event may fall outside the ring of future windows.
 
 Inputs: the tiny and bursty workloads' request tables (the same arrivals and
 lengths as their traces) under scenario tables with 0 to 4 moves per tick,
-spare budget and replica caps that bind; budgets above n_models * r_cap; the
-oracle's hand cases; 1, 17 and 64 models; one and three slots per replica;
+spare budget and replica caps that bind; budgets above n_models * r_cap; an
+empty request table and models without requests; the oracle's hand cases; 1, 17 and 64 models; one and three slots per replica;
 argument errors (including slot heaps beyond the LDS).
 """
 import sys
@@ -199,6 +199,20 @@ def test_budget_above_the_replica_caps(lib):
         say(f"r_cap {r_cap}, slots per replica {spr}, budget {cfg['budget']}")
         _check(lib, f"cap{r_cap}-spr{spr}", cfg, tables, prof, w.slo_columns(1), w.service_columns(1),
                _scenarios(rng, 6, 1, ks=(1, 2, 4)), spr=spr, r_cap=r_cap)
+
+
+def test_empty_tables(lib):
+    """A trace with no requests, and models with none in the others."""
+    w = tg.standard(3).scaled(n_traces=3, duration_ms=300_000)
+    tables = [w.requests(t) for t in range(3)]
+    empty = {k: v[:0] for k, v in tables[0].items()}
+    keep = np.asarray(tables[2]["model"]) % 4 != 1  # models 1, 5, 9, 13 get nothing
+    thin = {k: np.asarray(v)[keep] for k, v in tables[2].items()}
+    tables = [tables[1], empty, thin]
+    rng = np.random.default_rng(9)
+    cfg = dict(w.trace_cfg(), budget=w.budget + 2)
+    _check(lib, "empty", cfg, tables, w.profile_columns(3), w.slo_columns(3), w.service_columns(3),
+           _scenarios(rng, 9, 3))
 
 
 def test_argument_errors(lib):
