@@ -455,7 +455,8 @@ def calibrate_main(args, w, dt, device, tre, torch, np):
     calib_only = [k for k in CALIB_KERNELS if k != "tss_stream"]
     dom = max(calib_only, key=lambda k: kms[k])
     roofline = {"bound": "hbm", "achieved": kernels[dom]["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(kernels[dom]["gbs"] / HBM_PEAK_GBS, 4), "traffic": None, "kernel": dom,
+                "frac": round(kernels[dom]["gbs"] / HBM_PEAK_GBS, 4),
+                "traffic": calib_traffic_for(w.name, dt.n_events, dom), "kernel": dom,
                 "kernel_ms": kernels[dom]["ms"], "alg_bytes_per_launch": alg[dom]}
     log("kernels " + ", ".join(f"{k} {kms[k]:.3f} ms" for k in CALIB_KERNELS) + f"; step {step_ms:.3f} ms")
     cpu = parity = None
@@ -617,6 +618,19 @@ def stage_cpu_leg(w, sample, out, threads):
     parity = {"traces_checked": len(sample), "mismatches": bad, "bit_exact": bad == 0}
     log(f"cpu oracle (stage shares): {cpu['value']:.3g} events/s on {n_workers} threads; parity {parity}")
     return cpu, parity
+
+
+def calib_traffic_for(workload_name: str, events: int, kernel: str):
+    """HBM bytes per launch of a calibration kernel from committed counters
+    taken on this kernel source and workload; else None."""
+    try:
+        t = json.load(open(os.path.join(ROOT, "profiles", "calib_traffic.json")))
+    except (OSError, ValueError):
+        return None
+    src = os.path.join(ROOT, "paper_2609_29160_amd", "csrc", "calib.hip")
+    if t.get("kernel_sha") != kernel_sha(src) or t.get("workload") != workload_name or t.get("events") != events:
+        return None
+    return t.get("traffic_bytes_per_launch", {}).get(kernel)
 
 
 def copy_calibration(gb, torch):
