@@ -98,6 +98,10 @@ class Oracle:
             L.oracle_loop.restype = ctypes.c_int
             L.oracle_loop.argtypes = ([i64, i64, i64, i64, i32, i32, vp, vp, vp, vp, i32, i32, i32, i32, vp, vp, vp, vp,
                                        vp, u32, vp, vp, vp, vp, vp, vp, vp, i64, vp, vp, vp, vp])
+            L.oracle_loop_act.restype = ctypes.c_int
+            L.oracle_loop_act.argtypes = ([i64, i64, i64, i64, i32, i32, vp, vp, vp, vp, i32, i32, i32, i32, vp, vp, vp,
+                                           vp, i64, i64, vp, vp, vp, u32, vp, vp, vp, vp, vp, vp, vp, vp, vp, i64, vp,
+                                           vp, vp, vp])
         self.has_stage = hasattr(L, "oracle_stage_tss")
         if self.has_stage:
             L.oracle_stage_raw_prefill.restype = f64
@@ -204,10 +208,13 @@ class Oracle:
     def loop(self, cfg: Dict[str, int], prof: np.ndarray, sc: np.ndarray, slo: np.ndarray, svc: np.ndarray,
              reqs: Dict[str, np.ndarray], spr: int = 8, r_cap: int = 16, prefill_chunk: int = 2048,
              decode_chunk: int = 24, move_cap: Optional[int] = None, want_events: bool = False,
-             want_tss: bool = False) -> Dict[str, np.ndarray]:
+             want_tss: bool = False, wake_w: int = 0, sleep_w: int = 0, footprint: Optional[np.ndarray] = None,
+             veto: Optional[np.ndarray] = None) -> Dict[str, np.ndarray]:
         """Closed-loop replay of one scenario over one trace's request table
         (arrival_ms, model, prompt, output; model by model, arrivals in
-        order within a model)."""
+        order within a model). With wake_w / sleep_w (whole windows),
+        footprint [M] (GPUs per replica, the budget then in GPUs) or veto
+        [n_ticks] (uint64 donor-release masks), the actuation model."""
         prof = np.ascontiguousarray(prof, dtype=PROFILE_DTYPE)
         sc = np.ascontiguousarray(np.atleast_1d(sc), dtype=SCENARIO_DTYPE)
         slo = np.ascontiguousarray(slo, dtype=SLO_DTYPE)
@@ -238,19 +245,31 @@ class Oracle:
             ev = {"ts": np.zeros(cap, np.int64), "model": np.zeros(cap, np.uint8), "type": np.zeros(cap, np.uint8),
                   "tokens": np.zeros(cap, np.uint16)}
         ptr = lambda a: None if a is None else a.ctypes.data
-        rc = self.L.oracle_loop(
-            cfg["window_ms"], cfg["duration_ms"], cfg["fast_period_ms"], cfg["slow_period_ms"], M, cfg["budget"],
-            prof.ctypes.data, sc.ctypes.data, slo.ctypes.data, svc.ctypes.data, spr, r_cap, prefill_chunk,
-            decode_chunk, req_off.ctypes.data, arr.ctypes.data, pr.ctypes.data, ou.ctypes.data, moves.ctypes.data,
-            move_cap, n_moves.ctypes.data, r_final.ctypes.data, r_windows.ctypes.data, stats.ctypes.data, ptr(S),
-            ptr(fl), n_ev.ctypes.data, cap, ptr(None if ev is None else ev["ts"]),
-            ptr(None if ev is None else ev["model"]), ptr(None if ev is None else ev["type"]),
-            ptr(None if ev is None else ev["tokens"]))
+        act = wake_w or sleep_w or footprint is not None or veto is not None
+        idle = np.zeros(1, np.int64)
+        held = np.zeros(M, np.int32)
+        evp = [ptr(None if ev is None else ev[k]) for k in ("ts", "model", "type", "tokens")]
+        common = (cfg["window_ms"], cfg["duration_ms"], cfg["fast_period_ms"], cfg["slow_period_ms"], M, cfg["budget"],
+                  prof.ctypes.data, sc.ctypes.data, slo.ctypes.data, svc.ctypes.data, spr, r_cap, prefill_chunk,
+                  decode_chunk, req_off.ctypes.data, arr.ctypes.data, pr.ctypes.data, ou.ctypes.data)
+        if act:
+            fp = None if footprint is None else np.ascontiguousarray(footprint, np.int32)
+            vt = None if veto is None else np.ascontiguousarray(veto, np.uint64)
+            rc = self.L.oracle_loop_act(*common, int(wake_w), int(sleep_w), ptr(fp), ptr(vt), moves.ctypes.data,
+                                        move_cap, n_moves.ctypes.data, r_final.ctypes.data, r_windows.ctypes.data,
+                                        stats.ctypes.data, idle.ctypes.data, held.ctypes.data, ptr(S), ptr(fl),
+                                        n_ev.ctypes.data, cap, *evp)
+        else:
+            rc = self.L.oracle_loop(*common, moves.ctypes.data, move_cap, n_moves.ctypes.data, r_final.ctypes.data,
+                                    r_windows.ctypes.data, stats.ctypes.data, ptr(S), ptr(fl), n_ev.ctypes.data, cap,
+                                    *evp)
         if rc:
             raise ValueError(f"oracle_loop rejected the scenario ({rc})")
         n = int(n_moves[0])
         out = {"moves": moves[:min(n, move_cap)].copy(), "n_moves": n, "r_final": r_final, "r_windows": r_windows,
                "stats": stats, "n_events": int(n_ev[0])}
+        if act:
+            out["idle_final"], out["held_final"] = int(idle[0]), held
         if want_tss:
             out["S"], out["flags"] = S, fl
         if want_events:

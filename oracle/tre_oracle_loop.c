@@ -38,7 +38,16 @@
  *     the base rule (idle budget first, surplus then nominal donors, up to
  *     K moves per tick, each model in at most one move per tick);
  *   - latency outcomes as in the calibration sweep: a request whose FINISH
- *     is in the trace is judged (TTFT, E2E, TPOT against its model's SLO).
+ *     is in the trace is judged (TTFT, E2E, TPOT against its model's SLO);
+ *   - with the actuation model (oracle_loop_act), the actuation replay's
+ *     rules (tre_oracle_act.c): the budget in GPUs with g_m GPUs per
+ *     replica, a woken replica routable wake_w windows after its wake
+ *     starts (its slots free from the start of the window after its wake
+ *     completes), a donor's replica hidden at once (its earliest-free slots
+ *     leave at the move) with its GPUs reaching the receiver after sleep_w
+ *     windows, when the receiver's wake starts, a model with a transition
+ *     in flight neither receiver nor donor, vetoed models not released; with
+ *     no delays, unit footprints and no vetoes it is the plain closed loop.
  */
 #include <math.h>
 #include <stdint.h>
@@ -56,6 +65,9 @@
 #define OL_IDLE 1
 #define OL_INIT 2
 #define OL_MAX_MODELS 256
+#define OL_NONE 0
+#define OL_WAKE 1
+#define OL_SLEEP 2
 
 typedef struct {
   double w_p, w_q, alpha, theta, tau_crit, tau_surplus;
@@ -179,33 +191,44 @@ static int settle(evbuf* fin, evbuf* pend, int64_t t_end) {
 }
 
 /*
- * Closed-loop replay of one scenario over one trace's requests.
- * req_off [M+1]: requests of model m are [req_off[m], req_off[m+1]) of
- * arrival_ms / prompt / output, in arrival order. Outputs as the base
- * replay (moves, n_moves, r_final, r_windows), per-model stats [M], and
- * optionally the whole trace's smoothed TSS and flags [n_windows][M], its
- * event count and its events (when they fit ev_cap). Returns 0, -1 on bad
- * arguments, -2 out of memory, -4 if the initial replicas exceed the
- * budget.
+ * Closed-loop replay of one scenario over one trace's requests, with the
+ * actuation model. req_off [M+1]: requests of model m are
+ * [req_off[m], req_off[m+1]) of arrival_ms / prompt / output, in arrival
+ * order. wake_w, sleep_w: delays in whole windows; footprint [M] GPUs per
+ * replica (NULL: 1), the budget then in GPUs; veto [n_ticks] donor-release
+ * masks (NULL: none). Outputs as the base replay (moves, n_moves, r_final
+ * counting transitions completed by the end of the last window,
+ * r_windows), per-model stats [M], optionally the idle GPUs at the end and
+ * the GPUs transitions still in flight hold ([M]), the whole trace's
+ * smoothed TSS and flags [n_windows][M], its event count and its events
+ * (when they fit ev_cap). Returns 0, -1 on bad arguments, -2 out of
+ * memory, -4 if the initial replicas exceed the budget.
  */
-int oracle_loop(int64_t window_ms, int64_t duration_ms, int64_t fast_ms, int64_t slow_ms, int32_t M,
-                int32_t budget, const ol_profile* prof, const ol_scenario* sc, const ol_slo* slo,
-                const ol_svc* svc, int32_t spr, int32_t r_cap, int32_t prefill_chunk, int32_t decode_chunk,
-                const int64_t* req_off, const int64_t* arrival_ms, const uint16_t* prompt,
-                const uint16_t* output, ol_move* moves, uint32_t move_cap, uint32_t* n_moves,
-                int32_t* r_final, int64_t* r_windows, ol_stats* stats, double* S_out, uint8_t* flags_out,
-                int64_t* n_events_out, int64_t ev_cap, int64_t* ev_ts, uint8_t* ev_model, uint8_t* ev_type,
-                uint16_t* ev_tokens) {
+int oracle_loop_act(int64_t window_ms, int64_t duration_ms, int64_t fast_ms, int64_t slow_ms, int32_t M,
+                    int32_t budget, const ol_profile* prof, const ol_scenario* sc, const ol_slo* slo,
+                    const ol_svc* svc, int32_t spr, int32_t r_cap, int32_t prefill_chunk, int32_t decode_chunk,
+                    const int64_t* req_off, const int64_t* arrival_ms, const uint16_t* prompt,
+                    const uint16_t* output, int64_t wake_w, int64_t sleep_w, const int32_t* footprint,
+                    const uint64_t* veto, ol_move* moves, uint32_t move_cap, uint32_t* n_moves, int32_t* r_final,
+                    int64_t* r_windows, ol_stats* stats, int64_t* idle_final, int32_t* held_final, double* S_out,
+                    uint8_t* flags_out, int64_t* n_events_out, int64_t ev_cap, int64_t* ev_ts, uint8_t* ev_model,
+                    uint8_t* ev_type, uint16_t* ev_tokens) {
   if (window_ms <= 0 || duration_ms % window_ms || fast_ms <= 0 || slow_ms <= 0 || M < 1 ||
-      M > OL_MAX_MODELS || spr < 1 || r_cap < 1 || prefill_chunk < 1 || decode_chunk < 1)
+      M > OL_MAX_MODELS || spr < 1 || r_cap < 1 || prefill_chunk < 1 || decode_chunk < 1 || wake_w < 0 ||
+      sleep_w < 0)
     return -1;
   const int64_t nW = duration_ms / window_ms;
-  int32_t R[OL_MAX_MODELS];
-  int64_t idle = budget;
+  int32_t R[OL_MAX_MODELS], g[OL_MAX_MODELS], kind[OL_MAX_MODELS];
+  int64_t until[OL_MAX_MODELS], ret[OL_MAX_MODELS];
+  int64_t idle = budget;  /* idle GPUs */
   for (int m = 0; m < M; ++m) {
     R[m] = prof[m].r_init;
-    if (R[m] < 0 || R[m] > r_cap) return -1;
-    idle -= R[m];
+    g[m] = footprint ? footprint[m] : 1;
+    if (R[m] < 0 || R[m] > r_cap || g[m] < 1) return -1;
+    idle -= (int64_t)g[m] * R[m];
+    kind[m] = OL_NONE;
+    until[m] = -1;
+    ret[m] = 0;
     r_windows[m] = 0;
     memset(&stats[m], 0, sizeof(ol_stats));
   }
@@ -238,8 +261,23 @@ int oracle_loop(int64_t window_ms, int64_t duration_ms, int64_t fast_ms, int64_t
     next_start[m] = req_off[m];
   }
   uint32_t nm = 0;
+  int64_t tick = 0;
   for (int64_t w = 0; w < nW; ++w) {
     const int64_t w_end = (w + 1) * window_ms;
+    /* transitions that completed at the end of an earlier window: a woken
+       replica's slots are free from the start of this window */
+    for (int m = 0; m < M; ++m) {
+      if (kind[m] != OL_NONE && until[m] < w) {
+        if (kind[m] == OL_WAKE) {
+          for (int q = 0; q < spr; ++q) slot[m][(int64_t)R[m] * spr + q] = w * window_ms;
+          R[m] += 1;
+        } else {
+          idle += ret[m];
+        }
+        kind[m] = OL_NONE;
+        ret[m] = 0;
+      }
+    }
     for (int m = 0; m < M; ++m) {
       /* arrivals in this window */
       while (next_arr[m] < req_off[m + 1] && arrival_ms[next_arr[m]] < w_end) {
@@ -300,6 +338,8 @@ int oracle_loop(int64_t window_ms, int64_t duration_ms, int64_t fast_ms, int64_t
     for (int m = 0; m < M; ++m) r_windows[m] += R[m];
     const int fast = w_end % fast_ms == 0, slow = w_end % slow_ms == 0;
     if (!fast && !slow) continue;
+    const uint64_t vetoed = veto ? veto[tick] : 0u;
+    tick += 1;
     /* the TSS of window w from the events final by its end */
     if (settle(&fin, &pend, w_end)) { rc = -2; goto done; }
     if (oracle_tss_trace(fin.ts, fin.model, fin.type, fin.tokens, (int64_t)fin.n, window_ms, duration_ms, M,
@@ -308,7 +348,7 @@ int oracle_loop(int64_t window_ms, int64_t duration_ms, int64_t fast_ms, int64_t
       goto done;
     }
     double Z[OL_MAX_MODELS];
-    int crit[OL_MAX_MODELS], surplus[OL_MAX_MODELS], ok[OL_MAX_MODELS], used[OL_MAX_MODELS];
+    int crit[OL_MAX_MODELS], surplus[OL_MAX_MODELS], ok[OL_MAX_MODELS];
     int any_crit = 0;
     for (int m = 0; m < M; ++m) {
       const uint8_t f = fl[w * M + m];
@@ -317,7 +357,6 @@ int oracle_loop(int64_t window_ms, int64_t duration_ms, int64_t fast_ms, int64_t
       crit[m] = Z[m] < tau_c;
       surplus[m] = Z[m] > prof[m].tau_surplus;
       any_crit |= crit[m];
-      used[m] = 0;
     }
     int path;
     if (any_crit) {
@@ -330,25 +369,33 @@ int oracle_loop(int64_t window_ms, int64_t duration_ms, int64_t fast_ms, int64_t
     } else {
       continue;
     }
+    /* a model in a move this tick, or with a transition in flight, has
+       kind != OL_NONE: neither receiver nor donor */
     for (uint32_t k = 0; k < sc->max_moves; ++k) {
       int r = -1;
       for (int m = 0; m < M; ++m)
-        if (ok[m] && !used[m] && R[m] < r_cap && (r < 0 || Z[m] < Z[r])) r = m;
+        if (ok[m] && kind[m] == OL_NONE && R[m] < r_cap && (r < 0 || Z[m] < Z[r])) r = m;
       if (r < 0) break;
       int d = OL_POOL;
-      if (idle > 0) {
-        idle -= 1;
+      if (idle >= g[r]) {
+        idle -= g[r];
+        kind[r] = OL_WAKE;
+        until[r] = w + wake_w;
       } else {
         int best = -1;
         for (int pass = 0; pass < 2 && best < 0; ++pass) {
           for (int m = 0; m < M; ++m) {
             const int in_class = pass == 0 ? surplus[m] : (!crit[m] && !surplus[m]);
-            if (!in_class || used[m] || m == r || R[m] <= prof[m].r_min || !(Z[m] > Z[r])) continue;
+            if (!in_class || kind[m] != OL_NONE || m == r || R[m] <= prof[m].r_min || !(Z[m] > Z[r]) ||
+                ((vetoed >> m) & 1u) || idle < (int64_t)g[r] - g[m])
+              continue;
             if (best < 0 || Z[m] > Z[best]) best = m;
           }
         }
         if (best < 0) break;
         d = best;
+        const int64_t short_by = (int64_t)g[r] - g[d];
+        if (short_by > 0) idle -= short_by;
         /* the donor's replica: its spr slots that free first leave */
         for (int q = 0; q < spr; ++q) {
           int64_t ns = (int64_t)R[d] * spr - q, lo = 0;
@@ -358,11 +405,12 @@ int oracle_loop(int64_t window_ms, int64_t duration_ms, int64_t fast_ms, int64_t
           for (int64_t x = lo; x + 1 < ns; ++x) slot[d][x] = slot[d][x + 1];
         }
         if (R[d] > 0) R[d] -= 1;  /* always: a donor is above its floor */
-        used[d] = 1;
+        kind[d] = OL_SLEEP;
+        until[d] = w + sleep_w;
+        ret[d] = short_by < 0 ? -short_by : 0;
+        kind[r] = OL_WAKE;
+        until[r] = w + sleep_w + wake_w;
       }
-      for (int q = 0; q < spr; ++q) slot[r][(int64_t)R[r] * spr + q] = w_end;
-      R[r] += 1;
-      used[r] = 1;
       if (nm < move_cap) {
         moves[nm].window = (uint32_t)w;
         moves[nm].path = (uint8_t)path;
@@ -374,7 +422,20 @@ int oracle_loop(int64_t window_ms, int64_t duration_ms, int64_t fast_ms, int64_t
     }
   }
   *n_moves = nm;
-  for (int m = 0; m < M; ++m) r_final[m] = R[m];
+  /* transitions completing at the end of the last window count as done */
+  for (int m = 0; m < M; ++m) {
+    if (kind[m] != OL_NONE && until[m] < nW) {
+      if (kind[m] == OL_WAKE) R[m] += 1;
+      else idle += ret[m];
+      kind[m] = OL_NONE;
+      ret[m] = 0;
+    }
+  }
+  for (int m = 0; m < M; ++m) {
+    r_final[m] = R[m];
+    if (held_final) held_final[m] = kind[m] == OL_WAKE ? g[m] : (kind[m] == OL_SLEEP ? (int32_t)ret[m] : 0);
+  }
+  if (idle_final) *idle_final = idle;
   if (settle(&fin, &pend, duration_ms)) { rc = -2; goto done; }
   if (n_events_out) *n_events_out = (int64_t)fin.n;
   if (ev_ts && (int64_t)fin.n <= ev_cap) {
@@ -407,4 +468,19 @@ done:
   ev_free(&fin);
   ev_free(&pend);
   return rc;
+}
+
+/* the closed loop with instantaneous actuation, unit footprints, no vetoes */
+int oracle_loop(int64_t window_ms, int64_t duration_ms, int64_t fast_ms, int64_t slow_ms, int32_t M,
+                int32_t budget, const ol_profile* prof, const ol_scenario* sc, const ol_slo* slo,
+                const ol_svc* svc, int32_t spr, int32_t r_cap, int32_t prefill_chunk, int32_t decode_chunk,
+                const int64_t* req_off, const int64_t* arrival_ms, const uint16_t* prompt,
+                const uint16_t* output, ol_move* moves, uint32_t move_cap, uint32_t* n_moves,
+                int32_t* r_final, int64_t* r_windows, ol_stats* stats, double* S_out, uint8_t* flags_out,
+                int64_t* n_events_out, int64_t ev_cap, int64_t* ev_ts, uint8_t* ev_model, uint8_t* ev_type,
+                uint16_t* ev_tokens) {
+  return oracle_loop_act(window_ms, duration_ms, fast_ms, slow_ms, M, budget, prof, sc, slo, svc, spr, r_cap,
+                         prefill_chunk, decode_chunk, req_off, arrival_ms, prompt, output, 0, 0, NULL, NULL, moves,
+                         move_cap, n_moves, r_final, r_windows, stats, NULL, NULL, S_out, flags_out, n_events_out,
+                         ev_cap, ev_ts, ev_model, ev_type, ev_tokens);
 }

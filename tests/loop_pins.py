@@ -9,7 +9,13 @@ oracle disagrees with something fixed independently of it:
 - a hand-derived case where a rescue adds a replica at a window end, the
   replica cap blocks a receiver, and a donor's slot leaves;
 - conservation (arrived / started / judged requests against the events);
-- more initial replicas never delay a request (FCFS on more servers).
+- more initial replicas never delay a request (FCFS on more servers);
+- with the actuation model: no delays, unit footprints and no vetoes give
+  the plain closed loop; the move log, replicas, replica-window sums and
+  GPU accounting equal the actuation replay (tre_oracle_act.c, itself
+  pinned) run over the closed loop's own final TSS; a hand-derived case
+  where the wake and sleep delays decide when a waiting request starts;
+  GPU conservation, no vetoed donor and at most K moves per tick.
 
 Readings followed (paper, Sections "Dual-Speed Control", "Bounded Pairwise
 Transfer", "System Boundary and Replica State"): FCFS per model on the slot
@@ -255,5 +261,121 @@ def pin_bad_arguments_are_rejected(o):
         raise AssertionError(f"accepted {kw} {c['budget']}")
 
 
+def _act_inputs(rng, w, nW_ticks):
+    M = w.n_models
+    g = rng.integers(1, 3, M).astype(np.int32)
+    veto = rng.integers(0, 1 << 62, nW_ticks, dtype=np.int64).astype(np.uint64) & np.uint64((1 << M) - 1)
+    veto[rng.random(nW_ticks) > 0.2] = 0
+    return g, veto
+
+
+def _n_ticks(cfg):
+    nW = cfg["duration_ms"] // cfg["window_ms"]
+    return sum(1 for x in range(nW) if ((x + 1) * cfg["window_ms"]) % cfg["fast_period_ms"] == 0
+               or ((x + 1) * cfg["window_ms"]) % cfg["slow_period_ms"] == 0)
+
+
+def pin_act_without_delays_is_the_plain_loop(o):
+    rng = np.random.default_rng(31)
+    for w, reqs in _workloads():
+        prof, slo, svc = _inputs(w)
+        for it in range(3):
+            sc = _sc(int(rng.choice([1, 2, 4])), float(rng.uniform(0.5, 2.0)))
+            cfg = dict(w.trace_cfg(), budget=int(prof["r_init"].sum()) + int(rng.integers(0, 4)))
+            a = o.loop(cfg, prof, sc, slo, svc, reqs, want_tss=True)
+            b = o.loop(cfg, prof, sc, slo, svc, reqs, want_tss=True, wake_w=0, sleep_w=0,
+                       footprint=np.ones(w.n_models, np.int32), veto=np.zeros(_n_ticks(cfg), np.uint64))
+            assert a["n_moves"] == b["n_moves"] and np.array_equal(a["moves"], b["moves"]), (w.name, it)
+            for k in ("r_final", "r_windows", "stats", "flags"):
+                assert np.array_equal(a[k], b[k]), (w.name, it, k)
+            assert np.array_equal(a["S"].view(np.uint64), b["S"].view(np.uint64)), (w.name, it)
+            assert b["idle_final"] == cfg["budget"] - int(b["r_final"].sum()) and not b["held_final"].any()
+
+
+def pin_act_moves_follow_the_actuation_replay(o):
+    """The closed loop decides on the TSS of its own service; replaying the
+    actuation rules (tre_oracle_act.c) over that TSS must give its moves."""
+    rng = np.random.default_rng(33)
+    for w, reqs in _workloads():
+        prof, slo, svc = _inputs(w)
+        total = 0
+        for it, (wake_w, sleep_w) in enumerate([(2, 3), (0, 4), (5, 0), (1, 1)]):
+            cfg = dict(w.trace_cfg())
+            g, veto = _act_inputs(rng, w, _n_ticks(cfg))
+            cfg["budget"] = int((g * prof["r_init"]).sum()) + int(rng.integers(0, 5))
+            sc = _sc(int(rng.choice([1, 2, 4])), float(rng.uniform(0.5, 2.0)))
+            r = o.loop(cfg, prof, sc, slo, svc, reqs, r_cap=10_000, want_tss=True, wake_w=wake_w, sleep_w=sleep_w,
+                       footprint=g, veto=veto)
+            a = o.control_act(cfg, prof, r["S"], r["flags"], sc, wake_w, sleep_w, footprint=g, veto=veto)
+            assert r["n_moves"] == a["n_moves"] and np.array_equal(r["moves"], a["moves"]), (w.name, it)
+            assert np.array_equal(r["r_final"], a["r_final"]) and np.array_equal(r["r_windows"], a["r_windows"])
+            assert r["idle_final"] == a["idle_final"] and np.array_equal(r["held_final"], a["held_final"])
+            total += r["n_moves"]
+        assert total > 0, f"{w.name}: the workload should see some moves"
+
+
+def pin_act_hand_wake_and_sleep_delays(o):
+    # The hand case above with wake_w = 2, sleep_w = 1, r_cap 3:
+    #  w0: r0 starts at 0 (FINISH 241); r1, r2 wait.
+    #  tick 0: rescue from the idle GPU: model 0's wake runs through
+    #    window 2, its slot is free from 300 (window 3).
+    #  ticks 1, 2: model 0 critical, but with a wake in flight: no receiver.
+    #  w2: r1 starts at 241 on r0's slot (FINISH 482).
+    #  w3: the new slot: r2 starts at 300 (FINISH 541).
+    #  tick 3: rescue, no idle GPU: donor model 1 (idle: surplus, above its
+    #    floor) hidden at once; its sleep runs through window 4, then model
+    #    0's wake through window 6: routable from window 7.
+    #  r_final [3, 0]; r_windows: model 0 1 x 3 + 2 x 4 + 3 x 3 = 20,
+    #  model 1 1 x 4 = 4; no GPU idle or held at the end.
+    cfg = {"window_ms": 100, "duration_ms": 1000, "fast_period_ms": 100, "slow_period_ms": 100,
+           "n_models": 2, "budget": 3}
+    prof = np.zeros(2, O.PROFILE_DTYPE)
+    prof["w_p"], prof["w_q"], prof["alpha"], prof["theta"] = 0.5, 2.0, 1.0, 1e12
+    prof["tau_crit"], prof["tau_surplus"], prof["r_min"], prof["r_init"] = 0.5, 1.5, 0, 1
+    slo = np.zeros(2, O.SLO_DTYPE)
+    slo["ttft_ms"] = slo["tpot_ms"] = slo["e2e_ms"] = 1e9
+    svc = np.zeros(2, O.SVC_DTYPE)
+    svc["prefill_us"], svc["decode_us"] = 1000, 10000
+    reqs = {"arrival_ms": np.zeros(3, np.int64), "model": np.zeros(3, np.uint8), "prompt": np.ones(3, np.uint16),
+            "output": np.full(3, 24, np.uint16)}
+    r = o.loop(cfg, prof, _sc(1), slo, svc, reqs, spr=1, r_cap=3, want_events=True, wake_w=2, sleep_w=1,
+               footprint=np.ones(2, np.int32))
+    mv = [(int(m["window"]), int(m["path"]), int(m["receiver"]), int(m["donor"])) for m in r["moves"]]
+    assert mv == [(0, RES, 0, POOL), (3, RES, 0, 1)], mv
+    ev = r["events"]
+    adm = sorted(int(t) for t, ty in zip(ev["ts"], ev["type"]) if ty == (P | ADMIT))
+    fin = sorted(int(t) for t, ty in zip(ev["ts"], ev["type"]) if ty == F)
+    assert adm == [0, 241, 300] and fin == [241, 482, 541], (adm, fin)
+    assert list(r["r_final"]) == [3, 0] and list(r["r_windows"]) == [20, 4]
+    assert r["idle_final"] == 0 and not r["held_final"].any()
+
+
+def pin_act_conservation(o):
+    rng = np.random.default_rng(35)
+    for w, reqs in _workloads():
+        prof, slo, svc = _inputs(w)
+        cfg = dict(w.trace_cfg())
+        nt = _n_ticks(cfg)
+        g, veto = _act_inputs(rng, w, nt)
+        cfg["budget"] = int((g * prof["r_init"]).sum()) + 3
+        K = 4
+        r = o.loop(cfg, prof, _sc(K, 1.5), slo, svc, reqs, wake_w=3, sleep_w=2, footprint=g, veto=veto)
+        assert r["idle_final"] + int((g * r["r_final"]).sum()) + int(r["held_final"].sum()) == cfg["budget"]
+        tick_of = {}
+        for x in range(cfg["duration_ms"] // cfg["window_ms"]):
+            if ((x + 1) * cfg["window_ms"]) % cfg["fast_period_ms"] == 0 or \
+               ((x + 1) * cfg["window_ms"]) % cfg["slow_period_ms"] == 0:
+                tick_of[x] = len(tick_of)
+        per_tick = {}
+        for m in r["moves"]:
+            wdw, d = int(m["window"]), int(m["donor"])
+            per_tick[wdw] = per_tick.get(wdw, 0) + 1
+            if d != POOL:
+                assert not (int(veto[tick_of[wdw]]) >> d) & 1, "a vetoed donor released"
+        assert max(per_tick.values(), default=0) <= K
+
+
 ALL = [pin_without_moves_equals_open_loop_service, pin_moves_equal_the_base_replay_over_the_loops_own_tss,
-       pin_hand_rescue_cap_and_donor, pin_donor_releases_its_earliest_free_slots, pin_conservation, pin_more_replicas_never_delay, pin_bad_arguments_are_rejected]
+       pin_hand_rescue_cap_and_donor, pin_donor_releases_its_earliest_free_slots, pin_conservation, pin_more_replicas_never_delay, pin_bad_arguments_are_rejected,
+       pin_act_without_delays_is_the_plain_loop, pin_act_moves_follow_the_actuation_replay,
+       pin_act_hand_wake_and_sleep_delays, pin_act_conservation]
