@@ -93,7 +93,8 @@ def main():
     ap.add_argument("--emit-tss", action="store_true", help="also write per-window fp32 TSS")
     ap.add_argument("--threads", type=int, default=None)
     ap.add_argument("--actuation", action="store_true",
-                    help="wake/sleep delays, 1-2 GPU footprints and vetoes (tre_sweep_act)")
+                    help="wake/sleep delays, 1-2 GPU footprints and vetoes (tre_sweep_act; with --loop, "
+                         "tre_loop_act)")
     ap.add_argument("--loop", action="store_true",
                     help="time the closed-loop replay (tre_loop) over the workload's request tables instead")
     ap.add_argument("--loop-cpu-scenarios", type=int, default=16,
@@ -287,12 +288,28 @@ def loop_main(args, w, tre, torch, np):
     class _Shape:
         n_models = M
 
+    act_in = None
+    if args.actuation:
+        act_in = actuation_inputs(w)
+        act_in["veto"] = actuation_vetoes(w, n_ticks)
+        act_in["g_dev"] = torch.from_numpy(act_in["g"]).cuda()
+        act_in["veto_dev"] = torch.from_numpy(act_in["veto"].view(np.int64)).cuda()
+        cfg = dict(cfg, budget=act_in["budget"])
+        act = tre.actuation(ACT_WAKE_MS, ACT_SLEEP_MS, act_in["g_dev"], act_in["veto_dev"])
+
+    def replay():
+        if act_in is None:
+            tre.tre_loop(cfg, T, rq, prof, sc, out, stats, ws)
+        else:
+            tre.tre_loop_act(cfg, T, rq, prof, sc, act, out, stats, ws)
+
     out = tre.ctl_outputs(_Shape(), n_sc, move_cap)
     stats = torch.zeros(n_sc * M * tre.LOOP_STATS_DTYPE.itemsize, dtype=torch.uint8, device="cuda")
     ws = torch.empty(tre.tre_loop_workspace_size(cfg, rq, n_sc), dtype=torch.uint8, device="cuda")
-    log(f"closed loop: {n_sc} scenarios, workspace {ws.numel() / 1e9:.2f} GB")
+    log(f"closed loop: {n_sc} scenarios, workspace {ws.numel() / 1e9:.2f} GB"
+        + ("" if act_in is None else f", actuation model (GPU budget {act_in['budget']})"))
     for _ in range(args.warmup):
-        tre.tre_loop(cfg, T, rq, prof, sc, out, stats, ws)
+        replay()
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
     tre.tre_set_timing(True)
@@ -302,7 +319,7 @@ def loop_main(args, w, tre, torch, np):
     torch.cuda.synchronize()
     e0.record(stream)
     for _ in range(args.steps):
-        tre.tre_loop(cfg, T, rq, prof, sc, out, stats, ws)
+        replay()
     e1.record(stream)
     torch.cuda.synchronize()
     tre.tre_set_timing(False)
@@ -315,7 +332,8 @@ def loop_main(args, w, tre, torch, np):
     log(f"step {step_ms:.3f} ms; loop_replay {kern_ms:.3f} ms; events beyond the ring {overflow}")
     cpu = parity = None
     if not args.no_cpu:
-        cpu, parity = loop_cpu_leg(w, tables, sc_cols, out, stats, move_cap, args.loop_cpu_scenarios, n_workers, tre)
+        cpu, parity = loop_cpu_leg(w, tables, sc_cols, out, stats, move_cap, args.loop_cpu_scenarios, n_workers, tre,
+                                   act_in)
     if args.copy_calib_gb > 0:
         del ws, out, stats, rq, keep
         torch.cuda.empty_cache()
@@ -329,7 +347,10 @@ def loop_main(args, w, tre, torch, np):
         "data": "synthetic (seeded generator; the paper's traces are not available)",
         "config": {"workload": w.name, "traces": T, "scenarios": n_sc, "models": M, "window_ms": w.window_ms,
                    "duration_s": w.duration_ms // 1000, "requests": int(n_req_trace.sum()), "logical_requests": logical,
-                   "slots_per_replica": 8, "r_cap": 16, "mode": "closed loop"},
+                   "slots_per_replica": 8, "r_cap": 16, "mode": "closed loop",
+                   "actuation": None if act_in is None else
+                   {"wake_ms": ACT_WAKE_MS, "sleep_ms": ACT_SLEEP_MS, "footprint_gpus": "1-2, seeded",
+                    "gpu_budget": act_in["budget"], "veto_ticks": "10%"}},
         "roofline": {"bound": "hbm", "achieved": round(alg / (kern_ms / 1e3) / 1e9, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(alg / (kern_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
                      "traffic": loop_traffic_for(w.name) if T == 4096 else None, "kernel": "loop_replay",
@@ -342,11 +363,12 @@ def loop_main(args, w, tre, torch, np):
     print(json.dumps(result), flush=True)
 
 
-def loop_cpu_leg(w, tables, sc_cols, out, stats, move_cap, n_sample, n_workers, tre):
+def loop_cpu_leg(w, tables, sc_cols, out, stats, move_cap, n_sample, n_workers, tre, act_in=None):
     """The oracle's closed-loop replay of the first n_sample scenarios on a
     pool of host threads (one scenario per call), timed like the other CPU
     legs; the GPU's moves, replicas and latency outcomes of those scenarios
-    must equal the oracle's."""
+    must equal the oracle's. With act_in, the oracle's replay under the same
+    actuation model (delays in whole windows, rounded up)."""
     from concurrent.futures import ThreadPoolExecutor
 
     import numpy as np
@@ -361,12 +383,18 @@ def loop_cpu_leg(w, tables, sc_cols, out, stats, move_cap, n_sample, n_workers, 
     svc_all = O.pack_svc(w.service_columns())
     sc_all = O.pack_scenarios(sc_cols)
     sample = list(range(min(n_sample, len(sc_all))))
+    kw_t = lambda t: {}
+    if act_in is not None:
+        cfg = dict(cfg, budget=act_in["budget"])
+        to_w = lambda ms: min(-(-ms // w.window_ms), w.n_windows + 1)
+        kw_t = lambda t: {"wake_w": to_w(ACT_WAKE_MS), "sleep_w": to_w(ACT_SLEEP_MS), "footprint": act_in["g"][t],
+                          "veto": act_in["veto"][t]}
 
     def one(s):
         c0 = time.thread_time()
         t = int(sc_all[s]["trace"])
         r = o.loop(cfg, prof_all[t * M:(t + 1) * M], sc_all[s:s + 1], slo_all[t * M:(t + 1) * M],
-                   svc_all[t * M:(t + 1) * M], tables[t], move_cap=move_cap)
+                   svc_all[t * M:(t + 1) * M], tables[t], move_cap=move_cap, **kw_t(t))
         return r, time.thread_time() - c0
 
     t0 = time.perf_counter()

@@ -459,6 +459,29 @@ int tre_loop(const tre_trace_cfg* cfg, uint32_t n_traces, const tre_loop_request
 int tre_stage_tss(const tre_events* ev, const tre_profile* prof, const tre_tss_out* tallies, double* stage64,
                   float* stage32, uint8_t* flags, void* stream);
 
+/* tre_loop with the actuation model (paper, Sections "System Boundary and
+   Replica State" and "Bounded Pairwise Transfer": transitions hide, drain,
+   sleep and wake replicas, budget-feasible in GPU footprints; act: host,
+   read during the call; its footprint and veto tables device
+   [n_traces][n_models] and [n_traces][n_ticks], either NULL). The budget
+   then counts GPUs, a replica of model
+   m holding footprint[m] (1 to budget); delays are whole windows rounded up
+   from wake_ms / sleep_ms, as tre_rebalance_act. A woken replica's slots
+   are free from the start of the window after its wake completes; a
+   donor's replica stops taking requests at the move (its slots that free
+   first leave) and its GPUs reach the receiver when its sleep completes,
+   when the receiver's wake starts; a model with a transition in flight is
+   neither receiver nor donor; veto bit m at a tick keeps model m from
+   releasing. r_final counts wakes completing by the end of the last
+   window. With zero delays, unit footprints and no vetoes the outputs
+   equal tre_loop's. Footprints outside 1 .. budget or initial replicas'
+   GPUs beyond the budget give unspecified results (never an access outside
+   the buffers). Same workspace as tre_loop; TRE_EINVAL also for a NULL act
+   or a negative delay. */
+int tre_loop_act(const tre_trace_cfg* cfg, uint32_t n_traces, const tre_loop_requests* rq, const tre_profile* prof,
+                 const tre_scenario* sc, uint32_t n_scenarios, const tre_actuation* act, const tre_ctl_out* out,
+                 tre_loop_stats* stats, double* tss64, void* ws, size_t ws_bytes, void* stream);
+
 /* Kernel timing (HIP events recorded around each launch on its stream).
    tre_set_timing(1) starts recording; tre_kernel_time waits for the
    recorded launches of `kernel` ("tss_stream", "rebalance", "validate",

@@ -80,6 +80,11 @@ struct LoopParams {
   double* tss64;                // [scenario][window][model] or NULL
   FarCell* far;                 // [scenario][ring_len][model]
   uint32_t* scratch;            // [scenario][pool_words]: heaps in transit at a repack
+  // the actuation model (the kAct instantiation)
+  const int32_t* footprint;     // [trace][M] GPUs per replica, or NULL (1); the budget is then in GPUs
+  const uint64_t* veto;         // [trace][n_ticks] donor releases refused, or NULL
+  int32_t wake_w, sleep_w;      // whole windows
+  int32_t n_ticks;
   unsigned long long* overflow; // events beyond the ring (declared bounds exceeded)
   uint32_t move_cap;
   uint32_t n_sc;
@@ -182,18 +187,31 @@ struct Heap {
 __device__ __forceinline__ void lds_add(uint32_t* a, uint32_t v) {
   __hip_atomic_fetch_add(a, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
+// a scenario's far ring is read and written by its own workgroup only, so
+// workgroup scope suffices (with agent scope the drain's loads and stores
+// carry the device-coherence bit, and the kernel writes a third more bytes
+// to HBM)
 __device__ __forceinline__ void far_add(uint32_t* a, uint32_t v) {
-  __hip_atomic_fetch_add(a, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_fetch_add(a, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 __device__ __forceinline__ uint32_t far_load(uint32_t* a) {
-  return __hip_atomic_load(a, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return __hip_atomic_load(a, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 __device__ __forceinline__ void far_store(uint32_t* a, uint32_t v) {
-  __hip_atomic_store(a, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(a, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
 __global__ void zero_u64(unsigned long long* x) { *x = 0ull; }
 
+// kAct: the actuation model. A woken replica is routable wake_w windows
+// after its wake starts (its slots free from the start of the window after
+// the wake completes); a donor's replica stops being routable at once (its
+// earliest-free slots leave at the move) and its GPUs reach the receiver
+// after sleep_w windows, when the receiver's wake starts (a shortfall comes
+// from the idle GPUs at the move, an excess returns when the sleep ends); a
+// model with a transition in flight is neither receiver nor donor; vetoed
+// models do not release; the budget counts GPUs (footprint g per replica).
+template <bool kAct>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void loop_replay(LoopParams p) {
   extern __shared__ __align__(16) uint32_t lds[];
   const int lane = threadIdx.x;
@@ -246,9 +264,17 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
     const int room = p.pool_reps - (incl - R);
     R = R < room ? R : (room > 0 ? room : 0);
   }
-  int rsum = R;
+  // GPUs per replica (1 without the actuation model); idle GPUs (replicas)
+  // (at least 1, so that the replicas never outnumber the budget's GPUs and
+  // the heaps' pool always holds their slots)
+  const int g_in = (kAct && p.footprint && act) ? p.footprint[tm] : 1;
+  const int g = g_in < 1 ? 1 : g_in;
+  int rsum = R * g;
   for (int o = 32; o > 0; o >>= 1) rsum += __shfl_xor(rsum, o);
   int pool = p.budget - rsum;
+  // the lane's transition in flight (0 none, 1 wake, 2 sleep), the window at
+  // whose end it completes, and the GPUs a sleep returns to the idle pool
+  int tkind = 0, tuntil = 0, tret = 0;
   int hs = R * spr;  // heap size (R <= r_hi)
   int base;          // first node in the current pool
   {
@@ -280,6 +306,34 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
     }
   }
   uint32_t bf = act && hs > 0 ? 0u : kNone;  // earliest slot free time (the heap's root)
+  // the donors' earliest-free slots leave their heaps; every heap is packed
+  // again (through the scratch: each lane copies its own heap out, then,
+  // after every lane's reads, back in at its new place); the receivers'
+  // slots, free from `from`, join there. Called by the whole wave.
+  auto repack = [&](int pops, int pushes, uint32_t from) {
+    const Heap old = heap();
+    for (int q = 0; q < pops && hs > 0; ++q) {
+      --hs;
+      if (hs > 0) old.replace_top(hs, old.at(hs));
+    }
+    const int want = act ? hs + pushes : 0;
+    int incl = want;
+    for (int o = 1; o < 64; o <<= 1) {
+      const int v = __shfl_up(incl, o);
+      if (lane >= o) incl += v;
+    }
+    const int nbase = incl - want + mc;
+    uint32_t* tmp = p.scratch + (uint64_t)s * p.pool_words + nbase;
+    if (act)
+      for (int i = 0; i < hs; ++i) tmp[i] = old.at(i);
+    const Heap fresh{hpool + nbase};
+    if (act)
+      for (int i = 0; i < hs; ++i) fresh.at(i) = tmp[i];
+    for (int q = 0; q < pushes; ++q) fresh.push(hs + q, from);
+    hs += pushes;
+    base = nbase;
+    bf = act && hs > 0 ? fresh.at(0) : kNone;
+  };
   const uint64_t wmagic = p.wmagic;
   const int wshift = p.wshift;
   auto win = [&](uint32_t x) { return (int32_t)((x * wmagic) >> wshift); };  // x / W for x < 2^31
@@ -331,10 +385,30 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
   int32_t e2e_max = 0;
   unsigned overflow = 0;
   uint32_t nm = 0;
+  int tick = 0;  // ticks so far (wave-uniform)
   const unsigned long long live = __ballot(act);
 
   for (int32_t w = 0; w < p.n_windows; ++w) {
     const int32_t w_end = (w + 1) * W;
+    if constexpr (kAct) {  // transitions that completed at the end of an earlier window
+      const bool done = tkind != 0 && tuntil < w;
+      int push = 0;
+      if (done && tkind == 1) {
+        push = R < r_hi ? spr : 0;
+        R += 1;
+      }
+      unsigned long long back = __ballot(done && tkind == 2 && tret > 0);
+      while (back) {
+        const int l = __ffsll((long long)back) - 1;
+        pool += __builtin_amdgcn_readlane(tret, l);
+        back &= back - 1ull;
+      }
+      if (done) {
+        tkind = 0;
+        tret = 0;
+      }
+      if (__ballot(push > 0)) repack(0, push, (uint32_t)(w * W));
+    }
     uint32_t P = 0, D = 0;
     int64_t eA = 0, eW = 0;
     int32_t dA = 0, dW = 0;
@@ -551,6 +625,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
     // ---- tick: the controller's rules on this window's TSS
     const bool fast = (w + 1) % p.fast_w == 0, slow = (w + 1) % p.slow_w == 0;
     if (!fast && !slow) continue;
+    const int tk = tick++;
     const tre_profile prt = p.prof[tm];  // the thresholds, read at ticks only
     const double theta_eff = prt.theta * sc.theta_scale;
     const double tau_c = sc.tau_crit_override >= 0.0 ? sc.tau_crit_override : prt.tau_crit;
@@ -569,29 +644,48 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
       continue;
     }
     const unsigned long long sur = __ballot(act && Z > prt.tau_surplus);
-    unsigned long long used = 0ull;
+    // models already in a move: earlier in this tick, or (kAct) in flight
+    unsigned long long used = kAct ? __ballot(tkind != 0) : 0ull;
+    const unsigned long long veto_mask = (kAct && p.veto) ? p.veto[(uint64_t)t * p.n_ticks + tk] : 0ull;
     int pops = 0, pushes = 0;  // this tick's slot changes of this lane (a model moves at most once per tick)
     for (uint32_t k = 0; k < sc.max_moves; ++k) {
       const int r = pick_lane<false>(ok & ~used & __ballot(act && R < p.r_cap), Z, lane);  // Eq. (3)
       if (r < 0) break;
+      const int g_r = kAct ? __builtin_amdgcn_readlane(g, r) : 1;
       int d;
-      if (pool > 0) {
-        pool -= 1;
+      if (pool >= g_r) {
+        pool -= g_r;
         d = TRE_DONOR_POOL;
+        if (kAct && lane == r) {
+          tkind = 1;
+          tuntil = w + p.wake_w;
+        }
       } else {
         const double Zr = lane_f64(Z, r);
-        const unsigned long long cd = __ballot(act && R > prt.r_min && Z > Zr) & ~crit & ~used & ~(1ull << r) & live;
+        const unsigned long long cd = __ballot(act && R > prt.r_min && Z > Zr && (!kAct || pool >= g_r - g)) &
+                                      ~crit & ~used & ~(1ull << r) & live & ~veto_mask;
         d = pick_lane<true>(cd & sur, Z, lane);
         if (d < 0) d = pick_lane<true>(cd & ~sur, Z, lane);
         if (d < 0) break;
         used |= 1ull << d;
+        const int short_by = kAct ? g_r - __builtin_amdgcn_readlane(g, d) : 0;
+        if (short_by > 0) pool -= short_by;
         if (lane == d && R > 0) {  // the replica's slots that free first leave
           pops = spr;
           R -= 1;
         }
+        if (kAct && lane == d) {
+          tkind = 2;
+          tuntil = w + p.sleep_w;
+          tret = short_by < 0 ? -short_by : 0;
+        }
+        if (kAct && lane == r) {
+          tkind = 1;
+          tuntil = w + p.sleep_w + p.wake_w;
+        }
       }
       used |= 1ull << r;
-      if (lane == r) {  // the new replica's slots, free from the window's end
+      if (!kAct && lane == r) {  // the new replica's slots, free from the window's end
         pushes = R < r_hi ? spr : 0;
         R += 1;
       }
@@ -606,34 +700,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
       }
       ++nm;
     }
-    if (__ballot(pops > 0 || pushes > 0)) {
-      // the donors' earliest-free slots leave their heaps; every heap is
-      // packed again (through the scratch: each lane copies its own heap out,
-      // then, after every lane's reads, back in at its new place); the
-      // receivers' slots join there
-      const Heap old = heap();
-      for (int q = 0; q < pops && hs > 0; ++q) {
-        --hs;
-        if (hs > 0) old.replace_top(hs, old.at(hs));
-      }
-      const int want = act ? hs + pushes : 0;
-      int incl = want;
-      for (int o = 1; o < 64; o <<= 1) {
-        const int v = __shfl_up(incl, o);
-        if (lane >= o) incl += v;
-      }
-      const int nbase = incl - want + mc;
-      uint32_t* tmp = p.scratch + (uint64_t)s * p.pool_words + nbase;
-      if (act)
-        for (int i = 0; i < hs; ++i) tmp[i] = old.at(i);
-      const Heap fresh{hpool + nbase};
-      if (act)
-        for (int i = 0; i < hs; ++i) fresh.at(i) = tmp[i];
-      for (int q = 0; q < pushes; ++q) fresh.push(hs + q, (uint32_t)w_end);
-      hs += pushes;
-      base = nbase;
-      bf = act && hs > 0 ? fresh.at(0) : kNone;
-    }
+    if (__ballot(pops > 0 || pushes > 0)) repack(pops, pushes, (uint32_t)w_end);
+  }
+  if constexpr (kAct) {  // wakes completing at the end of the last window count
+    if (tkind == 1 && tuntil < p.n_windows) R += 1;
   }
   if (act) {
     p.r_final[(uint64_t)s * M + lane] = R;
@@ -731,21 +801,32 @@ extern "C" int tre_loop_workspace_size(const tre_trace_cfg* cfg, const tre_loop_
   return TRE_OK;
 }
 
-extern "C" int tre_loop(const tre_trace_cfg* cfg, uint32_t n_traces, const tre_loop_requests* rq,
-                        const tre_profile* prof, const tre_scenario* sc, uint32_t n_scenarios,
-                        const tre_ctl_out* out, tre_loop_stats* stats, double* tss64, void* ws, size_t ws_bytes,
-                        void* stream) {
+static int loop_impl(const tre_trace_cfg* cfg, uint32_t n_traces, const tre_loop_requests* rq,
+                     const tre_profile* prof, const tre_scenario* sc, uint32_t n_scenarios, const tre_actuation* act,
+                     const tre_ctl_out* out, tre_loop_stats* stats, double* tss64, void* ws, size_t ws_bytes,
+                     void* stream, const char* who) {
   int rc = check_loop_args(cfg, rq);
   if (rc) return rc;
   if (!prof || !out || !stats || !ws || !rq->arrival_ms || !rq->prompt || !rq->output || !rq->req_off ||
       !rq->service || !rq->slo || (n_scenarios && (!sc || !out->moves || !out->n_moves || !out->r_final ||
                                                    !out->r_windows)))
-    return fail(TRE_EINVAL, "tre_loop: NULL argument");
-  if (n_traces == 0) return fail(TRE_EINVAL, "tre_loop: no traces");
-  if ((uintptr_t)ws & 15) return fail(TRE_EINVAL, "tre_loop: workspace needs 16-byte alignment");
+    return fail(TRE_EINVAL, "%s: NULL argument", who);
+  if (n_traces == 0) return fail(TRE_EINVAL, "%s: no traces", who);
+  if ((uintptr_t)ws & 15) return fail(TRE_EINVAL, "%s: workspace needs 16-byte alignment", who);
+  const int64_t nW = cfg->duration_ms / cfg->window_ms;
+  int32_t wake_w = 0, sleep_w = 0;
+  if (act) {
+    if (act->wake_ms < 0 || act->sleep_ms < 0) return fail(TRE_EINVAL, "%s: actuation delays must be >= 0", who);
+    // whole windows, rounded up; a transition completing after the last
+    // window never counts, so the delays are capped just past the trace
+    const int64_t win = cfg->window_ms, cap = nW + 1;
+    auto to_windows = [&](int64_t ms) { return ms > cap * win ? cap : (ms + win - 1) / win; };
+    wake_w = (int32_t)to_windows(act->wake_ms);
+    sleep_w = (int32_t)to_windows(act->sleep_ms);
+  }
   size_t need = 0;
   tre_loop_workspace_size(cfg, rq, n_scenarios, &need);
-  if (ws_bytes < need) return fail(TRE_ENOMEM, "tre_loop: workspace %zu < %zu bytes", ws_bytes, need);
+  if (ws_bytes < need) return fail(TRE_ENOMEM, "%s: workspace %zu < %zu bytes", who, ws_bytes, need);
   if (n_scenarios == 0) return TRE_OK;
   hipStream_t st = (hipStream_t)stream;
   const int M = cfg->n_models;
@@ -755,7 +836,8 @@ extern "C" int tre_loop(const tre_trace_cfg* cfg, uint32_t n_traces, const tre_l
   FarCell* far = (FarCell*)(base + 256);
   uint32_t* scratch = (uint32_t*)(base + 256 + (uint64_t)n_scenarios * M * L * sizeof(FarCell));
   const size_t lds = lds_bytes(cfg, rq);
-  HIP_TRY(hipFuncSetAttribute((const void*)loop_replay, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
+  const void* kern = act ? (const void*)loop_replay<true> : (const void*)loop_replay<false>;
+  HIP_TRY(hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
   hipLaunchKernelGGL(zero_u64, dim3(1), dim3(1), 0, st, overflow);
   LoopParams lp{};
   lp.arrival = rq->arrival_ms;
@@ -793,13 +875,43 @@ extern "C" int tre_loop(const tre_trace_cfg* cfg, uint32_t n_traces, const tre_l
   lp.ring_len = L;
   lp.window_ms = (int32_t)cfg->window_ms;
   lp.duration_ms = (int32_t)cfg->duration_ms;
-  lp.n_windows = (int32_t)(cfg->duration_ms / cfg->window_ms);
+  lp.n_windows = (int32_t)nW;
   // a period longer than the replay never ticks
   lp.fast_w = (int32_t)std::min<int64_t>(cfg->fast_period_ms / cfg->window_ms, lp.n_windows + 1);
   lp.slow_w = (int32_t)std::min<int64_t>(cfg->slow_period_ms / cfg->window_ms, lp.n_windows + 1);
+  if (act) {
+    lp.footprint = act->footprint;
+    lp.veto = act->veto;
+    lp.wake_w = wake_w;
+    lp.sleep_w = sleep_w;
+    int32_t nt = 0;
+    for (int64_t w = 0; w < nW; ++w)
+      if ((w + 1) % lp.fast_w == 0 || (w + 1) % lp.slow_w == 0) ++nt;
+    lp.n_ticks = nt;
+  }
   LaunchTimer lt("loop_replay", st);
-  hipLaunchKernelGGL(loop_replay, dim3(n_scenarios), dim3(64), lds, st, lp);
+  if (act)
+    hipLaunchKernelGGL(loop_replay<true>, dim3(n_scenarios), dim3(64), lds, st, lp);
+  else
+    hipLaunchKernelGGL(loop_replay<false>, dim3(n_scenarios), dim3(64), lds, st, lp);
   lt.done();
   HIP_TRY(hipGetLastError());
   return TRE_OK;
+}
+
+extern "C" int tre_loop(const tre_trace_cfg* cfg, uint32_t n_traces, const tre_loop_requests* rq,
+                        const tre_profile* prof, const tre_scenario* sc, uint32_t n_scenarios,
+                        const tre_ctl_out* out, tre_loop_stats* stats, double* tss64, void* ws, size_t ws_bytes,
+                        void* stream) {
+  return loop_impl(cfg, n_traces, rq, prof, sc, n_scenarios, nullptr, out, stats, tss64, ws, ws_bytes, stream,
+                   "tre_loop");
+}
+
+extern "C" int tre_loop_act(const tre_trace_cfg* cfg, uint32_t n_traces, const tre_loop_requests* rq,
+                            const tre_profile* prof, const tre_scenario* sc, uint32_t n_scenarios,
+                            const tre_actuation* act, const tre_ctl_out* out, tre_loop_stats* stats, double* tss64,
+                            void* ws, size_t ws_bytes, void* stream) {
+  if (!act) return fail(TRE_EINVAL, "tre_loop_act: NULL actuation model");
+  return loop_impl(cfg, n_traces, rq, prof, sc, n_scenarios, act, out, stats, tss64, ws, ws_bytes, stream,
+                   "tre_loop_act");
 }

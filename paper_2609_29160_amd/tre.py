@@ -86,7 +86,8 @@ class _Actuation(ctypes.Structure):
 EXPORTS = ["tre_last_error", "tre_load_events", "tre_free_events", "tre_events_info",
            "tre_check_params", "tre_workspace_size", "tre_eval_tss", "tre_rebalance", "tre_sweep",
            "tre_set_timing", "tre_kernel_time", "tre_check_actuation", "tre_rebalance_act", "tre_sweep_act",
-           "tre_calib_workspace_size", "tre_calibrate", "tre_loop_workspace_size", "tre_loop", "tre_stage_tss"]
+           "tre_calib_workspace_size", "tre_calibrate", "tre_loop_workspace_size", "tre_loop", "tre_loop_act",
+           "tre_stage_tss"]
 
 
 def _load():
@@ -129,6 +130,9 @@ def _load():
     L.tre_loop.restype = i32
     L.tre_loop.argtypes = [ctypes.POINTER(_TraceCfg), u32, ctypes.POINTER(_LoopRequests), vp, vp, u32,
                            ctypes.POINTER(_CtlOut), vp, vp, vp, sz, vp]
+    L.tre_loop_act.restype = i32
+    L.tre_loop_act.argtypes = [ctypes.POINTER(_TraceCfg), u32, ctypes.POINTER(_LoopRequests), vp, vp, u32,
+                               ctypes.POINTER(_Actuation), ctypes.POINTER(_CtlOut), vp, vp, vp, sz, vp]
     L.tre_stage_tss.restype = i32
     L.tre_stage_tss.argtypes = [vp, vp, ctypes.POINTER(_TssOut), vp, vp, vp, vp]
     L.tre_set_timing.restype = i32
@@ -415,6 +419,19 @@ def tre_loop(cfg: Dict[str, int], n_traces: int, rq: _LoopRequests, prof: torch.
     o = _ctl(out)
     _check(_L.tre_loop(ctypes.byref(c), n_traces, ctypes.byref(rq), _ptr(prof), _ptr(sc), n_sc, ctypes.byref(o),
                        _ptr(stats), _ptr(tss64), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def tre_loop_act(cfg: Dict[str, int], n_traces: int, rq: _LoopRequests, prof: torch.Tensor, sc: torch.Tensor,
+                 act: _Actuation, out: Dict[str, torch.Tensor], stats: torch.Tensor, ws: torch.Tensor,
+                 tss64: Optional[torch.Tensor] = None, stream=None):
+    """tre_loop with the actuation model (see actuation(); the budget in
+    cfg then counts GPUs)."""
+    n_sc = sc.numel() // SCENARIO_DTYPE.itemsize
+    c = _cfg(cfg)
+    o = _ctl(out)
+    _check(_L.tre_loop_act(ctypes.byref(c), n_traces, ctypes.byref(rq), _ptr(prof), _ptr(sc), n_sc, ctypes.byref(act),
+                           ctypes.byref(o), _ptr(stats), _ptr(tss64), _ptr(ws), ws.numel() * ws.element_size(),
+                           _stream(stream)))
 
 
 def tre_set_timing(enable: bool):

@@ -9,8 +9,8 @@ only at this scale), and sampled scenarios and per-cell fp32 TSS of sampled
 traces must match the CPU oracle exactly. The oracle regenerates each
 sampled trace on the host from the same seeds. The calibration sweep, the
 stage-aware shares and the closed-loop replay of the whole stress workload
-are run twice each and checked the same way (sampled traces or scenarios
-against the oracle).
+(with and without the actuation model) are run twice each and checked the
+same way (sampled traces or scenarios against the oracle).
 """
 import sys
 
@@ -229,11 +229,18 @@ def test_stress_full_size_stage_shares():
     torch.cuda.empty_cache()
 
 
-def test_stress_full_size_closed_loop():
+_STRESS_TABLES = {}
+
+
+@pytest.mark.parametrize("actuation", [False, True], ids=["plain", "actuation"])
+def test_stress_full_size_closed_loop(actuation):
     """The closed loop over every scenario of the stress workload (777 M
     requests), twice: identical results; sampled scenarios equal to the
     oracle's closed-loop replay (moves, replicas, replica-window sums,
-    latency statistics) with no event beyond the ring."""
+    latency statistics) with no event beyond the ring. With the actuation
+    model: the paper's wake and sleep times (1.31 s, 1.87 s), footprints of
+    1 or 2 GPUs per replica with the GPU budget at the largest initial
+    footprint sum plus 8, vetoes on 10% of the ticks."""
     from concurrent.futures import ThreadPoolExecutor
 
     import torch
@@ -242,8 +249,10 @@ def test_stress_full_size_closed_loop():
 
     w = tg.standard(4)
     T, M = w.n_traces, w.n_models
-    with ThreadPoolExecutor(max_workers=16) as pool:
-        tables = list(pool.map(w.requests, range(T)))
+    if w.name not in _STRESS_TABLES:
+        with ThreadPoolExecutor(max_workers=16) as pool:
+            _STRESS_TABLES[w.name] = list(pool.map(w.requests, range(T)))
+    tables = _STRESS_TABLES[w.name]
     say(f"{w.name}: {sum(len(t['arrival_ms']) for t in tables)} requests")
     svc = np.zeros(T * M, tre.SERVICE_DTYPE)
     for k, v in w.service_columns().items():
@@ -265,12 +274,29 @@ def test_stress_full_size_closed_loop():
     class _Shape:
         n_models = M
 
+    kw_t = lambda t: {}
+    if actuation:
+        rng = np.random.default_rng(31)
+        fp = rng.integers(1, 3, (T, M)).astype(np.int32)
+        r_init = np.asarray(w.profile_columns()["r_init"]).reshape(T, M)
+        cfg = dict(cfg, budget=int((fp * r_init).sum(axis=1).max()) + 8)
+        veto = np.frombuffer(rng.bytes(8 * T * n_ticks), np.uint64).reshape(T, n_ticks).copy()
+        veto &= np.uint64((1 << M) - 1)
+        veto[rng.random(veto.shape) >= 0.1] = 0
+        g_dev = torch.from_numpy(fp).cuda()
+        v_dev = torch.from_numpy(veto.view(np.int64)).cuda()
+        act = tre.actuation(1310, 1870, g_dev, v_dev)
+        to_w = lambda ms: min(-(-ms // w.window_ms), nW + 1)
+        kw_t = lambda t: {"wake_w": to_w(1310), "sleep_w": to_w(1870), "footprint": fp[t], "veto": veto[t]}
     ws = torch.empty(tre.tre_loop_workspace_size(cfg, rq, n_sc), dtype=torch.uint8, device="cuda")
     runs = []
     for _ in range(2):
         out = tre.ctl_outputs(_Shape(), n_sc, move_cap)
         stats = torch.zeros(n_sc * M * tre.LOOP_STATS_DTYPE.itemsize, dtype=torch.uint8, device="cuda")
-        tre.tre_loop(cfg, T, rq, prof, sc, out, stats, ws)
+        if actuation:
+            tre.tre_loop_act(cfg, T, rq, prof, sc, act, out, stats, ws)
+        else:
+            tre.tre_loop(cfg, T, rq, prof, sc, out, stats, ws)
         torch.cuda.synchronize()
         assert int(ws[:8].cpu().numpy().view(np.uint64)[0]) == 0, "events beyond the ring"
         runs.append((_outputs(out), stats.cpu().numpy().copy()))
@@ -288,7 +314,7 @@ def test_stress_full_size_closed_loop():
     def one(s):
         t = int(sc_all[s]["trace"])
         return o.loop(cfg, prof_all[t * M:(t + 1) * M], sc_all[s:s + 1], slo_all[t * M:(t + 1) * M],
-                      svc_all[t * M:(t + 1) * M], tables[t], move_cap=move_cap)
+                      svc_all[t * M:(t + 1) * M], tables[t], move_cap=move_cap, **kw_t(t))
 
     say(f"{w.name}: oracle closed loop of scenarios {sample}")
     with ThreadPoolExecutor(max_workers=len(sample)) as pool:
@@ -306,4 +332,7 @@ def test_stress_full_size_closed_loop():
         assert np.array_equal(g["r_windows"][s], ref["r_windows"]), s
         for f in tre.LOOP_STATS_DTYPE.names:
             assert np.array_equal(st[s][f], ref["stats"][f]), (s, f)
+    assert sum(int(g["n_moves"][s]) for s in sample) > 0, "no moves in the sampled scenarios"
     say(f"{w.name}: closed loop of {len(sample)} sampled scenarios matches the oracle")
+    if actuation:  # the last variant: free the host tables
+        _STRESS_TABLES.clear()

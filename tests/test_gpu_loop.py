@@ -8,8 +8,15 @@ oracle's, and no event may fall outside the ring of future windows.
 Inputs: the tiny and bursty workloads' request tables (the same arrivals and
 lengths as their traces) under scenario tables with 0 to 4 moves per tick,
 spare budget and replica caps that bind; budgets above n_models * r_cap; an
-empty request table and models without requests; the oracle's hand cases; 1, 17 and 64 models; one and three slots per replica;
-argument errors (including slot heaps beyond the LDS).
+empty request table and models without requests; the oracle's hand cases;
+1, 17 and 64 models; one and three slots per replica; argument errors
+(including slot heaps beyond the LDS and negative actuation delays).
+
+tre_loop_act against the oracle's closed loop under the actuation model, to
+the same bar: zero delays with unit footprints and no vetoes equal to
+tre_loop; the paper's wake and sleep times (1.31 s, 1.87 s) with footprints
+of 1 or 2 GPUs and vetoes on 20% of the ticks, with and without idle GPUs;
+delays longer than the trace; 1, 17 and 64 models; the oracle's hand case.
 """
 import sys
 
@@ -48,7 +55,9 @@ def _n_ticks(cfg):
                or ((w + 1) * cfg["window_ms"]) % cfg["slow_period_ms"] == 0)
 
 
-def _check(lib, name, cfg, tables, prof_cols, slo_cols, svc_cols, sc_cols, spr=8, r_cap=16):
+def _check(lib, name, cfg, tables, prof_cols, slo_cols, svc_cols, sc_cols, spr=8, r_cap=16, act=None):
+    """act: (wake_ms, sleep_ms, footprint [T][M] int32 or None, veto [T][n_ticks] uint64 or None) runs
+    tre_loop_act against the oracle's closed loop with the actuation model."""
     tre, device, torch = lib
     M = cfg["n_models"]
     T = len(tables)
@@ -68,7 +77,15 @@ def _check(lib, name, cfg, tables, prof_cols, slo_cols, svc_cols, sc_cols, spr=8
     stats = torch.zeros(n_sc * M * tre.LOOP_STATS_DTYPE.itemsize, dtype=torch.uint8, device="cuda")
     tss = torch.zeros((n_sc, nW, M), dtype=torch.float64, device="cuda")
     ws = torch.empty(tre.tre_loop_workspace_size(cfg, rq, n_sc), dtype=torch.uint8, device="cuda")
-    tre.tre_loop(cfg, T, rq, prof, sc, out, stats, ws, tss64=tss)
+    if act is None:
+        tre.tre_loop(cfg, T, rq, prof, sc, out, stats, ws, tss64=tss)
+    else:
+        wake_ms, sleep_ms, fp, veto = act
+        fp_t = None if fp is None else torch.from_numpy(np.ascontiguousarray(fp, np.int32)).cuda()
+        v_t = None if veto is None else torch.from_numpy(np.ascontiguousarray(veto, np.uint64).view(np.int64)).cuda()
+        tre.tre_loop_act(cfg, T, rq, prof, sc, tre.actuation(wake_ms, sleep_ms, fp_t, v_t), out, stats, ws, tss64=tss)
+        cap = nW + 1
+        to_w = lambda ms: cap if ms > cap * cfg["window_ms"] else -(-ms // cfg["window_ms"])
     torch.cuda.synchronize()
     assert int(ws[:8].cpu().numpy().view(np.uint64)[0]) == 0, f"{name}: events beyond the ring"
     moves = tre.unpack_moves(out["moves"]).reshape(n_sc, move_cap)
@@ -81,9 +98,14 @@ def _check(lib, name, cfg, tables, prof_cols, slo_cols, svc_cols, sc_cols, spr=8
         row = np.zeros(1, O.SCENARIO_DTYPE)
         for k in O.SCENARIO_DTYPE.names:
             row[k] = sc_cols[k][s]
+        kw = {}
+        if act is not None:
+            kw = {"wake_w": to_w(wake_ms), "sleep_w": to_w(sleep_ms),
+                  "footprint": np.ones(M, np.int32) if fp is None else np.asarray(fp)[t],
+                  "veto": None if veto is None else np.asarray(veto, np.uint64)[t]}
         ref = o.loop(cfg, _rows(prof_cols, t, M, O.PROFILE_DTYPE), row, _rows(slo_cols, t, M, O.SLO_DTYPE),
                      _rows(svc_cols, t, M, O.SVC_DTYPE), tables[t], spr=spr, r_cap=r_cap, move_cap=move_cap,
-                     want_tss=True)
+                     want_tss=True, **kw)
         what = f"{name} scenario {s}"
         n = int(out["n_moves"][s])
         assert n == ref["n_moves"], f"{what}: {n} moves vs {ref['n_moves']}"
@@ -215,6 +237,82 @@ def test_empty_tables(lib):
            _scenarios(rng, 9, 3))
 
 
+def _act_model(rng, n_traces, M, n_ticks, veto_frac=0.2):
+    fp = rng.integers(1, 3, (n_traces, M)).astype(np.int32)
+    veto = np.frombuffer(rng.bytes(8 * n_traces * n_ticks), np.uint64).reshape(n_traces, n_ticks).copy()
+    veto &= np.uint64((1 << M) - 1)
+    veto[rng.random(veto.shape) > veto_frac] = 0
+    return fp, veto
+
+
+def test_actuation_zero_delays_equal_the_plain_loop(lib):
+    w = tg.standard(0)
+    tables = [w.requests(0)]
+    rng = np.random.default_rng(41)
+    cfg = dict(w.trace_cfg(), budget=w.budget + 2)
+    sc = _scenarios(rng, 8, 1)
+    a = _check(lib, "act0", cfg, tables, w.profile_columns(1), w.slo_columns(1), w.service_columns(1), sc,
+               act=(0, 0, np.ones((1, w.n_models), np.int32), np.zeros((1, _n_ticks(cfg)), np.uint64)))
+    b = _check(lib, "plain", cfg, tables, w.profile_columns(1), w.slo_columns(1), w.service_columns(1), sc)
+    assert a == b > 0
+
+
+def test_actuation_paper_delays(lib):
+    """The paper's wake and sleep times (1.31 s, 1.87 s: 3 and 4 windows of
+    500 ms), footprints of 1 or 2 GPUs, vetoes on 20% of the ticks."""
+    w = tg.standard(1).scaled(duration_ms=900_000)
+    tables = [w.requests(0)]
+    rng = np.random.default_rng(42)
+    cfg = dict(w.trace_cfg())
+    fp, veto = _act_model(rng, 1, w.n_models, _n_ticks(cfg))
+    r_init = np.asarray(w.profile_columns(1)["r_init"])
+    for extra in (0, 6):
+        cfg["budget"] = int((fp[0] * r_init).sum()) + extra
+        say(f"paper delays, budget {cfg['budget']} GPUs")
+        n = _check(lib, f"act-paper-{extra}", cfg, tables, w.profile_columns(1), w.slo_columns(1),
+                   w.service_columns(1), _scenarios(rng, 12, 1), r_cap=10, act=(1310, 1870, fp, veto))
+        assert n > 0
+
+
+def test_actuation_delays_past_the_trace_and_model_counts(lib):
+    w = tg.standard(0)
+    tables = [w.requests(0)]
+    rng = np.random.default_rng(43)
+    cfg = dict(w.trace_cfg(), budget=w.budget + 3)
+    _check(lib, "act-long", cfg, tables, w.profile_columns(1), w.slo_columns(1), w.service_columns(1),
+           _scenarios(rng, 4, 1), act=(10 ** 9, 5000, None, None))
+    for M in (1, 17, 64):
+        wm = tg.Workload(name=f"m{M}", n_traces=1, model_classes=[["7B", "13B", "34B", "70B"][m % 4] for m in range(M)],
+                         interactive=[m % 2 == 0 for m in range(M)], r_init=[2] * M, budget=2 * M + 3,
+                         window_ms=500, duration_ms=600_000, process="mmpp2", rate=[0.8] * M,
+                         proc_params={"mmpp_mult": 6.0, "mmpp_dwell_s": 60.0}, seed=70 + M)
+        tables = [wm.requests(0)]
+        c = wm.trace_cfg()
+        fp, veto = _act_model(rng, 1, M, _n_ticks(c))
+        c["budget"] = int((fp[0] * 2).sum()) + 3
+        say(f"actuation, M {M}")
+        _check(lib, f"act-M{M}", c, tables, wm.profile_columns(1), wm.slo_columns(1), wm.service_columns(1),
+               _scenarios(rng, 4, 1), act=(1000, 1500, fp, veto))
+
+
+def test_actuation_hand_case(lib):
+    """The oracle's hand case: wake 2 windows, sleep 1 window."""
+    cfg = {"window_ms": 100, "duration_ms": 1000, "fast_period_ms": 100, "slow_period_ms": 100,
+           "n_models": 2, "budget": 3}
+    prof = {"w_p": np.full(2, 0.5), "w_q": np.full(2, 2.0), "alpha": np.ones(2), "theta": np.full(2, 1e12),
+            "tau_crit": np.full(2, 0.5), "tau_surplus": np.full(2, 1.5), "r_min": np.zeros(2, np.int32),
+            "r_init": np.ones(2, np.int32)}
+    slo = {"ttft_ms": np.full(2, 1e9), "tpot_ms": np.full(2, 1e9), "e2e_ms": np.full(2, 1e9),
+           "attain_q": np.full(2, 0.95), "reliability": np.full(2, 0.9)}
+    svc = {"prefill_us": np.full(2, 1000, np.uint32), "decode_us": np.full(2, 10000, np.uint32)}
+    table = {"arrival_ms": np.zeros(3, np.int64), "model": np.zeros(3, np.uint8), "prompt": np.ones(3, np.uint16),
+             "output": np.full(3, 24, np.uint16)}
+    sc = {"trace": np.zeros(1, np.uint32), "max_moves": np.ones(1, np.uint32), "theta_scale": np.ones(1),
+          "tau_crit_override": -np.ones(1)}
+    n = _check(lib, "act-hand", cfg, [table], prof, slo, svc, sc, spr=1, r_cap=3, act=(200, 100, None, None))
+    assert n == 2
+
+
 def test_argument_errors(lib):
     tre, device, torch = lib
     w = tg.standard(0)
@@ -244,3 +342,10 @@ def test_argument_errors(lib):
     with pytest.raises(tre.TreError) as e:
         tre.tre_loop_workspace_size(dict(cfg, budget=4096), big, 2)
     assert e.value.code == tre.TRE_EINVAL
+    # the actuation model: negative delays
+    ws = torch.empty(tre.tre_loop_workspace_size(cfg, rq, 2), dtype=torch.uint8, device="cuda")
+    for wake_ms, sleep_ms in ((-1, 0), (0, -250)):
+        with pytest.raises(tre.TreError) as e:
+            tre.tre_loop_act(cfg, 1, rq, prof, sc, tre.actuation(wake_ms, sleep_ms), out, stats, ws)
+        assert e.value.code == tre.TRE_EINVAL
+    torch.cuda.synchronize()
