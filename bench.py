@@ -100,7 +100,7 @@ def main():
     ap.add_argument("--loop-cpu-scenarios", type=int, default=16,
                     help="scenarios replayed by the oracle in the --loop CPU leg")
     ap.add_argument("--stage", action="store_true",
-                    help="time the stage-aware shares (tre_eval_tss tallies + tre_stage_tss) instead")
+                    help="time the stage-aware shares (tre_eval_stage, one pass; the two-pass path beside it) instead")
     ap.add_argument("--calibrate", action="store_true",
                     help="time the calibration sweep (tre_eval_tss + tre_calibrate) instead")
     ap.add_argument("--copy-calib-gb", type=float, default=0.0,
@@ -514,59 +514,73 @@ STAGE_KERNELS = ("tss_stream", "stage_tss")
 
 
 def stage_main(args, w, dt, device, tre, torch, np):
-    """One step = tre_eval_tss writing the per-cell tallies (prefill and
-    decode tokens, the active and waiting integrals), then tre_stage_tss
-    writing the prefill and decode shares (binary64) and their flags over
-    the whole resident workload. Algorithmic bytes per launch: tss_stream 12
-    per event + 24 per cell written; stage_tss 24 per cell read + 17 per
-    cell written."""
+    """One step = tre_eval_stage over the whole resident workload: one pass
+    over each trace's events writing the prefill and decode shares
+    (binary64) and their flags, the tallies never leaving the chip.
+    Algorithmic bytes per launch: 12 per event read + 17 per cell written.
+    The two-pass path (tre_eval_tss writing the per-cell tallies, then
+    tre_stage_tss) is timed beside it for comparison (24 bytes per cell
+    written and read back) and must give the same shares in every cell."""
     ev = device.load(dt, validate=True)
     prof = device.profiles(w)
     T, M, nW = ev.n_traces, ev.n_models, ev.n_windows
     cells = T * M * nW
-    tal = tre.tss_outputs(ev, which=("prefill", "decode", "a_int", "w_int"))
     out = tre.stage_outputs(ev, which=("stage64", "flags"))
     log(f"stage shares: {T} traces, {dt.n_events} events, {cells} cells")
 
-    def step():
-        tre.tre_eval_tss(ev, prof, tal)
-        tre.tre_stage_tss(ev, prof, tal, out)
+    def timed(step, n, names):
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
+        stream = torch.cuda.current_stream()
+        tre.tre_set_timing(True)
+        for k in names:
+            tre.tre_kernel_time(k)
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(n):
+            step()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        tre.tre_set_timing(False)
+        kms = {}
+        for k in names:
+            tot, c = tre.tre_kernel_time(k)
+            kms[k] = tot / max(c, 1)
+        return e0.elapsed_time(e1) / n, kms
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    stream = torch.cuda.current_stream()
-    tre.tre_set_timing(True)
-    for k in STAGE_KERNELS:
-        tre.tre_kernel_time(k)
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    e0.record(stream)
-    for _ in range(args.steps):
-        step()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    tre.tre_set_timing(False)
-    step_ms = e0.elapsed_time(e1) / args.steps
-    kms = {}
-    for k in STAGE_KERNELS:
-        tot, n = tre.tre_kernel_time(k)
-        kms[k] = tot / max(n, 1)
-    alg = {"tss_stream": ALG_BYTES_PER_EVENT * dt.n_events + 24 * cells, "stage_tss": 41 * cells}
-    kernels = {k: {"ms": round(kms[k], 4), "alg_bytes": alg[k],
-                   "gbs": round(alg[k] / (kms[k] / 1e3) / 1e9, 1) if kms[k] > 0 else None} for k in STAGE_KERNELS}
-    roofline = {"bound": "hbm", "achieved": kernels["stage_tss"]["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(kernels["stage_tss"]["gbs"] / HBM_PEAK_GBS, 4),
-                "traffic": stage_traffic_for(w.name, cells), "kernel": "stage_tss",
-                "kernel_ms": kernels["stage_tss"]["ms"], "alg_bytes_per_launch": alg["stage_tss"]}
-    log("kernels " + ", ".join(f"{k} {kms[k]:.3f} ms" for k in STAGE_KERNELS) + f"; step {step_ms:.3f} ms")
+    step_ms, kms = timed(lambda: tre.tre_eval_stage(ev, prof, out), args.steps, ("tss_stream",))
+    k_ms = kms["tss_stream"]
+    alg = ALG_BYTES_PER_EVENT * dt.n_events + 17 * cells
+    log(f"one pass: step {step_ms:.3f} ms, tss_stream (stage) {k_ms:.3f} ms")
+    # the two-pass path, for comparison
+    tal = tre.tss_outputs(ev, which=("prefill", "decode", "a_int", "w_int"))
+    two = tre.stage_outputs(ev, which=("stage64", "flags"))
+    two_ms, two_k = timed(lambda: (tre.tre_eval_tss(ev, prof, tal), tre.tre_stage_tss(ev, prof, tal, two)),
+                          min(args.steps, 3), STAGE_KERNELS)
+    same = bool(torch.equal(two["stage64"].view(torch.int64), out["stage64"].view(torch.int64)) and
+                torch.equal(two["flags"], out["flags"]))
+    log(f"two pass: step {two_ms:.3f} ms ({', '.join(f'{k} {v:.3f} ms' for k, v in two_k.items())}); "
+        f"same shares: {same}")
+    del tal, two
+    torch.cuda.empty_cache()
+    two_alg = {"tss_stream": ALG_BYTES_PER_EVENT * dt.n_events + 24 * cells, "stage_tss": 41 * cells}
+    two_pass = {"ms_per_step": round(two_ms, 4), "same_shares": same,
+                "kernels": {k: {"ms": round(two_k[k], 4), "alg_bytes": two_alg[k],
+                                "gbs": round(two_alg[k] / (two_k[k] / 1e3) / 1e9, 1) if two_k[k] > 0 else None}
+                            for k in STAGE_KERNELS}}
+    gbs = alg / (k_ms / 1e3) / 1e9
+    roofline = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": stage_traffic_for(w.name, cells),
+                "kernel": "tss_stream (stage)", "kernel_ms": round(k_ms, 4), "alg_bytes_per_launch": alg}
     cpu = parity = None
     if not args.no_cpu:
         n_s = max(1, int(np.searchsorted(np.cumsum(dt.counts), CPU_EVENT_BUDGET // 3, side="right")))
         cpu, parity = stage_cpu_leg(w, list(range(n_s)), out, args.threads)
     result = {
-        "metric": "request-events/sec through TSS tallies + stage-aware shares (1 GPU)",
+        "metric": "request-events/sec through stage-aware shares (1 GPU)",
         "value": round(dt.n_events / (step_ms / 1e3), 1),
         "unit": "request-events/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(step_ms, 4),
@@ -574,27 +588,27 @@ def stage_main(args, w, dt, device, tre, torch, np):
         "data": "synthetic (seeded generator; the paper's traces are not available)",
         "config": {"workload": w.name, "traces": T, "models": M, "window_ms": w.window_ms,
                    "duration_s": w.duration_ms // 1000, "events": dt.n_events, "cells": cells, "mode": "stage"},
-        "roofline": roofline, "kernels": kernels, "cpu_baseline": cpu, "parity": parity,
+        "roofline": roofline, "two_pass": two_pass, "cpu_baseline": cpu, "parity": parity,
     }
     print(json.dumps(result), flush=True)
     if args.copy_calib_gb > 0:
-        del tal, out
+        del out
         torch.cuda.empty_cache()
         copy_calibration(args.copy_calib_gb, torch)
     ev.close()
 
 
 def stage_traffic_for(workload_name: str, cells: int):
-    """HBM bytes per stage_tss launch from committed counters taken on this
-    kernel source and workload; else None."""
+    """HBM bytes per one-pass stage launch (tss_stream's stage
+    instantiation) from committed counters taken on this kernel source and
+    workload; else None."""
     try:
         t = json.load(open(os.path.join(ROOT, "profiles", "stage_traffic.json")))
     except (OSError, ValueError):
         return None
-    src = os.path.join(ROOT, "paper_2609_29160_amd", "csrc", "stage.hip")
-    if t.get("kernel_sha") != kernel_sha(src) or t.get("workload") != workload_name or t.get("cells") != cells:
+    if t.get("kernel_sha") != kernel_sha() or t.get("workload") != workload_name or t.get("cells") != cells:
         return None
-    return t.get("traffic_bytes_per_launch", {}).get("stage_tss")
+    return t.get("traffic_bytes_per_launch", {}).get("tss_stream_stage")
 
 
 def stage_cpu_leg(w, sample, out, threads):

@@ -459,6 +459,14 @@ int tre_loop(const tre_trace_cfg* cfg, uint32_t n_traces, const tre_loop_request
 int tre_stage_tss(const tre_events* ev, const tre_profile* prof, const tre_tss_out* tallies, double* stage64,
                   float* stage32, uint8_t* flags, void* stream);
 
+/* The same shares computed straight from the events (the tallies never
+   leave the chip): tre_eval_tss's pass over each trace with the two stage
+   ratios staged beside Eq. (1)'s and smoothed in the same chain. Outputs as
+   tre_stage_tss (each optional but not all NULL, same layout, alignment
+   and values bit for bit). Enqueued on `stream`. */
+int tre_eval_stage(const tre_events* ev, const tre_profile* prof, double* stage64, float* stage32,
+                   uint8_t* flags, void* stream);
+
 /* tre_loop with the actuation model (paper, Sections "System Boundary and
    Replica State" and "Bounded Pairwise Transfer": transitions hide, drain,
    sleep and wake replicas, budget-feasible in GPU footprints; act: host,

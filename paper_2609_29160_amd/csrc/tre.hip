@@ -100,6 +100,10 @@ struct StreamParams {
   float* tss32;
   uint8_t* flags;
   double* snap;     // [trace][tick][M]: S, or +inf when idle / not initialised
+  // the kStage instantiation: stage-aware shares per cell (tre_eval_stage)
+  double* stage64;  // [trace][w][M][2]: prefill, decode
+  float* stage32;
+  uint8_t* sflags;  // TRE_STAGE_*
 };
 
 // quotient and remainder of rel / window_ms for any 32-bit rel: the
@@ -314,8 +318,8 @@ __device__ __forceinline__ uint32_t mod_magic(uint32_t x, uint32_t d, uint32_t m
 //     over the chunk, window integrals, Eq. (1) -> raw ratio, staged in LDS
 //     (two staging buffers, by step parity);
 //   -- barrier -- the tile's rows are in; windows < wl are complete.
-template <int kWaves, int kEPT, bool kCells>
-__global__ __launch_bounds__(kWaves * 64) void tss_stream(StreamParams p) {
+template <int kWaves, int kEPT, bool kCells, bool kStage>
+__device__ __forceinline__ void stream_body(const StreamParams& p) {
   constexpr int kThreads = kWaves * 64;
   constexpr long long kTile = (long long)kThreads * kEPT;
   extern __shared__ unsigned long long ring[];
@@ -337,6 +341,15 @@ __global__ __launch_bounds__(kWaves * 64) void tss_stream(StreamParams p) {
   const int nring = (int)(wcap * sstride);
   // [2][C][M] staged raw ratios (>= 0), -1 marks an idle window
   double* st_raw = (double*)(ring + nring);
+  // kStage (no scalar TSS is written): the staged prefill ratios in the
+  // scalar ratios' place and the decode ratios after them ([2][C][M] each,
+  // -1 idle), then each model's smoothed shares and init flags
+  double* const st_p = st_raw;
+  double* const st_d = st_raw + 2 * C * M;
+  double* const s_Sp = st_d + 2 * C * M;
+  double* const s_Sd = s_Sp + M;
+  uint8_t* const s_ip = (uint8_t*)(s_Sd + M);
+  uint8_t* const s_id = s_ip + M;
   const long long e_begin = p.off[trace];
   const long long e_end = p.off[trace + 1];
   const long long win = p.window_ms;
@@ -369,6 +382,12 @@ __global__ __launch_bounds__(kWaves * 64) void tss_stream(StreamParams p) {
     s_alpha[tid] = p.prof[(int64_t)trace * M + tid].alpha;
     s_S[tid] = 0.0;
     s_init[tid] = 0;
+    if constexpr (kStage) {
+      s_Sp[tid] = 0.0;
+      s_Sd[tid] = 0.0;
+      s_ip[tid] = 0;
+      s_id[tid] = 0;
+    }
   }
   if (tid < 3) s_tick[tid] = 0;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -402,6 +421,14 @@ __global__ __launch_bounds__(kWaves * 64) void tss_stream(StreamParams p) {
       const double oma = 1.0 - alpha;
       double S = s_S[m];
       bool init = s_init[m] != 0;
+      double Sp = 0.0, Sd = 0.0;
+      bool ip = false, id = false;
+      if constexpr (kStage) {
+        Sp = s_Sp[m];
+        Sd = s_Sd[m];
+        ip = s_ip[m] != 0;
+        id = s_id[m] != 0;
+      }
       // windows since the last fast / slow tick before cA, ticks so far
       const uint32_t fctr = (uint32_t)s_tick[0], sctr = (uint32_t)s_tick[1];
       int tick = s_tick[2];
@@ -421,16 +448,41 @@ __global__ __launch_bounds__(kWaves * 64) void tss_stream(StreamParams p) {
             const int w = cA + u0 + u;
             const double raw = rv[u];
             const bool idle = raw < 0.0;
-            const double t1 = alpha * raw;
-            const double t2 = oma * S;
-            const double Sn = t1 + t2;
-            S = idle ? S : (init ? Sn : raw);
-            init = init || !idle;
+            if constexpr (!kStage) {
+              const double t1 = alpha * raw;
+              const double t2 = oma * S;
+              const double Sn = t1 + t2;
+              S = idle ? S : (init ? Sn : raw);
+              init = init || !idle;
+            }
             if (cells && own) {
               const int64_t c = ((int64_t)trace * nW + w) * M + m;
               if (p.tss64) p.tss64[c] = S;
               if (p.tss32) p.tss32[c] = (float)S;
               if (p.flags) p.flags[c] = (uint8_t)((idle ? TRE_FLAG_IDLE : 0) | (init ? TRE_FLAG_INIT : 0));
+            }
+            if constexpr (kStage) {  // the stage shares: the same smoothing per stage
+              const int j = ((u0 + u) & (C - 1)) * M + ((k + 1) & 1) * C * M + m;
+              const double rp = raw, rd = st_d[j];  // st_p is st_raw
+              const bool pi = rp < 0.0, di = rd < 0.0;
+              const double p1 = alpha * rp;
+              const double p2 = oma * Sp;
+              const double pn = p1 + p2;
+              Sp = pi ? Sp : (ip ? pn : rp);
+              ip = ip || !pi;
+              const double d1 = alpha * rd;
+              const double d2 = oma * Sd;
+              const double dn = d1 + d2;
+              Sd = di ? Sd : (id ? dn : rd);
+              id = id || !di;
+              if (own) {
+                const int64_t c = ((int64_t)trace * nW + w) * M + m;
+                if (p.stage64) *(double2*)(p.stage64 + 2 * c) = make_double2(Sp, Sd);
+                if (p.stage32) *(float2*)(p.stage32 + 2 * c) = make_float2((float)Sp, (float)Sd);
+                if (p.sflags)
+                  p.sflags[c] = (uint8_t)((pi ? TRE_STAGE_P_IDLE : 0) | (ip ? TRE_STAGE_P_INIT : 0) |
+                                          (di ? TRE_STAGE_D_IDLE : 0) | (id ? TRE_STAGE_D_INIT : 0));
+              }
             }
             if ((tm >> (u0 + u)) & 1u) {
               if (own && p.snap && tick < p.n_ticks)
@@ -443,6 +495,12 @@ __global__ __launch_bounds__(kWaves * 64) void tss_stream(StreamParams p) {
       if (own) {
         s_S[m] = S;
         s_init[m] = init ? 1 : 0;
+        if constexpr (kStage) {
+          s_Sp[m] = Sp;
+          s_Sd[m] = Sd;
+          s_ip[m] = ip ? 1 : 0;
+          s_id[m] = id ? 1 : 0;
+        }
       }
       if (lane == 0) {
         s_tick[0] = (int)mod_magic(fctr + (uint32_t)nw, (uint32_t)p.fast_w, p.magic_fast);
@@ -521,7 +579,7 @@ __global__ __launch_bounds__(kWaves * 64) void tss_stream(StreamParams p) {
         const uint32_t P = (uint32_t)pd, Dt = (uint32_t)(pd >> 32);
         const bool idle = pd == 0ull && A_f == 0.0 && W_f == 0.0;
         double raw = 0.0;
-        if (!idle) {
+        if (!kStage && !idle) {
           // Eq. (1), evaluated in the documented order
           double num = w_p * (double)P;
           num = num + (double)Dt;
@@ -531,7 +589,27 @@ __global__ __launch_bounds__(kWaves * 64) void tss_stream(StreamParams p) {
           if (den < dwin) den = dwin;
           raw = num / den;
         }
-        sr[rj * M + rm] = idle ? -1.0 : raw;
+        if constexpr (!kStage) sr[rj * M + rm] = idle ? -1.0 : raw;
+        if constexpr (kStage) {
+          // the two parts of Eq. (1), each with its one-request floor; a
+          // stage is idle when its tokens and its demand integral are zero
+          double rp = -1.0, rd = -1.0;
+          if (P != 0u || W_f != 0.0) {
+            double num = w_p * (double)P;
+            num = num * 1000.0;
+            double den = w_q * W_f;
+            if (den < dwin) den = dwin;
+            rp = num / den;
+          }
+          if (Dt != 0u || A_f != 0.0) {
+            const double num = (double)Dt * 1000.0;
+            double den = A_f;
+            if (den < dwin) den = dwin;
+            rd = num / den;
+          }
+          st_p[(k & 1) * C * M + rj * M + rm] = rp;
+          st_d[(k & 1) * C * M + rj * M + rm] = rd;
+        }
         if (cells) {
           const int64_t o = ((int64_t)trace * nW + w) * M + rm;
           if (p.prefill) p.prefill[o] = P;
@@ -587,6 +665,19 @@ __global__ __launch_bounds__(kWaves * 64) void tss_stream(StreamParams p) {
     if (step(buf0, buf1, k)) break;
     if (step(buf1, buf0, k + 1)) break;
   }
+}
+
+template <int kWaves, int kEPT, bool kCells>
+__global__ __launch_bounds__(kWaves * 64) void tss_stream(StreamParams p) {
+  stream_body<kWaves, kEPT, kCells, false>(p);
+}
+
+// the stage-share instantiation, held to 80 VGPRs so that six workgroups
+// fit on a CU (its LDS allows six)
+template <int kWaves, int kEPT>
+__global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(6))) void tss_stream_stage(
+    StreamParams p) {
+  stream_body<kWaves, kEPT, false, true>(p);
 }
 
 // --------------------------------------------------------------- rebalance
@@ -1008,9 +1099,12 @@ static int chunk_windows(int M, uint32_t wcap) {
   return c;
 }
 
-static size_t stream_lds(const tre_events* ev) {
+static size_t stream_lds(const tre_events* ev, bool stage = false) {
   const size_t M = (size_t)ev->cfg.n_models, C = (size_t)chunk_windows(ev->cfg.n_models, ev->wcap);
-  return ev->wcap * (3 * M + 1) * 8 + 2 * C * M * 8;
+  const size_t base = ev->wcap * (3 * M + 1) * 8 + 2 * C * M * 8;
+  // stage: the decode ratios beside the prefill ones (which take the scalar
+  // ratios' place), two shares and two flags per model
+  return stage ? base + 2 * C * M * 8 + 2 * M * 8 + ((2 * M + 7) & ~(size_t)7) : base;
 }
 
 extern "C" int tre_load_events(const int64_t* ts, const uint8_t* model, const uint32_t* req,
@@ -1219,10 +1313,14 @@ static StreamParams stream_params(const tre_events* ev, const tre_profile* prof)
 }
 
 static int launch_stream(const tre_events* ev, const StreamParams& p, hipStream_t st) {
-  const size_t lds = stream_lds(ev);
+  const bool stage = p.stage64 || p.stage32 || p.sflags;
+  const size_t lds = stream_lds(ev, stage);
   LaunchTimer lt("tss_stream", st);
   const bool cells = p.prefill || p.decode || p.a_int || p.w_int || p.tss64 || p.tss32 || p.flags;
-  if (cells)
+  if (stage)
+    hipLaunchKernelGGL((tss_stream_stage<kStreamWaves, kStreamEPT>), dim3(ev->n_traces),
+                       dim3(kStreamWaves * 64), lds, st, p);
+  else if (cells)
     hipLaunchKernelGGL((tss_stream<kStreamWaves, kStreamEPT, true>), dim3(ev->n_traces),
                        dim3(kStreamWaves * 64), lds, st, p);
   else
@@ -1317,6 +1415,21 @@ extern "C" int tre_eval_tss(const tre_events* ev, const tre_profile* prof, const
   p.tss64 = out->tss64;
   p.tss32 = out->tss32;
   p.flags = out->flags;
+  return launch_stream(ev, p, (hipStream_t)stream);
+}
+
+extern "C" int tre_eval_stage(const tre_events* ev, const tre_profile* prof, double* stage64, float* stage32,
+                              uint8_t* flags, void* stream) {
+  if (!ev || !prof) return fail(TRE_EINVAL, "tre_eval_stage: NULL handle or profiles");
+  if (!stage64 && !stage32 && !flags) return fail(TRE_EINVAL, "tre_eval_stage: no output");
+  if (((uintptr_t)stage64 & 15) || ((uintptr_t)stage32 & 7))
+    return fail(TRE_EINVAL, "tre_eval_stage: stage64 needs 16-byte, stage32 8-byte alignment");
+  int rc = check_device(ev);
+  if (rc) return rc;
+  StreamParams p = stream_params(ev, prof);
+  p.stage64 = stage64;
+  p.stage32 = stage32;
+  p.sflags = flags;
   return launch_stream(ev, p, (hipStream_t)stream);
 }
 

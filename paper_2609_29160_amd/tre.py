@@ -87,7 +87,7 @@ EXPORTS = ["tre_last_error", "tre_load_events", "tre_free_events", "tre_events_i
            "tre_check_params", "tre_workspace_size", "tre_eval_tss", "tre_rebalance", "tre_sweep",
            "tre_set_timing", "tre_kernel_time", "tre_check_actuation", "tre_rebalance_act", "tre_sweep_act",
            "tre_calib_workspace_size", "tre_calibrate", "tre_loop_workspace_size", "tre_loop", "tre_loop_act",
-           "tre_stage_tss"]
+           "tre_stage_tss", "tre_eval_stage"]
 
 
 def _load():
@@ -135,6 +135,8 @@ def _load():
                                ctypes.POINTER(_Actuation), ctypes.POINTER(_CtlOut), vp, vp, vp, sz, vp]
     L.tre_stage_tss.restype = i32
     L.tre_stage_tss.argtypes = [vp, vp, ctypes.POINTER(_TssOut), vp, vp, vp, vp]
+    L.tre_eval_stage.restype = i32
+    L.tre_eval_stage.argtypes = [vp, vp, vp, vp, vp, vp]
     L.tre_set_timing.restype = i32
     L.tre_set_timing.argtypes = [i32]
     L.tre_kernel_time.restype = i32
@@ -272,6 +274,13 @@ def tre_stage_tss(ev: Events, prof: torch.Tensor, tallies: Dict[str, torch.Tenso
     t = _TssOut(*[_ptr(tallies.get(k)) for k in ("prefill", "decode", "a_int", "w_int")], None, None, None)
     _check(_L.tre_stage_tss(ev.handle, _ptr(prof), ctypes.byref(t), _ptr(out.get("stage64")),
                             _ptr(out.get("stage32")), _ptr(out.get("flags")), _stream(stream)))
+
+
+def tre_eval_stage(ev: Events, prof: torch.Tensor, out: Dict[str, torch.Tensor], stream=None):
+    """Stage-aware shares straight from the events (one pass, no tallies in
+    HBM); fills the given outputs of stage_outputs()."""
+    _check(_L.tre_eval_stage(ev.handle, _ptr(prof), _ptr(out.get("stage64")), _ptr(out.get("stage32")),
+                             _ptr(out.get("flags")), _stream(stream)))
 
 
 def ctl_outputs(ev: Events, n_scenarios: int, move_cap: int, device="cuda") -> Dict[str, torch.Tensor]:

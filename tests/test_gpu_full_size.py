@@ -192,7 +192,8 @@ def test_stress_full_size_calibration():
 def test_stress_full_size_stage_shares():
     """Tallies and stage-aware shares over the whole stress workload, twice:
     identical results, and the shares and flags of sampled traces equal to
-    the oracle's bit for bit."""
+    the oracle's bit for bit; then the one-pass path (tre_eval_stage), equal
+    to them in every cell."""
     import torch
 
     from paper_2609_29160_amd import device, tre
@@ -224,8 +225,17 @@ def test_stress_full_size_stage_shares():
         assert np.array_equal(runs[0]["stage64"][t].view(np.uint64), r["S"].view(np.uint64)), t
         assert np.array_equal(runs[0]["flags"][t], r["flags"]), t
     say(f"{w.name}: stage shares of {len(sample)} sampled traces match the oracle")
+    # the one-pass path: equal to the two-pass shares everywhere
+    del tal
+    torch.cuda.empty_cache()
+    fused = tre.stage_outputs(ev, which=("stage64", "flags"))
+    tre.tre_eval_stage(ev, prof, fused)
+    torch.cuda.synchronize()
+    assert torch.equal(fused["stage64"].view(torch.int64), out["stage64"].view(torch.int64)), "one-pass shares differ"
+    assert torch.equal(fused["flags"], out["flags"]), "one-pass flags differ"
+    say(f"{w.name}: one-pass stage shares equal the two-pass ones in every cell")
     ev.close()
-    del tal, out, dt
+    del out, fused, dt
     torch.cuda.empty_cache()
 
 

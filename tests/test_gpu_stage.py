@@ -1,5 +1,6 @@
-"""GPU parity of the stage-aware service shares (tre_stage_tss) against the
-oracle's.
+"""GPU parity of the stage-aware service shares against the oracle's, by
+both paths: tre_stage_tss (from the tallies of tre_eval_tss) and
+tre_eval_stage (one pass over the events).
 
 For every trace: the per-window prefill and decode shares in binary64 bit
 for bit, their binary32 copies equal to the round-to-nearest conversion of
@@ -69,29 +70,35 @@ def _check(lib, name, cfg, traces, prof_cols, repeat=1):
     prof = tre.pack(prof_cols, tre.PROFILE_DTYPE)
     tal = tre.tss_outputs(ev, which=("prefill", "decode", "a_int", "w_int"))
     tre.tre_eval_tss(ev, prof, tal)
-    first = None
-    for _ in range(repeat):
-        out = tre.stage_outputs(ev)
-        tre.tre_stage_tss(ev, prof, tal, out)
-        torch.cuda.synchronize()
-        got = {k: v.cpu().numpy() for k, v in out.items()}
-        if first is None:
-            first = got
-        else:
-            for k in got:
-                assert np.array_equal(got[k].view(np.uint8), first[k].view(np.uint8)), f"{name}: {k} differs between launches"
+    results = {}
+    for path in ("two-pass", "fused"):
+        for _ in range(repeat):
+            out = tre.stage_outputs(ev)
+            if path == "two-pass":
+                tre.tre_stage_tss(ev, prof, tal, out)
+            else:
+                tre.tre_eval_stage(ev, prof, out)
+            torch.cuda.synchronize()
+            got = {k: v.cpu().numpy() for k, v in out.items()}
+            if path not in results:
+                results[path] = got
+            else:
+                for k in got:
+                    assert np.array_equal(got[k].view(np.uint8), results[path][k].view(np.uint8)), \
+                        f"{name}: {path} {k} differs between launches"
     o = O.get()
     for t, tr in enumerate(traces):
         p = PT.trace_profile(prof_cols, t, M)
         ref_t = o.tss_trace(tr, win, dur, O.pack_profiles(p))
         ref = o.stage_tss(ref_t, win, O.pack_profiles(p))
-        what = f"{name} trace {t}"
-        s64 = first["stage64"][t]
-        bad = np.flatnonzero(s64.view(np.uint64) != ref["S"].view(np.uint64))
-        assert bad.size == 0, f"{what}: binary64 shares differ at {bad[:5]}: {s64.reshape(-1)[bad[:5]]} vs {ref['S'].reshape(-1)[bad[:5]]}"
-        for k, stage in ((0, "prefill"), (1, "decode")):
-            PT.compare_tss32(first["stage32"][t][..., k], ref["S"][..., k], f"{what} {stage} binary32")
-        assert np.array_equal(first["flags"][t], ref["flags"]), f"{what}: flags"
+        for path, first in results.items():
+            what = f"{name} trace {t} ({path})"
+            s64 = first["stage64"][t]
+            bad = np.flatnonzero(s64.view(np.uint64) != ref["S"].view(np.uint64))
+            assert bad.size == 0, f"{what}: binary64 shares differ at {bad[:5]}: {s64.reshape(-1)[bad[:5]]} vs {ref['S'].reshape(-1)[bad[:5]]}"
+            for k, stage in ((0, "prefill"), (1, "decode")):
+                PT.compare_tss32(first["stage32"][t][..., k], ref["S"][..., k], f"{what} {stage} binary32")
+            assert np.array_equal(first["flags"][t], ref["flags"]), f"{what}: flags"
     ev.close()
 
 
@@ -196,5 +203,9 @@ def test_argument_errors(lib):
     with pytest.raises(tre.TreError) as e:
         tre.tre_stage_tss(ev, prof, tal, {"stage64": bad})
     assert e.value.code == tre.TRE_EINVAL
+    for o in ({}, {"stage64": bad}):
+        with pytest.raises(tre.TreError) as e:
+            tre.tre_eval_stage(ev, prof, o)
+        assert e.value.code == tre.TRE_EINVAL
     torch.cuda.synchronize()
     ev.close()
