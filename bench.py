@@ -672,6 +672,8 @@ def calib_traffic_for(workload_name: str, events: int, kernel: str):
     src = os.path.join(ROOT, "paper_2609_29160_amd", "csrc", "calib.hip")
     if t.get("kernel_sha") != kernel_sha(src) or t.get("workload") != workload_name or t.get("events") != events:
         return None
+    if kernel == "tss_stream" and t.get("tre_sha") != kernel_sha():  # tss_stream's own source
+        return None
     return t.get("traffic_bytes_per_launch", {}).get(kernel)
 
 
