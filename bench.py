@@ -203,6 +203,8 @@ def main():
                 "kernel": "tss_stream", "kernel_ms": round(stream_ms, 4),
                 "alg_bytes_per_launch": alg_bytes}
 
+    stream_read = flat_read_rate(dt.cols["ts"], torch)
+    log(f"flat read of the ts column: {stream_read['gbs']} GB/s")
     cpu = None
     parity = None
     if not args.no_cpu:
@@ -235,6 +237,7 @@ def main():
                    {"wake_ms": ACT_WAKE_MS, "sleep_ms": ACT_SLEEP_MS, "footprint_gpus": "1-2, seeded",
                     "budget_gpus": act_in["budget"], "veto_tick_fraction": 0.1}},
         "roofline": roofline,
+        "stream_read": stream_read,
         "cpu_baseline": cpu,
         "parity": parity,
         "rebalance_ms": round(reb_ms, 4),
@@ -675,6 +678,26 @@ def calib_traffic_for(workload_name: str, events: int, kernel: str):
     if kernel == "tss_stream" and t.get("tre_sha") != kernel_sha():  # tss_stream's own source
         return None
     return t.get("traffic_bytes_per_launch", {}).get(kernel)
+
+
+def flat_read_rate(col, torch, reps=3):
+    """What a plain contiguous read of a resident column reaches on this
+    GPU (torch's sum over the int64 ts column, after the timed region): the
+    ceiling beside the kernel's roofline fraction, not part of `value`."""
+    col.sum()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        col.sum()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    nbytes = col.numel() * col.element_size()
+    return {"what": "torch.sum over the resident ts column (a flat read)", "bytes": nbytes, "ms": round(ms, 3),
+            "gbs": round(nbytes / (ms / 1e3) / 1e9, 1)}
 
 
 def copy_calibration(gb, torch):
