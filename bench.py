@@ -54,9 +54,10 @@ def kernel_sha(src: str = None) -> str:
     return hashlib.sha256(open(src or KERNEL_SRC, "rb").read()).hexdigest()[:16]
 
 
-def loop_traffic_for(workload_name: str):
-    """HBM bytes per loop_replay launch from committed counters taken on
-    this kernel source and workload; else None."""
+def loop_traffic_for(workload_name: str, key: str = "loop_replay"):
+    """HBM bytes per loop_replay launch (key "loop_replay_act": the
+    actuation instantiation) from committed counters taken on this kernel
+    source and workload; else None."""
     try:
         t = json.load(open(os.path.join(ROOT, "profiles", "loop_traffic.json")))
     except (OSError, ValueError):
@@ -64,7 +65,7 @@ def loop_traffic_for(workload_name: str):
     src = os.path.join(ROOT, "paper_2609_29160_amd", "csrc", "loop.hip")
     if t.get("kernel_sha") != kernel_sha(src) or t.get("workload") != workload_name:
         return None
-    return t.get("traffic_bytes_per_launch", {}).get("loop_replay")
+    return t.get("traffic_bytes_per_launch", {}).get(key)
 
 
 def traffic_for(workload_name: str, events: int):
@@ -356,7 +357,8 @@ def loop_main(args, w, tre, torch, np):
                     "gpu_budget": act_in["budget"], "veto_ticks": "10%"}},
         "roofline": {"bound": "hbm", "achieved": round(alg / (kern_ms / 1e3) / 1e9, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(alg / (kern_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
-                     "traffic": loop_traffic_for(w.name) if T == 4096 else None, "kernel": "loop_replay",
+                     "traffic": loop_traffic_for(w.name, "loop_replay" if act_in is None else "loop_replay_act")
+                     if T == 4096 else None, "kernel": "loop_replay",
                      "kernel_ms": round(kern_ms, 4), "alg_bytes_per_launch": alg,
                      "note": "latency-bound: each scenario is a sequential chain of windows; HBM is not "
                              "the limit (profiles/loop_replay_sq_counters_stress.md)"},
