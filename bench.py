@@ -23,7 +23,10 @@ decisions on that sample.
 1.87 s, rounded up to whole windows), footprints of 1 or 2 GPUs per replica
 drawn from a fixed seed with the GPU budget set to the largest initial
 footprint sum plus 8, and donor-release vetoes on 10% of the ticks; the CPU
-leg then runs the oracle's actuation replay.
+leg then runs the oracle's actuation replay. With ``--loop`` it replays the
+closed loop (``tre_loop_act``) with footprints by model class (7B 1, 13B 1,
+34B 2, 70B 4 GPUs per replica), 8 spare GPUs and the replica bound that
+follows, declared so that the slot pool is sized for it.
 """
 import argparse
 import hashlib
@@ -275,7 +278,6 @@ def loop_main(args, w, tre, torch, np):
     slo = np.zeros(T * M, tre.SLO_DTYPE)
     for k, v in w.slo_columns().items():
         slo[k] = v
-    rq, keep = tre.loop_requests(tables, M, svc, slo)
     n_req_trace = np.array([len(tb["arrival_ms"]) for tb in tables], np.int64)
     log(f"request tables: {int(n_req_trace.sum())} requests in {T} traces ({time.time() - t0:.1f} s)")
     cfg = w.trace_cfg()
@@ -294,12 +296,13 @@ def loop_main(args, w, tre, torch, np):
 
     act_in = None
     if args.actuation:
-        act_in = actuation_inputs(w)
+        act_in = loop_actuation_inputs(w)
         act_in["veto"] = actuation_vetoes(w, n_ticks)
         act_in["g_dev"] = torch.from_numpy(act_in["g"]).cuda()
         act_in["veto_dev"] = torch.from_numpy(act_in["veto"].view(np.int64)).cuda()
         cfg = dict(cfg, budget=act_in["budget"])
         act = tre.actuation(ACT_WAKE_MS, ACT_SLEEP_MS, act_in["g_dev"], act_in["veto_dev"])
+    rq, keep = tre.loop_requests(tables, M, svc, slo, max_replicas=0 if act_in is None else act_in["max_replicas"])
 
     def replay():
         if act_in is None:
@@ -353,8 +356,9 @@ def loop_main(args, w, tre, torch, np):
                    "duration_s": w.duration_ms // 1000, "requests": int(n_req_trace.sum()), "logical_requests": logical,
                    "slots_per_replica": 8, "r_cap": 16, "mode": "closed loop",
                    "actuation": None if act_in is None else
-                   {"wake_ms": ACT_WAKE_MS, "sleep_ms": ACT_SLEEP_MS, "footprint_gpus": "1-2, seeded",
-                    "gpu_budget": act_in["budget"], "veto_ticks": "10%"}},
+                   {"wake_ms": ACT_WAKE_MS, "sleep_ms": ACT_SLEEP_MS,
+                    "footprint_gpus": "by model class: " + ", ".join(f"{k} {v}" for k, v in CLASS_GPUS.items()),
+                    "gpu_budget": act_in["budget"], "max_replicas": act_in["max_replicas"], "veto_ticks": "10%"}},
         "roofline": {"bound": "hbm", "achieved": round(alg / (kern_ms / 1e3) / 1e9, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(alg / (kern_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
                      "traffic": loop_traffic_for(w.name, "loop_replay" if act_in is None else "loop_replay_act")
@@ -779,6 +783,37 @@ def actuation_inputs(w):
     g = rng.integers(1, 3, (w.n_traces, w.n_models)).astype(np.int32)
     r_init = np.asarray(w.profile_columns()["r_init"]).reshape(w.n_traces, w.n_models)
     return {"g": g, "budget": int((g * r_init).sum(axis=1).max()) + 8}
+
+
+CLASS_GPUS = {"7B": 1, "13B": 1, "34B": 2, "70B": 4}  # GPUs per replica of each model class
+
+
+def replica_bound(g, budget, r_cap):
+    """The most replicas a model set can hold at once: each model below
+    r_cap + 1 replicas, their footprints within the GPU budget; filling the
+    budget from the smallest footprint up reaches it."""
+    n, left = 0, budget
+    for gm in sorted(int(x) for x in g):
+        k = min(r_cap, left // gm)
+        n += k
+        left -= k * gm
+    return n
+
+
+def loop_actuation_inputs(w, r_cap=16):
+    """The closed loop's actuation model: footprints by model class
+    ([trace][model]), the GPU budget that holds every trace's initial
+    replicas with 8 GPUs to spare, and the most replicas the budget and the
+    replica cap allow at once, declared to tre_loop_act (it sizes the slot
+    pool)."""
+    import numpy as np
+
+    g1 = np.array([CLASS_GPUS[c] for c in w.model_classes], np.int32)
+    g = np.ascontiguousarray(np.broadcast_to(g1, (w.n_traces, w.n_models)))
+    r_init = np.asarray(w.profile_columns()["r_init"]).reshape(w.n_traces, w.n_models)
+    budget = int((g * r_init).sum(axis=1).max()) + 8
+    bound = max(replica_bound(row, budget, r_cap) for row in {tuple(r) for r in g})
+    return {"g": g, "budget": budget, "max_replicas": bound}
 
 
 def actuation_vetoes(w, n_ticks):

@@ -396,6 +396,9 @@ typedef struct {
   int32_t decode_chunk;        /* output tokens per DECODE event                */
   uint32_t max_prompt, max_output;         /* bounds over the table (host)      */
   uint32_t max_prefill_us, max_decode_us;  /* bounds over service (host)        */
+  uint32_t max_replicas;       /* most replicas holding slots at once in one
+                                  scenario, a bound the caller declares (0:
+                                  none); it sizes the slot pool below       */
 } tre_loop_requests;
 
 typedef struct {
@@ -407,8 +410,8 @@ typedef struct {
    16-byte tallies of future windows, its length the power of two that
    covers the longest service the declared bounds allow (in windows, + 2),
    plus per scenario the words of its slot-heap pool (below) as scratch.
-   The pool holds min(budget, n_models * min(r_cap, budget)) *
-   slots_per_replica + n_models words, rounded up to 4; TRE_EINVAL when 4
+   The pool holds min(budget, n_models * min(r_cap, budget), max_replicas
+   when nonzero) * slots_per_replica + n_models words, rounded up to 4; TRE_EINVAL when 4
    bytes x (that pool + 44 x n_models) exceed the 160 KiB of LDS one
    scenario's workgroup may use; TRE_ERANGE when duration_ms plus that
    longest service reaches 2^31 ms. */
@@ -423,9 +426,11 @@ int tre_loop_workspace_size(const tre_trace_cfg* cfg, const tre_loop_requests* r
    (device [n_scenarios][n_windows][n_models], or NULL). r_init must lie in
    [0, min(r_cap, budget)] with the sum within the budget, and req_off must
    index the request arrays; other inputs give unspecified results (never an
-   access outside them). Requests beyond the declared bounds give
-   unspecified results too; the workspace's first 8 bytes then count the
-   events dropped (0 otherwise). Enqueued on `stream`. */
+   access outside them). Requests beyond the declared bounds, or more
+   replicas at once than max_replicas, give unspecified results too; the
+   workspace's first 8 bytes then count the events dropped plus the
+   replicas' slots the pool could not hold (0 otherwise). Enqueued on
+   `stream`. */
 int tre_loop(const tre_trace_cfg* cfg, uint32_t n_traces, const tre_loop_requests* rq, const tre_profile* prof,
              const tre_scenario* sc, uint32_t n_scenarios, const tre_ctl_out* out, tre_loop_stats* stats,
              double* tss64, void* ws, size_t ws_bytes, void* stream);

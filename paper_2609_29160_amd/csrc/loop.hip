@@ -85,7 +85,7 @@ struct LoopParams {
   const uint64_t* veto;         // [trace][n_ticks] donor releases refused, or NULL
   int32_t wake_w, sleep_w;      // whole windows
   int32_t n_ticks;
-  unsigned long long* overflow; // events beyond the ring (declared bounds exceeded)
+  unsigned long long* overflow; // declared bounds exceeded: events beyond the ring, replica slots beyond the pool
   uint32_t move_cap;
   uint32_t n_sc;
   uint32_t n_traces;
@@ -96,7 +96,7 @@ struct LoopParams {
   int32_t pchunk;
   int32_t dchunk;
   int32_t pool_words;           // the heap pool: pool_reps * spr + M (a skew word per lane), multiple of 4
-  int32_t pool_reps;            // replicas the pool holds: min(budget, M * r_hi)
+  int32_t pool_reps;            // replicas the pool holds: min(budget, M * r_hi, the declared bound)
   uint64_t wmagic;              // x / window_ms == (x * wmagic) >> wshift for x < 2^31
   int32_t wshift;
   uint64_t pmagic, dmagic;      // the same for the prompt and output chunk sizes
@@ -252,9 +252,11 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
   uint32_t* cst = lane_cnt + M + mc;
   FarCell* far = p.far + (uint64_t)s * L * M + mc;  // cell c at far[c * M]
   // initial replicas: at most r_hi per model and pool_reps in all (initial
-  // replicas within the budget are never cut)
+  // replicas within the budget and the declared bound are never cut; cut
+  // ones are counted as bounds exceeded)
   const int r_hi = p.r_hi;
   int R = act ? (r_init < 0 ? 0 : (r_init > r_hi ? r_hi : r_init)) : 0;
+  unsigned slots_over = 0;  // replicas / slots the pool could not hold
   {
     int incl = R;
     for (int o = 1; o < 64; o <<= 1) {
@@ -262,7 +264,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
       if (lane >= o) incl += v;
     }
     const int room = p.pool_reps - (incl - R);
+    const int R0 = R;
     R = R < room ? R : (room > 0 ? room : 0);
+    slots_over += (unsigned)(R0 - R);
   }
   // GPUs per replica (1 without the actuation model); idle GPUs (replicas)
   // (at least 1, so that the replicas never outnumber the budget's GPUs and
@@ -315,6 +319,20 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
     for (int q = 0; q < pops && hs > 0; ++q) {
       --hs;
       if (hs > 0) old.replace_top(hs, old.at(hs));
+    }
+    // the pool holds pool_reps * spr slots: pushes beyond it (a declared
+    // replica bound exceeded) are dropped, in lane order
+    {
+      int tot = hs, pin = pushes;
+      for (int o = 1; o < 64; o <<= 1) {
+        const int v = __shfl_up(pin, o);
+        if (lane >= o) pin += v;
+      }
+      for (int o = 32; o > 0; o >>= 1) tot += __shfl_xor(tot, o);
+      int allowed = p.pool_reps * spr - tot - (pin - pushes);
+      allowed = allowed < 0 ? 0 : (allowed > pushes ? pushes : allowed);
+      slots_over += (unsigned)(pushes - allowed);
+      pushes = allowed;
     }
     const int want = act ? hs + pushes : 0;
     int incl = want;
@@ -718,6 +736,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
     p.stats[(uint64_t)s * M + lane] = st;
   }
   if (lane == 0) p.n_moves[s] = nm;
+  overflow += slots_over;
   for (int o = 32; o > 0; o >>= 1) overflow += __shfl_xor(overflow, o);
   if (lane == 0 && overflow) atomicAdd(p.overflow, (unsigned long long)overflow);
 }
@@ -745,7 +764,9 @@ int r_hi(const tre_trace_cfg* cfg, const tre_loop_requests* rq) {
 // multiple of 4
 int pool_reps(const tre_trace_cfg* cfg, const tre_loop_requests* rq) {
   const int64_t all = (int64_t)cfg->n_models * r_hi(cfg, rq);
-  return (int)(cfg->budget < all ? cfg->budget : all);
+  int64_t v = cfg->budget < all ? cfg->budget : all;
+  if (rq->max_replicas > 0 && (int64_t)rq->max_replicas < v) v = rq->max_replicas;
+  return (int)v;
 }
 int pool_words(const tre_trace_cfg* cfg, const tre_loop_requests* rq) {
   return (int)(((int64_t)pool_reps(cfg, rq) * rq->slots_per_replica + cfg->n_models + 3) & ~3ll);

@@ -75,7 +75,8 @@ class _CtlOut(ctypes.Structure):
 class _LoopRequests(ctypes.Structure):
     _fields_ = [(k, ctypes.c_void_p) for k in ("arrival_ms", "prompt", "output", "req_off", "service", "slo")] + \
                [(k, ctypes.c_int32) for k in ("slots_per_replica", "r_cap", "prefill_chunk", "decode_chunk")] + \
-               [(k, ctypes.c_uint32) for k in ("max_prompt", "max_output", "max_prefill_us", "max_decode_us")]
+               [(k, ctypes.c_uint32) for k in ("max_prompt", "max_output", "max_prefill_us", "max_decode_us",
+                                               "max_replicas")]
 
 
 class _Actuation(ctypes.Structure):
@@ -387,10 +388,13 @@ def _cfg(cfg: Dict[str, int]) -> _TraceCfg:
 
 
 def loop_requests(tables, n_models: int, service: np.ndarray, slo: np.ndarray, slots_per_replica: int = 8,
-                  r_cap: int = 16, prefill_chunk: int = 2048, decode_chunk: int = 24, device="cuda"):
+                  r_cap: int = 16, prefill_chunk: int = 2048, decode_chunk: int = 24, max_replicas: int = 0,
+                  device="cuda"):
     """Device request tables of tre_loop from per-trace host tables
     (arrival_ms, model, prompt, output; grouped by model, arrivals in order
-    within a model). Returns (struct, tensors); keep the tensors alive."""
+    within a model). max_replicas: a declared bound on the replicas holding
+    slots at once in one scenario (0: none). Returns (struct, tensors); keep
+    the tensors alive."""
     counts = []
     for tb in tables:
         m = np.asarray(tb["model"], np.int64)
@@ -409,7 +413,8 @@ def loop_requests(tables, n_models: int, service: np.ndarray, slo: np.ndarray, s
     rq = _LoopRequests(_ptr(tens["arrival_ms"]), _ptr(tens["prompt"]), _ptr(tens["output"]), _ptr(tens["req_off"]),
                        _ptr(tens["service"]), _ptr(tens["slo"]), slots_per_replica, r_cap, prefill_chunk,
                        decode_chunk, int(host["prompt"].max(initial=1)), int(host["output"].max(initial=1)),
-                       int(svc["prefill_us"].max(initial=0)), int(svc["decode_us"].max(initial=0)))
+                       int(svc["prefill_us"].max(initial=0)), int(svc["decode_us"].max(initial=0)),
+                       int(max_replicas))
     return rq, tens
 
 

@@ -55,7 +55,8 @@ def _n_ticks(cfg):
                or ((w + 1) * cfg["window_ms"]) % cfg["slow_period_ms"] == 0)
 
 
-def _check(lib, name, cfg, tables, prof_cols, slo_cols, svc_cols, sc_cols, spr=8, r_cap=16, act=None):
+def _check(lib, name, cfg, tables, prof_cols, slo_cols, svc_cols, sc_cols, spr=8, r_cap=16, act=None,
+           max_replicas=0):
     """act: (wake_ms, sleep_ms, footprint [T][M] int32 or None, veto [T][n_ticks] uint64 or None) runs
     tre_loop_act against the oracle's closed loop with the actuation model."""
     tre, device, torch = lib
@@ -68,7 +69,7 @@ def _check(lib, name, cfg, tables, prof_cols, slo_cols, svc_cols, sc_cols, spr=8
     slo = np.zeros(T * M, tre.SLO_DTYPE)
     for k in tre.SLO_DTYPE.names:
         slo[k] = slo_cols[k]
-    rq, keep = tre.loop_requests(tables, M, svc, slo, slots_per_replica=spr, r_cap=r_cap)
+    rq, keep = tre.loop_requests(tables, M, svc, slo, slots_per_replica=spr, r_cap=r_cap, max_replicas=max_replicas)
     prof = tre.pack(prof_cols, tre.PROFILE_DTYPE)
     sc = tre.pack(sc_cols, tre.SCENARIO_DTYPE)
     n_sc = len(sc_cols["trace"])
@@ -311,6 +312,61 @@ def test_actuation_hand_case(lib):
           "tau_crit_override": -np.ones(1)}
     n = _check(lib, "act-hand", cfg, [table], prof, slo, svc, sc, spr=1, r_cap=3, act=(200, 100, None, None))
     assert n == 2
+
+
+CLASS_GPUS = {"7B": 1, "13B": 1, "34B": 2, "70B": 4}
+
+
+def test_declared_replica_bound(lib):
+    """Footprints by model class and a declared bound on the replicas
+    holding slots (the most the GPU budget and the replica cap allow): the
+    same results as the oracle's; and bounds that a replay exceeds are
+    counted, never written past the pool."""
+    tre, device, torch = lib
+    w = tg.standard(1).scaled(duration_ms=900_000)
+    tables = [w.requests(0)]
+    rng = np.random.default_rng(44)
+    M = w.n_models
+    fp = np.array([[CLASS_GPUS[c] for c in w.model_classes]], np.int32)
+    r_init = np.asarray(w.profile_columns(1)["r_init"])
+    spare = 6
+    cfg = dict(w.trace_cfg(), budget=int((fp[0] * r_init).sum()) + spare)
+    # the most replicas the budget allows with at most r_cap per model:
+    # filled from the smallest footprint up (a donor's excess GPUs can wake
+    # further small replicas, so the initial count plus the idle GPUs is no
+    # bound)
+    bound, left = 0, cfg["budget"]
+    for gm in sorted(fp[0].tolist()):
+        k = min(10, left // gm)
+        bound, left = bound + k, left - k * gm
+    assert bound < cfg["budget"]
+    sc_cols = _scenarios(rng, 12, 1)
+    act = (1310, 1870, fp, None)
+    n = _check(lib, "bound", cfg, tables, w.profile_columns(1), w.slo_columns(1), w.service_columns(1), sc_cols,
+               r_cap=10, act=act, max_replicas=bound)
+    assert n > 0
+    # too small: the initial replicas cut, or the pool's wakes beyond it
+    svc = np.zeros(M, tre.SERVICE_DTYPE)
+    for k in tre.SERVICE_DTYPE.names:
+        svc[k] = w.service_columns(1)[k]
+    slo = np.zeros(M, tre.SLO_DTYPE)
+    for k in tre.SLO_DTYPE.names:
+        slo[k] = w.slo_columns(1)[k]
+    prof = tre.pack(w.profile_columns(1), tre.PROFILE_DTYPE)
+    sc = tre.pack(sc_cols, tre.SCENARIO_DTYPE)
+    nW = cfg["duration_ms"] // cfg["window_ms"]
+    move_cap = max(1, _n_ticks(cfg) * int(np.max(sc_cols["max_moves"])))
+    fp_t = torch.from_numpy(fp).cuda()
+    for small in (int(r_init.sum()) - 1, int(r_init.sum())):
+        rq, keep = tre.loop_requests(tables, M, svc, slo, r_cap=10, max_replicas=small)
+        out = tre.ctl_outputs(_Ev(1, M, nW), 12, move_cap)
+        stats = torch.zeros(12 * M * tre.LOOP_STATS_DTYPE.itemsize, dtype=torch.uint8, device="cuda")
+        ws = torch.empty(tre.tre_loop_workspace_size(cfg, rq, 12), dtype=torch.uint8, device="cuda")
+        tre.tre_loop_act(cfg, 1, rq, prof, sc, tre.actuation(1310, 1870, fp_t), out, stats, ws)
+        torch.cuda.synchronize()
+        over = int(ws[:8].cpu().numpy().view(np.uint64)[0])
+        say(f"bound {small}: {over} counted beyond the declared bounds")
+        assert over > 0
 
 
 def test_argument_errors(lib):
