@@ -49,7 +49,7 @@ def test_struct_layouts():
     assert tre.SLO_DTYPE.itemsize == 40 and tre.FIT_DTYPE.itemsize == 24
     assert tre.REQ_LATENCY_DTYPE.itemsize == 24
     assert tre.SERVICE_DTYPE.itemsize == 8 and tre.LOOP_STATS_DTYPE.itemsize == 32
-    assert ctypes.sizeof(tre._LoopRequests) == 6 * 8 + 8 * 4
+    assert ctypes.sizeof(tre._LoopRequests) == 6 * 8 + 9 * 4 + 4  # padded to 8
 
 
 def test_error_message_without_gpu_call():
