@@ -62,7 +62,8 @@ extern "C" const char* tre_last_error(void) { return g_err.c_str(); }
 // ------------------------------------------------------------------ handle
 
 // ------------------------------------------------------------ constants
-constexpr int kStreamWaves = 4;            // tss_stream workgroup (waves)
+constexpr int kStreamWaves = 4;            // tss_stream workgroup (waves) with many traces
+constexpr int kEvalThreads = 256;          // threads that evaluate a step's cells (one cell each)
 constexpr int kStreamEPT = 4;              // rows per lane per tile
 constexpr int kRingBytes = 13 * 1024;      // LDS budget of the tally ring
 constexpr uint32_t kNoDefer = 0xFFFFFFFFu;
@@ -367,7 +368,7 @@ __device__ __forceinline__ void stream_body(const StreamParams& p) {
   }
 
   // the cell this thread evaluates: model rm, window offset rj in the chunk
-  // (C is a power of two and C * M <= threads)
+  // (C is a power of two and C * M <= kEvalThreads <= threads; the rest have no cell)
   const int rm = tid / C, rj = tid & (C - 1);
   const bool r_thread = rm < M;
   double w_p = 0.0, w_q = 0.0;
@@ -1091,12 +1092,22 @@ static uint32_t ring_windows(int M) {
   return w;
 }
 
-// windows evaluated per step: a power of two, one cell per thread, at most
-// half the ring
+// windows evaluated per step: a power of two, one cell per thread of the
+// first kEvalThreads, at most half the ring (the same for every workgroup
+// size, so the LDS layout does not depend on it)
 static int chunk_windows(int M, uint32_t wcap) {
   int c = 32;
-  while (c > 1 && (c * M > kStreamWaves * 64 || c > (int)wcap / 2)) c >>= 1;
+  while (c > 1 && (c * M > kEvalThreads || c > (int)wcap / 2)) c >>= 1;
   return c;
+}
+
+// Waves per tss_stream workgroup. One workgroup streams one trace; with 4
+// waves (about 75 VGPRs) six fit on a CU, so 1536 traces fill the chip.
+// With fewer traces the resident workgroups alone cannot keep enough loads
+// in flight, so each trace gets a larger workgroup: 16 waves (one per CU,
+// four per SIMD) up to 384 traces, 8 waves up to 768.
+static int stream_waves(uint32_t n_traces) {
+  return n_traces <= 384 ? 16 : (n_traces <= 768 ? 8 : kStreamWaves);
 }
 
 static size_t stream_lds(const tre_events* ev, bool stage = false) {
@@ -1317,9 +1328,18 @@ static int launch_stream(const tre_events* ev, const StreamParams& p, hipStream_
   const size_t lds = stream_lds(ev, stage);
   LaunchTimer lt("tss_stream", st);
   const bool cells = p.prefill || p.decode || p.a_int || p.w_int || p.tss64 || p.tss32 || p.flags;
+  const int waves = stream_waves(ev->n_traces);
   if (stage)
     hipLaunchKernelGGL((tss_stream_stage<kStreamWaves, kStreamEPT>), dim3(ev->n_traces),
                        dim3(kStreamWaves * 64), lds, st, p);
+  else if (waves == 16 && cells)
+    hipLaunchKernelGGL((tss_stream<16, kStreamEPT, true>), dim3(ev->n_traces), dim3(16 * 64), lds, st, p);
+  else if (waves == 16)
+    hipLaunchKernelGGL((tss_stream<16, kStreamEPT, false>), dim3(ev->n_traces), dim3(16 * 64), lds, st, p);
+  else if (waves == 8 && cells)
+    hipLaunchKernelGGL((tss_stream<8, kStreamEPT, true>), dim3(ev->n_traces), dim3(8 * 64), lds, st, p);
+  else if (waves == 8)
+    hipLaunchKernelGGL((tss_stream<8, kStreamEPT, false>), dim3(ev->n_traces), dim3(8 * 64), lds, st, p);
   else if (cells)
     hipLaunchKernelGGL((tss_stream<kStreamWaves, kStreamEPT, true>), dim3(ev->n_traces),
                        dim3(kStreamWaves * 64), lds, st, p);
