@@ -42,7 +42,11 @@ WORKLOADS = {"tiny": 0, "bursty": 1, "sweep": 2, "diverse": 3, "stress": 4}
 HBM_PEAK_GBS = 8000.0
 ALG_BYTES_PER_EVENT = 12
 CPU_EVENT_BUDGET = 3_000_000_000
-CPU_WORKERS = 16  # the host CPU share of one GPU
+# Oracle threads: the CPU share of one GPU on the measurement hosts (their
+# rules cap a one-GPU job's worker pools at 16 whatever the host shows);
+# cpu_baseline reports these threads as "cores" and the host's own CPU
+# count and model beside them.
+CPU_WORKERS = 16
 ACT_WAKE_MS, ACT_SLEEP_MS = 1310, 1870  # measured reactivation and sleep times
 ACT_SEED = 2609
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "tss_stream_traffic.json")
@@ -51,6 +55,24 @@ KERNEL_SRC = os.path.join(ROOT, "paper_2609_29160_amd", "csrc", "tre.hip")
 
 def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def host_cpu():
+    """The host's CPU model (from /proc/cpuinfo), its logical CPUs and the
+    CPUs this process may run on."""
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    try:
+        affinity = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        affinity = None
+    return {"cpu_model": model, "host_logical_cpus": os.cpu_count(), "affinity_cpus": affinity}
 
 
 def kernel_sha(src: str = None) -> str:
@@ -426,7 +448,7 @@ def loop_cpu_leg(w, tables, sc_cols, out, stats, move_cap, n_sample, n_workers, 
             all(np.array_equal(moves[s][:k][f], r["moves"][:k][f]) for f in ("window", "path", "receiver", "donor")) and \
             all(np.array_equal(st[s][f], r["stats"][f]) for f in tre.LOOP_STATS_DTYPE.names)
         bad += 0 if ok else 1
-    cpu = {"value": round(reqs / wall, 1), "unit": "requests/s", "cores": n_workers, "kind": "oracle",
+    cpu = {"value": round(reqs / wall, 1), "unit": "requests/s", "cores": n_workers, **host_cpu(), "kind": "oracle",
            "sample": f"{len(sample)} of {len(sc_all)} scenarios ({reqs} requests): {wall:.1f} s wall on {n_workers} "
                      f"host threads (one scenario per oracle call), {cpu_s:.1f} s of their CPU time",
            "one_core_value": round(reqs / cpu_s, 1)}
@@ -661,7 +683,7 @@ def stage_cpu_leg(w, sample, out, threads):
                 ok = np.array_equal(g64.view(np.uint64), rf["S"].view(np.uint64)) and np.array_equal(gfl, rf["flags"])
                 bad += 0 if ok else 1
             del host, evs
-    cpu = {"value": round(events / wall, 1), "unit": "request-events/s", "cores": n_workers, "kind": "oracle",
+    cpu = {"value": round(events / wall, 1), "unit": "request-events/s", "cores": n_workers, **host_cpu(), "kind": "oracle",
            "sample": f"{len(sample)} of {w.n_traces} traces ({events} events): {wall:.1f} s wall on {n_workers} "
                      f"host threads (one trace per oracle call: tallies, TSS and stage shares), {cpu_s:.1f} s of "
                      f"their CPU time",
@@ -765,7 +787,7 @@ def calib_cpu_leg(w, sample, out, tss, req_cap, tre, threads):
         for k in ("n_cand", "n_healthy", "n_above", "healthy_above"):
             ok = ok and np.array_equal(fit[t][k], rf["fit"][k])
         bad += 0 if ok else 1
-    cpu = {"value": round(events / wall, 1), "unit": "request-events/s", "cores": n_workers, "kind": "oracle",
+    cpu = {"value": round(events / wall, 1), "unit": "request-events/s", "cores": n_workers, **host_cpu(), "kind": "oracle",
            "sample": f"{len(sample)} of {w.n_traces} traces ({events} events): {wall:.1f} s wall on {n_workers} "
                      f"host threads (one trace per oracle call), {cpu_s:.1f} s of their CPU time",
            "one_core_value": round(events / cpu_s, 1)}
@@ -906,7 +928,7 @@ def cpu_leg(w, sample, sc_cols, out, move_cap, tre, threads, act_in=None):
             exp = ref["moves"][:min(k, move_cap)]
             ok = all(np.array_equal(got[f], exp[f]) for f in ("window", "path", "receiver", "donor"))
         bad += 0 if ok else 1
-    cpu = {"value": round(logical / wall, 1), "unit": "request-events/s", "cores": n_workers, "kind": "oracle",
+    cpu = {"value": round(logical / wall, 1), "unit": "request-events/s", "cores": n_workers, **host_cpu(), "kind": "oracle",
            "sample": f"{len(sample)} of {w.n_traces} traces ({events} events), {len(refs)} scenarios: "
                      f"{wall:.1f} s wall on {n_workers} host threads (one trace per oracle call), "
                      f"{cpu_s:.1f} s of their CPU time",

@@ -49,6 +49,8 @@ extern "C" {
 #define TRE_ERANGE 4  /* a trace exceeds the library's counting limits         */
 #define TRE_ENOMEM 5  /* workspace too small                                   */
 #define TRE_EHIP 6    /* HIP runtime error                                     */
+#define TRE_ESTATE 7  /* a request count of Eq. (1) below zero, or a request
+                         admitted twice (see tre_load_events)                 */
 
 /* Maximum models per trace (one wavefront lane per model). */
 #define TRE_MAX_MODELS 64
@@ -61,7 +63,8 @@ extern "C" {
  * One event per row, structure of arrays, sorted by ts within each trace:
  *   ts      int64   ms from trace start, 0 <= ts < duration_ms
  *   model   uint8   model index < n_models
- *   req     uint32  request id (stored, never read by the replay)
+ *   req     uint32  request id (read only by the load-time admission check
+ *                   and the calibration sweep; may be NULL otherwise)
  *   type    uint8   bits 0-1 kind: 0 ARRIVE (joins the model's waiting
  *                   queue), 1 PREFILL (prompt tokens served), 2 DECODE
  *                   (output tokens served), 3 FINISH (leaves the active set);
@@ -179,9 +182,26 @@ const char* tre_last_error(void);
    (row trace_off[n_traces] - 1): tile loads are rounded up to 16 bytes.
    duration_ms must be below 2^32 and a trace below 2^27 events.
    With flags & TRE_VALIDATE the events are checked on the device and the
-   call waits for the result (TRE_EORDER, TRE_ESCHEMA, TRE_ERANGE); without
-   it, events that break these rules give unspecified results, never an
-   access outside the columns, outputs or workspace. The
+   call waits for the result:
+     TRE_EORDER   a timestamp unsorted within its trace or outside
+                  [0, duration_ms);
+     TRE_ESCHEMA  a model index >= n_models or undefined type bits;
+     TRE_ERANGE   more events in one window of one trace than the limit;
+     TRE_ESTATE   the active or the waiting count of a model (A_m(t),
+                  W_m(t) of Eq. (1), Section "Design Rationale and
+                  Definition": numbers of requests) below zero at some
+                  instant t, i.e. after the last row with that timestamp
+                  (rows of one instant may come in any order); or, when
+                  `req` is given, one request id carrying the ADMIT bit on
+                  more than one row of a trace (a request is admitted once).
+   The first three are checked together and the message names the lowest
+   failing row and its kind; TRE_ESTATE is checked only when they pass
+   (the lowest failing row, or the smallest duplicated trace and id).
+   The id check allocates temporary device memory, one bit per id up to the
+   largest admitted id of each trace (at most 256 MiB at a time, or one
+   trace's bitmap if larger), freed before the call returns. Without
+   TRE_VALIDATE, events that break these rules give unspecified results,
+   never an access outside the columns, outputs or workspace. The
    handle owns small device tables (offsets, tick list); free it with
    tre_free_events. */
 #define TRE_VALIDATE 1u

@@ -80,6 +80,10 @@ class Oracle:
         L.oracle_smooth.argtypes = [f64, f64, f64]
         L.oracle_tss_trace.restype = ctypes.c_int
         L.oracle_tss_trace.argtypes = [vp, vp, vp, vp, i64, i64, i64, i32, vp, vp, vp, vp, vp, vp, vp]
+        self.has_admits = hasattr(L, "oracle_check_admits")
+        if self.has_admits:
+            L.oracle_check_admits.restype = ctypes.c_int
+            L.oracle_check_admits.argtypes = [vp, vp, i64, vp, vp]
         L.oracle_control.restype = ctypes.c_int
         L.oracle_control.argtypes = [i64, i64, i64, i64, i32, i32, vp, vp, vp, vp, vp, u32, vp, vp, vp]
         self.has_act = hasattr(L, "oracle_control_act")
@@ -141,6 +145,32 @@ class Oracle:
         if rc:
             raise ValueError(f"oracle_tss_trace rejected the trace ({rc})")
         return out
+
+    def trace_status(self, ev: Dict[str, np.ndarray], window_ms: int, duration_ms: int, M: int) -> int:
+        """The code oracle_tss_trace returns for a trace (0 when it accepts
+        it; -2 order, -3 schema, -5 a negative active or waiting count)."""
+        nW = duration_ms // window_ms
+        prof = np.zeros(M, PROFILE_DTYPE)
+        prof["alpha"] = 1.0
+        prof["theta"] = 1.0
+        ts = np.ascontiguousarray(ev["ts"], np.int64)
+        cols = [ts, np.ascontiguousarray(ev["model"], np.uint8), np.ascontiguousarray(ev["type"], np.uint8),
+                np.ascontiguousarray(ev["tokens"], np.uint16)]
+        outs = [np.zeros((nW, M), np.int64) for _ in range(4)] + [np.zeros((nW, M), np.float64),
+                                                                  np.zeros((nW, M), np.uint8)]
+        return int(self.L.oracle_tss_trace(*[c.ctypes.data for c in cols], ts.shape[0], window_ms, duration_ms, M,
+                                           prof.ctypes.data, *[o.ctypes.data for o in outs]))
+
+    def check_admits(self, ev: Dict[str, np.ndarray]):
+        """(0, None) when no request id is admitted twice in the trace, else
+        (-6, the smallest such id)."""
+        req = np.ascontiguousarray(ev["req"], np.uint32)
+        typ = np.ascontiguousarray(ev["type"], np.uint8)
+        scratch = np.zeros(max(1, req.shape[0]), np.uint32)
+        dup = np.zeros(1, np.uint32)
+        rc = int(self.L.oracle_check_admits(req.ctypes.data, typ.ctypes.data, req.shape[0], scratch.ctypes.data,
+                                            dup.ctypes.data))
+        return rc, (int(dup[0]) if rc else None)
 
     def control(self, cfg: Dict[str, int], prof: np.ndarray, S: np.ndarray, flags: np.ndarray,
                 sc: np.ndarray, move_cap: Optional[int] = None) -> Dict[str, np.ndarray]:

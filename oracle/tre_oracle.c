@@ -37,6 +37,7 @@
  */
 #include <math.h>
 #include <stdint.h>
+#include <stdlib.h>
 #include <string.h>
 
 /* event type byte: bits 0-1 kind, bit 7 admit */
@@ -129,7 +130,17 @@ static void integrate(int64_t* integ, int32_t M, int32_t m, int64_t window_ms, i
  * Window observations and smoothed TSS for one trace.
  * Events must be sorted by ts within the trace, 0 <= ts < duration_ms.
  * Outputs are [n_windows][n_models], n_windows = duration_ms / window_ms.
- * Returns 0, or a negative code for invalid input.
+ * Returns 0, or a negative code for invalid input:
+ *   -2  timestamp unsorted or outside [0, duration_ms)
+ *   -3  model index >= M or undefined type bits
+ *   -5  A_m(t) or W_m(t) negative at some instant t.
+ * The last code follows from the definition of Eq. (1) (Section "Design
+ * Rationale and Definition"): A_m(t) and W_m(t) are the numbers of active and
+ * of waiting requests of model m at time t, so neither can be negative. They
+ * are the right-continuous step functions of the transitions, so the value
+ * at t counts every event with ts <= t: the order of the rows that share one
+ * timestamp does not matter, only the counts after the last of them.
+ * The first two kinds are checked over the whole trace before the third.
  * -------------------------------------------------------------------- */
 int oracle_tss_trace(const int64_t* ts, const uint8_t* model, const uint8_t* type,
                      const uint16_t* tokens, int64_t n_events, int64_t window_ms,
@@ -144,6 +155,13 @@ int oracle_tss_trace(const int64_t* ts, const uint8_t* model, const uint8_t* typ
   memset(A_int, 0, sizeof(int64_t) * (size_t)(nW * M));
   memset(W_int, 0, sizeof(int64_t) * (size_t)(nW * M));
 
+  /* order and schema of every row first */
+  for (int64_t i = 0; i < n_events; ++i) {
+    if (ts[i] < 0 || ts[i] >= duration_ms || (i > 0 && ts[i] < ts[i - 1])) return -2;
+    const int admit = (type[i] & OR_ADMIT) != 0;
+    if (model[i] >= M || (type[i] & 0x7C) || (admit && (type[i] & 3) != OR_PREFILL)) return -3;
+  }
+
   /* A_m(t), W_m(t): right-continuous step functions starting at 0 */
   int64_t A[OR_MAX_MODELS], W[OR_MAX_MODELS], t_last[OR_MAX_MODELS];
   for (int m = 0; m < M; ++m) { A[m] = 0; W[m] = 0; t_last[m] = 0; }
@@ -151,10 +169,8 @@ int oracle_tss_trace(const int64_t* ts, const uint8_t* model, const uint8_t* typ
   for (int64_t i = 0; i < n_events; ++i) {
     const int64_t t = ts[i];
     const int m = model[i];
-    if (t < 0 || t >= duration_ms || m >= M || (i > 0 && t < ts[i - 1])) return -2;
     const int kind = type[i] & 3;
     const int admit = (type[i] & OR_ADMIT) != 0;
-    if ((type[i] & 0x7C) || (admit && kind != OR_PREFILL)) return -3;
     /* the counts held on [t_last, t) */
     integrate(A_int, M, m, window_ms, A[m], t_last[m], t);
     integrate(W_int, M, m, window_ms, W[m], t_last[m], t);
@@ -169,6 +185,11 @@ int oracle_tss_trace(const int64_t* ts, const uint8_t* model, const uint8_t* typ
       case OR_DECODE: D[w * M + m] += tokens[i]; break;
       case OR_FINISH: A[m] -= 1; break;               /* leaves the active set */
     }
+    /* after the last row at this instant every count is the value of its
+       step function there */
+    if (i == n_events - 1 || ts[i + 1] != t)
+      for (int k = 0; k < M; ++k)
+        if (A[k] < 0 || W[k] < 0) return -5;
   }
   for (int m = 0; m < M; ++m) {
     integrate(A_int, M, m, window_ms, A[m], t_last[m], duration_ms);
@@ -298,5 +319,31 @@ int oracle_control(int64_t window_ms, int64_t duration_ms, int64_t fast_ms, int6
   }
   for (int m = 0; m < M; ++m) r_final[m] = R[m];
   *n_moves = nm;
+  return 0;
+}
+
+static int cmp_u32(const void* a, const void* b) {
+  const uint32_t x = *(const uint32_t*)a, y = *(const uint32_t*)b;
+  return x < y ? -1 : (x > y ? 1 : 0);
+}
+
+/* ----------------------------------------------------------------------
+ * Request identity check for one trace: a request is admitted once, on its
+ * first prefill chunk (the ADMIT bit moves it from the waiting to the active
+ * set of Eq. (1), Section "Design Rationale and Definition"). Returns 0, or
+ * -6 when some request id carries the ADMIT bit on more than one row, with
+ * the smallest such id in *dup_id. ids_scratch holds n_events ids.
+ * -------------------------------------------------------------------- */
+int oracle_check_admits(const uint32_t* req, const uint8_t* type, int64_t n_events,
+                        uint32_t* ids_scratch, uint32_t* dup_id) {
+  int64_t n = 0;
+  for (int64_t i = 0; i < n_events; ++i)
+    if (type[i] == (OR_PREFILL | OR_ADMIT)) ids_scratch[n++] = req[i];
+  qsort(ids_scratch, (size_t)n, sizeof(uint32_t), cmp_u32);
+  for (int64_t i = 1; i < n; ++i)
+    if (ids_scratch[i] == ids_scratch[i - 1]) {
+      *dup_id = ids_scratch[i];
+      return -6;
+    }
   return 0;
 }

@@ -968,6 +968,9 @@ __global__ __launch_bounds__(256) void rebalance(CtlParams p) {
 }
 
 // ---------------------------------------------------------------- validate
+// Error kinds of the load-time checks, one bit and one lowest-row slot each.
+enum { kValOrder = 0, kValSchema = 1, kValRange = 2, kValState = 3, kValKinds = 4 };
+
 struct ValParams {
   const int64_t* ts;
   const uint8_t* model;
@@ -978,8 +981,8 @@ struct ValParams {
   int64_t window_ms;
   int32_t M;
   int64_t max_per_window;
-  unsigned* err;             // bit 0 order, bit 1 schema, bit 2 range
-  unsigned long long* first; // lowest failing row
+  unsigned* err;             // bit k: an error of kind k
+  unsigned long long* first; // [kValKinds] lowest failing row of each kind
 };
 
 constexpr int kValChunk = 16384;
@@ -994,14 +997,171 @@ __global__ __launch_bounds__(256) void validate(ValParams p) {
       const int64_t t_i = p.ts[i];
       const uint32_t ty = p.type[i];
       unsigned bad = 0;
-      if (t_i < 0 || t_i >= p.duration_ms || (i > b && t_i < p.ts[i - 1])) bad |= 1u;
-      if (p.model[i] >= p.M || (ty & 0x7Cu) || ((ty & TRE_ADMIT) && (ty & 3u) != TRE_PREFILL)) bad |= 2u;
+      if (t_i < 0 || t_i >= p.duration_ms || (i > b && t_i < p.ts[i - 1])) bad |= 1u << kValOrder;
+      if (p.model[i] >= p.M || (ty & 0x7Cu) || ((ty & TRE_ADMIT) && (ty & 3u) != TRE_PREFILL))
+        bad |= 1u << kValSchema;
       const int64_t j = i + p.max_per_window;
-      if (!(bad & 1u) && j < e && p.ts[j] / p.window_ms == t_i / p.window_ms) bad |= 4u;
+      if (!(bad & 1u) && j < e && p.ts[j] / p.window_ms == t_i / p.window_ms) bad |= 1u << kValRange;
       if (bad) {
         atomicOr(p.err, bad);
-        atomicMin(p.first, (unsigned long long)i);
+        for (int k = 0; k < kValState; ++k)
+          if (bad & (1u << k)) atomicMin(&p.first[k], (unsigned long long)i);
       }
+    }
+  }
+}
+
+// A_m(t) and W_m(t) of Eq. (1) count active and waiting requests, so a
+// stream whose transitions take either below zero at some instant is
+// invalid. They are right-continuous step functions: the value at t counts
+// every row with ts <= t, so only the counts after the last row of an
+// instant are checked (rows of one instant may come in any order). For
+// model m that is the count after its last row with that timestamp.
+//
+// One wave per trace (the trace's rows are already known sorted, with valid
+// models and types), 64 rows per step, one per lane. Rows of the same model
+// are found with ballots over the model's bits; a lane's count is its
+// model's carry plus the signed transitions of the same-model lanes up to
+// it. A row whose next same-model row in the step has a later timestamp is
+// the last of its instant and is checked at once; the model's last row of a
+// step is checked when the model's next row (in a later step) has a later
+// timestamp, or at the end of the trace. Per-model state (carries, the
+// timestamp and row of the last row seen) lives in the wave's LDS slice.
+struct StateParams {
+  const int64_t* ts;
+  const uint8_t* model;
+  const uint8_t* type;
+  const int64_t* off;
+  uint32_t n_traces;
+  int32_t M;
+  unsigned* err;
+  unsigned long long* first;
+};
+
+__global__ __launch_bounds__(256) void validate_state(StateParams p) {
+  __shared__ int s_a[4][TRE_MAX_MODELS], s_w[4][TRE_MAX_MODELS];  // counts after the rows seen
+  __shared__ long long s_t[4][TRE_MAX_MODELS];                     // timestamp of the model's last row, -1 none
+  __shared__ long long s_r[4][TRE_MAX_MODELS];                     // that row
+  const int wv = (int)(threadIdx.x >> 6), lane = (int)(threadIdx.x & 63);
+  const uint32_t t = blockIdx.x * 4u + (uint32_t)wv;
+  if (t >= p.n_traces) return;  // whole wave; the waves share no barrier
+  int* ca = s_a[wv];
+  int* cw = s_w[wv];
+  long long* lt = s_t[wv];
+  long long* lr = s_r[wv];
+  ca[lane] = 0;
+  cw[lane] = 0;
+  lt[lane] = -1;
+  lr[lane] = 0;
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  const int nbits = p.M > 1 ? 32 - __clz(p.M - 1) : 0;
+  const unsigned long long le = (2ull << lane) - 1ull;  // lanes <= this one
+  const int64_t b = p.off[t], e = p.off[t + 1];
+  long long bad = LLONG_MAX;
+  // rows of the next step are loaded before the current one is processed
+  auto load = [&](int64_t i, long long& ts, uint32_t& m, uint32_t& ty) {
+    const bool v = i < e;
+    ts = v ? (long long)p.ts[i] : 0;
+    m = v ? (uint32_t)p.model[i] & 63u : 0u;
+    ty = v ? (uint32_t)p.type[i] : 0xFFu;
+  };
+  long long tsn;
+  uint32_t mn, tyn;
+  load(b + lane, tsn, mn, tyn);
+  for (int64_t r0 = b; r0 < e; r0 += 64) {
+    const int64_t i = r0 + lane;
+    const bool v = i < e;
+    const long long ts = tsn;
+    const uint32_t m = mn, ty = tyn;
+    load(i + 64, tsn, mn, tyn);
+    const int dA = (ty == (TRE_PREFILL | TRE_ADMIT) ? 1 : 0) - (ty == TRE_FINISH ? 1 : 0);
+    const int dW = (ty == TRE_ARRIVE ? 1 : 0) - (ty == (TRE_PREFILL | TRE_ADMIT) ? 1 : 0);
+    unsigned long long same = __ballot(v);
+    for (int k = 0; k < nbits; ++k) {
+      const unsigned long long bk = __ballot((m >> k) & 1u);
+      same &= ((m >> k) & 1u) ? bk : ~bk;
+    }
+    const unsigned long long pa = __ballot(dA > 0), na = __ballot(dA < 0);
+    const unsigned long long pw = __ballot(dW > 0), nw = __ballot(dW < 0);
+    const unsigned long long upto = same & le;
+    const int va = ca[m] + __popcll(pa & upto) - __popcll(na & upto);
+    const int vw = cw[m] + __popcll(pw & upto) - __popcll(nw & upto);
+    const unsigned long long after = same & ~le;
+    const int nl = after ? __ffsll((long long)after) - 1 : lane;
+    const long long tnext = __shfl(ts, nl);
+    // the last row of its instant inside this step
+    if (v && after && tnext != ts && (va < 0 || vw < 0)) bad = bad < i ? bad : i;
+    // the model's first row in this step settles its last row of an earlier step
+    if (v && (upto & ~(1ull << lane)) == 0ull) {
+      const long long tp = lt[m];
+      if (tp >= 0 && tp != ts && (ca[m] < 0 || cw[m] < 0)) bad = bad < lr[m] ? bad : lr[m];
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    if (v && !after) {  // the model's last row in this step
+      ca[m] = va;
+      cw[m] = vw;
+      lt[m] = ts;
+      lr[m] = i;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+  // each model's last row is the last of its instant
+  if (lane < p.M && lt[lane] >= 0 && (ca[lane] < 0 || cw[lane] < 0)) bad = bad < lr[lane] ? bad : lr[lane];
+  if (bad != LLONG_MAX) {
+    atomicOr(p.err, 1u << kValState);
+    atomicMin(p.first, (unsigned long long)bad);
+  }
+}
+
+// A request is admitted once (its first prefill chunk carries the ADMIT
+// bit). With request ids given, pass 1 finds the largest admitted id of
+// each trace; pass 2 sets one bit per admitted id in a per-trace bitmap
+// and records the smallest (trace, id) whose bit was already set.
+struct AdmitParams {
+  const uint32_t* req;
+  const uint8_t* type;
+  const int64_t* off;
+  uint32_t t0, n_traces;        // traces [t0, t0 + n_traces) of this launch
+  uint32_t* maxid;              // pass 1: [all traces] largest admitted id
+  const uint64_t* word_off;     // pass 2: [all traces] first bitmap word of each trace
+  uint64_t word_base;           // word_off of trace t0
+  uint32_t* bits;               // pass 2: bitmaps of this launch's traces
+  unsigned long long* dup;      // pass 2: smallest (trace << 32 | id) admitted twice
+};
+
+template <bool kMark>
+__global__ __launch_bounds__(256) void admit_scan(AdmitParams p) {
+  for (uint32_t tt = blockIdx.y; tt < p.n_traces; tt += gridDim.y) {
+    const uint32_t t = p.t0 + tt;
+    const int64_t b = p.off[t], e = p.off[t + 1];
+    const int64_t c0 = b + (int64_t)blockIdx.x * kValChunk;
+    if (c0 >= e) continue;  // uniform over the block
+    const int64_t c1 = c0 + kValChunk < e ? c0 + kValChunk : e;
+    uint32_t mx = 0;
+    for (int64_t i = c0 + threadIdx.x; i < c1; i += 256) {
+      if (p.type[i] != (TRE_PREFILL | TRE_ADMIT)) continue;
+      const uint32_t id = p.req[i];
+      if constexpr (!kMark) {
+        mx = id > mx ? id : mx;
+      } else {
+        if ((uint64_t)(id >> 5) >= p.word_off[t + 1] - p.word_off[t]) continue;  // above pass 1's largest id
+        const uint32_t bit = 1u << (id & 31u);
+        const uint32_t old = atomicOr(&p.bits[p.word_off[t] - p.word_base + (id >> 5)], bit);
+        if (old & bit) atomicMin(p.dup, ((unsigned long long)t << 32) | id);
+      }
+    }
+    if constexpr (!kMark) {
+      for (int d = 32; d >= 1; d >>= 1) {
+        const uint32_t o = (uint32_t)__shfl_xor((int)mx, d);
+        mx = o > mx ? o : mx;
+      }
+      if ((threadIdx.x & 63) == 0 && mx) atomicMax(&p.maxid[t], mx);
     }
   }
 }
@@ -1118,6 +1278,133 @@ static size_t stream_lds(const tre_events* ev, bool stage = false) {
   return stage ? base + 2 * C * M * 8 + 2 * M * 8 + ((2 * M + 7) & ~(size_t)7) : base;
 }
 
+// The load-time checks (synchronous): order, schema and per-window range
+// of every row; then, on valid rows, counts never negative; then, with
+// request ids, no id admitted twice. The error reported is the kind of the
+// lowest failing row among the first three kinds (order before schema
+// before range on one row), else a negative count (its lowest row), else a
+// duplicate admission (the smallest trace, then id).
+static int validate_events(const tre_events* ev, hipStream_t st) {
+  const uint32_t n_traces = ev->n_traces;
+  const tre_trace_cfg& c = ev->cfg;
+  int64_t maxlen = 0;
+  for (uint32_t i = 0; i < n_traces; ++i) maxlen = std::max<int64_t>(maxlen, ev->h_off[i + 1] - ev->h_off[i]);
+  if (maxlen == 0) return TRE_OK;
+  // err (8 bytes), first rows [kValKinds], duplicate key
+  struct Slots {
+    unsigned err, pad;
+    unsigned long long first[kValKinds];
+    unsigned long long dup;
+  } h;
+  void* scratch = nullptr;
+  if (hipMalloc(&scratch, sizeof(Slots)) != hipSuccess) return fail(TRE_EHIP, "hipMalloc failed");
+  Slots* d = (Slots*)scratch;
+  memset(&h, 0xFF, sizeof h);
+  h.err = 0;
+  h.pad = 0;
+  const dim3 grid((unsigned)((maxlen + kValChunk - 1) / kValChunk), std::min<uint32_t>(n_traces, 65535u));
+  auto readback = [&]() {
+    return hipMemcpyAsync(&h, d, sizeof h, hipMemcpyDeviceToHost, st) == hipSuccess &&
+           hipStreamSynchronize(st) == hipSuccess;
+  };
+  bool ok = hipMemcpyAsync(d, &h, sizeof h, hipMemcpyHostToDevice, st) == hipSuccess;
+  if (ok) {
+    ValParams vp{ev->ts, ev->model, ev->type, ev->d_off, n_traces, c.duration_ms, c.window_ms, c.n_models,
+                 max_events_per_window(c.window_ms), &d->err, d->first};
+    LaunchTimer lt("validate", st);
+    hipLaunchKernelGGL(validate, grid, dim3(256), 0, st, vp);
+    ok = hipGetLastError() == hipSuccess;
+    lt.done();
+  }
+  ok = ok && readback();
+  int rc = TRE_OK;
+  if (ok && h.err) {
+    int kind = -1;
+    for (int k = 0; k < kValState; ++k)
+      if ((h.err >> k & 1u) && (kind < 0 || h.first[k] < h.first[kind])) kind = k;
+    const unsigned long long row = h.first[kind];
+    if (kind == kValOrder) rc = fail(TRE_EORDER, "row %llu: timestamp unsorted or outside [0, duration)", row);
+    else if (kind == kValSchema) rc = fail(TRE_ESCHEMA, "row %llu: model index or type byte invalid", row);
+    else
+      rc = fail(TRE_ERANGE, "row %llu: more than %lld events in one window", row,
+                (long long)max_events_per_window(c.window_ms));
+  }
+  if (ok && rc == TRE_OK) {
+    StateParams sp{ev->ts, ev->model, ev->type, ev->d_off, n_traces, c.n_models, &d->err, &d->first[kValState]};
+    hipLaunchKernelGGL(validate_state, dim3((n_traces + 3) / 4), dim3(256), 0, st, sp);
+    ok = hipGetLastError() == hipSuccess && readback();
+    if (ok && (h.err >> kValState & 1u))
+      rc = fail(TRE_ESTATE, "row %llu: an active or waiting count below zero after this instant",
+                h.first[kValState]);
+  }
+  if (ok && rc == TRE_OK && ev->req) {
+    // pass 1: largest admitted id per trace; then bitmaps of at most 2^26
+    // words (256 MiB) at a time, or one trace's if larger
+    uint32_t* d_max = nullptr;
+    uint64_t* d_woff = nullptr;
+    uint32_t* d_bits = nullptr;
+    std::vector<uint32_t> hmax(n_traces);
+    std::vector<uint64_t> woff(n_traces + 1);
+    ok = hipMalloc(&d_max, sizeof(uint32_t) * n_traces) == hipSuccess &&
+         hipMemsetAsync(d_max, 0, sizeof(uint32_t) * n_traces, st) == hipSuccess;
+    AdmitParams ap{};
+    ap.req = ev->req;
+    ap.type = ev->type;
+    ap.off = ev->d_off;
+    ap.maxid = d_max;
+    ap.dup = &d->dup;
+    for (uint32_t t0 = 0; ok && t0 < n_traces; t0 += 65535u) {
+      ap.t0 = t0;
+      ap.n_traces = std::min<uint32_t>(n_traces - t0, 65535u);
+      hipLaunchKernelGGL(admit_scan<false>, dim3(grid.x, ap.n_traces), dim3(256), 0, st, ap);
+      ok = hipGetLastError() == hipSuccess;
+    }
+    ok = ok && hipMemcpyAsync(hmax.data(), d_max, sizeof(uint32_t) * n_traces, hipMemcpyDeviceToHost, st) ==
+                   hipSuccess &&
+         hipStreamSynchronize(st) == hipSuccess;
+    woff[0] = 0;
+    uint64_t most = 0;
+    for (uint32_t t = 0; t < n_traces; ++t) {
+      const uint64_t w = (uint64_t)(hmax[t] >> 5) + 1u;
+      woff[t + 1] = woff[t] + w;
+      most = std::max(most, w);
+    }
+    const uint64_t cap = std::max<uint64_t>(most, std::min<uint64_t>(woff[n_traces], 1ull << 26));
+    ok = ok && hipMalloc(&d_woff, sizeof(uint64_t) * (n_traces + 1)) == hipSuccess &&
+         hipMalloc(&d_bits, sizeof(uint32_t) * cap) == hipSuccess &&
+         hipMemcpyAsync(d_woff, woff.data(), sizeof(uint64_t) * (n_traces + 1), hipMemcpyHostToDevice, st) ==
+             hipSuccess;
+    ap.word_off = d_woff;
+    ap.bits = d_bits;
+    for (uint32_t t0 = 0; ok && t0 < n_traces;) {
+      uint32_t t1 = t0 + 1;
+      while (t1 < n_traces && t1 - t0 < 65535u && woff[t1 + 1] - woff[t0] <= cap) ++t1;
+      int64_t len = 0;
+      for (uint32_t t = t0; t < t1; ++t) len = std::max<int64_t>(len, ev->h_off[t + 1] - ev->h_off[t]);
+      ap.t0 = t0;
+      ap.n_traces = t1 - t0;
+      ap.word_base = woff[t0];
+      ok = hipMemsetAsync(d_bits, 0, sizeof(uint32_t) * (woff[t1] - woff[t0]), st) == hipSuccess;
+      if (ok && len > 0) {
+        hipLaunchKernelGGL(admit_scan<true>, dim3((unsigned)((len + kValChunk - 1) / kValChunk), t1 - t0),
+                           dim3(256), 0, st, ap);
+        ok = hipGetLastError() == hipSuccess;
+      }
+      t0 = t1;
+    }
+    ok = ok && readback();
+    if (d_max) (void)hipFree(d_max);
+    if (d_woff) (void)hipFree(d_woff);
+    if (d_bits) (void)hipFree(d_bits);
+    if (ok && h.dup != ~0ull)
+      rc = fail(TRE_ESTATE, "trace %u: request id %u admitted more than once", (unsigned)(h.dup >> 32),
+                (unsigned)h.dup);
+  }
+  (void)hipFree(scratch);
+  if (!ok) return fail(TRE_EHIP, "validation launch failed");
+  return rc;
+}
+
 extern "C" int tre_load_events(const int64_t* ts, const uint8_t* model, const uint32_t* req,
                                const uint8_t* type, const uint16_t* tokens,
                                const int64_t* trace_off, uint32_t n_traces,
@@ -1196,36 +1483,7 @@ extern "C" int tre_load_events(const int64_t* ts, const uint8_t* model, const ui
     return cleanup(fail(TRE_EHIP, "copy of handle tables failed"));
 
   if (flags & TRE_VALIDATE) {
-    int64_t maxlen = 0;
-    for (uint32_t i = 0; i < n_traces; ++i)
-      maxlen = std::max<int64_t>(maxlen, trace_off[i + 1] - trace_off[i]);
-    void* scratch = nullptr;
-    if (hipMalloc(&scratch, 16) != hipSuccess) return cleanup(fail(TRE_EHIP, "hipMalloc failed"));
-    unsigned* d_err = (unsigned*)scratch;
-    unsigned long long* d_first = (unsigned long long*)((char*)scratch + 8);
-    unsigned h_init[4] = {0u, 0u, 0xFFFFFFFFu, 0xFFFFFFFFu};
-    unsigned long long h_first = ~0ull;
-    unsigned h_err = 0;
-    bool ok = hipMemcpyAsync(scratch, h_init, 16, hipMemcpyHostToDevice, st) == hipSuccess;
-    if (ok && maxlen > 0) {
-      ValParams vp{ts, model, type, ev->d_off, n_traces, c.duration_ms, c.window_ms, c.n_models,
-                   max_events_per_window(c.window_ms), d_err, d_first};
-      dim3 grid((unsigned)((maxlen + kValChunk - 1) / kValChunk), std::min<uint32_t>(n_traces, 65535u));
-      LaunchTimer lt("validate", st);
-      hipLaunchKernelGGL(validate, grid, dim3(256), 0, st, vp);
-      ok = hipGetLastError() == hipSuccess;
-      lt.done();
-    }
-    ok = ok && hipMemcpyAsync(&h_err, d_err, 4, hipMemcpyDeviceToHost, st) == hipSuccess &&
-         hipMemcpyAsync(&h_first, d_first, 8, hipMemcpyDeviceToHost, st) == hipSuccess &&
-         hipStreamSynchronize(st) == hipSuccess;
-    (void)hipFree(scratch);
-    if (!ok) return cleanup(fail(TRE_EHIP, "validation launch failed"));
-    if (h_err & 1u) rc = fail(TRE_EORDER, "row %llu: timestamp unsorted or outside [0, duration)", h_first);
-    else if (h_err & 2u) rc = fail(TRE_ESCHEMA, "row %llu: model index or type byte invalid", h_first);
-    else if (h_err & 4u)
-      rc = fail(TRE_ERANGE, "row %llu: more than %lld events in one window", h_first,
-                (long long)max_events_per_window(c.window_ms));
+    rc = validate_events(ev, st);
     if (rc != TRE_OK) return cleanup(rc);
   }
   *out = ev;

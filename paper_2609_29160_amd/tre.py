@@ -17,7 +17,7 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libtre.so")
 
-TRE_OK, TRE_EINVAL, TRE_EORDER, TRE_ESCHEMA, TRE_ERANGE, TRE_ENOMEM, TRE_EHIP = range(7)
+TRE_OK, TRE_EINVAL, TRE_EORDER, TRE_ESCHEMA, TRE_ERANGE, TRE_ENOMEM, TRE_EHIP, TRE_ESTATE = range(8)
 TRE_VALIDATE = 1
 TRE_FLAG_IDLE, TRE_FLAG_INIT = 1, 2
 TRE_PATH_RESCUE, TRE_PATH_REBALANCE, TRE_DONOR_POOL = 1, 2, 0xFF

@@ -528,6 +528,58 @@ def pin_bruteforce(o):
             assert mv == [(0, path, best[1], d)], (Zs, r_init, extra, mv, best)
 
 
+# ------------------------------------------------- counts never negative
+def pin_state(o):
+    """A_m(t) and W_m(t) of Eq. (1) are numbers of active and of waiting
+    requests (Section "Design Rationale and Definition"), so a stream that
+    takes either below zero at some instant is rejected. They are step
+    functions: the rows that share one instant may come in any order, only
+    the counts after the last of them are values of the functions. A
+    request is admitted once (the ADMIT bit moves it from waiting to
+    active), which the request ids make checkable."""
+    ARR, PF, ADM, DEC, FIN = 0, 1, 0x81, 2, 3
+
+    def st(rows, M=2):
+        return o.trace_status(events_from_rows(rows), 100, 1000, M)
+
+    life = [[10, 0, 1, ARR, 5], [20, 0, 1, ADM, 5], [30, 0, 1, DEC, 3], [40, 0, 1, FIN, 0]]
+    assert st(life) == 0
+    # FINISH with nothing active: A_0 = -1 on [15, 20)
+    assert st([[10, 0, 1, ARR, 5], [15, 0, 1, FIN, 0], [20, 0, 1, ADM, 5]]) == -5
+    # ADMIT with nothing waiting: W_0 = -1 while A_0 = 1
+    assert st([[20, 0, 1, ADM, 5], [30, 0, 1, FIN, 0]]) == -5
+    # the counts are per model: model 1 admits while only model 0 waits
+    assert st([[10, 0, 1, ARR, 5], [20, 1, 2, ADM, 5]]) == -5
+    # model 0 negative at an instant whose last row is model 1's
+    assert st([[10, 0, 1, ADM, 5], [10, 1, 2, ARR, 5], [50, 1, 2, ADM, 5]]) == -5
+    # negative at the last instant of the trace
+    assert st([[10, 0, 1, ARR, 5], [20, 0, 1, ADM, 5], [999, 0, 1, FIN, 0], [999, 0, 1, FIN, 0]]) == -5
+    # order is checked first: an unsorted stream is an order error
+    assert st([[20, 0, 1, ADM, 5], [10, 0, 1, ARR, 5]]) == -2
+    # rows of one instant out of lifecycle order (ADMIT listed before its
+    # ARRIVE, FINISH before the ADMIT of the same instant): accepted, with
+    # the tallies of the lifecycle order
+    odd = [[10, 0, 1, ADM, 5], [10, 0, 1, ARR, 5], [50, 1, 2, ARR, 4], [60, 1, 2, FIN, 0], [60, 1, 2, ADM, 4],
+           [70, 0, 1, FIN, 0]]
+    canon = [[10, 0, 1, ARR, 5], [10, 0, 1, ADM, 5], [50, 1, 2, ARR, 4], [60, 1, 2, ADM, 4], [60, 1, 2, FIN, 0],
+             [70, 0, 1, FIN, 0]]
+    assert st(odd) == 0
+    a, _ = _single(o, odd, M=2, window_ms=100, duration_ms=1000)
+    b, _ = _single(o, canon, M=2, window_ms=100, duration_ms=1000)
+    for k in ("P", "D", "A_int", "W_int", "flags"):
+        assert np.array_equal(a[k], b[k]), k
+    assert a["A_int"][0, 0] == 60 and a["W_int"][0, 1] == 10
+    # request ids: an id admitted twice; a later non-admitting PREFILL is fine
+    ev = events_from_rows([[10, 0, 7, ARR, 5], [11, 0, 8, ARR, 5], [20, 0, 7, ADM, 5], [21, 0, 7, ADM, 5],
+                           [30, 0, 8, PF, 5]])
+    assert o.check_admits(ev) == (-6, 7)
+    ev = events_from_rows([[10, 0, 7, ARR, 5], [20, 0, 7, ADM, 5], [25, 0, 7, PF, 5], [30, 1, 9, ADM, 5],
+                           [31, 1, 4, ADM, 5], [32, 1, 9, ADM, 5], [33, 0, 4, ADM, 5]])
+    assert o.check_admits(ev) == (-6, 4)
+    assert o.check_admits(events_from_rows(life)) == (0, None)
+    assert o.check_admits(events_from_rows([[5, 0, 3, ADM, 1], [6, 0, 4, ADM, 1], [7, 0, 3, PF, 1]])) == (0, None)
+
+
 ALL_PINS = [pin_hand_traces, pin_paper_pair, pin_floor, pin_closed_forms, pin_normalisation,
             pin_cadence, pin_control_rules, pin_integrals_and_tallies, pin_monotone,
-            pin_invariants, pin_bruteforce]
+            pin_invariants, pin_bruteforce, pin_state]

@@ -333,6 +333,165 @@ def test_validation_errors(lib):
     ev.close()
 
 
+def _perturbed(rng, tr, how):
+    """A copy of a host trace with one change: 'shuffle' permutes the rows
+    of every instant (a valid stream stays valid), 'drop_arrive' /
+    'drop_admit' delete one row of that kind, 'dup_admit' repeats one
+    admitting row (the same request id) at a later row of its instant or
+    after it."""
+    t = {k: v.copy() for k, v in tr.items()}
+    n = len(t["ts"])
+    if how == "shuffle":
+        order = np.lexsort((rng.random(n), t["ts"]))
+        return {k: v[order] for k, v in t.items()}
+    kind = {"drop_arrive": 0, "drop_admit": 0x81, "dup_admit": 0x81}[how]
+    rows = np.flatnonzero(t["type"] == kind)
+    r = int(rng.choice(rows))
+    if how.startswith("drop"):
+        keep = np.ones(n, bool)
+        keep[r] = False
+        return {k: v[keep] for k, v in t.items()}
+    j = int(rng.integers(r + 1, n + 1))  # insert a copy of row r before row j (ts kept sorted)
+    row = {k: v[r] for k, v in t.items()}
+    row["ts"] = max(int(t["ts"][r]), int(t["ts"][j - 1]))
+    return {k: np.insert(v, j, row[k]) for k, v in t.items()}
+
+
+def test_state_validation(lib):
+    """TRE_ESTATE at load against the oracle: the active / waiting counts of
+    Eq. (1) never below zero at any instant, and no request id admitted
+    twice. Traces with many rows per millisecond (so instants span the
+    kernel's 64-row steps), perturbed at random: rows of one instant
+    shuffled (accepted, same tallies), an ARRIVE or an ADMIT dropped, an
+    ADMIT repeated. The GPU must reject exactly what the oracle rejects."""
+    tre, device, torch = lib
+    o = O.get()
+    M, win, nW = 5, 10, 50
+    cfg = _cfg(M, win, nW, fast_w=2, slow_w=4)
+    rng = np.random.default_rng(77)
+    seen = {"ok": 0, "state": 0}
+    for case in range(48):
+        how = ("shuffle", "drop_arrive", "drop_admit", "dup_admit")[case % 4]
+        # every request admitted and finished in half the cases, so the
+        # counts return to zero and a dropped row takes one below it
+        full = (case // 4) % 2 == 1
+        base = E.trace_random(500 + case, M, win * nW, 400, max_span_ms=300,
+                              **({"admit_p": 1.0, "finish_p": 1.0} if full else {}))
+        tr = _perturbed(rng, base, how)
+        assert (np.diff(tr["ts"]) >= 0).all()
+        exp_state = o.trace_status(tr, win, win * nW, M)
+        assert exp_state in (0, -5), exp_state
+        exp_dup = o.check_admits(tr)[0]
+        cols, off = _columns_from_host(torch, [tr])
+        say(f"state case {case} ({how}): {len(tr['ts'])} rows, oracle {exp_state} / {exp_dup}")
+        if exp_state or exp_dup:
+            with pytest.raises(tre.TreError) as e:
+                tre.tre_load_events(cols["ts"], cols["model"], cols["req"], cols["type"], cols["tokens"], off, cfg)
+            assert e.value.code == tre.TRE_ESTATE, (case, how, str(e.value))
+            seen["state"] += 1
+        else:
+            ev = tre.tre_load_events(cols["ts"], cols["model"], cols["req"], cols["type"], cols["tokens"], off, cfg)
+            if how == "shuffle":
+                prof_cols = _prof(M, 1, case)
+                prof = tre.pack(prof_cols, tre.PROFILE_DTYPE)
+                g = _eval_all(tre, ev, prof)
+
+                class W:
+                    window_ms = win
+                    duration_ms = win * nW
+                ref = PT.oracle_tss(tr, W, PT.trace_profile(prof_cols, 0, M))
+                PT.compare_tss({k: v[0] for k, v in g.items()}, ref, f"shuffled instants, case {case}")
+            ev.close()
+            seen["ok"] += 1
+        # the same columns without request ids: only the counts are checked
+        if exp_dup and not exp_state:
+            ev = tre.tre_load_events(cols["ts"], cols["model"], None, cols["type"], cols["tokens"], off, cfg)
+            ev.close()
+    say("state validation:", seen)
+    assert seen["ok"] >= 24 and seen["state"] >= 18
+
+
+def test_state_validation_hand_cases(lib):
+    """Hand-built streams at chunk-boundary positions: a FINISH with nothing
+    active, an ADMIT with nothing waiting and a second ADMIT of one id, each
+    placed so that the failing instant is inside a 64-row step, at its last
+    row, across two steps, or at the last row of the trace; and an instant
+    out of lifecycle order straddling two steps (accepted)."""
+    tre, device, torch = lib
+    o = O.get()
+    M, win, nW = 3, 1000, 4
+    cfg = _cfg(M, win, nW, fast_w=1, slow_w=2)
+    ARR, ADM, DEC, FIN = 0, 0x81, 2, 3
+
+    def filler(n, t0=0):  # n complete requests of model 2, one row per ms from t0
+        rows = []
+        for r in range(n // 4):
+            t = t0 + 4 * r
+            rows += [(t, 2, 1000 + r, ARR, 3), (t + 1, 2, 1000 + r, ADM, 3), (t + 2, 2, 1000 + r, DEC, 2),
+                     (t + 3, 2, 1000 + r, FIN, 0)]
+        return rows
+
+    def run(rows, expect_state):
+        tr = E._pack(rows)
+        assert o.trace_status(tr, win, win * nW, M) == (-5 if expect_state == "count" else 0)
+        assert o.check_admits(tr)[0] == (-6 if expect_state == "dup" else 0)
+        cols, off = _columns_from_host(torch, [tr])
+        if expect_state:
+            with pytest.raises(tre.TreError) as e:
+                tre.tre_load_events(cols["ts"], cols["model"], cols["req"], cols["type"], cols["tokens"], off, cfg)
+            assert e.value.code == tre.TRE_ESTATE, str(e.value)
+        else:
+            tre.tre_load_events(cols["ts"], cols["model"], cols["req"], cols["type"], cols["tokens"], off, cfg).close()
+
+    for lead in (0, 60, 62, 63, 64, 124, 127):
+        f = filler(lead)
+        t = 4 * (lead // 4) + 10
+        # FINISH with nothing active (model 0), then its ADMIT at a later instant
+        run(f + [(t, 0, 1, ARR, 5), (t + 1, 0, 1, FIN, 0), (t + 2, 0, 1, ADM, 5)], "count")
+        # ADMIT with nothing waiting (model 1)
+        run(f + [(t, 1, 2, ADM, 5), (t + 1, 1, 2, FIN, 0)], "count")
+        # the same rows at one instant, ADMIT first: accepted
+        run(f + [(t, 1, 2, ADM, 5), (t, 1, 2, ARR, 5), (t + 1, 1, 2, FIN, 0)], None)
+        # an instant of 70 rows, out of lifecycle order, crossing a step
+        burst = [(t, 0, 10 + k, ADM, 1) for k in range(35)] + [(t, 0, 10 + k, ARR, 1) for k in range(35)]
+        run(f + burst, None)
+        # the same with one ARRIVE short: negative after the instant
+        run(f + burst[:-1], "count")
+        # a second ADMIT of one id (another request keeps the waiting count up)
+        run(f + [(t, 0, 5, ARR, 5), (t, 0, 6, ARR, 5), (t + 1, 0, 5, ADM, 5), (t + 2, 0, 5, ADM, 5)], "dup")
+        # negative at the very last row of the trace
+        run(f + [(t, 1, 3, ARR, 5), (t + 1, 1, 3, ADM, 5), (3999, 1, 3, FIN, 0), (3999, 1, 3, FIN, 0)], "count")
+
+
+def test_validation_reports_lowest_row_kind(lib):
+    """The message names the kind of the lowest failing row: a schema error
+    at row 5 with an unsorted timestamp at row 50 is TRE_ESCHEMA at row 5,
+    and the other way round TRE_EORDER."""
+    tre, device, torch = lib
+    M, win, nW = 4, 100, 100
+    cfg = _cfg(M, win, nW)
+    base = E.trace_random(40, M, win * nW, 300)
+
+    def load(tr):
+        cols, off = _columns_from_host(torch, [tr])
+        return tre.tre_load_events(cols["ts"], cols["model"], cols["req"], cols["type"], cols["tokens"], off, cfg)
+
+    bad = {k: v.copy() for k, v in base.items()}
+    bad["model"][5] = M
+    bad["ts"][50], bad["ts"][51] = bad["ts"][51] + 1, bad["ts"][50]
+    with pytest.raises(tre.TreError) as e:
+        load(bad)
+    assert e.value.code == tre.TRE_ESCHEMA and "row 5:" in str(e.value), str(e.value)
+    assert O.get().trace_status(bad, win, win * nW, M) == -3
+    bad = {k: v.copy() for k, v in base.items()}
+    bad["model"][50] = M
+    bad["ts"][5], bad["ts"][6] = bad["ts"][6] + 1, bad["ts"][5]
+    with pytest.raises(tre.TreError) as e:
+        load(bad)
+    assert e.value.code == tre.TRE_EORDER and "row 6:" in str(e.value), str(e.value)
+    assert O.get().trace_status(bad, win, win * nW, M) == -2
+
+
 def test_move_log_capacity(lib):
     """A short move log keeps the first entries; n_moves still counts all."""
     tre, device, torch = lib

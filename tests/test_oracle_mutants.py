@@ -80,6 +80,15 @@ MUTANTS = {
     "r_windows_after_tick": ("for (int m = 0; m < M; ++m) r_windows[m] += R[m];   /* replicas serving window w */",
                              "for (int m = 0; m < M; ++m) if (w > 0) r_windows[m] += R[m];"),
     "window_index_shift": ("moves[nm].window = (uint32_t)w;", "moves[nm].window = (uint32_t)(w + 1);"),
+    # counts never negative (readings of Eq. (1)'s definition)
+    "state_unchecked": ("if (A[k] < 0 || W[k] < 0) return -5;", ";"),
+    "state_active_only": ("if (A[k] < 0 || W[k] < 0)", "if (A[k] < 0)"),
+    "state_after_every_row": ("if (i == n_events - 1 || ts[i + 1] != t)", "if (1)"),
+    "state_at_end_only": ("if (i == n_events - 1 || ts[i + 1] != t)", "if (i == n_events - 1)"),
+    "state_own_model_only": ("for (int k = 0; k < M; ++k)\n        if (A[k] < 0", "for (int k = m; k <= m; ++k)\n        if (A[k] < 0"),
+    "admits_unchecked": ("if (ids_scratch[i] == ids_scratch[i - 1]) {", "if (0) {"),
+    "admits_any_prefill": ("if (type[i] == (OR_PREFILL | OR_ADMIT)) ids_scratch[n++] = req[i];",
+                           "if ((type[i] & 3) == OR_PREFILL) ids_scratch[n++] = req[i];"),
     "no_move_limit": ("for (uint32_t k = 0; k < sc->max_moves; ++k) {", "for (uint32_t k = 0; k < sc->max_moves + 1; ++k) {"),
 }
 
