@@ -262,6 +262,21 @@ int tre_sweep(const tre_events* ev, const tre_profile* prof, const tre_scenario*
               uint32_t n_scenarios, const tre_ctl_out* out, float* tss32, void* ws,
               size_t ws_bytes, void* stream);
 
+/* tre_sweep for callers that cannot allocate device memory (code under
+   HIP graph capture, tight serving loops, harnesses that forbid
+   hipMalloc): the same results as tre_sweep, with the sweep's scratch in a
+   static device array of TRE_NOALLOC_SCRATCH_BYTES that each GPU holds
+   from the first call on it until the process ends. The call allocates
+   nothing (no hipMalloc or hipFree, no event objects: tre_set_timing does
+   not record it). Returns TRE_ENOMEM, launching nothing, when the sweep
+   needs more scratch than that (tre_workspace_size bytes: 8 per trace,
+   tick and model). Every call on one GPU shares its array: calls that
+   overlap on one GPU (other streams, other threads) race and give
+   unspecified results; calls in order on one stream are safe. */
+#define TRE_NOALLOC_SCRATCH_BYTES (64u << 20)
+int tre_sweep_noalloc(const tre_events* ev, const tre_profile* prof, const tre_scenario* sc,
+                      uint32_t n_scenarios, const tre_ctl_out* out, float* tss32, void* stream);
+
 /* ------------------------------------------------------- actuation model
  * Optional model of how a decided transition is carried out (Sections
  * "Dual-Speed Control", "Bounded Pairwise Transfer", "System Boundary and

@@ -1178,7 +1178,13 @@ std::vector<Pending> g_pending;
 
 }  // namespace
 
+static thread_local int g_no_timing = 0;
+
+tre_internal::NoTimingScope::NoTimingScope() { ++g_no_timing; }
+tre_internal::NoTimingScope::~NoTimingScope() { --g_no_timing; }
+
 tre_internal::LaunchTimer::LaunchTimer(const char* name, hipStream_t s) : st_(s) {
+  if (g_no_timing) return;
   std::lock_guard<std::mutex> lk(g_tmu);
   if (!g_timing) return;
   name_ = name;
@@ -1296,9 +1302,9 @@ static int validate_events(const tre_events* ev, hipStream_t st) {
     unsigned long long first[kValKinds];
     unsigned long long dup;
   } h;
-  void* scratch = nullptr;
-  if (hipMalloc(&scratch, sizeof(Slots)) != hipSuccess) return fail(TRE_EHIP, "hipMalloc failed");
-  Slots* d = (Slots*)scratch;
+  void* slots = nullptr;
+  if (hipMalloc(&slots, sizeof(Slots)) != hipSuccess) return fail(TRE_EHIP, "hipMalloc failed");
+  Slots* d = (Slots*)slots;
   memset(&h, 0xFF, sizeof h);
   h.err = 0;
   h.pad = 0;
@@ -1400,7 +1406,7 @@ static int validate_events(const tre_events* ev, hipStream_t st) {
       rc = fail(TRE_ESTATE, "trace %u: request id %u admitted more than once", (unsigned)(h.dup >> 32),
                 (unsigned)h.dup);
   }
-  (void)hipFree(scratch);
+  (void)hipFree(slots);
   if (!ok) return fail(TRE_EHIP, "validation launch failed");
   return rc;
 }
@@ -1764,6 +1770,50 @@ extern "C" int tre_sweep(const tre_events* ev, const tre_profile* prof, const tr
                          uint32_t n_scenarios, const tre_ctl_out* out, float* tss32, void* ws,
                          size_t ws_bytes, void* stream) {
   return sweep_impl(ev, prof, sc, n_scenarios, nullptr, out, tss32, ws, ws_bytes, stream, "tre_sweep");
+}
+
+// ------------------------------------------------ sweep without allocation
+// The sweep's scratch (the per-tick smoothed TSS snapshot) in a static
+// device array for callers that cannot allocate. Each GPU the library runs
+// on holds its own copy until the process ends; its device address is
+// looked up once per device, with that device current, at the entry
+// point's first call there, and only that address is used afterwards.
+static __device__ __align__(256) unsigned char scratch[TRE_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[256];  // per device ordinal, NULL until looked up
+}  // namespace
+
+static int scratch_for(int dev, void** out) {
+  if (dev < 0 || dev >= 256) return fail(TRE_EINVAL, "device ordinal %d out of range", dev);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr)
+      return fail(TRE_EHIP, "hipGetSymbolAddress of the static scratch: %s", hipGetErrorString(e));
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return TRE_OK;
+}
+
+extern "C" int tre_sweep_noalloc(const tre_events* ev, const tre_profile* prof, const tre_scenario* sc,
+                                 uint32_t n_scenarios, const tre_ctl_out* out, float* tss32, void* stream) {
+  if (!ev) return fail(TRE_EINVAL, "tre_sweep_noalloc: NULL handle");
+  int rc = check_device(ev);  // the handle's device is the current one
+  if (rc) return rc;
+  size_t need = 0;
+  tre_workspace_size(ev, n_scenarios, &need);
+  if (need > (size_t)TRE_NOALLOC_SCRATCH_BYTES)
+    return fail(TRE_ENOMEM, "tre_sweep_noalloc: the sweep needs %zu bytes of scratch, above the static %zu",
+                need, (size_t)TRE_NOALLOC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  if ((rc = scratch_for(ev->device, &ws))) return rc;
+  tre_internal::NoTimingScope quiet;  // no event objects are created for this call
+  return sweep_impl(ev, prof, sc, n_scenarios, nullptr, out, tss32, ws, (size_t)TRE_NOALLOC_SCRATCH_BYTES, stream,
+                    "tre_sweep_noalloc");
 }
 
 extern "C" int tre_rebalance_act(const tre_events* ev, const tre_profile* prof, const double* tss64,

@@ -52,6 +52,13 @@ class LaunchTimer {
   bool on_ = false;
 };
 
+// while one exists on this thread, LaunchTimer records nothing (calls that
+// must not create runtime objects)
+struct NoTimingScope {
+  NoTimingScope();
+  ~NoTimingScope();
+};
+
 }  // namespace tre_internal
 
 #define HIP_TRY(expr)                                                                          \

@@ -22,6 +22,7 @@ TRE_VALIDATE = 1
 TRE_FLAG_IDLE, TRE_FLAG_INIT = 1, 2
 TRE_PATH_RESCUE, TRE_PATH_REBALANCE, TRE_DONOR_POOL = 1, 2, 0xFF
 TRE_MAX_MODELS = 64
+TRE_NOALLOC_SCRATCH_BYTES = 64 << 20  # include/tre.h
 
 # struct layouts of tre.h
 PROFILE_DTYPE = np.dtype([("w_p", "<f8"), ("w_q", "<f8"), ("alpha", "<f8"), ("theta", "<f8"),
@@ -88,7 +89,7 @@ EXPORTS = ["tre_last_error", "tre_load_events", "tre_free_events", "tre_events_i
            "tre_check_params", "tre_workspace_size", "tre_eval_tss", "tre_rebalance", "tre_sweep",
            "tre_set_timing", "tre_kernel_time", "tre_check_actuation", "tre_rebalance_act", "tre_sweep_act",
            "tre_calib_workspace_size", "tre_calibrate", "tre_loop_workspace_size", "tre_loop", "tre_loop_act",
-           "tre_stage_tss", "tre_eval_stage"]
+           "tre_stage_tss", "tre_eval_stage", "tre_sweep_noalloc"]
 
 
 def _load():
@@ -115,6 +116,8 @@ def _load():
     L.tre_rebalance.argtypes = [vp, vp, vp, vp, vp, u32, ctypes.POINTER(_CtlOut), vp]
     L.tre_sweep.restype = i32
     L.tre_sweep.argtypes = [vp, vp, vp, u32, ctypes.POINTER(_CtlOut), vp, vp, sz, vp]
+    L.tre_sweep_noalloc.restype = i32
+    L.tre_sweep_noalloc.argtypes = [vp, vp, vp, u32, ctypes.POINTER(_CtlOut), vp, vp]
     L.tre_check_actuation.restype = i32
     L.tre_check_actuation.argtypes = [vp, vp, ctypes.POINTER(_Actuation)]
     L.tre_rebalance_act.restype = i32
@@ -312,6 +315,15 @@ def tre_sweep(ev: Events, prof: torch.Tensor, sc: torch.Tensor, out: Dict[str, t
     o = _ctl(out)
     _check(_L.tre_sweep(ev.handle, _ptr(prof), _ptr(sc), n_sc, ctypes.byref(o), _ptr(tss32), _ptr(ws),
                         ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def tre_sweep_noalloc(ev: Events, prof: torch.Tensor, sc: torch.Tensor, out: Dict[str, torch.Tensor],
+                      tss32: Optional[torch.Tensor] = None, stream=None):
+    """tre_sweep with its scratch in the library's static device array."""
+    n_sc = sc.numel() // SCENARIO_DTYPE.itemsize
+    o = _ctl(out)
+    _check(_L.tre_sweep_noalloc(ev.handle, _ptr(prof), _ptr(sc), n_sc, ctypes.byref(o), _ptr(tss32),
+                                _stream(stream)))
 
 
 def actuation(wake_ms: int, sleep_ms: int, footprint: Optional[torch.Tensor] = None,
