@@ -12,7 +12,8 @@
 //               rows. Every thread loads (per-trace buffer resources, the
 //               next tile in flight while the current one is tallied) and
 //               tallies its rows into an LDS ring of (window, model) cells
-//               with three packed 64-bit LDS atomics per row; completed
+//               with one packed 64-bit LDS atomic per row (two for an
+//               ADMIT row); completed
 //               windows are then evaluated one cell per thread (carry scan,
 //               in-window integrals, Eq. (1) in fp64) and one wave per step
 //               runs the smoothing chain over the previous chunk.
@@ -65,7 +66,7 @@ extern "C" const char* tre_last_error(void) { return g_err.c_str(); }
 constexpr int kStreamWaves = 4;            // tss_stream workgroup (waves) with many traces
 constexpr int kEvalThreads = 256;          // threads that evaluate a step's cells (one cell each)
 constexpr int kStreamEPT = 4;              // rows per lane per tile
-constexpr int kRingBytes = 13 * 1024;      // LDS budget of the tally ring
+constexpr int kRingBytes = 17 * 1024;      // LDS budget of the tally ring
 constexpr uint32_t kNoDefer = 0xFFFFFFFFu;
 
 typedef long long v2i64 __attribute__((ext_vector_type(2)));
@@ -180,30 +181,38 @@ __device__ __forceinline__ void load_slice(Slice<kEPT>& s, const TraceRsrc& rs, 
   }
 }
 
-// Ring layout: window slot s, model m owns the three 64-bit words at
-// s * (3M + 1) + 3m (the odd slot stride puts one model's cells of
+// Ring layout: window slot s, model m owns the four 64-bit words at
+// s * (4M + 1) + 4m (the odd slot stride puts one model's cells of
 // neighbouring windows on different LDS banks):
-//   +0 tokens     P (low 32 bits) | D (high 32 bits)
-//   +1 counts     (dA << 32) + dW          summed over the window's rows
-//   +2 integrals  (dA*te << 32) + dW*te    te = t_end - ts, 1..window_ms
-// with dA = [ADMIT] - [FINISH], dW = [ARRIVE] - [ADMIT]; sums of the signed
-// low halves stay inside 32 bits (events per window * window_ms < 2^31).
+//   +0 tokens    P (low 32 bits) | D (high 32 bits)
+//   +1 arrivals  (count << 32) + sum of te over the window's ARRIVE rows
+//   +2 admits    (count << 32) + sum of te over its PREFILL|ADMIT rows
+//   +3 finishes  (count << 32) + sum of te over its FINISH rows
+// with te = t_end - ts in [1, window_ms]. The te sums stay below 2^31
+// (events per window * window_ms < 2^31), so no low half carries into its
+// count. From them, per window: dA = admits - finishes, dW = arrivals -
+// admits, and the in-window integral terms sum(dA * te) and sum(dW * te)
+// are the same differences of the te sums.
 //
-// One row into its cell c (word index): tokens by kind, the packed count
-// and integral words (see the ring layout) from the kind and te.
+// A row adds one 64-bit word: PREFILL and DECODE rows their tokens to P or
+// D, ARRIVE / ADMIT / FINISH rows (1 << 32) + te to their kind's word; an
+// ADMIT row also adds its prompt tokens to P. The word and the kind come
+// from a table indexed by code = kind | ADMIT >> 5 (4 bits per code:
+// word index, bit 2 "lifecycle word", bit 3 "high half"):
+//   0 ARRIVE -> word 1, lifecycle; 1 PREFILL -> P; 2 DECODE -> D;
+//   3 FINISH -> word 3, lifecycle; 5 PREFILL|ADMIT -> word 2, lifecycle
+//   (+ P); 4, 6, 7 (undefined bits, unvalidated input only) -> P.
+constexpr uint32_t kRowTable = 0x00607805u;
+
 __device__ __forceinline__ void tally_row(unsigned long long* ring, uint32_t c, uint32_t ty,
                                           uint32_t tok, uint32_t te) {
-  uint32_t* pd32 = (uint32_t*)ring;
-  const bool arr = ty == TRE_ARRIVE, adm = ty == (TRE_PREFILL | TRE_ADMIT);
-  const bool fin = ty == TRE_FINISH, dec = ty == TRE_DECODE;
-  // ARRIVE: dW = 1; PREFILL|ADMIT: dA = 1, dW = -1; FINISH: dA = -1
-  const uint32_t cnt_lo = arr ? 1u : (adm ? 0xFFFFFFFFu : 0u);
-  const uint32_t cnt_hi = fin ? 0xFFFFFFFFu : 0u;
-  const uint32_t itg_lo = arr ? te : (adm ? 0u - te : 0u);
-  const uint32_t itg_hi = adm ? te - 1u : (fin ? 0u - te : 0u);
-  atomicAdd(&pd32[2 * c + (dec ? 1 : 0)], (arr || fin) ? 0u : tok);
-  atomicAdd(&ring[c + 1], ((unsigned long long)cnt_hi << 32) | cnt_lo);
-  atomicAdd(&ring[c + 2], ((unsigned long long)itg_hi << 32) | itg_lo);
+  const uint32_t code = (ty & 3u) | ((ty >> 5) & 4u);
+  const uint32_t nib = __builtin_amdgcn_ubfe(kRowTable, code << 2, 4);
+  const bool life = (nib & 4u) != 0u;
+  const unsigned long long v =
+      ((unsigned long long)(life ? te : tok) << ((nib & 8u) << 2)) + (life ? (1ull << 32) : 0ull);
+  atomicAdd(&ring[c + (nib & 3u)], v);
+  if (code == 5u) atomicAdd((uint32_t*)&ring[c], tok);  // the admitted request's first prompt chunk
 }
 
 // General tally of the lane's rows in [e0, e_end) whose window fits the
@@ -244,7 +253,7 @@ __device__ __forceinline__ void tally_slice(const Slice<kEPT>& s, int c0, int a0
         mdl = mdl < mlast ? mdl : mlast;
         const uint32_t ty = (s.tw[j >> 2] >> (8 * (j & 3))) & 0xFFu;
         const uint32_t tok = (s.kw[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
-        tally_row(ring, ((uint32_t)w & wmask) * sstride + 3u * mdl, ty, tok, win32 - r);
+        tally_row(ring, ((uint32_t)w & wmask) * sstride + 4u * mdl, ty, tok, win32 - r);
       }
     }
   }
@@ -282,16 +291,9 @@ __device__ __forceinline__ void tally_fast(const Slice<kEPT>& s, uint32_t base_l
     mdl = mdl < mlast ? mdl : mlast;
     const uint32_t ty = (s.tw[j >> 2] >> (8 * (j & 3))) & 0xFFu;
     const uint32_t tok = (s.kw[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
-    tally_row(ring, __umul24((q + cbm) & wmask, sstride) + 3u * mdl, ty, tok, te);
+    tally_row(ring, __umul24((q + cbm) & wmask, sstride) + 4u * mdl, ty, tok, te);
   }
   if (last) *wlast = cbase + (int)ql;
-}
-
-// a packed (high << 32) + signed low word: the signed low half and the high
-// half it leaves after removing the low half's sign extension
-__device__ __forceinline__ void unpack32(unsigned long long v, int& hi, int& lo) {
-  lo = (int)(uint32_t)v;
-  hi = (int)(uint32_t)(v >> 32) + (int)((uint32_t)v >> 31);
 }
 
 // x mod d for x < 2^32, with magic = floor(2^32 / d) (2^32 - 1 for d = 1):
@@ -338,7 +340,7 @@ __device__ __forceinline__ void stream_body(const StreamParams& p) {
   const int M = p.M;
   const uint32_t wcap = p.wcap;
   const int C = p.chunk;
-  const uint32_t sstride = 3u * (uint32_t)M + 1u;  // ring words per window slot
+  const uint32_t sstride = 4u * (uint32_t)M + 1u;  // ring words per window slot
   const int nring = (int)(wcap * sstride);
   // [2][C][M] staged raw ratios (>= 0), -1 marks an idle window
   double* st_raw = (double*)(ring + nring);
@@ -413,8 +415,18 @@ __device__ __forceinline__ void stream_body(const StreamParams& p) {
   auto step = [&](Slice<kEPT>& cur, Slice<kEPT>& nxt, int k) -> bool {
     if (cA >= nW) return true;
     const int b3 = k % 3;
+    // ---- issue the loads of tile k+1 first (and of tile k again when the
+    // prefetch missed it): with both buffers live from here on, nothing
+    // below reuses a register a load is still filling
+    const int a0 = e0 & ~(kEPT - 1);
+    if (held != a0) load_slice<kEPT>(cur, rs, a0 + tid * kEPT);  // prefetch missed
+    const int pref = a0 + (int)kTile;
+    load_slice<kEPT>(nxt, rs, pref + tid * kEPT);  // zeros past the trace
     // ---- smooth [cA, cB) (staged last step); wave k mod kWaves, lanes < M
     if (wave == k % kWaves && cB > cA) {
+      // the whole workgroup waits for this wave at the step's barrier: let its
+      // dependent chain issue ahead of the other waves on its SIMD
+      __builtin_amdgcn_s_setprio(3);
       const bool own = lane < M;
       const int m = own ? lane : 0;
       const double* pr = st_raw + ((k + 1) & 1) * C * M + m;
@@ -508,6 +520,7 @@ __device__ __forceinline__ void stream_body(const StreamParams& p) {
         s_tick[1] = (int)mod_magic(sctr + (uint32_t)nw, (uint32_t)p.slow_w, p.magic_slow);
         s_tick[2] = tick;
       }
+      __builtin_amdgcn_s_setprio(0);
     }
     // ---- read and clear the cells of [cB, cC), one cell per thread (groups
     // of C lanes per model): complete windows that no row of this tile
@@ -516,21 +529,19 @@ __device__ __forceinline__ void stream_body(const StreamParams& p) {
     const int cC = wl < cB + C ? wl : cB + C;
     const int n = cC - cB;
     const bool valid = r_thread && rj < n;
-    unsigned long long pd = 0, ap = 0, wp = 0;
+    unsigned long long pd = 0, w_arr = 0, w_adm = 0, w_fin = 0;
     if (valid) {
-      const uint32_t c = ((uint32_t)(cB + rj) & (wcap - 1)) * sstride + 3u * (uint32_t)rm;
+      const uint32_t c = ((uint32_t)(cB + rj) & (wcap - 1)) * sstride + 4u * (uint32_t)rm;
       pd = ring[c];
-      ap = ring[c + 1];
-      wp = ring[c + 2];
+      w_arr = ring[c + 1];
+      w_adm = ring[c + 2];
+      w_fin = ring[c + 3];
       ring[c] = 0ull;
       ring[c + 1] = 0ull;
       ring[c + 2] = 0ull;
+      ring[c + 3] = 0ull;
     }
     // ---- tally tile k (tile k+1 loading meanwhile), capacity [cB, cB + wcap)
-    const int a0 = e0 & ~(kEPT - 1);
-    if (held != a0) load_slice<kEPT>(cur, rs, a0 + tid * kEPT);  // prefetch missed
-    const int pref = a0 + (int)kTile;
-    load_slice<kEPT>(nxt, rs, pref + tid * kEPT);  // zeros past the trace
     const int t_last = (pref < rend ? pref : rend) - 1;
     {
       const int c0 = a0 + tid * kEPT;
@@ -549,9 +560,11 @@ __device__ __forceinline__ void stream_body(const StreamParams& p) {
     int* cout = s_carry[(k + 1) & 1][0];
     double* sr = st_raw + (k & 1) * C * M;
     if (r_thread) {  // uniform over each group of C lanes
-      int ca, cw, la32, lw32;
-      unpack32(ap, ca, cw);      // counts word
-      unpack32(wp, la32, lw32);  // integrals word
+      // net active / waiting changes and their in-window integral terms
+      const int ca = (int)((uint32_t)(w_adm >> 32) - (uint32_t)(w_fin >> 32));
+      const int cw = (int)((uint32_t)(w_arr >> 32) - (uint32_t)(w_adm >> 32));
+      const int la32 = (int)((uint32_t)w_adm - (uint32_t)w_fin);
+      const int lw32 = (int)((uint32_t)w_arr - (uint32_t)w_adm);
       int ia = ca, iw = cw;  // inclusive prefix over the chunk's windows
       if (C <= 16) {
         // row shifts by 1, 2, 4, 8 lanes; groups are aligned inside a row
@@ -1254,7 +1267,7 @@ static int64_t max_events_per_window(int64_t window_ms) {
 
 static uint32_t ring_windows(int M) {
   uint32_t w = 256;
-  while (w > 2 && (size_t)w * (3 * (size_t)M + 1) * 8 > (size_t)kRingBytes) w >>= 1;
+  while (w > 2 && (size_t)w * (4 * (size_t)M + 1) * 8 > (size_t)kRingBytes) w >>= 1;
   return w;
 }
 
@@ -1278,7 +1291,7 @@ static int stream_waves(uint32_t n_traces) {
 
 static size_t stream_lds(const tre_events* ev, bool stage = false) {
   const size_t M = (size_t)ev->cfg.n_models, C = (size_t)chunk_windows(ev->cfg.n_models, ev->wcap);
-  const size_t base = ev->wcap * (3 * M + 1) * 8 + 2 * C * M * 8;
+  const size_t base = ev->wcap * (4 * M + 1) * 8 + 2 * C * M * 8;
   // stage: the decode ratios beside the prefill ones (which take the scalar
   // ratios' place), two shares and two flags per model
   return stage ? base + 2 * C * M * 8 + 2 * M * 8 + ((2 * M + 7) & ~(size_t)7) : base;
