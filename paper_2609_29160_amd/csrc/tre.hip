@@ -106,6 +106,17 @@ struct StreamParams {
   double* stage64;  // [trace][w][M][2]: prefill, decode
   float* stage32;
   uint8_t* sflags;  // TRE_STAGE_*
+  // the control replay streamed with its trace (tre_sweep without the
+  // actuation model, for traces that carry exactly one scenario)
+  const tre_scenario* sc;
+  const uint32_t* sc_count;  // [trace] scenarios on the trace, or NULL
+  const uint32_t* sc_first;  // [trace] the scenario when the count is 1
+  int32_t budget;
+  tre_move* moves;
+  uint32_t move_cap;
+  uint32_t* n_moves;
+  int32_t* r_final;
+  int64_t* r_windows;
 };
 
 // quotient and remainder of rel / window_ms for any 32-bit rel: the
@@ -303,6 +314,235 @@ __device__ __forceinline__ uint32_t mod_magic(uint32_t x, uint32_t d, uint32_t m
   return r >= d ? r - d : r;
 }
 
+// ------------------------------------------------------- control rules
+__device__ __forceinline__ unsigned long long dbits(double x) {
+  return (unsigned long long)__double_as_longlong(x);
+}
+
+// Wave-wide min / max of a 32-bit value, broadcast as a scalar: butterfly
+// within quads and rows (DPP quad_perm, half-row and row mirrors), then
+// rows folded through row broadcasts; lane 63 ends with the result.
+template <bool kMax>
+__device__ __forceinline__ uint32_t wave_fold(uint32_t x) {
+  // lanes a step does not reach read the identity, so each step is one
+  // DPP-sourced min / max
+  constexpr int id = kMax ? 0 : -1;
+  auto op = [](uint32_t a, uint32_t b) { return kMax ? (a > b ? a : b) : (a < b ? a : b); };
+  x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, (int)x, 0xB1, 0xF, 0xF, false));   // quad_perm 1,0,3,2
+  x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, (int)x, 0x4E, 0xF, 0xF, false));   // quad_perm 2,3,0,1
+  x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, (int)x, 0x141, 0xF, 0xF, false));  // row_half_mirror
+  x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, (int)x, 0x140, 0xF, 0xF, false));  // row_mirror
+  x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, (int)x, 0x142, 0xA, 0xF, false));  // row_bcast:15
+  x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, (int)x, 0x143, 0xC, 0xF, false));  // row_bcast:31
+  return (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
+}
+
+// Lowest lane among the candidates (bit per lane in cand) holding the
+// minimum (kMax: maximum) of Z, or -1. Z >= 0 and never NaN, so its bit
+// pattern orders like its value: the high words decide, and the low words
+// only where several candidates share the highest / lowest high word
+// (for +inf the low word is zero).
+template <bool kMax>
+__device__ __forceinline__ int wave_arg(unsigned long long cand, double Z, int lane) {
+  if (cand == 0ull) return -1;
+  const bool c = (cand >> lane) & 1ull;
+  const unsigned long long key = dbits(Z);
+  const uint32_t hi = (uint32_t)(key >> 32), lo = (uint32_t)key;
+  const uint32_t h = wave_fold<kMax>(c ? hi : (kMax ? 0u : 0xFFFFFFFFu));
+  unsigned long long tie = __ballot(c && hi == h);
+  if (__popcll(tie) > 1 && h != 0x7FF00000u) {
+    const bool c2 = (tie >> lane) & 1ull;
+    const uint32_t l = wave_fold<kMax>(c2 ? lo : (kMax ? 0u : 0xFFFFFFFFu));
+    tie = __ballot(c2 && lo == l);
+  }
+  return __ffsll((long long)tie) - 1;
+}
+
+__device__ __forceinline__ double read_lane_f64(double x, int l) {
+  const unsigned long long b = dbits(x);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)b, l);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(b >> 32), l);
+  return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+}
+
+constexpr int kTickBlock = 8;  // ticks loaded and normalised per block
+
+// Replica state of one scenario in the control replay, lane m = model m;
+// pool and nm hold the same value in every lane.
+struct CtlState {
+  int R;          // routable replicas of the lane's model
+  long long rw;   // replica-window sum over the windows before `since`
+  int since;
+  int pool;       // idle replicas (GPUs under the actuation model)
+  uint32_t nm;    // moves decided so far
+  int g;          // GPUs per replica (1 without the actuation model)
+  // actuation: transition in flight (0 none, 1 wake, 2 sleep), the window at
+  // whose end it completes, GPUs a sleep returns to the idle pool
+  int tkind, tuntil, tret;
+};
+
+// Per-scenario constants of the replay, lane m = model m.
+struct CtlConst {
+  double tau_c, tau_s;
+  int r_min;
+  uint32_t K;                    // moves allowed per tick
+  bool act;                      // the lane holds a model
+  unsigned long long live_lanes;
+  int32_t wake_w, sleep_w;       // actuation delays in windows
+  tre_move* moves;               // the scenario's move log
+  uint32_t move_cap;
+};
+
+// Transitions that completed before window w (actuation model only): a
+// finished wake closes the lane's replica-window sum and raises R; finished
+// sleeps return GPUs to the idle pool.
+template <bool kAct>
+__device__ __forceinline__ void ctl_complete(CtlState& st, int w) {
+  if constexpr (kAct) {
+    const bool done = st.tkind != 0 && st.tuntil < w;
+    if (done && st.tkind == 1) {
+      st.rw += (long long)st.R * (st.tuntil + 1 - st.since);
+      st.since = st.tuntil + 1;
+      st.R += 1;
+    }
+    unsigned long long back = __ballot(done && st.tkind == 2 && st.tret > 0);
+    while (back) {
+      const int l = __ffsll((long long)back) - 1;
+      st.pool += __builtin_amdgcn_readlane(st.tret, l);
+      back &= back - 1ull;
+    }
+    if (done) st.tkind = 0;
+  }
+}
+
+// One tick of the control rules at the end of window w (tws: w in bits
+// 0-29, kind in bits 30-31: bit 0 fast, bit 1 slow; wave-uniform), with the
+// lane's normalised state Z (Eq. (2); +inf when idle or not initialised):
+// the regions, the cadence rule, then up to K greedy moves with Eq. (3) for
+// the receiver and the donor order of the bounded transfer. Every decision
+// is wave-uniform (ballots are the candidate sets, receiver and donor are
+// scalars). kAct adds the actuation model: the budget counts GPUs
+// (footprint g per replica); a woken replica becomes routable wake_w
+// windows after its wake starts; a donor's replica stops being routable at
+// once and its GPUs reach the receiver after sleep_w windows, when the
+// receiver's wake starts (any shortfall g_r - g_d comes from the idle GPUs
+// at the move, any excess returns to them after the sleep); a model with a
+// transition in flight is neither receiver nor donor; vetoed models do not
+// release. A transition completing at the end of window u counts from
+// window u + 1.
+template <bool kAct>
+__device__ __forceinline__ void ctl_tick(CtlState& st, const CtlConst& c, int lane, uint32_t tws, double Z,
+                                         unsigned long long vetoed) {
+  const int w = (int)(tws & 0x3FFFFFFFu);
+  const uint32_t kind = tws >> 30;
+  ctl_complete<kAct>(st, w);
+  const unsigned long long crit = __ballot(c.act && Z < c.tau_c);
+  unsigned long long ok;
+  int path;
+  if (crit) {
+    if (!(kind & 1u)) return;  // rescue pending: rebalancing defers
+    path = TRE_PATH_RESCUE;
+    ok = crit;
+  } else if (kind & 2u) {
+    path = TRE_PATH_REBALANCE;
+    ok = __ballot(c.act && Z < 1.0);
+  } else {
+    return;
+  }
+  const unsigned long long sur = __ballot(c.act && Z > c.tau_s);
+  // models already in a transition: earlier in this tick, or in flight
+  unsigned long long used = kAct ? __ballot(st.tkind != 0) : 0ull;
+  // both halves widened as unsigned (a set bit 31 must not sign-extend)
+  const unsigned long long veto_mask =
+      kAct ? ((unsigned long long)(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)vetoed) |
+              ((unsigned long long)(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(vetoed >> 32)) << 32))
+           : 0ull;
+  for (uint32_t k = 0; k < c.K; ++k) {
+    const int r = wave_arg<false>(ok & ~used, Z, lane);  // Eq. (3)
+    if (r < 0) break;
+    const int g_r = kAct ? __builtin_amdgcn_readlane(st.g, r) : 1;
+    int d;
+    if (st.pool >= g_r) {
+      st.pool -= g_r;
+      d = TRE_DONOR_POOL;
+      if (kAct && lane == r) {
+        st.tkind = 1;
+        st.tuntil = w + c.wake_w;
+      }
+    } else {
+      const double Zr = read_lane_f64(Z, r);
+      const unsigned long long cd =
+          __ballot(c.act && st.R > c.r_min && Z > Zr && (!kAct || st.pool >= g_r - st.g)) & ~crit & ~used &
+          ~(1ull << r) & c.live_lanes & ~veto_mask;
+      d = wave_arg<true>(cd & sur, Z, lane);
+      if (d < 0) d = wave_arg<true>(cd & ~sur, Z, lane);
+      if (d < 0) break;
+      used |= 1ull << d;
+      if constexpr (kAct) {
+        const int short_by = g_r - __builtin_amdgcn_readlane(st.g, d);
+        if (short_by > 0) st.pool -= short_by;
+        if (lane == d) {
+          st.tkind = 2;
+          st.tuntil = w + c.sleep_w;
+          st.tret = short_by < 0 ? -short_by : 0;
+        }
+        if (lane == r) {
+          st.tkind = 1;
+          st.tuntil = w + c.sleep_w + c.wake_w;
+        }
+      }
+    }
+    used |= 1ull << r;
+    // routable changes: the donor's at once (from w+1), the receiver's here
+    // only without the actuation model (else when its wake completes)
+    if (lane == d || (!kAct && lane == r)) {
+      st.rw += (long long)st.R * (w + 1 - st.since);
+      st.since = w + 1;
+      st.R += lane == d ? -1 : 1;
+    }
+    if (lane == 0 && st.nm < c.move_cap) {
+      tre_move mv;
+      mv.window = (uint32_t)w;
+      mv.path = (uint8_t)path;
+      mv.receiver = (uint8_t)r;
+      mv.donor = (uint8_t)d;
+      mv.pad = 0;
+      c.moves[st.nm] = mv;
+    }
+    ++st.nm;
+  }
+}
+
+// One model's replay constants and state in LDS, for a replay that moves
+// between waves from step to step.
+struct CtlModel {
+  double theta;     // theta * theta_scale
+  double tau_c, tau_s;
+  long long rw;
+  int R, since, r_min, pad;
+};
+
+// Initial replica state of a scenario (lane m = model m): R = r_init, idle
+// = budget - sum of g * r_init over the models.
+__device__ __forceinline__ void ctl_init(CtlState& st, int r_init, int g, bool act, int budget) {
+  st.R = act ? r_init : 0;
+  st.g = g;
+  int rsum = st.R * g;
+  rsum += __shfl_xor(rsum, 1);
+  rsum += __shfl_xor(rsum, 2);
+  rsum += __shfl_xor(rsum, 4);
+  rsum += __shfl_xor(rsum, 8);
+  rsum += __shfl_xor(rsum, 16);
+  rsum += __shfl_xor(rsum, 32);
+  st.pool = budget - __builtin_amdgcn_readfirstlane(rsum);
+  st.rw = 0;
+  st.since = 0;
+  st.nm = 0;
+  st.tkind = 0;
+  st.tuntil = 0;
+  st.tret = 0;
+}
+
 // One workgroup per trace; every thread tallies and evaluates, one barrier
 // per step. Step k, with [cA, cB) the chunk evaluated in step k-1 and
 // [cB, cC), cC = min(wl, cB + C), the windows completed by earlier tiles
@@ -342,7 +582,12 @@ __device__ __forceinline__ void stream_body(const StreamParams& p) {
   const int C = p.chunk;
   const uint32_t sstride = 4u * (uint32_t)M + 1u;  // ring words per window slot
   const int nring = (int)(wcap * sstride);
-  // [2][C][M] staged raw ratios (>= 0), -1 marks an idle window
+  // [nbuf][C][M] staged raw ratios (>= 0), -1 marks an idle window. Step k's
+  // evaluation writes buffer k % nbuf and the smoothing chain of step k + 1
+  // reads it; with the control replay in the stream the chain writes the
+  // smoothed values of its tick windows back into it, and the replay reads
+  // them in step k + 2 (hence three buffers)
+  constexpr int nbuf = kStage ? 2 : 3;
   double* st_raw = (double*)(ring + nring);
   // kStage (no scalar TSS is written): the staged prefill ratios in the
   // scalar ratios' place and the decode ratios after them ([2][C][M] each,
@@ -353,6 +598,11 @@ __device__ __forceinline__ void stream_body(const StreamParams& p) {
   double* const s_Sd = s_Sp + M;
   uint8_t* const s_ip = (uint8_t*)(s_Sd + M);
   uint8_t* const s_id = s_ip + M;
+  // the control replay (not kStage): one record per model, then idle
+  // replicas, moves, and per staging buffer the fast- and slow-tick masks of
+  // its chunk and the chunk's first window
+  CtlModel* const s_cm = (CtlModel*)(st_raw + 3 * C * M);
+  uint32_t* const s_cmeta = (uint32_t*)(s_cm + M);  // [0] idle, [1] moves, [2+b] fast, [5+b] slow, [8+b] window
   const long long e_begin = p.off[trace];
   const long long e_end = p.off[trace + 1];
   const long long win = p.window_ms;
@@ -396,6 +646,92 @@ __device__ __forceinline__ void stream_body(const StreamParams& p) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = tid & 63;
 
+  // the trace's one scenario, replayed here (else -1: the tick snapshot is
+  // written for a separate replay)
+  int ctl_s = -1;
+  uint32_t ctl_K = 0;
+  if constexpr (!kStage) {
+    if (p.sc_count && p.sc_count[trace] == 1u) ctl_s = (int)p.sc_first[trace];
+  }
+  ctl_s = __builtin_amdgcn_readfirstlane(ctl_s);
+  if (ctl_s >= 0) {
+    const tre_scenario sc = p.sc[ctl_s];
+    ctl_K = sc.max_moves;
+    if (wave == 0) {
+      const bool act = lane < M;
+      const tre_profile pr = p.prof[(int64_t)trace * M + (act ? lane : 0)];
+      CtlState st;
+      ctl_init(st, pr.r_init, 1, act, p.budget);
+      if (act) {
+        CtlModel cm;
+        cm.theta = pr.theta * sc.theta_scale;
+        cm.tau_c = sc.tau_crit_override >= 0.0 ? sc.tau_crit_override : pr.tau_crit;
+        cm.tau_s = pr.tau_surplus;
+        cm.rw = 0;
+        cm.R = st.R;
+        cm.since = 0;
+        cm.r_min = pr.r_min;
+        cm.pad = 0;
+        s_cm[lane] = cm;
+      }
+      if (lane < 11) s_cmeta[lane] = lane == 0 ? (uint32_t)st.pool : 0u;
+    }
+  }
+  // the replay of the ticks the chain recorded in staging buffer b: state
+  // from LDS, ctl_tick per tick in window order, state back to LDS; the
+  // buffer's ticks are then consumed
+  auto ctl_run = [&](int b) {
+    const uint32_t tmf = (uint32_t)__builtin_amdgcn_readfirstlane((int)s_cmeta[2 + b]);
+    const uint32_t tms = (uint32_t)__builtin_amdgcn_readfirstlane((int)s_cmeta[5 + b]);
+    uint32_t tm = tmf | tms;
+    if (!tm) return;
+    const int w0 = __builtin_amdgcn_readfirstlane((int)s_cmeta[8 + b]);
+    const bool act = lane < M;
+    const int m = act ? lane : 0;
+    CtlModel* const cm = s_cm + m;
+    CtlState st;
+    st.R = cm->R;
+    st.rw = cm->rw;
+    st.since = cm->since;
+    st.pool = __builtin_amdgcn_readfirstlane((int)s_cmeta[0]);
+    st.nm = (uint32_t)__builtin_amdgcn_readfirstlane((int)s_cmeta[1]);
+    st.g = 1;
+    st.tkind = 0;
+    st.tuntil = 0;
+    st.tret = 0;
+    CtlConst c;
+    c.tau_c = cm->tau_c;
+    c.tau_s = cm->tau_s;
+    c.r_min = cm->r_min;
+    c.K = ctl_K;
+    c.act = act;
+    c.live_lanes = __ballot(act);
+    c.wake_w = 0;
+    c.sleep_w = 0;
+    c.moves = p.moves + (int64_t)ctl_s * p.move_cap;
+    c.move_cap = p.move_cap;
+    const double th = cm->theta;
+    const double* sb = st_raw + b * C * M + m;
+    while (tm) {
+      const int u = __ffs(tm) - 1;
+      tm &= tm - 1u;
+      const double Z = act ? sb[u * M] / th : INFINITY;  // Eq. (2); the buffer holds +inf when idle / not initialised
+      const uint32_t kind = ((tmf >> u) & 1u) | (((tms >> u) & 1u) << 1);
+      ctl_tick<false>(st, c, lane, (uint32_t)(w0 + u) | (kind << 30), Z, 0ull);
+    }
+    if (act) {
+      cm->R = st.R;
+      cm->rw = st.rw;
+      cm->since = st.since;
+    }
+    if (lane == 0) {
+      s_cmeta[0] = (uint32_t)st.pool;
+      s_cmeta[1] = st.nm;
+      s_cmeta[2 + b] = 0u;
+      s_cmeta[5 + b] = 0u;
+    }
+  };
+
   // rows are counted from the trace's first kEPT-aligned row (below 2^27)
   const long long brow = e_begin & ~(long long)(kEPT - 1);
   const int rend = (int)(e_end - brow);  // one past the trace's last row
@@ -429,7 +765,8 @@ __device__ __forceinline__ void stream_body(const StreamParams& p) {
       __builtin_amdgcn_s_setprio(3);
       const bool own = lane < M;
       const int m = own ? lane : 0;
-      const double* pr = st_raw + ((k + 1) & 1) * C * M + m;
+      const int bc = (k + nbuf - 1) % nbuf;  // staged in step k - 1
+      double* const pr = st_raw + bc * C * M + m;
       const double alpha = s_alpha[m];
       const double oma = 1.0 - alpha;
       double S = s_S[m];
@@ -446,11 +783,12 @@ __device__ __forceinline__ void stream_body(const StreamParams& p) {
       const uint32_t fctr = (uint32_t)s_tick[0], sctr = (uint32_t)s_tick[1];
       int tick = s_tick[2];
       const int nw = cB - cA;
-      // tick windows of the chunk: bit u for window cA + u (lanes u < nw)
+      // tick windows of the chunk: bit u for window cA + u (lanes u < nw),
+      // fast and slow cadences apart
       const uint32_t u1 = (uint32_t)lane + 1u;
-      const uint32_t tm = (uint32_t)__ballot(lane < nw &&
-          (mod_magic(fctr + u1, (uint32_t)p.fast_w, p.magic_fast) == 0u ||
-           mod_magic(sctr + u1, (uint32_t)p.slow_w, p.magic_slow) == 0u));
+      const uint32_t tmf = (uint32_t)__ballot(lane < nw && mod_magic(fctr + u1, (uint32_t)p.fast_w, p.magic_fast) == 0u);
+      const uint32_t tms = (uint32_t)__ballot(lane < nw && mod_magic(sctr + u1, (uint32_t)p.slow_w, p.magic_slow) == 0u);
+      const uint32_t tm = tmf | tms;
       for (int u0 = 0; u0 < nw; u0 += 4) {
         double rv[4];
 #pragma unroll
@@ -475,7 +813,7 @@ __device__ __forceinline__ void stream_body(const StreamParams& p) {
               if (p.flags) p.flags[c] = (uint8_t)((idle ? TRE_FLAG_IDLE : 0) | (init ? TRE_FLAG_INIT : 0));
             }
             if constexpr (kStage) {  // the stage shares: the same smoothing per stage
-              const int j = ((u0 + u) & (C - 1)) * M + ((k + 1) & 1) * C * M + m;
+              const int j = ((u0 + u) & (C - 1)) * M + bc * C * M + m;
               const double rp = raw, rd = st_d[j];  // st_p is st_raw
               const bool pi = rp < 0.0, di = rd < 0.0;
               const double p1 = alpha * rp;
@@ -498,8 +836,12 @@ __device__ __forceinline__ void stream_body(const StreamParams& p) {
               }
             }
             if ((tm >> (u0 + u)) & 1u) {
-              if (own && p.snap && tick < p.n_ticks)
-                p.snap[((int64_t)trace * p.n_ticks + tick) * M + m] = (idle || !init) ? INFINITY : S;
+              const double zs = (idle || !init) ? INFINITY : S;
+              if (ctl_s >= 0) {  // for the replay two steps on (the raw ratio is read already)
+                if (own) pr[((u0 + u) & (C - 1)) * M] = zs;
+              } else if (own && p.snap && tick < p.n_ticks) {
+                p.snap[((int64_t)trace * p.n_ticks + tick) * M + m] = zs;
+              }
               ++tick;
             }
           }
@@ -519,6 +861,11 @@ __device__ __forceinline__ void stream_body(const StreamParams& p) {
         s_tick[0] = (int)mod_magic(fctr + (uint32_t)nw, (uint32_t)p.fast_w, p.magic_fast);
         s_tick[1] = (int)mod_magic(sctr + (uint32_t)nw, (uint32_t)p.slow_w, p.magic_slow);
         s_tick[2] = tick;
+        if (ctl_s >= 0) {
+          s_cmeta[2 + bc] = tmf;
+          s_cmeta[5 + bc] = tms;
+          s_cmeta[8 + bc] = (uint32_t)cA;
+        }
       }
       __builtin_amdgcn_s_setprio(0);
     }
@@ -558,7 +905,7 @@ __device__ __forceinline__ void stream_body(const StreamParams& p) {
     // ---- evaluate [cB, cC): carry prefix, window integrals, Eq. (1)
     const int* cin = s_carry[k & 1][0];
     int* cout = s_carry[(k + 1) & 1][0];
-    double* sr = st_raw + (k & 1) * C * M;
+    double* sr = st_raw + (k % nbuf) * C * M;
     if (r_thread) {  // uniform over each group of C lanes
       // net active / waiting changes and their in-window integral terms
       const int ca = (int)((uint32_t)(w_adm >> 32) - (uint32_t)(w_fin >> 32));
@@ -621,8 +968,8 @@ __device__ __forceinline__ void stream_body(const StreamParams& p) {
             if (den < dwin) den = dwin;
             rd = num / den;
           }
-          st_p[(k & 1) * C * M + rj * M + rm] = rp;
-          st_d[(k & 1) * C * M + rj * M + rm] = rd;
+          st_p[(k % nbuf) * C * M + rj * M + rm] = rp;
+          st_d[(k % nbuf) * C * M + rj * M + rm] = rd;
         }
         if (cells) {
           const int64_t o = ((int64_t)trace * nW + w) * M + rm;
@@ -640,6 +987,14 @@ __device__ __forceinline__ void stream_body(const StreamParams& p) {
     if (n == 0 && tid < M) {
       cout[tid] = cin[tid];
       cout[TRE_MAX_MODELS + tid] = cin[TRE_MAX_MODELS + tid];
+    }
+    // ---- the control replay of the ticks the chain smoothed in step k - 1,
+    // on another wave than this step's chain, after its tally (the tile it
+    // tallied no longer holds registers)
+    if (ctl_s >= 0 && wave == (k + kWaves / 2) % kWaves) {
+      __builtin_amdgcn_s_setprio(3);
+      ctl_run((k + 1) % 3);
+      __builtin_amdgcn_s_setprio(0);
     }
     // entries rotate over three steps: step k writes entry k % 3, every wave
     // reads it right after the barrier that ends step k, and it is reset
@@ -675,9 +1030,27 @@ __device__ __forceinline__ void stream_body(const StreamParams& p) {
     cB = cC;
     return false;
   };
+  int k_end = 0;
   for (int k = 0;; k += 2) {
-    if (step(buf0, buf1, k)) break;
-    if (step(buf1, buf0, k + 1)) break;
+    if (step(buf0, buf1, k)) {
+      k_end = k;
+      break;
+    }
+    if (step(buf1, buf0, k + 1)) {
+      k_end = k + 1;
+      break;
+    }
+  }
+  // the ticks of the last chunk, then the replay's outputs (the last step's
+  // barrier made the chain's values visible)
+  if (ctl_s >= 0 && wave == 0) {
+    ctl_run((k_end + 1) % 3);
+    if (lane < M) {
+      const CtlModel cm = s_cm[lane];
+      p.r_final[(int64_t)ctl_s * M + lane] = cm.R;
+      p.r_windows[(int64_t)ctl_s * M + lane] = cm.rw + (long long)cm.R * (nW - cm.since);
+    }
+    if (lane == 0) p.n_moves[ctl_s] = s_cmeta[1];
   }
 }
 
@@ -718,72 +1091,12 @@ struct CtlParams {
   int32_t sleep_w;           // windows a released replica hides, drains and sleeps
   const int32_t* footprint;  // [trace][M] GPUs per replica, or NULL (1)
   const uint64_t* veto;      // [trace][tick] donor releases refused, or NULL
+  const uint32_t* sc_count;  // [trace] scenarios per trace of a sweep, or NULL
 };
 
-__device__ __forceinline__ unsigned long long dbits(double x) {
-  return (unsigned long long)__double_as_longlong(x);
-}
-
-// Wave-wide min / max of a 32-bit value, broadcast as a scalar: butterfly
-// within quads and rows (DPP quad_perm, half-row and row mirrors), then
-// rows folded through row broadcasts; lane 63 ends with the result.
-template <bool kMax>
-__device__ __forceinline__ uint32_t wave_fold(uint32_t x) {
-  // lanes a step does not reach read the identity, so each step is one
-  // DPP-sourced min / max
-  constexpr int id = kMax ? 0 : -1;
-  auto op = [](uint32_t a, uint32_t b) { return kMax ? (a > b ? a : b) : (a < b ? a : b); };
-  x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, (int)x, 0xB1, 0xF, 0xF, false));   // quad_perm 1,0,3,2
-  x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, (int)x, 0x4E, 0xF, 0xF, false));   // quad_perm 2,3,0,1
-  x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, (int)x, 0x141, 0xF, 0xF, false));  // row_half_mirror
-  x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, (int)x, 0x140, 0xF, 0xF, false));  // row_mirror
-  x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, (int)x, 0x142, 0xA, 0xF, false));  // row_bcast:15
-  x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, (int)x, 0x143, 0xC, 0xF, false));  // row_bcast:31
-  return (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
-}
-
-// Lowest lane among the candidates (bit per lane in cand) holding the
-// minimum (kMax: maximum) of Z, or -1. Z >= 0 and never NaN, so its bit
-// pattern orders like its value: the high words decide, and the low words
-// only where several candidates share the highest / lowest high word
-// (for +inf the low word is zero).
-template <bool kMax>
-__device__ __forceinline__ int wave_arg(unsigned long long cand, double Z, int lane) {
-  if (cand == 0ull) return -1;
-  const bool c = (cand >> lane) & 1ull;
-  const unsigned long long key = dbits(Z);
-  const uint32_t hi = (uint32_t)(key >> 32), lo = (uint32_t)key;
-  const uint32_t h = wave_fold<kMax>(c ? hi : (kMax ? 0u : 0xFFFFFFFFu));
-  unsigned long long tie = __ballot(c && hi == h);
-  if (__popcll(tie) > 1 && h != 0x7FF00000u) {
-    const bool c2 = (tie >> lane) & 1ull;
-    const uint32_t l = wave_fold<kMax>(c2 ? lo : (kMax ? 0u : 0xFFFFFFFFu));
-    tie = __ballot(c2 && lo == l);
-  }
-  return __ffsll((long long)tie) - 1;
-}
-
-__device__ __forceinline__ double read_lane_f64(double x, int l) {
-  const unsigned long long b = dbits(x);
-  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)b, l);
-  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(b >> 32), l);
-  return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
-}
-
-constexpr int kTickBlock = 8;  // ticks loaded and normalised per block
-
-// One wave per scenario, lane m = model m: every decision is wave-uniform
-// (ballots are the candidate sets, receiver and donor are scalars). Per
-// tick: Eq. (2), regions, the cadence rule, then up to K greedy moves with
-// Eq. (3) for the receiver and the donor order of the bounded transfer.
-// kAct adds the actuation model: the budget counts GPUs (footprint g per
-// replica); a woken replica becomes routable wake_w windows after its wake
-// starts; a donor's replica stops being routable at once and its GPUs reach
-// the receiver after sleep_w windows, when the receiver's wake starts (any
-// shortfall g_r - g_d comes from the idle GPUs at the move, any excess
-// returns to them after the sleep); a model with a transition in flight is
-// neither receiver nor donor; vetoed models do not release. A transition
-// completing at the end of window u counts from window u + 1.
+// One wave per scenario, lane m = model m: per tick Z = S / (theta * scale)
+// (Eq. (2)), then ctl_tick. Scenarios whose trace streamed its own replay
+// (sc_count[trace] == 1 in a sweep) are skipped.
 template <bool kAct>
 __global__ __launch_bounds__(256) void rebalance(CtlParams p) {
   const int lane = threadIdx.x & 63;
@@ -794,52 +1107,24 @@ __global__ __launch_bounds__(256) void rebalance(CtlParams p) {
   const int mc = act ? lane : 0;
   const tre_scenario sc = p.sc[s];
   const uint32_t trace = sc.trace < p.n_traces ? sc.trace : 0;
-  const uint32_t K = sc.max_moves;
+  if (p.sc_count && p.sc_count[trace] == 1u) return;  // replayed in the stream
   const tre_profile pr = p.prof[(int64_t)trace * M + mc];
   const double theta_eff = pr.theta * sc.theta_scale;
-  const double tau_c = sc.tau_crit_override >= 0.0 ? sc.tau_crit_override : pr.tau_crit;
-  const double tau_s = pr.tau_surplus;
-  const int r_min = pr.r_min;
-  int R = act ? pr.r_init : 0;
-  // GPUs per replica (1 without the actuation model)
+  CtlConst c;
+  c.tau_c = sc.tau_crit_override >= 0.0 ? sc.tau_crit_override : pr.tau_crit;
+  c.tau_s = pr.tau_surplus;
+  c.r_min = pr.r_min;
+  c.K = sc.max_moves;
+  c.act = act;
+  c.live_lanes = __ballot(act);
+  c.wake_w = p.wake_w;
+  c.sleep_w = p.sleep_w;
+  c.moves = p.moves + (int64_t)s * p.move_cap;
+  c.move_cap = p.move_cap;
   int g = 1;
   if (kAct && p.footprint && act) g = p.footprint[(int64_t)trace * M + lane];
-  int rsum = R * g;
-  rsum += __shfl_xor(rsum, 1);
-  rsum += __shfl_xor(rsum, 2);
-  rsum += __shfl_xor(rsum, 4);
-  rsum += __shfl_xor(rsum, 8);
-  rsum += __shfl_xor(rsum, 16);
-  rsum += __shfl_xor(rsum, 32);
-  int pool = p.budget - __builtin_amdgcn_readfirstlane(rsum);  // idle replicas / GPUs
-  const unsigned long long live_lanes = __ballot(act);
-  // replica-window sums accumulate when a lane's R changes: windows
-  // [since, w] ran with the old R, a change at the end of window w applies
-  // from w+1
-  long long rw = 0;
-  int since = 0;
-  uint32_t nm = 0;
-  // actuation state of the lane's model: transition in flight (0 none,
-  // 1 wake, 2 sleep), the window at whose end it completes, GPUs a sleep
-  // returns to the idle pool
-  int tkind = 0, tuntil = 0, tret = 0;
-  auto complete = [&](int w) {  // transitions that completed before window w
-    if constexpr (kAct) {
-      const bool done = tkind != 0 && tuntil < w;
-      if (done && tkind == 1) {
-        rw += (long long)R * (tuntil + 1 - since);
-        since = tuntil + 1;
-        R += 1;
-      }
-      unsigned long long back = __ballot(done && tkind == 2 && tret > 0);
-      while (back) {
-        const int l = __ffsll((long long)back) - 1;
-        pool += __builtin_amdgcn_readlane(tret, l);
-        back &= back - 1ull;
-      }
-      if (done) tkind = 0;
-    }
-  };
+  CtlState st;
+  ctl_init(st, pr.r_init, g, act, p.budget);
 
   const int nt = p.n_ticks;
   const int64_t tbase = (int64_t)trace * (p.flags ? p.n_windows : nt);
@@ -856,9 +1141,9 @@ __global__ __launch_bounds__(256) void rebalance(CtlParams p) {
       tw[u] = p.tick_window[t] | ((uint32_t)p.tick_kind[t] << 30);
       vt[u] = (kAct && p.veto) ? p.veto[(int64_t)trace * nt + t] : 0ull;
       if (p.flags) {
-        const int64_t c = (tbase + p.tick_window[t]) * M + mc;
-        v[u] = p.vals[c];
-        f[u] = p.flags[c];
+        const int64_t cc = (tbase + p.tick_window[t]) * M + mc;
+        v[u] = p.vals[cc];
+        f[u] = p.flags[cc];
       } else {
         v[u] = p.vals[(tbase + t) * M + mc];
         f[u] = TRE_FLAG_INIT;
@@ -873,85 +1158,7 @@ __global__ __launch_bounds__(256) void rebalance(CtlParams p) {
     }
   };
   auto decide = [&](uint32_t twk, double Z, unsigned long long vetoed) {
-    const uint32_t tws = (uint32_t)__builtin_amdgcn_readfirstlane((int)twk);
-    const int w = (int)(tws & 0x3FFFFFFFu);
-    const uint32_t kind = tws >> 30;
-    complete(w);
-    const unsigned long long crit = __ballot(act && Z < tau_c);
-    unsigned long long ok;
-    int path;
-    if (crit) {
-      if (!(kind & 1u)) return;  // rescue pending: rebalancing defers
-      path = TRE_PATH_RESCUE;
-      ok = crit;
-    } else if (kind & 2u) {
-      path = TRE_PATH_REBALANCE;
-      ok = __ballot(act && Z < 1.0);
-    } else {
-      return;
-    }
-    const unsigned long long sur = __ballot(act && Z > tau_s);
-    // models already in a transition: earlier in this tick, or in flight
-    unsigned long long used = kAct ? __ballot(tkind != 0) : 0ull;
-    // both halves widened as unsigned (a set bit 31 must not sign-extend)
-    const unsigned long long veto_mask =
-        kAct ? ((unsigned long long)(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)vetoed) |
-                ((unsigned long long)(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(vetoed >> 32)) << 32))
-             : 0ull;
-    for (uint32_t k = 0; k < K; ++k) {
-      const int r = wave_arg<false>(ok & ~used, Z, lane);  // Eq. (3)
-      if (r < 0) break;
-      const int g_r = kAct ? __builtin_amdgcn_readlane(g, r) : 1;
-      int d;
-      if (pool >= g_r) {
-        pool -= g_r;
-        d = TRE_DONOR_POOL;
-        if (kAct && lane == r) {
-          tkind = 1;
-          tuntil = w + p.wake_w;
-        }
-      } else {
-        const double Zr = read_lane_f64(Z, r);
-        const unsigned long long cd =
-            __ballot(act && R > r_min && Z > Zr && (!kAct || pool >= g_r - g)) & ~crit & ~used &
-            ~(1ull << r) & live_lanes & ~veto_mask;
-        d = wave_arg<true>(cd & sur, Z, lane);
-        if (d < 0) d = wave_arg<true>(cd & ~sur, Z, lane);
-        if (d < 0) break;
-        used |= 1ull << d;
-        if constexpr (kAct) {
-          const int short_by = g_r - __builtin_amdgcn_readlane(g, d);
-          if (short_by > 0) pool -= short_by;
-          if (lane == d) {
-            tkind = 2;
-            tuntil = w + p.sleep_w;
-            tret = short_by < 0 ? -short_by : 0;
-          }
-          if (lane == r) {
-            tkind = 1;
-            tuntil = w + p.sleep_w + p.wake_w;
-          }
-        }
-      }
-      used |= 1ull << r;
-      // routable changes: the donor's at once (from w+1), the receiver's
-      // here only without the actuation model (else when its wake completes)
-      if (lane == d || (!kAct && lane == r)) {
-        rw += (long long)R * (w + 1 - since);
-        since = w + 1;
-        R += lane == d ? -1 : 1;
-      }
-      if (lane == 0 && nm < p.move_cap) {
-        tre_move mv;
-        mv.window = (uint32_t)w;
-        mv.path = (uint8_t)path;
-        mv.receiver = (uint8_t)r;
-        mv.donor = (uint8_t)d;
-        mv.pad = 0;
-        p.moves[(int64_t)s * p.move_cap + nm] = mv;
-      }
-      ++nm;
-    }
+    ctl_tick<kAct>(st, c, lane, (uint32_t)__builtin_amdgcn_readfirstlane((int)twk), Z, vetoed);
   };
   if (nt > 0) {
     double va[kTickBlock], vb[kTickBlock];
@@ -971,13 +1178,13 @@ __global__ __launch_bounds__(256) void rebalance(CtlParams p) {
         if (t0 + kTickBlock + u < nt) decide(wb[u], vb[u], xb[u]);
     }
   }
-  complete(p.n_windows);  // transitions completing at the end of the last window count as done
-  rw += (long long)R * (p.n_windows - since);
+  ctl_complete<kAct>(st, p.n_windows);  // transitions completing at the end of the last window count as done
+  st.rw += (long long)st.R * (p.n_windows - st.since);
   if (act) {
-    p.r_final[(int64_t)s * M + lane] = R;
-    p.r_windows[(int64_t)s * M + lane] = rw;
+    p.r_final[(int64_t)s * M + lane] = st.R;
+    p.r_windows[(int64_t)s * M + lane] = st.rw;
   }
-  if (lane == 0) p.n_moves[s] = nm;
+  if (lane == 0) p.n_moves[s] = st.nm;
 }
 
 // ---------------------------------------------------------------- validate
@@ -1291,10 +1498,13 @@ static int stream_waves(uint32_t n_traces) {
 
 static size_t stream_lds(const tre_events* ev, bool stage = false) {
   const size_t M = (size_t)ev->cfg.n_models, C = (size_t)chunk_windows(ev->cfg.n_models, ev->wcap);
-  const size_t base = ev->wcap * (4 * M + 1) * 8 + 2 * C * M * 8;
-  // stage: the decode ratios beside the prefill ones (which take the scalar
-  // ratios' place), two shares and two flags per model
-  return stage ? base + 2 * C * M * 8 + 2 * M * 8 + ((2 * M + 7) & ~(size_t)7) : base;
+  const size_t ring = ev->wcap * (4 * M + 1) * 8;
+  // stage: two staging buffers of prefill ratios (in the scalar ratios'
+  // place) and two of decode ratios, two shares and two flags per model
+  if (stage) return ring + 4 * C * M * 8 + 2 * M * 8 + ((2 * M + 7) & ~(size_t)7);
+  // three staging buffers, then the control replay's per-model records and
+  // 11 words
+  return ring + 3 * C * M * 8 + M * sizeof(CtlModel) + ((11 * 4 + 7) & ~(size_t)7);
 }
 
 // The load-time checks (synchronous): order, schema and per-window range
@@ -1527,11 +1737,18 @@ extern "C" int tre_events_info(const tre_events* ev, tre_info* info) {
   return TRE_OK;
 }
 
+// tre_sweep's workspace: the per-tick smoothed TSS of every trace (read by
+// the separate replay of traces with several scenarios), then per trace
+// its scenario count and one of its scenarios
+static size_t snapshot_bytes(const tre_events* ev) {
+  return ((size_t)ev->n_traces * (size_t)ev->n_ticks * (size_t)ev->cfg.n_models * sizeof(double) + 255) &
+         ~(size_t)255;
+}
+
 extern "C" int tre_workspace_size(const tre_events* ev, uint32_t n_scenarios, size_t* bytes) {
   if (!ev || !bytes) return fail(TRE_EINVAL, "tre_workspace_size: NULL argument");
   (void)n_scenarios;
-  *bytes = (size_t)ev->n_traces * (size_t)ev->n_ticks * (size_t)ev->cfg.n_models * sizeof(double);
-  if (*bytes == 0) *bytes = 256;
+  *bytes = snapshot_bytes(ev) + 2 * sizeof(uint32_t) * (size_t)ev->n_traces;
   return TRE_OK;
 }
 
@@ -1600,6 +1817,22 @@ static StreamParams stream_params(const tre_events* ev, const tre_profile* prof)
   return p;
 }
 
+// Scenarios per trace of a sweep: count[t] and, for a trace with exactly
+// one, that scenario in first[t] (count is zeroed first)
+__global__ __launch_bounds__(256) void zero_u32(uint32_t* q, uint32_t n) {
+  const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) q[i] = 0u;
+}
+
+__global__ __launch_bounds__(256) void sweep_map(const tre_scenario* sc, uint32_t n_sc, uint32_t n_traces,
+                                                 uint32_t* count, uint32_t* first) {
+  const uint32_t s = blockIdx.x * blockDim.x + threadIdx.x;
+  if (s >= n_sc) return;
+  const uint32_t t = sc[s].trace;
+  if (t >= n_traces) return;
+  if (atomicAdd(&count[t], 1u) == 0u) first[t] = s;
+}
+
 static int launch_stream(const tre_events* ev, const StreamParams& p, hipStream_t st) {
   const bool stage = p.stage64 || p.stage32 || p.sflags;
   const size_t lds = stream_lds(ev, stage);
@@ -1654,8 +1887,10 @@ static int act_windows(const tre_events* ev, const tre_actuation* act, ActWindow
 
 static int launch_rebalance(const tre_events* ev, const tre_profile* prof, const double* vals,
                             const uint8_t* flags, const tre_scenario* sc, uint32_t n_sc,
-                            const tre_ctl_out* out, const ActWindows* aw, hipStream_t st) {
+                            const tre_ctl_out* out, const ActWindows* aw, hipStream_t st,
+                            const uint32_t* sc_count = nullptr) {
   CtlParams c{};
+  c.sc_count = sc_count;
   c.prof = prof;
   c.sc = sc;
   c.n_sc = n_sc;
@@ -1767,10 +2002,31 @@ static int sweep_impl(const tre_events* ev, const tre_profile* prof, const tre_s
   StreamParams p = stream_params(ev, prof);
   p.tss32 = tss32;
   p.snap = (double*)ws;
+  // without the actuation model, a trace with exactly one scenario replays
+  // it in the stream (rebalance skips it)
+  uint32_t* count = nullptr;
+  if (n_scenarios && !act) {
+    count = (uint32_t*)((char*)ws + snapshot_bytes(ev));
+    uint32_t* first = count + ev->n_traces;
+    hipLaunchKernelGGL(zero_u32, dim3((ev->n_traces + 255) / 256), dim3(256), 0, st, count, ev->n_traces);
+    hipLaunchKernelGGL(sweep_map, dim3((n_scenarios + 255) / 256), dim3(256), 0, st, sc, n_scenarios,
+                       ev->n_traces, count, (uint32_t*)first);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fail(TRE_EHIP, "sweep_map launch: %s", hipGetErrorString(e));
+    p.sc = sc;
+    p.sc_count = count;
+    p.sc_first = first;
+    p.budget = ev->cfg.budget;
+    p.moves = out->moves;
+    p.move_cap = out->move_cap;
+    p.n_moves = out->n_moves;
+    p.r_final = out->r_final;
+    p.r_windows = out->r_windows;
+  }
   rc = launch_stream(ev, p, st);
   if (rc || n_scenarios == 0) return rc;
   return launch_rebalance(ev, prof, (const double*)ws, nullptr, sc, n_scenarios, out,
-                          act ? &aw : nullptr, st);
+                          act ? &aw : nullptr, st, count);
 }
 
 extern "C" int tre_rebalance(const tre_events* ev, const tre_profile* prof, const double* tss64,
