@@ -172,6 +172,20 @@ def test_stress_32_models_short(lib):
     _check_set(lib, "stress", w.trace_cfg(), traces, prof, sc)
 
 
+def test_sweep_mixed_scenario_counts(lib):
+    """A sweep where traces carry one scenario (replayed inside the stream),
+    several (replayed by the separate kernel from the tick snapshot) or none,
+    in a shuffled scenario table: every scenario equal to the oracle."""
+    w = tg.standard(4).scaled(duration_ms=600_000, n_traces=5, proc_params={
+        "flash_mult": 10.0, "flash_len_s": 30.0, "flash_first_s": 100.0, "flash_every_s": 200.0,
+        "flash_models": 4})
+    traces, prof, _ = _workload_set(w, 0, 5)
+    sc = _random_scenarios(5, 7, 44)
+    sc["trace"] = np.array([1, 0, 3, 1, 4, 1, 3], np.uint32)  # trace 2 has none, 0 and 4 one, 1 three, 3 two
+    say("mixed: events", sum(len(t["ts"]) for t in traces))
+    _check_set(lib, "mixed", w.trace_cfg(), traces, prof, sc)
+
+
 # ------------------------------------------------------------- edge cases
 def _cfg(M, window_ms, n_windows, fast_w=5, slow_w=10, budget=None):
     return {"window_ms": window_ms, "duration_ms": window_ms * n_windows,
