@@ -780,14 +780,15 @@ __device__ __forceinline__ void stream_body(const StreamParams& p) {
         id = s_id[m] != 0;
       }
       // windows since the last fast / slow tick before cA, ticks so far
-      const uint32_t fctr = (uint32_t)s_tick[0], sctr = (uint32_t)s_tick[1];
-      int tick = s_tick[2];
+      const uint32_t fctr = (uint32_t)__builtin_amdgcn_readfirstlane(s_tick[0]);
+      const uint32_t sctr = (uint32_t)__builtin_amdgcn_readfirstlane(s_tick[1]);
+      int tick = __builtin_amdgcn_readfirstlane(s_tick[2]);
       const int nw = cB - cA;
-      // tick windows of the chunk: bit u for window cA + u (lanes u < nw),
-      // fast and slow cadences apart
-      const uint32_t u1 = (uint32_t)lane + 1u;
-      const uint32_t tmf = (uint32_t)__ballot(lane < nw && mod_magic(fctr + u1, (uint32_t)p.fast_w, p.magic_fast) == 0u);
-      const uint32_t tms = (uint32_t)__ballot(lane < nw && mod_magic(sctr + u1, (uint32_t)p.slow_w, p.magic_slow) == 0u);
+      // tick windows of the chunk: bit u for window cA + u (u < nw), fast
+      // and slow cadences apart (scalar loops over the period ends)
+      uint32_t tmf = 0u, tms = 0u;
+      for (uint32_t u = (uint32_t)p.fast_w - 1u - fctr; u < (uint32_t)nw; u += (uint32_t)p.fast_w) tmf |= 1u << u;
+      for (uint32_t u = (uint32_t)p.slow_w - 1u - sctr; u < (uint32_t)nw; u += (uint32_t)p.slow_w) tms |= 1u << u;
       const uint32_t tm = tmf | tms;
       for (int u0 = 0; u0 < nw; u0 += 4) {
         double rv[4];
