@@ -518,6 +518,18 @@ def calibrate_main(args, w, dt, device, tre, torch, np):
                 "traffic": calib_traffic_for(w.name, dt.n_events, dom), "kernel": dom,
                 "kernel_ms": kernels[dom]["ms"], "alg_bytes_per_launch": alg[dom]}
     log("kernels " + ", ".join(f"{k} {kms[k]:.3f} ms" for k in CALIB_KERNELS) + f"; step {step_ms:.3f} ms")
+    # the ordering check (outside the step): the fits again with the
+    # concordant / discordant pair counts, from the step's counts
+    tre.tre_set_timing(True)
+    tre.tre_kernel_time("calib_order")
+    tre.tre_calib_order(ev, slo, tss["tss64"], tss["flags"], out)
+    o_ms, _ = tre.tre_kernel_time("calib_order")
+    tre.tre_set_timing(False)
+    fit_o = tre.unpack_fit(out["fit"])
+    order = {"ms": round(o_ms, 4), "concordant": int(fit_o["concordant"].astype(np.int64).sum()),
+             "discordant": int(fit_o["discordant"].astype(np.int64).sum())}
+    log(f"ordering check: calib_order {o_ms:.3f} ms; concordant {order['concordant']}, "
+        f"discordant {order['discordant']} pairs over all (trace, model)")
     cpu = parity = None
     if not args.no_cpu:
         n_s = max(1, int(np.searchsorted(np.cumsum(dt.counts), CPU_EVENT_BUDGET // 3, side="right")))
@@ -532,7 +544,7 @@ def calibrate_main(args, w, dt, device, tre, torch, np):
         "config": {"workload": w.name, "traces": T, "models": M, "window_ms": w.window_ms,
                    "duration_s": w.duration_ms // 1000, "events": dt.n_events, "requests": dt.n_arrive,
                    "req_cap": dt.req_cap, "mode": "calibration"},
-        "roofline": roofline, "kernels": kernels, "cpu_baseline": cpu, "parity": parity,
+        "roofline": roofline, "kernels": kernels, "ordering_check": order, "cpu_baseline": cpu, "parity": parity,
     }
     print(json.dumps(result), flush=True)
     if args.copy_calib_gb > 0:
@@ -784,7 +796,7 @@ def calib_cpu_leg(w, sample, out, tss, req_cap, tre, threads):
         cnt = out["counts"][t].cpu().numpy().view(np.uint32)
         ok = np.array_equal(cnt >> 16, rf["judged"]) and np.array_equal(cnt & 0xFFFF, rf["ok"])
         ok = ok and np.array_equal(fit[t]["theta"].view(np.uint64), rf["fit"]["theta"].view(np.uint64))
-        for k in ("n_cand", "n_healthy", "n_above", "healthy_above"):
+        for k in ("n_cand", "n_healthy", "n_above", "healthy_above", "concordant", "discordant"):
             ok = ok and np.array_equal(fit[t][k], rf["fit"][k])
         bad += 0 if ok else 1
     cpu = {"value": round(events / wall, 1), "unit": "request-events/s", "cores": n_workers, **host_cpu(), "kind": "oracle",

@@ -344,7 +344,12 @@ int tre_sweep_act(const tre_events* ev, const tre_profile* prof, const tre_scena
  *   - candidates of (trace, model): windows with judged >= 1 whose TSS is
  *     initialised and not idle. theta = the smallest candidate S such that,
  *     over the candidates with S >= theta, healthy >= reliability * count
- *     (fp64); +inf when none qualifies. */
+ *     (fp64); +inf when none qualifies;
+ *   - the ordering check (RQ1 asks that TSS follow the SLO-health ordering):
+ *     over the pairs of candidates of one (trace, model) with different S,
+ *     one healthy and one not, `concordant` counts those whose larger S is
+ *     the healthy window's and `discordant` the others; pairs of equal S are
+ *     in neither (healthy * unhealthy - concordant - discordant of them). */
 typedef struct {
   double ttft_ms, tpot_ms, e2e_ms;  /* bounds; +inf disables one            */
   double attain_q;                  /* window healthy when ok >= q * judged */
@@ -355,7 +360,10 @@ typedef struct {
   double theta;                     /* +inf when no candidate qualifies     */
   uint32_t n_cand, n_healthy;       /* candidate windows, healthy ones      */
   uint32_t n_above, healthy_above;  /* candidates with S >= theta, healthy  */
-} tre_fit;                          /* 24 bytes */
+  uint32_t concordant;  /* candidate pairs whose higher S is the healthy one
+                           (tre_calib_order; 0 from tre_calibrate)        */
+  uint32_t discordant;  /* ... whose higher S is the unhealthy one        */
+} tre_fit;                          /* 32 bytes */
 
 #define TRE_REQ_ARRIVED 1   /* an ARRIVE event was seen                  */
 #define TRE_REQ_COMPLETE 2  /* judged: ARRIVE, DECODE and FINISH present */
@@ -387,6 +395,16 @@ int tre_calibrate(const tre_events* ev, const tre_slo* slo, const double* tss64,
                   const uint8_t* flags, uint32_t req_cap, uint32_t* counts, tre_fit* fit,
                   tre_req_latency* reqs, uint64_t* n_bad_ids, void* ws, size_t ws_bytes,
                   void* stream);
+
+/* The fits of tre_calibrate again, with the ordering check: concordant and
+   discordant filled (tre_calibrate leaves them 0). counts are the per-window
+   counts tre_calibrate wrote for the same handle, SLOs and TSS (the window
+   health comes from them); the other arguments as tre_calibrate. Costs a full
+   sort of each (trace, model)'s candidate windows where the buckets of the
+   fit's histogram that hold both healthy and unhealthy windows have more than
+   1024 of them. Enqueued on `stream`. */
+int tre_calib_order(const tre_events* ev, const tre_slo* slo, const double* tss64, const uint8_t* flags,
+                    const uint32_t* counts, tre_fit* fit, void* stream);
 
 /* ---------------------------------------------------- closed-loop replay
  * The requests of each trace are served by each model's routable replicas,
@@ -533,7 +551,7 @@ int tre_loop_act(const tre_trace_cfg* cfg, uint32_t n_traces, const tre_loop_req
 /* Kernel timing (HIP events recorded around each launch on its stream).
    tre_set_timing(1) starts recording; tre_kernel_time waits for the
    recorded launches of `kernel` ("tss_stream", "rebalance", "validate",
-   "calib_fill", "calib_join", "calib_judge", "calib_fit", "loop_replay",
+   "calib_fill", "calib_join", "calib_judge", "calib_fit", "calib_order", "loop_replay",
    "stage_tss")
    and returns their total milliseconds and count, then forgets them. */
 int tre_set_timing(int enable);

@@ -42,11 +42,11 @@ MOVE_DTYPE = np.dtype([("window", "<u4"), ("path", "u1"), ("receiver", "u1"), ("
 SLO_DTYPE = np.dtype([("ttft_ms", "<f8"), ("tpot_ms", "<f8"), ("e2e_ms", "<f8"), ("attain_q", "<f8"),
                       ("reliability", "<f8")])
 FIT_DTYPE = np.dtype([("theta", "<f8"), ("n_cand", "<u4"), ("n_healthy", "<u4"), ("n_above", "<u4"),
-                      ("healthy_above", "<u4")])
+                      ("healthy_above", "<u4"), ("concordant", "<u4"), ("discordant", "<u4")])
 REQ_DTYPE = np.dtype([("ttft_ms", "<i8"), ("e2e_ms", "<i8"), ("tpot_ms", "<f8"), ("model", "<i4"),
                       ("complete", "u1"), ("has_tpot", "u1"), ("ok", "u1"), ("pad", "u1")])
 assert PROFILE_DTYPE.itemsize == 56 and SCENARIO_DTYPE.itemsize == 24 and MOVE_DTYPE.itemsize == 8
-assert SLO_DTYPE.itemsize == 40 and FIT_DTYPE.itemsize == 24 and REQ_DTYPE.itemsize == 32
+assert SLO_DTYPE.itemsize == 40 and FIT_DTYPE.itemsize == 32 and REQ_DTYPE.itemsize == 32
 SVC_DTYPE = np.dtype([("prefill_us", "<u4"), ("decode_us", "<u4")])
 LOOP_STATS_DTYPE = np.dtype([("n_arrived", "<u4"), ("n_started", "<u4"), ("n_done", "<u4"), ("n_ok", "<u4"),
                              ("e2e_sum", "<i8"), ("e2e_max", "<i8")])

@@ -66,6 +66,7 @@ typedef struct {
   double theta;                     /* fitted boundary, +inf when none */
   uint32_t n_cand, n_healthy;       /* candidate windows, healthy among them */
   uint32_t n_above, healthy_above;  /* candidates with S >= theta, healthy among them */
+  uint32_t concordant, discordant;  /* pairs of different S: the larger S healthy / unhealthy */
 } oc_fit;
 
 typedef struct {
@@ -176,16 +177,26 @@ int oracle_calib_fit(int64_t n_windows, int32_t M, const double* S, const uint8_
     }
     qsort(c, (size_t)k, sizeof(oc_cand), by_s_descending);
     /* walk from the largest S down; a threshold s covers every candidate
-       with S >= s, so it is evaluated after the last of a run of equal S */
-    oc_fit best = {INFINITY, (uint32_t)k, n_healthy, 0, 0};
+       with S >= s, so it is evaluated after the last of a run of equal S.
+       The ordering check (RQ1: TSS should follow the SLO-health ordering):
+       every window already passed has a larger S than the run, so each
+       unhealthy window of the run pairs concordantly with the healthy ones
+       passed, and each healthy window discordantly with the unhealthy ones
+       passed; windows of equal S do not pair. */
+    oc_fit best = {INFINITY, (uint32_t)k, n_healthy, 0, 0, 0, 0};
     uint32_t N = 0, H = 0;
     for (int64_t i = 0; i < k;) {
       int64_t j = i;
+      uint32_t run_h = 0, run_n = 0;
       while (j < k && c[j].s == c[i].s) {
-        N += 1;
-        H += (uint32_t)c[j].healthy;
+        run_n += 1;
+        run_h += (uint32_t)c[j].healthy;
         ++j;
       }
+      best.concordant += (run_n - run_h) * H;
+      best.discordant += run_h * (N - H);
+      N += run_n;
+      H += run_h;
       if ((double)H >= slo[m].reliability * (double)N) {
         best.theta = c[i].s;  /* smaller than any earlier qualifying value */
         best.n_above = N;

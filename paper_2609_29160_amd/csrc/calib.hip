@@ -293,6 +293,7 @@ struct FitParams {
   const uint32_t* counts;       // [n_traces][M][n_windows]
   const tre_slo* slo;           // [n_traces][M]
   tre_fit* fit;                 // [n_traces][M]
+  int32_t order;                // also the ordering counts (tre_calib_order)
   uint32_t n_traces;
   int32_t M;
   int64_t n_windows;
@@ -391,6 +392,7 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
   __shared__ uint64_t sc64[kFitWaves];
   __shared__ uint32_t sc32[kFitWaves + 1];
   __shared__ uint32_t n_gathered;
+  __shared__ uint32_t hpre_s[kFitThreads];  // healthy keys before each gathered position
   static_assert(256 * kFitWaves == 2 * kBuckets, "radix histogram and bucket tables share LDS");
 
   // XCD-aware block order: consecutive blocks go to different XCDs, so the
@@ -443,6 +445,8 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
   out.n_healthy = Ht;
   out.n_above = 0;
   out.healthy_above = 0;
+  out.concordant = 0;  // no pair of candidates with different S: none either way
+  out.discordant = 0;
   if (n_cand == 0) {
     if (tid == 0) *dst = out;
     return;
@@ -479,14 +483,23 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
   uint32_t tot;
   const uint32_t ex = block_exclusive_sum(v0 + v1, sc32, tot);
   const uint32_t offs[2] = {ex, ex + v0}, cnts[2] = {v0, v1};
-  // ---- 2. bucket status
+  // ---- 2. bucket status; the ordering counts across buckets: every key of
+  // a lower bucket has a smaller S, so bucket b pairs its u unhealthy keys
+  // with the P healthy keys below it (discordant) and its healthy keys with
+  // the G - P unhealthy keys below it (concordant). Pairs inside a bucket
+  // need its keys in order; only buckets holding both kinds have any.
   uint32_t qual_b = kNone;
   bool maybe[2];
+  uint32_t d_cross = 0, c_cross = 0, hu_mixed = 0, mixed[2];
 #pragma unroll
   for (int q = 0; q < 2; ++q) {
-    const uint32_t c = cnts[q] & 0xFFFFu, u = c - (cnts[q] >> 16);
+    const uint32_t c = cnts[q] & 0xFFFFu, h = cnts[q] >> 16, u = c - h;
     const uint32_t G = offs[q] & 0xFFFFu, P = offs[q] >> 16;
     const uint32_t N = n_cand - G, H = Ht - P;
+    d_cross += u * P;
+    c_cross += h * (G - P);
+    mixed[q] = (h != 0u && u != 0u) ? c : 0u;
+    hu_mixed += h * u;
     maybe[q] = false;
     if (c == 0) continue;
     if ((double)H >= rho * (double)N) {
@@ -498,34 +511,35 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
     }
   }
   const uint32_t bstar = block_min_u32(qual_b, sc32);
+  uint32_t D_cross = 0, C_cross = 0, HU_mixed = 0, mx_tot = 0, mx_ex = 0;
+  if (p.order) {  // uniform
+    (void)block_exclusive_sum(d_cross, sc32, D_cross);
+    (void)block_exclusive_sum(c_cross, sc32, C_cross);
+    (void)block_exclusive_sum(hu_mixed, sc32, HU_mixed);
+    mx_ex = block_exclusive_sum(mixed[0] + mixed[1], sc32, mx_tot);
+  }
   // ---- 3. keys of the undecided buckets below b*
   uint32_t mc[2];
 #pragma unroll
   for (int q = 0; q < 2; ++q) mc[q] = (maybe[q] && 2u * tid + q < bstar) ? (cnts[q] & 0xFFFFu) : 0u;
   uint32_t mtot;
   const uint32_t mex = block_exclusive_sum(mc[0] + mc[1], sc32, mtot);
-  if (mtot <= (uint32_t)kResolveCap) {
-    // per bucket: (G, P) and the compact offset with bit 31 marking a gathered bucket
-    hist[2 * tid] = offs[0];
-    hist[2 * tid + 1] = offs[1];
-    hist[kBuckets + 2 * tid] = mex | (mc[0] ? 0x80000000u : 0u);
-    hist[kBuckets + 2 * tid + 1] = (mex + mc[0]) | (mc[1] ? 0x80000000u : 0u);
+  __shared__ tre_fit s_out;
+  // the keys of the listed buckets (bit 31 of their hist[kBuckets + b] entry),
+  // gathered into cmp at their compact offsets and sorted (bitonic); returns
+  // with every thread holding cmp[tid] (or ~0) in `ck`
+  auto gather_sort = [&](uint32_t n_keys, uint64_t& ck) {
     if (tid == 0) n_gathered = 0;
     __syncthreads();
-    uint64_t kstar = ~0ull;  // smallest key of bucket b*
 #pragma unroll 4
     for (int j = 0; j < KPT; ++j) {
       const uint64_t kk = keys_lds[wave * KPT * 64 + j * 64 + lane];
       if (kk == ~0ull) continue;
-      const uint32_t bk = bucket(kk);
-      if (bk == bstar) kstar = kk < kstar ? kk : kstar;
-      else if (hist[kBuckets + bk] & 0x80000000u) cmp[atomicAdd(&n_gathered, 1u)] = kk;
+      if (hist[kBuckets + bucket(kk)] & 0x80000000u) cmp[atomicAdd(&n_gathered, 1u)] = kk;
     }
-    kstar = block_reduce_u64<2>(kstar, sc64);
-    // bitonic sort of the gathered keys, padded to a power of two
     uint32_t p2 = 2;
-    while (p2 < mtot) p2 <<= 1;
-    for (uint32_t i = mtot + tid; i < p2; i += kFitThreads) cmp[i] = ~0ull;
+    while (p2 < n_keys) p2 <<= 1;
+    for (uint32_t i = n_keys + tid; i < p2; i += kFitThreads) cmp[i] = ~0ull;
     __syncthreads();
     for (uint32_t kk2 = 2; kk2 <= p2; kk2 <<= 1) {
       for (uint32_t jj = kk2 >> 1; jj > 0; jj >>= 1) {
@@ -540,12 +554,28 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
         __syncthreads();
       }
     }
+    ck = tid < (int)n_keys ? cmp[tid] : ~0ull;
+  };
+  if (mtot <= (uint32_t)kResolveCap && (!p.order || mx_tot <= (uint32_t)kResolveCap)) {
+    // per bucket: (G, P) and the compact offset with bit 31 marking a gathered bucket
+    hist[2 * tid] = offs[0];
+    hist[2 * tid + 1] = offs[1];
+    hist[kBuckets + 2 * tid] = mex | (mc[0] ? 0x80000000u : 0u);
+    hist[kBuckets + 2 * tid + 1] = (mex + mc[0]) | (mc[1] ? 0x80000000u : 0u);
+    uint64_t kstar = ~0ull;  // smallest key of bucket b*
+#pragma unroll 4
+    for (int j = 0; j < KPT; ++j) {
+      const uint64_t kk = keys_lds[wave * KPT * 64 + j * 64 + lane];
+      if (kk != ~0ull && bucket(kk) == bstar) kstar = kk < kstar ? kk : kstar;
+    }
+    kstar = block_reduce_u64<2>(kstar, sc64);
+    uint64_t ck;
+    gather_sort(mtot, ck);
     // healthy keys before each gathered position; the gathered keys of one
     // bucket are contiguous, from its compact offset
-    const uint64_t ck = tid < (int)mtot ? cmp[tid] : ~0ull;
     uint32_t unused;
     const uint32_t hpre = block_exclusive_sum(tid < (int)mtot ? (uint32_t)(ck & 1ull) : 0u, sc32, unused);
-    uint32_t* hpre_l = (uint32_t*)keys_lds;  // the keys are no longer needed
+    uint32_t* const hpre_l = hpre_s;
     hpre_l[tid] = hpre;
     __syncthreads();
     uint32_t cand_g = kNone, cand_h = 0;
@@ -564,18 +594,65 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
     const uint32_t gmin = block_min_u32(cand_g, sc32);
     if (gmin != kNone) {
       if (cand_g == gmin) {
-        out.theta = __longlong_as_double((long long)(ck >> 1));
-        out.n_above = n_cand - gmin;
-        out.healthy_above = cand_h;
-        *dst = out;
+        s_out.theta = __longlong_as_double((long long)(ck >> 1));
+        s_out.n_above = n_cand - gmin;
+        s_out.healthy_above = cand_h;
       }
     } else if (tid == 0) {
+      s_out.theta = INFINITY;
+      s_out.n_above = 0;
+      s_out.healthy_above = 0;
       if (bstar != kNone) {
         const uint32_t GP = hist[bstar];
-        out.theta = __longlong_as_double((long long)(kstar >> 1));
-        out.n_above = n_cand - (GP & 0xFFFFu);
-        out.healthy_above = Ht - (GP >> 16);
+        s_out.theta = __longlong_as_double((long long)(kstar >> 1));
+        s_out.n_above = n_cand - (GP & 0xFFFFu);
+        s_out.healthy_above = Ht - (GP >> 16);
       }
+    }
+    if (!p.order) {
+      if (tid == 0) {
+        out.theta = s_out.theta;
+        out.n_above = s_out.n_above;
+        out.healthy_above = s_out.healthy_above;
+        *dst = out;
+      }
+      return;
+    }
+    // ---- the ordering counts inside the buckets that hold both kinds:
+    // their keys gathered and sorted; in a run of equal S the unhealthy keys
+    // (bit 0 clear) come first, so the healthy keys before an unhealthy one
+    // inside its bucket all have a smaller S (discordant pairs); the mixed
+    // pairs of equal S are counted per run, the rest are concordant
+    hist[kBuckets + 2 * tid] = mx_ex | (mixed[0] ? 0x80000000u : 0u);
+    hist[kBuckets + 2 * tid + 1] = (mx_ex + mixed[0]) | (mixed[1] ? 0x80000000u : 0u);
+    uint64_t mk;
+    gather_sort(mx_tot, mk);
+    const bool in = tid < (int)mx_tot;
+    const uint32_t mh = block_exclusive_sum(in ? (uint32_t)(mk & 1ull) : 0u, sc32, unused);
+    hpre_l[tid] = mh;
+    __syncthreads();
+    uint32_t d_in = 0, tie = 0;
+    if (in) {
+      const uint32_t cf = hist[kBuckets + bucket(mk)] & 0x7FFFFFFFu;
+      if (!(mk & 1ull)) d_in = mh - hpre_l[cf];
+      if (tid == (int)cf || (cmp[tid - 1] >> 1) != (mk >> 1)) {  // a run start: walk the run
+        uint32_t ru = 0, rh = 0;
+        for (uint32_t i = (uint32_t)tid; i < mx_tot && (cmp[i] >> 1) == (mk >> 1); ++i) {
+          if (cmp[i] & 1ull) ++rh;
+          else ++ru;
+        }
+        tie = ru * rh;
+      }
+    }
+    uint32_t D_in, T_in;
+    (void)block_exclusive_sum(d_in, sc32, D_in);
+    (void)block_exclusive_sum(tie, sc32, T_in);
+    if (tid == 0) {
+      out.theta = s_out.theta;
+      out.n_above = s_out.n_above;
+      out.healthy_above = s_out.healthy_above;
+      out.discordant = D_cross + D_in;
+      out.concordant = C_cross + (HU_mixed - D_in - T_in);
       *dst = out;
     }
     return;
@@ -662,27 +739,51 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
   __syncthreads();
   uint32_t best = kNone, best_h = 0;
   uint32_t run = wbase;  // healthy candidates before the current slot
+  // the ordering counts: an unhealthy key pairs with every healthy key
+  // before it (all of a smaller S, since in a run of equal S the unhealthy
+  // keys come first); the mixed pairs of equal S are counted per run
+  uint32_t d_all = 0, tie = 0;
 #pragma unroll
   for (int j = 0; j < KPT; ++j) {
     const uint32_t e = (uint32_t)(wave * KPT * 64 + j * 64 + lane);
     const uint64_t hbal = __ballot((hbits >> j) & 1u);
     const uint32_t before = run + (uint32_t)__popcll(hbal & lt_mask);
     run += (uint32_t)__popcll(hbal);
+    if (e < n_cand && !((hbits >> j) & 1u)) d_all += before;
     if (e < n_cand && (e == 0 || (keys_lds[e - 1] >> 1) != (keys_lds[e] >> 1))) {
       const uint32_t N = n_cand - e, H = Ht - before;
       if ((double)H >= rho * (double)N && e < best) {
         best = e;
         best_h = H;
       }
+      uint32_t ru = 0, rh = 0;
+      for (uint32_t i = e; i < n_cand && (keys_lds[i] >> 1) == (keys_lds[e] >> 1); ++i) {
+        if (keys_lds[i] & 1ull) ++rh;
+        else ++ru;
+      }
+      tie += ru * rh;
     }
   }
   const uint32_t g = block_min_u32(best, sc32);
+  uint32_t D_all, T_all;
+  (void)block_exclusive_sum(d_all, sc32, D_all);
+  (void)block_exclusive_sum(tie, sc32, T_all);
   if (g != kNone && best == g) {
-    out.theta = __longlong_as_double((long long)(keys_lds[g] >> 1));
-    out.n_above = n_cand - g;
-    out.healthy_above = best_h;
-    *dst = out;
-  } else if (g == kNone && tid == 0) {
+    s_out.theta = __longlong_as_double((long long)(keys_lds[g] >> 1));
+    s_out.n_above = n_cand - g;
+    s_out.healthy_above = best_h;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    if (g != kNone) {
+      out.theta = s_out.theta;
+      out.n_above = s_out.n_above;
+      out.healthy_above = s_out.healthy_above;
+    }
+    if (p.order) {
+      out.discordant = D_all;
+      out.concordant = Ht * (n_cand - Ht) - D_all - T_all;
+    }
     *dst = out;
   }
 }
@@ -697,6 +798,27 @@ static uint64_t calib_table_bytes(const tre_events* ev, uint32_t req_cap) {
 extern "C" int tre_calib_workspace_size(const tre_events* ev, uint32_t req_cap, size_t* bytes) {
   if (!ev || !bytes) return fail(TRE_EINVAL, "tre_calib_workspace_size: NULL argument");
   *bytes = (size_t)(256 + calib_table_bytes(ev, req_cap));
+  return TRE_OK;
+}
+
+// the fit of every (trace, model), with the ordering counts when `order`
+static int launch_fit(const tre_events* ev, const tre_slo* slo, const double* tss64, const uint8_t* flags,
+                      const uint32_t* counts, tre_fit* fit, int order, hipStream_t st) {
+  const int M = ev->cfg.n_models;
+  const int64_t nW = ev->n_windows;
+  FitParams fp{tss64, flags, counts, slo, fit, order, ev->n_traces, M, nW};
+  const uint32_t blocks = ((ev->n_traces + 7) / 8) * 8 * (uint32_t)M;
+  const int kpt = nW <= 1024 ? 1 : nW <= 2048 ? 2 : nW <= 4096 ? 4 : nW <= 8192 ? 8 : 16;
+  LaunchTimer lt(order ? "calib_order" : "calib_fit", st);
+  switch (kpt) {
+    case 1: hipLaunchKernelGGL(calib_fit<1>, dim3(blocks), dim3(kFitThreads), 0, st, fp); break;
+    case 2: hipLaunchKernelGGL(calib_fit<2>, dim3(blocks), dim3(kFitThreads), 0, st, fp); break;
+    case 4: hipLaunchKernelGGL(calib_fit<4>, dim3(blocks), dim3(kFitThreads), 0, st, fp); break;
+    case 8: hipLaunchKernelGGL(calib_fit<8>, dim3(blocks), dim3(kFitThreads), 0, st, fp); break;
+    default: hipLaunchKernelGGL(calib_fit<16>, dim3(blocks), dim3(kFitThreads), 0, st, fp); break;
+  }
+  lt.done();
+  HIP_TRY(hipGetLastError());
   return TRE_OK;
 }
 
@@ -754,20 +876,16 @@ extern "C" int tre_calibrate(const tre_events* ev, const tre_slo* slo, const dou
     lt.done();
     HIP_TRY(hipGetLastError());
   }
-  {
-    FitParams fp{tss64, flags, counts, slo, fit, ev->n_traces, M, nW};
-    const uint32_t blocks = ((ev->n_traces + 7) / 8) * 8 * (uint32_t)M;
-    const int kpt = nW <= 1024 ? 1 : nW <= 2048 ? 2 : nW <= 4096 ? 4 : nW <= 8192 ? 8 : 16;
-    LaunchTimer lt("calib_fit", st);
-    switch (kpt) {
-      case 1: hipLaunchKernelGGL(calib_fit<1>, dim3(blocks), dim3(kFitThreads), 0, st, fp); break;
-      case 2: hipLaunchKernelGGL(calib_fit<2>, dim3(blocks), dim3(kFitThreads), 0, st, fp); break;
-      case 4: hipLaunchKernelGGL(calib_fit<4>, dim3(blocks), dim3(kFitThreads), 0, st, fp); break;
-      case 8: hipLaunchKernelGGL(calib_fit<8>, dim3(blocks), dim3(kFitThreads), 0, st, fp); break;
-      default: hipLaunchKernelGGL(calib_fit<16>, dim3(blocks), dim3(kFitThreads), 0, st, fp); break;
-    }
-    lt.done();
-    HIP_TRY(hipGetLastError());
-  }
-  return TRE_OK;
+  return launch_fit(ev, slo, tss64, flags, counts, fit, 0, st);
+}
+
+extern "C" int tre_calib_order(const tre_events* ev, const tre_slo* slo, const double* tss64, const uint8_t* flags,
+                               const uint32_t* counts, tre_fit* fit, void* stream) {
+  if (!ev || !slo || !tss64 || !flags || !counts || !fit) return fail(TRE_EINVAL, "tre_calib_order: NULL argument");
+  if (ev->n_windows > (int64_t)kFitThreads * kFitMaxKPT)
+    return fail(TRE_ERANGE, "tre_calib_order: %lld windows, at most %d", (long long)ev->n_windows,
+                kFitThreads * kFitMaxKPT);
+  const int rc = check_device(ev);
+  if (rc) return rc;
+  return launch_fit(ev, slo, tss64, flags, counts, fit, 1, (hipStream_t)stream);
 }

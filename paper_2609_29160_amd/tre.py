@@ -35,7 +35,7 @@ MOVE_DTYPE = np.dtype([("window", "<u4"), ("path", "u1"), ("receiver", "u1"), ("
 SLO_DTYPE = np.dtype([("ttft_ms", "<f8"), ("tpot_ms", "<f8"), ("e2e_ms", "<f8"), ("attain_q", "<f8"),
                       ("reliability", "<f8")])
 FIT_DTYPE = np.dtype([("theta", "<f8"), ("n_cand", "<u4"), ("n_healthy", "<u4"), ("n_above", "<u4"),
-                      ("healthy_above", "<u4")])
+                      ("healthy_above", "<u4"), ("concordant", "<u4"), ("discordant", "<u4")])
 REQ_LATENCY_DTYPE = np.dtype([("ttft_ms", "<u4"), ("e2e_ms", "<u4"), ("tpot_ms", "<f8"), ("model", "u1"),
                               ("flags", "u1"), ("pad", "u1", (6,))])
 TRE_REQ_ARRIVED, TRE_REQ_COMPLETE, TRE_REQ_TPOT, TRE_REQ_OK = 1, 2, 4, 8
@@ -89,7 +89,7 @@ EXPORTS = ["tre_last_error", "tre_load_events", "tre_free_events", "tre_events_i
            "tre_check_params", "tre_workspace_size", "tre_eval_tss", "tre_rebalance", "tre_sweep",
            "tre_set_timing", "tre_kernel_time", "tre_check_actuation", "tre_rebalance_act", "tre_sweep_act",
            "tre_calib_workspace_size", "tre_calibrate", "tre_loop_workspace_size", "tre_loop", "tre_loop_act",
-           "tre_stage_tss", "tre_eval_stage", "tre_sweep_noalloc"]
+           "tre_stage_tss", "tre_eval_stage", "tre_sweep_noalloc", "tre_calib_order"]
 
 
 def _load():
@@ -128,6 +128,8 @@ def _load():
     L.tre_calib_workspace_size.argtypes = [vp, u32, ctypes.POINTER(sz)]
     L.tre_calibrate.restype = i32
     L.tre_calibrate.argtypes = [vp, vp, vp, vp, u32, vp, vp, vp, vp, vp, sz, vp]
+    L.tre_calib_order.restype = i32
+    L.tre_calib_order.argtypes = [vp, vp, vp, vp, vp, vp, vp]
     L.tre_loop_workspace_size.restype = i32
     L.tre_loop_workspace_size.argtypes = [ctypes.POINTER(_TraceCfg), ctypes.POINTER(_LoopRequests), u32,
                                           ctypes.POINTER(sz)]
@@ -384,6 +386,13 @@ def tre_calibrate(ev: Events, slo: torch.Tensor, tss64: torch.Tensor, flags: tor
     _check(_L.tre_calibrate(ev.handle, _ptr(slo), _ptr(tss64), _ptr(flags), int(out["req_cap"]), _ptr(out["counts"]),
                             _ptr(out["fit"]), _ptr(out.get("reqs")), _ptr(out.get("n_bad")), _ptr(ws),
                             ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def tre_calib_order(ev: Events, slo: torch.Tensor, tss64: torch.Tensor, flags: torch.Tensor,
+                    out: Dict[str, torch.Tensor], stream=None):
+    """The fits again with the ordering counts, from tre_calibrate's counts."""
+    _check(_L.tre_calib_order(ev.handle, _ptr(slo), _ptr(tss64), _ptr(flags), _ptr(out["counts"]), _ptr(out["fit"]),
+                              _stream(stream)))
 
 
 def unpack_fit(fit: torch.Tensor) -> np.ndarray:

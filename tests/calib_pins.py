@@ -113,6 +113,30 @@ def pin_hand_fit_with_ties(o):
     assert int(f["n_cand"]) == 1 and math.isinf(f["theta"]) and int(f["n_above"]) == 0
 
 
+def pin_hand_ordering_counts(o):
+    # The ordering check (RQ1): pairs of candidate windows with different S,
+    # one healthy (h) and one not (u). S = 5h 4h 3h 3u 1u:
+    #   concordant (larger S healthy): 5h>3u 5h>1u 4h>3u 4h>1u 3h>1u = 5
+    #   discordant (larger S unhealthy): none (the unhealthy 3 ties with the
+    #   healthy 3, and no healthy window lies below 3)
+    f = _fit_one(o, [5.0, 3.0, 3.0, 1.0, 4.0], [1, 1, 0, 0, 1], rho=0.75)
+    assert (int(f["concordant"]), int(f["discordant"])) == (5, 0)
+    # S = 9u 7h 7u 2h: concordant none (no unhealthy window lies below a
+    # healthy one); discordant 9u>7h, 9u>2h, 7u>2h = 3; the tie 7h/7u is in
+    # neither (h * u = 2 * 2 = 4 = 0 + 3 + 1)
+    f = _fit_one(o, [7.0, 9.0, 2.0, 7.0], [1, 0, 1, 0], rho=0.5)
+    assert (int(f["concordant"]), int(f["discordant"])) == (0, 3)
+    # perfectly ordered: every healthy window above every unhealthy one
+    f = _fit_one(o, [10.0, 8.0, 6.0, 1.0, 0.5], [1, 1, 1, 0, 0], rho=0.5)
+    assert (int(f["concordant"]), int(f["discordant"])) == (6, 0)
+    # all one value of S: no pair counts either way
+    f = _fit_one(o, [2.0, 2.0, 2.0], [1, 0, 1], rho=0.5)
+    assert (int(f["concordant"]), int(f["discordant"])) == (0, 0)
+    # only healthy windows
+    f = _fit_one(o, [1.0, 2.0, 3.0], [1, 1, 1], rho=0.5)
+    assert (int(f["concordant"]), int(f["discordant"])) == (0, 0)
+
+
 def pin_window_health_threshold(o):
     # 19 of 20 meet the bound: healthy at q = 0.95 (equality), not at 0.951
     S = np.array([[1.0]])
@@ -134,7 +158,10 @@ def _brute_fit(S, flags, judged, ok, q, rho):
         H = sum(1 for t, h in cand if t >= s and h)
         if H >= rho * N and s < best[0]:
             best = (s, N, H)
-    return best, len(cand), sum(1 for _, h in cand if h)
+    # every ordered pair of candidates with S_i > S_j, by the health of each
+    conc = sum(1 for si, hi in cand for sj, hj in cand if si > sj and hi and not hj)
+    disc = sum(1 for si, hi in cand for sj, hj in cand if si > sj and not hi and hj)
+    return best, len(cand), sum(1 for _, h in cand if h), (conc, disc)
 
 
 def pin_fit_matches_brute_force(o):
@@ -151,11 +178,13 @@ def pin_fit_matches_brute_force(o):
                     for _ in range(M)])
         fit = o.calib_fit(S, flags, judged, ok, slo)
         for m in range(M):
-            (th, N, H), nc, nh = _brute_fit(S[:, m], flags[:, m], judged[m].astype(float), ok[m].astype(float),
-                                            slo[m]["attain_q"], slo[m]["reliability"])
+            (th, N, H), nc, nh, (conc, disc) = _brute_fit(S[:, m], flags[:, m], judged[m].astype(float),
+                                                          ok[m].astype(float), slo[m]["attain_q"],
+                                                          slo[m]["reliability"])
             got = fit[m]
             assert (got["theta"], int(got["n_above"]), int(got["healthy_above"])) == (th, N, H), (it, m)
             assert (int(got["n_cand"]), int(got["n_healthy"])) == (nc, nh), (it, m)
+            assert (int(got["concordant"]), int(got["discordant"])) == (conc, disc), (it, m)
 
 
 def _numpy_join(ev, window_ms, nW, M, slo, req_cap):
@@ -304,7 +333,8 @@ def pin_bad_arguments_are_rejected(o):
         raise AssertionError(f"accepted window {args[0]} duration {args[1]}")
 
 
-ALL = [pin_hand_trace_latencies_and_attainment, pin_hand_fit_with_ties, pin_window_health_threshold,
+ALL = [pin_hand_trace_latencies_and_attainment, pin_hand_fit_with_ties, pin_hand_ordering_counts,
+       pin_window_health_threshold,
        pin_fit_matches_brute_force, pin_join_matches_numpy_on_generated_traces,
        pin_judged_requests_are_the_finished_ones, pin_special_cases, pin_monotone_in_reliability_and_bounds,
        pin_bad_arguments_are_rejected]

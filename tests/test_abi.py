@@ -46,7 +46,7 @@ def test_struct_layouts():
     assert ctypes.sizeof(tre._CtlOut) == 40
     assert ctypes.sizeof(tre._TssOut) == 56
     assert ctypes.sizeof(tre._Actuation) == 32
-    assert tre.SLO_DTYPE.itemsize == 40 and tre.FIT_DTYPE.itemsize == 24
+    assert tre.SLO_DTYPE.itemsize == 40 and tre.FIT_DTYPE.itemsize == 32
     assert tre.REQ_LATENCY_DTYPE.itemsize == 24
     assert tre.SERVICE_DTYPE.itemsize == 8 and tre.LOOP_STATS_DTYPE.itemsize == 32
     assert ctypes.sizeof(tre._LoopRequests) == 6 * 8 + 9 * 4 + 4  # padded to 8

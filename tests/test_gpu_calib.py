@@ -74,7 +74,13 @@ def _check(lib, name, cfg, traces, prof_cols, slo_cols, req_cap, check_traces=No
     S = tss["tss64"].cpu().numpy()
     fl = tss["flags"].cpu().numpy()
     counts = out["counts"].cpu().numpy().view(np.uint32)
+    fit0 = tre.unpack_fit(out["fit"]).reshape(len(traces), M).copy()
+    assert (fit0["concordant"] == 0).all() and (fit0["discordant"] == 0).all()
+    # the same fits with the ordering counts
+    tre.tre_calib_order(ev, slo, tss["tss64"], tss["flags"], out)
     fit = tre.unpack_fit(out["fit"]).reshape(len(traces), M)
+    for k in ("theta", "n_cand", "n_healthy", "n_above", "healthy_above"):
+        assert np.array_equal(np.ascontiguousarray(fit0[k]).view(np.uint8), np.ascontiguousarray(fit[k]).view(np.uint8)), f"{name}: {k} of the two fits"
     reqs = tre.unpack_reqs(out["reqs"]).reshape(len(traces), req_cap)
     o = O.get()
     bad_total = 0
@@ -98,7 +104,7 @@ def _check(lib, name, cfg, traces, prof_cols, slo_cols, req_cap, check_traces=No
         assert np.array_equal(counts[t] >> 16, r["judged"]), f"{what}: judged per window"
         assert np.array_equal(counts[t] & 0xFFFF, r["ok"]), f"{what}: ok per window"
         ref = o.calib_fit(S[t], fl[t], r["judged"], r["ok"], slo_t)
-        for k in ("n_cand", "n_healthy", "n_above", "healthy_above"):
+        for k in ("n_cand", "n_healthy", "n_above", "healthy_above", "concordant", "discordant"):
             assert np.array_equal(fit[t][k], ref[k]), f"{what}: fit {k} {fit[t][k]} vs {ref[k]}"
         assert np.array_equal(fit[t]["theta"].view(np.uint64), ref["theta"].view(np.uint64)), \
             f"{what}: theta {fit[t]['theta']} vs {ref['theta']}"
@@ -257,7 +263,11 @@ def _fit_cases(nW, seed):
             (base, rng.random(nW) < 0.9, 0.9),
             (rng.choice([1.0, 2.0, 3.5, 8.0], nW), rng.random(nW) < 0.7, 0.75),
             (np.where(rng.random(nW) < 0.02, 1e6, 5.0 + rng.random(nW) * 1e-9), rng.random(nW) < 0.9, 0.9),
-            (np.full(nW, 7.0), rng.random(nW) < 0.95, 0.9)]
+            (np.full(nW, 7.0), rng.random(nW) < 0.95, 0.9),
+            # health ordered by S with noise near the boundary: the buckets
+            # holding both kinds are few (their keys gathered for the
+            # ordering counts)
+            (base, base + rng.normal(0.0, 3.0, nW) > 40, 0.95)]
 
 
 @pytest.mark.parametrize("nW,seed", [(1000, 1), (1000, 2), (14400, 1), (14400, 2)])
@@ -295,15 +305,19 @@ def test_fit_paths_with_given_tss(lib, nW, seed):
     flags = torch.from_numpy(fl.reshape(1, nWe, M).copy()).cuda()
     out = tre.calib_outputs(ev, rid)
     tre.tre_calibrate(ev, slo, tss64, flags, out)
+    fit0 = tre.unpack_fit(out["fit"]).copy()
+    tre.tre_calib_order(ev, slo, tss64, flags, out)
     torch.cuda.synchronize()
     fit = tre.unpack_fit(out["fit"])
+    for k in ("theta", "n_cand", "n_healthy", "n_above", "healthy_above"):
+        assert np.array_equal(np.ascontiguousarray(fit0[k]).view(np.uint8), np.ascontiguousarray(fit[k]).view(np.uint8)), k
     o = O.get()
     slo_h = _slo_rows(slo_cols, 0, M)
     r = o.calib_requests(ev_h, win, cfg["duration_ms"], slo_h, rid)
     assert (r["judged"][:, :nW] == 1).all()
     ref = o.calib_fit(S, fl, r["judged"], r["ok"], slo_h)
     for m in range(M):
-        for k in ("n_cand", "n_healthy", "n_above", "healthy_above"):
+        for k in ("n_cand", "n_healthy", "n_above", "healthy_above", "concordant", "discordant"):
             assert fit[m][k] == ref[m][k], (m, k, fit[m], ref[m])
         assert fit[m]["theta"].view(np.uint64) == ref[m]["theta"].view(np.uint64), (m, fit[m], ref[m])
     say(f"nW {nW} seed {seed}: theta {fit['theta']}")

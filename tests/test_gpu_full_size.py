@@ -169,7 +169,11 @@ def test_stress_full_size_calibration():
     assert np.array_equal(runs[0][1], runs[1][1]), "fits differ between launches"
     assert runs[0][2] == 0
     counts = runs[0][0].view(np.uint32)
-    fit = runs[0][1].view(tre.FIT_DTYPE).reshape(T, M)
+    tre.tre_calib_order(ev, slo, tss["tss64"], tss["flags"], out)
+    fit = tre.unpack_fit(out["fit"]).reshape(T, M)
+    fit0 = runs[0][1].view(tre.FIT_DTYPE).reshape(T, M)
+    for k in ("theta", "n_cand", "n_healthy", "n_above", "healthy_above"):
+        assert np.array_equal(np.ascontiguousarray(fit0[k]).view(np.uint8), np.ascontiguousarray(fit[k]).view(np.uint8)), k
     rng = np.random.default_rng(17)
     sample = sorted({0, T - 1, *rng.integers(0, T, 4).tolist()})
     o = PT.O.get()
@@ -181,7 +185,7 @@ def test_stress_full_size_calibration():
                         dt.req_cap)
         assert np.array_equal(counts[t] >> 16, r["judged"]) and np.array_equal(counts[t] & 0xFFFF, r["ok"]), t
         assert np.array_equal(fit[t]["theta"].view(np.uint64), r["fit"]["theta"].view(np.uint64)), t
-        for k in ("n_cand", "n_healthy", "n_above", "healthy_above"):
+        for k in ("n_cand", "n_healthy", "n_above", "healthy_above", "concordant", "discordant"):
             assert np.array_equal(fit[t][k], r["fit"][k]), (t, k)
     say(f"{w.name}: calibration of {len(sample)} sampled traces matches the oracle")
     ev.close()

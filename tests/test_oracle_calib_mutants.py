@@ -37,6 +37,9 @@ MUTANTS = {
     "uninitialised_windows_are_candidates": ("if (j == 0 || !(fl & OC_INIT) || (fl & OC_IDLE)) continue;",
                                              "if (j == 0 || (fl & OC_IDLE)) continue;"),
     "n_above_off_by_one": ("best.n_above = N;", "best.n_above = N - 1;"),
+    "order_counts_swapped": ("best.concordant += (run_n - run_h) * H;", "best.discordant += (run_n - run_h) * H;"),
+    "order_counts_ties": ("best.discordant += run_h * (N - H);", "best.discordant += run_h * (N + run_n - H - run_h);"),
+    "order_counts_all_pairs": ("best.concordant += (run_n - run_h) * H;", "best.concordant += (run_n - run_h) * N;"),
 }
 
 
