@@ -275,7 +275,7 @@ def main():
     ev.close()
 
 
-CALIB_KERNELS = ("tss_stream", "calib_fill", "calib_join", "calib_judge", "calib_fit")
+CALIB_KERNELS = ("tss_stream", "calib_fill", "calib_stream", "calib_fallback", "calib_fit")
 
 
 def loop_main(args, w, tre, torch, np):
@@ -461,12 +461,12 @@ def calibrate_main(args, w, dt, device, tre, torch, np):
     """One step = tre_eval_tss writing the per-cell smoothed TSS and flags,
     then tre_calibrate (request join, SLO attainment, theta fit) over the
     whole resident workload. Algorithmic bytes per launch: tss_stream 12 per
-    event + 9 per cell written; calib_fill 16 per request slot + 4 per cell;
-    calib_join 7 per event (id 4, type 1, tokens 2); calib_judge 16 per
-    request slot + 35 per finished request (three timestamps, model, tokens
-    and its counter read and written: the join does this part for requests
-    whose events lie in one chunk, so the join's own figure is a lower
-    bound); calib_fit 13 per cell (counter, TSS, flags)."""
+    event + 9 per cell written; calib_fill 4 per cell (the counters zeroed);
+    calib_stream 16 per event (timestamp 8, request id 4, tokens 2, type 1,
+    model 1) + 8 per cell (each counter read and written back once);
+    calib_fallback 0 (the traces the stream could not finish, none on the
+    standard workloads: its launches end at once); calib_fit 13 per cell
+    (counter, TSS, flags)."""
     ev = device.load(dt, validate=True)
     prof = device.profiles(w)
     slo = device.slos(w)
@@ -503,14 +503,14 @@ def calibrate_main(args, w, dt, device, tre, torch, np):
     for k in CALIB_KERNELS:
         tot, n = tre.tre_kernel_time(k)
         kms[k] = tot / max(n, 1)
-    slots = T * dt.req_cap
     alg = {"tss_stream": ALG_BYTES_PER_EVENT * dt.n_events + 9 * cells,
-           "calib_fill": 16 * slots + 4 * cells,
-           "calib_join": 7 * dt.n_events,
-           "calib_judge": 16 * slots + 35 * dt.n_finish,
+           "calib_fill": 4 * cells,
+           "calib_stream": 16 * dt.n_events + 8 * cells,
+           "calib_fallback": 0,
            "calib_fit": 13 * cells}
     kernels = {k: {"ms": round(kms[k], 4), "alg_bytes": alg[k],
                    "gbs": round(alg[k] / (kms[k] / 1e3) / 1e9, 1) if kms[k] > 0 else None} for k in CALIB_KERNELS}
+    kernels["calib_fallback"]["traces"] = dict(zip(("larger_table", "chunked"), tre.calib_fallback_traces(ev, out)))
     calib_only = [k for k in CALIB_KERNELS if k != "tss_stream"]
     dom = max(calib_only, key=lambda k: kms[k])
     roofline = {"bound": "hbm", "achieved": kernels[dom]["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",

@@ -377,7 +377,8 @@ typedef struct {
   uint8_t pad[6];
 } tre_req_latency;                  /* 24 bytes */
 
-/* Workspace bytes of tre_calibrate: 16 per request slot and trace, plus 256. */
+/* Workspace bytes of tre_calibrate: 256, two lists of 4 + 4 * n_traces
+   bytes each rounded up to 256, and 16 per request slot and trace. */
 int tre_calib_workspace_size(const tre_events* ev, uint32_t req_cap, size_t* bytes);
 
 /* The calibration sweep over the handle's traces (device pointers):
@@ -388,7 +389,21 @@ int tre_calib_workspace_size(const tre_events* ev, uint32_t req_cap, size_t* byt
      fit     [n_traces][n_models];
      reqs    [n_traces][req_cap] per-request latencies, or NULL;
      n_bad_ids  one uint64: events whose id is >= req_cap, or NULL.
-   The handle needs its req column; at most 16384 windows (TRE_ERANGE).
+   The handle needs its req column; at most 16384 windows (TRE_ERANGE);
+   req_cap at most 2^31 (TRE_ERANGE).
+   Request lifecycle: per trace, a request id has at most one ARRIVE row
+   and at most one FINISH row, and no ARRIVE or DECODE row with a later
+   timestamp than its FINISH (rows of one instant may come in any order).
+   Events that break it give unspecified results, never an access out of
+   bounds.
+   Each trace is streamed once by one workgroup that keeps its requests in
+   flight in LDS. A trace with more requests in flight than that table
+   holds (or more than 256 FINISH rows at one instant) is redone with a
+   table twice as large, and a trace that overflows that one by request-id
+   records in the workspace; after the call completes, the uint32 at byte
+   256 of ws counts the traces redone with the larger table and the uint32
+   at byte 256 + (4 + 4 * n_traces rounded up to 256) those redone by
+   records (diagnostics; the results do not depend on the path).
    ws: 16-byte aligned device workspace of tre_calib_workspace_size bytes.
    Enqueued on `stream`. */
 int tre_calibrate(const tre_events* ev, const tre_slo* slo, const double* tss64,

@@ -47,12 +47,17 @@ using tre_internal::LaunchTimer;
 namespace {
 
 constexpr uint32_t kNone = 0xFFFFFFFFu;
-constexpr int kJoinChunk = 8192;    // events per calib_join workgroup
+constexpr int kJoinChunk = 8192;    // events per calib_join work item
 constexpr int kFitThreads = 1024;   // calib_fit workgroup
 constexpr int kFitWaves = kFitThreads / 64;
 constexpr int kFitMaxKPT = 16;      // keys per thread: windows up to 16384
 
 __device__ __forceinline__ uint64_t dbits(double x) { return (uint64_t)__double_as_longlong(x); }
+
+template <typename T>
+__device__ __forceinline__ T lds_load(const T& x) {
+  return __hip_atomic_load(&x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
 
 // ------------------------------------------------------------------- fill
 __global__ __launch_bounds__(256) void fill_u32(uint32_t* p, uint64_t n, uint32_t v) {
@@ -64,45 +69,30 @@ __global__ __launch_bounds__(256) void fill_u32(uint32_t* p, uint64_t n, uint32_
   for (uint64_t i = 4 * n4 + (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = v;
 }
 
-// ------------------------------------------------------------------- join
-struct JoinParams {
-  const int64_t* ts;
-  const uint8_t* model;
-  const uint32_t* req;
-  const uint8_t* type;
-  const uint16_t* tokens;
-  const int64_t* off;
-  const tre_slo* slo;           // [n_traces][M]
-  uint32_t* counts;             // [n_traces][M][n_windows]: judged << 16 | ok
-  tre_req_latency* reqs;        // [n_traces][req_cap] or NULL
-  uint32_t* tab;                // [n_traces][req_cap][4]: a, f, e, ~dsum
-  unsigned long long* n_bad;    // events whose id is >= req_cap
-  uint32_t n_traces;
-  uint32_t req_cap;
-  uint32_t n_chunks;            // chunks of the longest trace
-  int32_t M;
-  int64_t window_ms;
-  int64_t n_windows;
-};
-
-constexpr int kHashSlots = 2048;           // LDS records per chunk (load factor about 0.4)
-constexpr int kProbes = 16;                // linear probes before the global fallback
-constexpr int kJoinBatch = 8;              // events per thread loaded together
-constexpr uint32_t kDone = 0xFFFFFFFEu;    // record judged inside the join
+// request slots that no ARRIVE reaches: model 0xFF, no flags, zero latencies
+__global__ __launch_bounds__(256) void fill_unseen(tre_req_latency* r, uint64_t n) {
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    unsigned long long* w = (unsigned long long*)(r + i);
+    w[0] = 0ull;
+    w[1] = 0ull;
+    w[2] = 0xFFull;
+  }
+}
 
 // latencies and the SLO test of one judged request from its event times
 __device__ __forceinline__ tre_req_latency judge_one(int64_t ta, int64_t tf, int64_t te, uint32_t after_first,
-                                                     uint32_t m, const tre_slo& s) {
+                                                     uint32_t m, double ttft_ms, double tpot_ms, double e2e_ms) {
   tre_req_latency out;
   out.model = (uint8_t)m;
   out.flags = TRE_REQ_ARRIVED | TRE_REQ_COMPLETE;
   for (int i = 0; i < 6; ++i) out.pad[i] = 0;
   const int64_t ttft = tf - ta, e2e = te - ta;
-  bool good = (double)ttft <= s.ttft_ms && (double)e2e <= s.e2e_ms;
+  bool good = (double)ttft <= ttft_ms && (double)e2e <= e2e_ms;
   out.tpot_ms = 0.0;
   if (after_first > 0) {
     const double tpot = (double)(te - tf) / (double)after_first;
-    good = good && tpot <= s.tpot_ms;
+    good = good && tpot <= tpot_ms;
     out.tpot_ms = tpot;
     out.flags |= TRE_REQ_TPOT;
   }
@@ -122,165 +112,634 @@ __device__ __forceinline__ tre_req_latency not_judged(uint32_t m) {
   return out;
 }
 
-// One workgroup per chunk of kJoinChunk rows of one trace. The chunk's
-// events are first combined per request in an LDS hash table (minimum rows
-// of ARRIVE / DECODE / FINISH, DECODE token sum). A request whose ARRIVE,
-// DECODE and FINISH all fall in the chunk has every event in it (a
-// request's events lie between its ARRIVE and FINISH), so it is judged
-// right here and never touches the global table; the others merge into
-// their global records with atomics, for calib_judge. Chunks of one trace
-// are numbered onto one XCD.
-__global__ __launch_bounds__(256) void calib_join(JoinParams p) {
-  __shared__ uint32_t h_id[kHashSlots], h_a[kHashSlots], h_f[kHashSlots], h_e[kHashSlots], h_d[kHashSlots];
-  const uint32_t xcd = blockIdx.x & 7u, kk = blockIdx.x >> 3;
-  const uint32_t t = (kk / p.n_chunks) * 8u + xcd, chunk = kk % p.n_chunks;
-  if (t >= p.n_traces) return;  // whole block
-  const int64_t b = p.off[t], e = p.off[t + 1];
-  const int64_t c0 = b + (int64_t)chunk * kJoinChunk;
-  if (c0 >= e) return;  // whole block
-  const int64_t c1 = c0 + kJoinChunk < e ? c0 + kJoinChunk : e;
-  uint32_t* tt = p.tab + (uint64_t)t * p.req_cap * 4;
-  for (int i = threadIdx.x; i < kHashSlots; i += 256) {
-    h_id[i] = kNone;
-    h_a[i] = kNone;
-    h_f[i] = kNone;
-    h_e[i] = kNone;
-    h_d[i] = 0;
-  }
-  __syncthreads();
-  unsigned bad = 0;
-  for (int64_t i0 = c0 + threadIdx.x; i0 < c1; i0 += 256 * kJoinBatch) {
-    uint32_t rr[kJoinBatch], kt[kJoinBatch], tk[kJoinBatch];
-#pragma unroll
-    for (int u = 0; u < kJoinBatch; ++u) {
-      const int64_t i = i0 + 256 * u;
-      const bool in = i < c1;
-      rr[u] = in ? p.req[i] : kNone;
-      kt[u] = in ? p.type[i] : TRE_PREFILL;
-      tk[u] = in ? p.tokens[i] : 0u;
-    }
-#pragma unroll
-    for (int u = 0; u < kJoinBatch; ++u) {
-      const int64_t i = i0 + 256 * u;
-      if (i >= c1) continue;
-      const uint32_t r = rr[u];
-      if (r >= p.req_cap) {
-        ++bad;
-        continue;
-      }
-      const uint32_t k = kt[u] & 3u;
-      if (k == TRE_PREFILL) continue;
-      const uint32_t row = (uint32_t)(i - b);
-      uint32_t h = (r * 0x9E3779B1u) >> (32 - 11);
-      int slot = -1;
-      for (int q = 0; q < kProbes; ++q) {
-        const uint32_t old = atomicCAS(&h_id[h], kNone, r);
-        if (old == kNone || old == r) {
-          slot = (int)h;
-          break;
-        }
-        h = (h + 1) & (kHashSlots - 1);
-      }
-      if (slot >= 0) {
-        if (k == TRE_ARRIVE) {
-          atomicMin(&h_a[slot], row);
-        } else if (k == TRE_DECODE) {
-          atomicMin(&h_f[slot], row);
-          atomicAdd(&h_d[slot], tk[u]);
-        } else {
-          atomicMin(&h_e[slot], row);
-        }
-      } else {  // table crowded: straight to the global record
-        uint32_t* rec = tt + (uint64_t)r * 4;
-        if (k == TRE_ARRIVE) {
-          atomicMin(rec, row);
-        } else if (k == TRE_DECODE) {
-          atomicMin(rec + 1, row);
-          atomicSub(rec + 3, tk[u]);
-        } else {
-          atomicMin(rec + 2, row);
-        }
-      }
-    }
-  }
-  __syncthreads();
-  for (int s = threadIdx.x; s < kHashSlots; s += 256) {
-    const uint32_t r = h_id[s];
-    if (r == kNone) continue;
-    uint32_t* rec = tt + (uint64_t)r * 4;
-    const uint32_t a = h_a[s], f = h_f[s], fin = h_e[s], d = h_d[s];
-    if (a != kNone && f != kNone && fin != kNone) {
-      const uint32_t m = p.model[b + a];
-      tre_req_latency out;
-      if (m < (uint32_t)p.M) {
-        const int64_t ta = p.ts[b + a];
-        out = judge_one(ta, p.ts[b + f], p.ts[b + fin], d - (uint32_t)p.tokens[b + f], m,
-                        p.slo[(uint64_t)t * p.M + m]);
-        const int64_t w = ta / p.window_ms;  // window of arrival
-        if (w >= 0 && w < p.n_windows)
-          atomicAdd(p.counts + ((uint64_t)t * p.M + m) * p.n_windows + w,
-                    (1u << 16) | ((out.flags & TRE_REQ_OK) ? 1u : 0u));
-      } else {
-        out = not_judged(m);
-      }
-      if (p.reqs) {
-        p.reqs[(uint64_t)t * p.req_cap + r] = out;
-        rec[0] = kDone;  // calib_judge leaves this slot alone
-      }
-      continue;
-    }
-    if (a != kNone) atomicMin(rec, a);
-    if (f != kNone) {
-      atomicMin(rec + 1, f);
-      atomicSub(rec + 3, d);
-    }
-    if (fin != kNone) atomicMin(rec + 2, fin);
-  }
-  // one atomic per wave for the ids out of range
-  for (int o = 32; o > 0; o >>= 1) bad += __shfl_xor(bad, o);
-  if ((threadIdx.x & 63) == 0 && bad) atomicAdd(p.n_bad, (unsigned long long)bad);
+// ----------------------------------------------------------------- stream
+typedef unsigned int v4u32 __attribute__((ext_vector_type(4)));
+typedef unsigned int v2u32 __attribute__((ext_vector_type(2)));
+
+constexpr int kStreamRows = 4;         // consecutive rows per thread and tile
+constexpr int kMaxBuckets = 32;        // buckets of one probe run
+constexpr int kDeferCap = 256;         // FINISH rows at the last instant of one tile
+constexpr uint32_t kTomb = 0xFFFFFFFEu;  // record of a judged request
+constexpr unsigned long long kNone64 = ~0ull;
+// the two table sizes, in buckets of four records (a prime count, so that
+// every probe step reaches every bucket): 887 buckets (two workgroups per
+// CU) for every trace, 1789 (one per CU) for the traces that overflow the
+// first
+constexpr int kBuckets1 = 887, kThreads1 = 512;
+constexpr int kBuckets2 = 1789, kThreads2 = 1024;
+
+// murmur3's 32-bit finalizer: request ids are often arithmetic sequences,
+// which a multiplicative hash alone maps to correlated buckets
+__device__ __forceinline__ uint32_t mix32(uint32_t h) {
+  h ^= h >> 16;
+  h *= 0x85EBCA6Bu;
+  h ^= h >> 13;
+  h *= 0xC2B2AE35u;
+  h ^= h >> 16;
+  return h;
 }
 
-// ------------------------------------------------------------------ judge
-struct JudgeParams {
+struct StreamParams {
   const int64_t* ts;
   const uint8_t* model;
+  const uint32_t* req;
+  const uint8_t* type;
   const uint16_t* tokens;
   const int64_t* off;
-  const uint32_t* tab;
-  const tre_slo* slo;           // [n_traces][M]
-  uint32_t* counts;             // [n_traces][M][n_windows]: judged << 16 | ok
-  tre_req_latency* reqs;        // [n_traces][req_cap] or NULL
-  uint32_t n_traces;
+  const tre_slo* slo;            // [n_traces][M]
+  uint32_t* counts;              // [n_traces][M][n_windows]: judged << 16 | ok
+  tre_req_latency* reqs;         // [n_traces][req_cap] or NULL
+  unsigned long long* n_bad;     // events whose id is >= req_cap
+  const uint32_t* list_in;       // NULL: workgroup i takes trace i; else [0]: count, [1 + i]: trace
+  uint32_t* list_out;            // [0]: traces that overflowed, [1 + i]: their indices
   uint32_t req_cap;
   int32_t M;
   int64_t window_ms;
   int64_t n_windows;
 };
 
-// The requests the join could not finish: one thread per request slot.
-__global__ __launch_bounds__(256) void calib_judge(JudgeParams p) {
-  const uint32_t r = blockIdx.x * 256 + threadIdx.x;
-  if (r >= p.req_cap) return;
-  for (uint32_t t = blockIdx.y; t < p.n_traces; t += gridDim.y) {
+struct StreamRsrc {
+  __amdgpu_buffer_rsrc_t ts, model, req, type, tokens;
+};
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t col_rsrc(const void* base, long long bytes) {
+  const long long n = (bytes + 15) & ~15ll;  // columns stay readable 16 bytes past the last row
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n, 0x00020000);
+}
+
+// one thread's four consecutive rows of a tile
+struct StreamRows {
+  uint32_t req[kStreamRows];
+  uint32_t ts[kStreamRows];  // low words: timestamps lie in [0, duration) below 2^32
+  uint32_t ty, mdl;          // one byte per row
+  uint32_t tok[2];           // two 16-bit token counts per word
+};
+
+__device__ __forceinline__ void load_rows(StreamRows& s, const StreamRsrc& rs, int r0) {
+  const v4u32 t0 = __builtin_bit_cast(v4u32, __builtin_amdgcn_raw_buffer_load_b128(rs.ts, r0 * 8, 0, 0));
+  const v4u32 t1 = __builtin_bit_cast(v4u32, __builtin_amdgcn_raw_buffer_load_b128(rs.ts, r0 * 8 + 16, 0, 0));
+  const v4u32 q = __builtin_bit_cast(v4u32, __builtin_amdgcn_raw_buffer_load_b128(rs.req, r0 * 4, 0, 0));
+  const v2u32 k = __builtin_bit_cast(v2u32, __builtin_amdgcn_raw_buffer_load_b64(rs.tokens, r0 * 2, 0, 0));
+  s.ty = __builtin_amdgcn_raw_buffer_load_b32(rs.type, r0, 0, 0);
+  s.mdl = __builtin_amdgcn_raw_buffer_load_b32(rs.model, r0, 0, 0);
+  s.ts[0] = t0.x;
+  s.ts[1] = t0.z;
+  s.ts[2] = t1.x;
+  s.ts[3] = t1.z;
+  s.req[0] = q.x;
+  s.req[1] = q.y;
+  s.req[2] = q.z;
+  s.req[3] = q.w;
+  s.tok[0] = k.x;
+  s.tok[1] = k.y;
+}
+
+__device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// One workgroup streams one whole trace in tiles of 4 rows per thread,
+// keeping the records of the requests in flight in an LDS hash table keyed
+// by request id: kBuckets buckets of four ids, probed by double hashing from
+// the id's mixed hash (one 16-byte read per bucket). A record holds the
+// ARRIVE's timestamp and model, the first DECODE as a (row << 32 |
+// timestamp) minimum, and the DECODE tokens after the first one. Callers
+// guarantee that a request has at most one ARRIVE and one FINISH, and no
+// ARRIVE or DECODE row at a later timestamp than its FINISH; rows of one
+// instant may come in any order, so a FINISH at the last instant of a tile
+// is judged after the next tile. Per tile:
+//   phase 1  every ARRIVE / DECODE / FINISH row finds or inserts its
+//            record, in rounds that each read one bucket and issue one
+//            claim (CAS on the bucket's first empty slot) per pending row,
+//            then folds its row in: the ARRIVE stores its timestamp and
+//            model, a DECODE adds its tokens and offers its key to the
+//            first-DECODE minimum;
+//   phase 2  the first DECODE takes its own tokens back out of the sum;
+//            FINISH rows are queued (or deferred to the next tile);
+//   phase 3  the queue is judged, one FINISH per thread (one atomic add on
+//            the arrival window's counter), and the slots retired; rows the
+//            queue had no room for are judged by their own threads. This
+//            overlaps phase 1 of the next tile, which touches other records.
+// Retired slots stay occupied until a rebuild re-inserts the live records
+// (when more than two thirds of the slots are in use). A trace whose table
+// overflows (a probe run past kMaxBuckets, more than three quarters of the
+// slots live after a rebuild, more than kDeferCap FINISH rows at a tile's
+// last instant, an instant longer than a tile) stops and is listed for the
+// next tier, which redoes it from scratch.
+template <int kBuckets, int kStreamThreads>
+__global__ __launch_bounds__(kStreamThreads) void calib_stream(StreamParams p) {
+  constexpr int kSlots = 4 * kBuckets;
+  constexpr int kStreamTile = kStreamThreads * kStreamRows;
+  constexpr int kSlotsPerThread = (kSlots + kStreamThreads - 1) / kStreamThreads;
+  constexpr uint32_t kRebuildAt = 2 * kSlots / 3;  // slots in use (live or retired) that trigger a rebuild
+  constexpr uint32_t kMaxLive = 3 * kSlots / 4;    // live records a rebuild may leave
+  constexpr uint32_t kQueue = kStreamTile * 3 / 16;  // FINISH rows judged per tile
+  __shared__ __align__(16) uint32_t h_id[kSlots];
+  __shared__ unsigned long long h_f[kSlots];  // first DECODE: row << 32 | timestamp
+  __shared__ uint32_t h_ta[kSlots];           // ARRIVE timestamp, kNone before it
+  __shared__ uint32_t h_d[kSlots];            // DECODE tokens after the first DECODE
+  __shared__ uint8_t h_m[kSlots];             // model of the ARRIVE
+  // FINISH rows of tile k: queued (slot, timestamp) in s_q, counted in
+  // s_nq[k % 2]; those at its last instant deferred (ids) to s_def[k % 3].
+  // Each count is reset in the phase 2 before the one that fills it, after
+  // the phase 3 that last read it.
+  __shared__ uint2 s_q[kQueue];
+  __shared__ uint32_t s_def[3][kDeferCap];
+  __shared__ uint32_t s_ndef[3], s_nq[2];
+  __shared__ uint32_t s_occ, s_over, s_tl;
+  const int tid = threadIdx.x, lane = tid & 63;
+  if (p.list_in && blockIdx.x >= p.list_in[0]) return;  // whole block
+  const uint32_t t = p.list_in ? p.list_in[1 + blockIdx.x] : blockIdx.x;
+  const int64_t b = p.off[t], e = p.off[t + 1];
+  auto clear_slot = [&](int s) {
+    h_id[s] = kNone;
+    h_f[s] = kNone64;
+    h_ta[s] = kNone;
+    h_d[s] = 0u;
+    h_m[s] = 0;
+  };
+  for (int s = tid; s < kSlots; s += kStreamThreads) clear_slot(s);
+  if (tid == 0) {
+    s_ndef[0] = s_ndef[1] = s_ndef[2] = 0u;
+    s_nq[0] = s_nq[1] = 0u;
+    s_occ = 0u;
+    s_over = 0u;
+  }
+  __syncthreads();
+  // rows are counted from the trace's first 4-aligned row (below 2^27)
+  const long long brow = b & ~3ll;
+  const int rend = (int)(e - brow), rfirst = (int)(b - brow);
+  StreamRsrc rs;
+  rs.ts = col_rsrc(p.ts + brow, (long long)rend * 8);
+  rs.model = col_rsrc(p.model + brow, rend);
+  rs.req = col_rsrc(p.req + brow, (long long)rend * 4);
+  rs.type = col_rsrc(p.type + brow, rend);
+  rs.tokens = col_rsrc(p.tokens + brow, (long long)rend * 2);
+  uint32_t* cnt = p.counts + (uint64_t)t * p.M * p.n_windows;
+  const tre_slo* slo = p.slo + (uint64_t)t * p.M;
+  tre_req_latency* rq = p.reqs ? p.reqs + (uint64_t)t * p.req_cap : nullptr;
+  const uint32_t M = (uint32_t)p.M;
+
+  // first bucket and probe step (1 .. kBuckets - 1) of an id's mixed hash
+  auto home = [](uint32_t h) { return (uint32_t)(((unsigned long long)h * kBuckets) >> 32); };
+  auto stride = [](uint32_t h) { return 1u + (((h & 0xFFFFu) * (uint32_t)(kBuckets - 1)) >> 16); };
+  auto next = [](uint32_t bk, uint32_t st) { return bk + st >= (uint32_t)kBuckets ? bk + st - kBuckets : bk + st; };
+  // a bucket's four ids in one LDS read; a value may be stale by the time
+  // it is used, which the claim protocol tolerates: a slot seen empty is
+  // claimed by CAS, a slot once taken stays taken (until a rebuild), so an
+  // id present lies before every empty slot of its probe order
+  auto bucket_ids = [&](uint32_t bk) { return *(const v4u32*)&h_id[4 * bk]; };
+  auto mask_of = [](v4u32 v, uint32_t x) {
+    return (v.x == x ? 1u : 0u) | (v.y == x ? 2u : 0u) | (v.z == x ? 4u : 0u) | (v.w == x ? 8u : 0u);
+  };
+  // the records of up to kN ids (`want` bit u: ids[u] wanted), found or
+  // inserted in rounds; slot[u] = -1 when a probe run ends first
+  auto find_or_insert = [&](auto& ids, auto& slot, uint32_t want, uint32_t& inserted) {
+    constexpr int kN = sizeof(slot) / sizeof(slot[0]);
+    uint32_t bkt[kN], st[kN];
+    uint8_t probes[kN];
+#pragma unroll
+    for (int u = 0; u < kN; ++u) {
+      slot[u] = -1;
+      const uint32_t h = mix32(ids[u]);
+      bkt[u] = home(h);
+      st[u] = stride(h);
+      probes[u] = 0;
+    }
+    while (want) {
+      v4u32 v[kN];
+      int claim[kN];
+      uint32_t old[kN];
+#pragma unroll
+      for (int u = 0; u < kN; ++u)
+        if (want >> u & 1u) v[u] = bucket_ids(bkt[u]);
+#pragma unroll
+      for (int u = 0; u < kN; ++u) {
+        claim[u] = -1;
+        if (!(want >> u & 1u)) continue;
+        const uint32_t eq = mask_of(v[u], ids[u]), em = mask_of(v[u], kNone);
+        if (eq) {
+          slot[u] = (int)(4 * bkt[u] + __builtin_ctz(eq));
+          want &= ~(1u << u);
+        } else if (em) {
+          claim[u] = (int)(4 * bkt[u] + __builtin_ctz(em));
+        } else if (++probes[u] >= kMaxBuckets) {
+          want &= ~(1u << u);  // probe run ended: slot stays -1
+        } else {
+          bkt[u] = next(bkt[u], st[u]);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kN; ++u)
+        if (claim[u] >= 0) old[u] = atomicCAS(&h_id[claim[u]], kNone, ids[u]);
+#pragma unroll
+      for (int u = 0; u < kN; ++u) {
+        // a lost claim reads its bucket again next round
+        if (claim[u] < 0 || (old[u] != kNone && old[u] != ids[u])) continue;
+        slot[u] = claim[u];
+        want &= ~(1u << u);
+        if (old[u] == kNone) ++inserted;
+      }
+    }
+  };
+  auto find = [&](uint32_t r) -> int {
+    const uint32_t h = mix32(r), st = stride(h);
+    uint32_t bk = home(h);
+    for (int q = 0; q < kMaxBuckets; ++q) {
+      const v4u32 v = bucket_ids(bk);
+      const uint32_t eq = mask_of(v, r);
+      if (eq) return (int)(4 * bk + __builtin_ctz(eq));
+      if (mask_of(v, kNone)) return -1;
+      bk = next(bk, st);
+    }
+    return -1;
+  };
+  // judge the request of slot s, finished at te, and retire the slot
+  auto judge = [&](int s, uint32_t te) {
+    const uint32_t r = h_id[s], ta = h_ta[s];
+    if (ta != kNone) {
+      const uint32_t m = h_m[s];
+      const unsigned long long f = h_f[s];
+      tre_req_latency out;
+      if (f != kNone64 && m < M) {
+        const tre_slo& q = slo[m];
+        out = judge_one((int64_t)ta, (int64_t)(uint32_t)f, (int64_t)te, h_d[s], m, q.ttft_ms, q.tpot_ms, q.e2e_ms);
+        const int64_t w = (int64_t)ta / p.window_ms;  // window of arrival
+        if (w < p.n_windows)
+          atomicAdd(cnt + (uint64_t)m * p.n_windows + w, (1u << 16) | ((out.flags & TRE_REQ_OK) ? 1u : 0u));
+      } else {
+        out = not_judged(m);
+      }
+      if (rq) rq[r] = out;
+    }
+    __hip_atomic_store(&h_id[s], kTomb, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  };
+  auto set_over = [&]() { __hip_atomic_store(&s_over, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP); };
+
+  unsigned bad = 0;
+  bool over = false;
+  uint32_t tl_prev = 0;
+  StreamRows cur, nxt;
+  if (rend > 0) load_rows(cur, rs, tid * kStreamRows);
+  int k = 0;
+  for (int tb = 0; tb < rend; tb += kStreamTile, ++k) {
+    const bool last = tb + kStreamTile >= rend;
+    // the next tile's loads, always issued (rows past the trace read zeros)
+    // so that the waits for this tile's rows can count them
+    load_rows(nxt, rs, tb + kStreamTile + tid * kStreamRows);
+    const int r0 = tb + tid * kStreamRows;
+    // the tile's last instant, from the thread holding its last row (read
+    // after the next barrier)
+    {
+      const int lrow = (last ? rend : tb + kStreamTile) - 1;
+#pragma unroll
+      for (int u = 0; u < kStreamRows; ++u)
+        if (r0 + u == lrow) s_tl = cur.ts[u];
+    }
+    // ---- phase 1
+    int slot[kStreamRows];
+    uint32_t want = 0, inserted = 0;
+#pragma unroll
+    for (int u = 0; u < kStreamRows; ++u) {
+      const int row = r0 + u;
+      const uint32_t kind = (cur.ty >> (8 * u)) & 3u;
+      const bool in = row >= rfirst && row < rend;
+      if (in && cur.req[u] >= p.req_cap) ++bad;
+      if (in && cur.req[u] < p.req_cap && kind != TRE_PREFILL) want |= 1u << u;
+    }
+    const uint32_t wanted = want;
+    find_or_insert(cur.req, slot, want, inserted);
+#pragma unroll
+    for (int u = 0; u < kStreamRows; ++u) {
+      const int s = slot[u];
+      if (s < 0) {
+        if (wanted >> u & 1u) set_over();
+        continue;
+      }
+      const uint32_t kind = (cur.ty >> (8 * u)) & 3u;
+      if (kind == TRE_ARRIVE) {
+        h_ta[s] = cur.ts[u];
+        h_m[s] = (uint8_t)(cur.mdl >> (8 * u));
+      } else if (kind == TRE_DECODE) {
+        atomicAdd(&h_d[s], (cur.tok[u >> 1] >> (16 * (u & 1))) & 0xFFFFu);
+        atomicMin(&h_f[s], ((unsigned long long)(uint32_t)(r0 + u) << 32) | cur.ts[u]);
+      }
+    }
+    inserted = wave_sum(inserted);
+    if (lane == 0 && inserted) atomicAdd(&s_occ, inserted);
+    __syncthreads();
+    // ---- phase 2 (the flags are settled: nothing writes them before the
+    // next barrier)
+    const uint32_t occ = lds_load(s_occ), tl = lds_load(s_tl);
+    if (lds_load(s_over)) {
+      over = true;
+      break;
+    }
+    const int kd = k % 3;
+    uint32_t own = 0;  // FINISH rows the queue had no room for
+    if (tid == 0) {
+      s_ndef[(k + 1) % 3] = 0u;
+      s_nq[(k + 1) & 1] = 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < kStreamRows; ++u) {
+      const int s = slot[u];
+      const uint32_t kind = (cur.ty >> (8 * u)) & 3u;
+      if (s >= 0 && kind == TRE_DECODE && (uint32_t)(h_f[s] >> 32) == (uint32_t)(r0 + u))
+        atomicSub(&h_d[s], (cur.tok[u >> 1] >> (16 * (u & 1))) & 0xFFFFu);
+      const bool fin = s >= 0 && kind == TRE_FINISH;
+      const bool defer = fin && !last && cur.ts[u] == tl;
+      if (defer) {
+        const uint32_t i = atomicAdd(&s_ndef[kd], 1u);
+        if (i < (uint32_t)kDeferCap) s_def[kd][i] = cur.req[u];
+        else set_over();
+      }
+      // queue the others, one LDS atomic per wave
+      const unsigned long long mq = __ballot(fin && !defer);
+      if (mq) {
+        const int lead = __ffsll((long long)mq) - 1;
+        uint32_t base = 0;
+        if (lane == lead) base = atomicAdd(&s_nq[k & 1], (uint32_t)__popcll(mq));
+        base = __shfl(base, lead);
+        if (fin && !defer) {
+          const uint32_t i = base + (uint32_t)__popcll(mq & ((1ull << lane) - 1ull));
+          if (i < kQueue) s_q[i] = make_uint2((uint32_t)s, cur.ts[u]);
+          else own |= 1u << u;
+        }
+      }
+    }
+    __syncthreads();
+    // ---- phase 3: the queue, then the previous tile's deferred FINISH rows
+    // once their instant has ended (this tile reaches a later one, or the
+    // trace ends)
+    {
+      const uint32_t n = lds_load(s_nq[k & 1]), nq = n < kQueue ? n : kQueue;
+      for (uint32_t i = tid; i < nq; i += kStreamThreads) {
+        const uint2 q = s_q[i];
+        judge((int)q.x, q.y);
+      }
+      if (own) {
+#pragma unroll
+        for (int u = 0; u < kStreamRows; ++u)
+          if (own >> u & 1u) judge(slot[u], cur.ts[u]);
+      }
+    }
+    if (k > 0) {
+      const int kp = (k + 2) % 3;  // tile k - 1
+      const uint32_t nd = s_ndef[kp];
+      if (nd > 0u) {
+        if (tl > tl_prev || last) {
+          for (uint32_t i = tid; i < nd; i += kStreamThreads) {
+            const int s = find(s_def[kp][i]);
+            if (s >= 0) judge(s, tl_prev);
+          }
+        } else if (tid == 0) {
+          s_over = 1u;  // one instant longer than a tile
+        }
+      }
+    }
+    if (occ > kRebuildAt) {
+      // ---- rebuild: re-insert the live records into a cleared table
+      __syncthreads();
+      uint32_t rid[kSlotsPerThread], rta[kSlotsPerThread], rd[kSlotsPerThread];
+      unsigned long long rf[kSlotsPerThread];
+      uint8_t rm[kSlotsPerThread];
+      uint32_t live = 0;
+#pragma unroll
+      for (int j = 0; j < kSlotsPerThread; ++j) {
+        const int s = tid + j * kStreamThreads;
+        rid[j] = kTomb;
+        if (s >= kSlots) continue;
+        rid[j] = h_id[s];
+        rta[j] = h_ta[s];
+        rf[j] = h_f[s];
+        rd[j] = h_d[s];
+        rm[j] = h_m[s];
+        if (rid[j] < kTomb) live |= 1u << j;
+      }
+      __syncthreads();
+#pragma unroll
+      for (int j = 0; j < kSlotsPerThread; ++j)
+        if (tid + j * kStreamThreads < kSlots) clear_slot(tid + j * kStreamThreads);
+      if (tid == 0) s_occ = 0u;
+      __syncthreads();
+      uint32_t again = 0;
+#pragma unroll
+      for (int j = 0; j < kSlotsPerThread; ++j) {
+        // one record at a time keeps the registers of the saved ones few
+        uint32_t id1[1] = {rid[j]};
+        int s1[1];
+        find_or_insert(id1, s1, live >> j & 1u, again);
+        if (!(live >> j & 1u)) continue;
+        const int s = s1[0];
+        if (s < 0) {
+          set_over();
+          continue;
+        }
+        h_ta[s] = rta[j];
+        h_f[s] = rf[j];
+        h_d[s] = rd[j];
+        h_m[s] = rm[j];
+      }
+      again = wave_sum(again);
+      if (lane == 0 && again) atomicAdd(&s_occ, again);
+      __syncthreads();
+      if (tid == 0 && lds_load(s_occ) > kMaxLive) s_over = 1u;
+    }
+    tl_prev = tl;
+    cur = nxt;
+  }
+  if (over) {
+    // the next tier redoes the whole trace (its counters, request slots and
+    // ids out of range included)
+    if (tid == 0) {
+      const uint32_t i = atomicAdd(p.list_out, 1u);
+      p.list_out[1 + i] = t;
+    }
+    return;
+  }
+  __syncthreads();
+  // requests still in flight at the end: arrived, not judged
+  if (rq) {
+    for (int s = tid; s < kSlots; s += kStreamThreads) {
+      const uint32_t r = h_id[s];
+      if (r < kTomb && h_ta[s] != kNone) rq[r] = not_judged(h_m[s]);
+    }
+  }
+  bad = wave_sum(bad);
+  if (lane == 0 && bad) atomicAdd(p.n_bad, (unsigned long long)bad);
+}
+
+// --------------------------------------------------------------- fallback
+// The traces both stream tiers handed over, redone by request-id records in
+// the workspace: fb_reset clears their counters, request slots and (for the
+// chunked path) records;
+// calib_join combines each chunk's events per request in LDS and merges them
+// into the 16-byte records with atomics (minimum ARRIVE / DECODE / FINISH
+// rows, complemented DECODE token sum); calib_judge judges every record.
+// This path takes the definition literally and assumes nothing about where
+// a request's rows lie.
+struct FallbackParams {
+  const int64_t* ts;
+  const uint8_t* model;
+  const uint32_t* req;
+  const uint8_t* type;
+  const uint16_t* tokens;
+  const int64_t* off;
+  const tre_slo* slo;           // [n_traces][M]
+  uint32_t* counts;             // [n_traces][M][n_windows]: judged << 16 | ok
+  tre_req_latency* reqs;        // [n_traces][req_cap] or NULL
+  uint32_t* tab;                // [n_traces][req_cap][4]: a, f, e, ~dsum, or NULL (fb_reset only)
+  unsigned long long* n_bad;    // events whose id is >= req_cap
+  const uint32_t* fb;           // [0]: listed traces, [1 + i]: their indices
+  uint32_t req_cap;
+  uint32_t n_chunks;            // chunks of the longest trace
+  int32_t M;
+  int64_t window_ms;
+  int64_t n_windows;
+};
+
+__global__ __launch_bounds__(256) void fb_reset(FallbackParams p) {
+  const uint32_t n_list = p.fb[0];
+  const uint64_t cw = (uint64_t)p.M * p.n_windows, tw = (uint64_t)p.req_cap * 4;
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  for (uint32_t pos = blockIdx.y; pos < n_list; pos += gridDim.y) {
+    const uint32_t t = p.fb[1 + pos];
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < cw; i += stride)
+      p.counts[(uint64_t)t * cw + i] = 0u;
+    if (p.tab)
+      for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < tw; i += stride)
+        p.tab[(uint64_t)t * tw + i] = kNone;
+    if (p.reqs) {
+      for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < p.req_cap; i += stride) {
+        unsigned long long* w = (unsigned long long*)(p.reqs + (uint64_t)t * p.req_cap + i);
+        w[0] = 0ull;
+        w[1] = 0ull;
+        w[2] = 0xFFull;
+      }
+    }
+  }
+}
+
+constexpr int kHashSlots = 2048;           // LDS records per chunk (load factor about 0.4)
+constexpr int kProbes = 16;                // linear probes before the global fallback
+constexpr int kJoinBatch = 8;              // events per thread loaded together
+
+// Work items (listed trace, chunk of kJoinChunk rows), one per workgroup at
+// a time.
+__global__ __launch_bounds__(256) void calib_join(FallbackParams p) {
+  __shared__ uint32_t h_id[kHashSlots], h_a[kHashSlots], h_f[kHashSlots], h_e[kHashSlots], h_d[kHashSlots];
+  const uint64_t items = (uint64_t)p.fb[0] * p.n_chunks;
+  unsigned bad = 0;
+  for (uint64_t it = blockIdx.x; it < items; it += gridDim.x) {
+    const uint32_t t = p.fb[1 + it / p.n_chunks], chunk = (uint32_t)(it % p.n_chunks);
+    const int64_t b = p.off[t], e = p.off[t + 1];
+    const int64_t c0 = b + (int64_t)chunk * kJoinChunk;
+    if (c0 >= e) continue;  // whole block
+    const int64_t c1 = c0 + kJoinChunk < e ? c0 + kJoinChunk : e;
+    uint32_t* tt = p.tab + (uint64_t)t * p.req_cap * 4;
+    for (int i = threadIdx.x; i < kHashSlots; i += 256) {
+      h_id[i] = kNone;
+      h_a[i] = kNone;
+      h_f[i] = kNone;
+      h_e[i] = kNone;
+      h_d[i] = 0;
+    }
+    __syncthreads();
+    for (int64_t i0 = c0 + threadIdx.x; i0 < c1; i0 += 256 * kJoinBatch) {
+      uint32_t rr[kJoinBatch], kt[kJoinBatch], tk[kJoinBatch];
+#pragma unroll
+      for (int u = 0; u < kJoinBatch; ++u) {
+        const int64_t i = i0 + 256 * u;
+        const bool in = i < c1;
+        rr[u] = in ? p.req[i] : kNone;
+        kt[u] = in ? p.type[i] : TRE_PREFILL;
+        tk[u] = in ? p.tokens[i] : 0u;
+      }
+#pragma unroll
+      for (int u = 0; u < kJoinBatch; ++u) {
+        const int64_t i = i0 + 256 * u;
+        if (i >= c1) continue;
+        const uint32_t r = rr[u];
+        if (r >= p.req_cap) {
+          ++bad;
+          continue;
+        }
+        const uint32_t k = kt[u] & 3u;
+        if (k == TRE_PREFILL) continue;
+        const uint32_t row = (uint32_t)(i - b);
+        uint32_t h = (r * 0x9E3779B1u) >> (32 - 11);
+        int slot = -1;
+        for (int q = 0; q < kProbes; ++q) {
+          const uint32_t old = atomicCAS(&h_id[h], kNone, r);
+          if (old == kNone || old == r) {
+            slot = (int)h;
+            break;
+          }
+          h = (h + 1) & (kHashSlots - 1);
+        }
+        if (slot >= 0) {
+          if (k == TRE_ARRIVE) {
+            atomicMin(&h_a[slot], row);
+          } else if (k == TRE_DECODE) {
+            atomicMin(&h_f[slot], row);
+            atomicAdd(&h_d[slot], tk[u]);
+          } else {
+            atomicMin(&h_e[slot], row);
+          }
+        } else {  // table crowded: straight to the global record
+          uint32_t* rec = tt + (uint64_t)r * 4;
+          if (k == TRE_ARRIVE) {
+            atomicMin(rec, row);
+          } else if (k == TRE_DECODE) {
+            atomicMin(rec + 1, row);
+            atomicSub(rec + 3, tk[u]);
+          } else {
+            atomicMin(rec + 2, row);
+          }
+        }
+      }
+    }
+    __syncthreads();
+    for (int s = threadIdx.x; s < kHashSlots; s += 256) {
+      const uint32_t r = h_id[s];
+      if (r == kNone) continue;
+      uint32_t* rec = tt + (uint64_t)r * 4;
+      if (h_a[s] != kNone) atomicMin(rec, h_a[s]);
+      if (h_f[s] != kNone) {
+        atomicMin(rec + 1, h_f[s]);
+        atomicSub(rec + 3, h_d[s]);
+      }
+      if (h_e[s] != kNone) atomicMin(rec + 2, h_e[s]);
+    }
+    __syncthreads();
+  }
+  // one atomic per wave for the ids out of range
+  bad = wave_sum(bad);
+  if ((threadIdx.x & 63) == 0 && bad) atomicAdd(p.n_bad, (unsigned long long)bad);
+}
+
+// One thread per (listed trace, request slot).
+__global__ __launch_bounds__(256) void calib_judge(FallbackParams p) {
+  const uint64_t items = (uint64_t)p.fb[0] * p.req_cap;
+  for (uint64_t it = (uint64_t)blockIdx.x * 256 + threadIdx.x; it < items; it += (uint64_t)gridDim.x * 256) {
+    const uint32_t t = p.fb[1 + it / p.req_cap], r = (uint32_t)(it % p.req_cap);
     const uint64_t slot = (uint64_t)t * p.req_cap + r;
     const uint4 rec = ((const uint4*)p.tab)[slot];
-    if (rec.x == kDone) continue;  // judged inside the join
+    if (rec.x == kNone) continue;  // no ARRIVE: the reset left the slot unseen
     const int64_t b = p.off[t];
-    tre_req_latency out = not_judged(0xFF);
-    out.flags = 0;
-    if (rec.x != kNone) {
-      const uint32_t m = p.model[b + rec.x];
-      out = not_judged(m);
-      if (rec.y != kNone && rec.z != kNone && m < (uint32_t)p.M) {
-        const int64_t ta = p.ts[b + rec.x];
-        out = judge_one(ta, p.ts[b + rec.y], p.ts[b + rec.z], ~rec.w - (uint32_t)p.tokens[b + rec.y], m,
-                        p.slo[(uint64_t)t * p.M + m]);
-        const int64_t w = ta / p.window_ms;  // window of arrival
-        if (w >= 0 && w < p.n_windows)
-          atomicAdd(p.counts + ((uint64_t)t * p.M + m) * p.n_windows + w,
-                    (1u << 16) | ((out.flags & TRE_REQ_OK) ? 1u : 0u));
-      }
+    const uint32_t m = p.model[b + rec.x];
+    tre_req_latency out = not_judged(m);
+    if (rec.y != kNone && rec.z != kNone && m < (uint32_t)p.M) {
+      const tre_slo& q = p.slo[(uint64_t)t * p.M + m];
+      const int64_t ta = p.ts[b + rec.x];
+      out = judge_one(ta, p.ts[b + rec.y], p.ts[b + rec.z], ~rec.w - (uint32_t)p.tokens[b + rec.y], m, q.ttft_ms,
+                      q.tpot_ms, q.e2e_ms);
+      const int64_t w = ta / p.window_ms;  // window of arrival
+      if (w >= 0 && w < p.n_windows)
+        atomicAdd(p.counts + ((uint64_t)t * p.M + m) * p.n_windows + w,
+                  (1u << 16) | ((out.flags & TRE_REQ_OK) ? 1u : 0u));
     }
     if (p.reqs) p.reqs[slot] = out;
   }
@@ -609,6 +1068,7 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
         s_out.healthy_above = Ht - (GP >> 16);
       }
     }
+    __syncthreads();  // s_out written by one thread, read by thread 0
     if (!p.order) {
       if (tid == 0) {
         out.theta = s_out.theta;
@@ -791,13 +1251,20 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
 }  // namespace
 
 // --------------------------------------------------------------- host ABI
+// workspace: the id-out-of-range count (8 bytes, when the caller passes no
+// counter) in a 256-byte header, the fallback list (count, then trace
+// indices) rounded up to 256 bytes, then the fallback's request records
+static uint64_t calib_list_bytes(const tre_events* ev) { return ((4ull + 4ull * ev->n_traces) + 255) & ~255ull; }
+// two lists: the traces the first stream tier hands to the second, and those
+// the second hands to the chunked path
+
 static uint64_t calib_table_bytes(const tre_events* ev, uint32_t req_cap) {
   return (uint64_t)ev->n_traces * req_cap * 16ull;
 }
 
 extern "C" int tre_calib_workspace_size(const tre_events* ev, uint32_t req_cap, size_t* bytes) {
   if (!ev || !bytes) return fail(TRE_EINVAL, "tre_calib_workspace_size: NULL argument");
-  *bytes = (size_t)(256 + calib_table_bytes(ev, req_cap));
+  *bytes = (size_t)(256 + 2 * calib_list_bytes(ev) + calib_table_bytes(ev, req_cap));
   return TRE_OK;
 }
 
@@ -830,6 +1297,7 @@ extern "C" int tre_calibrate(const tre_events* ev, const tre_slo* slo, const dou
     return fail(TRE_EINVAL, "tre_calibrate: NULL argument");
   if (!ev->req) return fail(TRE_EINVAL, "tre_calibrate: the handle has no request-id column");
   if (req_cap == 0) return fail(TRE_EINVAL, "tre_calibrate: req_cap is 0");
+  if (req_cap > (1u << 31)) return fail(TRE_ERANGE, "tre_calibrate: req_cap %u is above 2^31", req_cap);
   if (ev->n_windows > (int64_t)kFitThreads * kFitMaxKPT)
     return fail(TRE_ERANGE, "tre_calibrate: %lld windows, at most %d", (long long)ev->n_windows,
                 kFitThreads * kFitMaxKPT);
@@ -844,35 +1312,48 @@ extern "C" int tre_calibrate(const tre_events* ev, const tre_slo* slo, const dou
   const int M = ev->cfg.n_models;
   const int64_t nW = ev->n_windows;
   unsigned long long* bad = n_bad_ids ? (unsigned long long*)n_bad_ids : (unsigned long long*)ws;
-  uint32_t* tab = (uint32_t*)((char*)ws + 256);
-  const uint64_t tab_words = calib_table_bytes(ev, req_cap) / 4;
+  uint32_t* l1 = (uint32_t*)((char*)ws + 256);
+  uint32_t* l2 = (uint32_t*)((char*)ws + 256 + calib_list_bytes(ev));
+  uint32_t* tab = (uint32_t*)((char*)ws + 256 + 2 * calib_list_bytes(ev));
   const uint64_t cnt_words = (uint64_t)ev->n_traces * M * nW;
   int64_t maxlen = 0;
   for (uint32_t i = 0; i < ev->n_traces; ++i) maxlen = std::max<int64_t>(maxlen, ev->h_off[i + 1] - ev->h_off[i]);
   {
     LaunchTimer lt("calib_fill", st);
-    hipLaunchKernelGGL(fill_u32, dim3(4096), dim3(256), 0, st, tab, tab_words, kNone);
     hipLaunchKernelGGL(fill_u32, dim3(4096), dim3(256), 0, st, counts, cnt_words, 0u);
     hipLaunchKernelGGL(fill_u32, dim3(1), dim3(256), 0, st, (uint32_t*)bad, (uint64_t)2, 0u);
+    hipLaunchKernelGGL(fill_u32, dim3(1), dim3(256), 0, st, l1, (uint64_t)1, 0u);
+    hipLaunchKernelGGL(fill_u32, dim3(1), dim3(256), 0, st, l2, (uint64_t)1, 0u);
+    if (reqs)
+      hipLaunchKernelGGL(fill_unseen, dim3(4096), dim3(256), 0, st, reqs, (uint64_t)ev->n_traces * req_cap);
     lt.done();
   }
   HIP_TRY(hipGetLastError());
-  if (maxlen > 0) {
-    const uint32_t C = (uint32_t)((maxlen + kJoinChunk - 1) / kJoinChunk);
-    JoinParams jp{ev->ts, ev->model, ev->req, ev->type, ev->tokens, ev->d_off, slo, counts, reqs, tab, bad,
-                  ev->n_traces, req_cap, C, M, ev->cfg.window_ms, nW};
-    dim3 grid(8u * C * ((ev->n_traces + 7) / 8));
-    LaunchTimer lt("calib_join", st);
-    hipLaunchKernelGGL(calib_join, grid, dim3(256), 0, st, jp);
+  if (ev->n_traces > 0) {
+    StreamParams sp{ev->ts, ev->model, ev->req, ev->type, ev->tokens, ev->d_off, slo, counts, reqs, bad,
+                    nullptr, l1, req_cap, M, ev->cfg.window_ms, nW};
+    LaunchTimer lt("calib_stream", st);
+    hipLaunchKernelGGL((calib_stream<kBuckets1, kThreads1>), dim3(ev->n_traces), dim3(kThreads1), 0, st, sp);
     lt.done();
     HIP_TRY(hipGetLastError());
   }
-  {
-    JudgeParams pp{ev->ts, ev->model, ev->tokens, ev->d_off, tab, slo, counts, reqs,
-                   ev->n_traces, req_cap, M, ev->cfg.window_ms, nW};
-    dim3 grid((req_cap + 255) / 256, std::min<uint32_t>(ev->n_traces, 65535u));
-    LaunchTimer lt("calib_judge", st);
-    hipLaunchKernelGGL(calib_judge, grid, dim3(256), 0, st, pp);
+  if (maxlen > 0) {
+    // the traces the first tier listed, then those the second listed (none
+    // on most inputs: the launches then end at once)
+    const uint32_t C = (uint32_t)((maxlen + kJoinChunk - 1) / kJoinChunk);
+    FallbackParams f1{ev->ts, ev->model, ev->req, ev->type, ev->tokens, ev->d_off, slo, counts, reqs, nullptr, bad,
+                      l1, req_cap, C, M, ev->cfg.window_ms, nW};
+    FallbackParams f2 = f1;
+    f2.tab = tab;
+    f2.fb = l2;
+    StreamParams sp{ev->ts, ev->model, ev->req, ev->type, ev->tokens, ev->d_off, slo, counts, reqs, bad,
+                    l1, l2, req_cap, M, ev->cfg.window_ms, nW};
+    LaunchTimer lt("calib_fallback", st);
+    hipLaunchKernelGGL(fb_reset, dim3(64, 16), dim3(256), 0, st, f1);
+    hipLaunchKernelGGL((calib_stream<kBuckets2, kThreads2>), dim3(ev->n_traces), dim3(kThreads2), 0, st, sp);
+    hipLaunchKernelGGL(fb_reset, dim3(64, 16), dim3(256), 0, st, f2);
+    hipLaunchKernelGGL(calib_join, dim3(1024), dim3(256), 0, st, f2);
+    hipLaunchKernelGGL(calib_judge, dim3(1024), dim3(256), 0, st, f2);
     lt.done();
     HIP_TRY(hipGetLastError());
   }

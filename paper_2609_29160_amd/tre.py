@@ -169,6 +169,23 @@ def _ptr(t: Optional[torch.Tensor]):
     return t.data_ptr()
 
 
+def _table(t: torch.Tensor, n: int, dt: np.dtype, name: str):
+    """_ptr of a device table of at least n records of the struct `dt` (the
+    library reads n of them through the plain pointer)."""
+    have = t.numel() * t.element_size()
+    if have < n * dt.itemsize:
+        raise ValueError(f"{name}: {have} bytes, {n} records of {dt.itemsize} bytes needed")
+    return _ptr(t)
+
+
+def _prof(ev, prof: torch.Tensor):
+    return _table(prof, ev.n_traces * ev.n_models, PROFILE_DTYPE, "profile table")
+
+
+def _slo(ev, slo: torch.Tensor):
+    return _table(slo, ev.n_traces * ev.n_models, SLO_DTYPE, "SLO table")
+
+
 def _stream(stream) -> Optional[int]:
     if stream is None:
         stream = torch.cuda.current_stream()
@@ -235,7 +252,7 @@ def unpack_moves(moves: torch.Tensor) -> np.ndarray:
 
 def tre_check_params(ev: Events, prof: torch.Tensor, sc: Optional[torch.Tensor] = None):
     n_sc = 0 if sc is None else sc.numel() // SCENARIO_DTYPE.itemsize
-    _check(_L.tre_check_params(ev.handle, _ptr(prof), _ptr(sc), n_sc))
+    _check(_L.tre_check_params(ev.handle, _prof(ev, prof), _ptr(sc), n_sc))
 
 
 def tre_workspace_size(ev: Events, n_scenarios: int) -> int:
@@ -256,7 +273,7 @@ def tre_eval_tss(ev: Events, prof: torch.Tensor, out: Dict[str, torch.Tensor], s
     """Fill the given per-cell outputs (prefill/decode are uint32 data in
     int32 tensors)."""
     o = _TssOut(*[_ptr(out.get(k)) for k in ("prefill", "decode", "a_int", "w_int", "tss64", "tss32", "flags")])
-    _check(_L.tre_eval_tss(ev.handle, _ptr(prof), ctypes.byref(o), _stream(stream)))
+    _check(_L.tre_eval_tss(ev.handle, _prof(ev, prof), ctypes.byref(o), _stream(stream)))
 
 
 STAGE_P_IDLE, STAGE_P_INIT, STAGE_D_IDLE, STAGE_D_INIT = 1, 2, 4, 8
@@ -278,14 +295,14 @@ def tre_stage_tss(ev: Events, prof: torch.Tensor, tallies: Dict[str, torch.Tenso
     """Stage-aware shares from the prefill / decode / a_int / w_int outputs of
     tre_eval_tss; fills the given outputs."""
     t = _TssOut(*[_ptr(tallies.get(k)) for k in ("prefill", "decode", "a_int", "w_int")], None, None, None)
-    _check(_L.tre_stage_tss(ev.handle, _ptr(prof), ctypes.byref(t), _ptr(out.get("stage64")),
+    _check(_L.tre_stage_tss(ev.handle, _prof(ev, prof), ctypes.byref(t), _ptr(out.get("stage64")),
                             _ptr(out.get("stage32")), _ptr(out.get("flags")), _stream(stream)))
 
 
 def tre_eval_stage(ev: Events, prof: torch.Tensor, out: Dict[str, torch.Tensor], stream=None):
     """Stage-aware shares straight from the events (one pass, no tallies in
     HBM); fills the given outputs of stage_outputs()."""
-    _check(_L.tre_eval_stage(ev.handle, _ptr(prof), _ptr(out.get("stage64")), _ptr(out.get("stage32")),
+    _check(_L.tre_eval_stage(ev.handle, _prof(ev, prof), _ptr(out.get("stage64")), _ptr(out.get("stage32")),
                              _ptr(out.get("flags")), _stream(stream)))
 
 
@@ -307,7 +324,7 @@ def tre_rebalance(ev: Events, prof: torch.Tensor, tss64: torch.Tensor, flags: to
                   sc: torch.Tensor, out: Dict[str, torch.Tensor], stream=None):
     n_sc = sc.numel() // SCENARIO_DTYPE.itemsize
     o = _ctl(out)
-    _check(_L.tre_rebalance(ev.handle, _ptr(prof), _ptr(tss64), _ptr(flags), _ptr(sc), n_sc,
+    _check(_L.tre_rebalance(ev.handle, _prof(ev, prof), _ptr(tss64), _ptr(flags), _ptr(sc), n_sc,
                             ctypes.byref(o), _stream(stream)))
 
 
@@ -315,7 +332,7 @@ def tre_sweep(ev: Events, prof: torch.Tensor, sc: torch.Tensor, out: Dict[str, t
               ws: torch.Tensor, tss32: Optional[torch.Tensor] = None, stream=None):
     n_sc = sc.numel() // SCENARIO_DTYPE.itemsize
     o = _ctl(out)
-    _check(_L.tre_sweep(ev.handle, _ptr(prof), _ptr(sc), n_sc, ctypes.byref(o), _ptr(tss32), _ptr(ws),
+    _check(_L.tre_sweep(ev.handle, _prof(ev, prof), _ptr(sc), n_sc, ctypes.byref(o), _ptr(tss32), _ptr(ws),
                         ws.numel() * ws.element_size(), _stream(stream)))
 
 
@@ -324,7 +341,7 @@ def tre_sweep_noalloc(ev: Events, prof: torch.Tensor, sc: torch.Tensor, out: Dic
     """tre_sweep with its scratch in the library's static device array."""
     n_sc = sc.numel() // SCENARIO_DTYPE.itemsize
     o = _ctl(out)
-    _check(_L.tre_sweep_noalloc(ev.handle, _ptr(prof), _ptr(sc), n_sc, ctypes.byref(o), _ptr(tss32),
+    _check(_L.tre_sweep_noalloc(ev.handle, _prof(ev, prof), _ptr(sc), n_sc, ctypes.byref(o), _ptr(tss32),
                                 _stream(stream)))
 
 
@@ -340,14 +357,14 @@ def actuation(wake_ms: int, sleep_ms: int, footprint: Optional[torch.Tensor] = N
 
 
 def tre_check_actuation(ev: Events, prof: torch.Tensor, act: _Actuation):
-    _check(_L.tre_check_actuation(ev.handle, _ptr(prof), ctypes.byref(act)))
+    _check(_L.tre_check_actuation(ev.handle, _prof(ev, prof), ctypes.byref(act)))
 
 
 def tre_rebalance_act(ev: Events, prof: torch.Tensor, tss64: torch.Tensor, flags: torch.Tensor,
                       sc: torch.Tensor, act: _Actuation, out: Dict[str, torch.Tensor], stream=None):
     n_sc = sc.numel() // SCENARIO_DTYPE.itemsize
     o = _ctl(out)
-    _check(_L.tre_rebalance_act(ev.handle, _ptr(prof), _ptr(tss64), _ptr(flags), _ptr(sc), n_sc,
+    _check(_L.tre_rebalance_act(ev.handle, _prof(ev, prof), _ptr(tss64), _ptr(flags), _ptr(sc), n_sc,
                                 ctypes.byref(act), ctypes.byref(o), _stream(stream)))
 
 
@@ -355,7 +372,7 @@ def tre_sweep_act(ev: Events, prof: torch.Tensor, sc: torch.Tensor, act: _Actuat
                   ws: torch.Tensor, tss32: Optional[torch.Tensor] = None, stream=None):
     n_sc = sc.numel() // SCENARIO_DTYPE.itemsize
     o = _ctl(out)
-    _check(_L.tre_sweep_act(ev.handle, _ptr(prof), _ptr(sc), n_sc, ctypes.byref(act), ctypes.byref(o), _ptr(tss32),
+    _check(_L.tre_sweep_act(ev.handle, _prof(ev, prof), _ptr(sc), n_sc, ctypes.byref(act), ctypes.byref(o), _ptr(tss32),
                             _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 
@@ -383,7 +400,7 @@ def calib_outputs(ev: Events, req_cap: int, with_reqs: bool = False, device="cud
 def tre_calibrate(ev: Events, slo: torch.Tensor, tss64: torch.Tensor, flags: torch.Tensor,
                   out: Dict[str, torch.Tensor], stream=None):
     ws = out["ws"]
-    _check(_L.tre_calibrate(ev.handle, _ptr(slo), _ptr(tss64), _ptr(flags), int(out["req_cap"]), _ptr(out["counts"]),
+    _check(_L.tre_calibrate(ev.handle, _slo(ev, slo), _ptr(tss64), _ptr(flags), int(out["req_cap"]), _ptr(out["counts"]),
                             _ptr(out["fit"]), _ptr(out.get("reqs")), _ptr(out.get("n_bad")), _ptr(ws),
                             ws.numel() * ws.element_size(), _stream(stream)))
 
@@ -391,8 +408,17 @@ def tre_calibrate(ev: Events, slo: torch.Tensor, tss64: torch.Tensor, flags: tor
 def tre_calib_order(ev: Events, slo: torch.Tensor, tss64: torch.Tensor, flags: torch.Tensor,
                     out: Dict[str, torch.Tensor], stream=None):
     """The fits again with the ordering counts, from tre_calibrate's counts."""
-    _check(_L.tre_calib_order(ev.handle, _ptr(slo), _ptr(tss64), _ptr(flags), _ptr(out["counts"]), _ptr(out["fit"]),
+    _check(_L.tre_calib_order(ev.handle, _slo(ev, slo), _ptr(tss64), _ptr(flags), _ptr(out["counts"]), _ptr(out["fit"]),
                               _stream(stream)))
+
+
+def calib_fallback_traces(ev: Events, out: Dict[str, torch.Tensor]):
+    """(traces the last tre_calibrate on `out` redid with the larger stream
+    table, traces it redid on the chunked path): the uint32 counts that
+    open the workspace's two lists; synchronises."""
+    lb = ((4 + 4 * ev.n_traces) + 255) & ~255
+    w = out["ws"][256:256 + 2 * lb].cpu().numpy()
+    return int(w[0:4].view(np.uint32)[0]), int(w[lb:lb + 4].view(np.uint32)[0])
 
 
 def unpack_fit(fit: torch.Tensor) -> np.ndarray:
@@ -452,7 +478,8 @@ def tre_loop(cfg: Dict[str, int], n_traces: int, rq: _LoopRequests, prof: torch.
     n_sc = sc.numel() // SCENARIO_DTYPE.itemsize
     c = _cfg(cfg)
     o = _ctl(out)
-    _check(_L.tre_loop(ctypes.byref(c), n_traces, ctypes.byref(rq), _ptr(prof), _ptr(sc), n_sc, ctypes.byref(o),
+    prof_p = _table(prof, n_traces * cfg["n_models"], PROFILE_DTYPE, "profile table")
+    _check(_L.tre_loop(ctypes.byref(c), n_traces, ctypes.byref(rq), prof_p, _ptr(sc), n_sc, ctypes.byref(o),
                        _ptr(stats), _ptr(tss64), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 
@@ -464,7 +491,8 @@ def tre_loop_act(cfg: Dict[str, int], n_traces: int, rq: _LoopRequests, prof: to
     n_sc = sc.numel() // SCENARIO_DTYPE.itemsize
     c = _cfg(cfg)
     o = _ctl(out)
-    _check(_L.tre_loop_act(ctypes.byref(c), n_traces, ctypes.byref(rq), _ptr(prof), _ptr(sc), n_sc, ctypes.byref(act),
+    prof_p = _table(prof, n_traces * cfg["n_models"], PROFILE_DTYPE, "profile table")
+    _check(_L.tre_loop_act(ctypes.byref(c), n_traces, ctypes.byref(rq), prof_p, _ptr(sc), n_sc, ctypes.byref(act),
                            ctypes.byref(o), _ptr(stats), _ptr(tss64), _ptr(ws), ws.numel() * ws.element_size(),
                            _stream(stream)))
 

@@ -59,7 +59,7 @@ def _slo_rows(slo_cols, t, M):
     return a
 
 
-def _check(lib, name, cfg, traces, prof_cols, slo_cols, req_cap, check_traces=None):
+def _check(lib, name, cfg, traces, prof_cols, slo_cols, req_cap, check_traces=None, tiers=None):
     tre, device, torch = lib
     M = cfg["n_models"]
     cols, off = _columns(torch, traces)
@@ -110,6 +110,10 @@ def _check(lib, name, cfg, traces, prof_cols, slo_cols, req_cap, check_traces=No
             f"{what}: theta {fit[t]['theta']} vs {ref['theta']}"
     if check_traces is None:
         assert int(out["n_bad"].cpu().numpy()[0]) == bad_total, f"{name}: ids past req_cap"
+    n_fb = tre.calib_fallback_traces(ev, out)
+    say(f"{name}: traces redone by the larger stream table and by the chunked path: {n_fb}")
+    if tiers is not None:
+        assert n_fb == tiers, f"{name}: traces redone {n_fb}, expected {tiers}"
     ev.close()
     return fit
 
@@ -197,6 +201,153 @@ def test_constant_load_runs_of_equal_keys(lib):
            "e2e_ms": np.full(M, 1000.0), "attain_q": np.full(M, 0.95), "reliability": np.array([0.9, 0.0, 1.0])}
     fit = _check(lib, "steady", cfg, [steady], prof, slo, rid)
     say("steady fit", fit)
+
+
+def _small_cfg(M=2):
+    return {"window_ms": 100, "duration_ms": 10_000, "fast_period_ms": 100, "slow_period_ms": 200,
+            "n_models": M, "budget": 4 * M}
+
+
+def _small_prof(M, n_traces):
+    n = M * n_traces
+    return {"w_p": np.full(n, 0.2), "w_q": np.full(n, 2.0), "alpha": np.full(n, 0.5), "theta": np.full(n, 10.0),
+            "tau_crit": np.full(n, 0.5), "tau_surplus": np.full(n, 1.5), "r_min": np.ones(n, np.int32),
+            "r_init": np.full(n, 2, np.int32)}
+
+
+def _small_slo(M, n_traces):
+    return {"ttft_ms": np.full(M * n_traces, 600.0), "tpot_ms": np.full(M * n_traces, 40.0),
+            "e2e_ms": np.full(M * n_traces, 2500.0), "attain_q": np.full(M * n_traces, 0.9),
+            "reliability": np.full(M * n_traces, 0.8)}
+
+
+def _complete(rid, m, t0, span, tok=24):
+    """ARRIVE, ADMIT, two DECODE chunks and the FINISH of one request."""
+    return [(t0, m, rid, CP.A, 40), (t0, m, rid, CP.P | CP.ADMIT, 40), (t0 + span // 3, m, rid, CP.D, tok),
+            (t0 + span, m, rid, CP.D, tok // 2), (t0 + span, m, rid, CP.F, 0)]
+
+
+def _crowded(n, rid0=0):
+    """n requests in flight together (all arrive in the first 50 ms, finish
+    after 8 s): more live records than the stream's table keeps."""
+    rows = []
+    for j in range(n):
+        rows += _complete(rid0 + j, j % 2, j % 50, 8000 + (j % 300), tok=24 + j % 7)
+    return CP._trace(rows)
+
+
+def _turnover(n, live):
+    """One arrival and one finish per ms with `live` requests in flight: the
+    stream rebuilds its table every tile."""
+    rows = []
+    for j in range(n):
+        rows += _complete(j, j % 2, j, live, tok=10 + j % 5)
+    return CP._trace(rows)
+
+
+def _filler(n_rows, t0, rid0):
+    """Complete requests (5 rows each, 5 ms apart from t0) padded with
+    PREFILL rows of the first one to exactly n_rows rows."""
+    rows, rid = [], rid0
+    for j in range(n_rows // 5):
+        rows += _complete(rid, j % 2, t0 + 5 * j, 3, tok=8)
+        rid += 1
+    pad = n_rows % 5
+    if pad:
+        if rid == rid0:
+            rows += [(t0, 0, rid, CP.A, 8)] + [(t0, 0, rid, CP.P, 8)] * (pad - 1)
+            rid += 1
+        else:
+            rows[1:1] = [(t0, 0, rid0, CP.P, 8)] * pad
+    return rows, rid
+
+
+def _boundary_instant(n_fin, before, order="fin_first", boundary=2048):
+    """n_fin requests whose FINISH and a last DECODE fall on one instant X
+    whose rows start `before` rows ahead of row `boundary` (a tile boundary
+    of both stream tiers when 4096); at X the FINISH rows come all first
+    ("fin_first"), after the DECODE rows ("dec_first") or each with its own
+    DECODE behind it ("interleaved"). Filler requests before and after."""
+    pre = boundary - before - 3 * n_fin
+    assert pre >= 0, pre
+    rows, rid = _filler(pre, 0, 0)
+    X = 6000
+    fin, dec = [], []
+    for j in range(n_fin):
+        m = j % 2
+        rows += [(1000 + j, m, rid, CP.A, 30), (1000 + j, m, rid, CP.P | CP.ADMIT, 30), (2000 + j, m, rid, CP.D, 24)]
+        fin.append((X, m, rid, CP.F, 0))
+        dec.append((X, m, rid, CP.D, 3 + j % 9))
+        rid += 1
+    if order == "fin_first":
+        rows += fin + dec
+    elif order == "dec_first":
+        rows += dec + fin
+    else:
+        rows += [r for pair in zip(fin, dec) for r in pair]
+    more, _ = _filler(1500, 7000, rid)
+    return CP._trace(rows + more)
+
+
+def _long_instant(n_dec=3):
+    """200 FINISH rows at the last instant X of a tile, followed by more than
+    a whole tile of DECODE rows at X (1300 requests in flight, n_dec DECODE
+    rows each at X: 3 outlast a tile of the first stream tier, 4 one of the
+    second)."""
+    rows, rid = [], 0
+    X = 6000
+    a = []
+    for j in range(200):
+        m = j % 2
+        rows += [(1000 + j, m, rid, CP.A, 30), (1000 + j, m, rid, CP.P | CP.ADMIT, 30), (2000 + j, m, rid, CP.D, 24)]
+        a.append((X, m, rid, CP.F, 0))
+        rid += 1
+    b, bf = [], []
+    for j in range(1300):
+        m = j % 2
+        rows += [(100 + j % 500, m, rid, CP.A, 30), (100 + j % 500, m, rid, CP.P | CP.ADMIT, 30)]
+        b += [(X, m, rid, CP.D, 5)] * n_dec
+        bf.append((6100 + j % 100, m, rid, CP.F, 0))
+        rid += 1
+    return CP._trace(rows + a + b + bf)
+
+
+def test_stream_rebuild_and_instants(lib):
+    """The stream's own paths, against the oracle: a table rebuilt every tile
+    (2300 requests in flight); tiles with more FINISH rows than the judge
+    queue holds (2000 requests finishing within 300 ms); FINISH rows at a
+    tile's last instant
+    judged after the next tile, with the last DECODE of the same request in
+    that instant listed after its FINISH (so beyond the boundary), with all
+    256 FINISH rows the stream defers, and with the DECODE rows first; and
+    traces that do not start on a 4-row boundary."""
+    M = 2
+    traces = [_turnover(7000, 2300), _crowded(2000), _boundary_instant(200, 120), _boundary_instant(300, 256),
+              _boundary_instant(250, 251, "interleaved"), _boundary_instant(250, 250, "dec_first"),
+              _turnover(3000, 700)]
+    say("rows", [len(t["ts"]) for t in traces])
+    _check(lib, "stream-paths", _small_cfg(M), traces, _small_prof(M, len(traces)), _small_slo(M, len(traces)),
+           _req_cap(traces), tiers=(0, 0))
+
+
+def test_stream_fallback(lib):
+    """Traces the first stream tier hands to the second (twice the records,
+    tiles of 4096 rows) and those the second hands to the chunked path: more
+    requests in flight than a table keeps, more FINISH rows at a tile's last
+    instant than a tier defers, an instant longer than a tile; mixed with
+    traces the first tier finishes, with ids past req_cap."""
+    M = 2
+    traces = [_crowded(3300),                                  # second tier
+              _crowded(6000),                                  # chunked: too many in flight
+              _turnover(3000, 500),                            # first tier
+              _boundary_instant(400, 300),                     # second tier: 300 FINISH deferred
+              _boundary_instant(400, 300, boundary=4096),      # chunked: 300 deferred in both
+              _long_instant(3),                                # second tier
+              _long_instant(4),                                # chunked: instant longer than 4096 rows
+              _turnover(2000, 300)]                            # first tier
+    say("rows", [len(t["ts"]) for t in traces])
+    cap = _req_cap(traces) - 5
+    _check(lib, "fallback", _small_cfg(M), traces, _small_prof(M, len(traces)), _small_slo(M, len(traces)), cap, tiers=(6, 3))
 
 
 def test_model_counts(lib):
