@@ -50,7 +50,7 @@ extern "C" {
 #define TRE_ENOMEM 5  /* workspace too small                                   */
 #define TRE_EHIP 6    /* HIP runtime error                                     */
 #define TRE_ESTATE 7  /* a request count of Eq. (1) below zero, or a request
-                         admitted twice (see tre_load_events)                 */
+                         id off its lifecycle (see tre_load_events)          */
 
 /* Maximum models per trace (one wavefront lane per model). */
 #define TRE_MAX_MODELS 64
@@ -192,14 +192,20 @@ const char* tre_last_error(void);
                   Definition": numbers of requests) below zero at some
                   instant t, i.e. after the last row with that timestamp
                   (rows of one instant may come in any order); or, when
-                  `req` is given, one request id carrying the ADMIT bit on
-                  more than one row of a trace (a request is admitted once).
+                  `req` is given, a request id off its lifecycle within a
+                  trace: the ADMIT bit on more than one row (a request is
+                  admitted once), more than one ARRIVE or more than one
+                  FINISH row, or an ARRIVE or DECODE row with a later
+                  timestamp than the id's FINISH (a finished request
+                  neither arrives nor produces output again; rows of its
+                  FINISH instant may come in any order).
    The first three are checked together and the message names the lowest
    failing row and its kind; TRE_ESTATE is checked only when they pass
-   (the lowest failing row, or the smallest duplicated trace and id).
-   The id check allocates temporary device memory, one bit per id up to the
-   largest admitted id of each trace (at most 256 MiB at a time, or one
-   trace's bitmap if larger), freed before the call returns. Without
+   (the lowest failing row, or the smallest trace and id in error).
+   The id checks allocate temporary device memory: one bit per id up to the
+   largest admitted id of each trace, then 4 bytes and one bit per id up to
+   the largest ARRIVE or FINISH id (at most 256 MiB at a time, or one
+   trace's tables if larger), freed before the call returns. Without
    TRE_VALIDATE, events that break these rules give unspecified results,
    never an access outside the columns, outputs or workspace. The
    handle owns small device tables (offsets, tick list); free it with
@@ -391,7 +397,8 @@ int tre_calib_workspace_size(const tre_events* ev, uint32_t req_cap, size_t* byt
      n_bad_ids  one uint64: events whose id is >= req_cap, or NULL.
    The handle needs its req column; at most 16384 windows (TRE_ERANGE);
    req_cap at most 2^31 (TRE_ERANGE).
-   Request lifecycle: per trace, a request id has at most one ARRIVE row
+   Request lifecycle (checked by tre_load_events with TRE_VALIDATE and a req
+   column, TRE_ESTATE): per trace, a request id has at most one ARRIVE row
    and at most one FINISH row, and no ARRIVE or DECODE row with a later
    timestamp than its FINISH (rows of one instant may come in any order).
    Events that break it give unspecified results, never an access out of

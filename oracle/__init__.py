@@ -84,6 +84,10 @@ class Oracle:
         if self.has_admits:
             L.oracle_check_admits.restype = ctypes.c_int
             L.oracle_check_admits.argtypes = [vp, vp, i64, vp, vp]
+        self.has_lifecycle = hasattr(L, "oracle_check_lifecycle")
+        if self.has_lifecycle:
+            L.oracle_check_lifecycle.restype = ctypes.c_int
+            L.oracle_check_lifecycle.argtypes = [vp, vp, vp, i64, vp, vp]
         L.oracle_control.restype = ctypes.c_int
         L.oracle_control.argtypes = [i64, i64, i64, i64, i32, i32, vp, vp, vp, vp, vp, u32, vp, vp, vp]
         self.has_act = hasattr(L, "oracle_control_act")
@@ -171,6 +175,19 @@ class Oracle:
         rc = int(self.L.oracle_check_admits(req.ctypes.data, typ.ctypes.data, req.shape[0], scratch.ctypes.data,
                                             dup.ctypes.data))
         return rc, (int(dup[0]) if rc else None)
+
+    def check_lifecycle(self, ev: Dict[str, np.ndarray]):
+        """(0, None) when every request id of the trace arrives at most once,
+        finishes at most once and neither arrives nor decodes at a later
+        timestamp than its FINISH; else (-7, the smallest offending id)."""
+        req = np.ascontiguousarray(ev["req"], np.uint32)
+        typ = np.ascontiguousarray(ev["type"], np.uint8)
+        ts = np.ascontiguousarray(ev["ts"], np.int64)
+        scratch = np.zeros(max(1, req.shape[0]), np.uint64)
+        bad = np.zeros(1, np.uint32)
+        rc = int(self.L.oracle_check_lifecycle(req.ctypes.data, typ.ctypes.data, ts.ctypes.data, req.shape[0],
+                                               scratch.ctypes.data, bad.ctypes.data))
+        return rc, (int(bad[0]) if rc else None)
 
     def control(self, cfg: Dict[str, int], prof: np.ndarray, S: np.ndarray, flags: np.ndarray,
                 sc: np.ndarray, move_cap: Optional[int] = None) -> Dict[str, np.ndarray]:

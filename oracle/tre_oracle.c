@@ -347,3 +347,52 @@ int oracle_check_admits(const uint32_t* req, const uint8_t* type, int64_t n_even
     }
   return 0;
 }
+
+static int cmp_u64(const void* a, const void* b) {
+  const uint64_t x = *(const uint64_t*)a, y = *(const uint64_t*)b;
+  return x < y ? -1 : (x > y ? 1 : 0);
+}
+
+/* ----------------------------------------------------------------------
+ * Request lifecycle check for one trace. A request enters the waiting set
+ * once (its ARRIVE), leaves the active set once (its FINISH), and no longer
+ * arrives or produces output afterwards (the request counts of Eq. (1),
+ * Section "Design Rationale and Definition"): per request id at most one
+ * ARRIVE row and one FINISH row, and no ARRIVE or DECODE row with a later
+ * timestamp than the FINISH (rows of one instant may come in any order).
+ * Returns 0, or -7 with the smallest offending id in *bad_id. keys_scratch
+ * holds n_events uint64 words.
+ * -------------------------------------------------------------------- */
+int oracle_check_lifecycle(const uint32_t* req, const uint8_t* type, const int64_t* ts, int64_t n_events,
+                           uint64_t* keys_scratch, uint32_t* bad_id) {
+  int64_t n = 0;
+  for (int64_t i = 0; i < n_events; ++i) {
+    const uint32_t kind = type[i] & 3u;
+    if (kind == OR_ARRIVE || kind == OR_DECODE || kind == OR_FINISH)
+      keys_scratch[n++] = ((uint64_t)req[i] << 32) | (uint64_t)i;
+  }
+  qsort(keys_scratch, (size_t)n, sizeof(uint64_t), cmp_u64);
+  for (int64_t g = 0; g < n;) {  /* the rows of one id */
+    const uint32_t id = (uint32_t)(keys_scratch[g] >> 32);
+    int64_t h = g;
+    int arrivals = 0, finishes = 0;
+    int64_t fin_ts = 0, last_ad_ts = INT64_MIN;
+    for (; h < n && (uint32_t)(keys_scratch[h] >> 32) == id; ++h) {
+      const int64_t row = (int64_t)(uint32_t)keys_scratch[h];
+      const uint32_t kind = type[row] & 3u;
+      if (kind == OR_FINISH) {
+        ++finishes;
+        fin_ts = ts[row];
+      } else {
+        if (kind == OR_ARRIVE) ++arrivals;
+        if (ts[row] > last_ad_ts) last_ad_ts = ts[row];
+      }
+    }
+    if (arrivals > 1 || finishes > 1 || (finishes == 1 && last_ad_ts > fin_ts)) {
+      *bad_id = id;
+      return -7;
+    }
+    g = h;
+  }
+  return 0;
+}

@@ -1387,6 +1387,71 @@ __global__ __launch_bounds__(256) void admit_scan(AdmitParams p) {
   }
 }
 
+// A request arrives once, finishes once, and neither arrives nor decodes
+// after it finished (rows of its FINISH instant in any order): the request
+// counts of Eq. (1) follow one lifecycle per id. Pass 0 finds the largest
+// id of an ARRIVE or FINISH row per trace; pass 1 marks each id's ARRIVE in
+// a bitmap and stores its FINISH timestamp (a second one of either is an
+// error); pass 2 checks every ARRIVE and DECODE row against the FINISH
+// timestamp of its id. The smallest (trace, id) in error is kept.
+struct LifeParams {
+  const int64_t* ts;
+  const uint32_t* req;
+  const uint8_t* type;
+  const int64_t* off;
+  uint32_t t0, n_traces;        // traces [t0, t0 + n_traces) of this launch
+  uint32_t* maxid;              // pass 0: [all traces] largest id of an ARRIVE or FINISH row
+  const uint64_t* slot_off;     // passes 1, 2: [all traces] first slot of each trace's ids
+  uint64_t slot_base;           // slot_off of trace t0
+  uint32_t* fin;                // FINISH timestamp per slot, 0xFFFFFFFF when none
+  uint32_t* arr;                // ARRIVE bit per slot
+  unsigned long long* bad;      // smallest (trace << 32 | id) in error
+};
+
+template <int kPass>
+__global__ __launch_bounds__(256) void life_scan(LifeParams p) {
+  for (uint32_t tt = blockIdx.y; tt < p.n_traces; tt += gridDim.y) {
+    const uint32_t t = p.t0 + tt;
+    const int64_t b = p.off[t], e = p.off[t + 1];
+    const int64_t c0 = b + (int64_t)blockIdx.x * kValChunk;
+    if (c0 >= e) continue;  // uniform over the block
+    const int64_t c1 = c0 + kValChunk < e ? c0 + kValChunk : e;
+    uint32_t mx = 0;
+    for (int64_t i = c0 + threadIdx.x; i < c1; i += 256) {
+      const uint32_t ty = p.type[i], kind = ty & 3u, id = p.req[i];
+      if constexpr (kPass == 0) {
+        if ((kind == TRE_ARRIVE || kind == TRE_FINISH) && id > mx) mx = id;
+      } else {
+        if ((uint64_t)id >= p.slot_off[t + 1] - p.slot_off[t]) continue;  // no ARRIVE or FINISH of this id
+        const uint64_t sl = p.slot_off[t] - p.slot_base + id;
+        const uint32_t ts = (uint32_t)p.ts[i];  // timestamps lie in [0, duration) below 2^32
+        bool err = false;
+        if constexpr (kPass == 1) {
+          if (kind == TRE_ARRIVE) {
+            const uint32_t bit = 1u << (sl & 31u);
+            err = (atomicOr(&p.arr[sl >> 5], bit) & bit) != 0;
+          } else if (kind == TRE_FINISH) {
+            err = atomicCAS(&p.fin[sl], 0xFFFFFFFFu, ts) != 0xFFFFFFFFu;
+          }
+        } else {
+          if (kind == TRE_ARRIVE || kind == TRE_DECODE) {
+            const uint32_t f = p.fin[sl];
+            err = f != 0xFFFFFFFFu && ts > f;
+          }
+        }
+        if (err) atomicMin(p.bad, ((unsigned long long)t << 32) | id);
+      }
+    }
+    if constexpr (kPass == 0) {
+      for (int d = 32; d >= 1; d >>= 1) {
+        const uint32_t o = (uint32_t)__shfl_xor((int)mx, d);
+        mx = o > mx ? o : mx;
+      }
+      if ((threadIdx.x & 63) == 0 && mx) atomicMax(&p.maxid[t], mx);
+    }
+  }
+}
+
 // ------------------------------------------------------------------ timing
 namespace {
 struct Pending {
@@ -1524,7 +1589,7 @@ static int validate_events(const tre_events* ev, hipStream_t st) {
   struct Slots {
     unsigned err, pad;
     unsigned long long first[kValKinds];
-    unsigned long long dup;
+    unsigned long long dup, life;
   } h;
   void* slots = nullptr;
   if (hipMalloc(&slots, sizeof(Slots)) != hipSuccess) return fail(TRE_EHIP, "hipMalloc failed");
@@ -1629,6 +1694,78 @@ static int validate_events(const tre_events* ev, hipStream_t st) {
     if (ok && h.dup != ~0ull)
       rc = fail(TRE_ESTATE, "trace %u: request id %u admitted more than once", (unsigned)(h.dup >> 32),
                 (unsigned)h.dup);
+  }
+  if (ok && rc == TRE_OK && ev->req) {
+    // the lifecycle of each id: pass 0 sizes per-trace tables (ids up to the
+    // largest ARRIVE or FINISH id), passes 1 and 2 run over batches of at
+    // most 2^26 slots (256 MiB of FINISH timestamps), or one trace if larger
+    uint32_t* d_max = nullptr;
+    uint64_t* d_soff = nullptr;
+    uint32_t* d_fin = nullptr;
+    uint32_t* d_arr = nullptr;
+    std::vector<uint32_t> hmax(n_traces);
+    std::vector<uint64_t> soff(n_traces + 1);
+    ok = hipMalloc(&d_max, sizeof(uint32_t) * n_traces) == hipSuccess &&
+         hipMemsetAsync(d_max, 0, sizeof(uint32_t) * n_traces, st) == hipSuccess;
+    LifeParams lp{};
+    lp.ts = ev->ts;
+    lp.req = ev->req;
+    lp.type = ev->type;
+    lp.off = ev->d_off;
+    lp.maxid = d_max;
+    lp.bad = &d->life;
+    for (uint32_t t0 = 0; ok && t0 < n_traces; t0 += 65535u) {
+      lp.t0 = t0;
+      lp.n_traces = std::min<uint32_t>(n_traces - t0, 65535u);
+      hipLaunchKernelGGL(life_scan<0>, dim3(grid.x, lp.n_traces), dim3(256), 0, st, lp);
+      ok = hipGetLastError() == hipSuccess;
+    }
+    ok = ok && hipMemcpyAsync(hmax.data(), d_max, sizeof(uint32_t) * n_traces, hipMemcpyDeviceToHost, st) ==
+                   hipSuccess &&
+         hipStreamSynchronize(st) == hipSuccess;
+    soff[0] = 0;
+    uint64_t most = 0;
+    for (uint32_t t = 0; t < n_traces; ++t) {
+      const uint64_t n = (uint64_t)hmax[t] + 1u;
+      soff[t + 1] = soff[t] + n;
+      most = std::max(most, n);
+    }
+    const uint64_t cap = std::max<uint64_t>(most, std::min<uint64_t>(soff[n_traces], 1ull << 26));
+    ok = ok && hipMalloc(&d_soff, sizeof(uint64_t) * (n_traces + 1)) == hipSuccess &&
+         hipMalloc(&d_fin, sizeof(uint32_t) * cap) == hipSuccess &&
+         hipMalloc(&d_arr, sizeof(uint32_t) * (cap / 32 + 1)) == hipSuccess &&
+         hipMemcpyAsync(d_soff, soff.data(), sizeof(uint64_t) * (n_traces + 1), hipMemcpyHostToDevice, st) ==
+             hipSuccess;
+    lp.slot_off = d_soff;
+    lp.fin = d_fin;
+    lp.arr = d_arr;
+    for (uint32_t t0 = 0; ok && t0 < n_traces;) {
+      uint32_t t1 = t0 + 1;
+      while (t1 < n_traces && t1 - t0 < 65535u && soff[t1 + 1] - soff[t0] <= cap) ++t1;
+      int64_t len = 0;
+      for (uint32_t t = t0; t < t1; ++t) len = std::max<int64_t>(len, ev->h_off[t + 1] - ev->h_off[t]);
+      const uint64_t slots = soff[t1] - soff[t0];
+      lp.t0 = t0;
+      lp.n_traces = t1 - t0;
+      lp.slot_base = soff[t0];
+      ok = hipMemsetAsync(d_fin, 0xFF, sizeof(uint32_t) * slots, st) == hipSuccess &&
+           hipMemsetAsync(d_arr, 0, sizeof(uint32_t) * (slots / 32 + 1), st) == hipSuccess;
+      if (ok && len > 0) {
+        const dim3 g((unsigned)((len + kValChunk - 1) / kValChunk), t1 - t0);
+        hipLaunchKernelGGL(life_scan<1>, g, dim3(256), 0, st, lp);
+        hipLaunchKernelGGL(life_scan<2>, g, dim3(256), 0, st, lp);
+        ok = hipGetLastError() == hipSuccess;
+      }
+      t0 = t1;
+    }
+    ok = ok && readback();
+    if (d_max) (void)hipFree(d_max);
+    if (d_soff) (void)hipFree(d_soff);
+    if (d_fin) (void)hipFree(d_fin);
+    if (d_arr) (void)hipFree(d_arr);
+    if (ok && h.life != ~0ull)
+      rc = fail(TRE_ESTATE, "trace %u: request id %u arrives or finishes twice, or arrives or decodes after its FINISH",
+                (unsigned)(h.life >> 32), (unsigned)h.life);
   }
   (void)hipFree(slots);
   if (!ok) return fail(TRE_EHIP, "validation launch failed");

@@ -578,6 +578,23 @@ def pin_state(o):
     assert o.check_admits(ev) == (-6, 4)
     assert o.check_admits(events_from_rows(life)) == (0, None)
     assert o.check_admits(events_from_rows([[5, 0, 3, ADM, 1], [6, 0, 4, ADM, 1], [7, 0, 3, PF, 1]])) == (0, None)
+    # request ids: a request arrives once, finishes once, and neither arrives
+    # nor decodes after its FINISH (rows of its FINISH instant in any order)
+    lc = lambda rows: o.check_lifecycle(events_from_rows(rows))
+    assert lc(life) == (0, None)
+    assert lc([[10, 0, 7, ARR, 5], [20, 0, 7, ARR, 5], [30, 0, 8, ARR, 5]]) == (-7, 7)
+    assert lc([[10, 0, 3, ARR, 5], [40, 0, 3, FIN, 0], [50, 0, 3, FIN, 0]]) == (-7, 3)
+    assert lc([[10, 0, 4, ARR, 5], [40, 0, 4, FIN, 0], [41, 0, 4, DEC, 2]]) == (-7, 4)
+    assert lc([[40, 0, 5, FIN, 0], [41, 0, 5, ARR, 2]]) == (-7, 5)
+    # the smallest offending id, not the first in row order
+    assert lc([[10, 0, 9, ARR, 5], [11, 0, 9, ARR, 5], [12, 0, 2, FIN, 0], [13, 0, 2, FIN, 0]]) == (-7, 2)
+    # accepted: a DECODE listed after the FINISH of the same instant, a
+    # PREFILL or ADMIT after the FINISH, a DECODE before the ARRIVE, ids with
+    # no ARRIVE or no FINISH
+    assert lc([[10, 0, 1, ARR, 5], [40, 0, 1, FIN, 0], [40, 0, 1, DEC, 3]]) == (0, None)
+    assert lc([[10, 0, 1, ARR, 5], [40, 0, 1, FIN, 0], [45, 0, 1, PF, 3], [46, 0, 1, ADM, 3]]) == (0, None)
+    assert lc([[5, 0, 1, DEC, 2], [10, 0, 1, ARR, 5], [40, 0, 1, FIN, 0]]) == (0, None)
+    assert lc([[5, 0, 1, DEC, 2], [9, 0, 1, FIN, 0], [12, 0, 2, ARR, 5], [30, 0, 2, DEC, 3]]) == (0, None)
 
 
 ALL_PINS = [pin_hand_traces, pin_paper_pair, pin_floor, pin_closed_forms, pin_normalisation,

@@ -347,18 +347,34 @@ def test_validation_errors(lib):
     ev.close()
 
 
-def _perturbed(rng, tr, how):
+def _perturbed(rng, tr, how, duration_ms=None):
     """A copy of a host trace with one change: 'shuffle' permutes the rows
     of every instant (a valid stream stays valid), 'drop_arrive' /
-    'drop_admit' delete one row of that kind, 'dup_admit' repeats one
-    admitting row (the same request id) at a later row of its instant or
-    after it."""
+    'drop_admit' delete one row of that kind, 'dup_admit' / 'dup_arrive' /
+    'dup_finish' repeat one row of that kind (the same request id) at a
+    later row of its instant or after it, 'decode_after' adds a DECODE of a
+    finished request one ms after its FINISH, 'decode_same' one listed right
+    after its FINISH in the same instant (allowed)."""
     t = {k: v.copy() for k, v in tr.items()}
     n = len(t["ts"])
     if how == "shuffle":
         order = np.lexsort((rng.random(n), t["ts"]))
         return {k: v[order] for k, v in t.items()}
-    kind = {"drop_arrive": 0, "drop_admit": 0x81, "dup_admit": 0x81}[how]
+    if how in ("decode_after", "decode_same"):
+        fin = np.flatnonzero(t["type"] == 3)
+        if how == "decode_after":
+            fin = fin[t["ts"][fin] + 1 < duration_ms]
+        r = int(rng.choice(fin))
+        row = {k: v[r] for k, v in t.items()}
+        row["type"] = 2
+        row["tokens"] = 5
+        if how == "decode_same":
+            j = r + 1
+        else:
+            row["ts"] = int(t["ts"][r]) + 1
+            j = int(np.searchsorted(t["ts"], row["ts"]))
+        return {k: np.insert(v, j, row[k]) for k, v in t.items()}
+    kind = {"drop_arrive": 0, "drop_admit": 0x81, "dup_admit": 0x81, "dup_arrive": 0, "dup_finish": 3}[how]
     rows = np.flatnonzero(t["type"] == kind)
     r = int(rng.choice(rows))
     if how.startswith("drop"):
@@ -373,32 +389,42 @@ def _perturbed(rng, tr, how):
 
 def test_state_validation(lib):
     """TRE_ESTATE at load against the oracle: the active / waiting counts of
-    Eq. (1) never below zero at any instant, and no request id admitted
-    twice. Traces with many rows per millisecond (so instants span the
-    kernel's 64-row steps), perturbed at random: rows of one instant
-    shuffled (accepted, same tallies), an ARRIVE or an ADMIT dropped, an
-    ADMIT repeated. The GPU must reject exactly what the oracle rejects."""
+    Eq. (1) never below zero at any instant, no request id admitted twice,
+    and every id on one lifecycle (one ARRIVE, one FINISH, no ARRIVE or
+    DECODE after the FINISH). Traces with many rows per millisecond (so
+    instants span the kernel's 64-row steps), perturbed at random: rows of
+    one instant shuffled (accepted, same tallies), an ARRIVE or an ADMIT
+    dropped, an ADMIT, ARRIVE or FINISH repeated, a DECODE after a FINISH or
+    listed after it in the same instant (accepted). The GPU must reject
+    exactly what the oracle rejects."""
     tre, device, torch = lib
     o = O.get()
     M, win, nW = 5, 10, 50
     cfg = _cfg(M, win, nW, fast_w=2, slow_w=4)
     rng = np.random.default_rng(77)
     seen = {"ok": 0, "state": 0}
-    for case in range(48):
-        how = ("shuffle", "drop_arrive", "drop_admit", "dup_admit")[case % 4]
+    kinds = ("shuffle", "drop_arrive", "drop_admit", "dup_admit", "dup_arrive", "dup_finish", "decode_after",
+             "decode_same")
+    for case in range(64):
+        how = kinds[case % 8]
         # every request admitted and finished in half the cases, so the
         # counts return to zero and a dropped row takes one below it
-        full = (case // 4) % 2 == 1
+        full = (case // 8) % 2 == 1
         base = E.trace_random(500 + case, M, win * nW, 400, max_span_ms=300,
                               **({"admit_p": 1.0, "finish_p": 1.0} if full else {}))
-        tr = _perturbed(rng, base, how)
+        tr = _perturbed(rng, base, how, win * nW)
         assert (np.diff(tr["ts"]) >= 0).all()
         exp_state = o.trace_status(tr, win, win * nW, M)
         assert exp_state in (0, -5), exp_state
         exp_dup = o.check_admits(tr)[0]
+        exp_life = o.check_lifecycle(tr)[0]
+        if how in ("dup_arrive", "dup_finish", "decode_after"):
+            assert exp_life == -7, how
+        if how == "decode_same":
+            assert exp_life == 0
         cols, off = _columns_from_host(torch, [tr])
-        say(f"state case {case} ({how}): {len(tr['ts'])} rows, oracle {exp_state} / {exp_dup}")
-        if exp_state or exp_dup:
+        say(f"state case {case} ({how}): {len(tr['ts'])} rows, oracle {exp_state} / {exp_dup} / {exp_life}")
+        if exp_state or exp_dup or exp_life:
             with pytest.raises(tre.TreError) as e:
                 tre.tre_load_events(cols["ts"], cols["model"], cols["req"], cols["type"], cols["tokens"], off, cfg)
             assert e.value.code == tre.TRE_ESTATE, (case, how, str(e.value))
@@ -418,11 +444,46 @@ def test_state_validation(lib):
             ev.close()
             seen["ok"] += 1
         # the same columns without request ids: only the counts are checked
-        if exp_dup and not exp_state:
+        if (exp_dup or exp_life) and not exp_state:
             ev = tre.tre_load_events(cols["ts"], cols["model"], None, cols["type"], cols["tokens"], off, cfg)
             ev.close()
     say("state validation:", seen)
-    assert seen["ok"] >= 24 and seen["state"] >= 18
+    assert seen["ok"] >= 20 and seen["state"] >= 30
+
+
+def test_lifecycle_validation_across_traces(lib):
+    """The lifecycle check over several traces at once, with sparse large
+    request ids (per-trace tables sized by the largest ARRIVE or FINISH
+    id): accepted when every trace is valid; otherwise TRE_ESTATE naming the
+    smallest trace in error, whichever trace holds it."""
+    tre, device, torch = lib
+    o = O.get()
+    M, win, nW = 3, 100, 20
+    cfg = _cfg(M, win, nW, fast_w=2, slow_w=4)
+    ARR, ADM, DEC, FIN = 0, 0x81, 2, 3
+
+    def life(rid, m, t0, t1):
+        return [(t0, m, rid, ARR, 5), (t0, m, rid, ADM, 5), (t1, m, rid, DEC, 3), (t1, m, rid, FIN, 0)]
+
+    def tr(rows):
+        return E._pack(rows)
+
+    good = [tr(life(7, 0, 10, 500) + life(3_000_000, 1, 20, 700)),
+            tr(life(1, 2, 5, 1999) + life(999_999, 0, 100, 1500) + [(1500, 0, 999_999, DEC, 2)]),
+            tr(life(42, 1, 0, 10))]
+    for t in good:
+        assert o.check_lifecycle(t) == (0, None)
+    cols, off = _columns_from_host(torch, good)
+    tre.tre_load_events(cols["ts"], cols["model"], cols["req"], cols["type"], cols["tokens"], off, cfg).close()
+    for bad_at in (0, 1, 2):
+        traces = [dict(t) for t in good]
+        rows = life(2_000_000 + bad_at, 0, 30, 600) + [(601, 0, 2_000_000 + bad_at, DEC, 1)]
+        traces[bad_at] = tr(rows + life(5, 1, 40, 50))
+        assert o.check_lifecycle(traces[bad_at]) == (-7, 2_000_000 + bad_at)
+        cols, off = _columns_from_host(torch, traces)
+        with pytest.raises(tre.TreError) as e:
+            tre.tre_load_events(cols["ts"], cols["model"], cols["req"], cols["type"], cols["tokens"], off, cfg)
+        assert e.value.code == tre.TRE_ESTATE and f"trace {bad_at}:" in str(e.value), str(e.value)
 
 
 def test_state_validation_hand_cases(lib):

@@ -87,6 +87,15 @@ MUTANTS = {
     "state_at_end_only": ("if (i == n_events - 1 || ts[i + 1] != t)", "if (i == n_events - 1)"),
     "state_own_model_only": ("for (int k = 0; k < M; ++k)\n        if (A[k] < 0", "for (int k = m; k <= m; ++k)\n        if (A[k] < 0"),
     "admits_unchecked": ("if (ids_scratch[i] == ids_scratch[i - 1]) {", "if (0) {"),
+    "lifecycle_unchecked": ("    if (arrivals > 1 || finishes > 1 || (finishes == 1 && last_ad_ts > fin_ts)) {",
+                            "    if (0) {"),
+    "lifecycle_same_instant": ("(finishes == 1 && last_ad_ts > fin_ts)", "(finishes == 1 && last_ad_ts >= fin_ts)"),
+    "lifecycle_arrivals_free": ("if (arrivals > 1 || finishes > 1", "if (finishes > 1"),
+    "lifecycle_finishes_free": ("if (arrivals > 1 || finishes > 1 ||", "if (arrivals > 1 ||"),
+    "lifecycle_decode_free": ("        if (kind == OR_ARRIVE) ++arrivals;\n        if (ts[row] > last_ad_ts) last_ad_ts = ts[row];",
+                              "        if (kind == OR_ARRIVE) ++arrivals;\n        if (kind == OR_ARRIVE && ts[row] > last_ad_ts) last_ad_ts = ts[row];"),
+    "lifecycle_prefill_counted": ("    if (kind == OR_ARRIVE || kind == OR_DECODE || kind == OR_FINISH)\n      keys_scratch",
+                                  "    if (1)\n      keys_scratch"),
     "admits_any_prefill": ("if (type[i] == (OR_PREFILL | OR_ADMIT)) ids_scratch[n++] = req[i];",
                            "if ((type[i] & 3) == OR_PREFILL) ids_scratch[n++] = req[i];"),
     "no_move_limit": ("for (uint32_t k = 0; k < sc->max_moves; ++k) {", "for (uint32_t k = 0; k < sc->max_moves + 1; ++k) {"),
