@@ -222,7 +222,7 @@ __device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
 //            queue had no room for are judged by their own threads. This
 //            overlaps phase 1 of the next tile, which touches other records.
 // Retired slots stay occupied until a rebuild re-inserts the live records
-// (when more than two thirds of the slots are in use). A trace whose table
+// (when more than half the slots are in use). A trace whose table
 // overflows (a probe run past kMaxBuckets, more than three quarters of the
 // slots live after a rebuild, more than kDeferCap FINISH rows at a tile's
 // last instant, an instant longer than a tile) stops and is listed for the
@@ -232,10 +232,12 @@ __global__ __launch_bounds__(kStreamThreads) void calib_stream(StreamParams p) {
   constexpr int kSlots = 4 * kBuckets;
   constexpr int kStreamTile = kStreamThreads * kStreamRows;
   constexpr int kSlotsPerThread = (kSlots + kStreamThreads - 1) / kStreamThreads;
-  constexpr uint32_t kRebuildAt = 2 * kSlots / 3;  // slots in use (live or retired) that trigger a rebuild
+  constexpr uint32_t kRebuildAt = kSlots / 2;      // slots in use (live or retired) that trigger a rebuild
   constexpr uint32_t kMaxLive = 3 * kSlots / 4;    // live records a rebuild may leave
   constexpr uint32_t kQueue = kStreamTile * 3 / 16;  // FINISH rows judged per tile
-  __shared__ __align__(16) uint32_t h_id[kSlots];
+  // ids; 64 words past the table are per-lane targets for the claims of
+  // rows that claim nothing (never the empty marker, so their CAS fails)
+  __shared__ __align__(16) uint32_t h_id[kSlots + 64];
   __shared__ unsigned long long h_f[kSlots];  // first DECODE: row << 32 | timestamp
   __shared__ uint32_t h_ta[kSlots];           // ARRIVE timestamp, kNone before it
   __shared__ uint32_t h_d[kSlots];            // DECODE tokens after the first DECODE
@@ -260,6 +262,7 @@ __global__ __launch_bounds__(kStreamThreads) void calib_stream(StreamParams p) {
     h_m[s] = 0;
   };
   for (int s = tid; s < kSlots; s += kStreamThreads) clear_slot(s);
+  if (tid < 64) h_id[kSlots + tid] = 0u;
   if (tid == 0) {
     s_ndef[0] = s_ndef[1] = s_ndef[2] = 0u;
     s_nq[0] = s_nq[1] = 0u;
@@ -294,11 +297,13 @@ __global__ __launch_bounds__(kStreamThreads) void calib_stream(StreamParams p) {
     return (v.x == x ? 1u : 0u) | (v.y == x ? 2u : 0u) | (v.z == x ? 4u : 0u) | (v.w == x ? 8u : 0u);
   };
   // the records of up to kN ids (`want` bit u: ids[u] wanted), found or
-  // inserted in rounds; slot[u] = -1 when a probe run ends first
+  // inserted in rounds; slot[u] = -1 when a probe run ends first. Each
+  // round reads one bucket and issues one CAS per id, all of them without
+  // branches (ids not wanted read and claim harmlessly) so that the reads,
+  // and then the CAS, are in flight together.
   auto find_or_insert = [&](auto& ids, auto& slot, uint32_t want, uint32_t& inserted) {
     constexpr int kN = sizeof(slot) / sizeof(slot[0]);
-    uint32_t bkt[kN], st[kN];
-    uint8_t probes[kN];
+    uint32_t bkt[kN], st[kN], probes[kN];
 #pragma unroll
     for (int u = 0; u < kN; ++u) {
       slot[u] = -1;
@@ -307,39 +312,33 @@ __global__ __launch_bounds__(kStreamThreads) void calib_stream(StreamParams p) {
       st[u] = stride(h);
       probes[u] = 0;
     }
+    const uint32_t dummy = (uint32_t)(kSlots + lane);
     while (want) {
       v4u32 v[kN];
-      int claim[kN];
-      uint32_t old[kN];
+      uint32_t claim[kN], old[kN];
 #pragma unroll
-      for (int u = 0; u < kN; ++u)
-        if (want >> u & 1u) v[u] = bucket_ids(bkt[u]);
+      for (int u = 0; u < kN; ++u) v[u] = bucket_ids(bkt[u]);
 #pragma unroll
       for (int u = 0; u < kN; ++u) {
-        claim[u] = -1;
-        if (!(want >> u & 1u)) continue;
+        const bool w = (want >> u & 1u) != 0;
         const uint32_t eq = mask_of(v[u], ids[u]), em = mask_of(v[u], kNone);
-        if (eq) {
-          slot[u] = (int)(4 * bkt[u] + __builtin_ctz(eq));
-          want &= ~(1u << u);
-        } else if (em) {
-          claim[u] = (int)(4 * bkt[u] + __builtin_ctz(em));
-        } else if (++probes[u] >= kMaxBuckets) {
-          want &= ~(1u << u);  // probe run ended: slot stays -1
-        } else {
-          bkt[u] = next(bkt[u], st[u]);
-        }
+        const bool found = w && eq != 0u, full = w && !eq && !em;
+        claim[u] = (w && !eq && em) ? 4 * bkt[u] + (uint32_t)__builtin_ctz(em) : dummy;
+        if (found) slot[u] = (int)(4 * bkt[u] + (uint32_t)__builtin_ctz(eq));
+        probes[u] += full ? 1u : 0u;
+        const bool ended = full && probes[u] >= (uint32_t)kMaxBuckets;  // slot stays -1
+        bkt[u] = full ? next(bkt[u], st[u]) : bkt[u];
+        want &= (found || ended) ? ~(1u << u) : ~0u;
       }
 #pragma unroll
-      for (int u = 0; u < kN; ++u)
-        if (claim[u] >= 0) old[u] = atomicCAS(&h_id[claim[u]], kNone, ids[u]);
+      for (int u = 0; u < kN; ++u) old[u] = atomicCAS(&h_id[claim[u]], kNone, ids[u]);
 #pragma unroll
       for (int u = 0; u < kN; ++u) {
         // a lost claim reads its bucket again next round
-        if (claim[u] < 0 || (old[u] != kNone && old[u] != ids[u])) continue;
-        slot[u] = claim[u];
-        want &= ~(1u << u);
-        if (old[u] == kNone) ++inserted;
+        const bool won = claim[u] != dummy && (old[u] == kNone || old[u] == ids[u]);
+        if (won) slot[u] = (int)claim[u];
+        want &= won ? ~(1u << u) : ~0u;
+        inserted += (claim[u] != dummy && old[u] == kNone) ? 1u : 0u;
       }
     }
   };
@@ -426,8 +425,7 @@ __global__ __launch_bounds__(kStreamThreads) void calib_stream(StreamParams p) {
         atomicMin(&h_f[s], ((unsigned long long)(uint32_t)(r0 + u) << 32) | cur.ts[u]);
       }
     }
-    inserted = wave_sum(inserted);
-    if (lane == 0 && inserted) atomicAdd(&s_occ, inserted);
+    if (inserted) atomicAdd(&s_occ, inserted);  // no return: nothing waits on it
     __syncthreads();
     // ---- phase 2 (the flags are settled: nothing writes them before the
     // next barrier)
@@ -442,30 +440,52 @@ __global__ __launch_bounds__(kStreamThreads) void calib_stream(StreamParams p) {
       s_ndef[(k + 1) % 3] = 0u;
       s_nq[(k + 1) & 1] = 0u;
     }
+    uint32_t fin = 0, dfr = 0;  // FINISH rows to queue, to defer
+    unsigned long long hf[kStreamRows];
+#pragma unroll
+    for (int u = 0; u < kStreamRows; ++u) hf[u] = slot[u] >= 0 ? h_f[slot[u]] : 0ull;
 #pragma unroll
     for (int u = 0; u < kStreamRows; ++u) {
       const int s = slot[u];
       const uint32_t kind = (cur.ty >> (8 * u)) & 3u;
-      if (s >= 0 && kind == TRE_DECODE && (uint32_t)(h_f[s] >> 32) == (uint32_t)(r0 + u))
+      if (s >= 0 && kind == TRE_DECODE && (uint32_t)(hf[u] >> 32) == (uint32_t)(r0 + u))
         atomicSub(&h_d[s], (cur.tok[u >> 1] >> (16 * (u & 1))) & 0xFFFFu);
-      const bool fin = s >= 0 && kind == TRE_FINISH;
-      const bool defer = fin && !last && cur.ts[u] == tl;
-      if (defer) {
+      const bool f = s >= 0 && kind == TRE_FINISH;
+      const bool d = f && !last && cur.ts[u] == tl;
+      fin |= (f && !d) ? 1u << u : 0u;
+      dfr |= d ? 1u << u : 0u;
+    }
+    if (dfr) {
+#pragma unroll
+      for (int u = 0; u < kStreamRows; ++u) {
+        if (!(dfr >> u & 1u)) continue;
         const uint32_t i = atomicAdd(&s_ndef[kd], 1u);
         if (i < (uint32_t)kDeferCap) s_def[kd][i] = cur.req[u];
         else set_over();
       }
-      // queue the others, one LDS atomic per wave
-      const unsigned long long mq = __ballot(fin && !defer);
-      if (mq) {
-        const int lead = __ffsll((long long)mq) - 1;
+    }
+    // queue the others: one LDS atomic per wave for its four row positions
+    {
+      unsigned long long mq[kStreamRows];
+      uint32_t wtot = 0;
+#pragma unroll
+      for (int u = 0; u < kStreamRows; ++u) {
+        mq[u] = __ballot((fin >> u & 1u) != 0);
+        wtot += (uint32_t)__popcll(mq[u]);
+      }
+      if (wtot) {
         uint32_t base = 0;
-        if (lane == lead) base = atomicAdd(&s_nq[k & 1], (uint32_t)__popcll(mq));
-        base = __shfl(base, lead);
-        if (fin && !defer) {
-          const uint32_t i = base + (uint32_t)__popcll(mq & ((1ull << lane) - 1ull));
-          if (i < kQueue) s_q[i] = make_uint2((uint32_t)s, cur.ts[u]);
-          else own |= 1u << u;
+        if (lane == 0) base = atomicAdd(&s_nq[k & 1], wtot);
+        base = __builtin_amdgcn_readfirstlane(base);
+        const unsigned long long below = (1ull << lane) - 1ull;
+#pragma unroll
+        for (int u = 0; u < kStreamRows; ++u) {
+          if (fin >> u & 1u) {
+            const uint32_t i = base + (uint32_t)__popcll(mq[u] & below);
+            if (i < kQueue) s_q[i] = make_uint2((uint32_t)slot[u], cur.ts[u]);
+            else own |= 1u << u;
+          }
+          base += (uint32_t)__popcll(mq[u]);
         }
       }
     }
@@ -542,8 +562,7 @@ __global__ __launch_bounds__(kStreamThreads) void calib_stream(StreamParams p) {
         h_d[s] = rd[j];
         h_m[s] = rm[j];
       }
-      again = wave_sum(again);
-      if (lane == 0 && again) atomicAdd(&s_occ, again);
+      if (again) atomicAdd(&s_occ, again);
       __syncthreads();
       if (tid == 0 && lds_load(s_occ) > kMaxLive) s_over = 1u;
     }
