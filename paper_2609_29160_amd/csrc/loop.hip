@@ -57,8 +57,13 @@ constexpr int64_t kNever = INT64_MAX;
 constexpr int32_t kArrNever = INT32_MAX;
 constexpr int kLdsMax = 160 * 1024;
 
-struct FarCell {    // tallies of one window of one model, beyond the LDS ring
-  uint32_t p, d;    // prompt / output tokens of its PREFILL / DECODE events
+// Tallies of one window of one model beyond the LDS ring, in two rings: the
+// output tokens of DECODE events (one add per output chunk) in 4-byte cells,
+// so that one window's cells of 32 models share one cache line and the few
+// dozen windows a scenario is adding into stay in L2; the rest (one or two
+// adds per request) in FarCell.
+struct FarCell {
+  uint32_t p;       // prompt tokens of its PREFILL events
   uint32_t n_fin;   // FINISH events in it
   uint32_t e_fin;   // sum over them of (window end - finish time)
 };
@@ -79,6 +84,7 @@ struct LoopParams {
   tre_loop_stats* stats;
   double* tss64;                // [scenario][window][model] or NULL
   FarCell* far;                 // [scenario][ring_len][model]
+  uint32_t* far_d;              // [scenario][ring_len][model]: output tokens
   uint32_t* scratch;            // [scenario][pool_words]: heaps in transit at a repack
   // the actuation model (the kAct instantiation)
   const int32_t* footprint;     // [trace][M] GPUs per replica, or NULL (1); the budget is then in GPUs
@@ -251,6 +257,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
   uint32_t* lane_cnt = lane_off + M;
   uint32_t* cst = lane_cnt + M + mc;
   FarCell* far = p.far + (uint64_t)s * L * M + mc;  // cell c at far[c * M]
+  uint32_t* fard = p.far_d + (uint64_t)s * L * M + mc;  // and fard[c * M]
   // initial replicas: at most r_hi per model and pool_reps in all (initial
   // replicas within the budget and the declared bound are never cut; cut
   // ones are counted as bounds exceeded)
@@ -304,7 +311,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
     for (uint32_t c = 0; c < L; ++c) {
       FarCell* fc = far + (uint64_t)c * M;
       far_store(&fc->p, 0u);
-      far_store(&fc->d, 0u);
+      far_store(&fard[(uint64_t)c * M], 0u);
       far_store(&fc->n_fin, 0u);
       far_store(&fc->e_fin, 0u);
     }
@@ -574,7 +581,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
           if (ahead < (uint32_t)kNear) {
             lds_add(near + (l - mc) + (f * kNear + (x & (kNear - 1))) * M, tok);
           } else if (ahead < L) {
-            far_add(&far[(uint64_t)(x & (L - 1)) * M + (l - mc)].p + f, tok);
+            const uint64_t fcell = (uint64_t)(x & (L - 1)) * M + (l - mc);
+            far_add(f ? &fard[fcell] : &far[fcell].p, tok);
           } else {
             ++overflow;
           }
@@ -603,15 +611,17 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
           if (fd) lds_add(nc + kNear * M, fd);
           if (fn) lds_add(nc + 2 * kNear * M, fn);
           if (fe) lds_add(nc + 3 * kNear * M, fe);
-          FarCell* fc = far + (uint64_t)((uint32_t)(w - 1 + kNear) & (L - 1)) * M;
+          const uint64_t c0 = (uint64_t)((uint32_t)(w - 1 + kNear) & (L - 1)) * M;
+          FarCell* fc = far + c0;
           far_store(&fc->p, 0u);
-          far_store(&fc->d, 0u);
+          far_store(&fard[c0], 0u);
           far_store(&fc->n_fin, 0u);
           far_store(&fc->e_fin, 0u);
         }
-        FarCell* fc = far + (uint64_t)((uint32_t)(w + kNear) & (L - 1)) * M;
+        const uint64_t c1 = (uint64_t)((uint32_t)(w + kNear) & (L - 1)) * M;
+        FarCell* fc = far + c1;
         fp = far_load(&fc->p);
-        fd = far_load(&fc->d);
+        fd = far_load(&fard[c1]);
         fn = far_load(&fc->n_fin);
         fe = far_load(&fc->e_fin);
       }
@@ -817,7 +827,7 @@ extern "C" int tre_loop_workspace_size(const tre_trace_cfg* cfg, const tre_loop_
   if (!bytes) return fail(TRE_EINVAL, "tre_loop_workspace_size: NULL bytes");
   const int rc = check_loop_args(cfg, rq);
   if (rc) return rc;
-  *bytes = (size_t)(256 + (uint64_t)n_scenarios * cfg->n_models * ring_len(cfg, rq) * sizeof(FarCell) +
+  *bytes = (size_t)(256 + (uint64_t)n_scenarios * cfg->n_models * ring_len(cfg, rq) * (sizeof(FarCell) + 4) +
                     (uint64_t)n_scenarios * pool_words(cfg, rq) * 4);
   return TRE_OK;
 }
@@ -855,7 +865,8 @@ static int loop_impl(const tre_trace_cfg* cfg, uint32_t n_traces, const tre_loop
   char* base = (char*)ws;
   unsigned long long* overflow = (unsigned long long*)base;
   FarCell* far = (FarCell*)(base + 256);
-  uint32_t* scratch = (uint32_t*)(base + 256 + (uint64_t)n_scenarios * M * L * sizeof(FarCell));
+  uint32_t* far_d = (uint32_t*)(base + 256 + (uint64_t)n_scenarios * M * L * sizeof(FarCell));
+  uint32_t* scratch = (uint32_t*)(base + 256 + (uint64_t)n_scenarios * M * L * (sizeof(FarCell) + 4));
   const size_t lds = lds_bytes(cfg, rq);
   const void* kern = act ? (const void*)loop_replay<true> : (const void*)loop_replay<false>;
   HIP_TRY(hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
@@ -876,6 +887,7 @@ static int loop_impl(const tre_trace_cfg* cfg, uint32_t n_traces, const tre_loop
   lp.stats = stats;
   lp.tss64 = tss64;
   lp.far = far;
+  lp.far_d = far_d;
   lp.scratch = scratch;
   lp.overflow = overflow;
   lp.move_cap = out->move_cap;
