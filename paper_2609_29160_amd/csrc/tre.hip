@@ -219,10 +219,11 @@ __device__ __forceinline__ void tally_row(unsigned long long* ring, uint32_t c, 
                                           uint32_t tok, uint32_t te) {
   const uint32_t code = (ty & 3u) | ((ty >> 5) & 4u);
   const uint32_t nib = __builtin_amdgcn_ubfe(kRowTable, code << 2, 4);
-  const bool life = (nib & 4u) != 0u;
-  const unsigned long long v =
-      ((unsigned long long)(life ? te : tok) << ((nib & 8u) << 2)) + (life ? (1ull << 32) : 0ull);
-  atomicAdd(&ring[c + (nib & 3u)], v);
+  const bool life = (nib & 4u) != 0u, high = (nib & 8u) != 0u;
+  // the word's two halves chosen directly: lifecycle rows (te, 1), token
+  // rows (tok, 0) or (0, tok)
+  const uint32_t lo = life ? te : (high ? 0u : tok), hi = life ? 1u : (high ? tok : 0u);
+  atomicAdd(&ring[c + (nib & 3u)], ((unsigned long long)hi << 32) | lo);
   if (code == 5u) atomicAdd((uint32_t*)&ring[c], tok);  // the admitted request's first prompt chunk
 }
 
