@@ -116,7 +116,6 @@ __device__ __forceinline__ tre_req_latency not_judged(uint32_t m) {
 typedef unsigned int v4u32 __attribute__((ext_vector_type(4)));
 typedef unsigned int v2u32 __attribute__((ext_vector_type(2)));
 
-constexpr int kStreamRows = 4;         // consecutive rows per thread and tile
 constexpr int kMaxBuckets = 32;        // buckets of one probe run
 constexpr int kDeferCap = 256;         // FINISH rows at the last instant of one tile
 constexpr uint32_t kTomb = 0xFFFFFFFEu;  // record of a judged request
@@ -125,8 +124,8 @@ constexpr unsigned long long kNone64 = ~0ull;
 // every probe step reaches every bucket): 887 buckets (two workgroups per
 // CU) for every trace, 1789 (one per CU) for the traces that overflow the
 // first
-constexpr int kBuckets1 = 887, kThreads1 = 512;
-constexpr int kBuckets2 = 1789, kThreads2 = 1024;
+constexpr int kBuckets1 = 887, kThreads1 = 768, kRows1 = 2;
+constexpr int kBuckets2 = 1789, kThreads2 = 1024, kRows2 = 4;
 
 // murmur3's 32-bit finalizer: request ids are often arithmetic sequences,
 // which a multiplicative hash alone maps to correlated buckets
@@ -167,31 +166,43 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t col_rsrc(const void* base, lon
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n, 0x00020000);
 }
 
-// one thread's four consecutive rows of a tile
+// one thread's kR (2 or 4) consecutive rows of a tile
+template <int kR>
 struct StreamRows {
-  uint32_t req[kStreamRows];
-  uint32_t ts[kStreamRows];  // low words: timestamps lie in [0, duration) below 2^32
+  uint32_t req[kR];
+  uint32_t ts[kR];  // low words: timestamps lie in [0, duration) below 2^32
   uint32_t ty, mdl;          // one byte per row
-  uint32_t tok[2];           // two 16-bit token counts per word
+  uint32_t tok[kR / 2];      // two 16-bit token counts per word
 };
 
-__device__ __forceinline__ void load_rows(StreamRows& s, const StreamRsrc& rs, int r0) {
+template <int kR>
+__device__ __forceinline__ void load_rows(StreamRows<kR>& s, const StreamRsrc& rs, int r0) {
+  static_assert(kR == 2 || kR == 4, "two or four rows per thread");
   const v4u32 t0 = __builtin_bit_cast(v4u32, __builtin_amdgcn_raw_buffer_load_b128(rs.ts, r0 * 8, 0, 0));
-  const v4u32 t1 = __builtin_bit_cast(v4u32, __builtin_amdgcn_raw_buffer_load_b128(rs.ts, r0 * 8 + 16, 0, 0));
-  const v4u32 q = __builtin_bit_cast(v4u32, __builtin_amdgcn_raw_buffer_load_b128(rs.req, r0 * 4, 0, 0));
-  const v2u32 k = __builtin_bit_cast(v2u32, __builtin_amdgcn_raw_buffer_load_b64(rs.tokens, r0 * 2, 0, 0));
-  s.ty = __builtin_amdgcn_raw_buffer_load_b32(rs.type, r0, 0, 0);
-  s.mdl = __builtin_amdgcn_raw_buffer_load_b32(rs.model, r0, 0, 0);
   s.ts[0] = t0.x;
   s.ts[1] = t0.z;
-  s.ts[2] = t1.x;
-  s.ts[3] = t1.z;
-  s.req[0] = q.x;
-  s.req[1] = q.y;
-  s.req[2] = q.z;
-  s.req[3] = q.w;
-  s.tok[0] = k.x;
-  s.tok[1] = k.y;
+  if constexpr (kR == 4) {
+    const v4u32 t1 = __builtin_bit_cast(v4u32, __builtin_amdgcn_raw_buffer_load_b128(rs.ts, r0 * 8 + 16, 0, 0));
+    const v4u32 q = __builtin_bit_cast(v4u32, __builtin_amdgcn_raw_buffer_load_b128(rs.req, r0 * 4, 0, 0));
+    const v2u32 k = __builtin_bit_cast(v2u32, __builtin_amdgcn_raw_buffer_load_b64(rs.tokens, r0 * 2, 0, 0));
+    s.ty = __builtin_amdgcn_raw_buffer_load_b32(rs.type, r0, 0, 0);
+    s.mdl = __builtin_amdgcn_raw_buffer_load_b32(rs.model, r0, 0, 0);
+    s.ts[2] = t1.x;
+    s.ts[3] = t1.z;
+    s.req[0] = q.x;
+    s.req[1] = q.y;
+    s.req[2] = q.z;
+    s.req[3] = q.w;
+    s.tok[0] = k.x;
+    s.tok[1] = k.y;
+  } else {
+    const v2u32 q = __builtin_bit_cast(v2u32, __builtin_amdgcn_raw_buffer_load_b64(rs.req, r0 * 4, 0, 0));
+    s.tok[0] = __builtin_amdgcn_raw_buffer_load_b32(rs.tokens, r0 * 2, 0, 0);
+    s.ty = __builtin_amdgcn_raw_buffer_load_b16(rs.type, r0, 0, 0);
+    s.mdl = __builtin_amdgcn_raw_buffer_load_b16(rs.model, r0, 0, 0);
+    s.req[0] = q.x;
+    s.req[1] = q.y;
+  }
 }
 
 __device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
@@ -227,7 +238,7 @@ __device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
 // slots live after a rebuild, more than kDeferCap FINISH rows at a tile's
 // last instant, an instant longer than a tile) stops and is listed for the
 // next tier, which redoes it from scratch.
-template <int kBuckets, int kStreamThreads>
+template <int kBuckets, int kStreamThreads, int kStreamRows>
 __global__ __launch_bounds__(kStreamThreads) void calib_stream(StreamParams p) {
   constexpr int kSlots = 4 * kBuckets;
   constexpr int kStreamTile = kStreamThreads * kStreamRows;
@@ -379,7 +390,7 @@ __global__ __launch_bounds__(kStreamThreads) void calib_stream(StreamParams p) {
   unsigned bad = 0;
   bool over = false;
   uint32_t tl_prev = 0;
-  StreamRows cur, nxt;
+  StreamRows<kStreamRows> cur, nxt;
   if (rend > 0) load_rows(cur, rs, tid * kStreamRows);
   int k = 0;
   for (int tb = 0; tb < rend; tb += kStreamTile, ++k) {
@@ -1352,7 +1363,7 @@ extern "C" int tre_calibrate(const tre_events* ev, const tre_slo* slo, const dou
     StreamParams sp{ev->ts, ev->model, ev->req, ev->type, ev->tokens, ev->d_off, slo, counts, reqs, bad,
                     nullptr, l1, req_cap, M, ev->cfg.window_ms, nW};
     LaunchTimer lt("calib_stream", st);
-    hipLaunchKernelGGL((calib_stream<kBuckets1, kThreads1>), dim3(ev->n_traces), dim3(kThreads1), 0, st, sp);
+    hipLaunchKernelGGL((calib_stream<kBuckets1, kThreads1, kRows1>), dim3(ev->n_traces), dim3(kThreads1), 0, st, sp);
     lt.done();
     HIP_TRY(hipGetLastError());
   }
@@ -1369,7 +1380,7 @@ extern "C" int tre_calibrate(const tre_events* ev, const tre_slo* slo, const dou
                     l1, l2, req_cap, M, ev->cfg.window_ms, nW};
     LaunchTimer lt("calib_fallback", st);
     hipLaunchKernelGGL(fb_reset, dim3(64, 16), dim3(256), 0, st, f1);
-    hipLaunchKernelGGL((calib_stream<kBuckets2, kThreads2>), dim3(ev->n_traces), dim3(kThreads2), 0, st, sp);
+    hipLaunchKernelGGL((calib_stream<kBuckets2, kThreads2, kRows2>), dim3(ev->n_traces), dim3(kThreads2), 0, st, sp);
     hipLaunchKernelGGL(fb_reset, dim3(64, 16), dim3(256), 0, st, f2);
     hipLaunchKernelGGL(calib_join, dim3(1024), dim3(256), 0, st, f2);
     hipLaunchKernelGGL(calib_judge, dim3(1024), dim3(256), 0, st, f2);

@@ -245,12 +245,12 @@ def _turnover(n, live):
     return CP._trace(rows)
 
 
-def _filler(n_rows, t0, rid0):
-    """Complete requests (5 rows each, 5 ms apart from t0) padded with
+def _filler(n_rows, t0, rid0, gap=5):
+    """Complete requests (5 rows each, `gap` ms apart from t0) padded with
     PREFILL rows of the first one to exactly n_rows rows."""
     rows, rid = [], rid0
     for j in range(n_rows // 5):
-        rows += _complete(rid, j % 2, t0 + 5 * j, 3, tok=8)
+        rows += _complete(rid, j % 2, t0 + gap * j, 3, tok=8)
         rid += 1
     pad = n_rows % 5
     if pad:
@@ -262,15 +262,21 @@ def _filler(n_rows, t0, rid0):
     return rows, rid
 
 
-def _boundary_instant(n_fin, before, order="fin_first", boundary=2048):
+# tile rows of the two stream tiers (768 threads x 2 rows, 1024 x 4) and a
+# row that is a tile boundary of both
+TILE1, TILE2 = 1536, 4096
+BOTH = 12288
+
+
+def _boundary_instant(n_fin, before, order="fin_first", boundary=TILE1):
     """n_fin requests whose FINISH and a last DECODE fall on one instant X
     whose rows start `before` rows ahead of row `boundary` (a tile boundary
-    of both stream tiers when 4096); at X the FINISH rows come all first
+    of the first tier by default, of both tiers at BOTH); at X the FINISH rows come all first
     ("fin_first"), after the DECODE rows ("dec_first") or each with its own
     DECODE behind it ("interleaved"). Filler requests before and after."""
     pre = boundary - before - 3 * n_fin
     assert pre >= 0, pre
-    rows, rid = _filler(pre, 0, 0)
+    rows, rid = _filler(pre, 0, 0, gap=max(1, min(5, 5000 // max(1, pre // 5))))
     X = 6000
     fin, dec = [], []
     for j in range(n_fin):
@@ -332,7 +338,7 @@ def test_stream_rebuild_and_instants(lib):
 
 def test_stream_fallback(lib):
     """Traces the first stream tier hands to the second (twice the records,
-    tiles of 4096 rows) and those the second hands to the chunked path: more
+    tiles of TILE2 rows) and those the second hands to the chunked path: more
     requests in flight than a table keeps, more FINISH rows at a tile's last
     instant than a tier defers, an instant longer than a tile; mixed with
     traces the first tier finishes, with ids past req_cap."""
@@ -341,7 +347,7 @@ def test_stream_fallback(lib):
               _crowded(6000),                                  # chunked: too many in flight
               _turnover(3000, 500),                            # first tier
               _boundary_instant(400, 300),                     # second tier: 300 FINISH deferred
-              _boundary_instant(400, 300, boundary=4096),      # chunked: 300 deferred in both
+              _boundary_instant(400, 300, boundary=BOTH),      # chunked: 300 deferred in both
               _long_instant(3),                                # second tier
               _long_instant(4),                                # chunked: instant longer than 4096 rows
               _turnover(2000, 300)]                            # first tier
