@@ -52,7 +52,6 @@ constexpr int kFitThreads = 1024;   // calib_fit workgroup
 constexpr int kFitWaves = kFitThreads / 64;
 constexpr int kFitMaxKPT = 16;      // keys per thread: windows up to 16384
 
-__device__ __forceinline__ uint64_t dbits(double x) { return (uint64_t)__double_as_longlong(x); }
 
 template <typename T>
 __device__ __forceinline__ T lds_load(const T& x) {
@@ -901,29 +900,64 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
   tre_fit* dst = p.fit + (uint64_t)t * p.M + m;
 
   // candidate keys to LDS in element order; non-candidates marked ~0 (no key
-  // of a finite S reaches it)
+  // of a finite S reaches it). Three rounds of loads, each issued for all KPT
+  // windows of the thread before any is waited on: the packed counts, the
+  // flags of the windows that judged a request, the TSS of the candidates. A
+  // load a lane skips gets an offset past its buffer, which reads zero and
+  // moves no bytes, so a TSS line that no model of it needs is not fetched.
+  constexpr uint32_t kSkip = 0x80000000u;  // past every buffer below (nW * M * 8 < 2^31)
+  const uint32_t Mu = (uint32_t)p.M;
+  const uint64_t tbase = (uint64_t)t * nW * Mu;
+  const __amdgpu_buffer_rsrc_t r_cnt =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t*>(cnt), (short)0, (int)(nW * 4), 0x00020000);
+  const __amdgpu_buffer_rsrc_t r_fl =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(p.flags + tbase), (short)0, (int)(nW * Mu), 0x00020000);
+  const __amdgpu_buffer_rsrc_t r_s =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<double*>(p.tss64 + tbase), (short)0, (int)(nW * Mu * 8), 0x00020000);
   uint64_t kmax = 0, kor = 0, kand = ~0ull;
   uint32_t n_real = 0, h_real = 0;
-#pragma unroll 2
-  for (int j = 0; j < KPT; ++j) {
-    const int64_t w = (int64_t)wave * KPT * 64 + j * 64 + lane;
-    uint64_t kk = ~0ull;
-    if (w < nW) {
-      const uint32_t c = cnt[w];
-      const uint32_t judged = c >> 16, ok = c & 0xFFFFu;
-      const uint64_t cell = ((uint64_t)t * nW + w) * p.M + m;
-      const uint8_t fl = p.flags[cell];
-      if (judged > 0 && (fl & TRE_FLAG_INIT) && !(fl & TRE_FLAG_IDLE)) {
-        const bool healthy = (double)ok >= s.attain_q * (double)judged;
-        kk = (dbits(p.tss64[cell]) << 1) | (healthy ? 1ull : 0ull);
+  constexpr int kLB = KPT < 8 ? KPT : 8;  // windows per batch of the three rounds
+#pragma unroll
+  for (int j0 = 0; j0 < KPT; j0 += kLB) {
+    uint32_t code[kLB];  // counts, then 0 (no candidate) or 2 | healthy
+#pragma unroll
+    for (int j = 0; j < kLB; ++j) {
+      const uint32_t w = (uint32_t)(wave * KPT * 64 + (j0 + j) * 64 + lane);
+      code[j] = __builtin_amdgcn_raw_buffer_load_b32(r_cnt, (int64_t)w < nW ? w * 4u : kSkip, 0, 0);
+    }
+    uint32_t fl[kLB];
+#pragma unroll
+    for (int j = 0; j < kLB; ++j) {
+      const uint32_t w = (uint32_t)(wave * KPT * 64 + (j0 + j) * 64 + lane);
+      fl[j] = __builtin_amdgcn_raw_buffer_load_b8(r_fl, (code[j] >> 16) ? w * Mu + m : kSkip, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < kLB; ++j) {
+      const uint32_t judged = code[j] >> 16, ok = code[j] & 0xFFFFu;
+      const bool cand = judged > 0 && (fl[j] & TRE_FLAG_INIT) && !(fl[j] & TRE_FLAG_IDLE);
+      const bool healthy = (double)ok >= s.attain_q * (double)judged;
+      code[j] = cand ? (2u | (healthy ? 1u : 0u)) : 0u;
+    }
+    uint64_t sb[kLB];
+#pragma unroll
+    for (int j = 0; j < kLB; ++j) {
+      const uint32_t w = (uint32_t)(wave * KPT * 64 + (j0 + j) * 64 + lane);
+      sb[j] = __builtin_bit_cast(uint64_t,
+                                 __builtin_amdgcn_raw_buffer_load_b64(r_s, code[j] ? (w * Mu + m) * 8u : kSkip, 0, 0));
+    }
+#pragma unroll
+    for (int j = 0; j < kLB; ++j) {
+      uint64_t kk = ~0ull;
+      if (code[j]) {
+        kk = (sb[j] << 1) | (code[j] & 1u);
         kmax = kk > kmax ? kk : kmax;
         kor |= kk;
         kand &= kk;
         ++n_real;
-        h_real += healthy ? 1u : 0u;
+        h_real += code[j] & 1u;
       }
+      keys_lds[wave * KPT * 64 + (j0 + j) * 64 + lane] = kk;
     }
-    keys_lds[wave * KPT * 64 + j * 64 + lane] = kk;
   }
   uint32_t n_cand, Ht;
   (void)block_exclusive_sum(n_real, sc32, n_cand);
