@@ -881,6 +881,9 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
   __shared__ uint32_t sc32[kFitWaves + 1];
   __shared__ uint32_t n_gathered;
   __shared__ uint32_t hpre_s[kFitThreads];  // healthy keys before each gathered position
+  __shared__ uint32_t red_n[kFitWaves];
+  __shared__ uint64_t red_k[3][kFitWaves];
+  __shared__ uint64_t s_kmin;               // smallest key of bucket b* when nothing is gathered
   static_assert(256 * kFitWaves == 2 * kBuckets, "radix histogram and bucket tables share LDS");
 
   // XCD-aware block order: consecutive blocks go to different XCDs, so the
@@ -900,11 +903,14 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
   tre_fit* dst = p.fit + (uint64_t)t * p.M + m;
 
   // candidate keys to LDS in element order; non-candidates marked ~0 (no key
-  // of a finite S reaches it). Three rounds of loads, each issued for all KPT
-  // windows of the thread before any is waited on: the packed counts, the
+  // of a finite S reaches it). Three rounds of loads, each issued for a batch
+  // of the thread's windows before any is waited on: the packed counts, the
   // flags of the windows that judged a request, the TSS of the candidates. A
   // load a lane skips gets an offset past its buffer, which reads zero and
-  // moves no bytes, so a TSS line that no model of it needs is not fetched.
+  // costs no cache-line request: the flags and TSS of one model lie M and 8M
+  // bytes apart, one line per window, and the per-CU line-request rate, not
+  // HBM, bounds this phase (a round that skips no lane is slower than the
+  // extra round trip).
   constexpr uint32_t kSkip = 0x80000000u;  // past every buffer below (nW * M * 8 < 2^31)
   const uint32_t Mu = (uint32_t)p.M;
   const uint64_t tbase = (uint64_t)t * nW * Mu;
@@ -914,18 +920,19 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(p.flags + tbase), (short)0, (int)(nW * Mu), 0x00020000);
   const __amdgpu_buffer_rsrc_t r_s =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<double*>(p.tss64 + tbase), (short)0, (int)(nW * Mu * 8), 0x00020000);
+  for (int i = tid; i < kBuckets; i += kFitThreads) hist[i] = 0;  // ordered by the reduction's barrier
+  if (tid == 0) s_kmin = ~0ull;
   uint64_t kmax = 0, kor = 0, kand = ~0ull;
   uint32_t n_real = 0, h_real = 0;
   constexpr int kLB = KPT < 8 ? KPT : 8;  // windows per batch of the three rounds
 #pragma unroll
   for (int j0 = 0; j0 < KPT; j0 += kLB) {
-    uint32_t code[kLB];  // counts, then 0 (no candidate) or 2 | healthy
+    uint32_t code[kLB], fl[kLB];  // code: counts, then 0 (no candidate) or 2 | healthy
 #pragma unroll
     for (int j = 0; j < kLB; ++j) {
       const uint32_t w = (uint32_t)(wave * KPT * 64 + (j0 + j) * 64 + lane);
       code[j] = __builtin_amdgcn_raw_buffer_load_b32(r_cnt, (int64_t)w < nW ? w * 4u : kSkip, 0, 0);
     }
-    uint32_t fl[kLB];
 #pragma unroll
     for (int j = 0; j < kLB; ++j) {
       const uint32_t w = (uint32_t)(wave * KPT * 64 + (j0 + j) * 64 + lane);
@@ -959,9 +966,34 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
       keys_lds[wave * KPT * 64 + (j0 + j) * 64 + lane] = kk;
     }
   }
-  uint32_t n_cand, Ht;
-  (void)block_exclusive_sum(n_real, sc32, n_cand);
-  (void)block_exclusive_sum(h_real, sc32, Ht);
+  // one workgroup reduction of the candidate and healthy counts (packed
+  // n << 16 | h, both at most 16384) and the keys' max, OR and AND
+  uint32_t nh = (n_real << 16) | h_real;
+  for (int o = 32; o > 0; o >>= 1) {
+    nh += (uint32_t)__shfl_xor((int)nh, o);
+    const uint64_t a = shfl_xor_u64(kmax, o);
+    kmax = a > kmax ? a : kmax;
+    kor |= shfl_xor_u64(kor, o);
+    kand &= shfl_xor_u64(kand, o);
+  }
+  if (lane == 0) {
+    red_n[wave] = nh;
+    red_k[0][wave] = kmax;
+    red_k[1][wave] = kor;
+    red_k[2][wave] = kand;
+  }
+  __syncthreads();
+  nh = 0;
+  kmax = 0;
+  kor = 0;
+  kand = ~0ull;
+  for (int v = 0; v < kFitWaves; ++v) {
+    nh += red_n[v];
+    kmax = red_k[0][v] > kmax ? red_k[0][v] : kmax;
+    kor |= red_k[1][v];
+    kand &= red_k[2][v];
+  }
+  const uint32_t n_cand = nh >> 16, Ht = nh & 0xFFFFu;
   tre_fit out;
   out.theta = INFINITY;
   out.n_cand = n_cand;
@@ -974,8 +1006,7 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
     if (tid == 0) *dst = out;
     return;
   }
-  kmax = block_reduce_u64<3>(kmax, sc64);
-  const uint64_t vary = block_reduce_u64<0>(kor, sc64) ^ block_reduce_u64<1>(kand, sc64);
+  const uint64_t vary = kor ^ kand;
   const uint64_t vary_s = vary & ~1ull;
   if (vary_s == 0) {  // one value of S: a single run covering every candidate
     if (tid == 0) {
@@ -993,8 +1024,6 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
   const int hb = 63 - __clzll((long long)vary_s);
   const int lo = hb >= 11 ? hb - 10 : 1;
   auto bucket = [&](uint64_t key) { return (uint32_t)(key >> lo) & (uint32_t)(kBuckets - 1); };
-  for (int i = tid; i < kBuckets; i += kFitThreads) hist[i] = 0;
-  __syncthreads();
 #pragma unroll 4
   for (int j = 0; j < KPT; ++j) {
     const uint64_t kk = keys_lds[wave * KPT * 64 + j * 64 + lane];
@@ -1047,6 +1076,32 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
   for (int q = 0; q < 2; ++q) mc[q] = (maybe[q] && 2u * tid + q < bstar) ? (cnts[q] & 0xFFFFu) : 0u;
   uint32_t mtot;
   const uint32_t mex = block_exclusive_sum(mc[0] + mc[1], sc32, mtot);
+  if (mtot == 0 && !p.order) {  // uniform: no bucket below b* can hold the answer
+    if (bstar != kNone) {        // b*'s first position: its smallest key
+      uint64_t kb = ~0ull;
+#pragma unroll 4
+      for (int j = 0; j < KPT; ++j) {
+        const uint64_t kk = keys_lds[wave * KPT * 64 + j * 64 + lane];
+        if (kk != ~0ull && bucket(kk) == bstar) kb = kk < kb ? kk : kb;
+      }
+      for (int o = 32; o > 0; o >>= 1) {
+        const uint64_t a = shfl_xor_u64(kb, o);
+        kb = a < kb ? a : kb;
+      }
+      if (lane == 0 && kb != ~0ull) atomicMin(&s_kmin, (unsigned long long)kb);
+      __syncthreads();
+      if (tid == (int)(bstar >> 1)) {  // the thread that holds b*'s (G, P)
+        const uint32_t GP = offs[bstar & 1u];
+        out.theta = __longlong_as_double((long long)(s_kmin >> 1));
+        out.n_above = n_cand - (GP & 0xFFFFu);
+        out.healthy_above = Ht - (GP >> 16);
+        *dst = out;
+      }
+    } else if (tid == 0) {
+      *dst = out;
+    }
+    return;
+  }
   __shared__ tre_fit s_out;
   // the keys of the listed buckets (bit 31 of their hist[kBuckets + b] entry),
   // gathered into cmp at their compact offsets and sorted (bitonic); returns
