@@ -209,22 +209,25 @@ __device__ __forceinline__ void load_slice(Slice<kEPT>& s, const TraceRsrc& rs, 
 // D, ARRIVE / ADMIT / FINISH rows (1 << 32) + te to their kind's word; an
 // ADMIT row also adds its prompt tokens to P. The word and the kind come
 // from a table indexed by code = kind | ADMIT >> 5 (4 bits per code:
-// word index, bit 2 "lifecycle word", bit 3 "high half"):
+// word index, bit 2 "high half", bit 3 "lifecycle word"):
 //   0 ARRIVE -> word 1, lifecycle; 1 PREFILL -> P; 2 DECODE -> D;
 //   3 FINISH -> word 3, lifecycle; 5 PREFILL|ADMIT -> word 2, lifecycle
 //   (+ P); 4, 6, 7 (undefined bits, unvalidated input only) -> P.
-constexpr uint32_t kRowTable = 0x00607805u;
+constexpr uint32_t kRowTable = 0x00A0B409u;
 
-__device__ __forceinline__ void tally_row(unsigned long long* ring, uint32_t c, uint32_t ty,
+// cb: byte offset of the row's cell (its word 0) in the ring
+__device__ __forceinline__ void tally_row(unsigned long long* ring, uint32_t cb, uint32_t ty,
                                           uint32_t tok, uint32_t te) {
   const uint32_t code = (ty & 3u) | ((ty >> 5) & 4u);
   const uint32_t nib = __builtin_amdgcn_ubfe(kRowTable, code << 2, 4);
-  const bool life = (nib & 4u) != 0u, high = (nib & 8u) != 0u;
-  // the word's two halves chosen directly: lifecycle rows (te, 1), token
-  // rows (tok, 0) or (0, tok)
-  const uint32_t lo = life ? te : (high ? 0u : tok), hi = life ? 1u : (high ? tok : 0u);
-  atomicAdd(&ring[c + (nib & 3u)], ((unsigned long long)hi << 32) | lo);
-  if (code == 5u) atomicAdd((uint32_t*)&ring[c], tok);  // the admitted request's first prompt chunk
+  // token rows (word 0): the tokens shifted into their half by 32 * "high
+  // half" (nib * 8 is that for them); lifecycle rows: (1 << 32) + te
+  const unsigned long long tv = (unsigned long long)tok << ((nib << 3) & 63u);
+  const bool life = nib >= 8u;
+  const uint32_t lo = life ? te : (uint32_t)tv, hi = life ? 1u : (uint32_t)(tv >> 32);
+  unsigned char* const cell = (unsigned char*)ring + cb;
+  atomicAdd((unsigned long long*)(cell + ((nib & 3u) << 3)), ((unsigned long long)hi << 32) | lo);
+  if (code == 5u) atomicAdd((uint32_t*)cell, tok);  // the admitted request's first prompt chunk
 }
 
 // General tally of the lane's rows in [e0, e_end) whose window fits the
@@ -265,7 +268,7 @@ __device__ __forceinline__ void tally_slice(const Slice<kEPT>& s, int c0, int a0
         mdl = mdl < mlast ? mdl : mlast;
         const uint32_t ty = (s.tw[j >> 2] >> (8 * (j & 3))) & 0xFFu;
         const uint32_t tok = (s.kw[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
-        tally_row(ring, ((uint32_t)w & wmask) * sstride + 4u * mdl, ty, tok, win32 - r);
+        tally_row(ring, (((uint32_t)w & wmask) * sstride + 4u * mdl) << 3, ty, tok, win32 - r);
       }
     }
   }
@@ -290,8 +293,12 @@ __device__ __forceinline__ void tally_fast(const Slice<kEPT>& s, uint32_t base_l
                                            uint32_t win32, uint32_t cbm, uint32_t wmask,
                                            uint32_t sstride, uint32_t mlast, bool last, int cbase,
                                            unsigned long long* ring, int* wlast) {
-  const uint32_t odd = 1u - 2u * base_lo;  // (ts << 1) + odd = 2d + 1
-  const uint32_t wb = win32 + base_lo;     // q * window + wb - ts = te
+  // (ts << 1) + odd = 2d + 1 (one shift-add: the compiler is not shown how
+  // odd derives from base_lo); q * window + wb - ts = te
+  uint32_t odd = 1u - 2u * base_lo;
+  __asm__("" : "+s"(odd));
+  const uint32_t wb = win32 + base_lo;
+  const uint32_t sstride8 = sstride << 3;  // ring bytes per window slot
   uint32_t ql = 0;
 #pragma unroll
   for (int j = 0; j < kEPT; ++j) {
@@ -303,7 +310,7 @@ __device__ __forceinline__ void tally_fast(const Slice<kEPT>& s, uint32_t base_l
     mdl = mdl < mlast ? mdl : mlast;
     const uint32_t ty = (s.tw[j >> 2] >> (8 * (j & 3))) & 0xFFu;
     const uint32_t tok = (s.kw[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
-    tally_row(ring, __umul24((q + cbm) & wmask, sstride) + 4u * mdl, ty, tok, te);
+    tally_row(ring, __umul24((q + cbm) & wmask, sstride8) + (mdl << 5), ty, tok, te);
   }
   if (last) *wlast = cbase + (int)ql;
 }
@@ -624,6 +631,13 @@ __device__ __forceinline__ void stream_body(const StreamParams& p) {
   // (C is a power of two and C * M <= kEvalThreads <= threads; the rest have no cell)
   const int rm = tid / C, rj = tid & (C - 1);
   const bool r_thread = rm < M;
+  // bit sh set where the lane 2^sh below lies in the same group of C lanes
+  // (rj >= 2^sh, so never for 2^sh >= C); opaque to the compiler so that it
+  // stays one per-lane register, not four lane masks held in SGPRs
+  uint32_t r_take = 0;
+#pragma unroll
+  for (int sh = 0; sh < 4; ++sh) r_take |= rj >= (1 << sh) ? 1u << sh : 0u;
+  __asm__("" : "+v"(r_take));
   double w_p = 0.0, w_q = 0.0;
   if (r_thread) {
     const tre_profile pr = p.prof[(int64_t)trace * M + rm];
@@ -916,11 +930,24 @@ __device__ __forceinline__ void stream_body(const StreamParams& p) {
       const int lw32 = (int)((uint32_t)w_arr - (uint32_t)w_adm);
       int ia = ca, iw = cw;  // inclusive prefix over the chunk's windows
       if (C <= 16) {
-        // row shifts by 1, 2, 4, 8 lanes; groups are aligned inside a row
-        if (C > 1) { const int ya = __builtin_amdgcn_update_dpp(0, ia, 0x111, 0xF, 0xF, false), yw = __builtin_amdgcn_update_dpp(0, iw, 0x111, 0xF, 0xF, false); if (rj >= 1) { ia += ya; iw += yw; } }
-        if (C > 2) { const int ya = __builtin_amdgcn_update_dpp(0, ia, 0x112, 0xF, 0xF, false), yw = __builtin_amdgcn_update_dpp(0, iw, 0x112, 0xF, 0xF, false); if (rj >= 2) { ia += ya; iw += yw; } }
-        if (C > 4) { const int ya = __builtin_amdgcn_update_dpp(0, ia, 0x114, 0xF, 0xF, false), yw = __builtin_amdgcn_update_dpp(0, iw, 0x114, 0xF, 0xF, false); if (rj >= 4) { ia += ya; iw += yw; } }
-        if (C > 8) { const int ya = __builtin_amdgcn_update_dpp(0, ia, 0x118, 0xF, 0xF, false), yw = __builtin_amdgcn_update_dpp(0, iw, 0x118, 0xF, 0xF, false); if (rj >= 8) { ia += ya; iw += yw; } }
+        uint32_t rt = r_take;  // re-read each step: the masks are not kept live across steps
+        __asm__ volatile("" : "+v"(rt));
+        // row shifts by 1, 2, 4, 8 lanes (groups are aligned inside a row),
+        // each taken where the neighbour lies in the lane's own group; the
+        // masks are per-lane integers, so no lane mask stays live in SGPRs
+#define TRE_ROW_SHR_STAGE(sh)                                                   \
+  {                                                                             \
+    const int ya = __builtin_amdgcn_mov_dpp(ia, 0x110 | (1 << (sh)), 0xF, 0xF, true); \
+    const int yw = __builtin_amdgcn_mov_dpp(iw, 0x110 | (1 << (sh)), 0xF, 0xF, true); \
+    const int mk = __builtin_amdgcn_sbfe((int)rt, (sh), 1); /* -1 or 0 */       \
+    ia += ya & mk;                                                              \
+    iw += yw & mk;                                                              \
+  }
+        TRE_ROW_SHR_STAGE(0)
+        TRE_ROW_SHR_STAGE(1)
+        TRE_ROW_SHR_STAGE(2)
+        TRE_ROW_SHR_STAGE(3)
+#undef TRE_ROW_SHR_STAGE
       } else {
         for (int dd = 1; dd < C; dd <<= 1) {
           const int ya = __shfl_up(ia, dd, C);
