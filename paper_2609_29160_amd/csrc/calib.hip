@@ -153,8 +153,15 @@ struct StreamParams {
   uint32_t req_cap;
   int32_t M;
   int64_t window_ms;
-  int64_t n_windows;
+  int64_t n_windows;             // at most 16384 (checked by tre_calibrate)
+  uint32_t magic_w;              // floor(2^32 / window_ms), 2^32 - 1 for a 1 ms window
 };
+
+// floor(2^32 / window_ms), clamped to 32 bits
+static uint32_t window_magic(int64_t window_ms) {
+  const unsigned long long m = (1ull << 32) / (unsigned long long)window_ms;
+  return m > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)m;
+}
 
 struct StreamRsrc {
   __amdgpu_buffer_rsrc_t ts, model, req, type, tokens;
@@ -374,9 +381,12 @@ __global__ __launch_bounds__(kStreamThreads) void calib_stream(StreamParams p) {
       if (f != kNone64 && m < M) {
         const tre_slo& q = slo[m];
         out = judge_one((int64_t)ta, (int64_t)(uint32_t)f, (int64_t)te, h_d[s], m, q.ttft_ms, q.tpot_ms, q.e2e_ms);
-        const int64_t w = (int64_t)ta / p.window_ms;  // window of arrival
-        if (w < p.n_windows)
-          atomicAdd(cnt + (uint64_t)m * p.n_windows + w, (1u << 16) | ((out.flags & TRE_REQ_OK) ? 1u : 0u));
+        // window of arrival, ta / window_ms: the multiply-high by magic_w
+        // undershoots by at most one (ta < 2^32, window_ms <= 2^23)
+        const uint32_t win = (uint32_t)p.window_ms, nw = (uint32_t)p.n_windows;
+        uint32_t w = __umulhi(ta, p.magic_w);
+        w += ta - w * win >= win ? 1u : 0u;
+        if (w < nw) atomicAdd(cnt + m * nw + w, (1u << 16) | ((out.flags & TRE_REQ_OK) ? 1u : 0u));
       } else {
         out = not_judged(m);
       }
@@ -1450,7 +1460,7 @@ extern "C" int tre_calibrate(const tre_events* ev, const tre_slo* slo, const dou
   HIP_TRY(hipGetLastError());
   if (ev->n_traces > 0) {
     StreamParams sp{ev->ts, ev->model, ev->req, ev->type, ev->tokens, ev->d_off, slo, counts, reqs, bad,
-                    nullptr, l1, req_cap, M, ev->cfg.window_ms, nW};
+                    nullptr, l1, req_cap, M, ev->cfg.window_ms, nW, window_magic(ev->cfg.window_ms)};
     LaunchTimer lt("calib_stream", st);
     hipLaunchKernelGGL((calib_stream<kBuckets1, kThreads1, kRows1>), dim3(ev->n_traces), dim3(kThreads1), 0, st, sp);
     lt.done();
@@ -1466,7 +1476,7 @@ extern "C" int tre_calibrate(const tre_events* ev, const tre_slo* slo, const dou
     f2.tab = tab;
     f2.fb = l2;
     StreamParams sp{ev->ts, ev->model, ev->req, ev->type, ev->tokens, ev->d_off, slo, counts, reqs, bad,
-                    l1, l2, req_cap, M, ev->cfg.window_ms, nW};
+                    l1, l2, req_cap, M, ev->cfg.window_ms, nW, window_magic(ev->cfg.window_ms)};
     LaunchTimer lt("calib_fallback", st);
     hipLaunchKernelGGL(fb_reset, dim3(64, 16), dim3(256), 0, st, f1);
     hipLaunchKernelGGL((calib_stream<kBuckets2, kThreads2, kRows2>), dim3(ev->n_traces), dim3(kThreads2), 0, st, sp);
