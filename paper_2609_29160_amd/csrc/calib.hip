@@ -791,7 +791,7 @@ struct FitParams {
   const uint32_t* counts;       // [n_traces][M][n_windows]
   const tre_slo* slo;           // [n_traces][M]
   tre_fit* fit;                 // [n_traces][M]
-  int32_t order;                // also the ordering counts (tre_calib_order)
+  int32_t order;                // also the ordering counts (tre_calib_order): calib_fit<KPT, true>
   uint32_t n_traces;
   int32_t M;
   int64_t n_windows;
@@ -882,7 +882,9 @@ constexpr int kResolveCap = 1024;   // keys sorted exactly before the radix fall
 //   4. If those keys exceed kResolveCap, every key is sorted instead (LSD
 //      radix, 8-bit digits, constant digits skipped, stable ranks from wave
 //      ballots) and every run start tested.
-template <int KPT>
+// kOrder: also the ordering counts (tre_calib_order); the instantiation
+// without them carries none of their registers.
+template <int KPT, bool kOrder>
 __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
   __shared__ uint64_t keys_lds[kFitThreads * KPT];
   __shared__ uint32_t hist[2 * kBuckets];  // buckets: counts then (G, P), compact offsets; radix: [digit][wave]
@@ -1045,6 +1047,11 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
   uint32_t tot;
   const uint32_t ex = block_exclusive_sum(v0 + v1, sc32, tot);
   const uint32_t offs[2] = {ex, ex + v0}, cnts[2] = {v0, v1};
+  // each bucket's (G, P) replaces its count (read above by this thread
+  // only): read back from LDS where needed, so that no register holds it
+  // across the scans below
+  hist[2 * tid] = offs[0];
+  hist[2 * tid + 1] = offs[1];
   // ---- 2. bucket status; the ordering counts across buckets: every key of
   // a lower bucket has a smaller S, so bucket b pairs its u unhealthy keys
   // with the P healthy keys below it (discordant) and its healthy keys with
@@ -1074,7 +1081,7 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
   }
   const uint32_t bstar = block_min_u32(qual_b, sc32);
   uint32_t D_cross = 0, C_cross = 0, HU_mixed = 0, mx_tot = 0, mx_ex = 0;
-  if (p.order) {  // uniform
+  if constexpr (kOrder) {
     (void)block_exclusive_sum(d_cross, sc32, D_cross);
     (void)block_exclusive_sum(c_cross, sc32, C_cross);
     (void)block_exclusive_sum(hu_mixed, sc32, HU_mixed);
@@ -1086,7 +1093,7 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
   for (int q = 0; q < 2; ++q) mc[q] = (maybe[q] && 2u * tid + q < bstar) ? (cnts[q] & 0xFFFFu) : 0u;
   uint32_t mtot;
   const uint32_t mex = block_exclusive_sum(mc[0] + mc[1], sc32, mtot);
-  if (mtot == 0 && !p.order) {  // uniform: no bucket below b* can hold the answer
+  if (mtot == 0 && !kOrder) {  // uniform: no bucket below b* can hold the answer
     if (bstar != kNone) {        // b*'s first position: its smallest key
       uint64_t kb = ~0ull;
 #pragma unroll 4
@@ -1100,8 +1107,8 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
       }
       if (lane == 0 && kb != ~0ull) atomicMin(&s_kmin, (unsigned long long)kb);
       __syncthreads();
-      if (tid == (int)(bstar >> 1)) {  // the thread that holds b*'s (G, P)
-        const uint32_t GP = offs[bstar & 1u];
+      if (tid == 0) {
+        const uint32_t GP = hist[bstar];
         out.theta = __longlong_as_double((long long)(s_kmin >> 1));
         out.n_above = n_cand - (GP & 0xFFFFu);
         out.healthy_above = Ht - (GP >> 16);
@@ -1144,10 +1151,9 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
     }
     ck = tid < (int)n_keys ? cmp[tid] : ~0ull;
   };
-  if (mtot <= (uint32_t)kResolveCap && (!p.order || mx_tot <= (uint32_t)kResolveCap)) {
-    // per bucket: (G, P) and the compact offset with bit 31 marking a gathered bucket
-    hist[2 * tid] = offs[0];
-    hist[2 * tid + 1] = offs[1];
+  if (mtot <= (uint32_t)kResolveCap && (!kOrder || mx_tot <= (uint32_t)kResolveCap)) {
+    // per bucket: (G, P) (written above) and the compact offset with bit 31
+    // marking a gathered bucket
     hist[kBuckets + 2 * tid] = mex | (mc[0] ? 0x80000000u : 0u);
     hist[kBuckets + 2 * tid + 1] = (mex + mc[0]) | (mc[1] ? 0x80000000u : 0u);
     uint64_t kstar = ~0ull;  // smallest key of bucket b*
@@ -1198,7 +1204,7 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
       }
     }
     __syncthreads();  // s_out written by one thread, read by thread 0
-    if (!p.order) {
+    if constexpr (!kOrder) {
       if (tid == 0) {
         out.theta = s_out.theta;
         out.n_above = s_out.n_above;
@@ -1369,7 +1375,7 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
       out.n_above = s_out.n_above;
       out.healthy_above = s_out.healthy_above;
     }
-    if (p.order) {
+    if constexpr (kOrder) {
       out.discordant = D_all;
       out.concordant = Ht * (n_cand - Ht) - D_all - T_all;
     }
@@ -1406,12 +1412,18 @@ static int launch_fit(const tre_events* ev, const tre_slo* slo, const double* ts
   const uint32_t blocks = ((ev->n_traces + 7) / 8) * 8 * (uint32_t)M;
   const int kpt = nW <= 1024 ? 1 : nW <= 2048 ? 2 : nW <= 4096 ? 4 : nW <= 8192 ? 8 : 16;
   LaunchTimer lt(order ? "calib_order" : "calib_fit", st);
-  switch (kpt) {
-    case 1: hipLaunchKernelGGL(calib_fit<1>, dim3(blocks), dim3(kFitThreads), 0, st, fp); break;
-    case 2: hipLaunchKernelGGL(calib_fit<2>, dim3(blocks), dim3(kFitThreads), 0, st, fp); break;
-    case 4: hipLaunchKernelGGL(calib_fit<4>, dim3(blocks), dim3(kFitThreads), 0, st, fp); break;
-    case 8: hipLaunchKernelGGL(calib_fit<8>, dim3(blocks), dim3(kFitThreads), 0, st, fp); break;
-    default: hipLaunchKernelGGL(calib_fit<16>, dim3(blocks), dim3(kFitThreads), 0, st, fp); break;
+  auto go = [&](auto kernel) { hipLaunchKernelGGL(kernel, dim3(blocks), dim3(kFitThreads), 0, st, fp); };
+  switch (kpt * 2 + (order ? 1 : 0)) {
+    case 2: go(calib_fit<1, false>); break;
+    case 3: go(calib_fit<1, true>); break;
+    case 4: go(calib_fit<2, false>); break;
+    case 5: go(calib_fit<2, true>); break;
+    case 8: go(calib_fit<4, false>); break;
+    case 9: go(calib_fit<4, true>); break;
+    case 16: go(calib_fit<8, false>); break;
+    case 17: go(calib_fit<8, true>); break;
+    case 32: go(calib_fit<16, false>); break;
+    default: go(calib_fit<16, true>); break;
   }
   lt.done();
   HIP_TRY(hipGetLastError());
