@@ -310,8 +310,11 @@ __global__ __launch_bounds__(kStreamThreads) void calib_stream(StreamParams p) {
   // claimed by CAS, a slot once taken stays taken (until a rebuild), so an
   // id present lies before every empty slot of its probe order
   auto bucket_ids = [&](uint32_t bk) { return *(const v4u32*)&h_id[4 * bk]; };
-  auto mask_of = [](v4u32 v, uint32_t x) {
-    return (v.x == x ? 1u : 0u) | (v.y == x ? 2u : 0u) | (v.z == x ? 4u : 0u) | (v.w == x ? 8u : 0u);
+  // the lowest of a bucket's four slots holding x, or -1 (the lowest empty
+  // one is the one every inserter of an id claims, so that two lanes adding
+  // the same id from the same read claim the same slot)
+  auto first_of = [](v4u32 v, uint32_t x) {
+    return v.x == x ? 0 : v.y == x ? 1 : v.z == x ? 2 : v.w == x ? 3 : -1;
   };
   // the records of up to kN ids (`want` bit u: ids[u] wanted), found or
   // inserted in rounds; slot[u] = -1 when a probe run ends first. Each
@@ -338,10 +341,10 @@ __global__ __launch_bounds__(kStreamThreads) void calib_stream(StreamParams p) {
 #pragma unroll
       for (int u = 0; u < kN; ++u) {
         const bool w = (want >> u & 1u) != 0;
-        const uint32_t eq = mask_of(v[u], ids[u]), em = mask_of(v[u], kNone);
-        const bool found = w && eq != 0u, full = w && !eq && !em;
-        claim[u] = (w && !eq && em) ? 4 * bkt[u] + (uint32_t)__builtin_ctz(em) : dummy;
-        if (found) slot[u] = (int)(4 * bkt[u] + (uint32_t)__builtin_ctz(eq));
+        const int ie = first_of(v[u], ids[u]), ix = first_of(v[u], kNone);
+        const bool found = w && ie >= 0, full = w && ie < 0 && ix < 0;
+        claim[u] = (w && ie < 0 && ix >= 0) ? 4 * bkt[u] + (uint32_t)ix : dummy;
+        if (found) slot[u] = (int)(4 * bkt[u]) + ie;
         probes[u] += full ? 1u : 0u;
         const bool ended = full && probes[u] >= (uint32_t)kMaxBuckets;  // slot stays -1
         bkt[u] = full ? next(bkt[u], st[u]) : bkt[u];
@@ -364,9 +367,9 @@ __global__ __launch_bounds__(kStreamThreads) void calib_stream(StreamParams p) {
     uint32_t bk = home(h);
     for (int q = 0; q < kMaxBuckets; ++q) {
       const v4u32 v = bucket_ids(bk);
-      const uint32_t eq = mask_of(v, r);
-      if (eq) return (int)(4 * bk + __builtin_ctz(eq));
-      if (mask_of(v, kNone)) return -1;
+      const int ie = first_of(v, r);
+      if (ie >= 0) return (int)(4 * bk) + ie;
+      if (first_of(v, kNone) >= 0) return -1;
       bk = next(bk, st);
     }
     return -1;
