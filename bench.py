@@ -461,9 +461,10 @@ def calibrate_main(args, w, dt, device, tre, torch, np):
     """One step = tre_eval_tss writing the per-cell smoothed TSS and flags,
     then tre_calibrate (request join, SLO attainment, theta fit) over the
     whole resident workload. Algorithmic bytes per launch: tss_stream 12 per
-    event + 9 per cell written; calib_fill 4 per cell (the counters zeroed);
-    calib_stream 16 per event (timestamp 8, request id 4, tokens 2, type 1,
-    model 1) + 8 per cell (each counter read and written back once);
+    event + 9 per cell written; calib_fill 0 (a few diagnostic words; the
+    per-request records when asked for); calib_stream 16 per event
+    (timestamp 8, request id 4, tokens 2, type 1, model 1) + 12 per cell
+    (each counter zeroed, then read and written back once by its adds);
     calib_fallback 0 (the traces the stream could not finish, none on the
     standard workloads: its launches end at once); calib_fit 13 per cell
     (counter, TSS, flags)."""
@@ -504,8 +505,8 @@ def calibrate_main(args, w, dt, device, tre, torch, np):
         tot, n = tre.tre_kernel_time(k)
         kms[k] = tot / max(n, 1)
     alg = {"tss_stream": ALG_BYTES_PER_EVENT * dt.n_events + 9 * cells,
-           "calib_fill": 4 * cells,
-           "calib_stream": 16 * dt.n_events + 8 * cells,
+           "calib_fill": 0,
+           "calib_stream": 16 * dt.n_events + 12 * cells,
            "calib_fallback": 0,
            "calib_fit": 13 * cells}
     kernels = {k: {"ms": round(kms[k], 4), "alg_bytes": alg[k],

@@ -573,8 +573,9 @@ int tre_loop_act(const tre_trace_cfg* cfg, uint32_t n_traces, const tre_loop_req
 /* Kernel timing (HIP events recorded around each launch on its stream).
    tre_set_timing(1) starts recording; tre_kernel_time waits for the
    recorded launches of `kernel` ("tss_stream", "rebalance", "validate",
-   "calib_fill", "calib_join", "calib_judge", "calib_fit", "calib_order", "loop_replay",
-   "stage_tss")
+   "calib_fill", "calib_stream", "calib_fallback" (the second stream tier
+   and the chunked path together), "calib_fit", "calib_order",
+   "loop_replay", "stage_tss")
    and returns their total milliseconds and count, then forgets them. */
 int tre_set_timing(int enable);
 int tre_kernel_time(const char* kernel, double* total_ms, uint64_t* launches);

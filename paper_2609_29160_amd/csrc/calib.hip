@@ -11,22 +11,28 @@
 // counts above the fitted boundary.
 //
 // Kernels (all on the caller's stream)
-//   fill_u32     sets the request table to all ones and the counts to zero.
-//   calib_join   one workgroup per chunk of a trace: streams (req, type,
-//                tokens), combines each request's events in an LDS hash table
-//                (minimum ARRIVE / DECODE / FINISH rows, DECODE token sum),
-//                judges the requests whose events all lie in the chunk
+//   fill_u32, fill_unseen  the diagnostic counts and tier lists to zero, the
+//                optional per-request records to the unseen pattern.
+//   calib_stream one workgroup per trace (first tier: 768 threads of two rows
+//                and a 3548-slot table; second tier: 1024 threads of four rows
+//                and twice the table, for the traces the first one lists):
+//                zeroes the trace's counters, streams its rows in tiles, keeps
+//                the requests in flight in an LDS hash table keyed by id
+//                (ARRIVE timestamp and model, first DECODE, DECODE tokens
+//                after the first), judges each request at its FINISH
 //                (latencies, SLO test, one atomic add into the arrival
-//                window's packed (judged, ok) counter) and merges the others
-//                into their 16-byte global records with atomics.
-//   calib_judge  one thread per request slot: the requests that spanned
-//                chunks or never finished, judged the same way from their
-//                records (ts, model and tokens gathered at the rows).
+//                window's packed (judged, ok) counter) and retires its slot;
+//                a trace that overflows the table is listed for the next tier.
+//   fb_reset, calib_join, calib_judge  the chunked path for the traces the
+//                second tier lists: per-chunk LDS combining merged into
+//                16-byte id-indexed records with atomics, then one thread per
+//                record judges it. It assumes nothing about row order.
 //   calib_fit    one 1024-thread workgroup per (trace, model): candidate keys
-//                (S bit pattern, health bit) in registers, an LSD radix sort
-//                in LDS (8-bit digits, constant digits skipped, stable ranks
-//                from wave ballots), then one scan for the smallest
-//                qualifying threshold.
+//                (S bit pattern, health bit) in LDS, a 2048-bucket histogram
+//                that decides most thresholds from bucket counts, a sort of
+//                the few undecided keys (bitonic in LDS; an LSD radix sort of
+//                all keys beyond 1024), and the ordering counts in its own
+//                instantiation.
 #include <hip/hip_runtime.h>
 
 #include <math.h>
@@ -285,6 +291,22 @@ __global__ __launch_bounds__(kStreamThreads) void calib_stream(StreamParams p) {
     s_nq[0] = s_nq[1] = 0u;
     s_occ = 0u;
     s_over = 0u;
+  }
+  if (!p.list_in) {
+    // the first tier zeroes its trace's counters (M * n_windows contiguous
+    // words; the base is 16-byte aligned, a trace's block need not be),
+    // overlapping the other workgroups' streams; a trace handed to a later
+    // tier has them zeroed again by that tier's reset. The barrier below
+    // orders these stores before every judge's atomic add.
+    uint32_t* const c = p.counts + (uint64_t)t * p.M * p.n_windows;
+    const uint64_t n = (uint64_t)p.M * (uint64_t)p.n_windows;
+    uint64_t head = ((16u - ((uintptr_t)c & 15u)) & 15u) / 4u;
+    head = head < n ? head : n;
+    const uint64_t n4 = (n - head) / 4u;
+    for (uint64_t i = tid; i < head; i += kStreamThreads) c[i] = 0u;
+    uint4* const c4 = (uint4*)(c + head);
+    for (uint64_t i = tid; i < n4; i += kStreamThreads) c4[i] = make_uint4(0u, 0u, 0u, 0u);
+    for (uint64_t i = head + 4u * n4 + tid; i < n; i += kStreamThreads) c[i] = 0u;
   }
   __syncthreads();
   // rows are counted from the trace's first 4-aligned row (below 2^27)
@@ -1459,12 +1481,10 @@ extern "C" int tre_calibrate(const tre_events* ev, const tre_slo* slo, const dou
   uint32_t* l1 = (uint32_t*)((char*)ws + 256);
   uint32_t* l2 = (uint32_t*)((char*)ws + 256 + calib_list_bytes(ev));
   uint32_t* tab = (uint32_t*)((char*)ws + 256 + 2 * calib_list_bytes(ev));
-  const uint64_t cnt_words = (uint64_t)ev->n_traces * M * nW;
   int64_t maxlen = 0;
   for (uint32_t i = 0; i < ev->n_traces; ++i) maxlen = std::max<int64_t>(maxlen, ev->h_off[i + 1] - ev->h_off[i]);
   {
     LaunchTimer lt("calib_fill", st);
-    hipLaunchKernelGGL(fill_u32, dim3(4096), dim3(256), 0, st, counts, cnt_words, 0u);
     hipLaunchKernelGGL(fill_u32, dim3(1), dim3(256), 0, st, (uint32_t*)bad, (uint64_t)2, 0u);
     hipLaunchKernelGGL(fill_u32, dim3(1), dim3(256), 0, st, l1, (uint64_t)1, 0u);
     hipLaunchKernelGGL(fill_u32, dim3(1), dim3(256), 0, st, l2, (uint64_t)1, 0u);
