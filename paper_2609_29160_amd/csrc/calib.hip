@@ -387,6 +387,7 @@ __global__ __launch_bounds__(kStreamThreads) void calib_stream(StreamParams p) {
   auto find = [&](uint32_t r) -> int {
     const uint32_t h = mix32(r), st = stride(h);
     uint32_t bk = home(h);
+#pragma unroll 1  // kept a loop: unrolled, its exit masks took every SGPR and spilled across the kernel
     for (int q = 0; q < kMaxBuckets; ++q) {
       const v4u32 v = bucket_ids(bk);
       const int ie = first_of(v, r);
