@@ -69,6 +69,11 @@ def _check(lib, name, cfg, traces, prof_cols, slo_cols, req_cap, check_traces=No
     tss = tre.tss_outputs(ev, which=("tss64", "flags"))
     tre.tre_eval_tss(ev, prof, tss)
     out = tre.calib_outputs(ev, req_cap, with_reqs=True)
+    # every output and the workspace start as garbage: the counters, lists
+    # and records are the library's to clear (the stream zeroes its trace's
+    # counters, the fallback tiers reset those of the traces they take)
+    for k in ("counts", "fit", "n_bad", "ws", "reqs"):
+        out[k].view(torch.uint8).fill_(0xA5)
     tre.tre_calibrate(ev, slo, tss["tss64"], tss["flags"], out)
     torch.cuda.synchronize()
     S = tss["tss64"].cpu().numpy()
