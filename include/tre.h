@@ -486,7 +486,8 @@ typedef struct {
    covers the longest service the declared bounds allow (in windows, + 2),
    plus per scenario the words of its slot-heap pool (below) as scratch.
    The pool holds min(budget, n_models * min(r_cap, budget), max_replicas
-   when nonzero) * slots_per_replica + n_models words, rounded up to 4; TRE_EINVAL when 4
+   when nonzero) * slots_per_replica + 4 x n_models words (6 x n_models when
+   slots_per_replica is not a multiple of 4), rounded up to 4; TRE_EINVAL when 4
    bytes x (that pool + 44 x n_models) exceed the 160 KiB of LDS one
    scenario's workgroup may use; TRE_ERANGE when duration_ms plus that
    longest service reaches 2^31 ms. */

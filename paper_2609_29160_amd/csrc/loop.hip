@@ -101,7 +101,7 @@ struct LoopParams {
   int32_t r_cap;
   int32_t pchunk;
   int32_t dchunk;
-  int32_t pool_words;           // the heap pool: pool_reps * spr + M (a skew word per lane), multiple of 4
+  int32_t pool_words;           // the heap pool: pool_reps * spr + 4 or 6 words per model, multiple of 4
   int32_t pool_reps;            // replicas the pool holds: min(budget, M * r_hi, the declared bound)
   uint64_t wmagic;              // x / window_ms == (x * wmagic) >> wshift for x < 2^31
   int32_t wshift;
@@ -148,45 +148,61 @@ __device__ __forceinline__ double lane_f64(double x, int l) {
   return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
 }
 
-// A lane's slot free times in LDS as a binary min-heap (node i at h[i]);
-// only the multiset of free times matters, so the heap order is free.
+// A lane's slot free times in LDS as a 4-ary min-heap: node i at h[i + 3],
+// h 16-byte aligned, so that the children 4i + 1 .. 4i + 4 of node i fill
+// the aligned group h[4i + 4 .. 4i + 7] and one LDS read fetches them all
+// (half the depth of a binary heap on the chain each start waits for). A heap
+// of n > 0 nodes owns words h[0 .. (n + 6) & ~3): the nodes from n to the end
+// hold kNone, which no free time reaches (free times stay below 2^31), so the
+// sift-down needs no bounds on a group. Only the multiset of free times
+// matters, so the heap order is free.
 struct Heap {
   uint32_t* h;
 
-  __device__ uint32_t& at(int i) const { return h[i]; }
+  __device__ uint32_t& at(int i) const { return h[i + 3]; }
 
-  // the root (the smallest) replaced by v, n nodes
-  __device__ void replace_top(int n, uint32_t v) const {
+  // words a heap of n nodes owns
+  __host__ __device__ static int words(int n) { return n > 0 ? (n + 6) & ~3 : 0; }
+
+  // the root (the smallest) replaced by v, n > 0 nodes; returns the new root
+  __device__ uint32_t replace_top(int n, uint32_t v) const {
     int i = 0;
+    uint32_t top = v;
     for (;;) {
-      int c = 2 * i + 1;
+      const int c = 4 * i + 1;
       if (c >= n) break;
-      uint32_t cv = at(c);
-      if (c + 1 < n) {
-        const uint32_t c2 = at(c + 1);
-        if (c2 < cv) {
-          cv = c2;
-          ++c;
-        }
-      }
-      if (cv >= v) break;
-      at(i) = cv;
-      i = c;
+      const uint4 q = *(const uint4*)(h + 4 * i + 4);
+      const bool b1 = q.y < q.x, b2 = q.w < q.z;
+      const uint32_t m01 = b1 ? q.y : q.x, m23 = b2 ? q.w : q.z;
+      const bool b3 = m23 < m01;
+      const uint32_t m = b3 ? m23 : m01;
+      if (m >= v) break;
+      at(i) = m;
+      top = i == 0 ? m : top;
+      i = c + (b3 ? (b2 ? 3 : 2) : (b1 ? 1 : 0));
     }
     at(i) = v;
+    return top;
   }
 
-  // v added to n nodes
+  // v added to n nodes (node n inside the words the heap owns)
   __device__ void push(int n, uint32_t v) const {
     int i = n;
     while (i > 0) {
-      const int par = (i - 1) >> 1;
+      const int par = (i - 1) >> 2;
       const uint32_t pv = at(par);
       if (pv <= v) break;
       at(i) = pv;
       i = par;
     }
     at(i) = v;
+  }
+
+  // the root removed from n > 0 nodes (its last node marked free)
+  __device__ void pop(int n) const {
+    const uint32_t last = at(n - 1);
+    at(n - 1) = kNone;
+    if (n > 1) replace_top(n - 1, last);
   }
 };
 
@@ -237,9 +253,11 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
   const uint32_t L = p.ring_len;
   const int spr = p.spr;
   const int64_t p_full = ceil_ms(p.pchunk, sv.prefill_us), d_full = ceil_ms(p.dchunk, sv.decode_us);
-  // the slot heaps: the models' heaps packed one after another (a skew word
-  // per model keeps their roots in different banks); a tick that moves
-  // replicas repacks them through the scenario's scratch in HBM
+  // the slot heaps: the models' heaps packed one after another, each in the
+  // words it owns (a multiple of 4 words, so that a root's neighbour roots lie
+  // an odd number of 16-byte groups away when the heaps are alike: different
+  // banks); a tick that moves replicas repacks them through the scenario's
+  // scratch in HBM
   uint32_t* const hpool = lds;
   uint32_t* const rest = lds + p.pool_words;
   double* const slo_t = (double*)rest + mc;  // ttft, tpot, e2e bounds at slo_t[i * M]
@@ -287,15 +305,22 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
   // whose end it completes, and the GPUs a sleep returns to the idle pool
   int tkind = 0, tuntil = 0, tret = 0;
   int hs = R * spr;  // heap size (R <= r_hi)
-  int base;          // first node in the current pool
-  {
-    int incl = hs;
+  // each lane's heap of n nodes placed after the lower lanes' (the first
+  // word of its own, a multiple of 4), its unused nodes marked free; called
+  // by the whole wave
+  auto place = [&](int n) {
+    const int own = act ? Heap::words(n) : 0;
+    int incl = own;
     for (int o = 1; o < 64; o <<= 1) {
       const int v = __shfl_up(incl, o);
       if (lane >= o) incl += v;
     }
-    base = incl - hs + mc;
-  }
+    return incl - own;
+  };
+  auto mark_free = [&](const Heap& hp, int from, int n) {
+    for (int i = from; i < Heap::words(n) - 3; ++i) hp.at(i) = kNone;
+  };
+  int base = place(hs);  // the current heap's first word in the pool
   auto heap = [&]() { return Heap{hpool + base}; };
   if (act) {
     const tre_slo sl = p.slo[tm];
@@ -307,7 +332,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
     cst[2 * M] = sv.prefill_us;
     cst[3 * M] = sv.decode_us;
     for (int i = 0; i < 4 * kNear; ++i) near[i * M] = 0u;
-    for (int i = 0; i < hs; ++i) hpool[base + i] = 0u;  // equal keys form a heap
+    const Heap h0 = heap();
+    for (int i = 0; i < hs; ++i) h0.at(i) = 0u;  // equal keys form a heap
+    mark_free(h0, hs, hs);
     for (uint32_t c = 0; c < L; ++c) {
       FarCell* fc = far + (uint64_t)c * M;
       far_store(&fc->p, 0u);
@@ -323,12 +350,11 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
   // slots, free from `from`, join there. Called by the whole wave.
   auto repack = [&](int pops, int pushes, uint32_t from) {
     const Heap old = heap();
-    for (int q = 0; q < pops && hs > 0; ++q) {
-      --hs;
-      if (hs > 0) old.replace_top(hs, old.at(hs));
-    }
+    for (int q = 0; q < pops && hs > 0; ++q) old.pop(hs--);
     // the pool holds pool_reps * spr slots: pushes beyond it (a declared
-    // replica bound exceeded) are dropped, in lane order
+    // replica bound exceeded) are dropped, in lane order (in fours when spr is
+    // a multiple of 4, so that every heap size stays one: the pool's words
+    // then count 4, not 6, beyond each heap's nodes)
     {
       int tot = hs, pin = pushes;
       for (int o = 1; o < 64; o <<= 1) {
@@ -338,22 +364,20 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
       for (int o = 32; o > 0; o >>= 1) tot += __shfl_xor(tot, o);
       int allowed = p.pool_reps * spr - tot - (pin - pushes);
       allowed = allowed < 0 ? 0 : (allowed > pushes ? pushes : allowed);
+      if (spr % 4 == 0) allowed &= ~3;
       slots_over += (unsigned)(pushes - allowed);
       pushes = allowed;
     }
     const int want = act ? hs + pushes : 0;
-    int incl = want;
-    for (int o = 1; o < 64; o <<= 1) {
-      const int v = __shfl_up(incl, o);
-      if (lane >= o) incl += v;
-    }
-    const int nbase = incl - want + mc;
+    const int nbase = place(want);
     uint32_t* tmp = p.scratch + (uint64_t)s * p.pool_words + nbase;
     if (act)
       for (int i = 0; i < hs; ++i) tmp[i] = old.at(i);
     const Heap fresh{hpool + nbase};
-    if (act)
+    if (act) {
       for (int i = 0; i < hs; ++i) fresh.at(i) = tmp[i];
+      mark_free(fresh, hs, want);
+    }
     for (int q = 0; q < pushes; ++q) fresh.push(hs + q, from);
     hs += pushes;
     base = nbase;
@@ -513,8 +537,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
               e2e_max = e2e > (int64_t)e2e_max ? (int32_t)e2e : e2e_max;
             }
           }
-          slot.replace_top(ns, tt);  // tt >= st >= the root
-          bf = slot.at(0);
+          bf = slot.replace_top(ns, tt);  // tt >= st >= the root
           ent[(0 * kEnt + cnt) * M] = (uint32_t)st;
           ent[(1 * kEnt + cnt) * M] = po;
           ent[(2 * kEnt + cnt) * M] = td;
@@ -770,8 +793,9 @@ int r_hi(const tre_trace_cfg* cfg, const tre_loop_requests* rq) {
   return rq->r_cap < cfg->budget ? rq->r_cap : cfg->budget;
 }
 
-// replicas the heap pool holds, and its words (a skew word per model), a
-// multiple of 4
+// replicas the heap pool holds, and its words: the heaps' nodes, plus up to
+// 6 words per model that the heaps own beyond their nodes (4 when every heap
+// size is a multiple of 4), a multiple of 4
 int pool_reps(const tre_trace_cfg* cfg, const tre_loop_requests* rq) {
   const int64_t all = (int64_t)cfg->n_models * r_hi(cfg, rq);
   int64_t v = cfg->budget < all ? cfg->budget : all;
@@ -779,7 +803,8 @@ int pool_reps(const tre_trace_cfg* cfg, const tre_loop_requests* rq) {
   return (int)v;
 }
 int pool_words(const tre_trace_cfg* cfg, const tre_loop_requests* rq) {
-  return (int)(((int64_t)pool_reps(cfg, rq) * rq->slots_per_replica + cfg->n_models + 3) & ~3ll);
+  const int64_t pad = rq->slots_per_replica % 4 == 0 ? 4 : 6;
+  return (int)(((int64_t)pool_reps(cfg, rq) * rq->slots_per_replica + pad * cfg->n_models + 3) & ~3ll);
 }
 
 // LDS bytes of one scenario: the slot heaps' pool, then per model its SLO
