@@ -27,8 +27,10 @@
 //                second tier lists: per-chunk LDS combining merged into
 //                16-byte id-indexed records with atomics, then one thread per
 //                record judges it. It assumes nothing about row order.
-//   calib_fit    one 1024-thread workgroup per (trace, model): candidate keys
-//                (S bit pattern, health bit) in LDS, a 2048-bucket histogram
+//   calib_fit    one 1024-thread workgroup per pair of models of a trace
+//                (one load request for both models' TSS and flags of a
+//                window), or per (trace, model): candidate keys (S bit
+//                pattern, health bit) in LDS, a 2048-bucket histogram
 //                that decides most thresholds from bucket counts, a sort of
 //                the few undecided keys (bitonic in LDS; an LSD radix sort of
 //                all keys beyond 1024), and the ordering counts in its own
@@ -885,7 +887,8 @@ __device__ __forceinline__ uint32_t block_min_u32(uint32_t v, uint32_t* sc) {
 constexpr int kBuckets = 2048;      // histogram of the fit (2^11)
 constexpr int kResolveCap = 1024;   // keys sorted exactly before the radix fallback
 
-// One 1024-thread workgroup per (trace, model). Candidate keys
+// One 1024-thread workgroup per (trace, model), or (kPair) per two models
+// fitted one after the other. Candidate keys
 // (S bit pattern << 1 | healthy) go to LDS; they order like S, and equal S
 // differ only in bit 0. A threshold at a run of equal S covers the run and
 // every larger S; in ascending order the run starts at position g, with
@@ -910,8 +913,9 @@ constexpr int kResolveCap = 1024;   // keys sorted exactly before the radix fall
 //      ballots) and every run start tested.
 // kOrder: also the ordering counts (tre_calib_order); the instantiation
 // without them carries none of their registers.
-template <int KPT, bool kOrder>
+template <int KPT, bool kOrder, bool kPair>
 __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
+  static_assert(!(kPair && kOrder), "the ordering counts take one model per workgroup");
   __shared__ uint64_t keys_lds[kFitThreads * KPT];
   __shared__ uint32_t hist[2 * kBuckets];  // buckets: counts then (G, P), compact offsets; radix: [digit][wave]
   __shared__ uint64_t cmp[kResolveCap];
@@ -919,493 +923,618 @@ __global__ __launch_bounds__(kFitThreads) void calib_fit(FitParams p) {
   __shared__ uint32_t sc32[kFitWaves + 1];
   __shared__ uint32_t n_gathered;
   __shared__ uint32_t hpre_s[kFitThreads];  // healthy keys before each gathered position
-  __shared__ uint32_t red_n[kFitWaves];
-  __shared__ uint64_t red_k[3][kFitWaves];
+  __shared__ uint32_t red_n[2][kFitWaves];  // per model of the pair
+  __shared__ uint64_t red_k[2][2][kFitWaves];  // max, min
+  __shared__ uint32_t red_o[kFitWaves];     // waves whose pair of key runs met
   __shared__ uint64_t s_kmin;               // smallest key of bucket b* when nothing is gathered
+  __shared__ tre_fit s_out;
   static_assert(256 * kFitWaves == 2 * kBuckets, "radix histogram and bucket tables share LDS");
 
   // XCD-aware block order: consecutive blocks go to different XCDs, so the
   // models of one trace are numbered to land on one XCD and share its L2
-  // for the strided per-cell reads
+  // for the strided per-cell reads. kPair: models m, m + 1 (M even), whose
+  // TSS and flags lie side by side, so one load request serves both
   const uint32_t b = blockIdx.x;
   const uint32_t xcd = b & 7u, k = b >> 3;
-  const uint32_t t = (k / (uint32_t)p.M) * 8u + xcd;
-  const uint32_t m = k % (uint32_t)p.M;
+  const uint32_t per = kPair ? (uint32_t)p.M / 2u : (uint32_t)p.M;
+  const uint32_t t = (k / per) * 8u + xcd;
+  const uint32_t m = (k % per) * (kPair ? 2u : 1u);
   if (t >= p.n_traces) return;  // whole block
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int tid = threadIdx.x;
   const int64_t nW = p.n_windows;
-  const tre_slo s = p.slo[(uint64_t)t * p.M + m];
-  const double rho = s.reliability;
-  const uint32_t* cnt = p.counts + ((uint64_t)t * p.M + m) * nW;
-  tre_fit* dst = p.fit + (uint64_t)t * p.M + m;
 
-  // candidate keys to LDS in element order; non-candidates marked ~0 (no key
-  // of a finite S reaches it). Three rounds of loads, each issued for a batch
-  // of the thread's windows before any is waited on: the packed counts, the
-  // flags of the windows that judged a request, the TSS of the candidates. A
-  // load a lane skips gets an offset past its buffer, which reads zero and
-  // costs no cache-line request: the flags and TSS of one model lie M and 8M
-  // bytes apart, one line per window, and the per-CU line-request rate, not
-  // HBM, bounds this phase (a round that skips no lane is slower than the
-  // extra round trip).
+  // candidate keys to LDS, each wave's packed from the front of its KPT * 64
+  // slots in element order (kPair: the second model's from the back). Three
+  // rounds of loads, each issued for a batch of the thread's windows before
+  // any is waited on: the packed counts, the flags of the windows that judged
+  // a request, the TSS of the candidates. A load a lane skips gets an offset
+  // past its buffer, which reads zero and costs no cache-line request: the
+  // flags and TSS of one model lie M and 8M bytes apart, one line per window,
+  // and the per-CU line-request rate, not HBM, bounds this phase (a round that
+  // skips no lane is slower than the extra round trip).
   constexpr uint32_t kSkip = 0x80000000u;  // past every buffer below (nW * M * 8 < 2^31)
+  constexpr int kCap = KPT * 64;           // key slots per wave
   const uint32_t Mu = (uint32_t)p.M;
   const uint64_t tbase = (uint64_t)t * nW * Mu;
-  const __amdgpu_buffer_rsrc_t r_cnt =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t*>(cnt), (short)0, (int)(nW * 4), 0x00020000);
   const __amdgpu_buffer_rsrc_t r_fl =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(p.flags + tbase), (short)0, (int)(nW * Mu), 0x00020000);
   const __amdgpu_buffer_rsrc_t r_s =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<double*>(p.tss64 + tbase), (short)0, (int)(nW * Mu * 8), 0x00020000);
-  for (int i = tid; i < kBuckets; i += kFitThreads) hist[i] = 0;  // ordered by the reduction's barrier
-  if (tid == 0) s_kmin = ~0ull;
-  uint64_t kmax = 0, kor = 0, kand = ~0ull;
-  uint32_t n_real = 0, h_real = 0;
+  auto cnt_rsrc = [&](uint32_t mm) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t*>(p.counts + ((uint64_t)t * p.M + mm) * nW), (short)0,
+                                             (int)(nW * 4), 0x00020000);
+  };
+  // a window's code: 0 (no candidate) or 2 | healthy
+  auto code_of = [&](uint32_t c, uint32_t fl, const tre_slo& sl) {
+    const uint32_t judged = c >> 16, ok = c & 0xFFFFu;
+    const bool cand = judged > 0 && (fl & TRE_FLAG_INIT) && !(fl & TRE_FLAG_IDLE);
+    const bool healthy = (double)ok >= sl.attain_q * (double)judged;
+    return cand ? (2u | (healthy ? 1u : 0u)) : 0u;
+  };
+  const uint64_t lt = (1ull << lane) - 1ull;
+  uint64_t* const R = keys_lds + wave * kCap;  // this wave's slots
+  struct Sum {  // a lane's keys: count, healthy count, min, max
+    uint32_t n = 0, h = 0;
+    uint64_t kmin = ~0ull, kmax = 0;
+    __device__ void add(uint64_t kk) {
+      kmin = kk < kmin ? kk : kmin;
+      kmax = kk > kmax ? kk : kmax;
+      ++n;
+      h += (uint32_t)(kk & 1ull);
+    }
+  };
   constexpr int kLB = KPT < 8 ? KPT : 8;  // windows per batch of the three rounds
+  // one model's keys from the front of the wave's slots; returns their count
+  auto load_one = [&](uint32_t mm, Sum& su) {
+    // the lane index made opaque, so that the second model's reload derives
+    // its offsets afresh instead of keeping the pair loads' ones live (in
+    // scratch) across the first model's fit
+    int ln = lane;
+    __asm__ volatile("" : "+v"(ln));
+    const uint64_t lt1 = (1ull << ln) - 1ull;
+    const tre_slo sl = p.slo[(uint64_t)t * p.M + mm];
+    const __amdgpu_buffer_rsrc_t r_cnt = cnt_rsrc(mm);
+    int f = 0;
 #pragma unroll
-  for (int j0 = 0; j0 < KPT; j0 += kLB) {
-    uint32_t code[kLB], fl[kLB];  // code: counts, then 0 (no candidate) or 2 | healthy
+    for (int j0 = 0; j0 < KPT; j0 += kLB) {
+      uint32_t code[kLB], fl[kLB];
 #pragma unroll
-    for (int j = 0; j < kLB; ++j) {
-      const uint32_t w = (uint32_t)(wave * KPT * 64 + (j0 + j) * 64 + lane);
-      code[j] = __builtin_amdgcn_raw_buffer_load_b32(r_cnt, (int64_t)w < nW ? w * 4u : kSkip, 0, 0);
-    }
-#pragma unroll
-    for (int j = 0; j < kLB; ++j) {
-      const uint32_t w = (uint32_t)(wave * KPT * 64 + (j0 + j) * 64 + lane);
-      fl[j] = __builtin_amdgcn_raw_buffer_load_b8(r_fl, (code[j] >> 16) ? w * Mu + m : kSkip, 0, 0);
-    }
-#pragma unroll
-    for (int j = 0; j < kLB; ++j) {
-      const uint32_t judged = code[j] >> 16, ok = code[j] & 0xFFFFu;
-      const bool cand = judged > 0 && (fl[j] & TRE_FLAG_INIT) && !(fl[j] & TRE_FLAG_IDLE);
-      const bool healthy = (double)ok >= s.attain_q * (double)judged;
-      code[j] = cand ? (2u | (healthy ? 1u : 0u)) : 0u;
-    }
-    uint64_t sb[kLB];
-#pragma unroll
-    for (int j = 0; j < kLB; ++j) {
-      const uint32_t w = (uint32_t)(wave * KPT * 64 + (j0 + j) * 64 + lane);
-      sb[j] = __builtin_bit_cast(uint64_t,
-                                 __builtin_amdgcn_raw_buffer_load_b64(r_s, code[j] ? (w * Mu + m) * 8u : kSkip, 0, 0));
-    }
-#pragma unroll
-    for (int j = 0; j < kLB; ++j) {
-      uint64_t kk = ~0ull;
-      if (code[j]) {
-        kk = (sb[j] << 1) | (code[j] & 1u);
-        kmax = kk > kmax ? kk : kmax;
-        kor |= kk;
-        kand &= kk;
-        ++n_real;
-        h_real += code[j] & 1u;
+      for (int j = 0; j < kLB; ++j) {
+        const uint32_t w = (uint32_t)(wave * kCap + (j0 + j) * 64 + ln);
+        code[j] = __builtin_amdgcn_raw_buffer_load_b32(r_cnt, (int64_t)w < nW ? w * 4u : kSkip, 0, 0);
       }
-      keys_lds[wave * KPT * 64 + (j0 + j) * 64 + lane] = kk;
+#pragma unroll
+      for (int j = 0; j < kLB; ++j) {
+        const uint32_t w = (uint32_t)(wave * kCap + (j0 + j) * 64 + ln);
+        fl[j] = __builtin_amdgcn_raw_buffer_load_b8(r_fl, (code[j] >> 16) ? w * Mu + mm : kSkip, 0, 0);
+      }
+#pragma unroll
+      for (int j = 0; j < kLB; ++j) code[j] = code_of(code[j], fl[j], sl);
+      uint64_t sb[kLB];
+#pragma unroll
+      for (int j = 0; j < kLB; ++j) {
+        const uint32_t w = (uint32_t)(wave * kCap + (j0 + j) * 64 + ln);
+        sb[j] = __builtin_bit_cast(uint64_t,
+                                   __builtin_amdgcn_raw_buffer_load_b64(r_s, code[j] ? (w * Mu + mm) * 8u : kSkip, 0, 0));
+      }
+#pragma unroll
+      for (int j = 0; j < kLB; ++j) {
+        const uint64_t bal = __ballot(code[j] != 0u);
+        if (code[j]) {
+          const uint64_t kk = (sb[j] << 1) | (code[j] & 1u);
+          R[f + __popcll(bal & lt1)] = kk;
+          su.add(kk);
+        }
+        f += __popcll(bal);
+      }
+    }
+    return f;
+  };
+  // hist is first used after the reduction's barrier below
+  for (int i = tid; i < kBuckets; i += kFitThreads) hist[i] = 0;
+  if (tid == 0) s_kmin = ~0ull;
+  Sum su0, su1;
+  int n0 = 0, n1 = 0;  // the wave's key counts (the second model's at the back)
+  if constexpr (!kPair) {
+    n0 = load_one(m, su0);
+  } else {
+    // both models: counts from two rows, flags as 2 bytes, TSS as 16 bytes;
+    // the second model's keys go to the back of the wave's slots while they
+    // stay above the first model's (a wave where the two runs meet reloads
+    // the second model after the first one's fit)
+    const tre_slo sl0 = p.slo[(uint64_t)t * p.M + m], sl1 = p.slo[(uint64_t)t * p.M + m + 1];
+    const __amdgpu_buffer_rsrc_t r_c0 = cnt_rsrc(m), r_c1 = cnt_rsrc(m + 1);
+    constexpr int kPB = KPT < 8 ? KPT : 8;  // windows per batch
+#pragma unroll
+    for (int j0 = 0; j0 < KPT; j0 += kPB) {
+      uint32_t c0[kPB], c1[kPB], fl[kPB];
+#pragma unroll
+      for (int j = 0; j < kPB; ++j) {
+        const uint32_t w = (uint32_t)(wave * kCap + (j0 + j) * 64 + lane);
+        const uint32_t off = (int64_t)w < nW ? w * 4u : kSkip;
+        c0[j] = __builtin_amdgcn_raw_buffer_load_b32(r_c0, off, 0, 0);
+        c1[j] = __builtin_amdgcn_raw_buffer_load_b32(r_c1, off, 0, 0);
+      }
+#pragma unroll
+      for (int j = 0; j < kPB; ++j) {
+        const uint32_t w = (uint32_t)(wave * kCap + (j0 + j) * 64 + lane);
+        fl[j] = __builtin_amdgcn_raw_buffer_load_b16(r_fl, ((c0[j] | c1[j]) >> 16) ? w * Mu + m : kSkip, 0, 0);
+      }
+#pragma unroll
+      for (int j = 0; j < kPB; ++j)  // the two codes, 2 bits each
+        c0[j] = code_of(c0[j], fl[j] & 0xFFu, sl0) | (code_of(c1[j], fl[j] >> 8, sl1) << 2);
+      __attribute__((ext_vector_type(4))) uint32_t v[kPB];
+#pragma unroll
+      for (int j = 0; j < kPB; ++j) {
+        const uint32_t w = (uint32_t)(wave * kCap + (j0 + j) * 64 + lane);
+        v[j] = __builtin_amdgcn_raw_buffer_load_b128(r_s, c0[j] ? (w * Mu + m) * 8u : kSkip, 0, 0);
+      }
+#pragma unroll
+      for (int j = 0; j < kPB; ++j) {
+        const uint32_t q0 = c0[j] & 3u, q1 = c0[j] >> 2;
+        const uint64_t bal0 = __ballot(q0 != 0u), bal1 = __ballot(q1 != 0u);
+        if (q0) {
+          const uint64_t kk = ((((uint64_t)v[j][1] << 32) | v[j][0]) << 1) | (q0 & 1u);
+          R[n0 + __popcll(bal0 & lt)] = kk;
+          su0.add(kk);
+        }
+        n0 += __popcll(bal0);
+        if (q1) {
+          const uint64_t kk = ((((uint64_t)v[j][3] << 32) | v[j][2]) << 1) | (q1 & 1u);
+          const int q = kCap - 1 - (n1 + __popcll(bal1 & lt));
+          if (q >= n0) R[q] = kk;
+          su1.add(kk);
+        }
+        n1 += __popcll(bal1);
+      }
     }
   }
-  // one workgroup reduction of the candidate and healthy counts (packed
-  // n << 16 | h, both at most 16384) and the keys' max, OR and AND
-  uint32_t nh = (n_real << 16) | h_real;
-  for (int o = 32; o > 0; o >>= 1) {
-    nh += (uint32_t)__shfl_xor((int)nh, o);
-    const uint64_t a = shfl_xor_u64(kmax, o);
-    kmax = a > kmax ? a : kmax;
-    kor |= shfl_xor_u64(kor, o);
-    kand &= shfl_xor_u64(kand, o);
-  }
-  if (lane == 0) {
-    red_n[wave] = nh;
-    red_k[0][wave] = kmax;
-    red_k[1][wave] = kor;
-    red_k[2][wave] = kand;
+  // one workgroup reduction of each model's candidate and healthy counts
+  // (packed n << 16 | h, both at most 16384) and its smallest and largest key
+  auto reduce = [&](Sum& su, int q) {
+    uint32_t nh = (su.n << 16) | su.h;
+    for (int o = 32; o > 0; o >>= 1) {
+      nh += (uint32_t)__shfl_xor((int)nh, o);
+      const uint64_t a = shfl_xor_u64(su.kmax, o);
+      su.kmax = a > su.kmax ? a : su.kmax;
+      const uint64_t b = shfl_xor_u64(su.kmin, o);
+      su.kmin = b < su.kmin ? b : su.kmin;
+    }
+    if (lane == 0) {
+      red_n[q][wave] = nh;
+      red_k[q][0][wave] = su.kmax;
+      red_k[q][1][wave] = su.kmin;
+    }
+  };
+  auto gather = [&](Sum& su, int q) {
+    uint32_t nh = 0;
+    su.kmax = 0;
+    su.kmin = ~0ull;
+    for (int v = 0; v < kFitWaves; ++v) {
+      nh += red_n[q][v];
+      su.kmax = red_k[q][0][v] > su.kmax ? red_k[q][0][v] : su.kmax;
+      su.kmin = red_k[q][1][v] < su.kmin ? red_k[q][1][v] : su.kmin;
+    }
+    su.n = nh >> 16;
+    su.h = nh & 0xFFFFu;
+  };
+  reduce(su0, 0);
+  if constexpr (kPair) {
+    reduce(su1, 1);
+    if (lane == 0) red_o[wave] = n0 + n1 > kCap ? 1u : 0u;
   }
   __syncthreads();
-  nh = 0;
-  kmax = 0;
-  kor = 0;
-  kand = ~0ull;
-  for (int v = 0; v < kFitWaves; ++v) {
-    nh += red_n[v];
-    kmax = red_k[0][v] > kmax ? red_k[0][v] : kmax;
-    kor |= red_k[1][v];
-    kand &= red_k[2][v];
-  }
-  const uint32_t n_cand = nh >> 16, Ht = nh & 0xFFFFu;
-  tre_fit out;
-  out.theta = INFINITY;
-  out.n_cand = n_cand;
-  out.n_healthy = Ht;
-  out.n_above = 0;
-  out.healthy_above = 0;
-  out.concordant = 0;  // no pair of candidates with different S: none either way
-  out.discordant = 0;
-  if (n_cand == 0) {
-    if (tid == 0) *dst = out;
-    return;
-  }
-  const uint64_t vary = kor ^ kand;
-  const uint64_t vary_s = vary & ~1ull;
-  if (vary_s == 0) {  // one value of S: a single run covering every candidate
-    if (tid == 0) {
-      if ((double)Ht >= rho * (double)n_cand) {
-        out.theta = __longlong_as_double((long long)(kmax >> 1));
-        out.n_above = n_cand;
-        out.healthy_above = Ht;
-      }
-      *dst = out;
+  gather(su0, 0);
+  // the fit of one model from this wave's keys R[roff .. roff + nk) and the
+  // workgroup's summary su, written to dst; true when it sorted every slot
+  // (the radix fallback), which overwrites the other model's keys
+  auto fit_one = [&](const int roff, const int nk, const Sum& su, const tre_slo& s, tre_fit* const dst) -> bool {
+    const double rho = s.reliability;
+    const uint32_t n_cand = su.n, Ht = su.h;
+    const uint64_t kmax = su.kmax;
+    tre_fit out;
+    out.theta = INFINITY;
+    out.n_cand = n_cand;
+    out.n_healthy = Ht;
+    out.n_above = 0;
+    out.healthy_above = 0;
+    out.concordant = 0;  // no pair of candidates with different S: none either way
+    out.discordant = 0;
+    if (n_cand == 0) {
+      if (tid == 0) *dst = out;
+      return false;
     }
-    return;
-  }
-
-  // ---- 1. histogram over buckets, packed (healthy << 16) | count
-  const int hb = 63 - __clzll((long long)vary_s);
-  const int lo = hb >= 11 ? hb - 10 : 1;
-  auto bucket = [&](uint64_t key) { return (uint32_t)(key >> lo) & (uint32_t)(kBuckets - 1); };
-#pragma unroll 4
-  for (int j = 0; j < KPT; ++j) {
-    const uint64_t kk = keys_lds[wave * KPT * 64 + j * 64 + lane];
-    if (kk != ~0ull) atomicAdd(&hist[bucket(kk)], ((uint32_t)(kk & 1ull) << 16) | 1u);
-  }
-  __syncthreads();
-  // two buckets per thread; counts and healthy counts stay below 2^16
-  const uint32_t v0 = hist[2 * tid], v1 = hist[2 * tid + 1];
-  uint32_t tot;
-  const uint32_t ex = block_exclusive_sum(v0 + v1, sc32, tot);
-  const uint32_t offs[2] = {ex, ex + v0}, cnts[2] = {v0, v1};
-  // each bucket's (G, P) replaces its count (read above by this thread
-  // only): read back from LDS where needed, so that no register holds it
-  // across the scans below
-  hist[2 * tid] = offs[0];
-  hist[2 * tid + 1] = offs[1];
-  // ---- 2. bucket status; the ordering counts across buckets: every key of
-  // a lower bucket has a smaller S, so bucket b pairs its u unhealthy keys
-  // with the P healthy keys below it (discordant) and its healthy keys with
-  // the G - P unhealthy keys below it (concordant). Pairs inside a bucket
-  // need its keys in order; only buckets holding both kinds have any.
-  uint32_t qual_b = kNone;
-  bool maybe[2];
-  uint32_t d_cross = 0, c_cross = 0, hu_mixed = 0, mixed[2];
-#pragma unroll
-  for (int q = 0; q < 2; ++q) {
-    const uint32_t c = cnts[q] & 0xFFFFu, h = cnts[q] >> 16, u = c - h;
-    const uint32_t G = offs[q] & 0xFFFFu, P = offs[q] >> 16;
-    const uint32_t N = n_cand - G, H = Ht - P;
-    d_cross += u * P;
-    c_cross += h * (G - P);
-    mixed[q] = (h != 0u && u != 0u) ? c : 0u;
-    hu_mixed += h * u;
-    maybe[q] = false;
-    if (c == 0) continue;
-    if ((double)H >= rho * (double)N) {
-      if (qual_b == kNone) qual_b = 2u * tid + q;
-    } else if (c >= 2) {
-      const bool skip = (rho >= 0.0 && rho <= 1.0) ? rho * (double)(N - u) >= (double)H + 1.0
-                                                   : (double)H < rho * (double)(N - c + 1);
-      maybe[q] = !skip;
-    }
-  }
-  const uint32_t bstar = block_min_u32(qual_b, sc32);
-  uint32_t D_cross = 0, C_cross = 0, HU_mixed = 0, mx_tot = 0, mx_ex = 0;
-  if constexpr (kOrder) {
-    (void)block_exclusive_sum(d_cross, sc32, D_cross);
-    (void)block_exclusive_sum(c_cross, sc32, C_cross);
-    (void)block_exclusive_sum(hu_mixed, sc32, HU_mixed);
-    mx_ex = block_exclusive_sum(mixed[0] + mixed[1], sc32, mx_tot);
-  }
-  // ---- 3. keys of the undecided buckets below b*
-  uint32_t mc[2];
-#pragma unroll
-  for (int q = 0; q < 2; ++q) mc[q] = (maybe[q] && 2u * tid + q < bstar) ? (cnts[q] & 0xFFFFu) : 0u;
-  uint32_t mtot;
-  const uint32_t mex = block_exclusive_sum(mc[0] + mc[1], sc32, mtot);
-  if (mtot == 0 && !kOrder) {  // uniform: no bucket below b* can hold the answer
-    if (bstar != kNone) {        // b*'s first position: its smallest key
-      uint64_t kb = ~0ull;
-#pragma unroll 4
-      for (int j = 0; j < KPT; ++j) {
-        const uint64_t kk = keys_lds[wave * KPT * 64 + j * 64 + lane];
-        if (kk != ~0ull && bucket(kk) == bstar) kb = kk < kb ? kk : kb;
-      }
-      for (int o = 32; o > 0; o >>= 1) {
-        const uint64_t a = shfl_xor_u64(kb, o);
-        kb = a < kb ? a : kb;
-      }
-      if (lane == 0 && kb != ~0ull) atomicMin(&s_kmin, (unsigned long long)kb);
-      __syncthreads();
+    // the highest bit above bit 0 where keys differ: where the smallest and
+    // the largest differ (every key shares their common prefix)
+    const uint64_t vary_s = (kmax ^ su.kmin) & ~1ull;
+    if (vary_s == 0) {  // one value of S: a single run covering every candidate
       if (tid == 0) {
-        const uint32_t GP = hist[bstar];
-        out.theta = __longlong_as_double((long long)(s_kmin >> 1));
-        out.n_above = n_cand - (GP & 0xFFFFu);
-        out.healthy_above = Ht - (GP >> 16);
+        if ((double)Ht >= rho * (double)n_cand) {
+          out.theta = __longlong_as_double((long long)(kmax >> 1));
+          out.n_above = n_cand;
+          out.healthy_above = Ht;
+        }
         *dst = out;
       }
-    } else if (tid == 0) {
-      *dst = out;
+      return false;
     }
-    return;
-  }
-  __shared__ tre_fit s_out;
-  // the keys of the listed buckets (bit 31 of their hist[kBuckets + b] entry),
-  // gathered into cmp at their compact offsets and sorted (bitonic); returns
-  // with every thread holding cmp[tid] (or ~0) in `ck`
-  auto gather_sort = [&](uint32_t n_keys, uint64_t& ck) {
-    if (tid == 0) n_gathered = 0;
-    __syncthreads();
-#pragma unroll 4
-    for (int j = 0; j < KPT; ++j) {
-      const uint64_t kk = keys_lds[wave * KPT * 64 + j * 64 + lane];
-      if (kk == ~0ull) continue;
-      if (hist[kBuckets + bucket(kk)] & 0x80000000u) cmp[atomicAdd(&n_gathered, 1u)] = kk;
+
+    // ---- 1. histogram over buckets, packed (healthy << 16) | count
+    const int hb = 63 - __clzll((long long)vary_s);
+    const int lo = hb >= 11 ? hb - 10 : 1;
+    auto bucket = [&](uint64_t key) { return (uint32_t)(key >> lo) & (uint32_t)(kBuckets - 1); };
+    for (int e = lane; e < nk; e += 64) {
+      const uint64_t kk = R[roff + e];
+      atomicAdd(&hist[bucket(kk)], ((uint32_t)(kk & 1ull) << 16) | 1u);
     }
-    uint32_t p2 = 2;
-    while (p2 < n_keys) p2 <<= 1;
-    for (uint32_t i = n_keys + tid; i < p2; i += kFitThreads) cmp[i] = ~0ull;
     __syncthreads();
-    for (uint32_t kk2 = 2; kk2 <= p2; kk2 <<= 1) {
-      for (uint32_t jj = kk2 >> 1; jj > 0; jj >>= 1) {
-        const uint32_t i = tid, ixj = tid ^ jj;
-        if (i < p2 && ixj > i) {
-          const uint64_t x = cmp[i], y = cmp[ixj];
-          if ((x > y) == ((i & kk2) == 0)) {
-            cmp[i] = y;
-            cmp[ixj] = x;
+    // two buckets per thread; counts and healthy counts stay below 2^16
+    const uint32_t v0 = hist[2 * tid], v1 = hist[2 * tid + 1];
+    uint32_t tot;
+    const uint32_t ex = block_exclusive_sum(v0 + v1, sc32, tot);
+    const uint32_t offs[2] = {ex, ex + v0}, cnts[2] = {v0, v1};
+    // each bucket's (G, P) replaces its count (read above by this thread
+    // only): read back from LDS where needed, so that no register holds it
+    // across the scans below
+    hist[2 * tid] = offs[0];
+    hist[2 * tid + 1] = offs[1];
+    // ---- 2. bucket status; the ordering counts across buckets: every key of
+    // a lower bucket has a smaller S, so bucket b pairs its u unhealthy keys
+    // with the P healthy keys below it (discordant) and its healthy keys with
+    // the G - P unhealthy keys below it (concordant). Pairs inside a bucket
+    // need its keys in order; only buckets holding both kinds have any.
+    uint32_t qual_b = kNone;
+    bool maybe[2];
+    uint32_t d_cross = 0, c_cross = 0, hu_mixed = 0, mixed[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const uint32_t c = cnts[q] & 0xFFFFu, h = cnts[q] >> 16, u = c - h;
+      const uint32_t G = offs[q] & 0xFFFFu, P = offs[q] >> 16;
+      const uint32_t N = n_cand - G, H = Ht - P;
+      d_cross += u * P;
+      c_cross += h * (G - P);
+      mixed[q] = (h != 0u && u != 0u) ? c : 0u;
+      hu_mixed += h * u;
+      maybe[q] = false;
+      if (c == 0) continue;
+      if ((double)H >= rho * (double)N) {
+        if (qual_b == kNone) qual_b = 2u * tid + q;
+      } else if (c >= 2) {
+        const bool skip = (rho >= 0.0 && rho <= 1.0) ? rho * (double)(N - u) >= (double)H + 1.0
+                                                     : (double)H < rho * (double)(N - c + 1);
+        maybe[q] = !skip;
+      }
+    }
+    const uint32_t bstar = block_min_u32(qual_b, sc32);
+    uint32_t D_cross = 0, C_cross = 0, HU_mixed = 0, mx_tot = 0, mx_ex = 0;
+    if constexpr (kOrder) {
+      (void)block_exclusive_sum(d_cross, sc32, D_cross);
+      (void)block_exclusive_sum(c_cross, sc32, C_cross);
+      (void)block_exclusive_sum(hu_mixed, sc32, HU_mixed);
+      mx_ex = block_exclusive_sum(mixed[0] + mixed[1], sc32, mx_tot);
+    }
+    // ---- 3. keys of the undecided buckets below b*
+    uint32_t mc[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) mc[q] = (maybe[q] && 2u * tid + q < bstar) ? (cnts[q] & 0xFFFFu) : 0u;
+    uint32_t mtot;
+    const uint32_t mex = block_exclusive_sum(mc[0] + mc[1], sc32, mtot);
+    if (mtot == 0 && !kOrder) {  // uniform: no bucket below b* can hold the answer
+      if (bstar != kNone) {        // b*'s first position: its smallest key
+        uint64_t kb = ~0ull;
+        for (int e = lane; e < nk; e += 64) {
+          const uint64_t kk = R[roff + e];
+          if (bucket(kk) == bstar) kb = kk < kb ? kk : kb;
+        }
+        for (int o = 32; o > 0; o >>= 1) {
+          const uint64_t a = shfl_xor_u64(kb, o);
+          kb = a < kb ? a : kb;
+        }
+        if (lane == 0 && kb != ~0ull) atomicMin(&s_kmin, (unsigned long long)kb);
+        __syncthreads();
+        if (tid == 0) {
+          const uint32_t GP = hist[bstar];
+          out.theta = __longlong_as_double((long long)(s_kmin >> 1));
+          out.n_above = n_cand - (GP & 0xFFFFu);
+          out.healthy_above = Ht - (GP >> 16);
+          *dst = out;
+        }
+      } else if (tid == 0) {
+        *dst = out;
+      }
+      return false;
+    }
+    // the keys of the listed buckets (bit 31 of their hist[kBuckets + b] entry),
+    // gathered into cmp at their compact offsets and sorted (bitonic); returns
+    // with every thread holding cmp[tid] (or ~0) in `ck`
+    auto gather_sort = [&](uint32_t n_keys, uint64_t& ck) {
+      if (tid == 0) n_gathered = 0;
+      __syncthreads();
+      for (int e = lane; e < nk; e += 64) {
+        const uint64_t kk = R[roff + e];
+        if (hist[kBuckets + bucket(kk)] & 0x80000000u) cmp[atomicAdd(&n_gathered, 1u)] = kk;
+      }
+      uint32_t p2 = 2;
+      while (p2 < n_keys) p2 <<= 1;
+      for (uint32_t i = n_keys + tid; i < p2; i += kFitThreads) cmp[i] = ~0ull;
+      __syncthreads();
+      for (uint32_t kk2 = 2; kk2 <= p2; kk2 <<= 1) {
+        for (uint32_t jj = kk2 >> 1; jj > 0; jj >>= 1) {
+          const uint32_t i = tid, ixj = tid ^ jj;
+          if (i < p2 && ixj > i) {
+            const uint64_t x = cmp[i], y = cmp[ixj];
+            if ((x > y) == ((i & kk2) == 0)) {
+              cmp[i] = y;
+              cmp[ixj] = x;
+            }
+          }
+          __syncthreads();
+        }
+      }
+      ck = tid < (int)n_keys ? cmp[tid] : ~0ull;
+    };
+    if (mtot <= (uint32_t)kResolveCap && (!kOrder || mx_tot <= (uint32_t)kResolveCap)) {
+      // per bucket: (G, P) (written above) and the compact offset with bit 31
+      // marking a gathered bucket
+      hist[kBuckets + 2 * tid] = mex | (mc[0] ? 0x80000000u : 0u);
+      hist[kBuckets + 2 * tid + 1] = (mex + mc[0]) | (mc[1] ? 0x80000000u : 0u);
+      uint64_t kstar = ~0ull;  // smallest key of bucket b*
+      for (int e = lane; e < nk; e += 64) {
+        const uint64_t kk = R[roff + e];
+        if (bucket(kk) == bstar) kstar = kk < kstar ? kk : kstar;
+      }
+      kstar = block_reduce_u64<2>(kstar, sc64);
+      uint64_t ck;
+      gather_sort(mtot, ck);
+      // healthy keys before each gathered position; the gathered keys of one
+      // bucket are contiguous, from its compact offset
+      uint32_t unused;
+      const uint32_t hpre = block_exclusive_sum(tid < (int)mtot ? (uint32_t)(ck & 1ull) : 0u, sc32, unused);
+      uint32_t* const hpre_l = hpre_s;
+      hpre_l[tid] = hpre;
+      __syncthreads();
+      uint32_t cand_g = kNone, cand_h = 0;
+      if (tid < (int)mtot) {
+        const uint32_t bk = bucket(ck);
+        const uint32_t cf = hist[kBuckets + bk] & 0x7FFFFFFFu, GP = hist[bk];
+        const uint32_t i = (uint32_t)tid - cf, g = (GP & 0xFFFFu) + i;
+        if (i == 0 || (cmp[tid - 1] >> 1) != (ck >> 1)) {
+          const uint32_t H = Ht - ((GP >> 16) + hpre - hpre_l[cf]), N = n_cand - g;
+          if ((double)H >= rho * (double)N) {
+            cand_g = g;
+            cand_h = H;
           }
         }
-        __syncthreads();
       }
-    }
-    ck = tid < (int)n_keys ? cmp[tid] : ~0ull;
-  };
-  if (mtot <= (uint32_t)kResolveCap && (!kOrder || mx_tot <= (uint32_t)kResolveCap)) {
-    // per bucket: (G, P) (written above) and the compact offset with bit 31
-    // marking a gathered bucket
-    hist[kBuckets + 2 * tid] = mex | (mc[0] ? 0x80000000u : 0u);
-    hist[kBuckets + 2 * tid + 1] = (mex + mc[0]) | (mc[1] ? 0x80000000u : 0u);
-    uint64_t kstar = ~0ull;  // smallest key of bucket b*
-#pragma unroll 4
-    for (int j = 0; j < KPT; ++j) {
-      const uint64_t kk = keys_lds[wave * KPT * 64 + j * 64 + lane];
-      if (kk != ~0ull && bucket(kk) == bstar) kstar = kk < kstar ? kk : kstar;
-    }
-    kstar = block_reduce_u64<2>(kstar, sc64);
-    uint64_t ck;
-    gather_sort(mtot, ck);
-    // healthy keys before each gathered position; the gathered keys of one
-    // bucket are contiguous, from its compact offset
-    uint32_t unused;
-    const uint32_t hpre = block_exclusive_sum(tid < (int)mtot ? (uint32_t)(ck & 1ull) : 0u, sc32, unused);
-    uint32_t* const hpre_l = hpre_s;
-    hpre_l[tid] = hpre;
-    __syncthreads();
-    uint32_t cand_g = kNone, cand_h = 0;
-    if (tid < (int)mtot) {
-      const uint32_t bk = bucket(ck);
-      const uint32_t cf = hist[kBuckets + bk] & 0x7FFFFFFFu, GP = hist[bk];
-      const uint32_t i = (uint32_t)tid - cf, g = (GP & 0xFFFFu) + i;
-      if (i == 0 || (cmp[tid - 1] >> 1) != (ck >> 1)) {
-        const uint32_t H = Ht - ((GP >> 16) + hpre - hpre_l[cf]), N = n_cand - g;
-        if ((double)H >= rho * (double)N) {
-          cand_g = g;
-          cand_h = H;
+      const uint32_t gmin = block_min_u32(cand_g, sc32);
+      if (gmin != kNone) {
+        if (cand_g == gmin) {
+          s_out.theta = __longlong_as_double((long long)(ck >> 1));
+          s_out.n_above = n_cand - gmin;
+          s_out.healthy_above = cand_h;
+        }
+      } else if (tid == 0) {
+        s_out.theta = INFINITY;
+        s_out.n_above = 0;
+        s_out.healthy_above = 0;
+        if (bstar != kNone) {
+          const uint32_t GP = hist[bstar];
+          s_out.theta = __longlong_as_double((long long)(kstar >> 1));
+          s_out.n_above = n_cand - (GP & 0xFFFFu);
+          s_out.healthy_above = Ht - (GP >> 16);
         }
       }
-    }
-    const uint32_t gmin = block_min_u32(cand_g, sc32);
-    if (gmin != kNone) {
-      if (cand_g == gmin) {
-        s_out.theta = __longlong_as_double((long long)(ck >> 1));
-        s_out.n_above = n_cand - gmin;
-        s_out.healthy_above = cand_h;
+      __syncthreads();  // s_out written by one thread, read by thread 0
+      if constexpr (!kOrder) {
+        if (tid == 0) {
+          out.theta = s_out.theta;
+          out.n_above = s_out.n_above;
+          out.healthy_above = s_out.healthy_above;
+          *dst = out;
+        }
+        return false;
       }
-    } else if (tid == 0) {
-      s_out.theta = INFINITY;
-      s_out.n_above = 0;
-      s_out.healthy_above = 0;
-      if (bstar != kNone) {
-        const uint32_t GP = hist[bstar];
-        s_out.theta = __longlong_as_double((long long)(kstar >> 1));
-        s_out.n_above = n_cand - (GP & 0xFFFFu);
-        s_out.healthy_above = Ht - (GP >> 16);
+      // ---- the ordering counts inside the buckets that hold both kinds:
+      // their keys gathered and sorted; in a run of equal S the unhealthy keys
+      // (bit 0 clear) come first, so the healthy keys before an unhealthy one
+      // inside its bucket all have a smaller S (discordant pairs); the mixed
+      // pairs of equal S are counted per run, the rest are concordant
+      hist[kBuckets + 2 * tid] = mx_ex | (mixed[0] ? 0x80000000u : 0u);
+      hist[kBuckets + 2 * tid + 1] = (mx_ex + mixed[0]) | (mixed[1] ? 0x80000000u : 0u);
+      uint64_t mk;
+      gather_sort(mx_tot, mk);
+      const bool in = tid < (int)mx_tot;
+      const uint32_t mh = block_exclusive_sum(in ? (uint32_t)(mk & 1ull) : 0u, sc32, unused);
+      hpre_l[tid] = mh;
+      __syncthreads();
+      uint32_t d_in = 0, tie = 0;
+      if (in) {
+        const uint32_t cf = hist[kBuckets + bucket(mk)] & 0x7FFFFFFFu;
+        if (!(mk & 1ull)) d_in = mh - hpre_l[cf];
+        if (tid == (int)cf || (cmp[tid - 1] >> 1) != (mk >> 1)) {  // a run start: walk the run
+          uint32_t ru = 0, rh = 0;
+          for (uint32_t i = (uint32_t)tid; i < mx_tot && (cmp[i] >> 1) == (mk >> 1); ++i) {
+            if (cmp[i] & 1ull) ++rh;
+            else ++ru;
+          }
+          tie = ru * rh;
+        }
       }
-    }
-    __syncthreads();  // s_out written by one thread, read by thread 0
-    if constexpr (!kOrder) {
+      uint32_t D_in, T_in;
+      (void)block_exclusive_sum(d_in, sc32, D_in);
+      (void)block_exclusive_sum(tie, sc32, T_in);
       if (tid == 0) {
         out.theta = s_out.theta;
         out.n_above = s_out.n_above;
         out.healthy_above = s_out.healthy_above;
+        out.discordant = D_cross + D_in;
+        out.concordant = C_cross + (HU_mixed - D_in - T_in);
         *dst = out;
       }
-      return;
+      return false;
     }
-    // ---- the ordering counts inside the buckets that hold both kinds:
-    // their keys gathered and sorted; in a run of equal S the unhealthy keys
-    // (bit 0 clear) come first, so the healthy keys before an unhealthy one
-    // inside its bucket all have a smaller S (discordant pairs); the mixed
-    // pairs of equal S are counted per run, the rest are concordant
-    hist[kBuckets + 2 * tid] = mx_ex | (mixed[0] ? 0x80000000u : 0u);
-    hist[kBuckets + 2 * tid + 1] = (mx_ex + mixed[0]) | (mixed[1] ? 0x80000000u : 0u);
-    uint64_t mk;
-    gather_sort(mx_tot, mk);
-    const bool in = tid < (int)mx_tot;
-    const uint32_t mh = block_exclusive_sum(in ? (uint32_t)(mk & 1ull) : 0u, sc32, unused);
-    hpre_l[tid] = mh;
+
+    // ---- 4. fallback: sort every slot. The slots that hold no key of this
+    // model become copies of the largest key, so they sort after every
+    // candidate; only positions below n_cand are counted. Element e lives in
+    // wave e / (KPT*64), slot (e / 64) % KPT, lane e % 64: ranks that follow
+    // (wave, slot, lane) order keep every pass stable. Digits equal in every
+    // key are skipped.
+    uint64_t k_or = 0, k_and = ~0ull;
+    for (int e = lane; e < nk; e += 64) {
+      const uint64_t kk = R[roff + e];
+      k_or |= kk;
+      k_and &= kk;
+    }
+    const uint64_t vary = block_reduce_u64<0>(k_or, sc64) ^ block_reduce_u64<1>(k_and, sc64);
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) {
+      const int e = j * 64 + lane;
+      if (e < roff || e >= roff + nk) R[e] = kmax;
+    }
     __syncthreads();
-    uint32_t d_in = 0, tie = 0;
-    if (in) {
-      const uint32_t cf = hist[kBuckets + bucket(mk)] & 0x7FFFFFFFu;
-      if (!(mk & 1ull)) d_in = mh - hpre_l[cf];
-      if (tid == (int)cf || (cmp[tid - 1] >> 1) != (mk >> 1)) {  // a run start: walk the run
+    const uint64_t lt_mask = (1ull << lane) - 1ull;
+    for (int pass = 0; pass < 8; ++pass) {
+      const int shift = pass * 8;
+      if (((vary >> shift) & 0xFFull) == 0) continue;  // digit equal in every key
+      for (int i = tid; i < 256 * kFitWaves; i += kFitThreads) hist[i] = 0;
+      __syncthreads();
+      uint32_t pos[(KPT + 1) / 2];  // ranks within the wave's digit bucket, two 16-bit halves each
+#pragma unroll
+      for (int j = 0; j < KPT; ++j) {
+        const uint32_t d = (uint32_t)(keys_lds[wave * KPT * 64 + j * 64 + lane] >> shift) & 0xFFu;
+        uint64_t peers = ~0ull;
+#pragma unroll
+        for (int bit = 0; bit < 8; ++bit) {
+          const uint64_t bl = __ballot((d >> bit) & 1u);
+          peers &= ((d >> bit) & 1u) ? bl : ~bl;
+        }
+        const uint32_t below = (uint32_t)__popcll(peers & lt_mask);
+        uint32_t* h = hist + d * kFitWaves + wave;
+        const uint32_t base = *h;
+        if (j & 1) pos[j >> 1] |= (base + below) << 16;
+        else pos[j >> 1] = base + below;
+        // the lowest lane of each digit group advances the wave's count; the
+        // loads above complete first (a wave's LDS operations stay in order)
+        __builtin_amdgcn_wave_barrier();
+        if (below == 0) *h = base + (uint32_t)__popcll(peers);
+        __builtin_amdgcn_wave_barrier();
+      }
+      __syncthreads();
+      // exclusive offsets in (digit, wave) order: 4 entries per thread
+      {
+        uint32_t* h4 = hist + tid * 4;
+        const uint32_t a0 = h4[0], a1 = h4[1], a2 = h4[2], a3 = h4[3];
+        uint32_t tot4;
+        const uint32_t base = block_exclusive_sum(a0 + a1 + a2 + a3, sc32, tot4);
+        h4[0] = base;
+        h4[1] = base + a0;
+        h4[2] = base + a0 + a1;
+        h4[3] = base + a0 + a1 + a2;
+      }
+      // every key is read before any is written back
+      uint64_t key[KPT];
+#pragma unroll
+      for (int j = 0; j < KPT; ++j) key[j] = keys_lds[wave * KPT * 64 + j * 64 + lane];
+      __syncthreads();
+#pragma unroll
+      for (int j = 0; j < KPT; ++j) {
+        const uint32_t d = (uint32_t)(key[j] >> shift) & 0xFFu;
+        keys_lds[hist[d * kFitWaves + wave] + ((pos[j >> 1] >> ((j & 1) * 16)) & 0xFFFFu)] = key[j];
+      }
+      __syncthreads();
+    }
+    // keys_lds holds the keys in ascending order; healthy count per wave (a
+    // wave's elements are one contiguous block)
+    uint32_t hsum = 0, hbits = 0;
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) {
+      const uint32_t e = (uint32_t)(wave * KPT * 64 + j * 64 + lane);
+      const uint32_t hbit = (e < n_cand) ? (uint32_t)(keys_lds[e] & 1ull) : 0u;
+      hbits |= hbit << j;
+      hsum += hbit;
+    }
+    __syncthreads();
+    for (int o = 32; o > 0; o >>= 1) hsum += __shfl_xor(hsum, o);
+    if (lane == 0) sc32[wave] = hsum;
+    __syncthreads();
+    uint32_t wbase = 0;
+    for (int w = 0; w < kFitWaves; ++w) wbase += w < wave ? sc32[w] : 0u;
+    __syncthreads();
+    uint32_t best = kNone, best_h = 0;
+    uint32_t run = wbase;  // healthy candidates before the current slot
+    // the ordering counts: an unhealthy key pairs with every healthy key
+    // before it (all of a smaller S, since in a run of equal S the unhealthy
+    // keys come first); the mixed pairs of equal S are counted per run
+    uint32_t d_all = 0, tie = 0;
+#pragma unroll
+    for (int j = 0; j < KPT; ++j) {
+      const uint32_t e = (uint32_t)(wave * KPT * 64 + j * 64 + lane);
+      const uint64_t hbal = __ballot((hbits >> j) & 1u);
+      const uint32_t before = run + (uint32_t)__popcll(hbal & lt_mask);
+      run += (uint32_t)__popcll(hbal);
+      if (e < n_cand && !((hbits >> j) & 1u)) d_all += before;
+      if (e < n_cand && (e == 0 || (keys_lds[e - 1] >> 1) != (keys_lds[e] >> 1))) {
+        const uint32_t N = n_cand - e, H = Ht - before;
+        if ((double)H >= rho * (double)N && e < best) {
+          best = e;
+          best_h = H;
+        }
         uint32_t ru = 0, rh = 0;
-        for (uint32_t i = (uint32_t)tid; i < mx_tot && (cmp[i] >> 1) == (mk >> 1); ++i) {
-          if (cmp[i] & 1ull) ++rh;
+        for (uint32_t i = e; i < n_cand && (keys_lds[i] >> 1) == (keys_lds[e] >> 1); ++i) {
+          if (keys_lds[i] & 1ull) ++rh;
           else ++ru;
         }
-        tie = ru * rh;
+        tie += ru * rh;
       }
     }
-    uint32_t D_in, T_in;
-    (void)block_exclusive_sum(d_in, sc32, D_in);
-    (void)block_exclusive_sum(tie, sc32, T_in);
+    const uint32_t g = block_min_u32(best, sc32);
+    uint32_t D_all, T_all;
+    (void)block_exclusive_sum(d_all, sc32, D_all);
+    (void)block_exclusive_sum(tie, sc32, T_all);
+    if (g != kNone && best == g) {
+      s_out.theta = __longlong_as_double((long long)(keys_lds[g] >> 1));
+      s_out.n_above = n_cand - g;
+      s_out.healthy_above = best_h;
+    }
+    __syncthreads();
     if (tid == 0) {
-      out.theta = s_out.theta;
-      out.n_above = s_out.n_above;
-      out.healthy_above = s_out.healthy_above;
-      out.discordant = D_cross + D_in;
-      out.concordant = C_cross + (HU_mixed - D_in - T_in);
+      if (g != kNone) {
+        out.theta = s_out.theta;
+        out.n_above = s_out.n_above;
+        out.healthy_above = s_out.healthy_above;
+      }
+      if constexpr (kOrder) {
+        out.discordant = D_all;
+        out.concordant = Ht * (n_cand - Ht) - D_all - T_all;
+      }
       *dst = out;
     }
-    return;
-  }
-
-  // ---- 4. fallback: sort every key. Non-candidates become copies of the
-  // largest key, so they sort after every candidate; only positions below
-  // n_cand are counted. Element e lives in wave e / (KPT*64), slot
-  // (e / 64) % KPT, lane e % 64: ranks that follow (wave, slot, lane) order
-  // keep every pass stable.
-#pragma unroll
-  for (int j = 0; j < KPT; ++j) {
-    uint64_t* q = keys_lds + wave * KPT * 64 + j * 64 + lane;
-    if (*q == ~0ull) *q = kmax;
-  }
-  __syncthreads();
-  const uint64_t lt_mask = (1ull << lane) - 1ull;
-  for (int pass = 0; pass < 8; ++pass) {
-    const int shift = pass * 8;
-    if (((vary >> shift) & 0xFFull) == 0) continue;  // digit equal in every key
-    for (int i = tid; i < 256 * kFitWaves; i += kFitThreads) hist[i] = 0;
-    __syncthreads();
-    uint32_t pos[(KPT + 1) / 2];  // ranks within the wave's digit bucket, two 16-bit halves each
-#pragma unroll
-    for (int j = 0; j < KPT; ++j) {
-      const uint32_t d = (uint32_t)(keys_lds[wave * KPT * 64 + j * 64 + lane] >> shift) & 0xFFu;
-      uint64_t peers = ~0ull;
-#pragma unroll
-      for (int bit = 0; bit < 8; ++bit) {
-        const uint64_t bl = __ballot((d >> bit) & 1u);
-        peers &= ((d >> bit) & 1u) ? bl : ~bl;
-      }
-      const uint32_t below = (uint32_t)__popcll(peers & lt_mask);
-      uint32_t* h = hist + d * kFitWaves + wave;
-      const uint32_t base = *h;
-      if (j & 1) pos[j >> 1] |= (base + below) << 16;
-      else pos[j >> 1] = base + below;
-      // the lowest lane of each digit group advances the wave's count; the
-      // loads above complete first (a wave's LDS operations stay in order)
-      __builtin_amdgcn_wave_barrier();
-      if (below == 0) *h = base + (uint32_t)__popcll(peers);
-      __builtin_amdgcn_wave_barrier();
+    return true;
+  };
+  const bool sorted_all = fit_one(0, n0, su0, p.slo[(uint64_t)t * p.M + m], p.fit + (uint64_t)t * p.M + m);
+  if constexpr (kPair) {
+    // the second model: its keys where the runs never met and the first fit
+    // left every slot in place; else loaded again on its own
+    bool met = sorted_all;
+    for (int v = 0; v < kFitWaves; ++v) met = met || red_o[v] != 0u;
+    int roff = kCap - n1;
+    __syncthreads();  // the first fit's last reads of the keys and tables
+    for (int i = tid; i < kBuckets; i += kFitThreads) hist[i] = 0;
+    if (tid == 0) s_kmin = ~0ull;
+    if (met) {
+      Sum su;
+      n1 = load_one(m + 1, su);
+      roff = 0;
+      reduce(su, 1);
     }
     __syncthreads();
-    // exclusive offsets in (digit, wave) order: 4 entries per thread
-    {
-      uint32_t* h4 = hist + tid * 4;
-      const uint32_t a0 = h4[0], a1 = h4[1], a2 = h4[2], a3 = h4[3];
-      uint32_t tot4;
-      const uint32_t base = block_exclusive_sum(a0 + a1 + a2 + a3, sc32, tot4);
-      h4[0] = base;
-      h4[1] = base + a0;
-      h4[2] = base + a0 + a1;
-      h4[3] = base + a0 + a1 + a2;
-    }
-    // every key is read before any is written back
-    uint64_t key[KPT];
-#pragma unroll
-    for (int j = 0; j < KPT; ++j) key[j] = keys_lds[wave * KPT * 64 + j * 64 + lane];
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < KPT; ++j) {
-      const uint32_t d = (uint32_t)(key[j] >> shift) & 0xFFu;
-      keys_lds[hist[d * kFitWaves + wave] + ((pos[j >> 1] >> ((j & 1) * 16)) & 0xFFFFu)] = key[j];
-    }
-    __syncthreads();
-  }
-  // keys_lds holds the keys in ascending order; healthy count per wave (a
-  // wave's elements are one contiguous block)
-  uint32_t hsum = 0, hbits = 0;
-#pragma unroll
-  for (int j = 0; j < KPT; ++j) {
-    const uint32_t e = (uint32_t)(wave * KPT * 64 + j * 64 + lane);
-    const uint32_t hbit = (e < n_cand) ? (uint32_t)(keys_lds[e] & 1ull) : 0u;
-    hbits |= hbit << j;
-    hsum += hbit;
-  }
-  __syncthreads();
-  for (int o = 32; o > 0; o >>= 1) hsum += __shfl_xor(hsum, o);
-  if (lane == 0) sc32[wave] = hsum;
-  __syncthreads();
-  uint32_t wbase = 0;
-  for (int w = 0; w < kFitWaves; ++w) wbase += w < wave ? sc32[w] : 0u;
-  __syncthreads();
-  uint32_t best = kNone, best_h = 0;
-  uint32_t run = wbase;  // healthy candidates before the current slot
-  // the ordering counts: an unhealthy key pairs with every healthy key
-  // before it (all of a smaller S, since in a run of equal S the unhealthy
-  // keys come first); the mixed pairs of equal S are counted per run
-  uint32_t d_all = 0, tie = 0;
-#pragma unroll
-  for (int j = 0; j < KPT; ++j) {
-    const uint32_t e = (uint32_t)(wave * KPT * 64 + j * 64 + lane);
-    const uint64_t hbal = __ballot((hbits >> j) & 1u);
-    const uint32_t before = run + (uint32_t)__popcll(hbal & lt_mask);
-    run += (uint32_t)__popcll(hbal);
-    if (e < n_cand && !((hbits >> j) & 1u)) d_all += before;
-    if (e < n_cand && (e == 0 || (keys_lds[e - 1] >> 1) != (keys_lds[e] >> 1))) {
-      const uint32_t N = n_cand - e, H = Ht - before;
-      if ((double)H >= rho * (double)N && e < best) {
-        best = e;
-        best_h = H;
-      }
-      uint32_t ru = 0, rh = 0;
-      for (uint32_t i = e; i < n_cand && (keys_lds[i] >> 1) == (keys_lds[e] >> 1); ++i) {
-        if (keys_lds[i] & 1ull) ++rh;
-        else ++ru;
-      }
-      tie += ru * rh;
-    }
-  }
-  const uint32_t g = block_min_u32(best, sc32);
-  uint32_t D_all, T_all;
-  (void)block_exclusive_sum(d_all, sc32, D_all);
-  (void)block_exclusive_sum(tie, sc32, T_all);
-  if (g != kNone && best == g) {
-    s_out.theta = __longlong_as_double((long long)(keys_lds[g] >> 1));
-    s_out.n_above = n_cand - g;
-    s_out.healthy_above = best_h;
-  }
-  __syncthreads();
-  if (tid == 0) {
-    if (g != kNone) {
-      out.theta = s_out.theta;
-      out.n_above = s_out.n_above;
-      out.healthy_above = s_out.healthy_above;
-    }
-    if constexpr (kOrder) {
-      out.discordant = D_all;
-      out.concordant = Ht * (n_cand - Ht) - D_all - T_all;
-    }
-    *dst = out;
+    Sum su1w;
+    gather(su1w, 1);
+    (void)fit_one(roff, n1, su1w, p.slo[(uint64_t)t * p.M + m + 1], p.fit + (uint64_t)t * p.M + m + 1);
+  } else {
+    (void)sorted_all;
   }
 }
 
@@ -1435,21 +1564,29 @@ static int launch_fit(const tre_events* ev, const tre_slo* slo, const double* ts
   const int M = ev->cfg.n_models;
   const int64_t nW = ev->n_windows;
   FitParams fp{tss64, flags, counts, slo, fit, order, ev->n_traces, M, nW};
-  const uint32_t blocks = ((ev->n_traces + 7) / 8) * 8 * (uint32_t)M;
+  // models in pairs (one load request for both models' TSS and flags) when
+  // their pairs' TSS are 16-byte aligned and their flags 2-byte aligned
+  const bool pair = !order && M % 2 == 0 && ((uintptr_t)tss64 & 15) == 0 && ((uintptr_t)flags & 1) == 0;
+  const uint32_t blocks = ((ev->n_traces + 7) / 8) * 8 * (uint32_t)(pair ? M / 2 : M);
   const int kpt = nW <= 1024 ? 1 : nW <= 2048 ? 2 : nW <= 4096 ? 4 : nW <= 8192 ? 8 : 16;
   LaunchTimer lt(order ? "calib_order" : "calib_fit", st);
   auto go = [&](auto kernel) { hipLaunchKernelGGL(kernel, dim3(blocks), dim3(kFitThreads), 0, st, fp); };
-  switch (kpt * 2 + (order ? 1 : 0)) {
-    case 2: go(calib_fit<1, false>); break;
-    case 3: go(calib_fit<1, true>); break;
-    case 4: go(calib_fit<2, false>); break;
-    case 5: go(calib_fit<2, true>); break;
-    case 8: go(calib_fit<4, false>); break;
-    case 9: go(calib_fit<4, true>); break;
-    case 16: go(calib_fit<8, false>); break;
-    case 17: go(calib_fit<8, true>); break;
-    case 32: go(calib_fit<16, false>); break;
-    default: go(calib_fit<16, true>); break;
+  switch (kpt * 4 + (order ? 1 : 0) + (pair ? 2 : 0)) {
+    case 4: go(calib_fit<1, false, false>); break;
+    case 5: go(calib_fit<1, true, false>); break;
+    case 6: go(calib_fit<1, false, true>); break;
+    case 8: go(calib_fit<2, false, false>); break;
+    case 9: go(calib_fit<2, true, false>); break;
+    case 10: go(calib_fit<2, false, true>); break;
+    case 16: go(calib_fit<4, false, false>); break;
+    case 17: go(calib_fit<4, true, false>); break;
+    case 18: go(calib_fit<4, false, true>); break;
+    case 32: go(calib_fit<8, false, false>); break;
+    case 33: go(calib_fit<8, true, false>); break;
+    case 34: go(calib_fit<8, false, true>); break;
+    case 64: go(calib_fit<16, false, false>); break;
+    case 65: go(calib_fit<16, true, false>); break;
+    default: go(calib_fit<16, false, true>); break;
   }
   lt.done();
   HIP_TRY(hipGetLastError());

@@ -432,19 +432,28 @@ def _fit_cases(nW, seed):
             (base, base + rng.normal(0.0, 3.0, nW) > 40, 0.95)]
 
 
-@pytest.mark.parametrize("nW,seed", [(1000, 1), (1000, 2), (14400, 1), (14400, 2)])
-def test_fit_paths_with_given_tss(lib, nW, seed):
+@pytest.mark.parametrize("nW,seed,density", [(1000, 1, 1.0), (1000, 2, 1.0), (14400, 1, 1.0), (14400, 2, 1.0),
+                                              (1000, 3, 0.35), (3000, 5, 0.5), (6000, 6, 0.5), (14400, 3, 0.35),
+                                              (14400, 4, 0.6)])
+def test_fit_paths_with_given_tss(lib, nW, seed, density):
     """tre_calibrate takes the smoothed TSS as an input: feed chosen values,
     with one request per (window, model) whose TTFT meets or misses the
-    bound, so every window's health is set by hand."""
+    bound, so every window's health is set by hand. With density below 1 a
+    (window, model) has its request with that probability (the others judge
+    nothing and are no candidates): the fit of a model pair then keeps both
+    models' keys side by side, where dense windows make it load the second
+    model again."""
     tre, device, torch = lib
     cases = _fit_cases(nW, seed)
     M = len(cases)
     win = 100
     rows = []
     rid = 0
+    present = np.random.default_rng(seed + 100).random((nW, M)) < density
     for w in range(nW):
         for m, (_, healthy, _) in enumerate(cases):
+            if not present[w, m]:
+                continue
             t0 = w * win + 5 * m
             first = 10 if healthy[w] else 60  # TTFT bound 30 ms
             rows += [(t0, m, rid, CP.A, 8), (t0, m, rid, CP.P | CP.ADMIT, 8), (t0 + first, m, rid, CP.D, 8),
@@ -476,7 +485,7 @@ def test_fit_paths_with_given_tss(lib, nW, seed):
     o = O.get()
     slo_h = _slo_rows(slo_cols, 0, M)
     r = o.calib_requests(ev_h, win, cfg["duration_ms"], slo_h, rid)
-    assert (r["judged"][:, :nW] == 1).all()
+    assert (r["judged"][:, :nW] == present.T).all()
     ref = o.calib_fit(S, fl, r["judged"], r["ok"], slo_h)
     for m in range(M):
         for k in ("n_cand", "n_healthy", "n_above", "healthy_above", "concordant", "discordant"):
