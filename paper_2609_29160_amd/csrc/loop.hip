@@ -103,10 +103,10 @@ struct LoopParams {
   int32_t dchunk;
   int32_t pool_words;           // the heap pool: pool_reps * spr + 4 or 6 words per model, multiple of 4
   int32_t pool_reps;            // replicas the pool holds: min(budget, M * r_hi, the declared bound)
-  uint64_t wmagic;              // x / window_ms == (x * wmagic) >> wshift for x < 2^31
+  uint32_t wmagic;              // x / window_ms == umulhi(x, wmagic) >> wshift for x < 2^31 (wshift < 0: x)
   int32_t wshift;
-  uint64_t pmagic, dmagic;      // the same for the prompt and output chunk sizes
-  int32_t pshift, dshift;
+  uint32_t pmagic, dmagic;      // x / chunk == umulhi(x, magic) for x < 2^16 (magic 0: chunk 1, x)
+  int32_t svc32;                // every remainder chunk's tokens * us + 999 below 2^32 (declared bounds)
   int32_t r_hi;                 // min(r_cap, budget): replicas one model may hold
   uint32_t ring_len;            // power of two above the longest span of a request in windows
   int32_t window_ms;
@@ -117,6 +117,12 @@ struct LoopParams {
 
 __device__ __forceinline__ int64_t ceil_ms(int64_t tokens, uint32_t us) {
   return (tokens * (int64_t)us + 999) / 1000;
+}
+// the same when tokens * us + 999 < 2^32: y / 1000 == umulhi(y, ceil(2^38 / 1000)) >> 6
+// for every 32-bit y (the multiplier's excess, 0.056 / 2^38 per unit of y,
+// stays below the 1/1000 gap to the next integer)
+__device__ __forceinline__ uint32_t ceil_ms32(uint32_t tokens, uint32_t us) {
+  return __umulhi(tokens * us + 999u, 0x10624DD3u) >> 6;
 }
 
 __device__ __forceinline__ uint64_t dbits(double x) { return (uint64_t)__double_as_longlong(x); }
@@ -383,13 +389,15 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
     base = nbase;
     bf = act && hs > 0 ? fresh.at(0) : kNone;
   };
-  const uint64_t wmagic = p.wmagic;
+  const uint32_t wmagic = p.wmagic, pmagic = p.pmagic, dmagic = p.dmagic;
   const int wshift = p.wshift;
-  auto win = [&](uint32_t x) { return (int32_t)((x * wmagic) >> wshift); };  // x / W for x < 2^31
-  const uint64_t pmagic = p.pmagic, dmagic = p.dmagic;
-  const int pshift = p.pshift, dshift = p.dshift;
-  auto div_p = [&](uint32_t x) { return (uint32_t)((x * pmagic) >> pshift); };  // x / prefill_chunk
-  auto div_d = [&](uint32_t x) { return (uint32_t)((x * dmagic) >> dshift); };  // x / decode_chunk
+  // x / W for x < 2^31; x / prefill_chunk and x / decode_chunk for x < 2^16
+  auto win = [&](uint32_t x) { return (int32_t)(wshift < 0 ? x : __umulhi(x, wmagic) >> wshift); };
+  auto div_p = [&](uint32_t x) { return pmagic ? __umulhi(x, pmagic) : x; };
+  auto div_d = [&](uint32_t x) { return dmagic ? __umulhi(x, dmagic) : x; };
+  // a remainder chunk's time (ms): 32-bit when the declared bounds allow
+  const bool svc32 = p.svc32 != 0;
+  auto rem_ms = [&](uint32_t tok, uint32_t us) { return svc32 ? ceil_ms32(tok, us) : (uint32_t)ceil_ms(tok, us); };
   const uint32_t udur = (uint32_t)dur;
   // the model's requests: rq0 + [0, nq); indices below relative to rq0
   const int64_t rq0 = act ? p.req_off[tm] : 0;
@@ -504,8 +512,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
           const uint32_t pt = po & 0xffffu, out_tok = po >> 16;
           const uint32_t npf = div_p(pt), prem = pt - npf * (uint32_t)p.pchunk;
           const uint32_t ndf = div_d(out_tok), drem = out_tok - ndf * (uint32_t)p.dchunk;
-          const uint32_t t_prem = prem ? (uint32_t)ceil_ms(prem, cst[2 * M]) : 0u;
-          const uint32_t t_drem = drem ? (uint32_t)ceil_ms(drem, cst[3 * M]) : 0u;
+          const uint32_t t_prem = prem ? rem_ms(prem, cst[2 * M]) : 0u;
+          const uint32_t t_drem = drem ? rem_ms(drem, cst[3 * M]) : 0u;
           const uint32_t td = (uint32_t)st + npf * (uint32_t)p_full + t_prem;  // end of the prompt
           const uint32_t tt = td + ndf * (uint32_t)d_full + t_drem;            // the last output chunk
           if (tt < udur) {  // FINISH: active -> gone
@@ -526,15 +534,18 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
               ++overflow;
             }
             if (out_tok) {  // judged as in the calibration sweep
-              const int64_t t_first = (int64_t)td + (ndf ? d_full : (int64_t)t_drem);
+              // 32-bit differences: every time here is in [0, 2^31) (arrivals
+              // non-negative, the duration plus the longest service below 2^31)
+              const uint32_t t_first = td + (ndf ? (uint32_t)d_full : t_drem);
               const uint32_t first_ch = ndf ? (uint32_t)p.dchunk : drem;
-              const int64_t ttft = t_first - a, e2e = (int64_t)tt - a, after = (int64_t)out_tok - first_ch;
+              const int32_t ttft = (int32_t)(t_first - (uint32_t)a), e2e = (int32_t)(tt - (uint32_t)a);
+              const int32_t after = (int32_t)(out_tok - first_ch);
               bool good = (double)ttft <= slo_t[0] && (double)e2e <= slo_t[2 * M];
-              if (after > 0) good = good && (double)((int64_t)tt - t_first) / (double)after <= slo_t[M];
+              if (after > 0) good = good && (double)(int32_t)(tt - t_first) / (double)after <= slo_t[M];
               ++n_done;
               n_ok += good ? 1u : 0u;
               e2e_sum += e2e;
-              e2e_max = e2e > (int64_t)e2e_max ? (int32_t)e2e : e2e_max;
+              e2e_max = e2e > e2e_max ? e2e : e2e_max;
             }
           }
           bf = slot.replace_top(ns, tt);  // tt >= st >= the root
@@ -593,7 +604,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
             tok = (uint32_t)p.dchunk;
           } else {
             const uint32_t drem = out_tok - ndf * (uint32_t)p.dchunk;
-            t = td + ndf * cl[M] + (uint32_t)ceil_ms(drem, cl[3 * M]);
+            t = td + ndf * cl[M] + rem_ms(drem, cl[3 * M]);
             tok = drem;
           }
           f = 1;
@@ -815,12 +826,24 @@ size_t lds_bytes(const tre_trace_cfg* cfg, const tre_loop_requests* rq) {
   return ((size_t)pool_words(cfg, rq) + (size_t)(6 + 4 * kNear + 2 * kStage + 4 * kEnt + 2 + 4) * cfg->n_models) * 4;
 }
 
-// x / d == (x * m) >> sh for x < 2^32: m = ceil(2^(32 + l) / d), 2^l >= d
-void magic_div(int64_t d, uint64_t* m, int32_t* sh) {
+// x / d == umulhi(x, m) >> sh for x < 2^31 and 1 <= d < 2^31: with 2^(l-1) < d
+// <= 2^l, m = ceil(2^(31 + l) / d) < 2^32 and sh = l - 1 (the multiplier's
+// excess adds less than x / 2^(31 + l) < 1 / d, below the gap to the next
+// integer); d = 1 gives sh = -1 (x itself)
+void magic31(int64_t d, uint32_t* m, int32_t* sh) {
   int l = 0;
   while ((1ll << l) < d) ++l;
-  *sh = 32 + l;
-  *m = (uint64_t)(((1ull << (32 + l)) + (uint64_t)d - 1) / (uint64_t)d);
+  *sh = l - 1;
+  *m = l == 0 ? 0u : (uint32_t)(((1ull << (31 + l)) + (uint64_t)d - 1) / (uint64_t)d);
+}
+
+// x / d == umulhi(x, m) for x < 2^16 and d >= 2: m = floor(2^32 / d) + 1 (the
+// excess adds at most x / 2^32 < 1 / d while x * d < 2^32; m = 1 for d >=
+// 2^16, where every such x / d is 0); m = 0 for d = 1 (x itself)
+uint32_t magic16(int64_t d) {
+  if (d == 1) return 0u;
+  if (d >= 65536) return 1u;
+  return (uint32_t)((1ull << 32) / (uint64_t)d) + 1u;
 }
 
 int check_loop_args(const tre_trace_cfg* cfg, const tre_loop_requests* rq) {
@@ -927,9 +950,11 @@ static int loop_impl(const tre_trace_cfg* cfg, uint32_t n_traces, const tre_loop
   lp.pool_words = pool_words(cfg, rq);
   lp.pool_reps = pool_reps(cfg, rq);
   lp.r_hi = r_hi(cfg, rq);
-  magic_div(cfg->window_ms, &lp.wmagic, &lp.wshift);
-  magic_div(rq->prefill_chunk, &lp.pmagic, &lp.pshift);
-  magic_div(rq->decode_chunk, &lp.dmagic, &lp.dshift);
+  magic31(cfg->window_ms, &lp.wmagic, &lp.wshift);
+  lp.pmagic = magic16(rq->prefill_chunk);
+  lp.dmagic = magic16(rq->decode_chunk);
+  lp.svc32 = (int64_t)rq->prefill_chunk * rq->max_prefill_us + 999 < (1ll << 32) &&
+             (int64_t)rq->decode_chunk * rq->max_decode_us + 999 < (1ll << 32);
   lp.ring_len = L;
   lp.window_ms = (int32_t)cfg->window_ms;
   lp.duration_ms = (int32_t)cfg->duration_ms;
