@@ -417,13 +417,21 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
   // the next kStage requests to start, fetched together (one wait per kStage starts)
   uint32_t sbase = next_start;
   auto stage = [&](uint32_t from) {
-    int64_t av[kStage];
-    uint32_t pv[kStage];
+    int64_t av[kStage] = {};
+    uint32_t pv[kStage] = {};
+    if (nq) {  // every load issued before any is used (one wait); past the table, the last request's
+#pragma unroll
+      for (int e = 0; e < kStage; ++e) {
+        const uint32_t i = from + e < nq ? from + e : nq - 1;
+        av[e] = arrival[i];
+        pv[e] = (uint32_t)p.prompt[rq0 + i] | (uint32_t)p.output[rq0 + i] << 16;
+      }
+    }
 #pragma unroll
     for (int e = 0; e < kStage; ++e) {
       const bool in = from + e < nq;
-      av[e] = in ? arrival[from + e] : kNever;
-      pv[e] = in ? (uint32_t)p.prompt[rq0 + from + e] | (uint32_t)p.output[rq0 + from + e] << 16 : 0u;
+      av[e] = in ? av[e] : kNever;
+      pv[e] = in ? pv[e] : 0u;
     }
 #pragma unroll
     for (int e = 0; e < kStage; ++e) {
