@@ -57,16 +57,13 @@ constexpr int64_t kNever = INT64_MAX;
 constexpr int32_t kArrNever = INT32_MAX;
 constexpr int kLdsMax = 160 * 1024;
 
-// Tallies of one window of one model beyond the LDS ring, in two rings: the
-// output tokens of DECODE events (one add per output chunk) in 4-byte cells,
+// Tallies of one window of one model beyond the LDS ring, in three rings of
+// [scenario][ring cell][model]: the output tokens of DECODE events (one add
+// per output chunk) and the prompt tokens of PREFILL events in 4-byte cells,
 // so that one window's cells of 32 models share one cache line and the few
-// dozen windows a scenario is adding into stay in L2; the rest (one or two
-// adds per request) in FarCell.
-struct FarCell {
-  uint32_t p;       // prompt tokens of its PREFILL events
-  uint32_t n_fin;   // FINISH events in it
-  uint32_t e_fin;   // sum over them of (window end - finish time)
-};
+// dozen windows a scenario is adding into stay in L2; its FINISH events in
+// 8-byte cells, count << 32 plus the sum of (window end - finish time) (below
+// 2^32, as the LDS ring's 32-bit cell), one add per finishing request.
 
 struct LoopParams {
   const int64_t* arrival;
@@ -83,8 +80,9 @@ struct LoopParams {
   int64_t* r_windows;
   tre_loop_stats* stats;
   double* tss64;                // [scenario][window][model] or NULL
-  FarCell* far;                 // [scenario][ring_len][model]
+  uint32_t* far_p;              // [scenario][ring_len][model]: prompt tokens
   uint32_t* far_d;              // [scenario][ring_len][model]: output tokens
+  unsigned long long* far_f;    // [scenario][ring_len][model]: FINISH count << 32 | sum of time to window end
   uint32_t* scratch;            // [scenario][pool_words]: heaps in transit at a repack
   // the actuation model (the kAct instantiation)
   const int32_t* footprint;     // [trace][M] GPUs per replica, or NULL (1); the budget is then in GPUs
@@ -228,6 +226,15 @@ __device__ __forceinline__ uint32_t far_load(uint32_t* a) {
 __device__ __forceinline__ void far_store(uint32_t* a, uint32_t v) {
   __hip_atomic_store(a, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
+__device__ __forceinline__ void far_add(unsigned long long* a, unsigned long long v) {
+  __hip_atomic_fetch_add(a, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+__device__ __forceinline__ unsigned long long far_load(unsigned long long* a) {
+  return __hip_atomic_load(a, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+__device__ __forceinline__ void far_store(unsigned long long* a, unsigned long long v) {
+  __hip_atomic_store(a, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
 
 __global__ void zero_u64(unsigned long long* x) { *x = 0ull; }
 
@@ -280,8 +287,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
   uint32_t* lane_off = rest + (6 + 4 * kNear + 2 * kStage + 4 * kEnt) * M;
   uint32_t* lane_cnt = lane_off + M;
   uint32_t* cst = lane_cnt + M + mc;
-  FarCell* far = p.far + (uint64_t)s * L * M + mc;  // cell c at far[c * M]
-  uint32_t* fard = p.far_d + (uint64_t)s * L * M + mc;  // and fard[c * M]
+  // the far rings' cell c of this lane at index fo + c * M (one offset for
+  // the three rings keeps one register pair)
+  const uint64_t fo = (uint64_t)s * L * M + mc;
   // initial replicas: at most r_hi per model and pool_reps in all (initial
   // replicas within the budget and the declared bound are never cut; cut
   // ones are counted as bounds exceeded)
@@ -342,11 +350,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
     for (int i = 0; i < hs; ++i) h0.at(i) = 0u;  // equal keys form a heap
     mark_free(h0, hs, hs);
     for (uint32_t c = 0; c < L; ++c) {
-      FarCell* fc = far + (uint64_t)c * M;
-      far_store(&fc->p, 0u);
-      far_store(&fard[(uint64_t)c * M], 0u);
-      far_store(&fc->n_fin, 0u);
-      far_store(&fc->e_fin, 0u);
+      far_store(&p.far_p[fo + (uint64_t)c * M], 0u);
+      far_store(&p.far_d[fo + (uint64_t)c * M], 0u);
+      far_store(&p.far_f[fo + (uint64_t)c * M], 0ull);
     }
   }
   uint32_t bf = act && hs > 0 ? 0u : kNone;  // earliest slot free time (the heap's root)
@@ -535,9 +541,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
               lds_add(nc + 2 * kNear * M, 1u);
               lds_add(nc + 3 * kNear * M, ef);
             } else if (ahead < L) {
-              FarCell* fc = far + (uint64_t)(xw & (L - 1)) * M;
-              far_add(&fc->n_fin, 1u);
-              far_add(&fc->e_fin, ef);
+              far_add(&p.far_f[fo + (uint64_t)(xw & (L - 1)) * M], (1ull << 32) | ef);
             } else {
               ++overflow;
             }
@@ -624,7 +628,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
             lds_add(near + (l - mc) + (f * kNear + (x & (kNear - 1))) * M, tok);
           } else if (ahead < L) {
             const uint64_t fcell = (uint64_t)(x & (L - 1)) * M + (l - mc);
-            far_add(f ? &fard[fcell] : &far[fcell].p, tok);
+            far_add(f ? &p.far_d[fo + fcell] : &p.far_p[fo + fcell], tok);
           } else {
             ++overflow;
           }
@@ -654,18 +658,16 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
           if (fn) lds_add(nc + 2 * kNear * M, fn);
           if (fe) lds_add(nc + 3 * kNear * M, fe);
           const uint64_t c0 = (uint64_t)((uint32_t)(w - 1 + kNear) & (L - 1)) * M;
-          FarCell* fc = far + c0;
-          far_store(&fc->p, 0u);
-          far_store(&fard[c0], 0u);
-          far_store(&fc->n_fin, 0u);
-          far_store(&fc->e_fin, 0u);
+          far_store(&p.far_p[fo + c0], 0u);
+          far_store(&p.far_d[fo + c0], 0u);
+          far_store(&p.far_f[fo + c0], 0ull);
         }
         const uint64_t c1 = (uint64_t)((uint32_t)(w + kNear) & (L - 1)) * M;
-        FarCell* fc = far + c1;
-        fp = far_load(&fc->p);
-        fd = far_load(&fard[c1]);
-        fn = far_load(&fc->n_fin);
-        fe = far_load(&fc->e_fin);
+        fp = far_load(&p.far_p[fo + c1]);
+        fd = far_load(&p.far_d[fo + c1]);
+        const unsigned long long ff = far_load(&p.far_f[fo + c1]);
+        fn = (uint32_t)(ff >> 32);
+        fe = (uint32_t)ff;
       }
       // the window's tallies, Eq. (1) and the smoothing
       const int64_t A_int = (int64_t)W * cA + eA, W_int = (int64_t)W * cW + eW;  // counts below 2^31
@@ -883,7 +885,7 @@ extern "C" int tre_loop_workspace_size(const tre_trace_cfg* cfg, const tre_loop_
   if (!bytes) return fail(TRE_EINVAL, "tre_loop_workspace_size: NULL bytes");
   const int rc = check_loop_args(cfg, rq);
   if (rc) return rc;
-  *bytes = (size_t)(256 + (uint64_t)n_scenarios * cfg->n_models * ring_len(cfg, rq) * (sizeof(FarCell) + 4) +
+  *bytes = (size_t)(256 + (uint64_t)n_scenarios * cfg->n_models * ring_len(cfg, rq) * 16 +
                     (uint64_t)n_scenarios * pool_words(cfg, rq) * 4);
   return TRE_OK;
 }
@@ -920,9 +922,11 @@ static int loop_impl(const tre_trace_cfg* cfg, uint32_t n_traces, const tre_loop
   const uint32_t L = ring_len(cfg, rq);
   char* base = (char*)ws;
   unsigned long long* overflow = (unsigned long long*)base;
-  FarCell* far = (FarCell*)(base + 256);
-  uint32_t* far_d = (uint32_t*)(base + 256 + (uint64_t)n_scenarios * M * L * sizeof(FarCell));
-  uint32_t* scratch = (uint32_t*)(base + 256 + (uint64_t)n_scenarios * M * L * (sizeof(FarCell) + 4));
+  const uint64_t cells = (uint64_t)n_scenarios * M * L;  // the rings: 4 + 4 + 8 bytes per cell
+  uint32_t* far_p = (uint32_t*)(base + 256);
+  uint32_t* far_d = (uint32_t*)(base + 256 + cells * 4);
+  unsigned long long* far_f = (unsigned long long*)(base + 256 + cells * 8);
+  uint32_t* scratch = (uint32_t*)(base + 256 + cells * 16);
   const size_t lds = lds_bytes(cfg, rq);
   const void* kern = act ? (const void*)loop_replay<true> : (const void*)loop_replay<false>;
   HIP_TRY(hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
@@ -942,8 +946,9 @@ static int loop_impl(const tre_trace_cfg* cfg, uint32_t n_traces, const tre_loop
   lp.r_windows = out->r_windows;
   lp.stats = stats;
   lp.tss64 = tss64;
-  lp.far = far;
+  lp.far_p = far_p;
   lp.far_d = far_d;
+  lp.far_f = far_f;
   lp.scratch = scratch;
   lp.overflow = overflow;
   lp.move_cap = out->move_cap;
