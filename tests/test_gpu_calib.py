@@ -477,6 +477,16 @@ def test_fit_paths_with_given_tss(lib, nW, seed, density):
     out = tre.calib_outputs(ev, rid)
     tre.tre_calibrate(ev, slo, tss64, flags, out)
     fit0 = tre.unpack_fit(out["fit"]).copy()
+    # the same TSS 8 bytes off a 16-byte boundary: one model per workgroup
+    # (pairs need 16-byte TSS loads); the same fits
+    shifted = torch.zeros(tss64.numel() + 1, dtype=torch.float64, device="cuda")
+    shifted[1:] = tss64.reshape(-1)
+    tss64_u = shifted[1:].view(tss64.shape)
+    assert tss64_u.data_ptr() % 16 == 8
+    tre.tre_calibrate(ev, slo, tss64_u, flags, out)
+    fit_u = tre.unpack_fit(out["fit"]).copy()
+    for k in ("theta", "n_cand", "n_healthy", "n_above", "healthy_above"):
+        assert np.array_equal(np.ascontiguousarray(fit0[k]).view(np.uint8), np.ascontiguousarray(fit_u[k]).view(np.uint8)), k
     tre.tre_calib_order(ev, slo, tss64, flags, out)
     torch.cuda.synchronize()
     fit = tre.unpack_fit(out["fit"])

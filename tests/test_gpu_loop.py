@@ -167,6 +167,21 @@ def test_several_traces(lib):
            _scenarios(rng, 9, 3))
 
 
+def test_wide_service_bounds(lib):
+    """A model whose prompt tokens take 2.2 s each: a full prompt chunk's
+    tokens * us then passes 2^32, so the remainder-chunk times take their
+    64-bit path for every model; results as the oracle's."""
+    w = tg.standard(0)
+    tables = [w.requests(0)]
+    rng = np.random.default_rng(14)
+    svc = {k: np.array(v, copy=True) for k, v in w.service_columns(1).items()}
+    svc["prefill_us"][0] = 2_200_000
+    svc["decode_us"][-1] = svc["decode_us"][-1] * 50
+    assert 2048 * int(svc["prefill_us"].max()) + 999 >= 1 << 32
+    cfg = dict(w.trace_cfg(), budget=w.budget + 2)
+    _check(lib, "wide-service", cfg, tables, w.profile_columns(1), w.slo_columns(1), svc, _scenarios(rng, 8, 1))
+
+
 def test_slots_per_replica(lib):
     w = tg.standard(0)
     tables = [w.requests(0)]
