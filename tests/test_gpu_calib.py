@@ -362,7 +362,7 @@ def test_stream_fallback(lib):
 
 
 def test_model_counts(lib):
-    for M in (1, 17, 64):
+    for M in (1, 2, 17, 64):  # 2 and 64: the fit in model pairs
         w = tg.Workload(name=f"m{M}", n_traces=2, model_classes=[["7B", "13B", "34B", "70B"][m % 4] for m in range(M)],
                         interactive=[m % 2 == 0 for m in range(M)], r_init=[2] * M, budget=2 * M,
                         window_ms=500, duration_ms=900_000, process="mmpp2", rate=[0.5] * M,
